@@ -1,0 +1,395 @@
+"""Pins for the CPU oracle: each check ties it to something other than itself --
+brute force on tiny inputs, closed forms, invariants, independent library
+routines, and the values the paper prints.  CPU only."""
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import pipeline as opipe
+from paper_2412_09282_amd import inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rv(n, d, seed, scale=1.0):
+    return inputs.random_vectors(n, d, seed, scale)
+
+
+# ------------------------------------------------------------------------------------------------
+# assignment (Sec. 3.1 Eq. 3-4)
+# ------------------------------------------------------------------------------------------------
+
+def _brute_codes(V, C):
+    """Independent enumeration: exact squared distances on integer-valued data (exact in fp64)."""
+    best = []
+    for v in V.astype(np.int64):
+        ds = [int(((v - c) ** 2).sum()) for c in C.astype(np.int64)]
+        m = min(ds)
+        best.append((ds.index(m), m))
+    return np.array([b[0] for b in best]), np.array([b[1] for b in best])
+
+
+@pytest.mark.parametrize("d", [1, 2, 3, 8])
+@pytest.mark.parametrize("K", [1, 2, 7, 16])
+def test_assign_bruteforce_integer_grid(oracle_mod, d, K):
+    """Integer-valued data makes every distance exact, so equal distances are real ties and the
+    oracle must pick the lowest index among them."""
+    g = np.random.default_rng(1000 + 10 * d + K)
+    V = g.integers(-3, 4, size=(64, d)).astype(np.float32)
+    C = g.integers(-3, 4, size=(K, d)).astype(np.float32)
+    codes, dist = oracle.assign(V, C)
+    bc, bd = _brute_codes(V, C)
+    np.testing.assert_array_equal(codes, bc)
+    np.testing.assert_array_equal(dist, bd.astype(np.float64))
+
+
+def test_assign_duplicate_codewords_take_lowest_index(oracle_mod):
+    V = _rv(100, 8, 1)
+    C = np.concatenate([_rv(5, 8, 2), _rv(5, 8, 2)])  # rows 5..9 duplicate rows 0..4
+    codes, _ = oracle.assign(V, C)
+    assert codes.max() < 5
+
+
+def test_assign_k1_closed_form(oracle_mod):
+    V = _rv(50, 8, 3)
+    C = _rv(1, 8, 4)
+    codes, dist = oracle.assign(V, C)
+    assert (codes == 0).all()
+    ref = ((V.astype(np.float64) - C.astype(np.float64)) ** 2).sum(1)
+    np.testing.assert_allclose(dist, ref, rtol=1e-15)
+
+
+def test_assign_d1_sorted_nearest(oracle_mod):
+    """1-D nearest neighbour through a sorted codebook and searchsorted."""
+    g = np.random.default_rng(5)
+    C = g.choice(np.arange(-1000, 1000), size=40, replace=False).astype(np.float32)[:, None] / 64
+    V = g.uniform(-20, 20, size=(500, 1)).astype(np.float32)
+    codes, _ = oracle.assign(V, C)
+    order = np.argsort(C[:, 0])
+    cs = C[order, 0].astype(np.float64)
+    pos = np.searchsorted(cs, V[:, 0].astype(np.float64))
+    lo = np.clip(pos - 1, 0, len(cs) - 1)
+    hi = np.clip(pos, 0, len(cs) - 1)
+    dlo = np.abs(V[:, 0] - cs[lo])
+    dhi = np.abs(V[:, 0] - cs[hi])
+    pick = np.where(dhi < dlo, hi, lo)
+    tie = dhi == dlo
+    exp = order[pick]
+    exp[tie] = np.minimum(order[lo[tie]], order[hi[tie]])
+    np.testing.assert_array_equal(codes, exp)
+
+
+def test_assign_exact_reconstruction(oracle_mod):
+    """Codebook = the vectors themselves (distinct): every vector encodes to itself at distance 0."""
+    V = _rv(256, 8, 6)
+    g = np.random.default_rng(6)
+    p = g.permutation(256)
+    codes, dist = oracle.assign(V, V[p])
+    np.testing.assert_array_equal(p[codes], np.arange(256))
+    assert (dist == 0).all()
+
+
+def test_assign_matches_scipy_vq(oracle_mod):
+    from scipy.cluster.vq import vq
+    V = _rv(2000, 8, 7, 0.02)
+    C = _rv(300, 8, 8, 0.02)
+    codes, dist = oracle.assign(V, C)
+    sc, sd = vq(V.astype(np.float64), C.astype(np.float64), check_finite=False)
+    D = ((V.astype(np.float64)[:, None, :] - C.astype(np.float64)[None]) ** 2).sum(-1)
+    Ds = np.sort(D, axis=1)
+    clear = (Ds[:, 1] - Ds[:, 0]) > 1e-9 * Ds[:, 0]
+    assert clear.mean() > 0.99
+    np.testing.assert_array_equal(codes[clear], sc[clear])
+    np.testing.assert_allclose(np.sqrt(dist), sd, rtol=1e-12)
+
+
+def test_assign_bf16_inputs_widen_exactly(oracle_mod):
+    V = inputs.f32_to_bf16_bits(_rv(300, 8, 9, 0.02))
+    C = inputs.f32_to_bf16_bits(_rv(40, 8, 10, 0.02))
+    codes, dist = oracle.assign(V, C, "bf16", "bf16")
+    c2, d2 = oracle.assign(inputs.bf16_bits_to_f32(V), inputs.bf16_bits_to_f32(C))
+    np.testing.assert_array_equal(codes, c2)
+    np.testing.assert_array_equal(dist, d2)
+
+
+# ------------------------------------------------------------------------------------------------
+# K-means update (Sec. 3.1 Eq. 2)
+# ------------------------------------------------------------------------------------------------
+
+def test_kmeans_k1_is_global_mean(oracle_mod):
+    V = _rv(1000, 8, 11)
+    C, counts, means = oracle.kmeans_update(V, np.zeros(1000, np.int32), _rv(1, 8, 12))
+    assert counts[0] == 1000
+    np.testing.assert_allclose(means[0], V.astype(np.float64).mean(0), rtol=1e-13, atol=1e-16)
+    np.testing.assert_array_equal(C[0], means[0].astype(np.float32))
+
+
+def test_kmeans_hand_example(oracle_mod):
+    V = np.array([[0, 0], [2, 0], [0, 4], [10, 10], [12, 10]], np.float32)
+    q = np.array([0, 0, 0, 2, 2], np.int32)
+    C0 = np.array([[9, 9], [7, 7], [5, 5]], np.float32)
+    C, counts, _ = oracle.kmeans_update(V, q, C0)
+    np.testing.assert_array_equal(counts, [3, 0, 2])
+    np.testing.assert_array_equal(C, np.array([[2 / 3, 4 / 3], [7, 7], [11, 10]], np.float32))
+
+
+def test_kmeans_matches_sklearn_lloyd(oracle_mod):
+    from sklearn.cluster import KMeans
+    g = np.random.default_rng(13)
+    centers = g.normal(size=(12, 8)) * 5
+    V = (centers[g.integers(0, 12, 3000)] + g.normal(size=(3000, 8))).astype(np.float32)
+    C0 = V[g.choice(3000, 12, replace=False)]
+    C = C0.copy()
+    T = 6
+    for _ in range(T):
+        q, _ = oracle.assign(V, C)
+        assert np.bincount(q, minlength=12).min() > 0
+        C, _, _ = oracle.kmeans_update(V, q, C)
+    km = KMeans(n_clusters=12, init=C0.astype(np.float64), n_init=1, algorithm="lloyd", max_iter=T, tol=0.0)
+    km.fit(V.astype(np.float64))
+    np.testing.assert_allclose(C, km.cluster_centers_, rtol=1e-5, atol=1e-6)
+
+
+def test_kmeans_objective_never_increases(oracle_mod):
+    V = _rv(4000, 8, 14, 0.02)
+    C = V[np.random.default_rng(14).choice(4000, 64, replace=False)]
+    _, _, _, J = opipe.kmeans(V, C, 8, "f32", "f32")
+    for a, b in zip(J, J[1:]):
+        assert b <= a * (1 + 1e-6)
+
+
+# ------------------------------------------------------------------------------------------------
+# column reductions: Hessian diagonal and channel importance (Sec. 4.1 Eq. 7, App. A.2 Eq. 9-10)
+# ------------------------------------------------------------------------------------------------
+
+def test_hdiag_is_diag_of_gram(oracle_mod):
+    X = _rv(300, 40, 15)  # tokens x N
+    h = oracle.colreduce(X)
+    np.testing.assert_allclose(h, np.diag(X.astype(np.float64).T @ X.astype(np.float64)), rtol=1e-12)
+
+
+def test_importance_max_mode_exact(oracle_mod):
+    W = _rv(64, 48, 16)
+    Wq = _rv(64, 48, 17)
+    s = np.abs(_rv(1, 48, 18)[0]).astype(np.float64)
+    got = oracle.colreduce(W, Wq, s, reduce="max")
+    diff = W.astype(np.float64) - Wq.astype(np.float64)
+    np.testing.assert_array_equal(got, s * (diff * diff).max(0))
+
+
+def test_importance_eq10_equals_matrix_form(oracle_mod):
+    """App. A.2: max_j 1/2 sum_k (x_ik dw_ji)^2 equals max_j dw_ji^2 * [XX^T]_ii / 2."""
+    X = _rv(200, 24, 19)   # tokens x N
+    dW = _rv(32, 24, 20)   # M x N
+    h = oracle.colreduce(X)
+    got = oracle.colreduce(dW, None, h / 2, reduce="max")
+    direct = np.array([max(0.5 * sum((float(X[k, i]) * float(dW[j, i])) ** 2 for k in range(200))
+                           for j in range(32)) for i in range(24)])
+    np.testing.assert_allclose(got, direct, rtol=1e-12)
+
+
+def test_importance_sum_mode(oracle_mod):
+    W = _rv(80, 56, 21)
+    h = np.abs(_rv(1, 56, 22)[0]).astype(np.float64)
+    got = oracle.colreduce(W, scale=h)
+    np.testing.assert_allclose(got, h * (W.astype(np.float64) ** 2).sum(0), rtol=1e-13)
+
+
+# ------------------------------------------------------------------------------------------------
+# channel reordering (Sec. 4.2)
+# ------------------------------------------------------------------------------------------------
+
+def test_rank_perm_is_stable_descending(oracle_mod):
+    g = np.random.default_rng(23)
+    I = g.integers(0, 5, size=200).astype(np.float32)  # many ties
+    perm = oracle.rank_perm(I)
+    np.testing.assert_array_equal(np.sort(perm), np.arange(200))
+    np.testing.assert_array_equal(perm, np.lexsort((np.arange(200), -I)))
+
+
+def test_rank_perm_nan_last(oracle_mod):
+    I = np.array([1.0, np.nan, 3.0, np.nan, 2.0, 3.0], np.float32)
+    np.testing.assert_array_equal(oracle.rank_perm(I), [2, 5, 4, 0, 1, 3])
+
+
+def test_reorder_roundtrip(oracle_mod):
+    W = _rv(16, 40, 24)
+    perm = np.random.default_rng(24).permutation(40).astype(np.int32)
+    Ws = oracle.gather_columns(W, perm)
+    np.testing.assert_array_equal(Ws[:, 3], W[:, perm[3]])
+    np.testing.assert_array_equal(oracle.scatter_columns(Ws, perm), W)
+
+
+def test_outlier_channels_are_critical():
+    """Workload 4's structure: the 1% of input channels scaled x10 dominate sum_i W_ij^2, so the
+    importance ordering must put all of them among the critical channels.  Checked on a reduced
+    layer of the same recipe (t4 weights, 1% outlier columns x10, N(0,1) activations)."""
+    import oracle as o
+    wl = inputs.Workload(4, "reduced", [inputs.LayerSpec("r", 512, 2048, 256, "f32", "t4_outliers", "normal")],
+                         d=8, K_base=64, K_ext=[64], crit_frac=0.02, beam=1, iters=1)
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    h = o.round_to(o.colreduce(X), "f32")
+    I = o.round_to(o.colreduce(W, scale=h.astype(np.float64)), "f32")
+    perm = o.rank_perm(I)
+    n_crit = o.n_crit_columns(2048, 8, 0.02)
+    outl = inputs.outlier_columns(4, 0, 2048)
+    assert set(outl.tolist()) <= set(perm[:n_crit].tolist())
+
+
+# ------------------------------------------------------------------------------------------------
+# residual beam search (Sec. 3.1, Sec. 4.3, Alg. 1 BeamSearchOptimize)
+# ------------------------------------------------------------------------------------------------
+
+def test_beam1_is_greedy_residual(oracle_mod):
+    V = _rv(500, 8, 25, 0.02)
+    C0 = _rv(32, 8, 26, 0.02)
+    C1 = _rv(16, 8, 27, 0.005)
+    C2 = _rv(16, 8, 28, 0.002)
+    codes, err = oracle.beam(V, [C0, C1, C2], 1)
+    r = V.astype(np.float64)
+    for t, C in enumerate([C0, C1, C2]):
+        D = ((r[:, None, :] - C.astype(np.float64)[None]) ** 2).sum(-1)
+        q = D.argmin(1)
+        np.testing.assert_array_equal(codes[t], q)
+        r = r - C.astype(np.float64)[q]
+    np.testing.assert_allclose(err, (r ** 2).sum(1), rtol=1e-12)
+
+
+def test_beam_wide_is_exhaustive(oracle_mod):
+    """Width >= K^(m-1) keeps every partial tuple, so the answer is the exhaustive optimum."""
+    V = _rv(60, 4, 29, 1.0)
+    books = [_rv(5, 4, 30, 1.0), _rv(5, 4, 31, 0.5), _rv(4, 4, 32, 0.25)]
+    codes, err = oracle.beam(V, books, 25)
+    Vd = V.astype(np.float64)
+    for i in range(60):
+        best = None
+        for tup in itertools.product(*[range(len(b)) for b in books]):
+            s = sum(books[t].astype(np.float64)[tup[t]] for t in range(3))
+            e = float(((Vd[i] - s) ** 2).sum())
+            if best is None or e < best[0] - 1e-12:
+                best = (e, tup)
+        assert abs(err[i] - best[0]) <= 1e-12 * max(best[0], 1e-30)
+        got = tuple(int(codes[t, i]) for t in range(3))
+        if got != best[1]:  # only an exact-tie alternative is acceptable
+            s = sum(books[t].astype(np.float64)[got[t]] for t in range(3))
+            assert abs(float(((Vd[i] - s) ** 2).sum()) - best[0]) <= 1e-12 * best[0]
+
+
+def test_beam_err_matches_codes(oracle_mod):
+    V = _rv(300, 8, 33, 0.02)
+    books = [_rv(64, 8, 34, 0.02), _rv(16, 8, 35, 0.01)]
+    for width in (1, 3, 8):
+        codes, err = oracle.beam(V, books, width)
+        R = oracle.reconstruct([codes[0], codes[1]], books, np.ones(300, np.uint8))
+        np.testing.assert_allclose(err, ((V.astype(np.float64) - R) ** 2).sum(1), rtol=1e-9, atol=1e-18)
+
+
+def test_beam_single_book_is_assign(oracle_mod):
+    V = _rv(400, 8, 36, 0.02)
+    C = _rv(50, 8, 37, 0.02)
+    codes, err = oracle.beam(V, [C], 4)
+    q, dist = oracle.assign(V, C)
+    np.testing.assert_array_equal(codes[0], q)
+    np.testing.assert_array_equal(err, dist)
+
+
+# ------------------------------------------------------------------------------------------------
+# reconstruction / dequantization (Sec. 4.3, Fig. 3)
+# ------------------------------------------------------------------------------------------------
+
+def test_reconstruct_identity_codebook(oracle_mod):
+    V = _rv(128, 8, 38)
+    R = oracle.reconstruct([np.arange(128, dtype=np.int32)], [V], np.zeros(128, np.uint8))
+    np.testing.assert_array_equal(R, V.astype(np.float64))
+
+
+def test_reconstruct_additive_only_on_critical(oracle_mod):
+    C0 = np.array([[1, 2], [3, 4]], np.float32)
+    C1 = np.array([[0.5, 0.25], [10, 20]], np.float32)
+    codes = [np.array([0, 1, 1], np.int32), np.array([1, 0, 1], np.int32)]
+    R = oracle.reconstruct(codes, [C0, C1], np.array([1, 0, 1], np.uint8))
+    np.testing.assert_array_equal(R, [[11, 22], [3, 4], [13, 24]])
+
+
+def test_residual_definition(oracle_mod):
+    V = _rv(64, 8, 39)
+    C = _rv(8, 8, 40)
+    q = np.random.default_rng(40).integers(0, 8, 64).astype(np.int32)
+    E = oracle.residual(V, q, C)
+    np.testing.assert_array_equal(E, (V.astype(np.float64) - C.astype(np.float64)[q]).astype(np.float32))
+
+
+# ------------------------------------------------------------------------------------------------
+# storage rounding
+# ------------------------------------------------------------------------------------------------
+
+def test_bf16_rounding_against_generator_and_ties(oracle_mod):
+    g = np.random.default_rng(41)
+    x = (g.standard_normal(20000) * 10.0 ** g.uniform(-30, 30, 20000)).astype(np.float32)
+    np.testing.assert_array_equal(oracle.round_to(x.astype(np.float64), "bf16"), inputs.f32_to_bf16_bits(x))
+    one = 1.0
+    cases = {one + 2 ** -8: one,                         # tie -> even (1.0)
+             one + 3 * 2 ** -8: one + 2 ** -6,           # tie -> even (1 + 2^-6)
+             one + 2 ** -8 + 2 ** -40: one + 2 ** -7,    # above the tie: up (a double rounding via fp32 would tie down)
+             -(one + 2 ** -8 + 2 ** -40): -(one + 2 ** -7)}
+    for xin, want in cases.items():
+        got = inputs.bf16_bits_to_f32(oracle.round_to(np.array([xin]), "bf16"))[0]
+        assert float(got) == want, (xin, got, want)
+
+
+# ------------------------------------------------------------------------------------------------
+# pipeline-level invariants and the paper's printed values
+# ------------------------------------------------------------------------------------------------
+
+def test_extended_codebook_never_raises_error(oracle_mod):
+    V = _rv(3000, 8, 42, 0.02)
+    C0 = V[np.random.default_rng(42).choice(3000, 32, replace=False)]
+    C, q, _, _ = opipe.kmeans(V, C0, 3, "f32", "f32")
+    E = oracle.residual(V, q, C)
+    Ce, qe, _, _ = opipe.kmeans(E, E[np.random.default_rng(43).choice(3000, 16, replace=False)], 1, "f32", "f32")
+    E2 = oracle.residual(E, qe, Ce)
+    assert float((E2.astype(np.float64) ** 2).sum()) <= float((E.astype(np.float64) ** 2).sum())
+
+
+def test_workload1_pipeline_invariants(oracle_mod):
+    """Workload 1 end to end on the oracle.  Its extended book has as many codewords as there are
+    critical vectors and starts from all of them, so the extended stage reconstructs its residual
+    exactly (the exact-reconstruction special case)."""
+    wl = inputs.WORKLOADS[1]
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    M, N, d = 256, 256, 8
+    n = M * N // d
+    n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    assert n_crit == 8
+    ext_idx = [inputs.ext_init_indices(wl, 0, 1, M * n_crit // d)]
+    res = opipe.quantize_layer(W, X, "f32", d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters,
+                               inputs.base_init_indices(wl, 0, n), ext_idx)
+    J = res.objectives["base"]
+    assert all(b <= a * (1 + 1e-6) for a, b in zip(J, J[1:]))
+    assert res.objectives["ext1"][-1] == 0.0
+    # critical vectors are reconstructed to within fp32 rounding of their residual
+    Ws = oracle.gather_columns(W, res.perm)
+    What_s = oracle.gather_columns(res.W_hat, res.perm)
+    crit_err = np.abs(Ws[:, :n_crit].astype(np.float64) - What_s[:, :n_crit]).max()
+    assert crit_err < 1e-8
+    np.testing.assert_array_equal(np.sort(res.perm), np.arange(N))
+
+
+def test_bits_printed_values():
+    gold = json.load(open(os.path.join(GOLDEN, "bits_per_weight.json")))
+    g = gold["vq_m1_e8_d8"]
+    v = oracle.bits_per_weight_vq(g["m"], g["e"], g["d"], g["rows"], g["cols"])
+    assert abs(v - g["printed"]) <= g["printed_precision"]
+    assert abs(v - (1 + 2 ** -9)) < 1e-12
+    g = gold["crvq_8p8x3_lam002"]
+    v = oracle.bits_per_weight_crvq(g["m"], g["e"], g["d"], g["lam"], g["rows"], g["cols"])
+    assert abs(v - 1.0678125) < 1e-9  # Eq. 8 as printed
+    v1 = g["e"] / g["d"] + (g["m"] - 1) * g["lam"] * g["e"] / g["d"] + 2 ** (g["e"] - 20) * 1 * g["d"]
+    assert abs(v1 - g["printed"]) <= g["printed_precision"]

@@ -1,0 +1,190 @@
+"""Benchmark: one CRVQ layer quantization per step on one MI355X.
+
+Workload: a LLaMA-7B attention projection, W 4096 x 4096 fp32 ~ N(0, 0.02), calibration activations
+2048 x 4096 with log-uniform per-channel scales, d = 8 (2,097,152 sub-vectors), one basic codebook of
+K = 65536 codewords fitted by one Lloyd iteration, the top 3 % of input channels (128) with one
+extended codebook of K = 256, greedy (beam width 1) residual search.  Inputs are seeded synthetic data
+resident in HBM before the timed region.
+
+A step runs the whole path: Hessian diagonal, channel importance, reorder, codebook init, assign +
+update + final assign with the basic codebook, critical residual, extended codebook fit, residual
+beam search, dequantization with the reverse reorder.
+
+value = nearest-codeword assignments against the K = 65536 codebook per second of step time (the
+basic assign passes over all vectors plus the beam's first stage over the critical vectors).
+
+Prints ONE JSON line.  Only N = 1 GPU is supported.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sub-vectors assigned/sec at K=65536,d=8 (1 GPU) + MFMA util % of peak"
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+WORKLOAD_ID = 2
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class EventTimer:
+    """HIP events (via torch, on the stream the library launches on) around selected library calls."""
+
+    def __init__(self, prefix):
+        import torch
+        self.torch = torch
+        self.prefix = prefix
+        self.pairs = []
+        self.open = None
+
+    def begin(self, name):
+        if name.startswith(self.prefix):
+            e = self.torch.cuda.Event(enable_timing=True)
+            e.record()
+            self.open = e
+
+    def end(self, name):
+        if name.startswith(self.prefix) and self.open is not None:
+            e = self.torch.cuda.Event(enable_timing=True)
+            e.record()
+            self.pairs.append((self.open, e))
+            self.open = None
+
+    def times_ms(self):
+        return [a.elapsed_time(b) for a, b in self.pairs]
+
+
+def file_sha(path):
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2412_09282_amd import crvq, inputs
+    from paper_2412_09282_amd.pipeline import LayerConfig, LayerQuantizer
+
+    crvq.lib(build_if_missing=True)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    wl = inputs.WORKLOADS[WORKLOAD_ID]
+    L = wl.layers[0]
+    M, N, d = L.M, L.N, wl.d
+    n = M * N // d
+    log(f"generating workload {WORKLOAD_ID}: W {M}x{N}, X {L.tokens}x{N}")
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    ncv_total = M * n_crit // d
+    base_idx = inputs.base_init_indices(wl, 0, n)
+    ext_idx = [inputs.ext_init_indices(wl, 0, t, ncv_total) for t in range(1, len(wl.K_ext) + 1)]
+    Wd = torch.from_numpy(W).to(dev)
+    Xd = torch.from_numpy(X).to(dev)
+    bi = torch.from_numpy(base_idx).to(dev)
+    ei = [torch.from_numpy(e).to(dev) for e in ext_idx]
+    cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
+    q = LayerQuantizer(M, N, torch.float32, cfg, L.tokens, device=dev)
+    torch.cuda.synchronize()
+
+    for i in range(args.warmup):
+        q.run(Wd, Xd, bi, ei)
+        torch.cuda.synchronize()
+        log(f"warmup step {i + 1}/{args.warmup} done")
+
+    timer = EventTimer("assign_base")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        st = q.run(Wd, Xd, bi, ei, timer=timer)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    log(f"timed {args.steps} steps")
+    step_s = (t1 - t0) / args.steps
+    assigns_per_step = n * (wl.iters + 1) + ncv_total  # K=65536 passes: Lloyd + final + beam stage 1
+    value = assigns_per_step / step_s
+
+    ev = timer.times_ms()
+    avg_ms = float(np.mean(ev))
+    flops_per_launch = 2.0 * wl.K_base * d * n
+    achieved_tflops = flops_per_launch / (avg_ms * 1e-3) / 1e12
+
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", "assign_k65536_traffic.json")
+    if os.path.exists(tpath):
+        tj = json.load(open(tpath))
+        if tj.get("source_sha") == file_sha(os.path.join(ROOT, "paper_2412_09282_amd", "csrc", "k_screen.hip")):
+            traffic = tj.get("bytes_per_launch")
+
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "sub-vectors/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": step_s * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "LLaMA-7B attention projection 4096x4096 fp32, d=8, K=65536 basic (1 Lloyd iter) "
+                               "+ 1 ext K=256 on top 3% channels, beam 1",
+                   "sub_vectors": n, "K": wl.K_base, "d": d, "critical_columns": n_crit,
+                   "assignments_per_step": assigns_per_step},
+        "roofline": {"bound": "mfma", "kernel": "crvq_assign (K=65536 screen + exact finalize)",
+                     "achieved": achieved_tflops, "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved_tflops / PEAK_FP32_MFMA_TFLOPS, "traffic": traffic,
+                     "avg_launch_ms": avg_ms, "launches": len(ev), "flop_per_launch": flops_per_launch},
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        oracle.build()
+        Cb = st.C_base.detach().cpu().numpy()
+        codes_gpu = st.codes.detach().cpu().numpy()
+        Vs = oracle.vectors(st.Ws.detach().cpu().numpy(), d)
+        # calibrate, then time a sample sized for about --cpu-seconds of oracle work
+        probe = inputs.sample_rows(wl, 0, n, 64)
+        tc = time.perf_counter()
+        oracle.assign(Vs[probe], Cb)
+        rate = 64 / max(time.perf_counter() - tc, 1e-6)
+        k = int(min(65536, max(256, rate * args.cpu_seconds)))
+        idx = inputs.sample_rows(wl, 0, n, k)
+        tc = time.perf_counter()
+        oc, _ = oracle.assign(Vs[idx], Cb)
+        dt_cpu = time.perf_counter() - tc
+        # the final basic codes of non-critical vectors are the last assign's; compare on those
+        g = idx % (N // d)
+        nc = g >= n_crit // d
+        mism = int((oc[nc] != codes_gpu[idx][nc]).sum())
+        out["cpu_baseline"] = {"value": k / dt_cpu, "unit": "sub-vectors/s", "cores": oracle.num_threads(),
+                               "kind": "oracle",
+                               "sample": f"{k} seeded sub-vectors assigned against the same K=65536 codebook "
+                                         f"(fp64 direct form, {dt_cpu:.1f} s)",
+                               "sample_code_mismatches": mism}
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

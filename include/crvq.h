@@ -1,0 +1,213 @@
+/*
+ * crvq.h -- C ABI of libcrvq, the MI355X (gfx950) hot path of CRVQ,
+ * "Channel-Relaxed Vector Quantization for Extreme Compression of LLMs"
+ * (arXiv 2412.09282).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Array arguments are DEVICE pointers owned by the caller.  The library
+ *   never allocates, frees or retains them after the call returns.  Arrays of
+ *   pointers (books, codes of several codebooks) are HOST arrays whose
+ *   entries are device pointers.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Work is enqueued on it asynchronously; the call returns after enqueue.
+ * - All arguments are validated on the host before anything is enqueued.  On
+ *   a validation error nothing runs, outputs are untouched and a nonzero
+ *   crvq_status is returned; crvq_last_error() gives the reason (thread-local
+ *   text).  No exception crosses the ABI and the library never aborts.
+ *   Launch failures return CRVQ_ERR_HIP.
+ * - Device-resident indices (codes, perm, initial-codeword indices) cannot be
+ *   checked on the host; every kernel bounds-checks them and treats an
+ *   out-of-range entry as documented per call (it never reads out of bounds).
+ * - Scratch memory comes from a caller-supplied `workspace` of at least the
+ *   size the matching *_workspace_size() function returns (256-byte aligned).
+ * - Layouts are row-major.  A codebook is K x d elements.  Codes are int32.
+ * - A "vector set" is the paper's sub-vector partition (Sec. 3.1 Eq. 1): a
+ *   matrix of n_rows rows is cut into vecs_per_row contiguous d-vectors per
+ *   row; vector v = r * vecs_per_row + g starts at element r * ld + g * d of
+ *   `X`.  The critical slab of a reordered matrix (its first n_crit columns,
+ *   Sec. 4.3) is the vector set with vecs_per_row = n_crit / d, ld = N.
+ * - Element types: CRVQ_F32 (float) and CRVQ_BF16 (bfloat16, stored as
+ *   uint16 bit patterns).  Floating-point inputs must be finite.
+ * - Results are deterministic: no floating-point atomics are used anywhere,
+ *   so equal inputs give bitwise-equal outputs.
+ */
+#ifndef CRVQ_H
+#define CRVQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CRVQ_OK = 0,
+  CRVQ_ERR_INVALID = 1,     /* a NULL required pointer or an out-of-range size / option */
+  CRVQ_ERR_UNSUPPORTED = 2, /* a valid request outside what this build implements */
+  CRVQ_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace_size() result */
+  CRVQ_ERR_HIP = 4          /* the HIP runtime reported an error while enqueueing */
+} crvq_status;
+
+typedef enum { CRVQ_F32 = 0, CRVQ_BF16 = 1 } crvq_dtype;
+typedef enum { CRVQ_REDUCE_SUM = 0, CRVQ_REDUCE_MAX = 1 } crvq_reduce;
+
+#define CRVQ_MAX_K 65536   /* codewords per codebook (e <= 16 bits) */
+#define CRVQ_MAX_D 16      /* sub-vector length */
+#define CRVQ_MAX_BEAM 16   /* residual beam width */
+#define CRVQ_MAX_BOOKS 8   /* basic + extended codebooks */
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int crvq_version(void);
+
+/* Text describing the last error returned on the calling thread ("" if none). */
+const char* crvq_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * crvq_channel_importance -- column (input-channel) reduction.
+ *
+ *   out[j] = s_j * R_{i < M} (A[i*lda + j] - B[i*ldb + j])^2,   j < N
+ *
+ * R = sum (CRVQ_REDUCE_SUM, accumulated in fp64) or max (CRVQ_REDUCE_MAX,
+ * exact); B may be NULL (treated as 0); scale may be NULL (s_j = 1).
+ * The paper's channel-importance metrics are modes of this one reduction:
+ *  - Hessian diagonal h_j = [X X^T]_jj (Appendix A.2 Eq. 9): A = the
+ *    calibration activations stored tokens x N, B = NULL, scale = NULL, SUM.
+ *  - W-only importance I_j = max_i w_ij^2 (Sec. 4.1): A = W, MAX.
+ *  - W-A importance (Sec. 4.1 Eq. 7 / Appendix A.2 Eq. 10): A = W,
+ *    B = the prequantized W, MAX, scale = h/2 (Eq. 10) or 1/(2[H^-1]_jj) (Eq. 7).
+ *  - Energy-weighted importance I_j = h_j * sum_i w_ij^2: A = W, SUM, scale = h.
+ * A, B: M x N matrices of `dtype` with leading dimensions lda, ldb >= N.
+ * scale: float[N] or NULL.  out: float[N] (fp32, rounded once from fp64).
+ * workspace: crvq_importance_workspace_size(M, N) bytes.
+ */
+size_t crvq_importance_workspace_size(int64_t M, int64_t N);
+crvq_status crvq_channel_importance(const void* A, int64_t lda, const void* B, int64_t ldb, int dtype,
+                                    int64_t M, int64_t N, const float* scale, int reduce, float* out,
+                                    void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_reorder -- channel reordering (Sec. 4.2, Alg. 1 ReorderChannels) and
+ * its reverse (Sec. 4.3 / Fig. 3 right).
+ *
+ * If importance != NULL, first writes perm[N]: the channels in descending
+ * importance, equal importance in ascending channel index, NaN last (a
+ * stable descending sort).  Otherwise perm is an input and must hold a
+ * permutation of 0..N-1.
+ * Then forward (inverse == 0):  out[r*ld_out + k]       = in[r*ld_in + perm[k]]
+ *      inverse (inverse != 0):  out[r*ld_out + perm[k]] = in[r*ld_in + k]
+ * for r < M, k < N.  in and out are M x N of `dtype`, must not overlap.
+ * in may be NULL (then only perm is computed; M is ignored).  An
+ * out-of-range perm entry leaves the affected output elements unwritten.
+ * workspace: crvq_reorder_workspace_size(N) bytes.
+ */
+size_t crvq_reorder_workspace_size(int64_t N);
+crvq_status crvq_reorder(const void* in, int64_t ld_in, void* out, int64_t ld_out, int dtype, int64_t M,
+                         int64_t N, const float* importance, int32_t* perm, int inverse, void* workspace,
+                         size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_assign -- nearest-codeword encoding (Sec. 3.1 Eq. 3-4; Alg. 1
+ * VectorQuant):  codes[v] = argmin_k ||x_v - C_k||_2, v < n_rows*vecs_per_row.
+ *
+ * Exact: the chosen k minimises the fp64 squared distance
+ * sum_t (x_vt - C_kt)^2 (t ascending); among equal distances the lowest k
+ * wins.  dist[v] (optional) = that fp64 distance rounded to float.
+ * X: vector set (see conventions) of x_dtype, d <= 16.
+ * C: K x d codebook of c_dtype, 1 <= K <= 65536.
+ * codes: int32[n]; dist: float[n] or NULL.
+ * workspace: crvq_assign_workspace_size(n, d, K) bytes.
+ */
+size_t crvq_assign_workspace_size(int64_t n_vectors, int32_t d, int64_t K);
+crvq_status crvq_assign(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                        int32_t d, const void* C, int c_dtype, int64_t K, int32_t* codes, float* dist,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_assign_residual_beam -- joint code choice over additive codebooks by
+ * beam search (Sec. 3.1 last paragraph; Sec. 4.3; Alg. 1 BeamSearchOptimize),
+ * under the squared Euclidean error of the residual.
+ *
+ * books[0] is the basic codebook, books[1..n_books-1] the extended ones, in
+ * the order they were fitted.  For each vector, starting from one empty
+ * tuple with residual x: for book t, every kept tuple (rank p, residual r)
+ * is extended by every codeword c of book t; a candidate's key is
+ * (sum_j (r_j - c_j)^2 in fp64, p, codeword index), the `beam` smallest keys
+ * survive in key order, and a survivor's residual is r - c (fp64).  The
+ * answer is the rank-0 tuple after the last book.  beam = 1 is the greedy
+ * additive fit of Alg. 1's extended-codebook loop.
+ * X: vector set of x_dtype.  books: host array of n_books device pointers,
+ * book t is Ks[t] x d of book_dtypes[t].  codes: host array of n_books
+ * device pointers; the code of vector v = r * vecs_per_row + g for book t is
+ * written to codes[t][r * ldc[t] + g] (ldc = NULL means ldc[t] = vecs_per_row;
+ * otherwise ldc[t] >= vecs_per_row, so the basic codes of a critical slab can
+ * land directly in the full matrix's code array).  err: float[n] (final
+ * squared error, vector order) or NULL.
+ * 1 <= beam <= 16, 1 <= n_books <= 8.
+ * workspace: crvq_beam_workspace_size(n, d, n_books, Ks, beam) bytes.
+ */
+size_t crvq_beam_workspace_size(int64_t n_vectors, int32_t d, int32_t n_books, const int64_t* Ks, int32_t beam);
+crvq_status crvq_assign_residual_beam(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row,
+                                      int64_t ld, int32_t d, int32_t n_books, const void* const* books,
+                                      const int32_t* book_dtypes, const int64_t* Ks, int32_t beam,
+                                      int32_t* const* codes, const int64_t* ldc, float* err, void* workspace,
+                                      size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_kmeans_update -- one Lloyd update of a K-means codebook (Sec. 3.1
+ * Eq. 2; Alg. 1 KMeansCodebook):
+ *
+ *   C[k] := mean{ x_v : codes[v] == k }  (fp64 sums, rounded to c_dtype
+ *   round-to-nearest-even); a codeword with no members is left unchanged.
+ *
+ * Atomic-free and deterministic: codes are stably counting-sorted, every
+ * centroid is a fixed-order fp64 reduction over its segment.  Codes outside
+ * [0, K) belong to no cluster.  counts: int32[K] member counts, or NULL.
+ * workspace: crvq_kmeans_workspace_size(n, d, K) bytes.
+ */
+size_t crvq_kmeans_workspace_size(int64_t n_vectors, int32_t d, int64_t K);
+crvq_status crvq_kmeans_update(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                               int32_t d, const int32_t* codes, int64_t K, void* C, int c_dtype,
+                               int32_t* counts, void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_gather_vectors -- out[k] = x_{idx[k]} for k < count (the K-means
+ * initial codewords drawn from the vector set, Alg. 1 KMeansCodebook).
+ * idx: int64[count] device array; an index outside [0, n) yields a NaN row.
+ * out: count x d of out_dtype (same as x_dtype, or F32 from BF16 widening).
+ */
+crvq_status crvq_gather_vectors(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                                int32_t d, const int64_t* idx, int64_t count, void* out, int out_dtype,
+                                void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_dequant -- additive reconstruction, the ComputeError / Update steps of
+ * Alg. 1, and the reverse reordering at inference (Sec. 4.3, Fig. 3 right).
+ *
+ * For an M x n_cols matrix in reordered channel order, vector (r, g), g <
+ * n_cols/d, is rebuilt as
+ *   R[r, g*d+t] = C_base[q_base[r*ldq_base+g]][t]
+ *                 + sum_{e < n_ext, g < n_crit/d} C_ext[e][q_ext[e][r*ldq_ext+g]][t]
+ * summed in fp64 in book order.  Then
+ *   minuend != NULL (residual mode):  out[r*ld_out + c] = minuend[r*ld_min + c] - R[r, c]
+ *   perm != NULL (reverse reorder):   out[r*ld_out + perm[c]] = R[r, c]
+ *   otherwise:                        out[r*ld_out + c] = R[r, c]
+ * each rounded once to out_dtype.  perm and minuend are mutually exclusive.
+ * n_crit is a multiple of d, 0 <= n_crit <= n_cols.  A code outside its
+ * codebook yields NaN for that vector.
+ * workspace: crvq_dequant_workspace_size(n_cols) bytes (only used with perm).
+ */
+size_t crvq_dequant_workspace_size(int64_t n_cols);
+crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, const int32_t* q_base,
+                         int64_t ldq_base, const void* C_base, int base_dtype, int64_t K_base, int32_t n_ext,
+                         const int32_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
+                         const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm,
+                         const void* minuend, int minuend_dtype, int64_t ld_min, void* out, int out_dtype,
+                         int64_t ld_out, void* workspace, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CRVQ_H */

@@ -1,0 +1,234 @@
+"""ctypes binding of libcrvq.so -- argument marshalling only.
+
+Every function below has the name of the C entry point it wraps (include/crvq.h)
+and does nothing but turn torch tensors into device pointers, sizes and dtype
+codes, allocate the scratch workspace the C call asks for (torch's caching
+allocator), pass the current HIP stream, and raise on a nonzero status.  All
+computation happens in the library's HIP kernels.  If the library cannot be
+loaded, every call raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import threading
+from typing import Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcrvq.so")
+_lock = threading.Lock()
+_lib = None
+
+CRVQ_F32, CRVQ_BF16 = 0, 1
+CRVQ_REDUCE_SUM, CRVQ_REDUCE_MAX = 0, 1
+STATUS = {0: "CRVQ_OK", 1: "CRVQ_ERR_INVALID", 2: "CRVQ_ERR_UNSUPPORTED", 3: "CRVQ_ERR_WORKSPACE", 4: "CRVQ_ERR_HIP"}
+
+
+class CrvqError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: {STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+def lib(build_if_missing: bool = True):
+    """Load libcrvq.so (building it first only if no built library exists)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                if not build_if_missing:
+                    raise OSError(f"{LIB_PATH} is not built")
+                from . import build as _build
+                _build.build(verbose=False)
+            L = ctypes.CDLL(LIB_PATH)
+            P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+            PP = ctypes.POINTER(ctypes.c_void_p)
+            sigs = {
+                "crvq_version": ([], ctypes.c_int),
+                "crvq_last_error": ([], ctypes.c_char_p),
+                "crvq_importance_workspace_size": ([I64, I64], SZ),
+                "crvq_channel_importance": ([P, I64, P, I64, ctypes.c_int, I64, I64, P, ctypes.c_int, P, P, SZ, P], ctypes.c_int),
+                "crvq_reorder_workspace_size": ([I64], SZ),
+                "crvq_reorder": ([P, I64, P, I64, ctypes.c_int, I64, I64, P, P, ctypes.c_int, P, SZ, P], ctypes.c_int),
+                "crvq_assign_workspace_size": ([I64, I32, I64], SZ),
+                "crvq_assign": ([P, ctypes.c_int, I64, I64, I64, I32, P, ctypes.c_int, I64, P, P, P, SZ, P], ctypes.c_int),
+                "crvq_beam_workspace_size": ([I64, I32, I32, P, I32], SZ),
+                "crvq_assign_residual_beam": ([P, ctypes.c_int, I64, I64, I64, I32, I32, PP, P, P, I32, PP, P, P, P, SZ, P],
+                                              ctypes.c_int),
+                "crvq_kmeans_workspace_size": ([I64, I32, I64], SZ),
+                "crvq_kmeans_update": ([P, ctypes.c_int, I64, I64, I64, I32, P, I64, P, ctypes.c_int, P, P, SZ, P], ctypes.c_int),
+                "crvq_gather_vectors": ([P, ctypes.c_int, I64, I64, I64, I32, P, I64, P, ctypes.c_int, P], ctypes.c_int),
+                "crvq_dequant_workspace_size": ([I64], SZ),
+                "crvq_dequant": ([I64, I64, I32, I64, P, I64, P, ctypes.c_int, I64, I32, PP, I64, PP, P, P, P, P, ctypes.c_int,
+                                  I64, P, ctypes.c_int, I64, P, SZ, P], ctypes.c_int),
+            }
+            for name, (args, res) in sigs.items():
+                f = getattr(L, name)
+                f.argtypes = args
+                f.restype = res
+            _lib = L
+    return _lib
+
+
+# ------------------------------------------------------------------------------------------------
+# marshalling helpers
+# ------------------------------------------------------------------------------------------------
+
+def dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return CRVQ_F32
+    if t.dtype == torch.bfloat16:
+        return CRVQ_BF16
+    raise TypeError(f"unsupported element type {t.dtype}")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(fn: str, status: int):
+    if status != 0:
+        raise CrvqError(fn, status, lib().crvq_last_error().decode())
+
+
+def _workspace(nbytes: int, device) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return None
+    ws = torch.empty(int(nbytes), dtype=torch.uint8, device=device)
+    assert ws.data_ptr() % 256 == 0
+    return ws
+
+
+def _ptr_array(ts: Sequence[torch.Tensor]):
+    arr = (ctypes.c_void_p * max(1, len(ts)))()
+    for i, t in enumerate(ts):
+        arr[i] = t.data_ptr()
+    return arr
+
+
+@dataclasses.dataclass
+class VecSet:
+    """The paper's sub-vector partition (Sec. 3.1 Eq. 1) of a row-major matrix view: n_rows rows of
+    vecs_per_row contiguous d-vectors, row stride ld elements."""
+    t: torch.Tensor
+    n_rows: int
+    vecs_per_row: int
+    ld: int
+    d: int
+
+    @staticmethod
+    def of_matrix(W: torch.Tensor, d: int, n_cols: Optional[int] = None) -> "VecSet":
+        assert W.dim() == 2 and W.stride(1) == 1
+        n_cols = W.shape[1] if n_cols is None else n_cols
+        return VecSet(W, W.shape[0], n_cols // d, W.stride(0), d)
+
+    @staticmethod
+    def of_vectors(V: torch.Tensor) -> "VecSet":
+        assert V.dim() == 2 and V.is_contiguous()
+        return VecSet(V, V.shape[0], 1, V.shape[1], V.shape[1])
+
+    @property
+    def n(self) -> int:
+        return self.n_rows * self.vecs_per_row
+
+    def args(self):
+        return (_ptr(self.t), dtype_code(self.t), self.n_rows, self.vecs_per_row, self.ld, self.d)
+
+
+# ------------------------------------------------------------------------------------------------
+# the C entry points
+# ------------------------------------------------------------------------------------------------
+
+def crvq_version() -> int:
+    return int(lib().crvq_version())
+
+
+def crvq_channel_importance(A: torch.Tensor, out: torch.Tensor, B: Optional[torch.Tensor] = None,
+                            scale: Optional[torch.Tensor] = None, reduce: int = CRVQ_REDUCE_SUM, stream=None) -> None:
+    L = lib()
+    M, N = A.shape
+    assert A.stride(1) == 1 and (B is None or (B.stride(1) == 1 and B.dtype == A.dtype))
+    ws = _workspace(L.crvq_importance_workspace_size(M, N), A.device)
+    _check("crvq_channel_importance", L.crvq_channel_importance(
+        _ptr(A), A.stride(0), _ptr(B), 0 if B is None else B.stride(0), dtype_code(A), M, N, _ptr(scale), reduce,
+        _ptr(out), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_reorder(inp: Optional[torch.Tensor], out: Optional[torch.Tensor], perm: torch.Tensor,
+                 importance: Optional[torch.Tensor] = None, inverse: bool = False, stream=None) -> None:
+    L = lib()
+    N = perm.numel()
+    M = 0 if inp is None else inp.shape[0]
+    dev = perm.device
+    ws = _workspace(L.crvq_reorder_workspace_size(N), dev) if inverse else None
+    _check("crvq_reorder", L.crvq_reorder(
+        _ptr(inp), 0 if inp is None else inp.stride(0), _ptr(out), 0 if out is None else out.stride(0),
+        CRVQ_F32 if inp is None else dtype_code(inp), M, N, _ptr(importance), _ptr(perm), int(bool(inverse)),
+        _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_assign(X: VecSet, C: torch.Tensor, codes: torch.Tensor, dist: Optional[torch.Tensor] = None,
+                stream=None) -> None:
+    L = lib()
+    K = C.shape[0]
+    ws = _workspace(L.crvq_assign_workspace_size(X.n, X.d, K), C.device)
+    _check("crvq_assign", L.crvq_assign(*X.args(), _ptr(C), dtype_code(C), K, _ptr(codes), _ptr(dist), _ptr(ws),
+                                        0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_assign_residual_beam(X: VecSet, books: Sequence[torch.Tensor], beam: int, codes: Sequence[torch.Tensor],
+                              err: Optional[torch.Tensor] = None, ldc: Optional[Sequence[int]] = None,
+                              stream=None) -> None:
+    L = lib()
+    nb = len(books)
+    ldc_arr = None if ldc is None else (ctypes.c_int64 * nb)(*ldc)
+    Ks = (ctypes.c_int64 * nb)(*[b.shape[0] for b in books])
+    dts = (ctypes.c_int32 * nb)(*[dtype_code(b) for b in books])
+    ws = _workspace(L.crvq_beam_workspace_size(X.n, X.d, nb, ctypes.cast(Ks, ctypes.c_void_p), beam), books[0].device)
+    _check("crvq_assign_residual_beam", L.crvq_assign_residual_beam(
+        *X.args(), nb, ctypes.cast(_ptr_array(books), ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(dts, ctypes.c_void_p),
+        ctypes.cast(Ks, ctypes.c_void_p), beam, ctypes.cast(_ptr_array(codes), ctypes.POINTER(ctypes.c_void_p)),
+        None if ldc_arr is None else ctypes.cast(ldc_arr, ctypes.c_void_p),
+        _ptr(err), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_kmeans_update(X: VecSet, codes: torch.Tensor, C: torch.Tensor, counts: Optional[torch.Tensor] = None,
+                       stream=None) -> None:
+    L = lib()
+    K = C.shape[0]
+    ws = _workspace(L.crvq_kmeans_workspace_size(X.n, X.d, K), C.device)
+    _check("crvq_kmeans_update", L.crvq_kmeans_update(*X.args(), _ptr(codes), K, _ptr(C), dtype_code(C), _ptr(counts),
+                                                      _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_gather_vectors(X: VecSet, idx: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    _check("crvq_gather_vectors", lib().crvq_gather_vectors(*X.args(), _ptr(idx), idx.numel(), _ptr(out),
+                                                            dtype_code(out), _stream(stream)))
+
+
+def crvq_dequant(M: int, n_cols: int, d: int, q_base: torch.Tensor, ldq_base: int, C_base: torch.Tensor,
+                 out: torch.Tensor, n_crit: int = 0, q_ext: Sequence[torch.Tensor] = (), ldq_ext: int = 0,
+                 C_ext: Sequence[torch.Tensor] = (), perm: Optional[torch.Tensor] = None,
+                 minuend: Optional[torch.Tensor] = None, stream=None) -> None:
+    L = lib()
+    ne = len(C_ext)
+    ws = _workspace(L.crvq_dequant_workspace_size(n_cols), out.device) if perm is not None else None
+    dts = (ctypes.c_int32 * max(1, ne))(*[dtype_code(c) for c in C_ext])
+    Ks = (ctypes.c_int64 * max(1, ne))(*[c.shape[0] for c in C_ext])
+    _check("crvq_dequant", L.crvq_dequant(
+        M, n_cols, d, n_crit, _ptr(q_base), ldq_base, _ptr(C_base), dtype_code(C_base), C_base.shape[0], ne,
+        ctypes.cast(_ptr_array(q_ext), ctypes.POINTER(ctypes.c_void_p)) if ne else None, ldq_ext,
+        ctypes.cast(_ptr_array(C_ext), ctypes.POINTER(ctypes.c_void_p)) if ne else None,
+        ctypes.cast(dts, ctypes.c_void_p) if ne else None, ctypes.cast(Ks, ctypes.c_void_p) if ne else None,
+        _ptr(perm), _ptr(minuend), CRVQ_F32 if minuend is None else dtype_code(minuend),
+        0 if minuend is None else minuend.stride(0), _ptr(out), dtype_code(out), out.stride(0), _ptr(ws),
+        0 if ws is None else ws.numel(), _stream(stream)))

@@ -1,0 +1,406 @@
+// Host side of the libcrvq C ABI: argument validation (before anything is enqueued), workspace
+// sizing, and dispatch to the kernel launchers.  See include/crvq.h for the contract of each call.
+#include "crvq.h"
+#include "crvq_internal.h"
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+using namespace crvq;
+
+namespace {
+
+thread_local std::string g_err;
+
+crvq_status fail(crvq_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+crvq_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return CRVQ_OK;
+  return fail(CRVQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool dtype_ok(int t) { return t == CRVQ_F32 || t == CRVQ_BF16; }
+int esize(int t) { return t == CRVQ_F32 ? 4 : 2; }
+
+crvq_status check_vectors(const void* X, int dtype, int64_t n_rows, int64_t vpr, int64_t ld, int32_t d,
+                          const char* fn) {
+  if (!dtype_ok(dtype)) return fail(CRVQ_ERR_INVALID, "%s: x_dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, dtype);
+  if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
+  if (n_rows < 0 || vpr < 0) return fail(CRVQ_ERR_INVALID, "%s: negative n_rows or vecs_per_row", fn);
+  if (ld < vpr * d) return fail(CRVQ_ERR_INVALID, "%s: ld = %lld < vecs_per_row * d = %lld", fn, (long long)ld,
+                                (long long)(vpr * d));
+  const int64_t n = n_rows * vpr;
+  if (n > 0x7fffffffLL) return fail(CRVQ_ERR_UNSUPPORTED, "%s: %lld vectors exceed 2^31 - 1", fn, (long long)n);
+  if (n > 0 && !X) return fail(CRVQ_ERR_INVALID, "%s: X is NULL", fn);
+  return CRVQ_OK;
+}
+
+crvq_status check_K(int64_t K, const char* fn, const char* what) {
+  if (K < 1 || K > CRVQ_MAX_K) return fail(CRVQ_ERR_INVALID, "%s: %s = %lld outside [1, %d]", fn, what, (long long)K, CRVQ_MAX_K);
+  return CRVQ_OK;
+}
+
+crvq_status check_ws(void* ws, size_t have, size_t need, const char* fn) {
+  if (need == 0) return CRVQ_OK;
+  if (!ws || have < need)
+    return fail(CRVQ_ERR_WORKSPACE, "%s: workspace of %zu bytes needed, %zu given%s", fn, need, ws ? have : 0,
+                ws ? "" : " (NULL)");
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return fail(CRVQ_ERR_WORKSPACE, "%s: workspace is not 256-byte aligned", fn);
+  return CRVQ_OK;
+}
+
+RowSrc vec_src(const void* X, int dtype, int64_t n_rows, int64_t vpr, int64_t ld, int32_t d) {
+  RowSrc s;
+  s.base = X;
+  s.type = dtype;
+  s.d = d;
+  s.vpr = vpr > 0 ? vpr : 1;
+  s.ld = ld;
+  s.n = n_rows * vpr;
+  return s;
+}
+
+size_t assign_ws(int64_t n, int32_t d, int64_t K) {
+  WsCursor c(nullptr);
+  ScreenPlan p = plan_screen(n, d, K, 1);
+  carve_screen(c, p, n, K);
+  return c.used;
+}
+
+size_t beam_screen_bytes(int64_t n, int32_t d, int32_t n_books, const int64_t* Ks, int32_t beam) {
+  size_t mx = 0;
+  int64_t n_par = 1;
+  for (int t = 0; t < n_books; ++t) {
+    WsCursor c(nullptr);
+    const int64_t rows = n * n_par;
+    ScreenPlan p = plan_screen(rows, d, Ks[t], beam);
+    carve_screen(c, p, rows, Ks[t]);
+    if (c.used > mx) mx = c.used;
+    const int64_t nn = n_par * Ks[t];
+    n_par = nn < beam ? nn : beam;
+  }
+  return mx;
+}
+
+struct BeamWs {
+  double* res[2];
+  int* tup[2];
+  double* err;
+  double* rowD;
+  int* rowK;
+  char* screen;
+};
+
+BeamWs carve_beam(WsCursor& c, int64_t n, int32_t d, int32_t n_books, int32_t beam, size_t screen_bytes) {
+  BeamWs w;
+  const size_t nb = static_cast<size_t>(n) * beam;
+  for (int b = 0; b < 2; ++b) {
+    w.res[b] = c.take<double>(nb * d);
+    w.tup[b] = c.take<int>(nb * n_books);
+  }
+  w.err = c.take<double>(nb);
+  w.rowD = c.take<double>(nb * beam);
+  w.rowK = c.take<int>(nb * beam);
+  w.screen = c.take<char>(screen_bytes);
+  return w;
+}
+
+bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + bn && pb < pa + an;
+}
+
+}  // namespace
+
+extern "C" {
+
+int crvq_version(void) { return 100; }
+
+const char* crvq_last_error(void) { return g_err.c_str(); }
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_importance_workspace_size(int64_t M, int64_t N) {
+  if (M < 1 || N < 1) return 0;
+  return colreduce_ws_bytes(M, N);
+}
+
+crvq_status crvq_channel_importance(const void* A, int64_t lda, const void* B, int64_t ldb, int dtype, int64_t M,
+                                    int64_t N, const float* scale, int reduce, float* out, void* workspace,
+                                    size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_channel_importance";
+  g_err.clear();
+  if (!dtype_ok(dtype)) return fail(CRVQ_ERR_INVALID, "%s: dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, dtype);
+  if (M < 1 || N < 1) return fail(CRVQ_ERR_INVALID, "%s: M and N must be >= 1 (got %lld, %lld)", fn, (long long)M, (long long)N);
+  if (!A || !out) return fail(CRVQ_ERR_INVALID, "%s: A and out must not be NULL", fn);
+  if (lda < N) return fail(CRVQ_ERR_INVALID, "%s: lda < N", fn);
+  if (B && ldb < N) return fail(CRVQ_ERR_INVALID, "%s: ldb < N", fn);
+  if (reduce != CRVQ_REDUCE_SUM && reduce != CRVQ_REDUCE_MAX) return fail(CRVQ_ERR_INVALID, "%s: unknown reduce %d", fn, reduce);
+  crvq_status s = check_ws(workspace, ws_bytes, colreduce_ws_bytes(M, N), fn);
+  if (s) return s;
+  return hip_status(launch_colreduce(A, lda, B, ldb, dtype, M, N, scale, reduce, out, workspace,
+                                     static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_reorder_workspace_size(int64_t N) { return N < 1 ? 0 : align256(static_cast<size_t>(N) * 4); }
+
+crvq_status crvq_reorder(const void* in, int64_t ld_in, void* out, int64_t ld_out, int dtype, int64_t M, int64_t N,
+                         const float* importance, int32_t* perm, int inverse, void* workspace, size_t ws_bytes,
+                         void* stream) {
+  static const char* fn = "crvq_reorder";
+  g_err.clear();
+  if (N < 1 || N > (1LL << 24)) return fail(CRVQ_ERR_INVALID, "%s: N = %lld outside [1, 2^24]", fn, (long long)N);
+  if (!perm) return fail(CRVQ_ERR_INVALID, "%s: perm must not be NULL", fn);
+  if (!importance && !in) return fail(CRVQ_ERR_INVALID, "%s: nothing to do (importance and in are both NULL)", fn);
+  if (in) {
+    if (!dtype_ok(dtype)) return fail(CRVQ_ERR_INVALID, "%s: dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, dtype);
+    if (M < 0) return fail(CRVQ_ERR_INVALID, "%s: M < 0", fn);
+    if (!out) return fail(CRVQ_ERR_INVALID, "%s: out must not be NULL", fn);
+    if (ld_in < N || ld_out < N) return fail(CRVQ_ERR_INVALID, "%s: ld_in and ld_out must be >= N", fn);
+    if (M > 0) {
+      const size_t es = esize(dtype);
+      const size_t span_in = static_cast<size_t>((M - 1) * ld_in + N) * es;
+      const size_t span_out = static_cast<size_t>((M - 1) * ld_out + N) * es;
+      if (overlaps(in, span_in, out, span_out)) return fail(CRVQ_ERR_INVALID, "%s: in and out overlap", fn);
+    }
+    if (inverse) {
+      crvq_status s = check_ws(workspace, ws_bytes, crvq_reorder_workspace_size(N), fn);
+      if (s) return s;
+    }
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (importance) {
+    crvq_status s = hip_status(launch_rank_perm(importance, N, perm, st), fn);
+    if (s) return s;
+  }
+  if (!in || M == 0) return CRVQ_OK;
+  const int32_t* src = perm;
+  if (inverse) {
+    int32_t* inv = static_cast<int32_t*>(workspace);
+    crvq_status s = hip_status(launch_inverse_perm(perm, N, inv, st), fn);
+    if (s) return s;
+    src = inv;
+  }
+  return hip_status(launch_gather_columns(in, ld_in, out, ld_out, esize(dtype), M, N, src, st), fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_assign_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
+  if (n_vectors < 1 || d < 1 || d > CRVQ_MAX_D || K < 1 || K > CRVQ_MAX_K) return 0;
+  return assign_ws(n_vectors, d, K);
+}
+
+crvq_status crvq_assign(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
+                        const void* C, int c_dtype, int64_t K, int32_t* codes, float* dist, void* workspace,
+                        size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_assign";
+  g_err.clear();
+  crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
+  if (s) return s;
+  if (!dtype_ok(c_dtype)) return fail(CRVQ_ERR_INVALID, "%s: c_dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, c_dtype);
+  if ((s = check_K(K, fn, "K"))) return s;
+  if (!C) return fail(CRVQ_ERR_INVALID, "%s: C must not be NULL", fn);
+  const int64_t n = n_rows * vecs_per_row;
+  if (n > 0 && !codes) return fail(CRVQ_ERR_INVALID, "%s: codes must not be NULL", fn);
+  if (n == 0) return CRVQ_OK;
+  if ((s = check_ws(workspace, ws_bytes, assign_ws(n, d, K), fn))) return s;
+  RowSrc src = vec_src(X, x_dtype, n_rows, vecs_per_row, ld, d);
+  ScreenPlan p = plan_screen(n, d, K, 1);
+  WsCursor c(workspace);
+  ScreenWs w = carve_screen(c, p, n, K);
+  return hip_status(launch_screen(src, C, c_dtype, K, 1, p, w, codes, dist, nullptr, nullptr,
+                                  static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_beam_workspace_size(int64_t n_vectors, int32_t d, int32_t n_books, const int64_t* Ks, int32_t beam) {
+  if (n_vectors < 1 || d < 1 || d > CRVQ_MAX_D || n_books < 1 || n_books > CRVQ_MAX_BOOKS || !Ks || beam < 1 ||
+      beam > CRVQ_MAX_BEAM)
+    return 0;
+  for (int t = 0; t < n_books; ++t)
+    if (Ks[t] < 1 || Ks[t] > CRVQ_MAX_K) return 0;
+  const size_t sb = beam_screen_bytes(n_vectors, d, n_books, Ks, beam);
+  WsCursor c(nullptr);
+  carve_beam(c, n_vectors, d, n_books, beam, sb);
+  return c.used;
+}
+
+crvq_status crvq_assign_residual_beam(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                                      int32_t d, int32_t n_books, const void* const* books, const int32_t* book_dtypes,
+                                      const int64_t* Ks, int32_t beam, int32_t* const* codes, const int64_t* ldc,
+                                      float* err, void* workspace, size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_assign_residual_beam";
+  g_err.clear();
+  crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
+  if (s) return s;
+  if (n_books < 1 || n_books > CRVQ_MAX_BOOKS)
+    return fail(CRVQ_ERR_INVALID, "%s: n_books = %d outside [1, %d]", fn, n_books, CRVQ_MAX_BOOKS);
+  if (beam < 1 || beam > CRVQ_MAX_BEAM) return fail(CRVQ_ERR_INVALID, "%s: beam = %d outside [1, %d]", fn, beam, CRVQ_MAX_BEAM);
+  if (!books || !book_dtypes || !Ks || !codes) return fail(CRVQ_ERR_INVALID, "%s: books, book_dtypes, Ks and codes must not be NULL", fn);
+  for (int t = 0; t < n_books; ++t) {
+    if (!books[t] || !codes[t]) return fail(CRVQ_ERR_INVALID, "%s: books[%d] or codes[%d] is NULL", fn, t, t);
+    if (!dtype_ok(book_dtypes[t])) return fail(CRVQ_ERR_INVALID, "%s: book_dtypes[%d] = %d invalid", fn, t, book_dtypes[t]);
+    if ((s = check_K(Ks[t], fn, "Ks[t]"))) return s;
+    if (ldc && ldc[t] < vecs_per_row) return fail(CRVQ_ERR_INVALID, "%s: ldc[%d] < vecs_per_row", fn, t);
+  }
+  const int64_t n = n_rows * vecs_per_row;
+  if (n == 0) return CRVQ_OK;
+  const size_t sb = beam_screen_bytes(n, d, n_books, Ks, beam);
+  {
+    WsCursor dry(nullptr);
+    carve_beam(dry, n, d, n_books, beam, sb);
+    if ((s = check_ws(workspace, ws_bytes, dry.used, fn))) return s;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  WsCursor c(workspace);
+  BeamWs w = carve_beam(c, n, d, n_books, beam, sb);
+  const RowSrc src0 = vec_src(X, x_dtype, n_rows, vecs_per_row, ld, d);
+  int64_t n_par = 1;
+  int cur = 0;
+  for (int t = 0; t < n_books; ++t) {
+    const int64_t rows = n * n_par;
+    RowSrc src = src0;
+    if (t > 0) {
+      src.base = w.res[cur];
+      src.type = ET_F64;
+      src.vpr = 1;
+      src.ld = d;
+      src.n = rows;
+    }
+    ScreenPlan p = plan_screen(rows, d, Ks[t], beam);
+    WsCursor sc(w.screen);
+    ScreenWs sw = carve_screen(sc, p, rows, Ks[t]);
+    hipError_t e = launch_screen(src, books[t], book_dtypes[t], Ks[t], beam, p, sw, nullptr, nullptr, w.rowD, w.rowK, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+    e = launch_beam_merge(n, static_cast<int>(n_par), beam, t, n_books, w.rowD, w.rowK, src0, w.res[cur], w.res[cur ^ 1],
+                          w.tup[cur], w.tup[cur ^ 1], w.err, books[t], book_dtypes[t], Ks[t], d, st);
+    if (e != hipSuccess) return hip_status(e, fn);
+    const int64_t nn = n_par * Ks[t];
+    n_par = nn < beam ? nn : beam;
+    cur ^= 1;
+  }
+  CodePtrs outs = {};
+  for (int t = 0; t < n_books; ++t) {
+    outs.q[t] = codes[t];
+    outs.ld[t] = ldc ? ldc[t] : vecs_per_row;
+  }
+  return hip_status(launch_beam_emit(n, vecs_per_row, static_cast<int>(n_par), n_books, w.tup[cur], w.err, outs, err, st),
+                    fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_kmeans_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
+  (void)d;
+  if (n_vectors < 0 || K < 1 || K > CRVQ_MAX_K) return 0;
+  return kmeans_ws_bytes(n_vectors, K);
+}
+
+crvq_status crvq_kmeans_update(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
+                               const int32_t* codes, int64_t K, void* C, int c_dtype, int32_t* counts, void* workspace,
+                               size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_kmeans_update";
+  g_err.clear();
+  crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
+  if (s) return s;
+  if ((s = check_K(K, fn, "K"))) return s;
+  if (!C) return fail(CRVQ_ERR_INVALID, "%s: C must not be NULL", fn);
+  if (!dtype_ok(c_dtype)) return fail(CRVQ_ERR_INVALID, "%s: c_dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, c_dtype);
+  const int64_t n = n_rows * vecs_per_row;
+  if (n > 0 && !codes) return fail(CRVQ_ERR_INVALID, "%s: codes must not be NULL", fn);
+  if ((s = check_ws(workspace, ws_bytes, kmeans_ws_bytes(n, K), fn))) return s;
+  return hip_status(launch_kmeans_update(vec_src(X, x_dtype, n_rows, vecs_per_row, ld, d), codes, K, C, c_dtype, counts,
+                                         workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+crvq_status crvq_gather_vectors(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                                int32_t d, const int64_t* idx, int64_t count, void* out, int out_dtype, void* stream) {
+  static const char* fn = "crvq_gather_vectors";
+  g_err.clear();
+  crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
+  if (s) return s;
+  if (count < 0) return fail(CRVQ_ERR_INVALID, "%s: count < 0", fn);
+  if (out_dtype != x_dtype && !(x_dtype == CRVQ_BF16 && out_dtype == CRVQ_F32))
+    return fail(CRVQ_ERR_INVALID, "%s: out_dtype must equal x_dtype (or be F32 for BF16 input)", fn);
+  if (count == 0) return CRVQ_OK;
+  if (!idx || !out) return fail(CRVQ_ERR_INVALID, "%s: idx and out must not be NULL", fn);
+  return hip_status(launch_gather_vectors(vec_src(X, x_dtype, n_rows, vecs_per_row, ld, d), idx, count, out, out_dtype,
+                                          static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_dequant_workspace_size(int64_t n_cols) { return n_cols < 1 ? 0 : align256(static_cast<size_t>(n_cols) * 4); }
+
+crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, const int32_t* q_base,
+                         int64_t ldq_base, const void* C_base, int base_dtype, int64_t K_base, int32_t n_ext,
+                         const int32_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
+                         const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* minuend,
+                         int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out, void* workspace,
+                         size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_dequant";
+  g_err.clear();
+  if (M < 0 || n_cols < 1) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and n_cols >= 1", fn);
+  if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
+  if (n_cols % d) return fail(CRVQ_ERR_INVALID, "%s: n_cols = %lld is not a multiple of d = %d", fn, (long long)n_cols, d);
+  if (n_crit < 0 || n_crit > n_cols || n_crit % d)
+    return fail(CRVQ_ERR_INVALID, "%s: n_crit = %lld must be a multiple of d in [0, n_cols]", fn, (long long)n_crit);
+  if (!q_base || !C_base || !out) return fail(CRVQ_ERR_INVALID, "%s: q_base, C_base and out must not be NULL", fn);
+  if (!dtype_ok(base_dtype) || !dtype_ok(out_dtype)) return fail(CRVQ_ERR_INVALID, "%s: invalid base or out dtype", fn);
+  crvq_status s = check_K(K_base, fn, "K_base");
+  if (s) return s;
+  if (ldq_base < n_cols / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_base < n_cols / d", fn);
+  if (n_ext < 0 || n_ext > CRVQ_MAX_BOOKS - 1) return fail(CRVQ_ERR_INVALID, "%s: n_ext = %d outside [0, %d]", fn, n_ext, CRVQ_MAX_BOOKS - 1);
+  if (ld_out < n_cols) return fail(CRVQ_ERR_INVALID, "%s: ld_out < n_cols", fn);
+  if (perm && minuend) return fail(CRVQ_ERR_INVALID, "%s: perm and minuend are mutually exclusive", fn);
+  if (minuend) {
+    if (!dtype_ok(minuend_dtype)) return fail(CRVQ_ERR_INVALID, "%s: invalid minuend dtype", fn);
+    if (ld_min < n_cols) return fail(CRVQ_ERR_INVALID, "%s: ld_min < n_cols", fn);
+  }
+  DequantBooks b = {};
+  b.C[0] = C_base;
+  b.q[0] = q_base;
+  b.type[0] = base_dtype;
+  b.K[0] = K_base;
+  b.n = 1 + n_ext;
+  b.ldq_base = ldq_base;
+  b.ldq_ext = ldq_ext;
+  if (n_ext > 0) {
+    if (!q_ext || !C_ext || !ext_dtypes || !K_ext)
+      return fail(CRVQ_ERR_INVALID, "%s: q_ext, C_ext, ext_dtypes and K_ext must not be NULL when n_ext > 0", fn);
+    if (ldq_ext < n_crit / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_ext < n_crit / d", fn);
+    for (int e = 0; e < n_ext; ++e) {
+      if (!q_ext[e] || !C_ext[e]) return fail(CRVQ_ERR_INVALID, "%s: q_ext[%d] or C_ext[%d] is NULL", fn, e, e);
+      if (!dtype_ok(ext_dtypes[e])) return fail(CRVQ_ERR_INVALID, "%s: ext_dtypes[%d] invalid", fn, e);
+      if ((s = check_K(K_ext[e], fn, "K_ext[e]"))) return s;
+      b.C[e + 1] = C_ext[e];
+      b.q[e + 1] = q_ext[e];
+      b.type[e + 1] = ext_dtypes[e];
+      b.K[e + 1] = K_ext[e];
+    }
+  }
+  if (perm && (s = check_ws(workspace, ws_bytes, crvq_dequant_workspace_size(n_cols), fn))) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t* inv = nullptr;
+  if (perm) {
+    inv = static_cast<int32_t*>(workspace);
+    if ((s = hip_status(launch_inverse_perm(perm, n_cols, inv, st), fn))) return s;
+  }
+  return hip_status(launch_dequant(M, n_cols, d, n_crit, b, inv, minuend, minuend_dtype, ld_min, out, out_dtype, ld_out, st),
+                    fn);
+}
+
+}  // extern "C"

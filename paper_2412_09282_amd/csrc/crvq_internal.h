@@ -1,0 +1,119 @@
+// Internal declarations shared by the host API and the kernel translation units of libcrvq.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace crvq {
+
+enum ElemType : int { ET_F32 = 0, ET_BF16 = 1, ET_F64 = 2 };
+
+constexpr int kMaxBeam = 16;
+constexpr int kMaxBooks = 8;
+
+// Output code arrays of the beam search, one per codebook.
+struct CodePtrs {
+  int32_t* q[kMaxBooks];
+  int64_t ld[kMaxBooks];
+};
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Bump allocator over a caller-supplied workspace (or a dry run that only measures).
+struct WsCursor {
+  char* base;
+  size_t used = 0;
+  explicit WsCursor(void* b) : base(static_cast<char*>(b)) {}
+  template <class T>
+  T* take(size_t count) {
+    size_t off = used;
+    used = align256(used + count * sizeof(T));
+    return base ? reinterpret_cast<T*>(base + off) : nullptr;
+  }
+};
+
+// A set of rows of length d read by the distance kernels.  Either a vector set over a matrix
+// (ET_F32 / ET_BF16: row v = r * vpr + g at element r * ld + g * d) or a dense fp64 array of
+// rows (ET_F64: row v at element v * d).
+struct RowSrc {
+  const void* base;
+  int type;
+  int d;
+  int64_t vpr;
+  int64_t ld;
+  int64_t n;
+};
+
+// ---- codebook screen (k_screen.hip) -------------------------------------------------------------
+struct ScreenPlan {
+  int nb;            // best tiles tracked per lane (power of two >= requested top count)
+  int cb;            // 16-row column blocks per wave
+  int ks;            // 4-wide K steps of the fp32 MFMA (ceil(d / 4))
+  int64_t tiles;     // 16-codeword tiles (ceil(K / 16))
+  int64_t grid_x;    // row groups
+  int splits;        // codebook splits (grid y)
+  int64_t tiles_per_split;
+};
+ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top);
+
+struct ScreenWs {
+  float* apack;
+  float* cnp;
+  double* pD;
+  int* pK;
+  float* pR;
+  double* xn2;
+};
+// Carves the screen's scratch out of `ws`; returns it (pointers null on a dry run).
+ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc);
+
+// Prepares the codebook, runs the MFMA screen and the exact finalize (with rescue).  When
+// out_codes != nullptr (top == 1) writes codes / dist; otherwise writes the sorted top-`top`
+// (D, k) lists per row to rowD / rowK (row-major [n_rows][top]).
+hipError_t launch_screen(const RowSrc& src, const void* C, int c_type, int64_t K, int top, const ScreenPlan& p,
+                         const ScreenWs& w, int32_t* out_codes, float* out_dist, double* rowD, int* rowK,
+                         hipStream_t stream);
+
+// Beam bookkeeping kernels.
+hipError_t launch_beam_merge(int64_t n, int n_par, int beam, int step, int n_books, const double* rowD,
+                             const int* rowK, const RowSrc& src0, const double* res_in, double* res_out,
+                             const int* tup_in, int* tup_out, double* err_out, const void* book, int book_type,
+                             int64_t K, int d, hipStream_t stream);
+hipError_t launch_beam_emit(int64_t n, int64_t vpr, int n_par, int n_books, const int* tup, const double* err,
+                            const CodePtrs& outs, float* err_out, hipStream_t stream);
+
+// ---- K-means update (k_kmeans.hip) -------------------------------------------------------------
+size_t kmeans_ws_bytes(int64_t n, int64_t K);
+hipError_t launch_kmeans_update(const RowSrc& src, const int32_t* codes, int64_t K, void* C, int c_type,
+                                int32_t* counts, void* ws, hipStream_t stream);
+
+// ---- column reduction (k_colreduce.hip) --------------------------------------------------------
+size_t colreduce_ws_bytes(int64_t M, int64_t N);
+hipError_t launch_colreduce(const void* A, int64_t lda, const void* B, int64_t ldb, int type, int64_t M, int64_t N,
+                            const float* scale, int reduce, float* out, void* ws, hipStream_t stream);
+
+// ---- reorder / gathers (k_reorder.hip) -----------------------------------------------------------
+hipError_t launch_rank_perm(const float* importance, int64_t N, int32_t* perm, hipStream_t stream);
+hipError_t launch_inverse_perm(const int32_t* perm, int64_t N, int32_t* inv, hipStream_t stream);
+hipError_t launch_gather_columns(const void* in, int64_t ld_in, void* out, int64_t ld_out, int esize, int64_t M,
+                                 int64_t N, const int32_t* src_idx, hipStream_t stream);
+hipError_t launch_gather_vectors(const RowSrc& src, const int64_t* idx, int64_t count, void* out, int out_type,
+                                 hipStream_t stream);
+
+// ---- dequant (k_dequant.hip) ---------------------------------------------------------------------
+struct DequantBooks {
+  const void* C[8];
+  const int32_t* q[8];
+  int type[8];
+  int64_t K[8];
+  int n;             // books in use (1 = basic only)
+  int64_t ldq_base;
+  int64_t ldq_ext;
+};
+hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, const DequantBooks& books,
+                          const int32_t* inv_perm, const void* minuend, int min_type, int64_t ld_min, void* out,
+                          int out_type, int64_t ld_out, hipStream_t stream);
+
+}  // namespace crvq

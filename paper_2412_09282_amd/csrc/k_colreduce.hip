@@ -1,0 +1,123 @@
+// Column (input-channel) reduction behind CRVQ's channel importance (Sec. 4.1 Eq. 7, Appendix A.2
+// Eq. 9-10 of the paper) and the Hessian diagonal [X X^T]_jj:
+//   out[j] = s_j * R_i (A[i,j] - B[i,j])^2,  R = sum (fp64) or max.
+// Pass 1: threads own 4 adjacent columns (16-byte fp32 / 8-byte bf16 loads, so every row of a
+// wave is one contiguous 1 KiB / 512 B segment); the grid's second dimension splits the rows into
+// slabs that each write an fp64 partial per column.  Pass 2 folds the slabs in slab order and
+// applies the scale.  Both passes are deterministic.
+#include "crvq_internal.h"
+
+namespace crvq {
+namespace {
+
+constexpr int kCols = 4;  // columns per thread
+
+__device__ __forceinline__ void load4(const void* p, int type, int64_t idx, int valid_cols, double (&v)[kCols]) {
+  if (type == ET_F32) {
+    const float* f = static_cast<const float*>(p) + idx;
+    if (valid_cols == kCols && ((reinterpret_cast<uintptr_t>(f) & 15) == 0)) {
+      const float4 q = *reinterpret_cast<const float4*>(f);
+      v[0] = q.x;
+      v[1] = q.y;
+      v[2] = q.z;
+      v[3] = q.w;
+    } else {
+#pragma unroll
+      for (int c = 0; c < kCols; ++c) v[c] = (c < valid_cols) ? static_cast<double>(f[c]) : 0.0;
+    }
+  } else {
+    const uint16_t* h = static_cast<const uint16_t*>(p) + idx;
+    if (valid_cols == kCols && ((reinterpret_cast<uintptr_t>(h) & 7) == 0)) {
+      const uint2 q = *reinterpret_cast<const uint2*>(h);
+      v[0] = __uint_as_float(q.x << 16);
+      v[1] = __uint_as_float(q.x & 0xffff0000u);
+      v[2] = __uint_as_float(q.y << 16);
+      v[3] = __uint_as_float(q.y & 0xffff0000u);
+    } else {
+#pragma unroll
+      for (int c = 0; c < kCols; ++c)
+        v[c] = (c < valid_cols) ? static_cast<double>(__uint_as_float(static_cast<uint32_t>(h[c]) << 16)) : 0.0;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void colreduce_partial(const void* __restrict__ A, int64_t lda,
+                                                         const void* __restrict__ B, int64_t ldb, int type, int64_t M,
+                                                         int64_t N, int reduce, int64_t rows_per_slab,
+                                                         double* __restrict__ part) {
+  const int64_t j0 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * kCols;
+  if (j0 >= N) return;
+  const int valid_cols = static_cast<int>((N - j0) < kCols ? (N - j0) : kCols);
+  const int64_t i0 = static_cast<int64_t>(blockIdx.y) * rows_per_slab;
+  const int64_t i1 = (i0 + rows_per_slab < M) ? i0 + rows_per_slab : M;
+  double acc[kCols] = {0.0, 0.0, 0.0, 0.0};
+  for (int64_t i = i0; i < i1; ++i) {
+    double a[kCols];
+    load4(A, type, i * lda + j0, valid_cols, a);
+    if (B) {
+      double b[kCols];
+      load4(B, type, i * ldb + j0, valid_cols, b);
+#pragma unroll
+      for (int c = 0; c < kCols; ++c) a[c] = a[c] - b[c];
+    }
+#pragma unroll
+    for (int c = 0; c < kCols; ++c) {
+      const double sq = a[c] * a[c];
+      acc[c] = (reduce == 0) ? acc[c] + sq : (sq > acc[c] ? sq : acc[c]);
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < kCols; ++c)
+    if (c < valid_cols) part[static_cast<int64_t>(blockIdx.y) * N + j0 + c] = acc[c];
+}
+
+__global__ __launch_bounds__(256) void colreduce_final(const double* __restrict__ part, int slabs, int64_t N,
+                                                       const float* __restrict__ scale, int reduce,
+                                                       float* __restrict__ out) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= N) return;
+  double acc = 0.0;
+  for (int s = 0; s < slabs; ++s) {
+    const double v = part[static_cast<int64_t>(s) * N + j];
+    acc = (reduce == 0) ? acc + v : (v > acc ? v : acc);
+  }
+  out[j] = static_cast<float>(scale ? static_cast<double>(scale[j]) * acc : acc);
+}
+
+struct Plan {
+  int64_t col_blocks;
+  int64_t slabs;
+  int64_t rows_per_slab;
+};
+
+Plan plan(int64_t M, int64_t N) {
+  Plan p;
+  p.col_blocks = cdiv(cdiv(N, kCols), 256);
+  int64_t want = cdiv(4096, p.col_blocks);      // aim for >= 4096 blocks in flight
+  int64_t max_slabs = cdiv(M, 8);               // at least 8 rows per slab
+  p.slabs = want < max_slabs ? want : max_slabs;
+  if (p.slabs < 1) p.slabs = 1;
+  p.rows_per_slab = cdiv(M, p.slabs);
+  p.slabs = cdiv(M, p.rows_per_slab);
+  return p;
+}
+
+}  // namespace
+
+size_t colreduce_ws_bytes(int64_t M, int64_t N) {
+  Plan p = plan(M, N);
+  return align256(static_cast<size_t>(p.slabs * N) * sizeof(double));
+}
+
+hipError_t launch_colreduce(const void* A, int64_t lda, const void* B, int64_t ldb, int type, int64_t M, int64_t N,
+                            const float* scale, int reduce, float* out, void* ws, hipStream_t stream) {
+  Plan p = plan(M, N);
+  double* part = static_cast<double*>(ws);
+  hipLaunchKernelGGL(colreduce_partial, dim3(static_cast<unsigned>(p.col_blocks), static_cast<unsigned>(p.slabs)),
+                     dim3(256), 0, stream, A, lda, B, ldb, type, M, N, reduce, p.rows_per_slab, part);
+  hipLaunchKernelGGL(colreduce_final, dim3(static_cast<unsigned>(cdiv(N, 256))), dim3(256), 0, stream, part,
+                     static_cast<int>(p.slabs), N, scale, reduce, out);
+  return hipGetLastError();
+}
+
+}  // namespace crvq

@@ -1,0 +1,152 @@
+// Channel reordering (Sec. 4.2 of the paper, Alg. 1 ReorderChannels), its reverse (Sec. 4.3,
+// Fig. 3 right) and the row gathers that move columns and vectors.
+//
+// rank_perm: perm = stable descending order of the importance (NaN last, equal values by
+//   ascending channel).  Each thread owns one channel and counts, over the whole importance array
+//   streamed through LDS, the channels that precede it: its rank is exact and unique, so
+//   perm[rank] = channel is a permutation without any atomic.  N is at most a few ten thousand
+//   channels, so the O(N^2) comparisons take microseconds.
+// gather_columns: out[r, k] = in[r, src[k]] with the row staged in LDS (coalesced in and out);
+//   rows too long for LDS fall back to direct gathers.
+#include "crvq_internal.h"
+
+namespace crvq {
+namespace {
+
+__device__ __forceinline__ bool precedes(float vi, int i, float vj, int j) {
+  const bool ni = vi != vi, nj = vj != vj;  // NaN test that survives -fno-honor-nans builds of other TUs
+  if (ni != nj) return nj;                  // a number precedes a NaN
+  if (!ni && vi != vj) return vi > vj;      // larger importance first
+  return i < j;                             // equal (or both NaN): lower channel first
+}
+
+__global__ __launch_bounds__(256) void rank_perm_kernel(const float* __restrict__ imp, int64_t N, int32_t* __restrict__ perm) {
+  __shared__ float tile[1024];
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const float vj = (j < N) ? imp[j] : 0.0f;
+  int rank = 0;
+  for (int64_t base = 0; base < N; base += 1024) {
+    for (int t = threadIdx.x; t < 1024; t += 256) tile[t] = (base + t < N) ? imp[base + t] : 0.0f;
+    __syncthreads();
+    const int lim = static_cast<int>((N - base) < 1024 ? (N - base) : 1024);
+    if (j < N)
+      for (int t = 0; t < lim; ++t) rank += precedes(tile[t], static_cast<int>(base + t), vj, static_cast<int>(j)) ? 1 : 0;
+    __syncthreads();
+  }
+  if (j < N) perm[rank] = static_cast<int32_t>(j);
+}
+
+__global__ __launch_bounds__(256) void fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void inverse_perm_kernel(const int32_t* __restrict__ perm, int64_t N,
+                                                           int32_t* __restrict__ inv) {
+  const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (k >= N) return;
+  const int32_t p = perm[k];
+  if (p >= 0 && p < N) inv[p] = static_cast<int32_t>(k);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gather_cols_lds(const T* __restrict__ in, int64_t ld_in, T* __restrict__ out,
+                                                       int64_t ld_out, int64_t N, const int32_t* __restrict__ src) {
+  extern __shared__ unsigned char smem[];
+  T* row = reinterpret_cast<T*>(smem);
+  const int64_t r = blockIdx.x;
+  const T* ri = in + r * ld_in;
+  for (int64_t c = threadIdx.x; c < N; c += 256) row[c] = ri[c];
+  __syncthreads();
+  T* ro = out + r * ld_out;
+  for (int64_t k = threadIdx.x; k < N; k += 256) {
+    const int32_t s = src[k];
+    if (s >= 0 && s < N) ro[k] = row[s];
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void gather_cols_direct(const T* __restrict__ in, int64_t ld_in, T* __restrict__ out,
+                                                          int64_t ld_out, int64_t M, int64_t N,
+                                                          const int32_t* __restrict__ src) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= M * N) return;
+  const int64_t r = e / N;
+  const int64_t k = e - r * N;
+  const int32_t s = src[k];
+  if (s >= 0 && s < N) out[r * ld_out + k] = in[r * ld_in + s];
+}
+
+__device__ __forceinline__ int64_t vec_offset(const RowSrc& s, int64_t i) {
+  int64_t r = i / s.vpr;
+  int64_t g = i - r * s.vpr;
+  return r * s.ld + g * s.d;
+}
+
+__global__ __launch_bounds__(256) void gather_vectors_kernel(RowSrc src, const int64_t* __restrict__ idx, int64_t count,
+                                                             void* __restrict__ out, int out_type) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int d = src.d;
+  if (e >= count * d) return;
+  const int64_t k = e / d;
+  const int t = static_cast<int>(e - k * d);
+  const int64_t v = idx[k];
+  const bool ok = v >= 0 && v < src.n;
+  if (src.type == ET_F32) {
+    const float x = ok ? static_cast<const float*>(src.base)[vec_offset(src, v) + t] : __builtin_nanf("");
+    static_cast<float*>(out)[e] = x;
+  } else {
+    const uint16_t h = ok ? static_cast<const uint16_t*>(src.base)[vec_offset(src, v) + t] : static_cast<uint16_t>(0x7fc0);
+    if (out_type == ET_BF16)
+      static_cast<uint16_t*>(out)[e] = h;
+    else
+      static_cast<float*>(out)[e] = __uint_as_float(static_cast<uint32_t>(h) << 16);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rank_perm(const float* importance, int64_t N, int32_t* perm, hipStream_t stream) {
+  hipLaunchKernelGGL(rank_perm_kernel, dim3(static_cast<unsigned>(cdiv(N, 256))), dim3(256), 0, stream, importance, N, perm);
+  return hipGetLastError();
+}
+
+hipError_t launch_inverse_perm(const int32_t* perm, int64_t N, int32_t* inv, hipStream_t stream) {
+  const unsigned g = static_cast<unsigned>(cdiv(N, 256));
+  hipLaunchKernelGGL(fill_i32, dim3(g), dim3(256), 0, stream, inv, N, -1);
+  hipLaunchKernelGGL(inverse_perm_kernel, dim3(g), dim3(256), 0, stream, perm, N, inv);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_columns(const void* in, int64_t ld_in, void* out, int64_t ld_out, int esize, int64_t M,
+                                 int64_t N, const int32_t* src_idx, hipStream_t stream) {
+  if (M <= 0 || N <= 0) return hipSuccess;
+  const size_t lds = static_cast<size_t>(N) * esize;
+  if (lds <= 64 * 1024) {
+    if (esize == 4)
+      hipLaunchKernelGGL(gather_cols_lds<uint32_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream,
+                         static_cast<const uint32_t*>(in), ld_in, static_cast<uint32_t*>(out), ld_out, N, src_idx);
+    else
+      hipLaunchKernelGGL(gather_cols_lds<uint16_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream,
+                         static_cast<const uint16_t*>(in), ld_in, static_cast<uint16_t*>(out), ld_out, N, src_idx);
+  } else {
+    dim3 grid(static_cast<unsigned>(cdiv(M * N, 256)));
+    if (esize == 4)
+      hipLaunchKernelGGL(gather_cols_direct<uint32_t>, grid, dim3(256), 0, stream, static_cast<const uint32_t*>(in), ld_in,
+                         static_cast<uint32_t*>(out), ld_out, M, N, src_idx);
+    else
+      hipLaunchKernelGGL(gather_cols_direct<uint16_t>, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(in), ld_in,
+                         static_cast<uint16_t*>(out), ld_out, M, N, src_idx);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_vectors(const RowSrc& src, const int64_t* idx, int64_t count, void* out, int out_type,
+                                 hipStream_t stream) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_vectors_kernel, dim3(static_cast<unsigned>(cdiv(count * src.d, 256))), dim3(256), 0, stream,
+                     src, idx, count, out, out_type);
+  return hipGetLastError();
+}
+
+}  // namespace crvq

@@ -1,0 +1,617 @@
+// Nearest-codeword search for CRVQ on gfx950 (Sec. 3.1 Eq. 3-4 of the paper; the beam's
+// per-parent top-B search of Sec. 3.1 / Alg. 1 BeamSearchOptimize).
+//
+// Distances are split as ||x - c||^2 = ||x||^2 + s(c),  s(c) = ||c||^2 - 2 x.c.
+//
+// 1. prep: the codebook is repacked into the fp32 MFMA A-operand order, 16 codewords per tile,
+//    with ||c||^2 per codeword (+inf for padding) as the accumulator input.
+// 2. screen: every wave keeps 16*CB rows resident as the MFMA B operand (scaled by -2) and streams
+//    all codeword tiles of its codebook split.  v_mfma_f32_16x16x4_f32 leaves each lane 4 values of
+//    s for one row; the lane reduces them to the tile minimum and keeps, per row, the NB tiles with
+//    the smallest minimum and the smallest minimum of every other tile ("rest").  Nothing of the
+//    N x K distance matrix leaves the registers.
+// 3. exact: the codewords of the kept tiles are re-scored in fp64 with the same direct form as the
+//    definition (sum_t (x_t - c_t)^2, t ascending), merged across the four lane groups, the codebook
+//    splits and the tie order (D, k).
+// 4. certify / rescue: with R = ||x|| + sqrt(D_top), every codeword that could beat the kept ones
+//    has ||c|| <= R, hence a screen error below delta(R); if rest + ||x||^2 - delta > D_top the kept
+//    list is provably the exact answer, otherwise the row is re-searched exactly over the whole
+//    codebook in fp64 by its workgroup.  Codes therefore equal the fp64 definition's, ties included.
+#include "crvq_internal.h"
+
+#include <climits>
+
+namespace crvq {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float bf16_to_f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+
+__device__ __forceinline__ int64_t row_offset(const RowSrc& s, int64_t i) {
+  if (s.type == ET_F64) return i * s.d;
+  int64_t r = i / s.vpr;
+  int64_t g = i - r * s.vpr;
+  return r * s.ld + g * s.d;
+}
+
+__device__ __forceinline__ double row_elem(const RowSrc& s, int64_t off, int t) {
+  if (s.type == ET_F32) return static_cast<double>(static_cast<const float*>(s.base)[off + t]);
+  if (s.type == ET_BF16) return static_cast<double>(bf16_to_f(static_cast<const uint16_t*>(s.base)[off + t]));
+  return static_cast<const double*>(s.base)[off + t];
+}
+
+__device__ __forceinline__ double cb_elem(const void* C, int type, int64_t k, int d, int t) {
+  if (type == ET_F32) return static_cast<double>(static_cast<const float*>(C)[k * d + t]);
+  return static_cast<double>(bf16_to_f(static_cast<const uint16_t*>(C)[k * d + t]));
+}
+
+// fp64 direct-form squared distance, t ascending (no contraction: the library is built with
+// -ffp-contract=off).
+__device__ __forceinline__ double exact_dist(const double (&x)[16], const void* C, int ct, int64_t k, int d) {
+  double acc = 0.0;
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    if (t < d) {
+      double diff = x[t] - cb_elem(C, ct, k, d, t);
+      acc = acc + diff * diff;
+    }
+  }
+  return acc;
+}
+
+__device__ __forceinline__ bool cless(double Da, int ka, double Db, int kb) {
+  return Da < Db || (Da == Db && ka < kb);
+}
+
+// Insert (D, k) into an ascending list of NB entries, dropping the largest.
+template <int NB>
+__device__ __forceinline__ void list_insert(double (&LD)[NB], int (&LK)[NB], double D, int k) {
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    bool lt = cless(D, k, LD[j], LK[j]);
+    double tD = lt ? LD[j] : D;
+    int tk = lt ? LK[j] : k;
+    LD[j] = lt ? D : LD[j];
+    LK[j] = lt ? k : LK[j];
+    D = tD;
+    k = tk;
+  }
+}
+
+// Keep the NB smallest of two ascending lists (bitonic merge; both operands end identical when
+// called symmetrically across lanes).
+template <int NB>
+__device__ __forceinline__ void list_merge(double (&LD)[NB], int (&LK)[NB], const double (&OD)[NB],
+                                           const int (&OK)[NB]) {
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    bool take = cless(OD[NB - 1 - j], OK[NB - 1 - j], LD[j], LK[j]);
+    LD[j] = take ? OD[NB - 1 - j] : LD[j];
+    LK[j] = take ? OK[NB - 1 - j] : LK[j];
+  }
+#pragma unroll
+  for (int s = NB / 2; s >= 1; s /= 2) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      if ((j & s) == 0) {
+        bool sw = cless(LD[j + s], LK[j + s], LD[j], LK[j]);
+        double a = LD[j], b = LD[j + s];
+        int ka = LK[j], kb = LK[j + s];
+        LD[j] = sw ? b : a;
+        LD[j + s] = sw ? a : b;
+        LK[j] = sw ? kb : ka;
+        LK[j + s] = sw ? ka : kb;
+      }
+    }
+  }
+}
+
+template <int NB>
+__device__ __forceinline__ void list_merge_xor(double (&LD)[NB], int (&LK)[NB], int mask) {
+  double OD[NB];
+  int OK[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    OD[j] = __shfl_xor(LD[j], mask);
+    OK[j] = __shfl_xor(LK[j], mask);
+  }
+  list_merge<NB>(LD, LK, OD, OK);
+}
+
+// ------------------------------------------------------------------------------------------------
+// 1. codebook repack
+// ------------------------------------------------------------------------------------------------
+template <int KS>
+__global__ __launch_bounds__(256) void prep_codebook(const void* __restrict__ C, int ct, int64_t K, int d,
+                                                     int64_t tiles, float* __restrict__ apack,
+                                                     float* __restrict__ cnp) {
+  int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (k >= tiles * 16) return;
+  float c[16];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) c[t] = (k < K && t < d) ? static_cast<float>(cb_elem(C, ct, k, d, t)) : 0.0f;
+  float cn = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 16; ++t) cn = cn + c[t] * c[t];
+  cnp[k] = (k < K) ? cn : __builtin_inff();
+  const int64_t tile = k >> 4;
+  const int i = static_cast<int>(k & 15);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int s = 0; s < KS; ++s) apack[((tile * 64) + i + 16 * q) * KS + s] = c[4 * s + q];
+  }
+}
+
+template <int KS>
+struct AVec;
+template <>
+struct AVec<1> {
+  float v[1];
+  __device__ __forceinline__ void load(const float* p) { v[0] = *p; }
+};
+template <>
+struct AVec<2> {
+  float v[2];
+  __device__ __forceinline__ void load(const float* p) {
+    f2 t = *reinterpret_cast<const f2*>(p);
+    v[0] = t[0];
+    v[1] = t[1];
+  }
+};
+template <>
+struct AVec<4> {
+  float v[4];
+  __device__ __forceinline__ void load(const float* p) {
+    f4 t = *reinterpret_cast<const f4*>(p);
+    v[0] = t[0];
+    v[1] = t[1];
+    v[2] = t[2];
+    v[3] = t[3];
+  }
+};
+
+// ------------------------------------------------------------------------------------------------
+// 2 + 3. MFMA screen with fused top-tile tracking, then exact re-scoring of the kept tiles
+// ------------------------------------------------------------------------------------------------
+template <int KS, int NB, int CB>
+__global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __restrict__ apack,
+                                                     const float* __restrict__ cnp, int64_t tiles, int64_t tps,
+                                                     const void* __restrict__ C, int ct, int64_t K,
+                                                     double* __restrict__ pD, int* __restrict__ pK,
+                                                     float* __restrict__ pR, double* __restrict__ xn2o) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int jl = lane & 15;
+  const int g = lane >> 4;
+  const int split = blockIdx.y;
+  const int64_t n = src.n;
+  const int d = src.d;
+  const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (16 * CB);
+  if (row0 >= n) return;  // no barriers below: a wave past the end simply leaves
+
+  float bop[CB][KS];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int64_t i = row0 + cb * 16 + jl;
+    const int64_t off = (i < n) ? row_offset(src, i) : 0;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int t = 4 * s + g;
+      bop[cb][s] = (i < n && t < d) ? -2.0f * static_cast<float>(row_elem(src, off, t)) : 0.0f;
+    }
+  }
+
+  float m[CB][NB];
+  int id[CB][NB];
+  float rest[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    rest[cb] = __builtin_inff();
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      m[cb][j] = __builtin_inff();
+      id[cb][j] = -1;
+    }
+  }
+
+  const int64_t t0 = static_cast<int64_t>(split) * tps;
+  const int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
+  if (t0 < t1) {
+    AVec<KS> a_nx;
+    a_nx.load(apack + (t0 * 64 + lane) * KS);
+    f4 c_nx = *reinterpret_cast<const f4*>(cnp + t0 * 16 + 4 * g);
+    for (int64_t T = t0; T < t1; ++T) {
+      const AVec<KS> a = a_nx;
+      const f4 c4 = c_nx;
+      const int64_t Tn = (T + 1 < t1) ? T + 1 : T;
+      a_nx.load(apack + (Tn * 64 + lane) * KS);
+      c_nx = *reinterpret_cast<const f4*>(cnp + Tn * 16 + 4 * g);
+      const int Ti = static_cast<int>(T);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[0], bop[cb][0], c4, 0, 0, 0);
+#pragma unroll
+        for (int s = 1; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[s], bop[cb][s], acc, 0, 0, 0);
+        float x = fminf(fminf(acc[0], acc[1]), fminf(acc[2], acc[3]));
+        if constexpr (NB == 1) {
+          rest[cb] = __builtin_amdgcn_fmed3f(m[cb][0], rest[cb], x);
+          const bool lt = x < m[cb][0];
+          m[cb][0] = fminf(m[cb][0], x);
+          id[cb][0] = lt ? Ti : id[cb][0];
+        } else {
+          int xi = Ti;
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const bool lt = x < m[cb][j];
+            const float nv = fminf(x, m[cb][j]);
+            const float cv = fmaxf(x, m[cb][j]);
+            const int ni = lt ? xi : id[cb][j];
+            xi = lt ? id[cb][j] : xi;
+            m[cb][j] = nv;
+            id[cb][j] = ni;
+            x = cv;
+          }
+          rest[cb] = fminf(rest[cb], x);
+        }
+      }
+    }
+  }
+
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int64_t i = row0 + cb * 16 + jl;
+    const bool valid = i < n;
+    double xd[16];
+    double xn2 = 0.0;
+    const int64_t off = valid ? row_offset(src, i) : 0;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) xd[t] = (valid && t < d) ? row_elem(src, off, t) : 0.0;
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      if (t < d) xn2 = xn2 + xd[t] * xd[t];
+    double LD[NB];
+    int LK[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      LD[j] = __builtin_inf();
+      LK[j] = INT_MAX;
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int T = id[cb][j];
+      if (valid && T >= 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t k = static_cast<int64_t>(T) * 16 + 4 * g + r;
+          if (k < K) list_insert<NB>(LD, LK, exact_dist(xd, C, ct, k, d), static_cast<int>(k));
+        }
+      }
+    }
+    list_merge_xor<NB>(LD, LK, 16);
+    list_merge_xor<NB>(LD, LK, 32);
+    float rs = rest[cb];
+    rs = fminf(rs, __shfl_xor(rs, 16));
+    rs = fminf(rs, __shfl_xor(rs, 32));
+    if (g == 0 && valid) {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        pD[(static_cast<int64_t>(split) * NB + j) * n + i] = LD[j];
+        pK[(static_cast<int64_t>(split) * NB + j) * n + i] = LK[j];
+      }
+      pR[static_cast<int64_t>(split) * n + i] = rs;
+      if (split == 0) xn2o[i] = xn2;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// 4. merge the splits, certify, rescue uncertain rows exactly, emit
+// ------------------------------------------------------------------------------------------------
+template <int NB>
+__global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top,
+                                                       const double* __restrict__ pD, const int* __restrict__ pK,
+                                                       const float* __restrict__ pR, const double* __restrict__ xn2a,
+                                                       const void* __restrict__ C, int ct, int64_t K,
+                                                       int32_t* __restrict__ codes, float* __restrict__ dist,
+                                                       double* __restrict__ rowD, int* __restrict__ rowK) {
+  __shared__ int scan[256];
+  __shared__ int flagged[256];
+  __shared__ double sD[128 * NB];
+  __shared__ int sK[128 * NB];
+  const int tid = threadIdx.x;
+  const int64_t n = src.n;
+  const int d = src.d;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + tid;
+  const bool valid = i < n;
+  const int need = static_cast<int>((top < K) ? top : K);
+
+  double LD[NB];
+  int LK[NB];
+  float rest = __builtin_inff();
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    LD[j] = __builtin_inf();
+    LK[j] = INT_MAX;
+  }
+  bool certain = false;
+  if (valid) {
+    for (int s = 0; s < splits; ++s) {
+      double OD[NB];
+      int OK[NB];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        OD[j] = pD[(static_cast<int64_t>(s) * NB + j) * n + i];
+        OK[j] = pK[(static_cast<int64_t>(s) * NB + j) * n + i];
+      }
+      list_merge<NB>(LD, LK, OD, OK);
+      rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
+    }
+    double Dl = LD[0];
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (j == need - 1) Dl = LD[j];
+    if (rest == __builtin_inff()) {
+      certain = true;  // every codeword was scored exactly
+    } else {
+      const double xn2 = xn2a[i];
+      const double xn = sqrt(xn2);
+      const double R = xn + sqrt(Dl);
+      const double delta = static_cast<double>(4 * d + 24) * 0x1p-24 * (R * R + 2.0 * xn * R) + 1e-35;
+      certain = Dl < static_cast<double>(rest) + xn2 - delta;
+    }
+  }
+
+  auto emit = [&](int64_t row, const double (&ED)[NB], const int (&EK)[NB]) {
+    if (codes) {
+      codes[row] = EK[0];
+      if (dist) dist[row] = static_cast<float>(ED[0]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < NB; ++j) {
+        if (j < top) {
+          const bool real = j < need;
+          rowD[row * top + j] = real ? ED[j] : __builtin_inf();
+          rowK[row * top + j] = real ? EK[j] : -1;
+        }
+      }
+    }
+  };
+  if (valid && certain) emit(i, LD, LK);
+
+  // compaction of the uncertain rows of this block (inclusive scan of the flags)
+  const int flag = (valid && !certain) ? 1 : 0;
+  scan[tid] = flag;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    int v = (tid >= off) ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  if (flag) flagged[scan[tid] - 1] = tid;
+  const int nflag = scan[255];
+  __syncthreads();
+
+  for (int f = 0; f < nflag; ++f) {
+    const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + flagged[f];
+    const int64_t off = row_offset(src, row);
+    double xd[16];
+#pragma unroll
+    for (int t = 0; t < 16; ++t) xd[t] = (t < d) ? row_elem(src, off, t) : 0.0;
+    double TD[NB];
+    int TK[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      TD[j] = __builtin_inf();
+      TK[j] = INT_MAX;
+    }
+    for (int64_t k = tid; k < K; k += 256) list_insert<NB>(TD, TK, exact_dist(xd, C, ct, k, d), static_cast<int>(k));
+    for (int stride = 128; stride >= 1; stride >>= 1) {
+      if (tid >= stride && tid < 2 * stride) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          sD[(tid - stride) * NB + j] = TD[j];
+          sK[(tid - stride) * NB + j] = TK[j];
+        }
+      }
+      __syncthreads();
+      if (tid < stride) {
+        double OD[NB];
+        int OK[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          OD[j] = sD[tid * NB + j];
+          OK[j] = sK[tid * NB + j];
+        }
+        list_merge<NB>(TD, TK, OD, OK);
+      }
+      __syncthreads();
+    }
+    if (tid == 0) emit(row, TD, TK);
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// beam bookkeeping
+// ------------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void beam_merge_kernel(int64_t n, int n_par, int n_next, int beam, int step,
+                                                         int n_books, const double* __restrict__ rowD,
+                                                         const int* __restrict__ rowK, RowSrc src0,
+                                                         const double* __restrict__ res_in,
+                                                         double* __restrict__ res_out, const int* __restrict__ tup_in,
+                                                         int* __restrict__ tup_out, double* __restrict__ err_out,
+                                                         const void* __restrict__ book, int bt, int64_t K, int d) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  int head[kMaxBeam];
+  for (int b = 0; b < n_par; ++b) head[b] = 0;
+  const int64_t off0 = (step == 0) ? row_offset(src0, i) : 0;
+  for (int s = 0; s < n_next; ++s) {
+    int bb = -1, bk = 0;
+    double bD = 0.0;
+    for (int b = 0; b < n_par; ++b) {
+      if (head[b] >= beam) continue;
+      const int64_t r = (i * n_par + b) * beam + head[b];
+      const int k = rowK[r];
+      if (k < 0 || k >= K) continue;
+      const double D = rowD[r];
+      if (bb < 0 || D < bD || (D == bD && (b < bb || (b == bb && k < bk)))) {
+        bb = b;
+        bk = k;
+        bD = D;
+      }
+    }
+    double* ro = res_out + (i * n_next + s) * d;
+    int* to = tup_out + (i * n_next + s) * n_books;
+    if (bb < 0) {  // cannot happen when n_next = min(beam, n_par * K); kept as a guard
+      err_out[i * n_next + s] = __builtin_inf();
+      for (int t = 0; t < d; ++t) ro[t] = 0.0;
+      for (int u = 0; u <= step; ++u) to[u] = 0;
+      continue;
+    }
+    head[bb] += 1;
+    for (int t = 0; t < d; ++t) {
+      const double parent = (step == 0) ? row_elem(src0, off0, t) : res_in[(i * n_par + bb) * d + t];
+      ro[t] = parent - cb_elem(book, bt, bk, d, t);
+    }
+    for (int u = 0; u < step; ++u) to[u] = tup_in[(i * n_par + bb) * n_books + u];
+    to[step] = bk;
+    err_out[i * n_next + s] = bD;
+  }
+}
+
+__global__ __launch_bounds__(256) void beam_emit_kernel(int64_t n, int64_t vpr, int n_par, int n_books,
+                                                        const int* __restrict__ tup, const double* __restrict__ err,
+                                                        CodePtrs outs, float* __restrict__ err_out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  const int64_t r = i / vpr;
+  const int64_t g = i - r * vpr;
+  for (int t = 0; t < n_books; ++t) outs.q[t][r * outs.ld[t] + g] = tup[(i * n_par) * n_books + t];
+  if (err_out) err_out[i] = static_cast<float>(err[i * n_par]);
+}
+
+template <int KS, int NB, int CB>
+hipError_t launch_screen_t(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
+                           const ScreenWs& w, hipStream_t stream) {
+  dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
+  hipLaunchKernelGGL((screen_kernel<KS, NB, CB>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
+                     p.tiles_per_split, C, ct, K, w.pD, w.pK, w.pR, w.xn2);
+  return hipGetLastError();
+}
+
+template <int KS>
+hipError_t launch_screen_ks(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
+                            const ScreenWs& w, hipStream_t stream) {
+  switch (p.nb) {
+    case 1: return launch_screen_t<KS, 1, 8>(src, C, ct, K, p, w, stream);
+    case 2: return launch_screen_t<KS, 2, 8>(src, C, ct, K, p, w, stream);
+    case 4: return launch_screen_t<KS, 4, 4>(src, C, ct, K, p, w, stream);
+    case 8: return launch_screen_t<KS, 8, 2>(src, C, ct, K, p, w, stream);
+    case 16: return launch_screen_t<KS, 16, 1>(src, C, ct, K, p, w, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <int NB>
+hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K, int top, const ScreenPlan& p,
+                             const ScreenWs& w, int32_t* codes, float* dist, double* rowD, int* rowK,
+                             hipStream_t stream) {
+  hipLaunchKernelGGL((finalize_kernel<NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream, src,
+                     p.splits, top, w.pD, w.pK, w.pR, w.xn2, C, ct, K, codes, dist, rowD, rowK);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+static int next_pow2_nb(int top) {
+  int nb = 1;
+  while (nb < top) nb <<= 1;
+  return nb;
+}
+
+ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
+  ScreenPlan p;
+  p.nb = next_pow2_nb(top);
+  p.cb = p.nb <= 2 ? 8 : (p.nb == 4 ? 4 : (p.nb == 8 ? 2 : 1));
+  p.ks = d <= 4 ? 1 : (d <= 8 ? 2 : 4);
+  p.tiles = cdiv(K, 16);
+  p.grid_x = cdiv(n_rows, 64 * p.cb);
+  int64_t splits = 1;
+  const int64_t want_blocks = 2048;
+  if (p.grid_x < want_blocks) {
+    int64_t want = cdiv(want_blocks, p.grid_x > 0 ? p.grid_x : 1);
+    int64_t maxs = p.tiles / 32 > 1 ? p.tiles / 32 : 1;
+    splits = want < maxs ? want : maxs;
+  }
+  p.tiles_per_split = cdiv(p.tiles, splits);
+  p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
+  return p;
+}
+
+ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc) {
+  ScreenWs w;
+  const int64_t tiles = cdiv(K_alloc, 16);
+  w.apack = ws.take<float>(static_cast<size_t>(tiles * 64 * p.ks));
+  w.cnp = ws.take<float>(static_cast<size_t>(tiles * 16));
+  w.pD = ws.take<double>(static_cast<size_t>(p.splits) * p.nb * n_rows);
+  w.pK = ws.take<int>(static_cast<size_t>(p.splits) * p.nb * n_rows);
+  w.pR = ws.take<float>(static_cast<size_t>(p.splits) * n_rows);
+  w.xn2 = ws.take<double>(static_cast<size_t>(n_rows));
+  return w;
+}
+
+hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, int top, const ScreenPlan& p,
+                         const ScreenWs& w, int32_t* out_codes, float* out_dist, double* rowD, int* rowK,
+                         hipStream_t stream) {
+  if (src.n <= 0) return hipSuccess;
+  const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
+  hipError_t e;
+  switch (p.ks) {
+    case 1: hipLaunchKernelGGL(prep_codebook<1>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+    case 2: hipLaunchKernelGGL(prep_codebook<2>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+    default: hipLaunchKernelGGL(prep_codebook<4>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+  }
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  switch (p.ks) {
+    case 1: e = launch_screen_ks<1>(src, C, ct, K, p, w, stream); break;
+    case 2: e = launch_screen_ks<2>(src, C, ct, K, p, w, stream); break;
+    default: e = launch_screen_ks<4>(src, C, ct, K, p, w, stream); break;
+  }
+  if (e != hipSuccess) return e;
+  switch (p.nb) {
+    case 1: return launch_finalize_t<1>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    case 2: return launch_finalize_t<2>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    case 4: return launch_finalize_t<4>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    case 8: return launch_finalize_t<8>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    case 16: return launch_finalize_t<16>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_beam_merge(int64_t n, int n_par, int beam, int step, int n_books, const double* rowD,
+                             const int* rowK, const RowSrc& src0, const double* res_in, double* res_out,
+                             const int* tup_in, int* tup_out, double* err_out, const void* book, int book_type,
+                             int64_t K, int d, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  int64_t nn = static_cast<int64_t>(n_par) * K;
+  const int n_next = static_cast<int>(nn < beam ? nn : beam);
+  hipLaunchKernelGGL(beam_merge_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0, stream, n, n_par,
+                     n_next, beam, step, n_books, rowD, rowK, src0, res_in, res_out, tup_in, tup_out, err_out, book,
+                     book_type, K, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_beam_emit(int64_t n, int64_t vpr, int n_par, int n_books, const int* tup, const double* err,
+                            const CodePtrs& outs, float* err_out, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(beam_emit_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0, stream, n, vpr, n_par,
+                     n_books, tup, err, outs, err_out);
+  return hipGetLastError();
+}
+
+}  // namespace crvq

@@ -1,0 +1,190 @@
+"""CRVQ per-layer quantization on the GPU, as a sequence of libcrvq calls.
+
+The order follows Alg. 1 of the paper for one weight matrix:
+ComputeImportance -> ReorderChannels -> KMeansCodebook + VectorQuant (basic)
+-> for every extended codebook: ComputeError, KMeansCodebook, VectorQuant,
+Update on the critical groups -> beam search over all codebooks for the
+critical vectors -> reconstruction with the reverse reordering.
+
+Readings where the paper leaves a choice open (shared with the design notes):
+importance I_j = h_j * sum_i W_ij^2 with h = diag(X X^T); the critical channels
+are the first d * ceil(lambda N / d) reordered columns; K-means starts from the
+vectors at given indices, one iteration is assign + update, `iters` iterations
+are followed by a final assign, an empty cluster keeps its centroid; stored
+residuals are float32; the critical vectors' final codes come from the beam
+search (width 1 = greedy) on the exact residual.
+
+Every arithmetic step runs in the library's kernels; this module only
+allocates device tensors and sequences the calls.  Passing `trace` (a list)
+records the inputs and outputs of every call (copied to the host) so a test
+can re-run each call on the oracle from the same bytes.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional
+
+import torch
+
+from . import crvq as C
+from .crvq import VecSet
+
+
+@dataclasses.dataclass
+class LayerConfig:
+    d: int
+    K_base: int
+    K_ext: List[int]
+    crit_frac: float
+    beam: int
+    iters: int
+
+
+def n_crit_columns(N: int, d: int, frac: float) -> int:
+    return min(N, d * int(math.ceil(frac * N / d - 1e-9)))
+
+
+@dataclasses.dataclass
+class LayerState:
+    hdiag: torch.Tensor
+    importance: torch.Tensor
+    perm: torch.Tensor
+    Ws: torch.Tensor
+    n_crit: int
+    C_base: torch.Tensor
+    C_ext: List[torch.Tensor]
+    codes_base: torch.Tensor     # [M * N/d]; critical entries hold the beam's basic codes at the end
+    codes_ext: List[torch.Tensor]  # [M * n_crit/d] per extended book
+    beam_err: torch.Tensor       # [M * n_crit/d]
+    W_hat: torch.Tensor
+
+
+class LayerQuantizer:
+    """Holds the device buffers for one layer shape so repeated runs allocate nothing new."""
+
+    def __init__(self, M: int, N: int, dtype: torch.dtype, cfg: LayerConfig, tokens: int, device="cuda"):
+        d = cfg.d
+        assert N % d == 0
+        self.M, self.N, self.dtype, self.cfg, self.device = M, N, dtype, cfg, device
+        self.n = M * N // d
+        self.n_crit = n_crit_columns(N, d, cfg.crit_frac)
+        self.ncv = self.n_crit // d
+        f32, i32 = torch.float32, torch.int32
+        self.hdiag = torch.empty(N, dtype=f32, device=device)
+        self.imp = torch.empty(N, dtype=f32, device=device)
+        self.perm = torch.empty(N, dtype=i32, device=device)
+        self.Ws = torch.empty(M, N, dtype=dtype, device=device)
+        self.C_base = torch.empty(cfg.K_base, d, dtype=dtype, device=device)
+        self.codes = torch.empty(self.n, dtype=i32, device=device)
+        self.dist = torch.empty(self.n, dtype=f32, device=device)
+        self.E = [torch.empty(M, self.n_crit, dtype=f32, device=device) for _ in range(2)]
+        self.C_ext = [torch.empty(K, d, dtype=f32, device=device) for K in cfg.K_ext]
+        self.q_ext_fit = torch.empty(M * self.ncv, dtype=i32, device=device)
+        self.codes_ext = [torch.empty(M * self.ncv, dtype=i32, device=device) for _ in cfg.K_ext]
+        self.beam_err = torch.empty(M * self.ncv, dtype=f32, device=device)
+        self.W_hat = torch.empty(M, N, dtype=dtype, device=device)
+
+    def run(self, W: torch.Tensor, X: torch.Tensor, base_idx: torch.Tensor, ext_idx: List[torch.Tensor],
+            trace: Optional[list] = None, timer=None) -> LayerState:
+        """timer: optional object with begin(name) / end(name), called right around each library call."""
+        cfg, d, M, N = self.cfg, self.cfg.d, self.M, self.N
+        rec = _Recorder(trace, timer)
+
+        rec.pre("hdiag", A=X)
+        C.crvq_channel_importance(X, self.hdiag)
+        rec.post("hdiag", out=self.hdiag)
+
+        rec.pre("importance", A=W, scale=self.hdiag)
+        C.crvq_channel_importance(W, self.imp, scale=self.hdiag)
+        rec.post("importance", out=self.imp)
+
+        rec.pre("reorder", inp=W, importance=self.imp)
+        C.crvq_reorder(W, self.Ws, self.perm, importance=self.imp)
+        rec.post("reorder", perm=self.perm, out=self.Ws)
+
+        V = VecSet.of_matrix(self.Ws, d)
+        C.crvq_gather_vectors(V, base_idx, self.C_base)
+        self._kmeans(V, self.C_base, self.codes, rec, "base")
+        rec.pre("assign_base_final", X=self.Ws, C=self.C_base)
+        C.crvq_assign(V, self.C_base, self.codes, self.dist)
+        rec.post("assign_base_final", codes=self.codes, dist=self.dist)
+
+        # residual of the critical slab after the basic codebook (Alg. 1 ComputeError)
+        cur = 0
+        if self.n_crit > 0:
+            rec.pre("residual_base", minuend=self.Ws[:, :self.n_crit], codes=self.codes.view(M, N // d)[:, :self.ncv],
+                    book=self.C_base)
+            C.crvq_dequant(M, self.n_crit, d, self.codes, N // d, self.C_base, self.E[cur], minuend=self.Ws)
+            rec.post("residual_base", out=self.E[cur])
+            for t, Ct in enumerate(self.C_ext):
+                VE = VecSet.of_matrix(self.E[cur], d)
+                C.crvq_gather_vectors(VE, ext_idx[t], Ct)
+                self._kmeans(VE, Ct, self.q_ext_fit, rec, f"ext{t + 1}")
+                rec.pre(f"assign_ext{t + 1}_final", X=self.E[cur], C=Ct)
+                C.crvq_assign(VE, Ct, self.q_ext_fit)
+                rec.post(f"assign_ext{t + 1}_final", codes=self.q_ext_fit)
+                if t + 1 < len(self.C_ext):
+                    rec.pre(f"residual_ext{t + 1}", minuend=self.E[cur], codes=self.q_ext_fit, book=Ct)
+                    C.crvq_dequant(M, self.n_crit, d, self.q_ext_fit, self.ncv, Ct, self.E[cur ^ 1],
+                                   minuend=self.E[cur])
+                    rec.post(f"residual_ext{t + 1}", out=self.E[cur ^ 1])
+                    cur ^= 1
+
+            # beam over all books for the critical vectors; basic codes land in the full code array
+            Vc = VecSet.of_matrix(self.Ws, d, self.n_crit)
+            books = [self.C_base] + self.C_ext
+            rec.pre("beam", X=self.Ws[:, :self.n_crit], books=books, beam=cfg.beam)
+            C.crvq_assign_residual_beam(Vc, books, cfg.beam, [self.codes] + self.codes_ext, self.beam_err,
+                                        ldc=[N // d] + [self.ncv] * len(self.C_ext))
+            rec.post("beam", codes_base=self.codes.view(M, N // d)[:, :self.ncv],
+                     codes_ext=list(self.codes_ext), err=self.beam_err)
+
+        rec.pre("dequant", codes=self.codes, codes_ext=list(self.codes_ext), books=[self.C_base] + self.C_ext,
+                perm=self.perm)
+        C.crvq_dequant(M, N, d, self.codes, N // d, self.C_base, self.W_hat, n_crit=self.n_crit,
+                       q_ext=self.codes_ext, ldq_ext=self.ncv, C_ext=self.C_ext, perm=self.perm)
+        rec.post("dequant", out=self.W_hat)
+
+        return LayerState(self.hdiag, self.imp, self.perm, self.Ws, self.n_crit, self.C_base, self.C_ext, self.codes,
+                          self.codes_ext, self.beam_err, self.W_hat)
+
+    def _kmeans(self, V: VecSet, Cb: torch.Tensor, codes: torch.Tensor, rec, tag: str):
+        for it in range(self.cfg.iters):
+            rec.pre(f"assign_{tag}_{it}", X=V.t, C=Cb)
+            C.crvq_assign(V, Cb, codes)
+            rec.post(f"assign_{tag}_{it}", codes=codes)
+            rec.pre(f"update_{tag}_{it}", X=V.t, codes=codes, C=Cb)
+            C.crvq_kmeans_update(V, codes, Cb)
+            rec.post(f"update_{tag}_{it}", C=Cb)
+
+
+class _Recorder:
+    """Copies the inputs and outputs of each call to the host when tracing."""
+
+    def __init__(self, trace: Optional[list], timer):
+        self.trace = trace
+        self.timer = timer
+        self.cur: Dict = {}
+
+    @staticmethod
+    def _host(v):
+        if isinstance(v, torch.Tensor):
+            return v.detach().to("cpu", copy=True)
+        if isinstance(v, (list, tuple)):
+            return [_Recorder._host(x) for x in v]
+        return v
+
+    def pre(self, name: str, **kw):
+        if self.trace is not None:
+            self.cur = {"name": name, "in": {k: self._host(v) for k, v in kw.items()}}
+        if self.timer is not None:
+            self.timer.begin(name)
+
+    def post(self, name: str, **kw):
+        if self.timer is not None:
+            self.timer.end(name)
+        if self.trace is not None:
+            self.cur["out"] = {k: self._host(v) for k, v in kw.items()}
+            self.trace.append(self.cur)
+            self.cur = {}

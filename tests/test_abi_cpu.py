@@ -1,0 +1,146 @@
+"""CPU-only checks of the C ABI: the library loads, exports every symbol the header declares, and
+rejects invalid arguments on the host before anything is enqueued (no GPU is touched).  Also checks
+that the oracle and the GPU path share no code."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2412_09282_amd import crvq
+    return crvq.lib()
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation first
+
+
+def test_exports_every_declared_symbol(L):
+    from paper_2412_09282_amd import build
+    declared = build.exported_symbols()
+    assert len(declared) >= 15
+    so = os.path.join(ROOT, "paper_2412_09282_amd", "libcrvq.so")
+    out = os.popen(f"nm -D --defined-only {so}").read()
+    exported = set(re.findall(r" T (crvq_[a-z0-9_]+)", out))
+    missing = [s for s in declared if s not in exported]
+    assert not missing, missing
+    for s in declared:
+        assert hasattr(L, s)
+
+
+def test_version_and_error_text(L):
+    assert L.crvq_version() >= 100
+    assert isinstance(L.crvq_last_error(), bytes)
+
+
+def err(L):
+    return L.crvq_last_error().decode()
+
+
+def test_assign_validation(L):
+    ws = ctypes.c_void_p(0x100000)
+    # bad dtype
+    assert L.crvq_assign(FAKE, 7, 4, 2, 16, 8, FAKE, 0, 16, FAKE, None, ws, 1 << 30, None) == 1
+    assert "x_dtype" in err(L)
+    # unsupported d
+    assert L.crvq_assign(FAKE, 0, 4, 2, 64, 32, FAKE, 0, 16, FAKE, None, ws, 1 << 30, None) == 2
+    # ld too small
+    assert L.crvq_assign(FAKE, 0, 4, 2, 15, 8, FAKE, 0, 16, FAKE, None, ws, 1 << 30, None) == 1
+    # K out of range
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, FAKE, 0, 0, FAKE, None, ws, 1 << 30, None) == 1
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, FAKE, 0, 65537, FAKE, None, ws, 1 << 30, None) == 1
+    # NULL codebook / codes
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, None, 0, 16, FAKE, None, ws, 1 << 30, None) == 1
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, FAKE, 0, 16, None, None, ws, 1 << 30, None) == 1
+    # workspace too small / NULL / misaligned
+    need = L.crvq_assign_workspace_size(8, 8, 16)
+    assert need > 0
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, FAKE, 0, 16, FAKE, None, ws, need - 1, None) == 3
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, FAKE, 0, 16, FAKE, None, None, need, None) == 3
+    assert L.crvq_assign(FAKE, 0, 4, 2, 16, 8, FAKE, 0, 16, FAKE, None, ctypes.c_void_p(0x100010), need, None) == 3
+    # empty input is a no-op
+    assert L.crvq_assign(None, 0, 0, 2, 16, 8, FAKE, 0, 16, None, None, None, 0, None) == 0
+
+
+def test_workspace_sizes_are_deterministic_and_monotone(L):
+    a = L.crvq_assign_workspace_size(1 << 20, 8, 65536)
+    assert a == L.crvq_assign_workspace_size(1 << 20, 8, 65536)
+    assert L.crvq_assign_workspace_size(1 << 21, 8, 65536) >= a
+    assert L.crvq_assign_workspace_size(10, 8, 0) == 0
+    assert L.crvq_kmeans_workspace_size(1000, 8, 256) > 0
+    assert L.crvq_importance_workspace_size(4096, 4096) > 0
+    Ks = (ctypes.c_int64 * 2)(256, 256)
+    assert L.crvq_beam_workspace_size(1000, 8, 2, ctypes.cast(Ks, ctypes.c_void_p), 4) > 0
+    assert L.crvq_beam_workspace_size(1000, 8, 2, ctypes.cast(Ks, ctypes.c_void_p), 17) == 0
+
+
+def test_beam_validation(L):
+    Ks = (ctypes.c_int64 * 2)(256, 256)
+    dts = (ctypes.c_int32 * 2)(0, 0)
+    books = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    codes = (ctypes.c_void_p * 2)(0x3000, 0x4000)
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    args = lambda nb, beam, ks=Ks: (FAKE, 0, 10, 2, 16, 8, nb, ctypes.cast(books, PP), ctypes.cast(dts, ctypes.c_void_p),
+                                    ctypes.cast(ks, ctypes.c_void_p), beam, ctypes.cast(codes, PP), None, None,
+                                    FAKE, 1 << 30, None)
+    assert L.crvq_assign_residual_beam(*args(0, 4)) == 1
+    assert L.crvq_assign_residual_beam(*args(9, 4)) == 1
+    assert L.crvq_assign_residual_beam(*args(2, 0)) == 1
+    assert L.crvq_assign_residual_beam(*args(2, 17)) == 1
+    bad = (ctypes.c_int64 * 2)(256, 70000)
+    assert L.crvq_assign_residual_beam(*args(2, 4, bad)) == 1
+    ldc = (ctypes.c_int64 * 2)(1, 2)
+    a = list(args(2, 4))
+    a[12] = ctypes.cast(ldc, ctypes.c_void_p)
+    assert L.crvq_assign_residual_beam(*a) == 1 and "ldc" in err(L)
+
+
+def test_kmeans_importance_reorder_dequant_validation(L):
+    ws = ctypes.c_void_p(0x100000)
+    assert L.crvq_kmeans_update(FAKE, 0, 4, 2, 16, 8, FAKE, 0, FAKE, 0, None, ws, 1 << 30, None) == 1
+    assert L.crvq_kmeans_update(FAKE, 0, 4, 2, 16, 8, None, 16, FAKE, 0, None, ws, 1 << 30, None) == 1
+    assert L.crvq_kmeans_update(FAKE, 0, 4, 2, 16, 8, FAKE, 16, FAKE, 0, None, ws, 0, None) == 3
+    assert L.crvq_channel_importance(FAKE, 4, None, 0, 0, 0, 4, None, 0, FAKE, ws, 1 << 30, None) == 1
+    assert L.crvq_channel_importance(FAKE, 3, None, 0, 0, 4, 4, None, 0, FAKE, ws, 1 << 30, None) == 1
+    assert L.crvq_channel_importance(FAKE, 4, None, 0, 0, 4, 4, None, 5, FAKE, ws, 1 << 30, None) == 1
+    assert L.crvq_channel_importance(FAKE, 4, None, 0, 0, 4, 4, None, 0, FAKE, None, 0, None) == 3
+    # reorder: in == out rejected, perm required
+    assert L.crvq_reorder(FAKE, 8, FAKE, 8, 0, 4, 8, None, FAKE, 0, None, 0, None) == 1
+    assert "overlap" in err(L)
+    assert L.crvq_reorder(FAKE, 8, ctypes.c_void_p(0x9000), 8, 0, 4, 8, None, None, 0, None, 0, None) == 1
+    assert L.crvq_reorder(None, 0, None, 0, 0, 0, 0, FAKE, FAKE, 0, None, 0, None) == 1
+    # dequant: n_cols % d, n_crit not multiple of d, perm + minuend
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    assert L.crvq_dequant(4, 12, 8, 0, FAKE, 2, FAKE, 0, 16, 0, None, 0, None, None, None, None, None, 0, 0, FAKE, 0, 12,
+                          None, 0, None) == 1
+    assert L.crvq_dequant(4, 16, 8, 4, FAKE, 2, FAKE, 0, 16, 0, None, 0, None, None, None, None, None, 0, 0, FAKE, 0, 16,
+                          None, 0, None) == 1
+    assert L.crvq_dequant(4, 16, 8, 8, FAKE, 2, FAKE, 0, 16, 0, None, 0, None, None, None, FAKE, FAKE, 0, 16, FAKE, 0, 16,
+                          ws, 1 << 20, None) == 1
+    assert "mutually exclusive" in err(L)
+    assert L.crvq_gather_vectors(FAKE, 0, 4, 2, 16, 8, None, 3, FAKE, 0, None) == 1
+    assert L.crvq_gather_vectors(FAKE, 0, 4, 2, 16, 8, FAKE, 3, FAKE, 1, None) == 1
+
+
+def _imports(path):
+    src = open(path).read()
+    return set(re.findall(r"^\s*(?:from|import)\s+([\w\.]+)", src, re.M))
+
+
+def test_oracle_and_gpu_path_share_no_code():
+    odir = os.path.join(ROOT, "oracle")
+    pdir = os.path.join(ROOT, "paper_2412_09282_amd")
+    for f in os.listdir(odir):
+        if f.endswith(".py"):
+            assert not any(m.startswith("paper_2412_09282_amd") for m in _imports(os.path.join(odir, f))), f
+    for root, _, files in os.walk(pdir):
+        for f in files:
+            p = os.path.join(root, f)
+            if f.endswith(".py"):
+                assert not any(m.startswith("oracle") for m in _imports(p)), p
+            if f.endswith((".hip", ".h", ".cpp")):
+                assert "oracle" not in open(p).read().lower(), p

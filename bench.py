@@ -162,7 +162,7 @@ def main():
         import oracle
         oracle.build()
         Cb = st.C_base.detach().cpu().numpy()
-        codes_gpu = st.codes.detach().cpu().numpy()
+        codes_gpu = st.codes_base.detach().cpu().numpy()
         Vs = oracle.vectors(st.Ws.detach().cpu().numpy(), d)
         # calibrate, then time a sample sized for about --cpu-seconds of oracle work
         probe = inputs.sample_rows(wl, 0, n, 64)

@@ -100,7 +100,8 @@ crvq_status crvq_channel_importance(const void* A, int64_t lda, const void* B, i
  * for r < M, k < N.  in and out are M x N of `dtype`, must not overlap.
  * in may be NULL (then only perm is computed; M is ignored).  An
  * out-of-range perm entry leaves the affected output elements unwritten.
- * workspace: crvq_reorder_workspace_size(N) bytes.
+ * workspace: crvq_reorder_workspace_size(N) bytes, needed when importance != NULL or
+ * inverse != 0.  N <= 2^20.
  */
 size_t crvq_reorder_workspace_size(int64_t N);
 crvq_status crvq_reorder(const void* in, int64_t ld_in, void* out, int64_t ld_out, int dtype, int64_t M,

@@ -169,7 +169,7 @@ def crvq_reorder(inp: Optional[torch.Tensor], out: Optional[torch.Tensor], perm:
     N = perm.numel()
     M = 0 if inp is None else inp.shape[0]
     dev = perm.device
-    ws = _workspace(L.crvq_reorder_workspace_size(N), dev) if inverse else None
+    ws = _workspace(L.crvq_reorder_workspace_size(N), dev) if (inverse or importance is not None) else None
     _check("crvq_reorder", L.crvq_reorder(
         _ptr(inp), 0 if inp is None else inp.stride(0), _ptr(out), 0 if out is None else out.stride(0),
         CRVQ_F32 if inp is None else dtype_code(inp), M, N, _ptr(importance), _ptr(perm), int(bool(inverse)),

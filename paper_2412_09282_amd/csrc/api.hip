@@ -153,14 +153,17 @@ crvq_status crvq_channel_importance(const void* A, int64_t lda, const void* B, i
 }
 
 // ------------------------------------------------------------------------------------------------
-size_t crvq_reorder_workspace_size(int64_t N) { return N < 1 ? 0 : align256(static_cast<size_t>(N) * 4); }
+size_t crvq_reorder_workspace_size(int64_t N) {
+  if (N < 1) return 0;
+  return align256(static_cast<size_t>(N) * 4) + align256(static_cast<size_t>(rank_chunks(N)) * N * 4);
+}
 
 crvq_status crvq_reorder(const void* in, int64_t ld_in, void* out, int64_t ld_out, int dtype, int64_t M, int64_t N,
                          const float* importance, int32_t* perm, int inverse, void* workspace, size_t ws_bytes,
                          void* stream) {
   static const char* fn = "crvq_reorder";
   g_err.clear();
-  if (N < 1 || N > (1LL << 24)) return fail(CRVQ_ERR_INVALID, "%s: N = %lld outside [1, 2^24]", fn, (long long)N);
+  if (N < 1 || N > (1LL << 20)) return fail(CRVQ_ERR_INVALID, "%s: N = %lld outside [1, 2^20]", fn, (long long)N);
   if (!perm) return fail(CRVQ_ERR_INVALID, "%s: perm must not be NULL", fn);
   if (!importance && !in) return fail(CRVQ_ERR_INVALID, "%s: nothing to do (importance and in are both NULL)", fn);
   if (in) {
@@ -174,23 +177,24 @@ crvq_status crvq_reorder(const void* in, int64_t ld_in, void* out, int64_t ld_ou
       const size_t span_out = static_cast<size_t>((M - 1) * ld_out + N) * es;
       if (overlaps(in, span_in, out, span_out)) return fail(CRVQ_ERR_INVALID, "%s: in and out overlap", fn);
     }
-    if (inverse) {
-      crvq_status s = check_ws(workspace, ws_bytes, crvq_reorder_workspace_size(N), fn);
-      if (s) return s;
-    }
+  }
+  if (importance || (in && inverse)) {
+    crvq_status s = check_ws(workspace, ws_bytes, crvq_reorder_workspace_size(N), fn);
+    if (s) return s;
   }
   hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t* inv_ws = static_cast<int32_t*>(workspace);
+  int32_t* rank_ws = inv_ws ? inv_ws + align256(static_cast<size_t>(N) * 4) / 4 : nullptr;
   if (importance) {
-    crvq_status s = hip_status(launch_rank_perm(importance, N, perm, st), fn);
+    crvq_status s = hip_status(launch_rank_perm(importance, N, perm, rank_ws, st), fn);
     if (s) return s;
   }
   if (!in || M == 0) return CRVQ_OK;
   const int32_t* src = perm;
   if (inverse) {
-    int32_t* inv = static_cast<int32_t*>(workspace);
-    crvq_status s = hip_status(launch_inverse_perm(perm, N, inv, st), fn);
+    crvq_status s = hip_status(launch_inverse_perm(perm, N, inv_ws, st), fn);
     if (s) return s;
-    src = inv;
+    src = inv_ws;
   }
   return hip_status(launch_gather_columns(in, ld_in, out, ld_out, esize(dtype), M, N, src, st), fn);
 }

@@ -95,7 +95,9 @@ hipError_t launch_colreduce(const void* A, int64_t lda, const void* B, int64_t l
                             const float* scale, int reduce, float* out, void* ws, hipStream_t stream);
 
 // ---- reorder / gathers (k_reorder.hip) -----------------------------------------------------------
-hipError_t launch_rank_perm(const float* importance, int64_t N, int32_t* perm, hipStream_t stream);
+int rank_chunks(int64_t N);
+// part: int32 scratch of rank_chunks(N) * N entries
+hipError_t launch_rank_perm(const float* importance, int64_t N, int32_t* perm, int32_t* part, hipStream_t stream);
 hipError_t launch_inverse_perm(const int32_t* perm, int64_t N, int32_t* inv, hipStream_t stream);
 hipError_t launch_gather_columns(const void* in, int64_t ld_in, void* out, int64_t ld_out, int esize, int64_t M,
                                  int64_t N, const int32_t* src_idx, hipStream_t stream);

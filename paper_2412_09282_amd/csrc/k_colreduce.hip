@@ -77,6 +77,7 @@ __global__ __launch_bounds__(256) void colreduce_final(const double* __restrict_
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (j >= N) return;
   double acc = 0.0;
+#pragma unroll 8
   for (int s = 0; s < slabs; ++s) {
     const double v = part[static_cast<int64_t>(s) * N + j];
     acc = (reduce == 0) ? acc + v : (v > acc ? v : acc);
@@ -93,8 +94,9 @@ struct Plan {
 Plan plan(int64_t M, int64_t N) {
   Plan p;
   p.col_blocks = cdiv(cdiv(N, kCols), 256);
-  int64_t want = cdiv(4096, p.col_blocks);      // aim for >= 4096 blocks in flight
-  int64_t max_slabs = cdiv(M, 8);               // at least 8 rows per slab
+  int64_t want = cdiv(1024, p.col_blocks);      // aim for >= 1024 blocks in flight
+  if (want > 64) want = 64;                     // the second pass folds at most 64 slabs per column
+  int64_t max_slabs = cdiv(M, 16);              // at least 16 rows per slab
   p.slabs = want < max_slabs ? want : max_slabs;
   if (p.slabs < 1) p.slabs = 1;
   p.rows_per_slab = cdiv(M, p.slabs);

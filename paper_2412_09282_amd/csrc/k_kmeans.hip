@@ -10,6 +10,7 @@
 // 3. each centroid is the fixed-order fp64 reduction of its segment, divided by the count and
 //    rounded once to the codebook's type; an empty segment leaves the centroid untouched.
 // Codes outside [0, K) are dropped in the first pass and belong to no cluster.
+// Codebooks of at most 256 codewords take a sort-free path (see small_k_partial).
 #include "crvq_internal.h"
 
 namespace crvq {
@@ -287,6 +288,126 @@ __global__ __launch_bounds__(256) void segment_mean_block(RowSrc src, const int*
   if (tid < d) store_centroid(C, ct, k, d, tid, sh[tid * 256] / static_cast<double>(e - s));
 }
 
+// ---- small codebooks (K <= 256): one thread per code, no global sort --------------------------
+// Each block walks a contiguous range of vectors in rounds of 2048.  A round's codes are stably
+// bucket-sorted in LDS (the same ballot multisplit as the radix passes, so no atomics), then
+// thread k adds the members of code k in ascending order to its fp64 accumulators.  The per-block
+// partial sums are folded in block order by a second kernel.
+constexpr int kRound = 2048;  // 4 waves x 8 batches x 64 lanes
+
+__global__ __launch_bounds__(256) void small_k_partial(RowSrc src, const int32_t* __restrict__ codes, int64_t K,
+                                                       int64_t per_block, double* __restrict__ part,
+                                                       int* __restrict__ pcount) {
+  __shared__ int s_pos[kRound];
+  __shared__ int s_start[257];
+  __shared__ int wh[4][256];
+  __shared__ int sh_scan[256];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int d = src.d;
+  const int64_t n = src.n;
+  const int64_t b0 = static_cast<int64_t>(blockIdx.x) * per_block;
+  const int64_t b1 = (b0 + per_block < n) ? b0 + per_block : n;
+  double acc[16];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) acc[t] = 0.0;
+  int cnt = 0;
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+  for (int64_t base = b0; base < b1; base += kRound) {
+    for (int b = tid; b < 1024; b += 256) (&wh[0][0])[b] = 0;
+    __syncthreads();
+    int dig[8];
+    uint64_t peer[8];
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt) {
+      const int64_t idx = base + w * 512 + bt * 64 + lane;
+      const int c = (idx < b1) ? codes[idx] : -1;
+      const bool valid = c >= 0 && c < K;
+      dig[bt] = valid ? c : -1;
+      peer[bt] = peer_mask(valid, valid ? c : 0);
+      if (valid && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) wh[w][c] += __popcll(peer[bt]);
+    }
+    __syncthreads();
+    // bucket starts: exclusive scan over codes of the round's per-code totals
+    const int tot = wh[0][tid] + wh[1][tid] + wh[2][tid] + wh[3][tid];
+    sh_scan[tid] = tot;
+    __syncthreads();
+    for (int off = 1; off < 256; off <<= 1) {
+      const int v = (tid >= off) ? sh_scan[tid - off] : 0;
+      __syncthreads();
+      sh_scan[tid] += v;
+      __syncthreads();
+    }
+    const int start = sh_scan[tid] - tot;
+    s_start[tid] = start;
+    if (tid == 255) s_start[256] = sh_scan[255];
+    int run = start;
+    for (int ww = 0; ww < 4; ++ww) {
+      const int c = wh[ww][tid];
+      wh[ww][tid] = run;
+      run += c;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int bt = 0; bt < 8; ++bt) {
+      if (dig[bt] >= 0) {
+        const int pos = wh[w][dig[bt]] + __popcll(peer[bt] & lt);
+        if (pos >= 0 && pos < kRound) s_pos[pos] = w * 512 + bt * 64 + lane;
+      }
+      if (dig[bt] >= 0 && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) wh[w][dig[bt]] += __popcll(peer[bt]);
+    }
+    __syncthreads();
+    if (tid < K) {
+      const int e = s_start[tid + 1];
+      for (int j = s_start[tid]; j < e; ++j) {
+        const int64_t off = row_offset(src, base + s_pos[j]);
+#pragma unroll
+        for (int t = 0; t < 16; ++t)
+          if (t < d) acc[t] = acc[t] + row_elem(src, off, t);
+      }
+      cnt += e - s_start[tid];
+    }
+    __syncthreads();
+  }
+  if (tid < K) {
+    double* pp = part + (static_cast<int64_t>(blockIdx.x) * K + tid) * d;
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      if (t < d) pp[t] = acc[t];
+    pcount[static_cast<int64_t>(blockIdx.x) * K + tid] = cnt;
+  }
+}
+
+__global__ __launch_bounds__(256) void small_k_final(const double* __restrict__ part, const int* __restrict__ pcount,
+                                                     int blocks, int64_t K, int d, void* C, int ct,
+                                                     int32_t* __restrict__ counts) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= K * d) return;
+  const int64_t k = e / d;
+  const int t = static_cast<int>(e - k * d);
+  double acc = 0.0;
+  int cnt = 0;
+  for (int b = 0; b < blocks; ++b) {
+    acc = acc + part[(static_cast<int64_t>(b) * K + k) * d + t];
+    cnt += pcount[static_cast<int64_t>(b) * K + k];
+  }
+  if (counts && t == 0) counts[k] = cnt;
+  if (cnt > 0) store_centroid(C, ct, k, d, t, acc / static_cast<double>(cnt));
+}
+
+struct SmallPlan {
+  int64_t blocks;
+  int64_t per_block;
+};
+
+SmallPlan small_plan(int64_t n) {
+  SmallPlan p;
+  const int64_t rounds = cdiv(n > 0 ? n : 1, kRound);
+  p.blocks = rounds < 512 ? rounds : 512;
+  p.per_block = cdiv(rounds, p.blocks) * kRound;
+  p.blocks = cdiv(n > 0 ? n : 1, p.per_block);
+  return p;
+}
+
 struct KmWs {
   int* keys[2];
   int* vals[2];
@@ -325,6 +446,12 @@ hipError_t exclusive_scan(const int* in, int64_t n, int* sums, int* out, int* to
 
 size_t kmeans_ws_bytes(int64_t n, int64_t K) {
   WsCursor c(nullptr);
+  if (K <= 256) {
+    SmallPlan p = small_plan(n);
+    c.take<double>(static_cast<size_t>(p.blocks * K * 16));
+    c.take<int>(static_cast<size_t>(p.blocks * K));
+    return c.used;
+  }
   carve(c, n, K);
   return c.used;
 }
@@ -333,6 +460,16 @@ hipError_t launch_kmeans_update(const RowSrc& src, const int32_t* codes, int64_t
                                 int32_t* counts, void* ws, hipStream_t stream) {
   const int64_t n = src.n;
   WsCursor cur(ws);
+  if (K <= 256) {
+    SmallPlan p = small_plan(n);
+    double* part = cur.take<double>(static_cast<size_t>(p.blocks * K * 16));
+    int* pcount = cur.take<int>(static_cast<size_t>(p.blocks * K));
+    hipLaunchKernelGGL(small_k_partial, dim3(static_cast<unsigned>(p.blocks)), dim3(256), 0, stream, src, codes, K,
+                       p.per_block, part, pcount);
+    hipLaunchKernelGGL(small_k_final, dim3(static_cast<unsigned>(cdiv(K * src.d, 256))), dim3(256), 0, stream, part,
+                       pcount, static_cast<int>(p.blocks), K, src.d, C, c_type, counts);
+    return hipGetLastError();
+  }
   KmWs w = carve(cur, n, K);
   const int64_t n_tiles = cdiv(n > 0 ? n : 1, kTile);
   const int passes = (K <= 256) ? 1 : 2;

@@ -2,8 +2,9 @@
 // Fig. 3 right) and the row gathers that move columns and vectors.
 //
 // rank_perm: perm = stable descending order of the importance (NaN last, equal values by
-//   ascending channel).  Each thread owns one channel and counts, over the whole importance array
-//   streamed through LDS, the channels that precede it: its rank is exact and unique, so
+//   ascending channel).  Each thread owns one channel and counts the channels that precede it; the
+//   count is split over up to 64 chunks of the importance array (grid y), each streamed through LDS,
+//   and the partial counts are summed in a second pass.  The rank is exact and unique, so
 //   perm[rank] = channel is a permutation without any atomic.  N is at most a few ten thousand
 //   channels, so the O(N^2) comparisons take microseconds.
 // gather_columns: out[r, k] = in[r, src[k]] with the row staged in LDS (coalesced in and out);
@@ -20,20 +21,34 @@ __device__ __forceinline__ bool precedes(float vi, int i, float vj, int j) {
   return i < j;                             // equal (or both NaN): lower channel first
 }
 
-__global__ __launch_bounds__(256) void rank_perm_kernel(const float* __restrict__ imp, int64_t N, int32_t* __restrict__ perm) {
+// Partial ranks: block (x, y) counts, for 256 channels, the channels of chunk y that precede them.
+__global__ __launch_bounds__(256) void rank_partial_kernel(const float* __restrict__ imp, int64_t N, int64_t chunk,
+                                                           int32_t* __restrict__ part) {
   __shared__ float tile[1024];
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   const float vj = (j < N) ? imp[j] : 0.0f;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.y) * chunk;
+  const int64_t i1 = (i0 + chunk < N) ? i0 + chunk : N;
   int rank = 0;
-  for (int64_t base = 0; base < N; base += 1024) {
-    for (int t = threadIdx.x; t < 1024; t += 256) tile[t] = (base + t < N) ? imp[base + t] : 0.0f;
+  for (int64_t base = i0; base < i1; base += 1024) {
+    for (int t = threadIdx.x; t < 1024; t += 256) tile[t] = (base + t < i1) ? imp[base + t] : 0.0f;
     __syncthreads();
-    const int lim = static_cast<int>((N - base) < 1024 ? (N - base) : 1024);
+    const int lim = static_cast<int>((i1 - base) < 1024 ? (i1 - base) : 1024);
     if (j < N)
       for (int t = 0; t < lim; ++t) rank += precedes(tile[t], static_cast<int>(base + t), vj, static_cast<int>(j)) ? 1 : 0;
     __syncthreads();
   }
-  if (j < N) perm[rank] = static_cast<int32_t>(j);
+  if (j < N) part[static_cast<int64_t>(blockIdx.y) * N + j] = rank;
+}
+
+// rank = sum of the partial ranks; perm[rank] = channel (ranks are distinct, so no two threads collide)
+__global__ __launch_bounds__(256) void rank_scatter_kernel(const int32_t* __restrict__ part, int chunks, int64_t N,
+                                                           int32_t* __restrict__ perm) {
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (j >= N) return;
+  int64_t rank = 0;
+  for (int s = 0; s < chunks; ++s) rank += part[static_cast<int64_t>(s) * N + j];
+  if (rank >= 0 && rank < N) perm[rank] = static_cast<int32_t>(j);
 }
 
 __global__ __launch_bounds__(256) void fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
@@ -106,8 +121,18 @@ __global__ __launch_bounds__(256) void gather_vectors_kernel(RowSrc src, const i
 
 }  // namespace
 
-hipError_t launch_rank_perm(const float* importance, int64_t N, int32_t* perm, hipStream_t stream) {
-  hipLaunchKernelGGL(rank_perm_kernel, dim3(static_cast<unsigned>(cdiv(N, 256))), dim3(256), 0, stream, importance, N, perm);
+int rank_chunks(int64_t N) {
+  const int64_t c = cdiv(N, 512);
+  return static_cast<int>(c < 1 ? 1 : (c > 64 ? 64 : c));
+}
+
+hipError_t launch_rank_perm(const float* importance, int64_t N, int32_t* perm, int32_t* part, hipStream_t stream) {
+  const int S = rank_chunks(N);
+  const int64_t chunk = cdiv(N, S);
+  hipLaunchKernelGGL(rank_partial_kernel, dim3(static_cast<unsigned>(cdiv(N, 256)), static_cast<unsigned>(S)), dim3(256),
+                     0, stream, importance, N, chunk, part);
+  hipLaunchKernelGGL(rank_scatter_kernel, dim3(static_cast<unsigned>(cdiv(N, 256))), dim3(256), 0, stream, part, S, N,
+                     perm);
   return hipGetLastError();
 }
 

@@ -21,6 +21,10 @@
 
 #include <climits>
 
+#ifndef CRVQ_MIN_TRACKED_TILES
+#define CRVQ_MIN_TRACKED_TILES 1
+#endif
+
 namespace crvq {
 namespace {
 
@@ -241,6 +245,15 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
           const bool lt = x < m[cb][0];
           m[cb][0] = fminf(m[cb][0], x);
           id[cb][0] = lt ? Ti : id[cb][0];
+        } else if constexpr (NB == 2) {
+          // m0 <= m1 <= rest is kept sorted with medians: 10 VALU ops per tile and row
+          const bool lt0 = x < m[cb][0];
+          const bool lt1 = x < m[cb][1];
+          rest[cb] = __builtin_amdgcn_fmed3f(m[cb][1], rest[cb], x);
+          m[cb][1] = __builtin_amdgcn_fmed3f(m[cb][0], m[cb][1], x);
+          m[cb][0] = fminf(m[cb][0], x);
+          id[cb][1] = lt0 ? id[cb][0] : (lt1 ? Ti : id[cb][1]);
+          id[cb][0] = lt0 ? Ti : id[cb][0];
         } else {
           int xi = Ti;
 #pragma unroll
@@ -408,7 +421,31 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
       TD[j] = __builtin_inf();
       TK[j] = INT_MAX;
     }
-    for (int64_t k = tid; k < K; k += 256) list_insert<NB>(TD, TK, exact_dist(xd, C, ct, k, d), static_cast<int>(k));
+    // four codewords per thread and round, loaded before any of them is scored, so the loads overlap
+    for (int64_t k0 = tid; k0 < K; k0 += 4 * 256) {
+      float cw[4][16];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t k = k0 + u * 256;
+#pragma unroll
+        for (int t = 0; t < 16; ++t) cw[u][t] = (k < K && t < d) ? static_cast<float>(cb_elem(C, ct, k, d, t)) : 0.0f;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t k = k0 + u * 256;
+        if (k < K) {
+          double acc = 0.0;
+#pragma unroll
+          for (int t = 0; t < 16; ++t) {
+            if (t < d) {
+              const double diff = xd[t] - static_cast<double>(cw[u][t]);
+              acc = acc + diff * diff;
+            }
+          }
+          list_insert<NB>(TD, TK, acc, static_cast<int>(k));
+        }
+      }
+    }
     for (int stride = 128; stride >= 1; stride >>= 1) {
       if (tid >= stride && tid < 2 * stride) {
 #pragma unroll
@@ -536,7 +573,9 @@ static int next_pow2_nb(int top) {
 
 ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   ScreenPlan p;
-  p.nb = next_pow2_nb(top);
+  // CRVQ_MIN_TRACKED_TILES = 2 would make the exact rescue almost never needed, but its extra VALU
+  // work and registers cost more screen time (12 % at K = 65536) than the rescues it saves.
+  p.nb = next_pow2_nb(top < CRVQ_MIN_TRACKED_TILES ? CRVQ_MIN_TRACKED_TILES : top);
   p.cb = p.nb <= 2 ? 8 : (p.nb == 4 ? 4 : (p.nb == 8 ? 2 : 1));
   p.ks = d <= 4 ? 1 : (d <= 8 ? 2 : 4);
   p.tiles = cdiv(K, 16);

@@ -45,13 +45,13 @@ class EventTimer:
         self.pairs = []
         self.open = None
 
-    def begin(self, name):
+    def pre(self, name, kw):
         if name.startswith(self.prefix):
             e = self.torch.cuda.Event(enable_timing=True)
             e.record()
             self.open = e
 
-    def end(self, name):
+    def post(self, name, kw):
         if name.startswith(self.prefix) and self.open is not None:
             e = self.torch.cuda.Event(enable_timing=True)
             e.record()
@@ -115,7 +115,7 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        st = q.run(Wd, Xd, bi, ei, timer=timer)
+        st = q.run(Wd, Xd, bi, ei, hooks=[timer])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     log(f"timed {args.steps} steps")

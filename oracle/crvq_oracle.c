@@ -91,19 +91,30 @@ void oracle_kmeans_means(const float* V, int64_t n, int d, const int32_t* codes,
  * 1); B may be NULL (treated as 0) and scale may be NULL (s_j = 1). */
 void oracle_colreduce(const float* A, int64_t lda, const float* B, int64_t ldb, int64_t M,
                       int64_t N, const double* scale, int reduce, double* out) {
-#pragma omp parallel for schedule(static)
-  for (int64_t j = 0; j < N; ++j) {
-    double acc = 0.0;
+  /* Every thread owns a contiguous range of columns and walks the rows in ascending i, so each
+   * column is still reduced in row order while the matrix is read row by row. */
+#pragma omp parallel
+  {
+    int64_t nt = 1, id = 0;
+#ifdef _OPENMP
+    nt = omp_get_num_threads();
+    id = omp_get_thread_num();
+#endif
+    int64_t j0 = N * id / nt, j1 = N * (id + 1) / nt;
+    double* acc = (double*)calloc((size_t)(j1 - j0 + 1), sizeof(double));
     for (int64_t i = 0; i < M; ++i) {
-      double x = (double)A[i * lda + j];
-      if (B) x = x - (double)B[i * ldb + j];
-      double sq = x * x;
-      if (reduce == 0)
-        acc = acc + sq;
-      else if (sq > acc)
-        acc = sq;
+      for (int64_t j = j0; j < j1; ++j) {
+        double x = (double)A[i * lda + j];
+        if (B) x = x - (double)B[i * ldb + j];
+        double sq = x * x;
+        if (reduce == 0)
+          acc[j - j0] = acc[j - j0] + sq;
+        else if (sq > acc[j - j0])
+          acc[j - j0] = sq;
+      }
     }
-    out[j] = scale ? scale[j] * acc : acc;
+    for (int64_t j = j0; j < j1; ++j) out[j] = scale ? scale[j] * acc[j - j0] : acc[j - j0];
+    free(acc);
   }
 }
 

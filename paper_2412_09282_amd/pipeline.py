@@ -15,9 +15,10 @@ residuals are float32; the critical vectors' final codes come from the beam
 search (width 1 = greedy) on the exact residual.
 
 Every arithmetic step runs in the library's kernels; this module only
-allocates device tensors and sequences the calls.  Passing `trace` (a list)
-records the inputs and outputs of every call (copied to the host) so a test
-can re-run each call on the oracle from the same bytes.
+allocates device tensors and sequences the calls.  Hooks see the device
+tensors right around every call; passing `trace` (a list) records host copies
+of every call's inputs and outputs, so a test can re-run each call from the
+same bytes.
 """
 from __future__ import annotations
 
@@ -86,10 +87,12 @@ class LayerQuantizer:
         self.W_hat = torch.empty(M, N, dtype=dtype, device=device)
 
     def run(self, W: torch.Tensor, X: torch.Tensor, base_idx: torch.Tensor, ext_idx: List[torch.Tensor],
-            trace: Optional[list] = None, timer=None) -> LayerState:
-        """timer: optional object with begin(name) / end(name), called right around each library call."""
+            trace: Optional[list] = None, hooks=()) -> LayerState:
+        """hooks: objects with pre(name, inputs) / post(name, outputs), called right around each library
+        call; trace: a list that receives host copies of every call's inputs and outputs."""
         cfg, d, M, N = self.cfg, self.cfg.d, self.M, self.N
-        rec = _Recorder(trace, timer)
+        hooks = list(hooks) + ([TraceHook(trace)] if trace is not None else [])
+        rec = _Recorder(hooks)
 
         rec.pre("hdiag", A=X)
         C.crvq_channel_importance(X, self.hdiag)
@@ -159,12 +162,11 @@ class LayerQuantizer:
             rec.post(f"update_{tag}_{it}", C=Cb)
 
 
-class _Recorder:
-    """Copies the inputs and outputs of each call to the host when tracing."""
+class TraceHook:
+    """Copies the inputs and outputs of every call to the host, in call order."""
 
-    def __init__(self, trace: Optional[list], timer):
+    def __init__(self, trace: list):
         self.trace = trace
-        self.timer = timer
         self.cur: Dict = {}
 
     @staticmethod
@@ -172,19 +174,29 @@ class _Recorder:
         if isinstance(v, torch.Tensor):
             return v.detach().to("cpu", copy=True)
         if isinstance(v, (list, tuple)):
-            return [_Recorder._host(x) for x in v]
+            return [TraceHook._host(x) for x in v]
         return v
 
+    def pre(self, name: str, kw: Dict):
+        self.cur = {"name": name, "in": {k: self._host(v) for k, v in kw.items()}}
+
+    def post(self, name: str, kw: Dict):
+        self.cur["out"] = {k: self._host(v) for k, v in kw.items()}
+        self.trace.append(self.cur)
+        self.cur = {}
+
+
+class _Recorder:
+    """Calls every hook's pre(name, inputs) right before and post(name, outputs) right after each
+    library call (inputs/outputs are the device tensors involved)."""
+
+    def __init__(self, hooks):
+        self.hooks = list(hooks)
+
     def pre(self, name: str, **kw):
-        if self.trace is not None:
-            self.cur = {"name": name, "in": {k: self._host(v) for k, v in kw.items()}}
-        if self.timer is not None:
-            self.timer.begin(name)
+        for h in self.hooks:
+            h.pre(name, kw)
 
     def post(self, name: str, **kw):
-        if self.timer is not None:
-            self.timer.end(name)
-        if self.trace is not None:
-            self.cur["out"] = {k: self._host(v) for k, v in kw.items()}
-            self.trace.append(self.cur)
-            self.cur = {}
+        for h in reversed(self.hooks):
+            h.post(name, kw)

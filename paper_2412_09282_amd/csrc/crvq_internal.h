@@ -59,12 +59,13 @@ struct ScreenPlan {
 ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top);
 
 struct ScreenWs {
-  float* apack;
-  float* cnp;
-  double* pD;
-  int* pK;
-  float* pR;
-  double* xn2;
+  float* apack;  // codebook in MFMA A-operand order, tiles x 64 lanes x ks
+  float* cnp;    // ||c||^2 per codeword, +inf for padding
+  int* pT;       // top-B: kept tile ids, [split][lane group][nb][row]
+  float* pR;     // smallest screen value outside the exactly scored codewords, [split][row]
+  double* pD;    // top-1: exact distance of the split's winner, [split][row]
+  int* pK;       // top-1: its codeword, [split][row]
+  double* xn2;   // top-1: ||x||^2 per row (fp64)
 };
 // Carves the screen's scratch out of `ws`; returns it (pointers null on a dry run).
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc);

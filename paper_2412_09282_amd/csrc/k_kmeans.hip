@@ -23,9 +23,10 @@ constexpr int kScanBlock = 4096;   // elements per scan block: 256 threads x 16
 __device__ __forceinline__ float bf16_to_f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 __device__ __forceinline__ int64_t row_offset(const RowSrc& s, int64_t i) {
-  int64_t r = i / s.vpr;
-  int64_t g = i - r * s.vpr;
-  return r * s.ld + g * s.d;
+  if (s.ld == s.vpr * s.d) return i * s.d;  // rows packed back to back
+  const uint32_t r = static_cast<uint32_t>(i) / static_cast<uint32_t>(s.vpr);
+  const uint32_t g = static_cast<uint32_t>(i) - r * static_cast<uint32_t>(s.vpr);
+  return static_cast<int64_t>(r) * s.ld + static_cast<int64_t>(g) * s.d;
 }
 
 __device__ __forceinline__ double row_elem(const RowSrc& s, int64_t off, int t) {

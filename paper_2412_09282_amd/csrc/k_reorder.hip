@@ -93,9 +93,10 @@ __global__ __launch_bounds__(256) void gather_cols_direct(const T* __restrict__ 
 }
 
 __device__ __forceinline__ int64_t vec_offset(const RowSrc& s, int64_t i) {
-  int64_t r = i / s.vpr;
-  int64_t g = i - r * s.vpr;
-  return r * s.ld + g * s.d;
+  if (s.ld == s.vpr * s.d) return i * s.d;  // rows packed back to back
+  const uint32_t r = static_cast<uint32_t>(i) / static_cast<uint32_t>(s.vpr);
+  const uint32_t g = static_cast<uint32_t>(i) - r * static_cast<uint32_t>(s.vpr);
+  return static_cast<int64_t>(r) * s.ld + static_cast<int64_t>(g) * s.d;
 }
 
 __global__ __launch_bounds__(256) void gather_vectors_kernel(RowSrc src, const int64_t* __restrict__ idx, int64_t count,

@@ -9,10 +9,10 @@
 //    all codeword tiles of its codebook split.  v_mfma_f32_16x16x4_f32 leaves each lane 4 values of
 //    s for one row; the lane reduces them to the tile minimum and keeps, per row, the NB tiles with
 //    the smallest minimum and the smallest minimum of every other tile ("rest").  Nothing of the
-//    N x K distance matrix leaves the registers.
-// 3. exact: the codewords of the kept tiles are re-scored in fp64 with the same direct form as the
-//    definition (sum_t (x_t - c_t)^2, t ascending), merged across the four lane groups, the codebook
-//    splits and the tie order (D, k).
+//    N x K distance matrix leaves the registers; per row only the kept tile ids and rest are written.
+// 3. exact (finalize, one thread per row): the codewords of the kept tiles of all lane groups and
+//    codebook splits are re-scored in fp64 with the same direct form as the definition
+//    (sum_t (x_t - c_t)^2, t ascending) and ordered by (D, k).
 // 4. certify / rescue: with R = ||x|| + sqrt(D_top), every codeword that could beat the kept ones
 //    has ||c|| <= R, hence a screen error below delta(R); if rest + ||x||^2 - delta > D_top the kept
 //    list is provably the exact answer, otherwise the row is re-searched exactly over the whole
@@ -34,10 +34,11 @@ typedef float f2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ float bf16_to_f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
 __device__ __forceinline__ int64_t row_offset(const RowSrc& s, int64_t i) {
-  if (s.type == ET_F64) return i * s.d;
-  int64_t r = i / s.vpr;
-  int64_t g = i - r * s.vpr;
-  return r * s.ld + g * s.d;
+  if (s.type == ET_F64 || s.ld == s.vpr * s.d) return i * s.d;  // rows packed back to back
+  // a column slab: 32-bit division (vector counts are below 2^31)
+  const uint32_t r = static_cast<uint32_t>(i) / static_cast<uint32_t>(s.vpr);
+  const uint32_t g = static_cast<uint32_t>(i) - r * static_cast<uint32_t>(s.vpr);
+  return static_cast<int64_t>(r) * s.ld + static_cast<int64_t>(g) * s.d;
 }
 
 __device__ __forceinline__ double row_elem(const RowSrc& s, int64_t off, int t) {
@@ -51,18 +52,72 @@ __device__ __forceinline__ double cb_elem(const void* C, int type, int64_t k, in
   return static_cast<double>(bf16_to_f(static_cast<const uint16_t*>(C)[k * d + t]));
 }
 
-// fp64 direct-form squared distance, t ascending (no contraction: the library is built with
-// -ffp-contract=off).
-__device__ __forceinline__ double exact_dist(const double (&x)[16], const void* C, int ct, int64_t k, int d) {
-  double acc = 0.0;
+// The first DM elements of row i in fp64 (zero past d or for an invalid row).  The type is
+// dispatched once and every load is issued before any is used.
+// DM fp32 / bf16 elements at p as floats: 16-byte vector loads when d fills DM and p is aligned
+// (every lane then reads one contiguous piece), element loads otherwise; zero past d or when !ok.
+template <int DM>
+__device__ __forceinline__ void load_f32_elems(const float* p, int d, bool ok, float (&v)[DM]) {
+  if (DM % 4 == 0 && d == DM && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
 #pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    if (t < d) {
-      double diff = x[t] - cb_elem(C, ct, k, d, t);
-      acc = acc + diff * diff;
+    for (int q = 0; q < DM / 4; ++q) {
+      const f4 w = ok ? reinterpret_cast<const f4*>(p)[q] : f4{0.0f, 0.0f, 0.0f, 0.0f};
+      v[4 * q] = w[0];
+      v[4 * q + 1] = w[1];
+      v[4 * q + 2] = w[2];
+      v[4 * q + 3] = w[3];
     }
+  } else {
+#pragma unroll
+    for (int t = 0; t < DM; ++t) v[t] = (ok && t < d) ? p[t] : 0.0f;
   }
-  return acc;
+}
+
+template <int DM>
+__device__ __forceinline__ void load_bf16_elems(const uint16_t* p, int d, bool ok, float (&v)[DM]) {
+  if (DM % 4 == 0 && d == DM && (reinterpret_cast<uintptr_t>(p) & 7) == 0) {
+#pragma unroll
+    for (int q = 0; q < DM / 4; ++q) {
+      const uint2 w = ok ? reinterpret_cast<const uint2*>(p)[q] : make_uint2(0u, 0u);
+      v[4 * q] = __uint_as_float(w.x << 16);
+      v[4 * q + 1] = __uint_as_float(w.x & 0xffff0000u);
+      v[4 * q + 2] = __uint_as_float(w.y << 16);
+      v[4 * q + 3] = __uint_as_float(w.y & 0xffff0000u);
+    }
+  } else {
+#pragma unroll
+    for (int t = 0; t < DM; ++t) v[t] = (ok && t < d) ? bf16_to_f(p[t]) : 0.0f;
+  }
+}
+
+// The first DM elements of row i in fp64 (zero past d or for an invalid row).  The type is
+// dispatched once and every load is issued before any is used.
+template <int DM>
+__device__ __forceinline__ void load_row_exact(const RowSrc& s, int64_t i, bool valid, double (&x)[DM]) {
+  const int d = s.d;
+  const int64_t off = valid ? row_offset(s, i) : 0;
+  if (s.type == ET_F64) {
+    const double* p = static_cast<const double*>(s.base) + off;
+#pragma unroll
+    for (int t = 0; t < DM; ++t) x[t] = (valid && t < d) ? p[t] : 0.0;
+    return;
+  }
+  float v[DM];
+  if (s.type == ET_F32)
+    load_f32_elems<DM>(static_cast<const float*>(s.base) + off, d, valid, v);
+  else
+    load_bf16_elems<DM>(static_cast<const uint16_t*>(s.base) + off, d, valid, v);
+#pragma unroll
+  for (int t = 0; t < DM; ++t) x[t] = static_cast<double>(v[t]);
+}
+
+// Codeword k as float (exact for fp32 and bf16 books), zero past d or when !ok.
+template <int DM>
+__device__ __forceinline__ void load_codeword(const void* C, int ct, int64_t k, int d, bool ok, float (&c)[DM]) {
+  if (ct == ET_F32)
+    load_f32_elems<DM>(static_cast<const float*>(C) + (ok ? k * d : 0), d, ok, c);
+  else
+    load_bf16_elems<DM>(static_cast<const uint16_t*>(C) + (ok ? k * d : 0), d, ok, c);
 }
 
 __device__ __forceinline__ bool cless(double Da, int ka, double Db, int kb) {
@@ -184,8 +239,9 @@ template <int KS, int NB, int CB>
 __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __restrict__ apack,
                                                      const float* __restrict__ cnp, int64_t tiles, int64_t tps,
                                                      const void* __restrict__ C, int ct, int64_t K,
+                                                     int* __restrict__ pT, float* __restrict__ pR,
                                                      double* __restrict__ pD, int* __restrict__ pK,
-                                                     float* __restrict__ pR, double* __restrict__ xn2o) {
+                                                     double* __restrict__ xn2o) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int jl = lane & 15;
@@ -273,49 +329,83 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
     }
   }
 
+  if constexpr (NB == 1) {
+    // Top-1.  The lane group whose kept tile has the smallest minimum wins the row; the best tiles
+    // of the other three groups join the bound ("rest").  The winner's four codewords are re-scored
+    // exactly, one per lane group, and reduced in (D, k) order.  A row whose true minimum sits in a
+    // losing group simply fails certification later and is re-searched exactly.
+    constexpr int DM = 4 * KS;
 #pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const int64_t i = row0 + cb * 16 + jl;
-    const bool valid = i < n;
-    double xd[16];
-    double xn2 = 0.0;
-    const int64_t off = valid ? row_offset(src, i) : 0;
+    for (int cb = 0; cb < CB; ++cb) {
+      const int64_t i = row0 + cb * 16 + jl;
+      const bool valid = i < n;
+      const float mg = m[cb][0];
+      float mw = mg;
+      int gw = g;
 #pragma unroll
-    for (int t = 0; t < 16; ++t) xd[t] = (valid && t < d) ? row_elem(src, off, t) : 0.0;
+      for (int msk = 16; msk <= 32; msk <<= 1) {
+        const float om = __shfl_xor(mw, msk);
+        const int og = __shfl_xor(gw, msk);
+        const bool take = om < mw || (om == mw && og < gw);
+        mw = take ? om : mw;
+        gw = take ? og : gw;
+      }
+      float rr = (g == gw) ? rest[cb] : fminf(rest[cb], mg);
+      rr = fminf(rr, __shfl_xor(rr, 16));
+      rr = fminf(rr, __shfl_xor(rr, 32));
+      const int Tw = __shfl(id[cb][0], jl + 16 * gw);
+      const int64_t k = static_cast<int64_t>(Tw) * 16 + 4 * gw + g;
+      const bool ok = valid && Tw >= 0 && k < K;
+      double xd[DM];
+      float cw[DM];
+      load_row_exact<DM>(src, i, valid, xd);
+      load_codeword<DM>(C, ct, k, d, ok, cw);
+      double D = __builtin_inf();
+      int kk = INT_MAX;
+      if (ok) {
+        D = 0.0;
 #pragma unroll
-    for (int t = 0; t < 16; ++t)
-      if (t < d) xn2 = xn2 + xd[t] * xd[t];
-    double LD[NB];
-    int LK[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      LD[j] = __builtin_inf();
-      LK[j] = INT_MAX;
-    }
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int T = id[cb][j];
-      if (valid && T >= 0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t k = static_cast<int64_t>(T) * 16 + 4 * g + r;
-          if (k < K) list_insert<NB>(LD, LK, exact_dist(xd, C, ct, k, d), static_cast<int>(k));
+        for (int t = 0; t < DM; ++t) {
+          if (t < d) {
+            const double diff = xd[t] - static_cast<double>(cw[t]);
+            D = D + diff * diff;
+          }
         }
+        kk = static_cast<int>(k);
+      }
+#pragma unroll
+      for (int msk = 16; msk <= 32; msk <<= 1) {
+        const double oD = __shfl_xor(D, msk);
+        const int ok2 = __shfl_xor(kk, msk);
+        const bool take = cless(oD, ok2, D, kk);
+        D = take ? oD : D;
+        kk = take ? ok2 : kk;
+      }
+      if (g == 0 && valid) {
+        double xn2 = 0.0;
+#pragma unroll
+        for (int t = 0; t < DM; ++t)
+          if (t < d) xn2 = xn2 + xd[t] * xd[t];
+        pD[static_cast<int64_t>(split) * n + i] = D;
+        pK[static_cast<int64_t>(split) * n + i] = kk;
+        pR[static_cast<int64_t>(split) * n + i] = rr;
+        if (split == 0) xn2o[i] = xn2;
       }
     }
-    list_merge_xor<NB>(LD, LK, 16);
-    list_merge_xor<NB>(LD, LK, 32);
-    float rs = rest[cb];
-    rs = fminf(rs, __shfl_xor(rs, 16));
-    rs = fminf(rs, __shfl_xor(rs, 32));
-    if (g == 0 && valid) {
+  } else {
+    // Top-B: per row and lane group the kept tile ids; per row the smallest minimum of every other
+    // tile over the four lane groups (a lower bound on the screen value of every codeword not kept).
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        pD[(static_cast<int64_t>(split) * NB + j) * n + i] = LD[j];
-        pK[(static_cast<int64_t>(split) * NB + j) * n + i] = LK[j];
+    for (int cb = 0; cb < CB; ++cb) {
+      const int64_t i = row0 + cb * 16 + jl;
+      float rs = rest[cb];
+      rs = fminf(rs, __shfl_xor(rs, 16));
+      rs = fminf(rs, __shfl_xor(rs, 32));
+      if (i < n) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) pT[((static_cast<int64_t>(split) * 4 + g) * NB + j) * n + i] = id[cb][j];
+        if (g == 0) pR[static_cast<int64_t>(split) * n + i] = rs;
       }
-      pR[static_cast<int64_t>(split) * n + i] = rs;
-      if (split == 0) xn2o[i] = xn2;
     }
   }
 }
@@ -323,13 +413,17 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
 // ------------------------------------------------------------------------------------------------
 // 4. merge the splits, certify, rescue uncertain rows exactly, emit
 // ------------------------------------------------------------------------------------------------
-template <int NB>
-__global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top,
-                                                       const double* __restrict__ pD, const int* __restrict__ pK,
-                                                       const float* __restrict__ pR, const double* __restrict__ xn2a,
+// One thread per row.  Top-1: merge the splits' exact winners.  Top-B: re-score in fp64 the four
+// codewords of every kept tile of every lane group and split.  Then order by (D, k) and certify
+// against the screen bound.
+template <int KS, int NB>
+__global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top, const int* __restrict__ pT,
+                                                       const float* __restrict__ pR, const double* __restrict__ pD,
+                                                       const int* __restrict__ pK, const double* __restrict__ xn2a,
                                                        const void* __restrict__ C, int ct, int64_t K,
                                                        int32_t* __restrict__ codes, float* __restrict__ dist,
                                                        double* __restrict__ rowD, int* __restrict__ rowK) {
+  constexpr int DM = 4 * KS;  // dimensions this instantiation covers (d <= DM)
   __shared__ int scan[256];
   __shared__ int flagged[256];
   __shared__ double sD[128 * NB];
@@ -341,6 +435,15 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
   const bool valid = i < n;
   const int need = static_cast<int>((top < K) ? top : K);
 
+  double xd[DM];
+  double xn2 = 0.0;
+  if constexpr (NB > 1) {
+    load_row_exact<DM>(src, i, valid, xd);
+#pragma unroll
+    for (int t = 0; t < DM; ++t)
+      if (t < d) xn2 = xn2 + xd[t] * xd[t];
+  }
+
   double LD[NB];
   int LK[NB];
   float rest = __builtin_inff();
@@ -350,17 +453,49 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     LK[j] = INT_MAX;
   }
   bool certain = false;
-  if (valid) {
+  if (valid && NB == 1) {
+    xn2 = xn2a[i];
     for (int s = 0; s < splits; ++s) {
-      double OD[NB];
-      int OK[NB];
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        OD[j] = pD[(static_cast<int64_t>(s) * NB + j) * n + i];
-        OK[j] = pK[(static_cast<int64_t>(s) * NB + j) * n + i];
+      const double D = pD[static_cast<int64_t>(s) * n + i];
+      const int k = pK[static_cast<int64_t>(s) * n + i];
+      if (cless(D, k, LD[0], LK[0])) {
+        LD[0] = D;
+        LK[0] = k;
       }
-      list_merge<NB>(LD, LK, OD, OK);
       rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
+    }
+  }
+  if (valid) {
+    for (int s = 0; s < (NB > 1 ? splits : 0); ++s) {
+      rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
+      for (int g = 0; g < 4; ++g) {
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+          const int T = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+          if (T < 0) continue;
+          float cw[4][DM];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int64_t k = static_cast<int64_t>(T) * 16 + 4 * g + r;
+            load_codeword<DM>(C, ct, k, d, k < K, cw[r]);
+          }
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int64_t k = static_cast<int64_t>(T) * 16 + 4 * g + r;
+            if (k < K) {
+              double acc = 0.0;
+#pragma unroll
+              for (int t = 0; t < DM; ++t) {
+                if (t < d) {
+                  const double diff = xd[t] - static_cast<double>(cw[r][t]);
+                  acc = acc + diff * diff;
+                }
+              }
+              list_insert<NB>(LD, LK, acc, static_cast<int>(k));
+            }
+          }
+        }
+      }
     }
     double Dl = LD[0];
 #pragma unroll
@@ -369,7 +504,6 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     if (rest == __builtin_inff()) {
       certain = true;  // every codeword was scored exactly
     } else {
-      const double xn2 = xn2a[i];
       const double xn = sqrt(xn2);
       const double R = xn + sqrt(Dl);
       const double delta = static_cast<double>(4 * d + 24) * 0x1p-24 * (R * R + 2.0 * xn * R) + 1e-35;
@@ -410,10 +544,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
 
   for (int f = 0; f < nflag; ++f) {
     const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + flagged[f];
-    const int64_t off = row_offset(src, row);
-    double xd[16];
-#pragma unroll
-    for (int t = 0; t < 16; ++t) xd[t] = (t < d) ? row_elem(src, off, t) : 0.0;
+    double xr[DM];
+    load_row_exact<DM>(src, row, true, xr);
     double TD[NB];
     int TK[NB];
 #pragma unroll
@@ -423,12 +555,11 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     }
     // four codewords per thread and round, loaded before any of them is scored, so the loads overlap
     for (int64_t k0 = tid; k0 < K; k0 += 4 * 256) {
-      float cw[4][16];
+      float cw[4][DM];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int64_t k = k0 + u * 256;
-#pragma unroll
-        for (int t = 0; t < 16; ++t) cw[u][t] = (k < K && t < d) ? static_cast<float>(cb_elem(C, ct, k, d, t)) : 0.0f;
+        load_codeword<DM>(C, ct, k, d, k < K, cw[u]);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -436,9 +567,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
         if (k < K) {
           double acc = 0.0;
 #pragma unroll
-          for (int t = 0; t < 16; ++t) {
+          for (int t = 0; t < DM; ++t) {
             if (t < d) {
-              const double diff = xd[t] - static_cast<double>(cw[u][t]);
+              const double diff = xr[t] - static_cast<double>(cw[u][t]);
               acc = acc + diff * diff;
             }
           }
@@ -537,7 +668,7 @@ hipError_t launch_screen_t(const RowSrc& src, const void* C, int ct, int64_t K, 
                            const ScreenWs& w, hipStream_t stream) {
   dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
   hipLaunchKernelGGL((screen_kernel<KS, NB, CB>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
-                     p.tiles_per_split, C, ct, K, w.pD, w.pK, w.pR, w.xn2);
+                     p.tiles_per_split, C, ct, K, w.pT, w.pR, w.pD, w.pK, w.xn2);
   return hipGetLastError();
 }
 
@@ -545,8 +676,10 @@ template <int KS>
 hipError_t launch_screen_ks(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
                             const ScreenWs& w, hipStream_t stream) {
   switch (p.nb) {
-    case 1: return launch_screen_t<KS, 1, 8>(src, C, ct, K, p, w, stream);
-    case 2: return launch_screen_t<KS, 2, 8>(src, C, ct, K, p, w, stream);
+    case 1: return p.cb == 8 ? launch_screen_t<KS, 1, 8>(src, C, ct, K, p, w, stream)
+                             : launch_screen_t<KS, 1, 2>(src, C, ct, K, p, w, stream);
+    case 2: return p.cb == 8 ? launch_screen_t<KS, 2, 8>(src, C, ct, K, p, w, stream)
+                             : launch_screen_t<KS, 2, 2>(src, C, ct, K, p, w, stream);
     case 4: return launch_screen_t<KS, 4, 4>(src, C, ct, K, p, w, stream);
     case 8: return launch_screen_t<KS, 8, 2>(src, C, ct, K, p, w, stream);
     case 16: return launch_screen_t<KS, 16, 1>(src, C, ct, K, p, w, stream);
@@ -554,13 +687,27 @@ hipError_t launch_screen_ks(const RowSrc& src, const void* C, int ct, int64_t K,
   return hipErrorInvalidValue;
 }
 
-template <int NB>
+template <int KS, int NB>
 hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K, int top, const ScreenPlan& p,
                              const ScreenWs& w, int32_t* codes, float* dist, double* rowD, int* rowK,
                              hipStream_t stream) {
-  hipLaunchKernelGGL((finalize_kernel<NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream, src,
-                     p.splits, top, w.pD, w.pK, w.pR, w.xn2, C, ct, K, codes, dist, rowD, rowK);
+  hipLaunchKernelGGL((finalize_kernel<KS, NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
+                     src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, codes, dist, rowD, rowK);
   return hipGetLastError();
+}
+
+template <int KS>
+hipError_t launch_finalize_ks(const RowSrc& src, const void* C, int ct, int64_t K, int top, const ScreenPlan& p,
+                              const ScreenWs& w, int32_t* codes, float* dist, double* rowD, int* rowK,
+                              hipStream_t stream) {
+  switch (p.nb) {
+    case 1: return launch_finalize_t<KS, 1>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
+    case 2: return launch_finalize_t<KS, 2>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
+    case 4: return launch_finalize_t<KS, 4>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
+    case 8: return launch_finalize_t<KS, 8>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
+    case 16: return launch_finalize_t<KS, 16>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -587,6 +734,11 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
     int64_t maxs = p.tiles / 32 > 1 ? p.tiles / 32 : 1;
     splits = want < maxs ? want : maxs;
   }
+  // small codebooks cannot be split further: spread the rows over more, smaller workgroups instead
+  if (p.grid_x * splits < 1024 && p.nb <= 2) {
+    p.cb = 2;
+    p.grid_x = cdiv(n_rows, 64 * p.cb);
+  }
   p.tiles_per_split = cdiv(p.tiles, splits);
   p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
   return p;
@@ -597,10 +749,18 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
   const int64_t tiles = cdiv(K_alloc, 16);
   w.apack = ws.take<float>(static_cast<size_t>(tiles * 64 * p.ks));
   w.cnp = ws.take<float>(static_cast<size_t>(tiles * 16));
-  w.pD = ws.take<double>(static_cast<size_t>(p.splits) * p.nb * n_rows);
-  w.pK = ws.take<int>(static_cast<size_t>(p.splits) * p.nb * n_rows);
   w.pR = ws.take<float>(static_cast<size_t>(p.splits) * n_rows);
-  w.xn2 = ws.take<double>(static_cast<size_t>(n_rows));
+  if (p.nb == 1) {
+    w.pT = nullptr;
+    w.pD = ws.take<double>(static_cast<size_t>(p.splits) * n_rows);
+    w.pK = ws.take<int>(static_cast<size_t>(p.splits) * n_rows);
+    w.xn2 = ws.take<double>(static_cast<size_t>(n_rows));
+  } else {
+    w.pT = ws.take<int>(static_cast<size_t>(p.splits) * 4 * p.nb * n_rows);
+    w.pD = nullptr;
+    w.pK = nullptr;
+    w.xn2 = nullptr;
+  }
   return w;
 }
 
@@ -622,14 +782,11 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     default: e = launch_screen_ks<4>(src, C, ct, K, p, w, stream); break;
   }
   if (e != hipSuccess) return e;
-  switch (p.nb) {
-    case 1: return launch_finalize_t<1>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
-    case 2: return launch_finalize_t<2>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
-    case 4: return launch_finalize_t<4>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
-    case 8: return launch_finalize_t<8>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
-    case 16: return launch_finalize_t<16>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+  switch (p.ks) {
+    case 1: return launch_finalize_ks<1>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    case 2: return launch_finalize_ks<2>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    default: return launch_finalize_ks<4>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
   }
-  return hipErrorInvalidValue;
 }
 
 hipError_t launch_beam_merge(int64_t n, int n_par, int beam, int step, int n_books, const double* rowD,

@@ -403,8 +403,8 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
     inv = static_cast<int32_t*>(workspace);
     if ((s = hip_status(launch_inverse_perm(perm, n_cols, inv, st), fn))) return s;
   }
-  return hip_status(launch_dequant(M, n_cols, d, n_crit, b, inv, minuend, minuend_dtype, ld_min, out, out_dtype, ld_out, st),
-                    fn);
+  return hip_status(
+      launch_dequant(M, n_cols, d, n_crit, b, inv, perm, minuend, minuend_dtype, ld_min, out, out_dtype, ld_out, st), fn);
 }
 
 }  // extern "C"

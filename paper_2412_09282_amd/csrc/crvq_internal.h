@@ -116,7 +116,7 @@ struct DequantBooks {
   int64_t ldq_ext;
 };
 hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, const DequantBooks& books,
-                          const int32_t* inv_perm, const void* minuend, int min_type, int64_t ld_min, void* out,
-                          int out_type, int64_t ld_out, hipStream_t stream);
+                          const int32_t* inv_perm, const int32_t* perm, const void* minuend, int min_type,
+                          int64_t ld_min, void* out, int out_type, int64_t ld_out, hipStream_t stream);
 
 }  // namespace crvq

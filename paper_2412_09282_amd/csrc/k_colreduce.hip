@@ -10,7 +10,8 @@
 namespace crvq {
 namespace {
 
-constexpr int kCols = 4;  // columns per thread
+constexpr int kCols = 4;          // columns per thread
+constexpr int kRowsInFlight = 8;  // row loads issued back to back per thread
 
 __device__ __forceinline__ void load4(const void* p, int type, int64_t idx, int valid_cols, double (&v)[kCols]) {
   if (type == ET_F32) {
@@ -51,7 +52,31 @@ __global__ __launch_bounds__(256) void colreduce_partial(const void* __restrict_
   const int64_t i0 = static_cast<int64_t>(blockIdx.y) * rows_per_slab;
   const int64_t i1 = (i0 + rows_per_slab < M) ? i0 + rows_per_slab : M;
   double acc[kCols] = {0.0, 0.0, 0.0, 0.0};
-  for (int64_t i = i0; i < i1; ++i) {
+  // rows in groups of kRowsInFlight: every load of a group is issued before any is consumed
+  int64_t i = i0;
+  for (; i + kRowsInFlight <= i1; i += kRowsInFlight) {
+    double a[kRowsInFlight][kCols];
+#pragma unroll
+    for (int u = 0; u < kRowsInFlight; ++u) load4(A, type, (i + u) * lda + j0, valid_cols, a[u]);
+    if (B) {
+      double b[kRowsInFlight][kCols];
+#pragma unroll
+      for (int u = 0; u < kRowsInFlight; ++u) load4(B, type, (i + u) * ldb + j0, valid_cols, b[u]);
+#pragma unroll
+      for (int u = 0; u < kRowsInFlight; ++u)
+#pragma unroll
+        for (int c = 0; c < kCols; ++c) a[u][c] = a[u][c] - b[u][c];
+    }
+#pragma unroll
+    for (int u = 0; u < kRowsInFlight; ++u) {
+#pragma unroll
+      for (int c = 0; c < kCols; ++c) {
+        const double sq = a[u][c] * a[u][c];
+        acc[c] = (reduce == 0) ? acc[c] + sq : (sq > acc[c] ? sq : acc[c]);
+      }
+    }
+  }
+  for (; i < i1; ++i) {
     double a[kCols];
     load4(A, type, i * lda + j0, valid_cols, a);
     if (B) {
@@ -71,18 +96,29 @@ __global__ __launch_bounds__(256) void colreduce_partial(const void* __restrict_
     if (c < valid_cols) part[static_cast<int64_t>(blockIdx.y) * N + j0 + c] = acc[c];
 }
 
+// Block of 256 threads per 64 columns: thread (column c, lane group q) folds slabs q, q + 4, ... in
+// order, then the four group sums are combined in group order.
 __global__ __launch_bounds__(256) void colreduce_final(const double* __restrict__ part, int slabs, int64_t N,
                                                        const float* __restrict__ scale, int reduce,
                                                        float* __restrict__ out) {
-  const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (j >= N) return;
+  __shared__ double sh[4][64];
+  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
+  const int64_t j = static_cast<int64_t>(blockIdx.x) * 64 + c;
   double acc = 0.0;
-#pragma unroll 8
-  for (int s = 0; s < slabs; ++s) {
-    const double v = part[static_cast<int64_t>(s) * N + j];
-    acc = (reduce == 0) ? acc + v : (v > acc ? v : acc);
+  if (j < N) {
+#pragma unroll 4
+    for (int s = q; s < slabs; s += 4) {
+      const double v = part[static_cast<int64_t>(s) * N + j];
+      acc = (reduce == 0) ? acc + v : (v > acc ? v : acc);
+    }
   }
-  out[j] = static_cast<float>(scale ? static_cast<double>(scale[j]) * acc : acc);
+  sh[q][c] = acc;
+  __syncthreads();
+  if (q == 0 && j < N) {
+    double r = sh[0][c];
+    for (int g = 1; g < 4; ++g) r = (reduce == 0) ? r + sh[g][c] : (sh[g][c] > r ? sh[g][c] : r);
+    out[j] = static_cast<float>(scale ? static_cast<double>(scale[j]) * r : r);
+  }
 }
 
 struct Plan {
@@ -94,8 +130,8 @@ struct Plan {
 Plan plan(int64_t M, int64_t N) {
   Plan p;
   p.col_blocks = cdiv(cdiv(N, kCols), 256);
-  int64_t want = cdiv(1024, p.col_blocks);      // aim for >= 1024 blocks in flight
-  if (want > 64) want = 64;                     // the second pass folds at most 64 slabs per column
+  int64_t want = cdiv(4096, p.col_blocks);      // aim for >= 4096 blocks in flight
+  if (want > 512) want = 512;                   // bounds the fp64 partials (slabs x N)
   int64_t max_slabs = cdiv(M, 16);              // at least 16 rows per slab
   p.slabs = want < max_slabs ? want : max_slabs;
   if (p.slabs < 1) p.slabs = 1;
@@ -117,7 +153,7 @@ hipError_t launch_colreduce(const void* A, int64_t lda, const void* B, int64_t l
   double* part = static_cast<double*>(ws);
   hipLaunchKernelGGL(colreduce_partial, dim3(static_cast<unsigned>(p.col_blocks), static_cast<unsigned>(p.slabs)),
                      dim3(256), 0, stream, A, lda, B, ldb, type, M, N, reduce, p.rows_per_slab, part);
-  hipLaunchKernelGGL(colreduce_final, dim3(static_cast<unsigned>(cdiv(N, 256))), dim3(256), 0, stream, part,
+  hipLaunchKernelGGL(colreduce_final, dim3(static_cast<unsigned>(cdiv(N, 64))), dim3(256), 0, stream, part,
                      static_cast<int>(p.slabs), N, scale, reduce, out);
   return hipGetLastError();
 }

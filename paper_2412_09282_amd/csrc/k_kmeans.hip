@@ -1,16 +1,14 @@
 // Lloyd update of a K-means codebook (Sec. 3.1 Eq. 2 of the paper; Alg. 1 KMeansCodebook):
 // every centroid becomes the mean of the vectors encoded to it.
 //
-// Atomic-free and deterministic:
-// 1. the (code, vector) pairs are stably sorted by code with an LSD radix sort (8-bit digits;
-//    one pass for K <= 256, two for K <= 65536).  Per 4096-key tile the digit counts and the
-//    stable ranks come from wave ballots (one leader per digit and batch updates a per-wave LDS
-//    counter -- no atomics), tile offsets from a device-wide exclusive scan;
-// 2. the segment of every code is found by binary search in the sorted codes;
-// 3. each centroid is the fixed-order fp64 reduction of its segment, divided by the count and
-//    rounded once to the codebook's type; an empty segment leaves the centroid untouched.
-// Codes outside [0, K) are dropped in the first pass and belong to no cluster.
-// Codebooks of at most 256 codewords take a sort-free path (see small_k_partial).
+// Atomic-free and deterministic.  Every centroid is a fixed-order fp64 sum of its members, divided
+// by their count and rounded once to the codebook's type; a codeword without members is left
+// untouched; codes outside [0, K) belong to no cluster.
+// * K <= 256 (small_k_partial): blocks walk contiguous vector ranges; each round of 1024 codes is
+//   bucket-sorted in LDS and thread k adds the members of code k.
+// * K > 256 (bucket_partial): one stable radix pass (per-tile ballot counting, device-wide scan,
+//   stable scatter -- no atomics) groups the vectors by the high byte of their code; each bucket is
+//   then reduced like a small codebook on the low byte.
 #include "crvq_internal.h"
 
 namespace crvq {
@@ -66,6 +64,23 @@ __device__ __forceinline__ int read_count(const int* n_dev, int64_t n_host) {
   return n_dev ? *n_dev : static_cast<int>(n_host);
 }
 
+// ---- device-wide exclusive scan of int32 ---------------------------------------------------------
+__device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) {
+  const int tid = threadIdx.x;
+  sh[tid] = v;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    int t = (tid >= off) ? sh[tid - off] : 0;
+    __syncthreads();
+    sh[tid] += t;
+    __syncthreads();
+  }
+  total = sh[255];
+  const int excl = sh[tid] - v;
+  __syncthreads();
+  return excl;
+}
+
 // Per-tile digit counts, hist[digit * n_tiles + tile].
 __global__ __launch_bounds__(256) void radix_hist(const int* __restrict__ keys, const int* __restrict__ n_dev,
                                                   int64_t n_host, int64_t K, int pass, int shift, int64_t n_tiles,
@@ -88,12 +103,19 @@ __global__ __launch_bounds__(256) void radix_hist(const int* __restrict__ keys, 
   hist[static_cast<int64_t>(tid) * n_tiles + blockIdx.x] = wh[0][tid] + wh[1][tid] + wh[2][tid] + wh[3][tid];
 }
 
-// Stable scatter: rank = (earlier waves of the tile) + (earlier batches of this wave) + (lower lanes).
+// Stable scatter.  The tile is first ranked into LDS by digit -- rank = (earlier waves of the tile)
+// + (earlier batches of this wave) + (lower lanes) -- and then copied out in LDS order, so every
+// digit's run of the tile is written to consecutive global positions.
 __global__ __launch_bounds__(256) void radix_scatter(const int* __restrict__ keys_in, const int* __restrict__ vals_in,
                                                      const int* __restrict__ n_dev, int64_t n_host, int64_t K, int pass,
                                                      int shift, int64_t n_tiles, const int* __restrict__ offsets,
                                                      int* __restrict__ keys_out, int* __restrict__ vals_out) {
   __shared__ int wh[4][256];
+  __shared__ int dstart[257];
+  __shared__ int gstart[256];
+  __shared__ int sh[256];
+  __shared__ int lkey[kTile];
+  __shared__ int lval[kTile];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   for (int b = tid; b < 1024; b += 256) (&wh[0][0])[b] = 0;
   __syncthreads();
@@ -112,10 +134,15 @@ __global__ __launch_bounds__(256) void radix_scatter(const int* __restrict__ key
     if (valid && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) wh[w][dig[bt]] += __popcll(peer[bt]);
   }
   __syncthreads();
-  // running start of every (wave, digit): tile offset + counts of the earlier waves
   {
     const int d = tid;
-    int run = offsets[static_cast<int64_t>(d) * n_tiles + blockIdx.x];
+    const int tot = wh[0][d] + wh[1][d] + wh[2][d] + wh[3][d];
+    int total;
+    const int ds = block_exclusive_scan(tot, sh, total);
+    dstart[d] = ds;
+    if (d == 255) dstart[256] = total;
+    gstart[d] = offsets[static_cast<int64_t>(d) * n_tiles + blockIdx.x];
+    int run = ds;
     for (int ww = 0; ww < 4; ++ww) {
       const int c = wh[ww][d];
       wh[ww][d] = run;
@@ -129,31 +156,25 @@ __global__ __launch_bounds__(256) void radix_scatter(const int* __restrict__ key
     const int64_t idx = base + bt * 64 + lane;
     if (dig[bt] >= 0) {
       const int pos = wh[w][dig[bt]] + __popcll(peer[bt] & lt);
-      if (pos >= 0 && pos < n) {  // always true for consistent counts; keeps every store in bounds
-        keys_out[pos] = key[bt];
-        vals_out[pos] = vals_in ? vals_in[idx] : static_cast<int>(idx);
+      if (pos >= 0 && pos < kTile) {
+        lkey[pos] = key[bt];
+        lval[pos] = vals_in ? vals_in[idx] : static_cast<int>(idx);
       }
     }
     // every leader has read its digit's start above; now advance it
     if (dig[bt] >= 0 && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) wh[w][dig[bt]] += __popcll(peer[bt]);
   }
-}
-
-// ---- device-wide exclusive scan of int32 ---------------------------------------------------------
-__device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int& total) {
-  const int tid = threadIdx.x;
-  sh[tid] = v;
   __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    int t = (tid >= off) ? sh[tid - off] : 0;
-    __syncthreads();
-    sh[tid] += t;
-    __syncthreads();
+  const int T = dstart[256];
+  for (int e = tid; e < T; e += 256) {
+    const int k = lkey[e];
+    const int dg = (k >> shift) & 255;
+    const int pos = gstart[dg] + (e - dstart[dg]);
+    if (pos >= 0 && pos < n) {  // always true for consistent counts; keeps every store in bounds
+      keys_out[pos] = k;
+      vals_out[pos] = lval[e];
+    }
   }
-  total = sh[255];
-  const int excl = sh[tid] - v;
-  __syncthreads();
-  return excl;
 }
 
 __global__ __launch_bounds__(256) void scan_block_sums(const int* __restrict__ in, int64_t n, int* __restrict__ sums) {
@@ -199,22 +220,6 @@ __global__ __launch_bounds__(256) void scan_apply(const int* __restrict__ in, in
   }
 }
 
-// seg[k] = first position whose code is >= k, k = 0..K
-__global__ __launch_bounds__(256) void segment_bounds(const int* __restrict__ sorted_keys, const int* __restrict__ n_dev,
-                                                      int64_t K, int* __restrict__ seg) {
-  const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (k > K) return;
-  int lo = 0, hi = *n_dev;
-  while (lo < hi) {
-    const int mid = lo + ((hi - lo) >> 1);
-    if (sorted_keys[mid] < k)
-      lo = mid + 1;
-    else
-      hi = mid;
-  }
-  seg[k] = lo;
-}
-
 __device__ __forceinline__ void store_centroid(void* C, int ct, int64_t k, int d, int t, double v) {
   if (ct == ET_F32)
     static_cast<float*>(C)[k * d + t] = static_cast<float>(v);
@@ -222,87 +227,108 @@ __device__ __forceinline__ void store_centroid(void* C, int ct, int64_t k, int d
     static_cast<uint16_t*>(C)[k * d + t] = bf16_from_double(v);
 }
 
-// One wave per code: lanes stride the segment, then a fixed xor-butterfly (identical in every lane).
-__global__ __launch_bounds__(256) void segment_mean_wave(RowSrc src, const int* __restrict__ vals,
-                                                         const int* __restrict__ seg, int64_t K, void* C, int ct,
-                                                         int32_t* __restrict__ counts) {
-  const int lane = threadIdx.x & 63;
-  const int64_t k = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
-  if (k >= K) return;
-  const int d = src.d;
-  const int s = seg[k], e = seg[k + 1];
-  if (counts && lane == 0) counts[k] = e - s;
-  if (e == s) return;
-  double acc[16];
-#pragma unroll
-  for (int t = 0; t < 16; ++t) acc[t] = 0.0;
-  for (int p = s + lane; p < e; p += 64) {
-    const int64_t off = row_offset(src, vals[p]);
-#pragma unroll
-    for (int t = 0; t < 16; ++t)
-      if (t < d) acc[t] = acc[t] + row_elem(src, off, t);
-  }
-#pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    if (t < d) {
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) acc[t] = acc[t] + __shfl_xor(acc[t], m);
-    }
-  }
-  const double cnt = static_cast<double>(e - s);
-#pragma unroll
-  for (int t = 0; t < 16; ++t)
-    if (t < d && lane == t) store_centroid(C, ct, k, d, t, acc[t] / cnt);
-}
+// ---- shared by both codebook sizes ---------------------------------------------------------------
+// A "round" is up to kRound (vector, digit) entries; it is stably bucket-sorted by digit (0..255)
+// in LDS with the ballot multisplit (one leader per digit and batch updates a per-wave counter, so
+// no atomics): afterwards s_pos[s_start[c] .. s_start[c + 1]) lists the round's entries of digit c
+// in ascending order.
+constexpr int kRoundBatches = 4;
+constexpr int kRound = 4 * kRoundBatches * 64;  // 1024 entries: 4 waves x 4 batches x 64 lanes
 
-// One block per code for large segments: per-thread strided sums, then a fixed LDS tree.
-__global__ __launch_bounds__(256) void segment_mean_block(RowSrc src, const int* __restrict__ vals,
-                                                          const int* __restrict__ seg, int64_t K, void* C, int ct,
-                                                          int32_t* __restrict__ counts) {
-  __shared__ double sh[256 * 16];
-  const int tid = threadIdx.x;
-  const int64_t k = blockIdx.x;
-  const int d = src.d;
-  const int s = seg[k], e = seg[k + 1];
-  if (counts && tid == 0) counts[k] = e - s;
-  if (e == s) return;  // uniform across the block
-  double acc[16];
-#pragma unroll
-  for (int t = 0; t < 16; ++t) acc[t] = 0.0;
-  for (int p = s + tid; p < e; p += 256) {
-    const int64_t off = row_offset(src, vals[p]);
-#pragma unroll
-    for (int t = 0; t < 16; ++t)
-      if (t < d) acc[t] = acc[t] + row_elem(src, off, t);
-  }
-#pragma unroll
-  for (int t = 0; t < 16; ++t) sh[t * 256 + tid] = acc[t];
+struct RoundLds {
+  int s_pos[kRound];
+  int s_start[257];
+  int wh[4][256];
+  int sh_scan[256];
+};
+
+// dig[bt] = digit of entry (wave, batch bt, lane) or -1 when absent.
+__device__ __forceinline__ void round_bucket_sort(const int (&dig)[kRoundBatches], RoundLds& L) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  for (int q = tid; q < 1024; q += 256) (&L.wh[0][0])[q] = 0;
   __syncthreads();
-  for (int stride = 128; stride >= 1; stride >>= 1) {
-    if (tid < stride) {
+  uint64_t peer[kRoundBatches];
 #pragma unroll
-      for (int t = 0; t < 16; ++t)
-        if (t < d) sh[t * 256 + tid] = sh[t * 256 + tid] + sh[t * 256 + tid + stride];
-    }
+  for (int bt = 0; bt < kRoundBatches; ++bt) {
+    const bool valid = dig[bt] >= 0;
+    peer[bt] = peer_mask(valid, valid ? dig[bt] : 0);
+    if (valid && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) L.wh[w][dig[bt]] += __popcll(peer[bt]);
+  }
+  __syncthreads();
+  const int tot = L.wh[0][tid] + L.wh[1][tid] + L.wh[2][tid] + L.wh[3][tid];
+  L.sh_scan[tid] = tot;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int v = (tid >= off) ? L.sh_scan[tid - off] : 0;
+    __syncthreads();
+    L.sh_scan[tid] += v;
     __syncthreads();
   }
-  if (tid < d) store_centroid(C, ct, k, d, tid, sh[tid * 256] / static_cast<double>(e - s));
+  const int start = L.sh_scan[tid] - tot;
+  L.s_start[tid] = start;
+  if (tid == 255) L.s_start[256] = L.sh_scan[255];
+  int run = start;
+  for (int ww = 0; ww < 4; ++ww) {
+    const int c = L.wh[ww][tid];
+    L.wh[ww][tid] = run;
+    run += c;
+  }
+  __syncthreads();
+  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+#pragma unroll
+  for (int bt = 0; bt < kRoundBatches; ++bt) {
+    if (dig[bt] >= 0) {
+      const int pos = L.wh[w][dig[bt]] + __popcll(peer[bt] & lt);
+      if (pos >= 0 && pos < kRound) L.s_pos[pos] = (w * kRoundBatches + bt) * 64 + lane;
+    }
+    if (dig[bt] >= 0 && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) L.wh[w][dig[bt]] += __popcll(peer[bt]);
+  }
+  __syncthreads();
 }
 
-// ---- small codebooks (K <= 256): one thread per code, no global sort --------------------------
-// Each block walks a contiguous range of vectors in rounds of 2048.  A round's codes are stably
-// bucket-sorted in LDS (the same ballot multisplit as the radix passes, so no atomics), then
-// thread k adds the members of code k in ascending order to its fp64 accumulators.  The per-block
-// partial sums are folded in block order by a second kernel.
-constexpr int kRound = 2048;  // 4 waves x 8 batches x 64 lanes
+// v += vector at element offset off (d <= 16): 16-byte loads for d = 8 / 4 when aligned.
+__device__ __forceinline__ void add_vector(const RowSrc& s, int64_t off, double (&v)[16]) {
+  const int d = s.d;
+  if (s.type == ET_F32) {
+    const float* p = static_cast<const float*>(s.base) + off;
+    if ((d == 8 || d == 4) && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        if (4 * q < d) {
+          const float4 w = reinterpret_cast<const float4*>(p)[q];
+          v[4 * q] = v[4 * q] + w.x;
+          v[4 * q + 1] = v[4 * q + 1] + w.y;
+          v[4 * q + 2] = v[4 * q + 2] + w.z;
+          v[4 * q + 3] = v[4 * q + 3] + w.w;
+        }
+      }
+      return;
+    }
+  } else if (d == 8 && (reinterpret_cast<uintptr_t>(static_cast<const uint16_t*>(s.base) + off) & 15) == 0) {
+    const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(s.base) + off);
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[2 * q] = v[2 * q] + __uint_as_float(u[q] << 16);
+      v[2 * q + 1] = v[2 * q + 1] + __uint_as_float(u[q] & 0xffff0000u);
+    }
+    return;
+  }
+#pragma unroll
+  for (int t = 0; t < 16; ++t)
+    if (t < d) v[t] = v[t] + row_elem(s, off, t);
+}
 
+// ---- small codebooks (K <= 256): one thread per code, no global sort ------------------------------
+// Each block walks a contiguous range of vectors in rounds of kRound.  A round's vectors are staged
+// in LDS with coalesced loads when the set is contiguous and d <= 8; its codes are bucket-sorted and
+// thread k adds the members of code k in ascending order to fp64 accumulators.  The per-block
+// partials (layout [k][t][block]) are folded in block order by one wave per centroid element.
 __global__ __launch_bounds__(256) void small_k_partial(RowSrc src, const int32_t* __restrict__ codes, int64_t K,
-                                                       int64_t per_block, double* __restrict__ part,
-                                                       int* __restrict__ pcount) {
-  __shared__ int s_pos[kRound];
-  __shared__ int s_start[257];
-  __shared__ int wh[4][256];
-  __shared__ int sh_scan[256];
+                                                       int64_t per_block, int staged, int64_t nblocks,
+                                                       double* __restrict__ part, int* __restrict__ pcount) {
+  __shared__ RoundLds L;
+  __shared__ float s_vec[kRound * 8];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int d = src.d;
   const int64_t n = src.n;
@@ -312,87 +338,76 @@ __global__ __launch_bounds__(256) void small_k_partial(RowSrc src, const int32_t
 #pragma unroll
   for (int t = 0; t < 16; ++t) acc[t] = 0.0;
   int cnt = 0;
-  const uint64_t lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
   for (int64_t base = b0; base < b1; base += kRound) {
-    for (int b = tid; b < 1024; b += 256) (&wh[0][0])[b] = 0;
-    __syncthreads();
-    int dig[8];
-    uint64_t peer[8];
+    const int rn = static_cast<int>((b1 - base) < kRound ? (b1 - base) : kRound);
+    if (staged) {  // vectors base .. base + rn are contiguous: one vector per thread and step
+      for (int v = tid; v < rn; v += 256) {
+        double tmp[16];
 #pragma unroll
-    for (int bt = 0; bt < 8; ++bt) {
-      const int64_t idx = base + w * 512 + bt * 64 + lane;
-      const int c = (idx < b1) ? codes[idx] : -1;
-      const bool valid = c >= 0 && c < K;
-      dig[bt] = valid ? c : -1;
-      peer[bt] = peer_mask(valid, valid ? c : 0);
-      if (valid && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) wh[w][c] += __popcll(peer[bt]);
-    }
-    __syncthreads();
-    // bucket starts: exclusive scan over codes of the round's per-code totals
-    const int tot = wh[0][tid] + wh[1][tid] + wh[2][tid] + wh[3][tid];
-    sh_scan[tid] = tot;
-    __syncthreads();
-    for (int off = 1; off < 256; off <<= 1) {
-      const int v = (tid >= off) ? sh_scan[tid - off] : 0;
-      __syncthreads();
-      sh_scan[tid] += v;
-      __syncthreads();
-    }
-    const int start = sh_scan[tid] - tot;
-    s_start[tid] = start;
-    if (tid == 255) s_start[256] = sh_scan[255];
-    int run = start;
-    for (int ww = 0; ww < 4; ++ww) {
-      const int c = wh[ww][tid];
-      wh[ww][tid] = run;
-      run += c;
-    }
-    __syncthreads();
+        for (int t = 0; t < 16; ++t) tmp[t] = 0.0;
+        add_vector(src, (base + v) * d, tmp);
 #pragma unroll
-    for (int bt = 0; bt < 8; ++bt) {
-      if (dig[bt] >= 0) {
-        const int pos = wh[w][dig[bt]] + __popcll(peer[bt] & lt);
-        if (pos >= 0 && pos < kRound) s_pos[pos] = w * 512 + bt * 64 + lane;
+        for (int t = 0; t < 8; ++t)
+          if (t < d) s_vec[v * d + t] = static_cast<float>(tmp[t]);
       }
-      if (dig[bt] >= 0 && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) wh[w][dig[bt]] += __popcll(peer[bt]);
     }
-    __syncthreads();
+    int dig[kRoundBatches];
+#pragma unroll
+    for (int bt = 0; bt < kRoundBatches; ++bt) {
+      const int e = (w * kRoundBatches + bt) * 64 + lane;
+      const int c = (e < rn) ? codes[base + e] : -1;
+      dig[bt] = (c >= 0 && c < K) ? c : -1;
+    }
+    round_bucket_sort(dig, L);  // ends with a barrier, so s_vec is complete too
     if (tid < K) {
-      const int e = s_start[tid + 1];
-      for (int j = s_start[tid]; j < e; ++j) {
-        const int64_t off = row_offset(src, base + s_pos[j]);
+      const int e = L.s_start[tid + 1];
+      for (int j = L.s_start[tid]; j < e; ++j) {
+        const int v = L.s_pos[j];
+        if (staged) {
 #pragma unroll
-        for (int t = 0; t < 16; ++t)
-          if (t < d) acc[t] = acc[t] + row_elem(src, off, t);
+          for (int t = 0; t < 8; ++t)
+            if (t < d) acc[t] = acc[t] + static_cast<double>(s_vec[v * d + t]);
+        } else {
+          add_vector(src, row_offset(src, base + v), acc);
+        }
       }
-      cnt += e - s_start[tid];
+      cnt += e - L.s_start[tid];
     }
     __syncthreads();
   }
   if (tid < K) {
-    double* pp = part + (static_cast<int64_t>(blockIdx.x) * K + tid) * d;
 #pragma unroll
     for (int t = 0; t < 16; ++t)
-      if (t < d) pp[t] = acc[t];
-    pcount[static_cast<int64_t>(blockIdx.x) * K + tid] = cnt;
+      if (t < d) part[(static_cast<int64_t>(tid) * d + t) * nblocks + blockIdx.x] = acc[t];
+    pcount[static_cast<int64_t>(tid) * nblocks + blockIdx.x] = cnt;
   }
 }
 
+// One wave per centroid element: lanes fold blocks lane, lane + 64, ... in order, then a fixed
+// xor butterfly (the same in every lane).
 __global__ __launch_bounds__(256) void small_k_final(const double* __restrict__ part, const int* __restrict__ pcount,
-                                                     int blocks, int64_t K, int d, void* C, int ct,
+                                                     int64_t nblocks, int64_t K, int d, void* C, int ct,
                                                      int32_t* __restrict__ counts) {
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (e >= K * d) return;
   const int64_t k = e / d;
   const int t = static_cast<int>(e - k * d);
   double acc = 0.0;
   int cnt = 0;
-  for (int b = 0; b < blocks; ++b) {
-    acc = acc + part[(static_cast<int64_t>(b) * K + k) * d + t];
-    cnt += pcount[static_cast<int64_t>(b) * K + k];
+  for (int64_t b = lane; b < nblocks; b += 64) {
+    acc = acc + part[e * nblocks + b];
+    cnt += pcount[k * nblocks + b];
   }
-  if (counts && t == 0) counts[k] = cnt;
-  if (cnt > 0) store_centroid(C, ct, k, d, t, acc / static_cast<double>(cnt));
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    acc = acc + __shfl_xor(acc, m);
+    cnt += __shfl_xor(cnt, m);
+  }
+  if (lane == 0) {
+    if (counts && t == 0) counts[k] = cnt;
+    if (cnt > 0) store_centroid(C, ct, k, d, t, acc / static_cast<double>(cnt));
+  }
 }
 
 struct SmallPlan {
@@ -403,35 +418,144 @@ struct SmallPlan {
 SmallPlan small_plan(int64_t n) {
   SmallPlan p;
   const int64_t rounds = cdiv(n > 0 ? n : 1, kRound);
-  p.blocks = rounds < 512 ? rounds : 512;
+  p.blocks = rounds < 2048 ? rounds : 2048;
   p.per_block = cdiv(rounds, p.blocks) * kRound;
   p.blocks = cdiv(n > 0 ? n : 1, p.per_block);
   return p;
 }
 
+// ---- large codebooks (256 < K <= 65536) ----------------------------------------------------------
+// One stable radix pass groups the vectors by the high byte of their code (256 buckets of 256 codes).
+// Every bucket is then cut into chunks of kChunk vectors; a block takes one chunk and runs the
+// small-codebook scheme on the low byte, gathering each member vector with 16-byte loads.  The
+// chunk partials of each code are folded in chunk order.
+constexpr int kChunk = 16384;
+
+// bounds of the 256 high-byte buckets and of their chunk ranges (one block)
+__global__ __launch_bounds__(256) void bucket_bounds(const int* __restrict__ offs, int64_t n_tiles,
+                                                     const int* __restrict__ n_valid, int* __restrict__ bstart,
+                                                     int* __restrict__ cstart) {
+  __shared__ int sh[256];
+  const int b = threadIdx.x;
+  const int s = offs[static_cast<int64_t>(b) * n_tiles];
+  const int e = (b < 255) ? offs[static_cast<int64_t>(b + 1) * n_tiles] : *n_valid;
+  const int chunks = (e - s + kChunk - 1) / kChunk;
+  int total;
+  const int ex = block_exclusive_scan(chunks, sh, total);
+  bstart[b] = s;
+  cstart[b] = ex;
+  if (b == 255) {
+    bstart[256] = e;
+    cstart[256] = total;
+  }
+}
+
+__global__ __launch_bounds__(256) void bucket_partial(RowSrc src, const int* __restrict__ keys,
+                                                      const int* __restrict__ vals, const int* __restrict__ bstart,
+                                                      const int* __restrict__ cstart, double* __restrict__ part,
+                                                      int* __restrict__ pcount) {
+  __shared__ RoundLds L;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int blk = blockIdx.x;
+  if (blk >= cstart[256]) return;  // uniform: more blocks are launched than there can be chunks
+  int lo = 0, hi = 256;            // bucket b with cstart[b] <= blk < cstart[b + 1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (cstart[mid] <= blk)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  const int b = lo;
+  const int64_t b0 = bstart[b] + static_cast<int64_t>(blk - cstart[b]) * kChunk;
+  const int64_t b1 = (b0 + kChunk < bstart[b + 1]) ? b0 + kChunk : bstart[b + 1];
+  const int d = src.d;
+  double acc[16];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) acc[t] = 0.0;
+  int cnt = 0;
+  for (int64_t base = b0; base < b1; base += kRound) {
+    int dig[kRoundBatches];
+#pragma unroll
+    for (int bt = 0; bt < kRoundBatches; ++bt) {
+      const int64_t idx = base + (w * kRoundBatches + bt) * 64 + lane;
+      dig[bt] = (idx < b1) ? (keys[idx] & 255) : -1;
+    }
+    round_bucket_sort(dig, L);
+    const int e = L.s_start[tid + 1];
+    int j = L.s_start[tid];
+    for (; j + 1 < e; j += 2) {  // two members' loads in flight, added in ascending order
+      double v0[16], v1[16];
+#pragma unroll
+      for (int t = 0; t < 16; ++t) {
+        v0[t] = 0.0;
+        v1[t] = 0.0;
+      }
+      add_vector(src, row_offset(src, vals[base + L.s_pos[j]]), v0);
+      add_vector(src, row_offset(src, vals[base + L.s_pos[j + 1]]), v1);
+#pragma unroll
+      for (int t = 0; t < 16; ++t)
+        if (t < d) acc[t] = (acc[t] + v0[t]) + v1[t];
+    }
+    if (j < e) add_vector(src, row_offset(src, vals[base + L.s_pos[j]]), acc);
+    cnt += e - L.s_start[tid];
+    __syncthreads();
+  }
+  double* pp = part + (static_cast<int64_t>(blk) * 256 + tid) * d;
+#pragma unroll
+  for (int t = 0; t < 16; ++t)
+    if (t < d) pp[t] = acc[t];
+  pcount[static_cast<int64_t>(blk) * 256 + tid] = cnt;
+}
+
+__global__ __launch_bounds__(256) void bucket_final(const double* __restrict__ part, const int* __restrict__ pcount,
+                                                    const int* __restrict__ cstart, int64_t K, int d, void* C, int ct,
+                                                    int32_t* __restrict__ counts) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= K * d) return;
+  const int64_t k = e / d;
+  const int t = static_cast<int>(e - k * d);
+  const int b = static_cast<int>(k >> 8), low = static_cast<int>(k & 255);
+  double acc = 0.0;
+  int cnt = 0;
+  for (int blk = cstart[b]; blk < cstart[b + 1]; ++blk) {
+    acc = acc + part[(static_cast<int64_t>(blk) * 256 + low) * d + t];
+    cnt += pcount[static_cast<int64_t>(blk) * 256 + low];
+  }
+  if (counts && t == 0) counts[k] = cnt;
+  if (cnt > 0) store_centroid(C, ct, k, d, t, acc / static_cast<double>(cnt));
+}
+
 struct KmWs {
-  int* keys[2];
-  int* vals[2];
+  int* keys;
+  int* vals;
   int* hist;
   int* offs;
   int* sums;
   int* n_valid;
-  int* seg;
+  int* bstart;
+  int* cstart;
+  double* part;
+  int* pcount;
+  int64_t max_chunks;
 };
 
 KmWs carve(WsCursor& ws, int64_t n, int64_t K) {
+  (void)K;
   KmWs w;
   const int64_t n_tiles = cdiv(n > 0 ? n : 1, kTile);
   const int64_t hn = 256 * n_tiles;
-  for (int b = 0; b < 2; ++b) {
-    w.keys[b] = ws.take<int>(static_cast<size_t>(n));
-    w.vals[b] = ws.take<int>(static_cast<size_t>(n));
-  }
+  w.keys = ws.take<int>(static_cast<size_t>(n));
+  w.vals = ws.take<int>(static_cast<size_t>(n));
   w.hist = ws.take<int>(static_cast<size_t>(hn));
   w.offs = ws.take<int>(static_cast<size_t>(hn));
   w.sums = ws.take<int>(static_cast<size_t>(cdiv(hn, kScanBlock)));
   w.n_valid = ws.take<int>(1);
-  w.seg = ws.take<int>(static_cast<size_t>(K + 1));
+  w.bstart = ws.take<int>(257);
+  w.cstart = ws.take<int>(257);
+  w.max_chunks = cdiv(n, kChunk) + 256;  // every bucket adds at most one partial chunk
+  w.part = ws.take<double>(static_cast<size_t>(w.max_chunks) * 256 * 16);
+  w.pcount = ws.take<int>(static_cast<size_t>(w.max_chunks) * 256);
   return w;
 }
 
@@ -465,38 +589,26 @@ hipError_t launch_kmeans_update(const RowSrc& src, const int32_t* codes, int64_t
     SmallPlan p = small_plan(n);
     double* part = cur.take<double>(static_cast<size_t>(p.blocks * K * 16));
     int* pcount = cur.take<int>(static_cast<size_t>(p.blocks * K));
+    const int staged = (src.ld == src.vpr * src.d) && src.d <= 8;
     hipLaunchKernelGGL(small_k_partial, dim3(static_cast<unsigned>(p.blocks)), dim3(256), 0, stream, src, codes, K,
-                       p.per_block, part, pcount);
-    hipLaunchKernelGGL(small_k_final, dim3(static_cast<unsigned>(cdiv(K * src.d, 256))), dim3(256), 0, stream, part,
-                       pcount, static_cast<int>(p.blocks), K, src.d, C, c_type, counts);
+                       p.per_block, staged, p.blocks, part, pcount);
+    hipLaunchKernelGGL(small_k_final, dim3(static_cast<unsigned>(cdiv(K * src.d, 4))), dim3(256), 0, stream, part,
+                       pcount, p.blocks, K, src.d, C, c_type, counts);
     return hipGetLastError();
   }
   KmWs w = carve(cur, n, K);
   const int64_t n_tiles = cdiv(n > 0 ? n : 1, kTile);
-  const int passes = (K <= 256) ? 1 : 2;
-  const int* kin = codes;
-  const int* vin = nullptr;
   hipError_t e;
-  for (int p = 0; p < passes; ++p) {
-    const int* ndev = (p == 0) ? nullptr : w.n_valid;
-    hipLaunchKernelGGL(radix_hist, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, kin, ndev, n, K, p, 8 * p,
-                       n_tiles, w.hist);
-    if ((e = exclusive_scan(w.hist, 256 * n_tiles, w.sums, w.offs, p == 0 ? w.n_valid : nullptr, stream)) != hipSuccess)
-      return e;
-    hipLaunchKernelGGL(radix_scatter, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, kin, vin, ndev, n, K, p,
-                       8 * p, n_tiles, w.offs, w.keys[p & 1], w.vals[p & 1]);
-    kin = w.keys[p & 1];
-    vin = w.vals[p & 1];
-  }
-  hipLaunchKernelGGL(segment_bounds, dim3(static_cast<unsigned>(cdiv(K + 1, 256))), dim3(256), 0, stream, kin,
-                     w.n_valid, K, w.seg);
-  if (n >= 256 * K) {
-    hipLaunchKernelGGL(segment_mean_block, dim3(static_cast<unsigned>(K)), dim3(256), 0, stream, src, vin, w.seg, K, C,
-                       c_type, counts);
-  } else {
-    hipLaunchKernelGGL(segment_mean_wave, dim3(static_cast<unsigned>(cdiv(K, 4))), dim3(256), 0, stream, src, vin, w.seg,
-                       K, C, c_type, counts);
-  }
+  hipLaunchKernelGGL(radix_hist, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, codes, nullptr, n, K, 0, 8,
+                     n_tiles, w.hist);
+  if ((e = exclusive_scan(w.hist, 256 * n_tiles, w.sums, w.offs, w.n_valid, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(radix_scatter, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, codes, nullptr, nullptr,
+                     n, K, 0, 8, n_tiles, w.offs, w.keys, w.vals);
+  hipLaunchKernelGGL(bucket_bounds, dim3(1), dim3(256), 0, stream, w.offs, n_tiles, w.n_valid, w.bstart, w.cstart);
+  hipLaunchKernelGGL(bucket_partial, dim3(static_cast<unsigned>(w.max_chunks)), dim3(256), 0, stream, src, w.keys,
+                     w.vals, w.bstart, w.cstart, w.part, w.pcount);
+  hipLaunchKernelGGL(bucket_final, dim3(static_cast<unsigned>(cdiv(K * src.d, 256))), dim3(256), 0, stream, w.part,
+                     w.pcount, w.cstart, K, src.d, C, c_type, counts);
   return hipGetLastError();
 }
 

@@ -80,6 +80,41 @@ __global__ __launch_bounds__(256) void gather_cols_lds(const T* __restrict__ in,
   }
 }
 
+// Same with 16-byte row segments (V = 16 / sizeof(T) elements): rows are read and written as uint4,
+// sources as int4.  Needs N % V == 0 and 16-byte aligned row starts (checked by the launcher).
+template <typename T>
+__global__ __launch_bounds__(256) void gather_cols_lds_v(const T* __restrict__ in, int64_t ld_in, T* __restrict__ out,
+                                                         int64_t ld_out, int64_t N, const int32_t* __restrict__ src) {
+  constexpr int V = 16 / sizeof(T);
+  extern __shared__ unsigned char smem[];
+  T* row = reinterpret_cast<T*>(smem);
+  const int64_t r = blockIdx.x;
+  const uint4* ri = reinterpret_cast<const uint4*>(in + r * ld_in);
+  const int64_t nv = N / V;
+  constexpr int U = 4;  // segments in flight per thread
+  for (int64_t c0 = threadIdx.x; c0 < nv; c0 += 256 * U) {
+    uint4 v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = (c0 + u * 256 < nv) ? ri[c0 + u * 256] : make_uint4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (c0 + u * 256 < nv) reinterpret_cast<uint4*>(row)[c0 + u * 256] = v[u];
+  }
+  __syncthreads();
+  uint4* ro = reinterpret_cast<uint4*>(out + r * ld_out);
+  for (int64_t c = threadIdx.x; c < nv; c += 256) {
+    T seg[V];
+#pragma unroll
+    for (int q = 0; q < V; q += 4) {
+      const int4 s4 = reinterpret_cast<const int4*>(src)[(c * V + q) / 4];
+      const int32_t s[4] = {s4.x, s4.y, s4.z, s4.w};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) seg[q + u] = (s[u] >= 0 && s[u] < N) ? row[s[u]] : T(0);
+    }
+    ro[c] = *reinterpret_cast<const uint4*>(seg);
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void gather_cols_direct(const T* __restrict__ in, int64_t ld_in, T* __restrict__ out,
                                                           int64_t ld_out, int64_t M, int64_t N,
@@ -148,7 +183,18 @@ hipError_t launch_gather_columns(const void* in, int64_t ld_in, void* out, int64
                                  int64_t N, const int32_t* src_idx, hipStream_t stream) {
   if (M <= 0 || N <= 0) return hipSuccess;
   const size_t lds = static_cast<size_t>(N) * esize;
-  if (lds <= 64 * 1024) {
+  const int V = 16 / esize;
+  const bool vec_ok = (N % V == 0) && ((ld_in * esize) % 16 == 0) && ((ld_out * esize) % 16 == 0) &&
+                      (reinterpret_cast<uintptr_t>(in) % 16 == 0) && (reinterpret_cast<uintptr_t>(out) % 16 == 0) &&
+                      (reinterpret_cast<uintptr_t>(src_idx) % 16 == 0);
+  if (lds <= 64 * 1024 && vec_ok) {
+    if (esize == 4)
+      hipLaunchKernelGGL(gather_cols_lds_v<uint32_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream,
+                         static_cast<const uint32_t*>(in), ld_in, static_cast<uint32_t*>(out), ld_out, N, src_idx);
+    else
+      hipLaunchKernelGGL(gather_cols_lds_v<uint16_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream,
+                         static_cast<const uint16_t*>(in), ld_in, static_cast<uint16_t*>(out), ld_out, N, src_idx);
+  } else if (lds <= 64 * 1024) {
     if (esize == 4)
       hipLaunchKernelGGL(gather_cols_lds<uint32_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream,
                          static_cast<const uint32_t*>(in), ld_in, static_cast<uint32_t*>(out), ld_out, N, src_idx);

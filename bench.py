@@ -73,6 +73,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run one plain 1 GiB device-to-device copy (reference kernel for memory counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
@@ -105,6 +107,15 @@ def main():
     cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
     q = LayerQuantizer(M, N, torch.float32, cfg, L.tokens, device=dev)
     torch.cuda.synchronize()
+
+    if args.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        log("calibration copy of 1 GiB done")
 
     for i in range(args.warmup):
         q.run(Wd, Xd, bi, ei)
@@ -169,7 +180,7 @@ def main():
         tc = time.perf_counter()
         oracle.assign(Vs[probe], Cb)
         rate = 64 / max(time.perf_counter() - tc, 1e-6)
-        k = int(min(65536, max(256, rate * args.cpu_seconds)))
+        k = int(min(1 << 20, max(256, rate * args.cpu_seconds)))
         idx = inputs.sample_rows(wl, 0, n, k)
         tc = time.perf_counter()
         oc, _ = oracle.assign(Vs[idx], Cb)

@@ -24,6 +24,12 @@
 #ifndef CRVQ_MIN_TRACKED_TILES
 #define CRVQ_MIN_TRACKED_TILES 1
 #endif
+#ifndef CRVQ_SCREEN_PREFETCH
+#define CRVQ_SCREEN_PREFETCH 1
+#endif
+#ifndef CRVQ_CB_WIDE
+#define CRVQ_CB_WIDE 8  // column blocks per wave for top-1/top-2 screens on large row counts
+#endif
 
 namespace crvq {
 namespace {
@@ -280,15 +286,26 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
   const int64_t t0 = static_cast<int64_t>(split) * tps;
   const int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
   if (t0 < t1) {
-    AVec<KS> a_nx;
-    a_nx.load(apack + (t0 * 64 + lane) * KS);
-    f4 c_nx = *reinterpret_cast<const f4*>(cnp + t0 * 16 + 4 * g);
+    // codebook tiles are loaded CRVQ_SCREEN_PREFETCH iterations ahead (clamped to the last tile)
+    AVec<KS> a_q[CRVQ_SCREEN_PREFETCH];
+    f4 c_q[CRVQ_SCREEN_PREFETCH];
+#pragma unroll
+    for (int u = 0; u < CRVQ_SCREEN_PREFETCH; ++u) {
+      const int64_t Tu = (t0 + u < t1) ? t0 + u : t1 - 1;
+      a_q[u].load(apack + (Tu * 64 + lane) * KS);
+      c_q[u] = *reinterpret_cast<const f4*>(cnp + Tu * 16 + 4 * g);
+    }
     for (int64_t T = t0; T < t1; ++T) {
-      const AVec<KS> a = a_nx;
-      const f4 c4 = c_nx;
-      const int64_t Tn = (T + 1 < t1) ? T + 1 : T;
-      a_nx.load(apack + (Tn * 64 + lane) * KS);
-      c_nx = *reinterpret_cast<const f4*>(cnp + Tn * 16 + 4 * g);
+      const AVec<KS> a = a_q[0];
+      const f4 c4 = c_q[0];
+#pragma unroll
+      for (int u = 0; u + 1 < CRVQ_SCREEN_PREFETCH; ++u) {
+        a_q[u] = a_q[u + 1];
+        c_q[u] = c_q[u + 1];
+      }
+      const int64_t Tn = (T + CRVQ_SCREEN_PREFETCH < t1) ? T + CRVQ_SCREEN_PREFETCH : t1 - 1;
+      a_q[CRVQ_SCREEN_PREFETCH - 1].load(apack + (Tn * 64 + lane) * KS);
+      c_q[CRVQ_SCREEN_PREFETCH - 1] = *reinterpret_cast<const f4*>(cnp + Tn * 16 + 4 * g);
       const int Ti = static_cast<int>(T);
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) {
@@ -676,9 +693,9 @@ template <int KS>
 hipError_t launch_screen_ks(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
                             const ScreenWs& w, hipStream_t stream) {
   switch (p.nb) {
-    case 1: return p.cb == 8 ? launch_screen_t<KS, 1, 8>(src, C, ct, K, p, w, stream)
+    case 1: return p.cb == CRVQ_CB_WIDE ? launch_screen_t<KS, 1, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
                              : launch_screen_t<KS, 1, 2>(src, C, ct, K, p, w, stream);
-    case 2: return p.cb == 8 ? launch_screen_t<KS, 2, 8>(src, C, ct, K, p, w, stream)
+    case 2: return p.cb == CRVQ_CB_WIDE ? launch_screen_t<KS, 2, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
                              : launch_screen_t<KS, 2, 2>(src, C, ct, K, p, w, stream);
     case 4: return launch_screen_t<KS, 4, 4>(src, C, ct, K, p, w, stream);
     case 8: return launch_screen_t<KS, 8, 2>(src, C, ct, K, p, w, stream);
@@ -723,7 +740,7 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   // CRVQ_MIN_TRACKED_TILES = 2 would make the exact rescue almost never needed, but its extra VALU
   // work and registers cost more screen time (12 % at K = 65536) than the rescues it saves.
   p.nb = next_pow2_nb(top < CRVQ_MIN_TRACKED_TILES ? CRVQ_MIN_TRACKED_TILES : top);
-  p.cb = p.nb <= 2 ? 8 : (p.nb == 4 ? 4 : (p.nb == 8 ? 2 : 1));
+  p.cb = p.nb <= 2 ? CRVQ_CB_WIDE : (p.nb == 4 ? 4 : (p.nb == 8 ? 2 : 1));
   p.ks = d <= 4 ? 1 : (d <= 8 ? 2 : 4);
   p.tiles = cdiv(K, 16);
   p.grid_x = cdiv(n_rows, 64 * p.cb);

@@ -50,7 +50,9 @@ struct RowSrc {
 struct ScreenPlan {
   int nb;            // best tiles tracked per lane (power of two >= requested top count)
   int cb;            // 16-row column blocks per wave
-  int ks;            // 4-wide K steps of the fp32 MFMA (ceil(d / 4))
+  int ks;            // 4-wide K steps of the fp32 MFMA (ceil(d / 4)); 2 (8 dimensions) when split
+  int split;         // 1: split-bf16 MFMA screen (d <= 8), 0: fp32 MFMA screen
+  int chunk;         // top-1: tiles per tracking chunk (1 = single tiles)
   int64_t tiles;     // 16-codeword tiles (ceil(K / 16))
   int64_t grid_x;    // row groups
   int splits;        // codebook splits (grid y)

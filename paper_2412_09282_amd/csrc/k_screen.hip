@@ -30,6 +30,15 @@
 #ifndef CRVQ_CB_WIDE
 #define CRVQ_CB_WIDE 8  // column blocks per wave for top-1/top-2 screens on large row counts
 #endif
+#ifndef CRVQ_SPLIT_SCREEN
+#define CRVQ_SPLIT_SCREEN 1  // split-bf16 MFMA screen for d <= 8 (0: fp32 MFMA for every d)
+#endif
+#ifndef CRVQ_CHUNK
+#define CRVQ_CHUNK 8  // tiles per tracking chunk of the top-1 screen on long tile ranges
+#endif
+#ifndef CRVQ_CHUNK_MIN_TILES
+#define CRVQ_CHUNK_MIN_TILES 128  // shorter tile ranges track single tiles (cheaper exact epilogue)
+#endif
 
 namespace crvq {
 namespace {
@@ -238,11 +247,143 @@ struct AVec<4> {
   }
 };
 
+// fp32 to bf16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t bf16_rn_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Two-term bf16 split of v: hi = bf16(v), lo = bf16(v - hi) (v - hi is exact in fp32), so that
+// |v - hi - lo| <= 2^-16 |v|.
+__device__ __forceinline__ void bf16_split(float v, uint16_t& hi, uint16_t& lo) {
+  hi = bf16_rn_bits(v);
+  lo = bf16_rn_bits(v - __uint_as_float(static_cast<uint32_t>(hi) << 16));
+}
+
+// Screen operand policies.  Each gives the per-lane A (codebook tile) and B (-2x of the wave's rows)
+// operands of one 16 x 16 tile of s values and the MFMA sequence that accumulates them onto ||c||^2.
+// Both leave lane l the values of codewords 4 (l / 16) + r, r = 0..3, for row l % 16.
+//
+// F32Ops: ceil(d / 4) v_mfma_f32_16x16x4_f32 steps; lane l holds dimension 4 s + l / 16 of
+//   codeword l % 16 (A) and of row l % 16 (B).
+template <int KS>
+struct F32Ops {
+  static constexpr int DM = 4 * KS;
+  struct A {
+    AVec<KS> a;
+  };
+  struct B {
+    float v[KS];
+  };
+  __device__ static __forceinline__ A load_a(const void* apack, int64_t T, int lane) {
+    A r;
+    r.a.load(static_cast<const float*>(apack) + (T * 64 + lane) * KS);
+    return r;
+  }
+  __device__ static __forceinline__ B make_b(const RowSrc& src, int64_t i, bool ok, int g) {
+    B b;
+    const int64_t off = ok ? row_offset(src, i) : 0;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const int t = 4 * s + g;
+      b.v[s] = (ok && t < src.d) ? -2.0f * static_cast<float>(row_elem(src, off, t)) : 0.0f;
+    }
+    return b;
+  }
+  __device__ static __forceinline__ f4 mfma(const A& a, const B& b, f4 c) {
+    f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.v[0], b.v[0], c, 0, 0, 0);
+#pragma unroll
+    for (int s = 1; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.a.v[s], b.v[s], acc, 0, 0, 0);
+    return acc;
+  }
+};
+
+// SplitOps (d <= 8): one v_mfma_f32_16x16x32_bf16 per tile.  Codewords and -2x are split into two
+// bf16 terms (c = c1 + c2 + e_c, -2x = x1 + x2 + e_x, |e| <= 2^-16 |.|) and the four 8-element groups
+// of the 32-long contraction hold c1.x1, c1.x2, c2.x1 and c2.x2: lane group g carries c1 (g < 2) or
+// c2 (g >= 2) of codeword l % 16 and x1 (g even) or x2 (g odd) of row l % 16.  bf16 products are
+// exact in fp32, so s is off by at most the split remainder 2^-15 sum_t |c_t| |2 x_t| plus the
+// accumulation roundings; both enter the certification bound.  For bf16 rows and codebooks the split
+// is exact (c2 = x2 = 0).
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+
+struct SplitOps {
+  static constexpr int DM = 8;
+  struct A {
+    bf8 v;
+  };
+  struct B {
+    bf8 v;
+  };
+  // codeword k of the packed book: 8 bf16 of c1, then 8 of c2 (32 bytes)
+  __device__ static __forceinline__ A load_a(const void* apack, int64_t T, int lane) {
+    A r;
+    r.v = *reinterpret_cast<const bf8*>(static_cast<const uint16_t*>(apack) + (T * 16 + (lane & 15)) * 16 +
+                                        (lane >> 5) * 8);
+    return r;
+  }
+  __device__ static __forceinline__ B make_b(const RowSrc& src, int64_t i, bool ok, int g) {
+    float v[8];
+    if (src.type == ET_F64) {
+      const int64_t off = ok ? row_offset(src, i) : 0;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (ok && t < src.d) ? static_cast<float>(row_elem(src, off, t)) : 0.0f;
+    } else {
+      const int64_t off = ok ? row_offset(src, i) : 0;
+      if (src.type == ET_F32)
+        load_f32_elems<8>(static_cast<const float*>(src.base) + off, src.d, ok, v);
+      else
+        load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, src.d, ok, v);
+    }
+    u16x8 h;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      uint16_t hi, lo;
+      bf16_split(-2.0f * v[t], hi, lo);
+      h[t] = (g & 1) ? lo : hi;
+    }
+    B b;
+    b.v = __builtin_bit_cast(bf8, h);
+    return b;
+  }
+  __device__ static __forceinline__ f4 mfma(const A& a, const B& b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a.v, b.v, c, 0, 0, 0);
+  }
+};
+
+// Split-bf16 codebook pack: per codeword 8 bf16 of c1 then 8 of c2 (zero past d), and ||c||^2.
+__global__ __launch_bounds__(256) void prep_codebook_split(const void* __restrict__ C, int ct, int64_t K, int d,
+                                                           int64_t tiles, uint16_t* __restrict__ apack,
+                                                           float* __restrict__ cnp) {
+  const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (k >= tiles * 16) return;
+  float c[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) c[t] = (k < K && t < d) ? static_cast<float>(cb_elem(C, ct, k, d, t)) : 0.0f;
+  float cn = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) cn = cn + c[t] * c[t];
+  cnp[k] = (k < K) ? cn : __builtin_inff();
+  u16x8 hi, lo;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    uint16_t h, l;
+    bf16_split(c[t], h, l);
+    hi[t] = h;
+    lo[t] = l;
+  }
+  u16x8* dst = reinterpret_cast<u16x8*>(apack + k * 16);
+  dst[0] = hi;
+  dst[1] = lo;
+}
+
 // ------------------------------------------------------------------------------------------------
 // 2 + 3. MFMA screen with fused top-tile tracking, then exact re-scoring of the kept tiles
 // ------------------------------------------------------------------------------------------------
-template <int KS, int NB, int CB>
-__global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __restrict__ apack,
+template <class OPS, int NB, int CB, int NC>
+__global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __restrict__ apack,
                                                      const float* __restrict__ cnp, int64_t tiles, int64_t tps,
                                                      const void* __restrict__ C, int ct, int64_t K,
                                                      int* __restrict__ pT, float* __restrict__ pR,
@@ -258,16 +399,11 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
   const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (16 * CB);
   if (row0 >= n) return;  // no barriers below: a wave past the end simply leaves
 
-  float bop[CB][KS];
+  typename OPS::B bop[CB];
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const int64_t i = row0 + cb * 16 + jl;
-    const int64_t off = (i < n) ? row_offset(src, i) : 0;
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int t = 4 * s + g;
-      bop[cb][s] = (i < n && t < d) ? -2.0f * static_cast<float>(row_elem(src, off, t)) : 0.0f;
-    }
+    bop[cb] = OPS::make_b(src, i, i < n, g);
   }
 
   float m[CB][NB];
@@ -287,71 +423,112 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
   const int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
   if (t0 < t1) {
     // codebook tiles are loaded CRVQ_SCREEN_PREFETCH iterations ahead (clamped to the last tile)
-    AVec<KS> a_q[CRVQ_SCREEN_PREFETCH];
+    typename OPS::A a_q[CRVQ_SCREEN_PREFETCH];
     f4 c_q[CRVQ_SCREEN_PREFETCH];
 #pragma unroll
     for (int u = 0; u < CRVQ_SCREEN_PREFETCH; ++u) {
       const int64_t Tu = (t0 + u < t1) ? t0 + u : t1 - 1;
-      a_q[u].load(apack + (Tu * 64 + lane) * KS);
+      a_q[u] = OPS::load_a(apack, Tu, lane);
       c_q[u] = *reinterpret_cast<const f4*>(cnp + Tu * 16 + 4 * g);
     }
-    for (int64_t T = t0; T < t1; ++T) {
-      const AVec<KS> a = a_q[0];
-      const f4 c4 = c_q[0];
+    // hands out tile T's operands and issues the load of tile T + CRVQ_SCREEN_PREFETCH
+    auto advance = [&](int64_t T, typename OPS::A& a, f4& c4) {
+      a = a_q[0];
+      c4 = c_q[0];
 #pragma unroll
       for (int u = 0; u + 1 < CRVQ_SCREEN_PREFETCH; ++u) {
         a_q[u] = a_q[u + 1];
         c_q[u] = c_q[u + 1];
       }
       const int64_t Tn = (T + CRVQ_SCREEN_PREFETCH < t1) ? T + CRVQ_SCREEN_PREFETCH : t1 - 1;
-      a_q[CRVQ_SCREEN_PREFETCH - 1].load(apack + (Tn * 64 + lane) * KS);
+      a_q[CRVQ_SCREEN_PREFETCH - 1] = OPS::load_a(apack, Tn, lane);
       c_q[CRVQ_SCREEN_PREFETCH - 1] = *reinterpret_cast<const f4*>(cnp + Tn * 16 + 4 * g);
-      const int Ti = static_cast<int>(T);
+    };
+    if constexpr (NB == 1) {
+      // Top-1: tiles are taken in chunks of NC.  Inside a chunk every value only folds into the
+      // chunk minimum (two v_min3 per tile and row); the kept-chunk and "rest" bookkeeping runs once
+      // per chunk.  Full chunks run unguarded; a shorter last chunk tile by tile.
+      float cm[CB];
+      auto tile = [&](int64_t T) {
+        typename OPS::A a;
+        f4 c4;
+        advance(T, a, c4);
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) {
-        f4 acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[0], bop[cb][0], c4, 0, 0, 0);
+        for (int cb = 0; cb < CB; ++cb) {
+          const f4 acc = OPS::mfma(a, bop[cb], c4);
+          cm[cb] = fminf(fminf(cm[cb], acc[0]), acc[1]);
+          cm[cb] = fminf(fminf(cm[cb], acc[2]), acc[3]);
+        }
+      };
+      auto fold = [&](int64_t T0) {
+        const int Ci = static_cast<int>(T0);
 #pragma unroll
-        for (int s = 1; s < KS; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v[s], bop[cb][s], acc, 0, 0, 0);
-        float x = fminf(fminf(acc[0], acc[1]), fminf(acc[2], acc[3]));
-        if constexpr (NB == 1) {
-          rest[cb] = __builtin_amdgcn_fmed3f(m[cb][0], rest[cb], x);
-          const bool lt = x < m[cb][0];
-          m[cb][0] = fminf(m[cb][0], x);
-          id[cb][0] = lt ? Ti : id[cb][0];
-        } else if constexpr (NB == 2) {
-          // m0 <= m1 <= rest is kept sorted with medians: 10 VALU ops per tile and row
-          const bool lt0 = x < m[cb][0];
-          const bool lt1 = x < m[cb][1];
-          rest[cb] = __builtin_amdgcn_fmed3f(m[cb][1], rest[cb], x);
-          m[cb][1] = __builtin_amdgcn_fmed3f(m[cb][0], m[cb][1], x);
-          m[cb][0] = fminf(m[cb][0], x);
-          id[cb][1] = lt0 ? id[cb][0] : (lt1 ? Ti : id[cb][1]);
-          id[cb][0] = lt0 ? Ti : id[cb][0];
-        } else {
-          int xi = Ti;
+        for (int cb = 0; cb < CB; ++cb) {
+          rest[cb] = __builtin_amdgcn_fmed3f(m[cb][0], rest[cb], cm[cb]);
+          const bool lt = cm[cb] < m[cb][0];
+          m[cb][0] = fminf(m[cb][0], cm[cb]);
+          id[cb][0] = lt ? Ci : id[cb][0];
+          cm[cb] = __builtin_inff();
+        }
+      };
 #pragma unroll
-          for (int j = 0; j < NB; ++j) {
-            const bool lt = x < m[cb][j];
-            const float nv = fminf(x, m[cb][j]);
-            const float cv = fmaxf(x, m[cb][j]);
-            const int ni = lt ? xi : id[cb][j];
-            xi = lt ? id[cb][j] : xi;
-            m[cb][j] = nv;
-            id[cb][j] = ni;
-            x = cv;
+      for (int cb = 0; cb < CB; ++cb) cm[cb] = __builtin_inff();
+      int64_t T0 = t0;
+      for (; T0 + NC <= t1; T0 += NC) {
+#pragma unroll
+        for (int u = 0; u < NC; ++u) tile(T0 + u);
+        fold(T0);
+      }
+      if (T0 < t1) {
+        for (int64_t T = T0; T < t1; ++T) tile(T);
+        fold(T0);
+      }
+    } else {
+      for (int64_t T = t0; T < t1; ++T) {
+        typename OPS::A a;
+        f4 c4;
+        advance(T, a, c4);
+        const int Ti = static_cast<int>(T);
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) {
+          const f4 acc = OPS::mfma(a, bop[cb], c4);
+          float x = fminf(fminf(acc[0], acc[1]), fminf(acc[2], acc[3]));
+          if constexpr (NB == 2) {
+            // m0 <= m1 <= rest is kept sorted with medians: 10 VALU ops per tile and row
+            const bool lt0 = x < m[cb][0];
+            const bool lt1 = x < m[cb][1];
+            rest[cb] = __builtin_amdgcn_fmed3f(m[cb][1], rest[cb], x);
+            m[cb][1] = __builtin_amdgcn_fmed3f(m[cb][0], m[cb][1], x);
+            m[cb][0] = fminf(m[cb][0], x);
+            id[cb][1] = lt0 ? id[cb][0] : (lt1 ? Ti : id[cb][1]);
+            id[cb][0] = lt0 ? Ti : id[cb][0];
+          } else {
+            int xi = Ti;
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+              const bool lt = x < m[cb][j];
+              const float nv = fminf(x, m[cb][j]);
+              const float cv = fmaxf(x, m[cb][j]);
+              const int ni = lt ? xi : id[cb][j];
+              xi = lt ? id[cb][j] : xi;
+              m[cb][j] = nv;
+              id[cb][j] = ni;
+              x = cv;
+            }
+            rest[cb] = fminf(rest[cb], x);
           }
-          rest[cb] = fminf(rest[cb], x);
         }
       }
     }
   }
 
   if constexpr (NB == 1) {
-    // Top-1.  The lane group whose kept tile has the smallest minimum wins the row; the best tiles
-    // of the other three groups join the bound ("rest").  The winner's four codewords are re-scored
-    // exactly, one per lane group, and reduced in (D, k) order.  A row whose true minimum sits in a
-    // losing group simply fails certification later and is re-searched exactly.
-    constexpr int DM = 4 * KS;
+    // Top-1.  The lane group whose kept chunk has the smallest minimum wins the row; the best chunks
+    // of the other three groups join the bound ("rest").  The winner group's codewords of that chunk
+    // (4 per tile) are re-scored exactly, lane group r taking codeword r of every tile, and reduced
+    // in (D, k) order.  A row whose true minimum sits elsewhere fails certification later and is
+    // re-searched exactly.
+    constexpr int DM = OPS::DM;
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
       const int64_t i = row0 + cb * 16 + jl;
@@ -371,24 +548,39 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
       rr = fminf(rr, __shfl_xor(rr, 16));
       rr = fminf(rr, __shfl_xor(rr, 32));
       const int Tw = __shfl(id[cb][0], jl + 16 * gw);
-      const int64_t k = static_cast<int64_t>(Tw) * 16 + 4 * gw + g;
-      const bool ok = valid && Tw >= 0 && k < K;
       double xd[DM];
-      float cw[DM];
       load_row_exact<DM>(src, i, valid, xd);
-      load_codeword<DM>(C, ct, k, d, ok, cw);
       double D = __builtin_inf();
       int kk = INT_MAX;
-      if (ok) {
-        D = 0.0;
 #pragma unroll
-        for (int t = 0; t < DM; ++t) {
-          if (t < d) {
-            const double diff = xd[t] - static_cast<double>(cw[t]);
-            D = D + diff * diff;
+      for (int u0 = 0; u0 < NC; u0 += 4) {
+        float cw[4][DM];
+        bool ok[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int64_t T = static_cast<int64_t>(Tw) + u0 + u;
+          const int64_t k = T * 16 + 4 * gw + g;
+          ok[u] = valid && Tw >= 0 && u0 + u < NC && T < t1 && k < K;
+          load_codeword<DM>(C, ct, k, d, ok[u], cw[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (ok[u]) {
+            double Du = 0.0;
+#pragma unroll
+            for (int t = 0; t < DM; ++t) {
+              if (t < d) {
+                const double diff = xd[t] - static_cast<double>(cw[u][t]);
+                Du = Du + diff * diff;
+              }
+            }
+            const int ku = static_cast<int>((static_cast<int64_t>(Tw) + u0 + u) * 16 + 4 * gw + g);
+            if (cless(Du, ku, D, kk)) {
+              D = Du;
+              kk = ku;
+            }
           }
         }
-        kk = static_cast<int>(k);
       }
 #pragma unroll
       for (int msk = 16; msk <= 32; msk <<= 1) {
@@ -433,13 +625,22 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const float* __
 // One thread per row.  Top-1: merge the splits' exact winners.  Top-B: re-score in fp64 the four
 // codewords of every kept tile of every lane group and split.  Then order by (D, k) and certify
 // against the screen bound.
+// Screen error bound (certification): delta = acc_ulps 2^-24 (R^2 + 2 ||x|| R) + split_coef ||x|| R
+// + abs_coef (||x|| + R + 1), with R = ||x|| + sqrt(D_top).
+struct ScreenBound {
+  double acc_ulps;
+  double split_coef;
+  double abs_coef;
+};
+
 template <int KS, int NB>
 __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top, const int* __restrict__ pT,
                                                        const float* __restrict__ pR, const double* __restrict__ pD,
                                                        const int* __restrict__ pK, const double* __restrict__ xn2a,
                                                        const void* __restrict__ C, int ct, int64_t K,
-                                                       int32_t* __restrict__ codes, float* __restrict__ dist,
-                                                       double* __restrict__ rowD, int* __restrict__ rowK) {
+                                                       ScreenBound bound, int32_t* __restrict__ codes,
+                                                       float* __restrict__ dist, double* __restrict__ rowD,
+                                                       int* __restrict__ rowK) {
   constexpr int DM = 4 * KS;  // dimensions this instantiation covers (d <= DM)
   __shared__ int scan[256];
   __shared__ int flagged[256];
@@ -523,7 +724,8 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     } else {
       const double xn = sqrt(xn2);
       const double R = xn + sqrt(Dl);
-      const double delta = static_cast<double>(4 * d + 24) * 0x1p-24 * (R * R + 2.0 * xn * R) + 1e-35;
+      const double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
+                           bound.abs_coef * (xn + R + 1.0) + 1e-35;
       certain = Dl < static_cast<double>(rest) + xn2 - delta;
     }
   }
@@ -680,51 +882,73 @@ __global__ __launch_bounds__(256) void beam_emit_kernel(int64_t n, int64_t vpr, 
   if (err_out) err_out[i] = static_cast<float>(err[i * n_par]);
 }
 
-template <int KS, int NB, int CB>
+template <class OPS, int NB, int CB, int NC = 1>
 hipError_t launch_screen_t(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
                            const ScreenWs& w, hipStream_t stream) {
   dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
-  hipLaunchKernelGGL((screen_kernel<KS, NB, CB>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
+  hipLaunchKernelGGL((screen_kernel<OPS, NB, CB, NC>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
                      p.tiles_per_split, C, ct, K, w.pT, w.pR, w.pD, w.pK, w.xn2);
   return hipGetLastError();
 }
 
-template <int KS>
-hipError_t launch_screen_ks(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
-                            const ScreenWs& w, hipStream_t stream) {
+template <class OPS>
+hipError_t launch_screen_ops(const RowSrc& src, const void* C, int ct, int64_t K, const ScreenPlan& p,
+                             const ScreenWs& w, hipStream_t stream) {
   switch (p.nb) {
-    case 1: return p.cb == CRVQ_CB_WIDE ? launch_screen_t<KS, 1, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
-                             : launch_screen_t<KS, 1, 2>(src, C, ct, K, p, w, stream);
-    case 2: return p.cb == CRVQ_CB_WIDE ? launch_screen_t<KS, 2, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
-                             : launch_screen_t<KS, 2, 2>(src, C, ct, K, p, w, stream);
-    case 4: return launch_screen_t<KS, 4, 4>(src, C, ct, K, p, w, stream);
-    case 8: return launch_screen_t<KS, 8, 2>(src, C, ct, K, p, w, stream);
-    case 16: return launch_screen_t<KS, 16, 1>(src, C, ct, K, p, w, stream);
+    case 1:
+      if (p.chunk > 1)
+        return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 1, CRVQ_CB_WIDE, CRVQ_CHUNK>(src, C, ct, K, p, w, stream)
+                                    : launch_screen_t<OPS, 1, 2, CRVQ_CHUNK>(src, C, ct, K, p, w, stream);
+      return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 1, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
+                                  : launch_screen_t<OPS, 1, 2>(src, C, ct, K, p, w, stream);
+    case 2: return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 2, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
+                             : launch_screen_t<OPS, 2, 2>(src, C, ct, K, p, w, stream);
+    case 4: return launch_screen_t<OPS, 4, 4>(src, C, ct, K, p, w, stream);
+    case 8: return launch_screen_t<OPS, 8, 2>(src, C, ct, K, p, w, stream);
+    case 16: return launch_screen_t<OPS, 16, 1>(src, C, ct, K, p, w, stream);
   }
   return hipErrorInvalidValue;
 }
 
 template <int KS, int NB>
 hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K, int top, const ScreenPlan& p,
-                             const ScreenWs& w, int32_t* codes, float* dist, double* rowD, int* rowK,
-                             hipStream_t stream) {
+                             const ScreenWs& w, const ScreenBound& bound, int32_t* codes, float* dist, double* rowD,
+                             int* rowK, hipStream_t stream) {
   hipLaunchKernelGGL((finalize_kernel<KS, NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
-                     src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, codes, dist, rowD, rowK);
+                     src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, codes, dist, rowD, rowK);
   return hipGetLastError();
 }
 
 template <int KS>
 hipError_t launch_finalize_ks(const RowSrc& src, const void* C, int ct, int64_t K, int top, const ScreenPlan& p,
-                              const ScreenWs& w, int32_t* codes, float* dist, double* rowD, int* rowK,
-                              hipStream_t stream) {
+                              const ScreenWs& w, const ScreenBound& bound, int32_t* codes, float* dist, double* rowD,
+                              int* rowK, hipStream_t stream) {
   switch (p.nb) {
-    case 1: return launch_finalize_t<KS, 1>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
-    case 2: return launch_finalize_t<KS, 2>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
-    case 4: return launch_finalize_t<KS, 4>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
-    case 8: return launch_finalize_t<KS, 8>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
-    case 16: return launch_finalize_t<KS, 16>(src, C, ct, K, top, p, w, codes, dist, rowD, rowK, stream);
+    case 1: return launch_finalize_t<KS, 1>(src, C, ct, K, top, p, w, bound, codes, dist, rowD, rowK, stream);
+    case 2: return launch_finalize_t<KS, 2>(src, C, ct, K, top, p, w, bound, codes, dist, rowD, rowK, stream);
+    case 4: return launch_finalize_t<KS, 4>(src, C, ct, K, top, p, w, bound, codes, dist, rowD, rowK, stream);
+    case 8: return launch_finalize_t<KS, 8>(src, C, ct, K, top, p, w, bound, codes, dist, rowD, rowK, stream);
+    case 16: return launch_finalize_t<KS, 16>(src, C, ct, K, top, p, w, bound, codes, dist, rowD, rowK, stream);
   }
   return hipErrorInvalidValue;
+}
+
+// The certification bound of a screen mode.  fp32 MFMA: the accumulation and ||c||^2 roundings.
+// Split bf16: a wider accumulation allowance (the 32-term bf16 MFMA sum, measured well below it),
+// the split remainder 2^-15 ||x|| R for each operand that is not bf16 already, and an absolute
+// term for subnormal operands or partial sums that the matrix core may flush.
+ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d) {
+  ScreenBound b;
+  b.acc_ulps = static_cast<double>(4 * d + 24);
+  b.split_coef = 0.0;
+  b.abs_coef = 0.0;
+  if (p.split) {
+    if (b.acc_ulps < 96.0) b.acc_ulps = 96.0;
+    const int inexact = (x_type != ET_BF16 ? 1 : 0) + (ct != ET_BF16 ? 1 : 0);
+    b.split_coef = 0x1p-15 * static_cast<double>(inexact) * (1.0 + 0x1p-6);
+    b.abs_coef = 0x1p-118;
+  }
+  return b;
 }
 
 }  // namespace
@@ -741,7 +965,9 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   // work and registers cost more screen time (12 % at K = 65536) than the rescues it saves.
   p.nb = next_pow2_nb(top < CRVQ_MIN_TRACKED_TILES ? CRVQ_MIN_TRACKED_TILES : top);
   p.cb = p.nb <= 2 ? CRVQ_CB_WIDE : (p.nb == 4 ? 4 : (p.nb == 8 ? 2 : 1));
-  p.ks = d <= 4 ? 1 : (d <= 8 ? 2 : 4);
+  // d <= 8: one split-bf16 MFMA per tile (a quarter of the matrix-core time of the two fp32 steps)
+  p.split = (CRVQ_SPLIT_SCREEN && d <= 8) ? 1 : 0;
+  p.ks = p.split ? 2 : (d <= 4 ? 1 : (d <= 8 ? 2 : 4));
   p.tiles = cdiv(K, 16);
   p.grid_x = cdiv(n_rows, 64 * p.cb);
   int64_t splits = 1;
@@ -758,13 +984,15 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   }
   p.tiles_per_split = cdiv(p.tiles, splits);
   p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
+  p.chunk = (p.nb == 1 && p.tiles_per_split >= CRVQ_CHUNK_MIN_TILES) ? CRVQ_CHUNK : 1;
   return p;
 }
 
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc) {
   ScreenWs w;
   const int64_t tiles = cdiv(K_alloc, 16);
-  w.apack = ws.take<float>(static_cast<size_t>(tiles * 64 * p.ks));
+  // fp32: 64 lanes x ks floats per tile; split: 16 codewords x 16 bf16 per tile
+  w.apack = ws.take<float>(static_cast<size_t>(p.split ? tiles * 128 : tiles * 64 * p.ks));
   w.cnp = ws.take<float>(static_cast<size_t>(tiles * 16));
   w.pR = ws.take<float>(static_cast<size_t>(p.splits) * n_rows);
   if (p.nb == 1) {
@@ -787,22 +1015,32 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
   if (src.n <= 0) return hipSuccess;
   const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
   hipError_t e;
-  switch (p.ks) {
-    case 1: hipLaunchKernelGGL(prep_codebook<1>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
-    case 2: hipLaunchKernelGGL(prep_codebook<2>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
-    default: hipLaunchKernelGGL(prep_codebook<4>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+  if (p.split) {
+    hipLaunchKernelGGL(prep_codebook_split, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles,
+                       reinterpret_cast<uint16_t*>(w.apack), w.cnp);
+  } else {
+    switch (p.ks) {
+      case 1: hipLaunchKernelGGL(prep_codebook<1>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+      case 2: hipLaunchKernelGGL(prep_codebook<2>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+      default: hipLaunchKernelGGL(prep_codebook<4>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  switch (p.ks) {
-    case 1: e = launch_screen_ks<1>(src, C, ct, K, p, w, stream); break;
-    case 2: e = launch_screen_ks<2>(src, C, ct, K, p, w, stream); break;
-    default: e = launch_screen_ks<4>(src, C, ct, K, p, w, stream); break;
+  if (p.split) {
+    e = launch_screen_ops<SplitOps>(src, C, ct, K, p, w, stream);
+  } else {
+    switch (p.ks) {
+      case 1: e = launch_screen_ops<F32Ops<1>>(src, C, ct, K, p, w, stream); break;
+      case 2: e = launch_screen_ops<F32Ops<2>>(src, C, ct, K, p, w, stream); break;
+      default: e = launch_screen_ops<F32Ops<4>>(src, C, ct, K, p, w, stream); break;
+    }
   }
   if (e != hipSuccess) return e;
+  const ScreenBound bound = screen_bound(p, src.type, ct, src.d);
   switch (p.ks) {
-    case 1: return launch_finalize_ks<1>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
-    case 2: return launch_finalize_ks<2>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
-    default: return launch_finalize_ks<4>(src, C, ct, K, top, p, w, out_codes, out_dist, rowD, rowK, stream);
+    case 1: return launch_finalize_ks<1>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
+    case 2: return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
+    default: return launch_finalize_ks<4>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
   }
 }
 

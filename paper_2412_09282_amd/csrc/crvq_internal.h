@@ -53,6 +53,7 @@ struct ScreenPlan {
   int ks;            // 4-wide K steps of the fp32 MFMA (ceil(d / 4)); 2 (8 dimensions) when split
   int split;         // 1: split-bf16 MFMA screen (d <= 8), 0: fp32 MFMA screen
   int chunk;         // top-1: tiles per tracking chunk (1 = single tiles)
+  int s32;           // 1: top-1 screen on 32 x 32 split-fp16 tiles (tiles then count 32 codewords)
   int64_t tiles;     // 16-codeword tiles (ceil(K / 16))
   int64_t grid_x;    // row groups
   int splits;        // codebook splits (grid y)
@@ -68,6 +69,7 @@ struct ScreenWs {
   double* pD;    // top-1: exact distance of the split's winner, [split][row]
   int* pK;       // top-1: its codeword, [split][row]
   double* xn2;   // top-1: ||x||^2 per row (fp64)
+  float* smax;   // 32 x 32 screen: partial maxima of |c|, then the scale alpha
 };
 // Carves the screen's scratch out of `ws`; returns it (pointers null on a dry run).
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc);

@@ -39,6 +39,21 @@
 #ifndef CRVQ_CHUNK_MIN_TILES
 #define CRVQ_CHUNK_MIN_TILES 128  // shorter tile ranges track single tiles (cheaper exact epilogue)
 #endif
+#ifndef CRVQ_S32_SCREEN
+#define CRVQ_S32_SCREEN 1  // 32 x 32 split-fp16 tiles for long top-1 searches
+#endif
+#ifndef CRVQ_S32_MIN_TILES
+#define CRVQ_S32_MIN_TILES 256  // 16-codeword tiles per split from which the 32 x 32 screen is used
+#endif
+#ifndef CRVQ_S32_CB
+#define CRVQ_S32_CB 4  // 32-row column blocks per wave
+#endif
+#ifndef CRVQ_S32_CHUNK
+#define CRVQ_S32_CHUNK 2  // 32-codeword tiles per tracking chunk (1 or 2)
+#endif
+#ifndef CRVQ_S32_SCHED
+#define CRVQ_S32_SCHED 1  // pin the MFMA / VALU interleave of the 32 x 32 screen
+#endif
 
 namespace crvq {
 namespace {
@@ -620,17 +635,324 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __r
 }
 
 // ------------------------------------------------------------------------------------------------
+// 2'. top-1 screen on 32 x 32 tiles with split-fp16 operands (d <= 8, long codebooks)
+// ------------------------------------------------------------------------------------------------
+// Codewords and -2x are scaled by one power of two alpha (alpha max|c| in [2^11, 2^12)) and split
+// into two fp16 terms: alpha c = c1 + c2 + e_c, alpha (-2x) = x1 + x2 + e_x with |e| <= 2^-22 |.|
+// (plus 2^-25 below the fp16 normal range).  Per 32 x 32 tile two v_mfma_f32_32x32x16_f16 form
+//   alpha^2 s = c1.x1 + c2.x1  (first: lanes 0-31 carry c1 / x1, lanes 32-63 c2 / x1)
+//             + c1.x2 + N      (second: lanes 0-31 c1 / x2, lanes 32-63 the three fp16 terms of
+//                               N 2^-12, N = sum_t (alpha c_t)^2, against 2^12)
+// fp16 products are exact in fp32.  The dropped c2.x2, the split remainders and the accumulation
+// roundings enter the certification bound.  Lane l ends with the 16 values of codewords
+// 8 (r / 4) + 4 (l / 32) + r % 4, r = 0..15, for row l % 32.  A row with an element whose scaled
+// value does not fit fp16 is not screened: its bound is set to -inf, so it is re-searched exactly.
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+constexpr int kS32Tile = 32;         // codewords per tile
+constexpr int kS32TileHalves = 768;  // packed fp16 per tile: c1, c2, N terms, 32 x 8 each
+constexpr int kS32MaxParts = 256;    // partial maxima of the codebook scale reduction
+
+// min(c, a[0..15]) as a depth-3 tree of eight v_min3
+__device__ __forceinline__ float min_fold16(float c, const f16v& a) {
+  const float m0 = fminf(fminf(a[0], a[1]), a[2]);
+  const float m1 = fminf(fminf(a[3], a[4]), a[5]);
+  const float m2 = fminf(fminf(a[6], a[7]), a[8]);
+  const float m3 = fminf(fminf(a[9], a[10]), a[11]);
+  const float m4 = fminf(fminf(a[12], a[13]), a[14]);
+  const float n0 = fminf(fminf(m0, m1), m2);
+  const float n1 = fminf(fminf(m3, m4), a[15]);
+  return fminf(fminf(c, n0), n1);
+}
+
+__device__ __forceinline__ uint16_t f16_bits(float v) { return __builtin_bit_cast(uint16_t, static_cast<_Float16>(v)); }
+__device__ __forceinline__ float f16_val(uint16_t b) { return static_cast<float>(__builtin_bit_cast(_Float16, b)); }
+
+// Partial maxima of |c| over the codebook (block b covers a strided share).
+__global__ __launch_bounds__(256) void cb_absmax_partial(const void* __restrict__ C, int ct, int64_t count,
+                                                         float* __restrict__ part) {
+  __shared__ float sh[256];
+  float m = 0.0f;
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; e < count;
+       e += static_cast<int64_t>(gridDim.x) * 256) {
+    const float v = (ct == ET_F32) ? static_cast<const float*>(C)[e]
+                                   : bf16_to_f(static_cast<const uint16_t*>(C)[e]);
+    m = fmaxf(m, fabsf(v));
+  }
+  sh[threadIdx.x] = m;
+  __syncthreads();
+  for (int s = 128; s >= 1; s >>= 1) {
+    if (static_cast<int>(threadIdx.x) < s) sh[threadIdx.x] = fmaxf(sh[threadIdx.x], sh[threadIdx.x + s]);
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[blockIdx.x] = sh[0];
+}
+
+// alpha = 2^(11 - floor(log2 max)), at most 2^126; 1 for an all-zero or non-finite codebook.
+__device__ __forceinline__ float s32_alpha(float mx) {
+  if (!(mx > 0.0f) || !(mx <= 3.402823466e38f)) return 1.0f;
+  int e = ilogbf(mx);
+  int s = 11 - e;
+  if (s > 126) s = 126;
+  return ldexpf(1.0f, s);
+}
+
+// Every block folds the partial maxima, block 0 publishes alpha; then thread k packs codeword k.
+__global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict__ C, int ct, int64_t K, int d,
+                                                         int64_t tiles, const float* __restrict__ part, int nparts,
+                                                         uint16_t* __restrict__ apack, float* __restrict__ alpha_out) {
+  __shared__ float sh[256];
+  sh[threadIdx.x] = (static_cast<int>(threadIdx.x) < nparts) ? part[threadIdx.x] : 0.0f;
+  __syncthreads();
+  for (int s = 128; s >= 1; s >>= 1) {
+    if (static_cast<int>(threadIdx.x) < s) sh[threadIdx.x] = fmaxf(sh[threadIdx.x], sh[threadIdx.x + s]);
+    __syncthreads();
+  }
+  const float alpha = s32_alpha(sh[0]);
+  if (blockIdx.x == 0 && threadIdx.x == 0) alpha_out[0] = alpha;
+  const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (k >= tiles * kS32Tile) return;
+  float c[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    c[t] = (k < K && t < d) ? alpha * static_cast<float>(cb_elem(C, ct, k, d, t)) : 0.0f;
+  u16x8 p1, p2, pn;
+  float N = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    N = N + c[t] * c[t];
+    const uint16_t h1 = f16_bits(c[t]);
+    p1[t] = h1;
+    p2[t] = f16_bits(c[t] - f16_val(h1));
+    pn[t] = 0;
+  }
+  if (k < K) {
+    const float v = N * 0x1p-12f;
+    const uint16_t n1 = f16_bits(v);
+    const float r1 = v - f16_val(n1);
+    const uint16_t n2 = f16_bits(r1);
+    pn[0] = n1;
+    pn[1] = n2;
+    pn[2] = f16_bits(r1 - f16_val(n2));
+  } else {
+    pn[0] = 0x7c00;  // +inf: padding never wins
+  }
+  uint16_t* tile = apack + (k >> 5) * kS32TileHalves + (k & 31) * 8;
+  *reinterpret_cast<u16x8*>(tile) = p1;
+  *reinterpret_cast<u16x8*>(tile + 256) = p2;
+  *reinterpret_cast<u16x8*>(tile + 512) = pn;
+}
+
+template <int CB, int NC>
+__global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_t* apack,
+                                                       const float* __restrict__ alpha_p, int64_t tiles, int64_t tps,
+                                                       const void* __restrict__ C, int ct, int64_t K,
+                                                       float* __restrict__ pR, double* __restrict__ pD,
+                                                       int* __restrict__ pK, double* __restrict__ xn2o) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int j = lane & 31;
+  const int h = lane >> 5;
+  const int split = blockIdx.y;
+  const int64_t n = src.n;
+  const int d = src.d;
+  const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
+  if (row0 >= n) return;  // no barriers below
+  const float alpha = alpha_p[0];
+
+  h8 b1[CB], b2[CB];
+  bool forced[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int64_t i = row0 + cb * 32 + j;
+    const bool ok = i < n;
+    float v[8];
+    const int64_t off = ok ? row_offset(src, i) : 0;
+    if (src.type == ET_F32) {
+      load_f32_elems<8>(static_cast<const float*>(src.base) + off, d, ok, v);
+    } else if (src.type == ET_BF16) {
+      load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, d, ok, v);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) v[t] = (ok && t < d) ? static_cast<float>(row_elem(src, off, t)) : 0.0f;
+    }
+    bool over = false;
+    float xs[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      xs[t] = alpha * (-2.0f * v[t]);
+      over = over || !(fabsf(xs[t]) < 65504.0f);
+    }
+    u16x8 p1, p2;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const float x = over ? 0.0f : xs[t];
+      const uint16_t x1 = f16_bits(x);
+      p1[t] = x1;
+      p2[t] = h ? static_cast<uint16_t>(t < 3 ? 0x6c00 : 0) : f16_bits(x - f16_val(x1));  // 0x6c00 = 2^12
+    }
+    b1[cb] = __builtin_bit_cast(h8, p1);
+    b2[cb] = __builtin_bit_cast(h8, p2);
+    forced[cb] = over;
+  }
+
+  float m[CB], rest[CB], cm[CB];
+  int id[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    m[cb] = __builtin_inff();
+    rest[cb] = __builtin_inff();
+    cm[cb] = __builtin_inff();
+    id[cb] = -1;
+  }
+
+  const int64_t t0 = static_cast<int64_t>(split) * tps;
+  const int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
+  if (t0 < t1) {
+    // lanes 0-31 read c1 twice, lanes 32-63 read c2 and the N terms: two 16-byte loads per lane
+    auto load = [&](int64_t T, h8& a1, h8& a2) {
+      const uint16_t* base = apack + T * kS32TileHalves + j * 8;
+      a1 = *reinterpret_cast<const h8*>(base + h * 256);
+      a2 = *reinterpret_cast<const h8*>(base + h * 512);
+    };
+    // Software-pipelined over the column blocks: the MFMA pair of block cb is issued before the
+    // minimum of block cb - 1 is folded (a depth-3 v_min3 tree), so a wave keeps the matrix core
+    // and the VALU busy at the same time.
+    auto tile = [&](const h8& a1, const h8& a2) {
+      f16v acc[2];
+#pragma unroll
+      for (int cb = 0; cb <= CB; ++cb) {
+        if (cb < CB) {
+          f16v z = {};
+          acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, b1[cb], z, 0, 0, 0);
+          acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b2[cb], acc[cb & 1], 0, 0, 0);
+        }
+        if (cb > 0) cm[cb - 1] = min_fold16(cm[cb - 1], acc[(cb - 1) & 1]);
+        if (CRVQ_S32_SCHED) {
+          if (cb < CB) __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+          if (cb > 0) __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+        }
+      }
+    };
+    auto fold = [&](int64_t T0) {
+      const int Ci = static_cast<int>(T0);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        rest[cb] = __builtin_amdgcn_fmed3f(m[cb], rest[cb], cm[cb]);
+        const bool lt = cm[cb] < m[cb];
+        m[cb] = fminf(m[cb], cm[cb]);
+        id[cb] = lt ? Ci : id[cb];
+        cm[cb] = __builtin_inff();
+      }
+    };
+    // Two tiles per iteration from two register sets; each set is refilled right after its MFMAs,
+    // one iteration ahead of its next use.
+    static_assert(NC == 1 || NC == 2, "chunks of one or two tiles");
+    h8 qa1, qa2, qb1, qb2;
+    load(t0, qa1, qa2);
+    load((t0 + 1 < t1) ? t0 + 1 : t1 - 1, qb1, qb2);
+    int64_t T = t0;
+    for (; T + 2 <= t1; T += 2) {
+      tile(qa1, qa2);
+      if (NC == 1) fold(T);
+      load((T + 2 < t1) ? T + 2 : t1 - 1, qa1, qa2);
+      tile(qb1, qb2);
+      fold(NC == 1 ? T + 1 : T);
+      load((T + 3 < t1) ? T + 3 : t1 - 1, qb1, qb2);
+    }
+    if (T < t1) {
+      tile(qa1, qa2);
+      fold(T);
+    }
+  }
+
+  // The lane half with the smaller kept-chunk minimum wins the row; the other half's best chunk
+  // joins the bound.  The winner half's 16 codewords of every tile of the kept chunk are re-scored
+  // exactly, 8 per lane half, and reduced in (D, k) order.
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int64_t i = row0 + cb * 32 + j;
+    const bool valid = i < n;
+    const float mg = m[cb];
+    const float om = __shfl_xor(mg, 32);
+    const int hw = (om < mg || (om == mg && h == 1)) ? 1 - h : h;
+    float rr = (h == hw) ? rest[cb] : fminf(rest[cb], mg);
+    rr = fminf(rr, __shfl_xor(rr, 32));
+    if (forced[cb]) rr = -__builtin_inff();
+    const int Tw = __shfl(id[cb], j + 32 * hw);
+    double xd[8];
+    load_row_exact<8>(src, i, valid, xd);
+    double D = __builtin_inf();
+    int kk = INT_MAX;
+#pragma unroll
+    for (int u = 0; u < NC; ++u) {
+      const int64_t T = static_cast<int64_t>(Tw) + u;
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        // codewords 8 (2 h + q) + 4 hw + s, s = 0..3, of the tile
+        const int64_t k0 = T * kS32Tile + 8 * (2 * h + q) + 4 * hw;
+        float cw[4][8];
+        bool ok[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          ok[s] = valid && Tw >= 0 && T < t1 && k0 + s < K;
+          load_codeword<8>(C, ct, k0 + s, d, ok[s], cw[s]);
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          if (ok[s]) {
+            double Du = 0.0;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+              if (t < d) {
+                const double diff = xd[t] - static_cast<double>(cw[s][t]);
+                Du = Du + diff * diff;
+              }
+            }
+            const int ku = static_cast<int>(k0 + s);
+            if (cless(Du, ku, D, kk)) {
+              D = Du;
+              kk = ku;
+            }
+          }
+        }
+      }
+    }
+    const double oD = __shfl_xor(D, 32);
+    const int ok2 = __shfl_xor(kk, 32);
+    if (cless(oD, ok2, D, kk)) {
+      D = oD;
+      kk = ok2;
+    }
+    if (h == 0 && valid) {
+      double xn2 = 0.0;
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        if (t < d) xn2 = xn2 + xd[t] * xd[t];
+      pD[static_cast<int64_t>(split) * n + i] = D;
+      pK[static_cast<int64_t>(split) * n + i] = kk;
+      pR[static_cast<int64_t>(split) * n + i] = rr;
+      if (split == 0) xn2o[i] = xn2;
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
 // 4. merge the splits, certify, rescue uncertain rows exactly, emit
 // ------------------------------------------------------------------------------------------------
 // One thread per row.  Top-1: merge the splits' exact winners.  Top-B: re-score in fp64 the four
 // codewords of every kept tile of every lane group and split.  Then order by (D, k) and certify
 // against the screen bound.
 // Screen error bound (certification): delta = acc_ulps 2^-24 (R^2 + 2 ||x|| R) + split_coef ||x|| R
-// + abs_coef (||x|| + R + 1), with R = ||x|| + sqrt(D_top).
+// + abs_coef (||x|| + R + 1), with R = ||x|| + sqrt(D_top).  A scaled screen (alpha != null) stores
+// alpha^2 s: its bound values are divided by alpha^2 and the fp16 underflow terms
+// 2^-24 sqrt(8) (R + 2 ||x||) / alpha + 2^-12 / alpha^2 are added.
 struct ScreenBound {
   double acc_ulps;
   double split_coef;
   double abs_coef;
+  const float* alpha;
 };
 
 template <int KS, int NB>
@@ -724,9 +1046,15 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     } else {
       const double xn = sqrt(xn2);
       const double R = xn + sqrt(Dl);
-      const double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
-                           bound.abs_coef * (xn + R + 1.0) + 1e-35;
-      certain = Dl < static_cast<double>(rest) + xn2 - delta;
+      double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
+                     bound.abs_coef * (xn + R + 1.0) + 1e-35;
+      double restd = static_cast<double>(rest);
+      if (bound.alpha) {
+        const double inv = 1.0 / static_cast<double>(bound.alpha[0]);
+        restd = restd * inv * inv;
+        delta += 0x1p-24 * 2.8285 * (R + 2.0 * xn) * inv + 0x1p-12 * inv * inv;
+      }
+      certain = Dl < restd + xn2 - delta;
     }
   }
 
@@ -937,12 +1265,17 @@ hipError_t launch_finalize_ks(const RowSrc& src, const void* C, int ct, int64_t 
 // Split bf16: a wider accumulation allowance (the 32-term bf16 MFMA sum, measured well below it),
 // the split remainder 2^-15 ||x|| R for each operand that is not bf16 already, and an absolute
 // term for subnormal operands or partial sums that the matrix core may flush.
-ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d) {
+ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d, const float* alpha) {
   ScreenBound b;
   b.acc_ulps = static_cast<double>(4 * d + 24);
   b.split_coef = 0.0;
   b.abs_coef = 0.0;
-  if (p.split) {
+  b.alpha = nullptr;
+  if (p.s32) {
+    // remainders of both splits and the dropped c2.x2, each <= 2^-22 sum |c_t| |2 x_t|
+    b.split_coef = 0x1p-19;
+    b.alpha = alpha;
+  } else if (p.split) {
     if (b.acc_ulps < 96.0) b.acc_ulps = 96.0;
     const int inexact = (x_type != ET_BF16 ? 1 : 0) + (ct != ET_BF16 ? 1 : 0);
     b.split_coef = 0x1p-15 * static_cast<double>(inexact) * (1.0 + 0x1p-6);
@@ -985,15 +1318,34 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   p.tiles_per_split = cdiv(p.tiles, splits);
   p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
   p.chunk = (p.nb == 1 && p.tiles_per_split >= CRVQ_CHUNK_MIN_TILES) ? CRVQ_CHUNK : 1;
+  // Long top-1 searches: 32 x 32 split-fp16 tiles (two MFMAs per 1024 values instead of four).
+  // The same rows per workgroup and codebook splits, counted in 32-codeword tiles.
+  p.s32 = (p.split && CRVQ_S32_SCREEN && p.nb == 1 && p.tiles_per_split >= CRVQ_S32_MIN_TILES) ? 1 : 0;
+  if (p.s32) {
+    p.cb = CRVQ_S32_CB;
+    p.grid_x = cdiv(n_rows, 128 * p.cb);
+    p.tiles = cdiv(K, kS32Tile);
+    p.tiles_per_split = cdiv(p.tiles, splits);
+    p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
+    p.chunk = CRVQ_S32_CHUNK;
+  }
   return p;
 }
 
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc) {
   ScreenWs w;
   const int64_t tiles = cdiv(K_alloc, 16);
-  // fp32: 64 lanes x ks floats per tile; split: 16 codewords x 16 bf16 per tile
-  w.apack = ws.take<float>(static_cast<size_t>(p.split ? tiles * 128 : tiles * 64 * p.ks));
-  w.cnp = ws.take<float>(static_cast<size_t>(tiles * 16));
+  if (p.s32) {
+    // 32-codeword tiles of 768 fp16, the scale reduction's partial maxima and alpha
+    w.apack = ws.take<float>(static_cast<size_t>(cdiv(K_alloc, kS32Tile) * kS32TileHalves / 2));
+    w.cnp = nullptr;
+    w.smax = ws.take<float>(static_cast<size_t>(kS32MaxParts + 1));
+  } else {
+    // fp32: 64 lanes x ks floats per tile; split: 16 codewords x 16 bf16 per tile
+    w.apack = ws.take<float>(static_cast<size_t>(p.split ? tiles * 128 : tiles * 64 * p.ks));
+    w.cnp = ws.take<float>(static_cast<size_t>(tiles * 16));
+    w.smax = nullptr;
+  }
   w.pR = ws.take<float>(static_cast<size_t>(p.splits) * n_rows);
   if (p.nb == 1) {
     w.pT = nullptr;
@@ -1013,8 +1365,30 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                          const ScreenWs& w, int32_t* out_codes, float* out_dist, double* rowD, int* rowK,
                          hipStream_t stream) {
   if (src.n <= 0) return hipSuccess;
-  const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
   hipError_t e;
+  if (p.s32) {
+    const int64_t count = K * src.d;
+    int nparts = static_cast<int>(cdiv(count, 4096));
+    if (nparts > kS32MaxParts) nparts = kS32MaxParts;
+    if (nparts < 1) nparts = 1;
+    float* alpha = w.smax + kS32MaxParts;
+    uint16_t* ap = reinterpret_cast<uint16_t*>(w.apack);
+    hipLaunchKernelGGL(cb_absmax_partial, dim3(nparts), dim3(256), 0, stream, C, ct, count, w.smax);
+    hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
+                       stream, C, ct, K, src.d, p.tiles, w.smax, nparts, ap, alpha);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
+    if (p.cb == 4)
+      hipLaunchKernelGGL((screen32_kernel<4, CRVQ_S32_CHUNK>), grid, dim3(256), 0, stream, src, ap, alpha, p.tiles,
+                         p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
+    else
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK>), grid, dim3(256), 0, stream, src, ap, alpha,
+                         p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const ScreenBound bound = screen_bound(p, src.type, ct, src.d, alpha);
+    return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
+  }
+  const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
   if (p.split) {
     hipLaunchKernelGGL(prep_codebook_split, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles,
                        reinterpret_cast<uint16_t*>(w.apack), w.cnp);
@@ -1036,7 +1410,7 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     }
   }
   if (e != hipSuccess) return e;
-  const ScreenBound bound = screen_bound(p, src.type, ct, src.d);
+  const ScreenBound bound = screen_bound(p, src.type, ct, src.d, nullptr);
   switch (p.ks) {
     case 1: return launch_finalize_ks<1>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
     case 2: return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);

@@ -1,0 +1,105 @@
+"""GPU parity of the nearest-codeword search on the shapes that select each screen variant.
+
+Long top-1 searches (at least 256 16-codeword tiles per codebook split, e.g. 65536 rows x 65536
+codewords) run on 32 x 32 tiles with split-fp16 operands under a power-of-two codebook scale; shorter
+ones on 16 x 16 tiles with split-bf16 operands.  Whatever the variant, the certified screen plus the
+exact rescue must return the oracle's codes (the fp64 definition of Eq. 3, ties to the lower index)
+and its distances, including rows the scaled screen cannot represent (forced to the exact rescue),
+codebooks of extreme magnitude and ragged tails."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2412_09282_amd import crvq as C
+from paper_2412_09282_amd import inputs
+from paper_2412_09282_amd.crvq import VecSet
+
+from gpu_util import dev, say
+
+pytestmark = pytest.mark.gpu
+
+
+def rv(n, d, seed, scale=0.02):
+    return inputs.random_vectors(n, d, seed, scale)
+
+
+def assign_both(V, Cb, dtype="f32"):
+    Vt = dev(V, dtype)
+    Ct = dev(Cb, dtype)
+    n = V.shape[0]
+    codes = torch.empty(n, dtype=torch.int32, device="cuda")
+    dist = torch.empty(n, dtype=torch.float32, device="cuda")
+    C.crvq_assign(VecSet.of_vectors(Vt), Ct, codes, dist)
+    torch.cuda.synchronize()
+    exp, ed = oracle.assign(V, Cb, dtype, dtype)
+    return codes.cpu().numpy(), dist.cpu().numpy(), exp, ed
+
+
+def check(V, Cb, dtype="f32"):
+    got, gd, exp, ed = assign_both(V, Cb, dtype)
+    bad = np.flatnonzero(got != exp)
+    assert len(bad) == 0, f"{len(bad)} codes differ, e.g. rows {bad[:5]} got {got[bad[:5]]} want {exp[bad[:5]]}"
+    np.testing.assert_array_equal(gd, ed.astype(np.float32))
+
+
+@pytest.mark.parametrize("n,K,d", [(65536, 65536, 8), (65536 + 37, 65536 - 5, 8), (70001, 32768 + 17, 5)])
+def test_long_search_f32(n, K, d):
+    say(f"long top-1 search fp32 n={n} K={K} d={d}")
+    check(rv(n, d, 31 + d), rv(K, d, 32 + K))
+
+
+def test_long_search_bf16():
+    say("long top-1 search bf16 n=65536 K=65536")
+    V = inputs.f32_to_bf16_bits(rv(65536, 8, 33))
+    Cb = inputs.f32_to_bf16_bits(rv(65536, 8, 34))
+    check(V, Cb, "bf16")
+
+
+def test_long_search_outlier_rows_and_heavy_tails():
+    say("long top-1 search: t4 codebook with outlier columns, rows far outside the codebook range")
+    g = np.random.default_rng(35)
+    K, n = 65536, 65536
+    Cb = (g.standard_t(4.0, size=(K, 8)) * 0.02).astype(np.float32)
+    Cb[:, 3] *= np.float32(10.0)
+    V = (g.standard_t(4.0, size=(n, 8)) * 0.02).astype(np.float32)
+    big = g.choice(n, 300, replace=False)
+    V[big, g.integers(0, 8, 300)] *= np.float32(1e5)   # beyond the scaled fp16 range: exact rescue
+    tiny = g.choice(n, 300, replace=False)
+    V[tiny] *= np.float32(1e-6)                       # far below the codebook scale
+    check(V, Cb)
+
+
+@pytest.mark.parametrize("scale", [1e-30, 1e30])
+def test_long_search_extreme_magnitude(scale):
+    say(f"long top-1 search at magnitude {scale:g}")
+    s = np.float32(scale)
+    check(rv(65536, 8, 36) * s, rv(65536, 8, 37) * s)
+
+
+def test_long_search_duplicates_and_ties():
+    say("long top-1 search with duplicated codewords and rows equal to codewords")
+    g = np.random.default_rng(38)
+    base = rv(16384, 8, 39)
+    Cb = np.ascontiguousarray(np.concatenate([base, base, base[::-1], base])[g.permutation(65536)])
+    V = np.concatenate([base[g.integers(0, 16384, 40000)], rv(25536, 8, 40)])
+    check(V, Cb)
+
+
+def test_beam_width_one_long_codebook():
+    say("residual beam, width 1, over a K=65536 basic and K=256 extended codebook")
+    n = 65536
+    V = rv(n, 8, 41)
+    books = [rv(65536, 8, 42), rv(256, 8, 43, 0.005)]
+    Vt = dev(V)
+    bt = [dev(b) for b in books]
+    codes = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in books]
+    err = torch.empty(n, dtype=torch.float32, device="cuda")
+    C.crvq_assign_residual_beam(VecSet.of_vectors(Vt), bt, 1, codes, err)
+    torch.cuda.synchronize()
+    exp_codes, exp_err = oracle.beam(V, books, 1)
+    for t in range(2):
+        got = codes[t].cpu().numpy()
+        bad = np.flatnonzero(got != exp_codes[t])
+        assert len(bad) == 0, f"book {t}: {len(bad)} codes differ, e.g. rows {bad[:5]}"
+    np.testing.assert_array_equal(err.cpu().numpy(), np.asarray(exp_err, dtype=np.float64).astype(np.float32))

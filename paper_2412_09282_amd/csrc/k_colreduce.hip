@@ -13,8 +13,11 @@ namespace {
 constexpr int kCols = 4;          // columns per thread
 constexpr int kRowsInFlight = 8;  // row loads issued back to back per thread
 
-__device__ __forceinline__ void load4(const void* p, int type, int64_t idx, int valid_cols, double (&v)[kCols]) {
-  if (type == ET_F32) {
+// kCols elements of one row as floats: one 16-byte (fp32) or 8-byte (bf16) load when the columns
+// are full and aligned, element loads otherwise; zero past the last column.
+template <int TY>
+__device__ __forceinline__ void load4f(const void* p, int64_t idx, int valid_cols, float (&v)[kCols]) {
+  if constexpr (TY == ET_F32) {
     const float* f = static_cast<const float*>(p) + idx;
     if (valid_cols == kCols && ((reinterpret_cast<uintptr_t>(f) & 15) == 0)) {
       const float4 q = *reinterpret_cast<const float4*>(f);
@@ -24,7 +27,7 @@ __device__ __forceinline__ void load4(const void* p, int type, int64_t idx, int 
       v[3] = q.w;
     } else {
 #pragma unroll
-      for (int c = 0; c < kCols; ++c) v[c] = (c < valid_cols) ? static_cast<double>(f[c]) : 0.0;
+      for (int c = 0; c < kCols; ++c) v[c] = (c < valid_cols) ? f[c] : 0.0f;
     }
   } else {
     const uint16_t* h = static_cast<const uint16_t*>(p) + idx;
@@ -37,59 +40,49 @@ __device__ __forceinline__ void load4(const void* p, int type, int64_t idx, int 
     } else {
 #pragma unroll
       for (int c = 0; c < kCols; ++c)
-        v[c] = (c < valid_cols) ? static_cast<double>(__uint_as_float(static_cast<uint32_t>(h[c]) << 16)) : 0.0;
+        v[c] = (c < valid_cols) ? __uint_as_float(static_cast<uint32_t>(h[c]) << 16) : 0.0f;
     }
   }
 }
 
+// Pass 1 of one (input type, B present, reduction) combination.  The raw row values stay floats
+// while in flight (fewer registers, more waves); each is widened to fp64 when it is accumulated:
+// x = a - b in fp64, x * x in fp64, then the fp64 sum or max, rows in ascending order.
+template <int TY, bool HAS_B, bool MAX>
 __global__ __launch_bounds__(256) void colreduce_partial(const void* __restrict__ A, int64_t lda,
-                                                         const void* __restrict__ B, int64_t ldb, int type, int64_t M,
-                                                         int64_t N, int reduce, int64_t rows_per_slab,
-                                                         double* __restrict__ part) {
+                                                         const void* __restrict__ B, int64_t ldb, int64_t M,
+                                                         int64_t N, int64_t rows_per_slab, double* __restrict__ part) {
   const int64_t j0 = (static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x) * kCols;
   if (j0 >= N) return;
   const int valid_cols = static_cast<int>((N - j0) < kCols ? (N - j0) : kCols);
   const int64_t i0 = static_cast<int64_t>(blockIdx.y) * rows_per_slab;
   const int64_t i1 = (i0 + rows_per_slab < M) ? i0 + rows_per_slab : M;
   double acc[kCols] = {0.0, 0.0, 0.0, 0.0};
-  // rows in groups of kRowsInFlight: every load of a group is issued before any is consumed
-  int64_t i = i0;
-  for (; i + kRowsInFlight <= i1; i += kRowsInFlight) {
-    double a[kRowsInFlight][kCols];
-#pragma unroll
-    for (int u = 0; u < kRowsInFlight; ++u) load4(A, type, (i + u) * lda + j0, valid_cols, a[u]);
-    if (B) {
-      double b[kRowsInFlight][kCols];
-#pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u) load4(B, type, (i + u) * ldb + j0, valid_cols, b[u]);
-#pragma unroll
-      for (int u = 0; u < kRowsInFlight; ++u)
-#pragma unroll
-        for (int c = 0; c < kCols; ++c) a[u][c] = a[u][c] - b[u][c];
-    }
-#pragma unroll
-    for (int u = 0; u < kRowsInFlight; ++u) {
-#pragma unroll
-      for (int c = 0; c < kCols; ++c) {
-        const double sq = a[u][c] * a[u][c];
-        acc[c] = (reduce == 0) ? acc[c] + sq : (sq > acc[c] ? sq : acc[c]);
-      }
-    }
-  }
-  for (; i < i1; ++i) {
-    double a[kCols];
-    load4(A, type, i * lda + j0, valid_cols, a);
-    if (B) {
-      double b[kCols];
-      load4(B, type, i * ldb + j0, valid_cols, b);
-#pragma unroll
-      for (int c = 0; c < kCols; ++c) a[c] = a[c] - b[c];
-    }
+  auto fold = [&](const float (&a)[kCols], const float (&b)[kCols]) {
 #pragma unroll
     for (int c = 0; c < kCols; ++c) {
-      const double sq = a[c] * a[c];
-      acc[c] = (reduce == 0) ? acc[c] + sq : (sq > acc[c] ? sq : acc[c]);
+      const double x = HAS_B ? static_cast<double>(a[c]) - static_cast<double>(b[c]) : static_cast<double>(a[c]);
+      const double sq = x * x;
+      acc[c] = MAX ? (sq > acc[c] ? sq : acc[c]) : acc[c] + sq;
     }
+  };
+  int64_t i = i0;
+  for (; i + kRowsInFlight <= i1; i += kRowsInFlight) {
+    float a[kRowsInFlight][kCols], b[kRowsInFlight][kCols];
+#pragma unroll
+    for (int u = 0; u < kRowsInFlight; ++u) load4f<TY>(A, (i + u) * lda + j0, valid_cols, a[u]);
+    if constexpr (HAS_B) {
+#pragma unroll
+      for (int u = 0; u < kRowsInFlight; ++u) load4f<TY>(B, (i + u) * ldb + j0, valid_cols, b[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kRowsInFlight; ++u) fold(a[u], b[u]);
+  }
+  for (; i < i1; ++i) {
+    float a[kCols], b[kCols];
+    load4f<TY>(A, i * lda + j0, valid_cols, a);
+    if constexpr (HAS_B) load4f<TY>(B, i * ldb + j0, valid_cols, b);
+    fold(a, b);
   }
 #pragma unroll
   for (int c = 0; c < kCols; ++c)
@@ -151,8 +144,24 @@ hipError_t launch_colreduce(const void* A, int64_t lda, const void* B, int64_t l
                             const float* scale, int reduce, float* out, void* ws, hipStream_t stream) {
   Plan p = plan(M, N);
   double* part = static_cast<double*>(ws);
-  hipLaunchKernelGGL(colreduce_partial, dim3(static_cast<unsigned>(p.col_blocks), static_cast<unsigned>(p.slabs)),
-                     dim3(256), 0, stream, A, lda, B, ldb, type, M, N, reduce, p.rows_per_slab, part);
+  const dim3 grid(static_cast<unsigned>(p.col_blocks), static_cast<unsigned>(p.slabs));
+  const int combo = (type == ET_BF16 ? 4 : 0) + (B ? 2 : 0) + (reduce != 0 ? 1 : 0);
+  switch (combo) {
+#define CRVQ_COLRED(CASE, TY, HB, MX)                                                                        \
+  case CASE:                                                                                                 \
+    hipLaunchKernelGGL((colreduce_partial<TY, HB, MX>), grid, dim3(256), 0, stream, A, lda, B, ldb, M, N, \
+                       p.rows_per_slab, part);                                                               \
+    break;
+    CRVQ_COLRED(0, ET_F32, false, false)
+    CRVQ_COLRED(1, ET_F32, false, true)
+    CRVQ_COLRED(2, ET_F32, true, false)
+    CRVQ_COLRED(3, ET_F32, true, true)
+    CRVQ_COLRED(4, ET_BF16, false, false)
+    CRVQ_COLRED(5, ET_BF16, false, true)
+    CRVQ_COLRED(6, ET_BF16, true, false)
+    CRVQ_COLRED(7, ET_BF16, true, true)
+#undef CRVQ_COLRED
+  }
   hipLaunchKernelGGL(colreduce_final, dim3(static_cast<unsigned>(cdiv(N, 64))), dim3(256), 0, stream, part,
                      static_cast<int>(p.slabs), N, scale, reduce, out);
   return hipGetLastError();

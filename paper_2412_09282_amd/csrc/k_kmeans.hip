@@ -91,11 +91,17 @@ __global__ __launch_bounds__(256) void radix_hist(const int* __restrict__ keys, 
   __syncthreads();
   const int n = read_count(n_dev, n_host);
   const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile + w * (kBatches * 64);
+  int key[kBatches];
+#pragma unroll
+  for (int bt = 0; bt < kBatches; ++bt) {  // every load issued before the first is counted
+    const int64_t idx = base + bt * 64 + lane;
+    key[bt] = (idx < n) ? keys[idx] : -1;
+  }
+#pragma unroll
   for (int bt = 0; bt < kBatches; ++bt) {
     const int64_t idx = base + bt * 64 + lane;
-    int key = (idx < n) ? keys[idx] : -1;
-    const bool valid = (idx < n) && (pass != 0 || (key >= 0 && key < K));
-    const int digit = valid ? (key >> shift) & 255 : 0;
+    const bool valid = (idx < n) && (pass != 0 || (key[bt] >= 0 && key[bt] < K));
+    const int digit = valid ? (key[bt] >> shift) & 255 : 0;
     const uint64_t peers = peer_mask(valid, digit);
     if (valid && (__ffsll(static_cast<long long>(peers)) - 1) == lane) wh[w][digit] += __popcll(peers);
   }
@@ -243,7 +249,8 @@ struct RoundLds {
 };
 
 // dig[bt] = digit of entry (wave, batch bt, lane) or -1 when absent.
-__device__ __forceinline__ void round_bucket_sort(const int (&dig)[kRoundBatches], RoundLds& L) {
+__device__ __forceinline__ void round_bucket_sort(const int (&dig)[kRoundBatches], RoundLds& L,
+                                                  int (*pos_out)[kRoundBatches] = nullptr) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   for (int q = tid; q < 1024; q += 256) (&L.wh[0][0])[q] = 0;
   __syncthreads();
@@ -280,6 +287,7 @@ __device__ __forceinline__ void round_bucket_sort(const int (&dig)[kRoundBatches
     if (dig[bt] >= 0) {
       const int pos = L.wh[w][dig[bt]] + __popcll(peer[bt] & lt);
       if (pos >= 0 && pos < kRound) L.s_pos[pos] = (w * kRoundBatches + bt) * 64 + lane;
+      if (pos_out) (*pos_out)[bt] = pos;
     }
     if (dig[bt] >= 0 && (__ffsll(static_cast<long long>(peer[bt])) - 1) == lane) L.wh[w][dig[bt]] += __popcll(peer[bt]);
   }
@@ -429,13 +437,20 @@ SmallPlan small_plan(int64_t n) {
 // Every bucket is then cut into chunks of kChunk vectors; a block takes one chunk and runs the
 // small-codebook scheme on the low byte, gathering each member vector with 16-byte loads.  The
 // chunk partials of each code are folded in chunk order.
-constexpr int kChunk = 16384;
+constexpr int kChunk = 8192;
 
 // bounds of the 256 high-byte buckets and of their chunk ranges (one block)
+// Chunks are also enumerated level by level (chunk j of every bucket that has one, buckets in
+// ascending order, before any chunk j + 1): lstart[j] = number of chunks below level j, for
+// j = 0 .. max_level, where level j holds the buckets with more than j chunks.  Blocks take the
+// chunks in that order, so the blocks in flight read vectors from about the same index range of
+// every bucket at once.
 __global__ __launch_bounds__(256) void bucket_bounds(const int* __restrict__ offs, int64_t n_tiles,
                                                      const int* __restrict__ n_valid, int* __restrict__ bstart,
-                                                     int* __restrict__ cstart) {
+                                                     int* __restrict__ cstart, int* __restrict__ lstart) {
   __shared__ int sh[256];
+  __shared__ int nch[256];
+  __shared__ int maxc;
   const int b = threadIdx.x;
   const int s = offs[static_cast<int64_t>(b) * n_tiles];
   const int e = (b < 255) ? offs[static_cast<int64_t>(b + 1) * n_tiles] : *n_valid;
@@ -448,6 +463,29 @@ __global__ __launch_bounds__(256) void bucket_bounds(const int* __restrict__ off
     bstart[256] = e;
     cstart[256] = total;
   }
+  nch[b] = chunks;
+  if (b == 0) maxc = 0;
+  __syncthreads();
+  if (b == 0) {
+    int m = 0;
+    for (int q = 0; q < 256; ++q) m = nch[q] > m ? nch[q] : m;
+    maxc = m;
+  }
+  __syncthreads();
+  const int levels = maxc;
+  int carry = 0;
+  for (int j0 = 0; j0 < levels; j0 += 256) {
+    const int j = j0 + b;
+    int cnt = 0;
+    if (j < levels)
+      for (int q = 0; q < 256; ++q) cnt += (nch[q] > j) ? 1 : 0;
+    int tot;
+    const int lex = block_exclusive_scan(cnt, sh, tot);
+    if (j < levels) lstart[j] = carry + lex;
+    carry += tot;
+  }
+  if (b == 0) lstart[levels] = carry;  // == total
+  if (b == 0) cstart[257] = levels;
 }
 
 __global__ __launch_bounds__(256) void bucket_partial(RowSrc src, const int* __restrict__ keys,
@@ -508,6 +546,111 @@ __global__ __launch_bounds__(256) void bucket_partial(RowSrc src, const int* __r
   pcount[static_cast<int64_t>(blk) * 256 + tid] = cnt;
 }
 
+// d <= 8: a round's member vectors are gathered all at once (kRoundBatches per thread, every load
+// issued before any is used) into LDS at their sorted position; thread k then adds the members of
+// code k from LDS in ascending order -- the same fp64 additions in the same order as above.
+__global__ __launch_bounds__(256) void bucket_partial8(RowSrc src, const int* __restrict__ keys,
+                                                       const int* __restrict__ vals, const int* __restrict__ bstart,
+                                                       const int* __restrict__ cstart, const int* __restrict__ lstart,
+                                                       double* __restrict__ part, int* __restrict__ pcount) {
+  __shared__ RoundLds L;
+  __shared__ float4 stage[kRound][2];
+  __shared__ int s_bucket;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int wi = blockIdx.x;
+  if (wi >= cstart[256]) return;  // uniform: more blocks are launched than there can be chunks
+  // level j of work item wi, then the (wi - lstart[j])-th bucket with more than j chunks
+  const int levels = cstart[257];
+  int lo = 0, hi = levels;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (lstart[mid] <= wi)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  const int j = lo;
+  const int rank = wi - lstart[j];
+  {
+    const int has = (cstart[tid + 1] - cstart[tid]) > j ? 1 : 0;
+    int tot;
+    const int before = block_exclusive_scan(has, L.sh_scan, tot);
+    if (has && before == rank) s_bucket = tid;
+    __syncthreads();
+  }
+  const int b = s_bucket;
+  const int blk = cstart[b] + j;  // partials stay in bucket-major order
+  const int64_t b0 = bstart[b] + static_cast<int64_t>(j) * kChunk;
+  const int64_t b1 = (b0 + kChunk < bstart[b + 1]) ? b0 + kChunk : bstart[b + 1];
+  const int d = src.d;
+  const bool packed = src.ld == src.vpr * d;
+  double acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = 0.0;
+  int cnt = 0;
+  for (int64_t base = b0; base < b1; base += kRound) {
+    int dig[kRoundBatches], vid[kRoundBatches], pos[kRoundBatches];
+#pragma unroll
+    for (int bt = 0; bt < kRoundBatches; ++bt) {
+      const int64_t idx = base + (w * kRoundBatches + bt) * 64 + lane;
+      const bool live = idx < b1;
+      dig[bt] = live ? (keys[idx] & 255) : -1;
+      vid[bt] = live ? vals[idx] : -1;
+    }
+    round_bucket_sort(dig, L, &pos);
+    float4 v[kRoundBatches][2];
+#pragma unroll
+    for (int bt = 0; bt < kRoundBatches; ++bt) {
+      v[bt][0] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      v[bt][1] = v[bt][0];
+      if (vid[bt] >= 0) {
+        const int64_t off = packed ? static_cast<int64_t>(vid[bt]) * d : row_offset(src, vid[bt]);
+        if (src.type == ET_F32 && d == 8 && (reinterpret_cast<uintptr_t>(static_cast<const float*>(src.base) + off) & 15) == 0) {
+          const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(src.base) + off);
+          v[bt][0] = p[0];
+          v[bt][1] = p[1];
+        } else if (src.type == ET_BF16 && d == 8 &&
+                   (reinterpret_cast<uintptr_t>(static_cast<const uint16_t*>(src.base) + off) & 15) == 0) {
+          const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(src.base) + off);
+          v[bt][0] = make_float4(__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xffff0000u),
+                                 __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xffff0000u));
+          v[bt][1] = make_float4(__uint_as_float(q.z << 16), __uint_as_float(q.z & 0xffff0000u),
+                                 __uint_as_float(q.w << 16), __uint_as_float(q.w & 0xffff0000u));
+        } else {
+          float e[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) e[t] = (t < d) ? static_cast<float>(row_elem(src, off, t)) : 0.0f;
+          v[bt][0] = make_float4(e[0], e[1], e[2], e[3]);
+          v[bt][1] = make_float4(e[4], e[5], e[6], e[7]);
+        }
+      }
+    }
+#pragma unroll
+    for (int bt = 0; bt < kRoundBatches; ++bt) {
+      if (vid[bt] >= 0 && pos[bt] >= 0 && pos[bt] < kRound) {
+        stage[pos[bt]][0] = v[bt][0];
+        stage[pos[bt]][1] = v[bt][1];
+      }
+    }
+    __syncthreads();
+    const int e1 = L.s_start[tid + 1];
+    for (int j = L.s_start[tid]; j < e1; ++j) {
+      const float4 a = stage[j][0], c = stage[j][1];
+      const float x[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+#pragma unroll
+      for (int t = 0; t < 8; ++t)
+        if (t < d) acc[t] = acc[t] + static_cast<double>(x[t]);
+    }
+    cnt += e1 - L.s_start[tid];
+    __syncthreads();
+  }
+  double* pp = part + (static_cast<int64_t>(blk) * 256 + tid) * d;
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+    if (t < d) pp[t] = acc[t];
+  pcount[static_cast<int64_t>(blk) * 256 + tid] = cnt;
+}
+
 __global__ __launch_bounds__(256) void bucket_final(const double* __restrict__ part, const int* __restrict__ pcount,
                                                     const int* __restrict__ cstart, int64_t K, int d, void* C, int ct,
                                                     int32_t* __restrict__ counts) {
@@ -535,6 +678,7 @@ struct KmWs {
   int* n_valid;
   int* bstart;
   int* cstart;
+  int* lstart;
   double* part;
   int* pcount;
   int64_t max_chunks;
@@ -552,8 +696,9 @@ KmWs carve(WsCursor& ws, int64_t n, int64_t K) {
   w.sums = ws.take<int>(static_cast<size_t>(cdiv(hn, kScanBlock)));
   w.n_valid = ws.take<int>(1);
   w.bstart = ws.take<int>(257);
-  w.cstart = ws.take<int>(257);
+  w.cstart = ws.take<int>(258);  // [256] = chunks, [257] = levels
   w.max_chunks = cdiv(n, kChunk) + 256;  // every bucket adds at most one partial chunk
+  w.lstart = ws.take<int>(static_cast<size_t>(w.max_chunks + 1));
   w.part = ws.take<double>(static_cast<size_t>(w.max_chunks) * 256 * 16);
   w.pcount = ws.take<int>(static_cast<size_t>(w.max_chunks) * 256);
   return w;
@@ -604,9 +749,14 @@ hipError_t launch_kmeans_update(const RowSrc& src, const int32_t* codes, int64_t
   if ((e = exclusive_scan(w.hist, 256 * n_tiles, w.sums, w.offs, w.n_valid, stream)) != hipSuccess) return e;
   hipLaunchKernelGGL(radix_scatter, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, codes, nullptr, nullptr,
                      n, K, 0, 8, n_tiles, w.offs, w.keys, w.vals);
-  hipLaunchKernelGGL(bucket_bounds, dim3(1), dim3(256), 0, stream, w.offs, n_tiles, w.n_valid, w.bstart, w.cstart);
-  hipLaunchKernelGGL(bucket_partial, dim3(static_cast<unsigned>(w.max_chunks)), dim3(256), 0, stream, src, w.keys,
-                     w.vals, w.bstart, w.cstart, w.part, w.pcount);
+  hipLaunchKernelGGL(bucket_bounds, dim3(1), dim3(256), 0, stream, w.offs, n_tiles, w.n_valid, w.bstart, w.cstart,
+                     w.lstart);
+  if (src.d <= 8 && src.type != ET_F64)
+    hipLaunchKernelGGL(bucket_partial8, dim3(static_cast<unsigned>(w.max_chunks)), dim3(256), 0, stream, src, w.keys,
+                       w.vals, w.bstart, w.cstart, w.lstart, w.part, w.pcount);
+  else
+    hipLaunchKernelGGL(bucket_partial, dim3(static_cast<unsigned>(w.max_chunks)), dim3(256), 0, stream, src, w.keys,
+                       w.vals, w.bstart, w.cstart, w.part, w.pcount);
   hipLaunchKernelGGL(bucket_final, dim3(static_cast<unsigned>(cdiv(K * src.d, 256))), dim3(256), 0, stream, w.part,
                      w.pcount, w.cstart, K, src.d, C, c_type, counts);
   return hipGetLastError();

@@ -19,6 +19,33 @@ struct CodePtrs {
 };
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Streaming loads and stores of data touched once (whole weight matrices, code arrays, outputs).
+// The nontemporal hint keeps such streams from displacing reused data in L2 and the last-level
+// cache and lets the memory system stream them: a plain read of a 940 MB array runs at about
+// 4 TB/s on MI355X, the same read with nontemporal loads at about 5.4 TB/s.
+#ifndef CRVQ_NT_STORE
+#define CRVQ_NT_STORE 1
+#endif
+typedef unsigned int crvq_u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int crvq_u2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+  const crvq_u4 t = __builtin_nontemporal_load(static_cast<const crvq_u4*>(p));
+  return make_uint4(t[0], t[1], t[2], t[3]);
+}
+__device__ __forceinline__ uint2 ld_stream8(const void* p) {
+  const crvq_u2 t = __builtin_nontemporal_load(static_cast<const crvq_u2*>(p));
+  return make_uint2(t[0], t[1]);
+}
+__device__ __forceinline__ int ld_stream_i32(const int* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ void st_stream(void* p, uint4 v) {
+  if (CRVQ_NT_STORE) {
+    const crvq_u4 t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, static_cast<crvq_u4*>(p));
+  } else {
+    *static_cast<uint4*>(p) = v;
+  }
+}
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // Bump allocator over a caller-supplied workspace (or a dry run that only measures).

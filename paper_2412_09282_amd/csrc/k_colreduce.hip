@@ -11,7 +11,10 @@ namespace crvq {
 namespace {
 
 constexpr int kCols = 4;          // columns per thread
-constexpr int kRowsInFlight = 8;  // row loads issued back to back per thread
+#ifndef CRVQ_CR_ROWS
+#define CRVQ_CR_ROWS 8
+#endif
+constexpr int kRowsInFlight = CRVQ_CR_ROWS;  // row loads issued back to back per thread
 
 // kCols elements of one row as floats: one 16-byte (fp32) or 8-byte (bf16) load when the columns
 // are full and aligned, element loads otherwise; zero past the last column.
@@ -20,11 +23,11 @@ __device__ __forceinline__ void load4f(const void* p, int64_t idx, int valid_col
   if constexpr (TY == ET_F32) {
     const float* f = static_cast<const float*>(p) + idx;
     if (valid_cols == kCols && ((reinterpret_cast<uintptr_t>(f) & 15) == 0)) {
-      const float4 q = *reinterpret_cast<const float4*>(f);
-      v[0] = q.x;
-      v[1] = q.y;
-      v[2] = q.z;
-      v[3] = q.w;
+      const uint4 q = ld_stream(f);
+      v[0] = __uint_as_float(q.x);
+      v[1] = __uint_as_float(q.y);
+      v[2] = __uint_as_float(q.z);
+      v[3] = __uint_as_float(q.w);
     } else {
 #pragma unroll
       for (int c = 0; c < kCols; ++c) v[c] = (c < valid_cols) ? f[c] : 0.0f;
@@ -32,7 +35,7 @@ __device__ __forceinline__ void load4f(const void* p, int64_t idx, int valid_col
   } else {
     const uint16_t* h = static_cast<const uint16_t*>(p) + idx;
     if (valid_cols == kCols && ((reinterpret_cast<uintptr_t>(h) & 7) == 0)) {
-      const uint2 q = *reinterpret_cast<const uint2*>(h);
+      const uint2 q = ld_stream8(h);
       v[0] = __uint_as_float(q.x << 16);
       v[1] = __uint_as_float(q.x & 0xffff0000u);
       v[2] = __uint_as_float(q.y << 16);

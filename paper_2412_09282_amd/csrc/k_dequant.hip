@@ -143,172 +143,167 @@ __global__ __launch_bounds__(256) void dequant_rows_perm(int64_t n_cols, int d, 
   }
 }
 
-// ---- d = 8 with 16-byte aligned books and rows: the same arithmetic with every load of a thread's
-// vectors issued before any is used, and 16-byte loads and stores.
-constexpr int kU = 4;  // vectors per thread and round in the row kernels
+// ---- d = 8 with 16-byte aligned books and rows: the same arithmetic, two lanes per vector.  Lane
+// half h of a pair reads and writes dimensions 4h .. 4h + 3, so both halves of a codeword gather
+// come from one cache line and every store of a wave is one contiguous piece.  All code and
+// codeword loads of a thread's vectors are issued before any is used.
+constexpr int kU = 4;  // vectors per lane pair and round in the row kernel
 
-// Codeword q (8 elements) as floats: two float4 (fp32) or one uint4 (bf16).
-__device__ __forceinline__ void load_cw8(const void* C, int type, int64_t q, float (&c)[8]) {
+// Half h (4 elements) of codeword q as floats: one float4 (fp32) or one 8-byte load (bf16).
+__device__ __forceinline__ void load_cw4(const void* C, int type, int64_t q, int h, float (&c)[4]) {
   if (type == ET_F32) {
-    const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(C) + q * 8);
-    const float4 a = p[0], b = p[1];
+    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(C) + q * 8 + 4 * h);
     c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w;
-    c[4] = b.x; c[5] = b.y; c[6] = b.z; c[7] = b.w;
   } else {
-    const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(C) + q * 8);
-    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      c[2 * k] = __uint_as_float(u[k] << 16);
-      c[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
-    }
+    const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(C) + q * 8 + 4 * h);
+    c[0] = __uint_as_float(w.x << 16);
+    c[1] = __uint_as_float(w.x & 0xffff0000u);
+    c[2] = __uint_as_float(w.y << 16);
+    c[3] = __uint_as_float(w.y & 0xffff0000u);
   }
 }
 
-// fp64 reconstruction of vector g of row r from its (already loaded) basic codeword c0: the
-// extended books of a critical vector are added in book order.  Returns false (NaN vector) on a
-// code out of range.
-__device__ __forceinline__ bool recon8(const DequantBooks& b, int64_t r, int64_t g, int64_t ncv, bool ok0,
-                                       const float (&c0)[8], double (&v)[8]) {
+// fp64 reconstruction of half h of vector g of row r from its (already loaded) basic codeword
+// half c0: the extended books of a critical vector are added in book order.  Returns false (NaN
+// vector) on a code out of range.
+__device__ __forceinline__ bool recon4(const DequantBooks& b, int64_t r, int64_t g, int h, int64_t ncv, bool ok0,
+                                       const float (&c0)[4], double (&v)[4]) {
 #pragma unroll
-  for (int t = 0; t < 8; ++t) v[t] = 0.0 + static_cast<double>(c0[t]);
+  for (int t = 0; t < 4; ++t) v[t] = 0.0 + static_cast<double>(c0[t]);
   bool ok = ok0;
   if (g < ncv) {
     for (int e = 1; e < b.n; ++e) {
       const int32_t q = b.q[e][r * b.ldq_ext + g];
       const bool in = q >= 0 && q < b.K[e];
       ok = ok && in;
-      float c[8];
-      load_cw8(b.C[e], b.type[e], in ? q : 0, c);
+      float c[4];
+      load_cw4(b.C[e], b.type[e], in ? q : 0, h, c);
 #pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = v[t] + static_cast<double>(c[t]);
+      for (int t = 0; t < 4; ++t) v[t] = v[t] + static_cast<double>(c[t]);
     }
   }
   return ok;
 }
 
-// 8 output elements from fp64 values, as 16-byte stores.
-template <typename T>
-__device__ __forceinline__ void store8(T* p, const double (&x)[8]) {
+// 4 output elements from fp64 values (fp32: 16 bytes, bf16: 8 bytes).  STREAM: a global output
+// written once (nontemporal); otherwise plain stores (LDS).
+template <typename T, bool STREAM>
+__device__ __forceinline__ void store4(T* p, const double (&x)[4]) {
   if constexpr (sizeof(T) == 4) {
-    float4 a, b;
-    a.x = static_cast<float>(x[0]); a.y = static_cast<float>(x[1]);
-    a.z = static_cast<float>(x[2]); a.w = static_cast<float>(x[3]);
-    b.x = static_cast<float>(x[4]); b.y = static_cast<float>(x[5]);
-    b.z = static_cast<float>(x[6]); b.w = static_cast<float>(x[7]);
-    reinterpret_cast<float4*>(p)[0] = a;
-    reinterpret_cast<float4*>(p)[1] = b;
+    uint4 a;
+    a.x = __float_as_uint(static_cast<float>(x[0]));
+    a.y = __float_as_uint(static_cast<float>(x[1]));
+    a.z = __float_as_uint(static_cast<float>(x[2]));
+    a.w = __float_as_uint(static_cast<float>(x[3]));
+    if (STREAM)
+      st_stream(p, a);
+    else
+      *reinterpret_cast<uint4*>(p) = a;
   } else {
-    uint4 w;
+    uint2 w;
     w.x = static_cast<uint32_t>(bf16_from_double(x[0])) | (static_cast<uint32_t>(bf16_from_double(x[1])) << 16);
     w.y = static_cast<uint32_t>(bf16_from_double(x[2])) | (static_cast<uint32_t>(bf16_from_double(x[3])) << 16);
-    w.z = static_cast<uint32_t>(bf16_from_double(x[4])) | (static_cast<uint32_t>(bf16_from_double(x[5])) << 16);
-    w.w = static_cast<uint32_t>(bf16_from_double(x[6])) | (static_cast<uint32_t>(bf16_from_double(x[7])) << 16);
-    *reinterpret_cast<uint4*>(p) = w;
+    *reinterpret_cast<uint2*>(p) = w;
   }
 }
 
-// One thread per vector, reconstruction or residual (minuend - reconstruction), no permutation.
+// Two lanes per vector, reconstruction or residual (minuend - reconstruction), no permutation.
 template <typename T, typename TM>
 __global__ __launch_bounds__(256) void dequant_rows8(int64_t M, int64_t vpr, int64_t ncv, DequantBooks b,
                                                      const TM* __restrict__ minuend, int64_t ld_min,
                                                      T* __restrict__ out, int64_t ld_out) {
-  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (e >= M * vpr) return;
+  const int64_t e2 = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e2 >= 2 * M * vpr) return;
+  const int h = static_cast<int>(e2 & 1);
+  const int64_t e = e2 >> 1;
   const int64_t r = e / vpr;
   const int64_t g = e - r * vpr;
-  const int32_t q0 = b.q[0][r * b.ldq_base + g];
-  float m[8];
+  const int32_t q0 = ld_stream_i32(b.q[0] + r * b.ldq_base + g);
+  float m[4];
   if (minuend) {
     if constexpr (sizeof(TM) == 4) {
-      const float4* p = reinterpret_cast<const float4*>(minuend + r * ld_min + g * 8);
-      const float4 a = p[0], c = p[1];
-      m[0] = a.x; m[1] = a.y; m[2] = a.z; m[3] = a.w;
-      m[4] = c.x; m[5] = c.y; m[6] = c.z; m[7] = c.w;
+      const uint4 a = ld_stream(minuend + r * ld_min + g * 8 + 4 * h);
+      m[0] = __uint_as_float(a.x); m[1] = __uint_as_float(a.y); m[2] = __uint_as_float(a.z); m[3] = __uint_as_float(a.w);
     } else {
-      const uint4 w = *reinterpret_cast<const uint4*>(minuend + r * ld_min + g * 8);
-      const uint32_t u[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        m[2 * k] = __uint_as_float(u[k] << 16);
-        m[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
-      }
+      const uint2 w = ld_stream8(minuend + r * ld_min + g * 8 + 4 * h);
+      m[0] = __uint_as_float(w.x << 16);
+      m[1] = __uint_as_float(w.x & 0xffff0000u);
+      m[2] = __uint_as_float(w.y << 16);
+      m[3] = __uint_as_float(w.y & 0xffff0000u);
     }
   }
   const bool in = q0 >= 0 && q0 < b.K[0];
-  float c0[8];
-  load_cw8(b.C[0], b.type[0], in ? q0 : 0, c0);
-  double v[8];
-  const bool ok = recon8(b, r, g, ncv, in, c0, v);
-  double x[8];
+  float c0[4];
+  load_cw4(b.C[0], b.type[0], in ? q0 : 0, h, c0);
+  double v[4];
+  const bool ok = recon4(b, r, g, h, ncv, in, c0, v);
+  double x[4];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
+  for (int t = 0; t < 4; ++t) {
     x[t] = ok ? v[t] : __builtin_nan("");
     if (minuend) x[t] = static_cast<double>(m[t]) - x[t];
   }
-  store8<T>(out + r * ld_out + g * 8, x);
+  store4<T, true>(out + r * ld_out + g * 8 + 4 * h, x);
 }
 
-// Reconstruction in original channel order: the row is rebuilt in LDS (kU vectors per thread and
-// round, all their code and codeword loads issued first), then written through the inverse
-// permutation in 16-byte segments.
+// Reconstruction in original channel order.  Persistent blocks keep the inverse permutation in LDS
+// (16-bit column indices, read from memory once per block) and walk rows r = block, block + grid,
+// ...: each row is rebuilt in LDS (kU vectors per lane pair and round), then written through the
+// inverse permutation in 16-byte segments.
 template <typename T>
-__global__ __launch_bounds__(256) void dequant_rows_perm8(int64_t n_cols, int64_t ncv, DequantBooks b,
+__global__ __launch_bounds__(256) void dequant_rows_perm8(int64_t M, int64_t n_cols, int64_t ncv, DequantBooks b,
                                                           const int32_t* __restrict__ inv, T* __restrict__ out,
                                                           int64_t ld_out) {
   extern __shared__ unsigned char smem[];
   T* row = reinterpret_cast<T*>(smem);
-  const int64_t r = blockIdx.x;
+  uint16_t* src = reinterpret_cast<uint16_t*>(smem + ((n_cols * sizeof(T) + 15) & ~static_cast<int64_t>(15)));
+  for (int64_t j = threadIdx.x; j < n_cols; j += 256) {
+    const int32_t sj = inv[j];
+    src[j] = (sj >= 0 && sj < n_cols) ? static_cast<uint16_t>(sj) : static_cast<uint16_t>(0xffff);  // 0xffff: zero
+  }
   const int64_t vpr = n_cols / 8;
-  for (int64_t g0 = threadIdx.x; g0 < vpr; g0 += 256 * kU) {
-    int32_t q[kU];
-    bool live[kU], in[kU];
+  const int h = threadIdx.x & 1;
+  const int pair = threadIdx.x >> 1;
+  constexpr int V = 16 / sizeof(T);
+  for (int64_t r = blockIdx.x; r < M; r += gridDim.x) {
+    for (int64_t g0 = pair; g0 < vpr; g0 += 128 * kU) {
+      int32_t q[kU];
+      bool live[kU], in[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int64_t g = g0 + 256 * u;
-      live[u] = g < vpr;
-      q[u] = live[u] ? b.q[0][r * b.ldq_base + g] : 0;
-    }
-    float c[kU][8];
+      for (int u = 0; u < kU; ++u) {
+        const int64_t g = g0 + 128 * u;
+        live[u] = g < vpr;
+        q[u] = live[u] ? ld_stream_i32(b.q[0] + r * b.ldq_base + g) : 0;
+      }
+      float c[kU][4];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      in[u] = q[u] >= 0 && q[u] < b.K[0];
-      load_cw8(b.C[0], b.type[0], (live[u] && in[u]) ? q[u] : 0, c[u]);
-    }
+      for (int u = 0; u < kU; ++u) {
+        in[u] = q[u] >= 0 && q[u] < b.K[0];
+        load_cw4(b.C[0], b.type[0], (live[u] && in[u]) ? q[u] : 0, h, c[u]);
+      }
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int64_t g = g0 + 256 * u;
-      if (!live[u]) continue;
-      double v[8];
-      const bool ok = recon8(b, r, g, ncv, in[u], c[u], v);
+      for (int u = 0; u < kU; ++u) {
+        const int64_t g = g0 + 128 * u;
+        if (!live[u]) continue;
+        double v[4];
+        const bool ok = recon4(b, r, g, h, ncv, in[u], c[u], v);
 #pragma unroll
-      for (int t = 0; t < 8; ++t) v[t] = ok ? v[t] : __builtin_nan("");
-      if constexpr (sizeof(T) == 4) {
-        uint4 a, d2;
-        a.x = __float_as_uint(static_cast<float>(v[0])); a.y = __float_as_uint(static_cast<float>(v[1]));
-        a.z = __float_as_uint(static_cast<float>(v[2])); a.w = __float_as_uint(static_cast<float>(v[3]));
-        d2.x = __float_as_uint(static_cast<float>(v[4])); d2.y = __float_as_uint(static_cast<float>(v[5]));
-        d2.z = __float_as_uint(static_cast<float>(v[6])); d2.w = __float_as_uint(static_cast<float>(v[7]));
-        reinterpret_cast<uint4*>(row + g * 8)[0] = a;
-        reinterpret_cast<uint4*>(row + g * 8)[1] = d2;
-      } else {
-        store8<T>(row + g * 8, v);
+        for (int t = 0; t < 4; ++t) v[t] = ok ? v[t] : __builtin_nan("");
+        store4<T, false>(row + g * 8 + 4 * h, v);
       }
     }
-  }
-  __syncthreads();
-  T* ro = out + r * ld_out;
-  constexpr int V = 16 / sizeof(T);
-  for (int64_t c = threadIdx.x; c < n_cols / V; c += 256) {
-    T seg[V];
+    __syncthreads();  // the row (and, first time round, the permutation) is in LDS
+    T* ro = out + r * ld_out;
+    for (int64_t c = threadIdx.x; c < n_cols / V; c += 256) {
+      T seg[V];
 #pragma unroll
-    for (int q = 0; q < V; q += 4) {
-      const int4 s4 = reinterpret_cast<const int4*>(inv)[(c * V + q) / 4];
-      const int32_t s[4] = {s4.x, s4.y, s4.z, s4.w};
-#pragma unroll
-      for (int u = 0; u < 4; ++u) seg[q + u] = (s[u] >= 0 && s[u] < n_cols) ? row[s[u]] : T(0);
+      for (int u = 0; u < V; ++u) {
+        const uint32_t sj = src[c * V + u];
+        seg[u] = (sj < static_cast<uint32_t>(n_cols)) ? row[sj] : T(0);
+      }
+      st_stream(reinterpret_cast<uint4*>(ro) + c, *reinterpret_cast<const uint4*>(seg));
     }
-    reinterpret_cast<uint4*>(ro)[c] = *reinterpret_cast<const uint4*>(seg);
+    __syncthreads();  // the row buffer is rewritten by the next row
   }
 }
 
@@ -355,7 +350,7 @@ hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, cons
     fast = (reinterpret_cast<uintptr_t>(minuend) % 16 == 0) && ((ld_min * msize) % 16 == 0);
   }
   if (fast && !inv_perm) {
-    const unsigned grid = static_cast<unsigned>(cdiv(nvec, 256));
+    const unsigned grid = static_cast<unsigned>(cdiv(2 * nvec, 256));
     const int64_t vpr = n_cols / 8;
 #define CRVQ_DQ8(T, TM)                                                                                       \
   hipLaunchKernelGGL((dequant_rows8<T, TM>), dim3(grid), dim3(256), 0, stream, M, vpr, ncv, books,          \
@@ -368,15 +363,17 @@ hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, cons
 #undef CRVQ_DQ8
     return hipGetLastError();
   }
-  if (fast && inv_perm && (reinterpret_cast<uintptr_t>(inv_perm) % 16 == 0) && n_cols % (16 / esize) == 0 &&
-      static_cast<size_t>(n_cols) * esize <= 64 * 1024) {
-    const size_t lds = static_cast<size_t>(n_cols) * esize;
+  const size_t lds8 = ((static_cast<size_t>(n_cols) * esize + 15) & ~static_cast<size_t>(15)) + 2 * n_cols;
+  if (fast && inv_perm && n_cols % (16 / esize) == 0 && n_cols < 65535 && lds8 <= 64 * 1024) {
+    // persistent: about as many blocks as fit on the device at once, each walking many rows
+    const int64_t per_cu = static_cast<int64_t>((160 * 1024) / lds8) > 8 ? 8 : static_cast<int64_t>((160 * 1024) / lds8);
+    const int64_t grid = M < 256 * per_cu ? M : 256 * per_cu;
     if (esize == 4)
-      hipLaunchKernelGGL(dequant_rows_perm8<uint32_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream, n_cols,
-                         ncv, books, inv_perm, static_cast<uint32_t*>(out), ld_out);
+      hipLaunchKernelGGL(dequant_rows_perm8<uint32_t>, dim3(static_cast<unsigned>(grid)), dim3(256), lds8, stream, M,
+                         n_cols, ncv, books, inv_perm, static_cast<uint32_t*>(out), ld_out);
     else
-      hipLaunchKernelGGL(dequant_rows_perm8<uint16_t>, dim3(static_cast<unsigned>(M)), dim3(256), lds, stream, n_cols,
-                         ncv, books, inv_perm, static_cast<uint16_t*>(out), ld_out);
+      hipLaunchKernelGGL(dequant_rows_perm8<uint16_t>, dim3(static_cast<unsigned>(grid)), dim3(256), lds8, stream, M,
+                         n_cols, ncv, books, inv_perm, static_cast<uint16_t*>(out), ld_out);
     return hipGetLastError();
   }
   if (!inv_perm) {

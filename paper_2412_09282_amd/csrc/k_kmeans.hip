@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void radix_hist(const int* __restrict__ keys, 
 #pragma unroll
   for (int bt = 0; bt < kBatches; ++bt) {  // every load issued before the first is counted
     const int64_t idx = base + bt * 64 + lane;
-    key[bt] = (idx < n) ? keys[idx] : -1;
+    key[bt] = (idx < n) ? ld_stream_i32(keys + idx) : -1;
   }
 #pragma unroll
   for (int bt = 0; bt < kBatches; ++bt) {
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(256) void radix_scatter(const int* __restrict__ key
 #pragma unroll
   for (int bt = 0; bt < kBatches; ++bt) {
     const int64_t idx = base + bt * 64 + lane;
-    key[bt] = (idx < n) ? keys_in[idx] : -1;
+    key[bt] = (idx < n) ? ld_stream_i32(keys_in + idx) : -1;
     const bool valid = (idx < n) && (pass != 0 || (key[bt] >= 0 && key[bt] < K));
     dig[bt] = valid ? (key[bt] >> shift) & 255 : -1;
     peer[bt] = peer_mask(valid, valid ? dig[bt] : 0);
@@ -594,8 +594,8 @@ __global__ __launch_bounds__(256) void bucket_partial8(RowSrc src, const int* __
     for (int bt = 0; bt < kRoundBatches; ++bt) {
       const int64_t idx = base + (w * kRoundBatches + bt) * 64 + lane;
       const bool live = idx < b1;
-      dig[bt] = live ? (keys[idx] & 255) : -1;
-      vid[bt] = live ? vals[idx] : -1;
+      dig[bt] = live ? (ld_stream_i32(keys + idx) & 255) : -1;
+      vid[bt] = live ? ld_stream_i32(vals + idx) : -1;
     }
     round_bucket_sort(dig, L, &pos);
     float4 v[kRoundBatches][2];

@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256) void gather_cols_lds_v(const T* __restrict__ i
   for (int64_t c0 = threadIdx.x; c0 < nv; c0 += 256 * U) {
     uint4 v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = (c0 + u * 256 < nv) ? ri[c0 + u * 256] : make_uint4(0, 0, 0, 0);
+    for (int u = 0; u < U; ++u) v[u] = (c0 + u * 256 < nv) ? ld_stream(ri + c0 + u * 256) : make_uint4(0, 0, 0, 0);
 #pragma unroll
     for (int u = 0; u < U; ++u)
       if (c0 + u * 256 < nv) reinterpret_cast<uint4*>(row)[c0 + u * 256] = v[u];
@@ -111,7 +111,7 @@ __global__ __launch_bounds__(256) void gather_cols_lds_v(const T* __restrict__ i
 #pragma unroll
       for (int u = 0; u < 4; ++u) seg[q + u] = (s[u] >= 0 && s[u] < N) ? row[s[u]] : T(0);
     }
-    ro[c] = *reinterpret_cast<const uint4*>(seg);
+    st_stream(ro + c, *reinterpret_cast<const uint4*>(seg));
   }
 }
 

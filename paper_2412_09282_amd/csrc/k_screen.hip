@@ -212,11 +212,13 @@ __device__ __forceinline__ void list_merge_xor(double (&LD)[NB], int (&LK)[NB], 
 // ------------------------------------------------------------------------------------------------
 // 1. codebook repack
 // ------------------------------------------------------------------------------------------------
+// (every prep kernel also clears the rescue counter of the call: thread 0 of block 0)
 template <int KS>
 __global__ __launch_bounds__(256) void prep_codebook(const void* __restrict__ C, int ct, int64_t K, int d,
                                                      int64_t tiles, float* __restrict__ apack,
-                                                     float* __restrict__ cnp) {
+                                                     float* __restrict__ cnp, int* __restrict__ rcount) {
   int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (k == 0) *rcount = 0;
   if (k >= tiles * 16) return;
   float c[16];
 #pragma unroll
@@ -371,8 +373,9 @@ struct SplitOps {
 // Split-bf16 codebook pack: per codeword 8 bf16 of c1 then 8 of c2 (zero past d), and ||c||^2.
 __global__ __launch_bounds__(256) void prep_codebook_split(const void* __restrict__ C, int ct, int64_t K, int d,
                                                            int64_t tiles, uint16_t* __restrict__ apack,
-                                                           float* __restrict__ cnp) {
+                                                           float* __restrict__ cnp, int* __restrict__ rcount) {
   const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (k == 0) *rcount = 0;
   if (k >= tiles * 16) return;
   float c[8];
 #pragma unroll
@@ -651,6 +654,7 @@ typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f16v __attribute__((ext_vector_type(16)));
 
 constexpr int kS32Tile = 32;         // codewords per tile
+constexpr int64_t kRescueBlocks = 1024;  // persistent grid of the exact rescue
 constexpr int kS32TileHalves = 768;  // packed fp16 per tile: c1, c2, N terms, 32 x 8 each
 constexpr int kS32MaxParts = 256;    // partial maxima of the codebook scale reduction
 
@@ -701,7 +705,8 @@ __device__ __forceinline__ float s32_alpha(float mx) {
 // Every block folds the partial maxima, block 0 publishes alpha; then thread k packs codeword k.
 __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict__ C, int ct, int64_t K, int d,
                                                          int64_t tiles, const float* __restrict__ part, int nparts,
-                                                         uint16_t* __restrict__ apack, float* __restrict__ alpha_out) {
+                                                         uint16_t* __restrict__ apack, float* __restrict__ alpha_out,
+                                                         int* __restrict__ rcount) {
   __shared__ float sh[256];
   sh[threadIdx.x] = (static_cast<int>(threadIdx.x) < nparts) ? part[threadIdx.x] : 0.0f;
   __syncthreads();
@@ -710,7 +715,10 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
     __syncthreads();
   }
   const float alpha = s32_alpha(sh[0]);
-  if (blockIdx.x == 0 && threadIdx.x == 0) alpha_out[0] = alpha;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    alpha_out[0] = alpha;
+    *rcount = 0;
+  }
   const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (k >= tiles * kS32Tile) return;
   float c[8];
@@ -939,11 +947,11 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
 }
 
 // ------------------------------------------------------------------------------------------------
-// 4. merge the splits, certify, rescue uncertain rows exactly, emit
+// 4. merge the splits, certify, emit; rescue the uncertain rows exactly
 // ------------------------------------------------------------------------------------------------
-// One thread per row.  Top-1: merge the splits' exact winners.  Top-B: re-score in fp64 the four
-// codewords of every kept tile of every lane group and split.  Then order by (D, k) and certify
-// against the screen bound.
+// Finalize, one thread per row.  Top-1: merge the splits' exact winners.  Top-B: re-score in fp64
+// the four codewords of every kept tile of every lane group and split.  Then order by (D, k) and
+// certify against the screen bound.
 // Screen error bound (certification): delta = acc_ulps 2^-24 (R^2 + 2 ||x|| R) + split_coef ||x|| R
 // + abs_coef (||x|| + R + 1), with R = ||x|| + sqrt(D_top).  A scaled screen (alpha != null) stores
 // alpha^2 s: its bound values are divided by alpha^2 and the fp16 underflow terms
@@ -955,19 +963,37 @@ struct ScreenBound {
   const float* alpha;
 };
 
+// Writes a row's result: its code and distance (top-1) or its sorted (D, k) list, padded with
+// (+inf, -1) past the codebook size.
+template <int NB>
+__device__ __forceinline__ void emit_row(int64_t row, const double (&ED)[NB], const int (&EK)[NB], int top, int need,
+                                         int32_t* codes, float* dist, double* rowD, int* rowK) {
+  if (codes) {
+    codes[row] = EK[0];
+    if (dist) dist[row] = static_cast<float>(ED[0]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      if (j < top) {
+        const bool real = j < need;
+        rowD[row * top + j] = real ? ED[j] : __builtin_inf();
+        rowK[row * top + j] = real ? EK[j] : -1;
+      }
+    }
+  }
+}
+
+// One thread per row; rows that fail the certification are appended to the rescue list.
 template <int KS, int NB>
 __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top, const int* __restrict__ pT,
                                                        const float* __restrict__ pR, const double* __restrict__ pD,
                                                        const int* __restrict__ pK, const double* __restrict__ xn2a,
                                                        const void* __restrict__ C, int ct, int64_t K,
-                                                       ScreenBound bound, int32_t* __restrict__ codes,
+                                                       ScreenBound bound, int* __restrict__ rcount,
+                                                       int* __restrict__ rlist, int32_t* __restrict__ codes,
                                                        float* __restrict__ dist, double* __restrict__ rowD,
                                                        int* __restrict__ rowK) {
   constexpr int DM = 4 * KS;  // dimensions this instantiation covers (d <= DM)
-  __shared__ int scan[256];
-  __shared__ int flagged[256];
-  __shared__ double sD[128 * NB];
-  __shared__ int sK[128 * NB];
   const int tid = threadIdx.x;
   const int64_t n = src.n;
   const int d = src.d;
@@ -1058,39 +1084,29 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     }
   }
 
-  auto emit = [&](int64_t row, const double (&ED)[NB], const int (&EK)[NB]) {
-    if (codes) {
-      codes[row] = EK[0];
-      if (dist) dist[row] = static_cast<float>(ED[0]);
-    } else {
-#pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        if (j < top) {
-          const bool real = j < need;
-          rowD[row * top + j] = real ? ED[j] : __builtin_inf();
-          rowK[row * top + j] = real ? EK[j] : -1;
-        }
-      }
-    }
-  };
-  if (valid && certain) emit(i, LD, LK);
+  if (valid && certain) emit_row<NB>(i, LD, LK, top, need, codes, dist, rowD, rowK);
+  // an uncertain row goes to the rescue list (its order there does not affect any result)
+  if (valid && !certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
+}
 
-  // compaction of the uncertain rows of this block (inclusive scan of the flags)
-  const int flag = (valid && !certain) ? 1 : 0;
-  scan[tid] = flag;
-  __syncthreads();
-  for (int off = 1; off < 256; off <<= 1) {
-    int v = (tid >= off) ? scan[tid - off] : 0;
-    __syncthreads();
-    scan[tid] += v;
-    __syncthreads();
-  }
-  if (flag) flagged[scan[tid] - 1] = tid;
-  const int nflag = scan[255];
-  __syncthreads();
-
-  for (int f = 0; f < nflag; ++f) {
-    const int64_t row = static_cast<int64_t>(blockIdx.x) * 256 + flagged[f];
+// Exact fp64 search of every listed row over the whole codebook.  Persistent: block b takes rows
+// b, b + grid, ... of the list; its 256 threads split the codebook (8 codewords per thread and
+// round, all loaded before any is scored) and the per-thread (D, k) lists are merged in LDS.
+template <int KS, int NB>
+__global__ __launch_bounds__(256) void rescue_kernel(RowSrc src, int top, const void* __restrict__ C, int ct, int64_t K,
+                                                     const int* __restrict__ rcount, const int* __restrict__ rlist,
+                                                     int32_t* __restrict__ codes, float* __restrict__ dist,
+                                                     double* __restrict__ rowD, int* __restrict__ rowK) {
+  constexpr int DM = 4 * KS;
+  constexpr int kRU = 8;
+  __shared__ double sD[128 * NB];
+  __shared__ int sK[128 * NB];
+  const int tid = threadIdx.x;
+  const int d = src.d;
+  const int need = static_cast<int>((top < K) ? top : K);
+  const int count = *rcount;
+  for (int f = blockIdx.x; f < count; f += gridDim.x) {
+    const int64_t row = rlist[f];
     double xr[DM];
     load_row_exact<DM>(src, row, true, xr);
     double TD[NB];
@@ -1100,16 +1116,15 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
       TD[j] = __builtin_inf();
       TK[j] = INT_MAX;
     }
-    // four codewords per thread and round, loaded before any of them is scored, so the loads overlap
-    for (int64_t k0 = tid; k0 < K; k0 += 4 * 256) {
-      float cw[4][DM];
+    for (int64_t k0 = tid; k0 < K; k0 += kRU * 256) {
+      float cw[kRU][DM];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < kRU; ++u) {
         const int64_t k = k0 + u * 256;
         load_codeword<DM>(C, ct, k, d, k < K, cw[u]);
       }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < kRU; ++u) {
         const int64_t k = k0 + u * 256;
         if (k < K) {
           double acc = 0.0;
@@ -1145,8 +1160,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
       }
       __syncthreads();
     }
-    if (tid == 0) emit(row, TD, TK);
-    __syncthreads();
+    if (tid == 0) emit_row<NB>(row, TD, TK, top, need, codes, dist, rowD, rowK);
   }
 }
 
@@ -1243,7 +1257,11 @@ hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K
                              const ScreenWs& w, const ScreenBound& bound, int32_t* codes, float* dist, double* rowD,
                              int* rowK, hipStream_t stream) {
   hipLaunchKernelGGL((finalize_kernel<KS, NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
-                     src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, codes, dist, rowD, rowK);
+                     src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
+                     dist, rowD, rowK);
+  const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
+  hipLaunchKernelGGL((rescue_kernel<KS, NB>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C, ct,
+                     K, w.rcount, w.rlist, codes, dist, rowD, rowK);
   return hipGetLastError();
 }
 
@@ -1347,6 +1365,8 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
     w.smax = nullptr;
   }
   w.pR = ws.take<float>(static_cast<size_t>(p.splits) * n_rows);
+  w.rcount = ws.take<int>(1);
+  w.rlist = ws.take<int>(static_cast<size_t>(n_rows));
   if (p.nb == 1) {
     w.pT = nullptr;
     w.pD = ws.take<double>(static_cast<size_t>(p.splits) * n_rows);
@@ -1375,7 +1395,7 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     uint16_t* ap = reinterpret_cast<uint16_t*>(w.apack);
     hipLaunchKernelGGL(cb_absmax_partial, dim3(nparts), dim3(256), 0, stream, C, ct, count, w.smax);
     hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
-                       stream, C, ct, K, src.d, p.tiles, w.smax, nparts, ap, alpha);
+                       stream, C, ct, K, src.d, p.tiles, w.smax, nparts, ap, alpha, w.rcount);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
     if (p.cb == 4)
@@ -1391,12 +1411,12 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
   const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
   if (p.split) {
     hipLaunchKernelGGL(prep_codebook_split, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles,
-                       reinterpret_cast<uint16_t*>(w.apack), w.cnp);
+                       reinterpret_cast<uint16_t*>(w.apack), w.cnp, w.rcount);
   } else {
     switch (p.ks) {
-      case 1: hipLaunchKernelGGL(prep_codebook<1>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
-      case 2: hipLaunchKernelGGL(prep_codebook<2>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
-      default: hipLaunchKernelGGL(prep_codebook<4>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp); break;
+      case 1: hipLaunchKernelGGL(prep_codebook<1>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp, w.rcount); break;
+      case 2: hipLaunchKernelGGL(prep_codebook<2>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp, w.rcount); break;
+      default: hipLaunchKernelGGL(prep_codebook<4>, dim3(prep_grid), dim3(256), 0, stream, C, ct, K, src.d, p.tiles, w.apack, w.cnp, w.rcount); break;
     }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -818,16 +818,21 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   const int64_t t0 = static_cast<int64_t>(split) * tps;
   const int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
   if (t0 < t1) {
-    // lanes 0-31 read c1 twice, lanes 32-63 read c2 and the N terms: two 16-byte loads per lane
-    auto load = [&](int64_t T, h8& a1, h8& a2) {
-      const uint16_t* base = apack + T * kS32TileHalves + j * 8;
-      a1 = *reinterpret_cast<const h8*>(base + h * 256);
-      a2 = *reinterpret_cast<const h8*>(base + h * 512);
+    // Codebook tiles come in through a buffer resource: the per-lane byte offset is fixed, the
+    // tile offset is a scalar, so a tile costs no vector address arithmetic.  Lanes 0-31 read c1
+    // twice, lanes 32-63 read c2 and the N terms.  (Tile indices fit in 32 bits.)
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(apack), 0, static_cast<int>(tiles * kS32TileHalves * 2), 0x00020000);
+    const int voff1 = (j * 8 + h * 256) * 2, voff2 = (j * 8 + h * 512) * 2;
+    const int T0 = static_cast<int>(t0), T1 = static_cast<int>(t1);
+    auto load = [&](int T, h8& a1, h8& a2) {
+      a1 = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rs, voff1, T * (kS32TileHalves * 2), 0));
+      a2 = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rs, voff2, T * (kS32TileHalves * 2), 0));
     };
     // Software-pipelined over the column blocks: the MFMA pair of block cb is issued before the
     // minimum of block cb - 1 is folded (a depth-3 v_min3 tree), so a wave keeps the matrix core
-    // and the VALU busy at the same time.
-    auto tile = [&](const h8& a1, const h8& a2) {
+    // and the VALU busy at the same time.  The first tile of a chunk starts its minimum afresh.
+    auto tile = [&](const h8& a1, const h8& a2, bool first) {
       f16v acc[2];
 #pragma unroll
       for (int cb = 0; cb <= CB; ++cb) {
@@ -836,41 +841,42 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
           acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, b1[cb], z, 0, 0, 0);
           acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b2[cb], acc[cb & 1], 0, 0, 0);
         }
-        if (cb > 0) cm[cb - 1] = min_fold16(cm[cb - 1], acc[(cb - 1) & 1]);
+        if (cb > 0) {
+          const f16v& a = acc[(cb - 1) & 1];
+          cm[cb - 1] = first ? min_fold16(a[0], a) : min_fold16(cm[cb - 1], a);
+        }
         if (CRVQ_S32_SCHED) {
           if (cb < CB) __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
           if (cb > 0) __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
         }
       }
     };
-    auto fold = [&](int64_t T0) {
-      const int Ci = static_cast<int>(T0);
+    auto fold = [&](int Ci) {
 #pragma unroll
       for (int cb = 0; cb < CB; ++cb) {
         rest[cb] = __builtin_amdgcn_fmed3f(m[cb], rest[cb], cm[cb]);
         const bool lt = cm[cb] < m[cb];
         m[cb] = fminf(m[cb], cm[cb]);
         id[cb] = lt ? Ci : id[cb];
-        cm[cb] = __builtin_inff();
       }
     };
     // Two tiles per iteration from two register sets; each set is refilled right after its MFMAs,
     // one iteration ahead of its next use.
     static_assert(NC == 1 || NC == 2, "chunks of one or two tiles");
     h8 qa1, qa2, qb1, qb2;
-    load(t0, qa1, qa2);
-    load((t0 + 1 < t1) ? t0 + 1 : t1 - 1, qb1, qb2);
-    int64_t T = t0;
-    for (; T + 2 <= t1; T += 2) {
-      tile(qa1, qa2);
+    load(T0, qa1, qa2);
+    load((T0 + 1 < T1) ? T0 + 1 : T1 - 1, qb1, qb2);
+    int T = T0;
+    for (; T + 2 <= T1; T += 2) {
+      tile(qa1, qa2, true);
       if (NC == 1) fold(T);
-      load((T + 2 < t1) ? T + 2 : t1 - 1, qa1, qa2);
-      tile(qb1, qb2);
+      load((T + 2 < T1) ? T + 2 : T1 - 1, qa1, qa2);
+      tile(qb1, qb2, NC == 1);
       fold(NC == 1 ? T + 1 : T);
-      load((T + 3 < t1) ? T + 3 : t1 - 1, qb1, qb2);
+      load((T + 3 < T1) ? T + 3 : T1 - 1, qb1, qb2);
     }
-    if (T < t1) {
-      tile(qa1, qa2);
+    if (T < T1) {
+      tile(qa1, qa2, true);
       fold(T);
     }
   }

@@ -3,10 +3,11 @@
 // kernels produce the residual E = minuend - reconstruction (Alg. 1 ComputeError / Update) and the
 // reverse reordering back to the original channel order (Sec. 4.3, Fig. 3 right).
 //
-// One thread per d-vector: its codes are read once, each codeword as one contiguous piece, every
-// element summed in fp64 in book order and rounded once.  With a permutation the block rebuilds a
-// whole row in LDS and writes it out in original channel order through the inverse permutation,
-// 16 bytes per thread and store, so codebook reads and output writes stay coalesced.
+// Every element is summed in fp64 in book order and rounded once.  d = 8 (the common case): two
+// lanes per vector, each gathering and writing one 16-byte half, codes and outputs streamed with
+// nontemporal accesses; with a permutation, persistent blocks rebuild one row at a time in LDS and
+// write it out in original channel order through the inverse permutation (kept in LDS), 16 bytes
+// per store.  Other d: one thread per vector with the same arithmetic.
 #include "crvq_internal.h"
 
 namespace crvq {

@@ -6,9 +6,11 @@
 // untouched; codes outside [0, K) belong to no cluster.
 // * K <= 256 (small_k_partial): blocks walk contiguous vector ranges; each round of 1024 codes is
 //   bucket-sorted in LDS and thread k adds the members of code k.
-// * K > 256 (bucket_partial): one stable radix pass (per-tile ballot counting, device-wide scan,
-//   stable scatter -- no atomics) groups the vectors by the high byte of their code; each bucket is
-//   then reduced like a small codebook on the low byte.
+// * K > 256 (bucket_partial8 / bucket_partial): one stable radix pass (per-tile ballot counting,
+//   device-wide scan, stable scatter -- no atomics) groups the vectors by the high byte of their
+//   code; each bucket is then reduced like a small codebook on the low byte, its member vectors
+//   gathered a round at a time into LDS.  Buckets are cut into chunks taken in chunk-major order,
+//   so the blocks in flight read about the same index range of every bucket.
 #include "crvq_internal.h"
 
 namespace crvq {

@@ -3,20 +3,25 @@
 //
 // Distances are split as ||x - c||^2 = ||x||^2 + s(c),  s(c) = ||c||^2 - 2 x.c.
 //
-// 1. prep: the codebook is repacked into the fp32 MFMA A-operand order, 16 codewords per tile,
-//    with ||c||^2 per codeword (+inf for padding) as the accumulator input.
-// 2. screen: every wave keeps 16*CB rows resident as the MFMA B operand (scaled by -2) and streams
-//    all codeword tiles of its codebook split.  v_mfma_f32_16x16x4_f32 leaves each lane 4 values of
-//    s for one row; the lane reduces them to the tile minimum and keeps, per row, the NB tiles with
-//    the smallest minimum and the smallest minimum of every other tile ("rest").  Nothing of the
-//    N x K distance matrix leaves the registers; per row only the kept tile ids and rest are written.
-// 3. exact (finalize, one thread per row): the codewords of the kept tiles of all lane groups and
-//    codebook splits are re-scored in fp64 with the same direct form as the definition
-//    (sum_t (x_t - c_t)^2, t ascending) and ordered by (D, k).
+// 1. prep: the codebook is repacked into MFMA A-operand order with ||c||^2 (+inf for padding).
+// 2. screen: every wave keeps its rows resident as the MFMA B operand (-2x) and streams all codeword
+//    tiles of its codebook split; the lanes reduce the s values they receive to running minima and
+//    keep, per row, the best tiles (or chunks of tiles) and the smallest minimum of everything else
+//    ("rest").  Nothing of the N x K distance matrix leaves the registers.  Three operand forms:
+//    * d <= 8, top-1 over long codebooks: 32 x 32 tiles, operands split into two fp16 terms under a
+//      power-of-two codebook scale, two v_mfma_f32_32x32x16_f16 per tile (screen32_kernel);
+//    * d <= 8 otherwise: 16 x 16 tiles, operands split into two bf16 terms, one
+//      v_mfma_f32_16x16x32_bf16 per tile (SplitOps);
+//    * d <= 16: fp32 operands, v_mfma_f32_16x16x4_f32 (F32Ops).
+//    Top-1 screens re-score the winning lane group's codewords of the kept tile or chunk exactly in
+//    fp64 before leaving; top-B screens hand the kept tile ids to the finalize.
+// 3. finalize (one thread per row): merge the codebook splits (top-B: re-score the kept tiles in
+//    fp64 in the definition's direct form, sum_t (x_t - c_t)^2 with t ascending) and order by (D, k).
 // 4. certify / rescue: with R = ||x|| + sqrt(D_top), every codeword that could beat the kept ones
-//    has ||c|| <= R, hence a screen error below delta(R); if rest + ||x||^2 - delta > D_top the kept
-//    list is provably the exact answer, otherwise the row is re-searched exactly over the whole
-//    codebook in fp64 by its workgroup.  Codes therefore equal the fp64 definition's, ties included.
+//    has ||c|| <= R, hence a screen error below delta(R) (accumulation, split remainder, underflow);
+//    if rest + ||x||^2 - delta > D_top the kept list is provably the exact answer, otherwise the
+//    row is appended to a list that the rescue kernel re-searches exactly over the whole codebook
+//    in fp64.  Codes therefore equal the fp64 definition's, ties included.
 #include "crvq_internal.h"
 
 #include <climits>

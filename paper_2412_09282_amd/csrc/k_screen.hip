@@ -56,6 +56,12 @@
 #ifndef CRVQ_S32_CHUNK
 #define CRVQ_S32_CHUNK 2  // 32-codeword tiles per tracking chunk (1 or 2)
 #endif
+#ifndef CRVQ_DEBUG_RESCUE
+#define CRVQ_DEBUG_RESCUE 0
+#endif
+#ifndef CRVQ_RESCUE_FILTER
+#define CRVQ_RESCUE_FILTER 1  // top-1 rescue: batched rows with a bounded fp32 filter before fp64
+#endif
 #ifndef CRVQ_S32_SCHED
 #define CRVQ_S32_SCHED 1  // pin the MFMA / VALU interleave of the 32 x 32 screen
 #endif
@@ -1095,9 +1101,169 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     }
   }
 
-  if (valid && certain) emit_row<NB>(i, LD, LK, top, need, codes, dist, rowD, rowK);
-  // an uncertain row goes to the rescue list (its order there does not affect any result)
+  // An uncertain row is written with its tentative result (the rescue starts from that exact
+  // distance) and goes to the rescue list; its order there does not affect any result.
+  if (valid) emit_row<NB>(i, LD, LK, top, need, codes, dist, rowD, rowK);
   if (valid && !certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
+}
+
+// Top-1 rescue.  Blocks take kRB listed rows at a time (rows b * kRB .., b = block, block + grid,
+// ...) and stream the codebook once for all of them.  For each codeword and row a fp32 direct-form
+// distance d_f = sum_t (x_t - c_t)^2 (fma, t ascending) is a filter: its error is at most ~10u of
+// the true distance (u = 2^-24; for fp64 rows x is rounded to fp32 first, which moves sqrt(D) by
+// at most u ||x||), so every codeword with D <= D_tent passes d_f <= thr = (1 + 2^-20)
+// (sqrt(D_tent) + 2^-22 ||x||)^2 + 2^-120, D_tent being the exact distance of the tentative
+// winner.  Codewords that pass are scored exactly in fp64 and merged in (D, k) order.  A
+// non-finite threshold lets every codeword through (plain exact search).
+template <int KS>
+__global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const void* __restrict__ C, int ct,
+                                                      int64_t K, const int* __restrict__ rcount,
+                                                      const int* __restrict__ rlist, int32_t* __restrict__ codes,
+                                                      float* __restrict__ dist, double* __restrict__ rowD,
+                                                      int* __restrict__ rowK) {
+  constexpr int DM = 4 * KS;
+  constexpr int kRB = 32 / DM;  // rows per batch: their 32 values live in scalar registers
+  constexpr int kU = 4;         // codewords per thread in flight
+  __shared__ float sx[kRB][DM];
+  __shared__ float sthr[kRB];
+  __shared__ int srow[kRB];
+  __shared__ double wD[4][kRB];
+  __shared__ int wK[4][kRB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int d = src.d;
+  const int count = *rcount;
+#if CRVQ_DEBUG_RESCUE
+  if (blockIdx.x == 0 && threadIdx.x == 0) printf("[rescue] rows %d of %ld, K %ld\n", count, (long)src.n, (long)K);
+#endif
+  const int nbatch = (count + kRB - 1) / kRB;
+  for (int bt = blockIdx.x; bt < nbatch; bt += gridDim.x) {
+    const int ns = (count - bt * kRB < kRB) ? count - bt * kRB : kRB;  // rows in this batch
+    if (tid < kRB) {
+      float thr = -__builtin_inff();  // an empty slot passes nothing
+      int row = -1;
+      double xd[DM];
+      if (tid < ns) {
+        row = rlist[bt * kRB + tid];
+        load_row_exact<DM>(src, row, true, xd);
+        double Dt;
+        if (codes) {
+          const int k0 = codes[row];
+          float c0[DM];
+          load_codeword<DM>(C, ct, k0, d, true, c0);
+          Dt = 0.0;
+#pragma unroll
+          for (int t = 0; t < DM; ++t) {
+            if (t < d) {
+              const double diff = xd[t] - static_cast<double>(c0[t]);
+              Dt = Dt + diff * diff;
+            }
+          }
+        } else {
+          Dt = rowD[static_cast<int64_t>(row) * top];
+        }
+        double xn2 = 0.0;
+#pragma unroll
+        for (int t = 0; t < DM; ++t)
+          if (t < d) xn2 = xn2 + xd[t] * xd[t];
+        const double rt = sqrt(Dt) + 0x1p-22 * sqrt(xn2);
+        const double th = (1.0 + 0x1p-20) * rt * rt + 0x1p-120;
+        thr = (th <= 3.0e38) ? static_cast<float>(th) * (1.0f + 0x1p-22f) : __builtin_inff();
+      } else {
+#pragma unroll
+        for (int t = 0; t < DM; ++t) xd[t] = 0.0;
+      }
+#pragma unroll
+      for (int t = 0; t < DM; ++t) sx[tid][t] = static_cast<float>(xd[t]);
+      sthr[tid] = thr;
+      srow[tid] = row;
+    }
+    __syncthreads();
+    float xr[kRB][DM], th[kRB];  // uniform over the block: held in scalar registers
+#pragma unroll
+    for (int s = 0; s < kRB; ++s) {
+      th[s] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(sthr[s])));
+#pragma unroll
+      for (int t = 0; t < DM; ++t) xr[s][t] = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(sx[s][t])));
+    }
+    double bD[kRB];
+    int bK[kRB];
+#pragma unroll
+    for (int s = 0; s < kRB; ++s) {
+      bD[s] = __builtin_inf();
+      bK[s] = INT_MAX;
+    }
+    for (int64_t k0 = tid; k0 < K; k0 += kU * 256) {
+      float c[kU][DM];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) load_codeword<DM>(C, ct, k0 + u * 256, d, k0 + u * 256 < K, c[u]);
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int64_t k = k0 + u * 256;
+        if (k >= K) continue;
+#pragma unroll
+        for (int s = 0; s < kRB; ++s) {
+          if (s >= ns) continue;  // uniform
+          float df = 0.0f;
+#pragma unroll
+          for (int t = 0; t < DM; ++t) {
+            if (t < d) {
+              const float diff = xr[s][t] - c[u][t];
+              df = __builtin_fmaf(diff, diff, df);
+            }
+          }
+          if (df <= th[s]) {  // rare: score exactly
+            double xe[DM];
+            load_row_exact<DM>(src, srow[s], true, xe);
+            double D = 0.0;
+#pragma unroll
+            for (int t = 0; t < DM; ++t) {
+              if (t < d) {
+                const double diff = xe[t] - static_cast<double>(c[u][t]);
+                D = D + diff * diff;
+              }
+            }
+            if (cless(D, static_cast<int>(k), bD[s], bK[s])) {
+              bD[s] = D;
+              bK[s] = static_cast<int>(k);
+            }
+          }
+        }
+      }
+    }
+    // (D, k) minimum per row: within each wave, then over the four waves in wave order
+#pragma unroll
+    for (int s = 0; s < kRB; ++s) {
+      if (s >= ns) continue;  // uniform
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) {
+        const double oD = __shfl_xor(bD[s], m);
+        const int oK = __shfl_xor(bK[s], m);
+        if (cless(oD, oK, bD[s], bK[s])) {
+          bD[s] = oD;
+          bK[s] = oK;
+        }
+      }
+      if (lane == 0) {
+        wD[w][s] = bD[s];
+        wK[w][s] = bK[s];
+      }
+    }
+    __syncthreads();
+    if (tid < ns) {
+      double D = wD[0][tid];
+      int k = wK[0][tid];
+      for (int ww = 1; ww < 4; ++ww) {
+        if (cless(wD[ww][tid], wK[ww][tid], D, k)) {
+          D = wD[ww][tid];
+          k = wK[ww][tid];
+        }
+      }
+      const double ED[1] = {D};
+      const int EK[1] = {k};
+      emit_row<1>(srow[tid], ED, EK, top, 1, codes, dist, rowD, rowK);
+    }
+    __syncthreads();
+  }
 }
 
 // Exact fp64 search of every listed row over the whole codebook.  Persistent: block b takes rows
@@ -1271,8 +1437,12 @@ hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K
                      src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
                      dist, rowD, rowK);
   const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
-  hipLaunchKernelGGL((rescue_kernel<KS, NB>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C, ct,
-                     K, w.rcount, w.rlist, codes, dist, rowD, rowK);
+  if (NB == 1 && CRVQ_RESCUE_FILTER)
+    hipLaunchKernelGGL((rescue1_kernel<KS>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C,
+                       ct, K, w.rcount, w.rlist, codes, dist, rowD, rowK);
+  else
+    hipLaunchKernelGGL((rescue_kernel<KS, NB>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C,
+                       ct, K, w.rcount, w.rlist, codes, dist, rowD, rowK);
   return hipGetLastError();
 }
 

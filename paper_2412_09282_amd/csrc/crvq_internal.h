@@ -92,6 +92,7 @@ struct ScreenWs {
   float* apack;  // codebook in MFMA A-operand order, tiles x 64 lanes x ks
   float* cnp;    // ||c||^2 per codeword, +inf for padding
   int* pT;       // top-B: kept tile ids, [split][lane group][nb][row]
+  float* pM;     // top-B: their screen minima, same layout
   float* pR;     // smallest screen value outside the exactly scored codewords, [split][row]
   double* pD;    // top-1: exact distance of the split's winner, [split][row]
   int* pK;       // top-1: its codeword, [split][row]

@@ -415,9 +415,9 @@ template <class OPS, int NB, int CB, int NC>
 __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __restrict__ apack,
                                                      const float* __restrict__ cnp, int64_t tiles, int64_t tps,
                                                      const void* __restrict__ C, int ct, int64_t K,
-                                                     int* __restrict__ pT, float* __restrict__ pR,
-                                                     double* __restrict__ pD, int* __restrict__ pK,
-                                                     double* __restrict__ xn2o) {
+                                                     int* __restrict__ pT, float* __restrict__ pM,
+                                                     float* __restrict__ pR, double* __restrict__ pD,
+                                                     int* __restrict__ pK, double* __restrict__ xn2o) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int jl = lane & 15;
@@ -641,7 +641,10 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __r
       rs = fminf(rs, __shfl_xor(rs, 32));
       if (i < n) {
 #pragma unroll
-        for (int j = 0; j < NB; ++j) pT[((static_cast<int64_t>(split) * 4 + g) * NB + j) * n + i] = id[cb][j];
+        for (int j = 0; j < NB; ++j) {
+          pT[((static_cast<int64_t>(split) * 4 + g) * NB + j) * n + i] = id[cb][j];
+          pM[((static_cast<int64_t>(split) * 4 + g) * NB + j) * n + i] = m[cb][j];
+        }
         if (g == 0) pR[static_cast<int64_t>(split) * n + i] = rs;
       }
     }
@@ -1003,6 +1006,7 @@ __device__ __forceinline__ void emit_row(int64_t row, const double (&ED)[NB], co
 // One thread per row; rows that fail the certification are appended to the rescue list.
 template <int KS, int NB>
 __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top, const int* __restrict__ pT,
+                                                       const float* __restrict__ pM,
                                                        const float* __restrict__ pR, const double* __restrict__ pD,
                                                        const int* __restrict__ pK, const double* __restrict__ xn2a,
                                                        const void* __restrict__ C, int ct, int64_t K,
@@ -1049,6 +1053,35 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     }
   }
   if (valid) {
+    // Top-B: only kept tiles whose screen minimum is within a small margin of the top-th smallest
+    // kept minimum can hold one of the top answers in practice; the others are not re-scored and
+    // their minima join "rest", so the certificate below stays exact (a row whose answer lies in
+    // a skipped tile fails it and is rescued).
+    float thr = __builtin_inff();
+    if (NB > 1 && valid) {
+      float sm[NB];  // the NB smallest kept tile minima, ascending
+#pragma unroll
+      for (int j = 0; j < NB; ++j) sm[j] = __builtin_inff();
+      for (int s = 0; s < splits; ++s) {
+        for (int g = 0; g < 4; ++g) {
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            float v = pM[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+#pragma unroll
+            for (int q = 0; q < NB; ++q) {
+              const float lo = fminf(sm[q], v);
+              v = fmaxf(sm[q], v);
+              sm[q] = lo;
+            }
+          }
+        }
+      }
+      float mt = sm[0];
+#pragma unroll
+      for (int q = 0; q < NB; ++q)
+        if (q == need - 1) mt = sm[q];
+      thr = mt + 0x1p-12f * (fabsf(mt) + static_cast<float>(xn2));
+    }
     for (int s = 0; s < (NB > 1 ? splits : 0); ++s) {
       rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
       for (int g = 0; g < 4; ++g) {
@@ -1056,6 +1089,11 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
         for (int j = 0; j < NB; ++j) {
           const int T = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
           if (T < 0) continue;
+          const float mj = pM[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+          if (!(mj <= thr)) {  // not re-scored: its minimum bounds its codewords
+            rest = fminf(rest, mj);
+            continue;
+          }
           float cw[4][DM];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -1390,6 +1428,95 @@ __global__ __launch_bounds__(256) void beam_merge_kernel(int64_t n, int n_par, i
   }
 }
 
+// The same selection with one wave per vector: the n_par x beam candidates (up to 4 per lane) are
+// ranked by counting, for each, the candidates with a smaller key (D, parent, code); a candidate
+// of rank r < n_next writes child slot r.  Keys are distinct (a parent lists a codeword once;
+// invalid entries get +inf and a key past every parent), so the ranks are a permutation and the
+// children come out in the order of the sequential merge above.
+__global__ __launch_bounds__(256) void beam_merge_wave(int64_t n, int n_par, int n_next, int beam, int step,
+                                                       int n_books, const double* __restrict__ rowD,
+                                                       const int* __restrict__ rowK, RowSrc src0,
+                                                       const double* __restrict__ res_in, double* __restrict__ res_out,
+                                                       const int* __restrict__ tup_in, int* __restrict__ tup_out,
+                                                       double* __restrict__ err_out, const void* __restrict__ book,
+                                                       int bt, int64_t K, int d) {
+  const int lane = threadIdx.x & 63;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (i >= n) return;  // whole waves leave together; no barriers below
+  const int nc = n_par * beam;  // <= kMaxBeam * kMaxBeam = 256
+  double cD[4];
+  int cB[4], cK[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = lane + 64 * q;
+    cD[q] = __builtin_inf();
+    cB[q] = n_par + c;  // invalid: after every parent, distinct
+    cK[q] = -1;
+    if (c < nc) {
+      const int b = c / beam;
+      const int64_t r = (i * n_par + b) * beam + (c - b * beam);
+      const int k = rowK[r];
+      if (k >= 0 && k < K) {
+        cD[q] = rowD[r];
+        cB[q] = b;
+        cK[q] = k;
+      }
+    }
+  }
+  auto less = [](double Da, int ba, int ka, double Db, int bb, int kb) {
+    return Da < Db || (Da == Db && (ba < bb || (ba == bb && ka < kb)));
+  };
+  int rank[4] = {0, 0, 0, 0};
+  const int rounds = (nc + 63) / 64;  // candidate slots in use per lane (uniform)
+  for (int q2 = 0; q2 < rounds; ++q2) {
+    const int jn = (nc - 64 * q2 < 64) ? nc - 64 * q2 : 64;
+    for (int j = 0; j < jn; ++j) {
+      const double oD = __shfl(cD[q2], j);
+      const int oB = __shfl(cB[q2], j);
+      const int oK = __shfl(cK[q2], j);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (q < rounds) rank[q] += less(oD, oB, oK, cD[q], cB[q], cK[q]) ? 1 : 0;
+    }
+  }
+  const int64_t off0 = (step == 0) ? row_offset(src0, i) : 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = lane + 64 * q;
+    if (c >= nc || rank[q] >= n_next) continue;
+    const int s = rank[q];
+    double* ro = res_out + (i * n_next + s) * d;
+    int* to = tup_out + (i * n_next + s) * n_books;
+    if (cK[q] < 0) {  // cannot happen when n_next = min(beam, n_par * K); kept as a guard
+      err_out[i * n_next + s] = __builtin_inf();
+      for (int t = 0; t < d; ++t) ro[t] = 0.0;
+      for (int u = 0; u <= step; ++u) to[u] = 0;
+      continue;
+    }
+    const int b = cB[q];
+    if (d == 8 && step > 0 && bt == ET_F32 && (reinterpret_cast<uintptr_t>(book) & 15) == 0) {  // 16-byte accesses
+      const double2* pr = reinterpret_cast<const double2*>(res_in + (i * n_par + b) * 8);
+      const float4* cw = reinterpret_cast<const float4*>(static_cast<const float*>(book) + static_cast<int64_t>(cK[q]) * 8);
+      const float4 c0 = cw[0], c1 = cw[1];
+      const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+      double2* rw = reinterpret_cast<double2*>(ro);
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const double2 pv = pr[h];
+        rw[h] = make_double2(pv.x - static_cast<double>(cc[2 * h]), pv.y - static_cast<double>(cc[2 * h + 1]));
+      }
+    } else {
+      for (int t = 0; t < d; ++t) {
+        const double parent = (step == 0) ? row_elem(src0, off0, t) : res_in[(i * n_par + b) * d + t];
+        ro[t] = parent - cb_elem(book, bt, cK[q], d, t);
+      }
+    }
+    for (int u = 0; u < step; ++u) to[u] = tup_in[(i * n_par + b) * n_books + u];
+    to[step] = cK[q];
+    err_out[i * n_next + s] = cD[q];
+  }
+}
+
 __global__ __launch_bounds__(256) void beam_emit_kernel(int64_t n, int64_t vpr, int n_par, int n_books,
                                                         const int* __restrict__ tup, const double* __restrict__ err,
                                                         CodePtrs outs, float* __restrict__ err_out) {
@@ -1406,7 +1533,7 @@ hipError_t launch_screen_t(const RowSrc& src, const void* C, int ct, int64_t K, 
                            const ScreenWs& w, hipStream_t stream) {
   dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
   hipLaunchKernelGGL((screen_kernel<OPS, NB, CB, NC>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
-                     p.tiles_per_split, C, ct, K, w.pT, w.pR, w.pD, w.pK, w.xn2);
+                     p.tiles_per_split, C, ct, K, w.pT, w.pM, w.pR, w.pD, w.pK, w.xn2);
   return hipGetLastError();
 }
 
@@ -1434,7 +1561,7 @@ hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K
                              const ScreenWs& w, const ScreenBound& bound, int32_t* codes, float* dist, double* rowD,
                              int* rowK, hipStream_t stream) {
   hipLaunchKernelGGL((finalize_kernel<KS, NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
-                     src, p.splits, top, w.pT, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
+                     src, p.splits, top, w.pT, w.pM, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
                      dist, rowD, rowK);
   const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
   if (NB == 1 && CRVQ_RESCUE_FILTER)
@@ -1550,11 +1677,13 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
   w.rlist = ws.take<int>(static_cast<size_t>(n_rows));
   if (p.nb == 1) {
     w.pT = nullptr;
+    w.pM = nullptr;
     w.pD = ws.take<double>(static_cast<size_t>(p.splits) * n_rows);
     w.pK = ws.take<int>(static_cast<size_t>(p.splits) * n_rows);
     w.xn2 = ws.take<double>(static_cast<size_t>(n_rows));
   } else {
     w.pT = ws.take<int>(static_cast<size_t>(p.splits) * 4 * p.nb * n_rows);
+    w.pM = ws.take<float>(static_cast<size_t>(p.splits) * 4 * p.nb * n_rows);
     w.pD = nullptr;
     w.pK = nullptr;
     w.xn2 = nullptr;
@@ -1626,9 +1755,15 @@ hipError_t launch_beam_merge(int64_t n, int n_par, int beam, int step, int n_boo
   if (n <= 0) return hipSuccess;
   int64_t nn = static_cast<int64_t>(n_par) * K;
   const int n_next = static_cast<int>(nn < beam ? nn : beam);
-  hipLaunchKernelGGL(beam_merge_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0, stream, n, n_par,
-                     n_next, beam, step, n_books, rowD, rowK, src0, res_in, res_out, tup_in, tup_out, err_out, book,
-                     book_type, K, d);
+  if (n_par * beam > 1) {  // a real merge: one wave per vector
+    hipLaunchKernelGGL(beam_merge_wave, dim3(static_cast<unsigned>(cdiv(n, 4))), dim3(256), 0, stream, n, n_par,
+                       n_next, beam, step, n_books, rowD, rowK, src0, res_in, res_out, tup_in, tup_out, err_out, book,
+                       book_type, K, d);
+  } else {
+    hipLaunchKernelGGL(beam_merge_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0, stream, n, n_par,
+                       n_next, beam, step, n_books, rowD, rowK, src0, res_in, res_out, tup_in, tup_out, err_out, book,
+                       book_type, K, d);
+  }
   return hipGetLastError();
 }
 

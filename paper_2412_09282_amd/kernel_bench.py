@@ -110,6 +110,30 @@ def main(argv=None):
     report("crvq_kmeans_update", ms, nbytes=(d * es + 4) * n + K * d * es + 4 * K, n=n, K=K)
 
     n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    # residual beam over the critical vectors: the basic book plus the workload's extended books
+    # (residual-scale random codewords standing in for fitted ones), width wl.beam
+    ncv = M * n_crit // d
+    Vc = VecSet.of_matrix(Ws, d, n_cols=n_crit)
+    # extended books initialised like the pipeline's: residual vectors of the critical slab drawn by
+    # the workload's own seeded indices (the residual after the basic book for every extended book)
+    Eb = torch.empty(M, n_crit, dtype=torch.float32, device="cuda")
+    C.crvq_dequant(M, n_crit, d, codes, N // d, Cb, Eb, minuend=Ws)
+    VE = VecSet.of_matrix(Eb, d)
+    ext = []
+    for t, Ke in enumerate(wl.K_ext):
+        Ct = torch.empty(Ke, d, dtype=torch.float32, device="cuda")
+        C.crvq_gather_vectors(VE, torch.from_numpy(inputs.ext_init_indices(wl, 0, t + 1, ncv)).cuda(), Ct)
+        ext.append(Ct)
+    books = [Cb] + ext
+    bcodes = [torch.empty(ncv, dtype=torch.int32, device="cuda") for _ in books]
+    berr = torch.empty(ncv, dtype=torch.float32, device="cuda")
+    flops, width = 0.0, 1
+    for Kt in [K] + list(wl.K_ext):  # step t screens min(beam, prod K before t) parents x K_t codewords
+        flops += 2.0 * d * width * Kt
+        width = min(wl.beam, width * Kt)
+    if not a.skip_assign:
+        ms = timed(lambda: C.crvq_assign_residual_beam(Vc, books, wl.beam, bcodes, berr), max(2, a.reps // 5))
+        report("crvq_assign_residual_beam", ms, flops=flops * ncv, n=ncv, beam=wl.beam, K=[K] + list(wl.K_ext))
     E = torch.empty(M, n_crit, dtype=torch.float32, device="cuda")
     ms = timed(lambda: C.crvq_dequant(M, n_crit, d, codes, N // d, Cb, E, minuend=Ws), a.reps, flush)
     report("crvq_dequant (residual of the critical slab)", ms,

@@ -1,9 +1,10 @@
 // Lloyd update of a K-means codebook (Sec. 3.1 Eq. 2 of the paper; Alg. 1 KMeansCodebook):
 // every centroid becomes the mean of the vectors encoded to it.
 //
-// Atomic-free and deterministic.  Every centroid is a fixed-order fp64 sum of its members, divided
-// by their count and rounded once to the codebook's type; a codeword without members is left
-// untouched; codes outside [0, K) belong to no cluster.
+// Deterministic: every centroid is a fixed-order fp64 sum of its members (no floating-point
+// atomics), divided by their count and rounded once to the codebook's type; a codeword without
+// members is left untouched; codes outside [0, K) belong to no cluster.  Only the radix histogram
+// counts with integer LDS atomics.
 // * K <= 256 (small_k_partial): blocks walk contiguous vector ranges; each round of 1024 codes is
 //   bucket-sorted in LDS and thread k adds the members of code k.
 // * K > 256 (bucket_partial8 / bucket_partial): one stable radix pass (per-tile ballot counting,
@@ -99,13 +100,12 @@ __global__ __launch_bounds__(256) void radix_hist(const int* __restrict__ keys, 
     const int64_t idx = base + bt * 64 + lane;
     key[bt] = (idx < n) ? ld_stream_i32(keys + idx) : -1;
   }
+  // counting only (no ranks): integer LDS atomics, whose totals do not depend on their order
 #pragma unroll
   for (int bt = 0; bt < kBatches; ++bt) {
     const int64_t idx = base + bt * 64 + lane;
     const bool valid = (idx < n) && (pass != 0 || (key[bt] >= 0 && key[bt] < K));
-    const int digit = valid ? (key[bt] >> shift) & 255 : 0;
-    const uint64_t peers = peer_mask(valid, digit);
-    if (valid && (__ffsll(static_cast<long long>(peers)) - 1) == lane) wh[w][digit] += __popcll(peers);
+    if (valid) atomicAdd(&wh[w][(key[bt] >> shift) & 255], 1);
   }
   __syncthreads();
   hist[static_cast<int64_t>(tid) * n_tiles + blockIdx.x] = wh[0][tid] + wh[1][tid] + wh[2][tid] + wh[3][tid];
@@ -439,7 +439,10 @@ SmallPlan small_plan(int64_t n) {
 // Every bucket is then cut into chunks of kChunk vectors; a block takes one chunk and runs the
 // small-codebook scheme on the low byte, gathering each member vector with 16-byte loads.  The
 // chunk partials of each code are folded in chunk order.
-constexpr int kChunk = 8192;
+#ifndef CRVQ_KM_CHUNK
+#define CRVQ_KM_CHUNK 4096
+#endif
+constexpr int kChunk = CRVQ_KM_CHUNK;
 
 // bounds of the 256 high-byte buckets and of their chunk ranges (one block)
 // Chunks are also enumerated level by level (chunk j of every bucket that has one, buckets in

@@ -148,7 +148,6 @@ __global__ __launch_bounds__(256) void dequant_rows_perm(int64_t n_cols, int d, 
 // half h of a pair reads and writes dimensions 4h .. 4h + 3, so both halves of a codeword gather
 // come from one cache line and every store of a wave is one contiguous piece.  All code and
 // codeword loads of a thread's vectors are issued before any is used.
-constexpr int kU = 4;  // vectors per lane pair and round in the row kernel
 
 // Half h (4 elements) of codeword q as floats: one float4 (fp32) or one 8-byte load (bf16).
 __device__ __forceinline__ void load_cw4(const void* C, int type, int64_t q, int h, float (&c)[4]) {
@@ -247,44 +246,51 @@ __global__ __launch_bounds__(256) void dequant_rows8(int64_t M, int64_t vpr, int
   store4<T, true>(out + r * ld_out + g * 8 + 4 * h, x);
 }
 
-// Reconstruction in original channel order.  Persistent blocks keep the inverse permutation in LDS
-// (16-bit column indices, read from memory once per block) and walk rows r = block, block + grid,
-// ...: each row is rebuilt in LDS (kU vectors per lane pair and round), then written through the
-// inverse permutation in 16-byte segments.
+// Reconstruction in original channel order.  Persistent blocks of 512 threads keep the inverse
+// permutation in LDS (16-bit column indices, read from memory once per block) and walk rows
+// r = block, block + grid, ...: each row is rebuilt in LDS (kUP vectors per lane pair and round, so a
+// row of up to 8192 columns takes one round), then written through the inverse permutation in
+// 16-byte segments.  This form takes any books; the extended codes of a critical vector are read
+// where it is rebuilt.
+constexpr int kPermThreads = 512;
+constexpr int kUP = 4;  // vectors per lane pair and round in the permuted-row kernels
+constexpr int kPE = 2;  // extended books handled by the specialised kernel
+
 template <typename T>
-__global__ __launch_bounds__(256) void dequant_rows_perm8(int64_t M, int64_t n_cols, int64_t ncv, DequantBooks b,
-                                                          const int32_t* __restrict__ inv, T* __restrict__ out,
-                                                          int64_t ld_out) {
+__global__ __launch_bounds__(kPermThreads) void dequant_rows_perm8(int64_t M, int64_t n_cols, int64_t ncv,
+                                                                   DequantBooks b, const int32_t* __restrict__ inv,
+                                                                   T* __restrict__ out, int64_t ld_out) {
   extern __shared__ unsigned char smem[];
   T* row = reinterpret_cast<T*>(smem);
   uint16_t* src = reinterpret_cast<uint16_t*>(smem + ((n_cols * sizeof(T) + 15) & ~static_cast<int64_t>(15)));
-  for (int64_t j = threadIdx.x; j < n_cols; j += 256) {
+  for (int64_t j = threadIdx.x; j < n_cols; j += kPermThreads) {
     const int32_t sj = inv[j];
     src[j] = (sj >= 0 && sj < n_cols) ? static_cast<uint16_t>(sj) : static_cast<uint16_t>(0xffff);  // 0xffff: zero
   }
   const int64_t vpr = n_cols / 8;
   const int h = threadIdx.x & 1;
   const int pair = threadIdx.x >> 1;
+  constexpr int kPairs = kPermThreads / 2;
   constexpr int V = 16 / sizeof(T);
   for (int64_t r = blockIdx.x; r < M; r += gridDim.x) {
-    for (int64_t g0 = pair; g0 < vpr; g0 += 128 * kU) {
-      int32_t q[kU];
-      bool live[kU], in[kU];
+    for (int64_t g0 = pair; g0 < vpr; g0 += kPairs * kUP) {
+      int32_t q[kUP];
+      bool live[kUP], in[kUP];
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const int64_t g = g0 + 128 * u;
+      for (int u = 0; u < kUP; ++u) {
+        const int64_t g = g0 + kPairs * u;
         live[u] = g < vpr;
         q[u] = live[u] ? ld_stream_i32(b.q[0] + r * b.ldq_base + g) : 0;
       }
-      float c[kU][4];
+      float c[kUP][4];
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
+      for (int u = 0; u < kUP; ++u) {
         in[u] = q[u] >= 0 && q[u] < b.K[0];
         load_cw4(b.C[0], b.type[0], (live[u] && in[u]) ? q[u] : 0, h, c[u]);
       }
 #pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const int64_t g = g0 + 128 * u;
+      for (int u = 0; u < kUP; ++u) {
+        const int64_t g = g0 + kPairs * u;
         if (!live[u]) continue;
         double v[4];
         const bool ok = recon4(b, r, g, h, ncv, in[u], c[u], v);
@@ -295,7 +301,138 @@ __global__ __launch_bounds__(256) void dequant_rows_perm8(int64_t M, int64_t n_c
     }
     __syncthreads();  // the row (and, first time round, the permutation) is in LDS
     T* ro = out + r * ld_out;
-    for (int64_t c = threadIdx.x; c < n_cols / V; c += 256) {
+    for (int64_t c = threadIdx.x; c < n_cols / V; c += kPermThreads) {
+      T seg[V];
+#pragma unroll
+      for (int u = 0; u < V; ++u) {
+        const uint32_t sj = src[c * V + u];
+        seg[u] = (sj < static_cast<uint32_t>(n_cols)) ? row[sj] : T(0);
+      }
+      st_stream(reinterpret_cast<uint4*>(ro) + c, *reinterpret_cast<const uint4*>(seg));
+    }
+    __syncthreads();  // the row buffer is rewritten by the next row
+  }
+}
+
+// The same kernel specialised for the common case, with every load of a round straight-line code
+// (no branch between a load and its use, so all of a round's gathers are in flight together; no
+// prefetch across rows either: waiting for codes loaded before a row's stores would also wait for
+// those stores):
+// basic book element type TB, exactly NE extended books (fp32), critical groups of a row within
+// the first 256 vectors (only a lane pair's first vector of a round can be critical).  Loads of
+// absent entries read a valid address (code 0, vector 0) and their values are discarded.
+template <typename TB>
+__device__ __forceinline__ void load_cw4t(const TB* C, int32_t q, int h, float (&c)[4]) {
+  if constexpr (sizeof(TB) == 4) {
+    const float4 a = *reinterpret_cast<const float4*>(C + static_cast<int64_t>(q) * 8 + 4 * h);
+    c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w;
+  } else {
+    const uint2 w = *reinterpret_cast<const uint2*>(C + static_cast<int64_t>(q) * 8 + 4 * h);
+    c[0] = __uint_as_float(w.x << 16);
+    c[1] = __uint_as_float(w.x & 0xffff0000u);
+    c[2] = __uint_as_float(w.y << 16);
+    c[3] = __uint_as_float(w.y & 0xffff0000u);
+  }
+}
+
+// 4 output elements from fp32 values: a vector with one codeword is that codeword, so its fp64 sum
+// rounds back to the same fp32 value (bf16: the same nearest-even rounding of the fp32 value).
+__device__ __forceinline__ uint16_t bf16_from_float(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if (x != x) return 0x7fc0;
+  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+template <typename T>
+__device__ __forceinline__ void store4f(T* p, const float (&x)[4]) {
+  if constexpr (sizeof(T) == 4) {
+    *reinterpret_cast<uint4*>(p) =
+        make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3]));
+  } else {
+    uint2 w;
+    w.x = static_cast<uint32_t>(bf16_from_float(x[0])) | (static_cast<uint32_t>(bf16_from_float(x[1])) << 16);
+    w.y = static_cast<uint32_t>(bf16_from_float(x[2])) | (static_cast<uint32_t>(bf16_from_float(x[3])) << 16);
+    *reinterpret_cast<uint2*>(p) = w;
+  }
+}
+
+template <typename T, typename TB, int NE>
+__global__ __launch_bounds__(kPermThreads) void dequant_rows_perm8_fast(int64_t M, int64_t n_cols, int64_t ncv,
+                                                                        DequantBooks b,
+                                                                        const int32_t* __restrict__ inv,
+                                                                        T* __restrict__ out, int64_t ld_out) {
+  extern __shared__ unsigned char smem[];
+  T* row = reinterpret_cast<T*>(smem);
+  uint16_t* src = reinterpret_cast<uint16_t*>(smem + ((n_cols * sizeof(T) + 15) & ~static_cast<int64_t>(15)));
+  for (int64_t j = threadIdx.x; j < n_cols; j += kPermThreads) {
+    const int32_t sj = inv[j];
+    src[j] = (sj >= 0 && sj < n_cols) ? static_cast<uint16_t>(sj) : static_cast<uint16_t>(0xffff);  // 0xffff: zero
+  }
+  const int64_t vpr = n_cols / 8;
+  const int h = threadIdx.x & 1;
+  const int pair = threadIdx.x >> 1;
+  constexpr int kPairs = kPermThreads / 2;
+  constexpr int kStep = kPairs * kUP;
+  constexpr int V = 16 / sizeof(T);
+  constexpr int NEa = NE > 0 ? NE : 1;
+  const TB* Cb = static_cast<const TB*>(b.C[0]);
+  const int32_t* qb = b.q[0];
+  const int64_t Kb = b.K[0];
+  for (int64_t r = blockIdx.x; r < M; r += gridDim.x) {
+    for (int64_t g0 = pair; g0 < vpr; g0 += kStep) {
+      // codes of the round (the extended codes of its first vector if that one is critical), then
+      // every codeword gather of the round at once
+      int32_t q[kUP], qe[NEa];
+#pragma unroll
+      for (int u = 0; u < kUP; ++u) {
+        const int64_t g = g0 + kPairs * u;
+        const int32_t v = ld_stream_i32(qb + (g < vpr ? r * b.ldq_base + g : 0));
+        q[u] = g < vpr ? v : 0;
+      }
+      const bool crit0 = NE > 0 && g0 < ncv;
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        const int32_t v = b.q[1 + e][crit0 ? r * b.ldq_ext + g0 : 0];
+        qe[e] = crit0 ? v : 0;
+      }
+      float c[kUP][4], ce[NEa][4];
+      bool ok[kUP];
+#pragma unroll
+      for (int u = 0; u < kUP; ++u) {
+        ok[u] = q[u] >= 0 && q[u] < Kb;
+        load_cw4t<TB>(Cb, ok[u] ? q[u] : 0, h, c[u]);
+      }
+#pragma unroll
+      for (int e = 0; e < NE; ++e) {
+        const bool in = qe[e] >= 0 && qe[e] < b.K[1 + e];
+        ok[0] = ok[0] && in;  // qe is 0 (in range) for a vector that is not critical
+        load_cw4t<float>(static_cast<const float*>(b.C[1 + e]), in ? qe[e] : 0, h, ce[e]);
+      }
+#pragma unroll
+      for (int u = 0; u < kUP; ++u) {
+        const int64_t g = g0 + kPairs * u;
+        if (u == 0 && crit0) {
+          // fp64 sum in book order: the basic codeword, then the extended books
+          double v[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = 0.0 + static_cast<double>(c[u][t]);
+#pragma unroll
+          for (int e = 0; e < NE; ++e)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) v[t] = v[t] + static_cast<double>(ce[e][t]);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = ok[u] ? v[t] : __builtin_nan("");
+          if (g < vpr) store4<T, false>(row + g * 8 + 4 * h, v);
+        } else {
+          float v[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) v[t] = ok[u] ? c[u][t] : __builtin_nanf("");
+          if (g < vpr) store4f<T>(row + g * 8 + 4 * h, v);
+        }
+      }
+    }
+    __syncthreads();  // the row (and, first time round, the permutation) is in LDS
+    T* ro = out + r * ld_out;
+    for (int64_t c = threadIdx.x; c < n_cols / V; c += kPermThreads) {
       T seg[V];
 #pragma unroll
       for (int u = 0; u < V; ++u) {
@@ -366,15 +503,36 @@ hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, cons
   }
   const size_t lds8 = ((static_cast<size_t>(n_cols) * esize + 15) & ~static_cast<size_t>(15)) + 2 * n_cols;
   if (fast && inv_perm && n_cols % (16 / esize) == 0 && n_cols < 65535 && lds8 <= 64 * 1024) {
-    // persistent: about as many blocks as fit on the device at once, each walking many rows
-    const int64_t per_cu = static_cast<int64_t>((160 * 1024) / lds8) > 8 ? 8 : static_cast<int64_t>((160 * 1024) / lds8);
-    const int64_t grid = M < 256 * per_cu ? M : 256 * per_cu;
-    if (esize == 4)
-      hipLaunchKernelGGL(dequant_rows_perm8<uint32_t>, dim3(static_cast<unsigned>(grid)), dim3(256), lds8, stream, M,
-                         n_cols, ncv, books, inv_perm, static_cast<uint32_t*>(out), ld_out);
+    // Persistent: as many blocks of 512 threads as are resident on the device at once (registers and
+    // LDS permitting), each walking rows block, block + grid, ...  Specialised kernel when there are
+    // at most kPE extended books, all fp32, and the critical groups of a row lie within the first
+    // vector of every lane pair's round.
+    bool spec = books.n - 1 <= kPE && ncv <= kPermThreads / 2;
+    for (int e = 1; e < books.n; ++e) spec = spec && books.type[e] == ET_F32;
+    const void* fn = nullptr;
+    const int ne = books.n - 1;
+    const bool bf = books.type[0] == ET_BF16;
+#define CRVQ_DQP_NE(T, TB)                                                                                      \
+  (ne == 0 ? reinterpret_cast<const void*>(dequant_rows_perm8_fast<T, TB, 0>)                                     \
+           : ne == 1 ? reinterpret_cast<const void*>(dequant_rows_perm8_fast<T, TB, 1>)                           \
+                     : reinterpret_cast<const void*>(dequant_rows_perm8_fast<T, TB, 2>))
+    if (spec)
+      fn = esize == 4 ? (bf ? CRVQ_DQP_NE(uint32_t, uint16_t) : CRVQ_DQP_NE(uint32_t, float))
+                      : (bf ? CRVQ_DQP_NE(uint16_t, uint16_t) : CRVQ_DQP_NE(uint16_t, float));
     else
-      hipLaunchKernelGGL(dequant_rows_perm8<uint16_t>, dim3(static_cast<unsigned>(grid)), dim3(256), lds8, stream, M,
-                         n_cols, ncv, books, inv_perm, static_cast<uint16_t*>(out), ld_out);
+      fn = esize == 4 ? reinterpret_cast<const void*>(dequant_rows_perm8<uint32_t>)
+                      : reinterpret_cast<const void*>(dequant_rows_perm8<uint16_t>);
+#undef CRVQ_DQP_NE
+    int per_cu = 1, dev = 0, cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kPermThreads, lds8) != hipSuccess || per_cu < 1)
+      per_cu = 1;
+    if (hipGetDevice(&dev) == hipSuccess) (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    const int64_t resident = static_cast<int64_t>(per_cu) * (cus > 0 ? cus : 256);
+    const int64_t grid = M < resident ? M : resident;
+    void* args[] = {&M, &n_cols, const_cast<int64_t*>(&ncv), const_cast<DequantBooks*>(&books),
+                    const_cast<int32_t**>(&inv_perm), &out, &ld_out};
+    (void)hipGetLastError();
+    return hipLaunchKernel(fn, dim3(static_cast<unsigned>(grid)), dim3(kPermThreads), args, lds8, stream);
     return hipGetLastError();
   }
   if (!inv_perm) {

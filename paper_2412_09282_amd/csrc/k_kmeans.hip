@@ -393,6 +393,138 @@ __global__ __launch_bounds__(256) void small_k_partial(RowSrc src, const int32_t
   }
 }
 
+// ---- small codebooks, d <= 8: per-wave tables, no sort ------------------------------------------
+// Every wave owns a private fp64 table of K x 8 sums in LDS and the batches of 64 vectors
+// j = wave, wave + W, wave + 2W, ... (W waves in the grid), so the waves in flight read one moving
+// window of memory.  It reads one vector per lane, kSkDepth batches in flight; within a batch the
+// lanes that share a code find each other with eight ballots, and the lowest of them adds its peers'
+// vectors (staged in LDS) to the table entry of that code in ascending order.  So every table entry
+// is a fixed-order sequential sum of its code's members over the wave's batches.  At the end the
+// block folds its wave tables in wave order into one partial per block (layout [k][t][block]);
+// small_k_final folds those in block order.
+constexpr int kSkWaves = 8;
+constexpr int kSkDepth = 4;
+
+struct SkTable {
+  double acc[256 * 8];
+  int cnt[256];
+  float4 stage[64][2];
+};
+
+// Vector i as 8 floats (zero past d).  KIND 0: fp32 d = 8 with 16-byte aligned vectors (two
+// nontemporal 16-byte loads), KIND 1: bf16 d = 8 aligned (one), KIND 2: element loads (any d <= 8).
+// KIND 0 / 1 are straight-line code: a lane outside the range reads vector 0 (its code is set to
+// -1, so the values are never used), which keeps every prefetched batch in flight.
+template <int KIND>
+__device__ __forceinline__ void sk_load(const RowSrc& s, int64_t i, bool ok, float4& a, float4& b) {
+  const int64_t off = row_offset(s, ok ? i : 0);
+  if constexpr (KIND == 0) {
+    const float* p = static_cast<const float*>(s.base) + off;
+    const uint4 x = ld_stream(p), y = ld_stream(p + 4);
+    a = make_float4(__uint_as_float(x.x), __uint_as_float(x.y), __uint_as_float(x.z), __uint_as_float(x.w));
+    b = make_float4(__uint_as_float(y.x), __uint_as_float(y.y), __uint_as_float(y.z), __uint_as_float(y.w));
+  } else if constexpr (KIND == 1) {
+    const uint4 q = ld_stream(static_cast<const uint16_t*>(s.base) + off);
+    a = make_float4(__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xffff0000u), __uint_as_float(q.y << 16),
+                    __uint_as_float(q.y & 0xffff0000u));
+    b = make_float4(__uint_as_float(q.z << 16), __uint_as_float(q.z & 0xffff0000u), __uint_as_float(q.w << 16),
+                    __uint_as_float(q.w & 0xffff0000u));
+  } else {
+    float e[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) e[t] = (ok && t < s.d) ? static_cast<float>(row_elem(s, off, t)) : 0.0f;
+    a = make_float4(e[0], e[1], e[2], e[3]);
+    b = make_float4(e[4], e[5], e[6], e[7]);
+  }
+}
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <int KIND>
+__global__ __launch_bounds__(64 * kSkWaves) void small_k_wave_partial(RowSrc src, const int32_t* __restrict__ codes,
+                                                                       int64_t K, int64_t per_wave, int64_t nblocks,
+                                                                       double* __restrict__ part,
+                                                                       int* __restrict__ pcount) {
+  __shared__ SkTable tab[kSkWaves];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  SkTable& T = tab[w];
+  const int d = src.d;
+  for (int e = lane; e < 256 * 8; e += 64) T.acc[e] = 0.0;
+  for (int e = lane; e < 256; e += 64) T.cnt[e] = 0;
+  const int64_t n = src.n;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kSkWaves * 64;  // elements between a wave's batches
+  const int64_t w0 = (static_cast<int64_t>(blockIdx.x) * kSkWaves + w) * 64;
+  const int64_t w1 = n;
+  (void)per_wave;
+  // kSkDepth batches in flight: slot s holds batch base + 64 s and is refilled right after use
+  // with the batch kSkDepth further on (the loop is unrolled over the slots, so no register holding
+  // a pending load is ever copied); a lane's code is masked to -1 only when its batch is used.
+  float4 va[kSkDepth], vb[kSkDepth];
+  int cq[kSkDepth];
+#pragma unroll
+  for (int s = 0; s < kSkDepth; ++s) {
+    const int64_t i = w0 + stride * s + lane;
+    const bool ok = i < w1;
+    sk_load<KIND>(src, i, ok, va[s], vb[s]);
+    cq[s] = ld_stream_i32(codes + (ok ? i : 0));
+  }
+  for (int64_t base = w0; base < w1; base += stride * kSkDepth) {
+#pragma unroll
+    for (int s = 0; s < kSkDepth; ++s) {
+      const int64_t bb = base + stride * s;
+      if (bb < w1) {  // uniform
+        const int c = (bb + lane < w1) ? cq[s] : -1;
+        const bool valid = c >= 0 && c < K;
+        T.stage[lane][0] = va[s];
+        T.stage[lane][1] = vb[s];
+        wave_lds_sync();  // staged vectors and the previous batch's table updates are visible
+        const uint64_t peers = peer_mask(valid, valid ? c : 0);
+        if (valid && (__ffsll(static_cast<long long>(peers)) - 1) == lane) {
+          double acc[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) acc[t] = T.acc[c * 8 + t];
+          uint64_t m = peers;
+          while (m) {
+            const int sl = __ffsll(static_cast<long long>(m)) - 1;
+            m &= m - 1;
+            const float4 x0 = T.stage[sl][0], x1 = T.stage[sl][1];
+            const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc[t] = acc[t] + static_cast<double>(x[t]);
+          }
+#pragma unroll
+          for (int t = 0; t < 8; ++t) T.acc[c * 8 + t] = acc[t];
+          T.cnt[c] += __popcll(peers);
+        }
+        wave_lds_sync();  // the stage is rewritten by the next batch
+      }
+      const int64_t i = bb + stride * kSkDepth + lane;
+      const bool ok = i < w1;
+      sk_load<KIND>(src, i, ok, va[s], vb[s]);
+      cq[s] = ld_stream_i32(codes + (ok ? i : 0));
+    }
+  }
+  __syncthreads();
+  for (int64_t e = tid; e < K * d; e += 64 * kSkWaves) {
+    const int64_t k = e / d;
+    const int t = static_cast<int>(e - k * d);
+    double acc = 0.0;
+#pragma unroll
+    for (int ww = 0; ww < kSkWaves; ++ww) acc = acc + tab[ww].acc[k * 8 + t];
+    part[e * nblocks + blockIdx.x] = acc;
+    if (t == 0) {
+      int cnt = 0;
+#pragma unroll
+      for (int ww = 0; ww < kSkWaves; ++ww) cnt += tab[ww].cnt[k];
+      pcount[k * nblocks + blockIdx.x] = cnt;
+    }
+  }
+}
+
 // One wave per centroid element: lanes fold blocks lane, lane + 64, ... in order, then a fixed
 // xor butterfly (the same in every lane).
 __global__ __launch_bounds__(256) void small_k_final(const double* __restrict__ part, const int* __restrict__ pcount,
@@ -424,6 +556,17 @@ struct SmallPlan {
   int64_t blocks;
   int64_t per_block;
 };
+
+// The per-wave scheme: one block of kSkWaves waves per CU (LDS holds one block), at most one wave
+// per batch of 64 vectors.
+SmallPlan wave_plan(int64_t n) {
+  SmallPlan p;
+  const int64_t batches = cdiv(n > 0 ? n : 1, 64);
+  const int64_t waves = batches < 256 * kSkWaves ? batches : 256 * kSkWaves;
+  p.blocks = cdiv(waves, kSkWaves);
+  p.per_block = 64;
+  return p;
+}
 
 SmallPlan small_plan(int64_t n) {
   SmallPlan p;
@@ -722,9 +865,10 @@ hipError_t exclusive_scan(const int* in, int64_t n, int* sums, int* out, int* to
 size_t kmeans_ws_bytes(int64_t n, int64_t K) {
   WsCursor c(nullptr);
   if (K <= 256) {
-    SmallPlan p = small_plan(n);
-    c.take<double>(static_cast<size_t>(p.blocks * K * 16));
-    c.take<int>(static_cast<size_t>(p.blocks * K));
+    SmallPlan p = small_plan(n), q = wave_plan(n);
+    const int64_t blocks = p.blocks > q.blocks ? p.blocks : q.blocks;
+    c.take<double>(static_cast<size_t>(blocks * K * 16));
+    c.take<int>(static_cast<size_t>(blocks * K));
     return c.used;
   }
   carve(c, n, K);
@@ -736,9 +880,25 @@ hipError_t launch_kmeans_update(const RowSrc& src, const int32_t* codes, int64_t
   const int64_t n = src.n;
   WsCursor cur(ws);
   if (K <= 256) {
-    SmallPlan p = small_plan(n);
-    double* part = cur.take<double>(static_cast<size_t>(p.blocks * K * 16));
-    int* pcount = cur.take<int>(static_cast<size_t>(p.blocks * K));
+    SmallPlan p = small_plan(n), q = wave_plan(n);
+    const int64_t blocks = p.blocks > q.blocks ? p.blocks : q.blocks;
+    double* part = cur.take<double>(static_cast<size_t>(blocks * K * 16));
+    int* pcount = cur.take<int>(static_cast<size_t>(blocks * K));
+    if (src.d <= 8 && src.type != ET_F64 && n > 0) {
+      const int es = src.type == ET_F32 ? 4 : 2;
+      const bool aligned = src.d == 8 && reinterpret_cast<uintptr_t>(src.base) % 16 == 0 && (src.ld * es) % 16 == 0;
+      const int kind = aligned ? (src.type == ET_F32 ? 0 : 1) : 2;
+      const dim3 g3(static_cast<unsigned>(q.blocks)), b3(64 * kSkWaves);
+      if (kind == 0)
+        hipLaunchKernelGGL(small_k_wave_partial<0>, g3, b3, 0, stream, src, codes, K, q.per_block, q.blocks, part, pcount);
+      else if (kind == 1)
+        hipLaunchKernelGGL(small_k_wave_partial<1>, g3, b3, 0, stream, src, codes, K, q.per_block, q.blocks, part, pcount);
+      else
+        hipLaunchKernelGGL(small_k_wave_partial<2>, g3, b3, 0, stream, src, codes, K, q.per_block, q.blocks, part, pcount);
+      hipLaunchKernelGGL(small_k_final, dim3(static_cast<unsigned>(cdiv(K * src.d, 4))), dim3(256), 0, stream, part,
+                         pcount, q.blocks, K, src.d, C, c_type, counts);
+      return hipGetLastError();
+    }
     const int staged = (src.ld == src.vpr * src.d) && src.d <= 8;
     hipLaunchKernelGGL(small_k_partial, dim3(static_cast<unsigned>(p.blocks)), dim3(256), 0, stream, src, codes, K,
                        p.per_block, staged, p.blocks, part, pcount);

@@ -766,7 +766,11 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
   *reinterpret_cast<u16x8*>(tile + 512) = pn;
 }
 
-template <int CB, int NC>
+// ONE (bf16 rows against a bf16 codebook): every scaled element is exact in fp16 (bf16 has fewer
+// significand bits and the power-of-two scale only moves the exponent; values that land below the
+// fp16 normal range are covered by the underflow terms of the bound), so c2 = x2 = 0 and the
+// second MFMA alone, (c1|N).(x1|2^12), forms alpha^2 s: one v_mfma_f32_32x32x16_f16 per tile.
+template <int CB, int NC, bool ONE>
 __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_t* apack,
                                                        const float* __restrict__ alpha_p, int64_t tiles, int64_t tps,
                                                        const void* __restrict__ C, int ct, int64_t K,
@@ -812,7 +816,8 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       const float x = over ? 0.0f : xs[t];
       const uint16_t x1 = f16_bits(x);
       p1[t] = x1;
-      p2[t] = h ? static_cast<uint16_t>(t < 3 ? 0x6c00 : 0) : f16_bits(x - f16_val(x1));  // 0x6c00 = 2^12
+      p2[t] = h ? static_cast<uint16_t>(t < 3 ? 0x6c00 : 0)  // 0x6c00 = 2^12
+                : (ONE ? x1 : f16_bits(x - f16_val(x1)));
     }
     b1[cb] = __builtin_bit_cast(h8, p1);
     b2[cb] = __builtin_bit_cast(h8, p2);
@@ -840,7 +845,8 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     const int voff1 = (j * 8 + h * 256) * 2, voff2 = (j * 8 + h * 512) * 2;
     const int T0 = static_cast<int>(t0), T1 = static_cast<int>(t1);
     auto load = [&](int T, h8& a1, h8& a2) {
-      a1 = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rs, voff1, T * (kS32TileHalves * 2), 0));
+      if (!ONE)
+        a1 = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rs, voff1, T * (kS32TileHalves * 2), 0));
       a2 = __builtin_bit_cast(h8, __builtin_amdgcn_raw_buffer_load_b128(rs, voff2, T * (kS32TileHalves * 2), 0));
     };
     // Software-pipelined over the column blocks: the MFMA pair of block cb is issued before the
@@ -852,15 +858,19 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       for (int cb = 0; cb <= CB; ++cb) {
         if (cb < CB) {
           f16v z = {};
-          acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, b1[cb], z, 0, 0, 0);
-          acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b2[cb], acc[cb & 1], 0, 0, 0);
+          if (ONE) {
+            acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b2[cb], z, 0, 0, 0);
+          } else {
+            acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a1, b1[cb], z, 0, 0, 0);
+            acc[cb & 1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a2, b2[cb], acc[cb & 1], 0, 0, 0);
+          }
         }
         if (cb > 0) {
           const f16v& a = acc[(cb - 1) & 1];
           cm[cb - 1] = first ? min_fold16(a[0], a) : min_fold16(cm[cb - 1], a);
         }
         if (CRVQ_S32_SCHED) {
-          if (cb < CB) __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+          if (cb < CB) __builtin_amdgcn_sched_group_barrier(0x008, ONE ? 1 : 2, 0);
           if (cb > 0) __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
         }
       }
@@ -1587,6 +1597,9 @@ hipError_t launch_finalize_ks(const RowSrc& src, const void* C, int ct, int64_t 
   return hipErrorInvalidValue;
 }
 
+// bf16 rows against a bf16 codebook: the 32 x 32 screen runs one MFMA per tile on exact operands.
+bool s32_exact_operands(int x_type, int ct) { return x_type == ET_BF16 && ct == ET_BF16; }
+
 // The certification bound of a screen mode.  fp32 MFMA: the accumulation and ||c||^2 roundings.
 // Split bf16: a wider accumulation allowance (the 32-term bf16 MFMA sum, measured well below it),
 // the split remainder 2^-15 ||x|| R for each operand that is not bf16 already, and an absolute
@@ -1598,8 +1611,9 @@ ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d, const f
   b.abs_coef = 0.0;
   b.alpha = nullptr;
   if (p.s32) {
-    // remainders of both splits and the dropped c2.x2, each <= 2^-22 sum |c_t| |2 x_t|
-    b.split_coef = 0x1p-19;
+    // remainders of both splits and the dropped c2.x2, each <= 2^-22 sum |c_t| |2 x_t|; none when
+    // both operands are bf16 (exact in fp16 under the scale)
+    b.split_coef = s32_exact_operands(x_type, ct) ? 0.0 : 0x1p-19;
     b.alpha = alpha;
   } else if (p.split) {
     if (b.acc_ulps < 96.0) b.acc_ulps = 96.0;
@@ -1708,12 +1722,12 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                        stream, C, ct, K, src.d, p.tiles, w.smax, nparts, ap, alpha, w.rcount);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
-    if (p.cb == 4)
-      hipLaunchKernelGGL((screen32_kernel<4, CRVQ_S32_CHUNK>), grid, dim3(256), 0, stream, src, ap, alpha, p.tiles,
-                         p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
+    if (s32_exact_operands(src.type, ct))
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true>), grid, dim3(256), 0, stream, src, ap,
+                         alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
     else
-      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK>), grid, dim3(256), 0, stream, src, ap, alpha,
-                         p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false>), grid, dim3(256), 0, stream, src, ap,
+                         alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const ScreenBound bound = screen_bound(p, src.type, ct, src.d, alpha);
     return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);

@@ -125,6 +125,86 @@ def test_kmeans_update_parity(n, K, dtype):
     np.testing.assert_array_equal(got[empty], C0[empty])  # empty clusters untouched, bitwise
 
 
+@pytest.mark.parametrize("n,K,d,dtype,layout", [(3_000_017, 256, 8, "f32", "packed"), (200_001, 256, 8, "bf16", "packed"),
+                                                 (50_000, 37, 5, "f32", "packed"), (40_000, 256, 8, "f32", "slab"),
+                                                 (30_000, 200, 3, "bf16", "slab"), (100_000, 1, 8, "f32", "packed"),
+                                                 (70_000, 256, 8, "f32", "skewed"), (63, 256, 8, "f32", "packed")])
+def test_kmeans_update_small_k(n, K, d, dtype, layout):
+    """K <= 256: per-wave tables over contiguous vector ranges (ragged tails, strided slabs, d < 8,
+    one code shared by most vectors)."""
+    say(f"kmeans update small K n={n} K={K} d={d} {dtype} {layout}")
+    g = np.random.default_rng(17)
+    if layout == "slab":  # the first `vpr` vectors of every row of a wider matrix
+        vpr, width = 4, 11 * d
+        rows = -(-n // vpr)
+        Wm = rv(rows, width, 18)
+        n = rows * vpr
+        V = np.ascontiguousarray(Wm[:, :vpr * d]).reshape(n, d)
+    else:
+        V = rv(n, d, 18)
+    codes = g.integers(0, K, n).astype(np.int32)
+    if layout == "skewed":
+        codes[g.random(n) < 0.9] = 7
+    if n > 100:
+        codes[3:8] = [-1, K, K + 7, -100, 2 ** 30]
+    C0 = rv(K, d, 19)
+    if dtype == "bf16":
+        V = inputs.f32_to_bf16_bits(V)
+        C0 = inputs.f32_to_bf16_bits(C0)
+        if layout == "slab":
+            Wm = inputs.f32_to_bf16_bits(Wm)
+    if layout == "slab":
+        Vs = VecSet(dev(Wm, dtype), rows, vpr, width, d)
+    else:
+        Vs = VecSet(dev(V, dtype), n, 1, d, d)
+    Ct = dev(C0, dtype)
+    counts = torch.empty(K, dtype=torch.int32, device="cuda")
+    C.crvq_kmeans_update(Vs, dev(codes), Ct, counts)
+    torch.cuda.synchronize()
+    valid = (codes >= 0) & (codes < K)
+    Cexp, cnt, _ = oracle.kmeans_update(V[valid], codes[valid], C0, dtype, dtype)
+    np.testing.assert_array_equal(counts.cpu().numpy(), cnt)
+    got = to_host_bits(Ct)
+    tol = 1e-5 if dtype == "f32" else 1e-2
+    rel_close(oracle.widen(got, dtype), oracle.widen(Cexp, dtype), tol, "centroids", axis_vec=True)
+    np.testing.assert_array_equal(got[cnt == 0], C0[cnt == 0])
+
+
+@pytest.mark.parametrize("M,N,dtype,n_ext,n_crit", [(37, 8200, "f32", 1, 200), (29, 13824, "bf16", 1, 344),
+                                                     (300, 5120, "bf16", 2, 128), (1, 64, "f32", 0, 0),
+                                                     (20, 4096, "f32", 3, 96), (16, 8192, "f32", 1, 2400),
+                                                     (9, 2048, "bf16", 2, 2048)])
+def test_dequant_reverse_reorder_rows(M, N, dtype, n_ext, n_crit):
+    """Reconstruction in original channel order for rows of one or several LDS rounds, 0-3 extended
+    books, critical groups beyond the first vector of a lane pair's round."""
+    say(f"dequant reverse reorder M={M} N={N} {dtype} ext={n_ext} n_crit={n_crit}")
+    d = 8
+    ncv = n_crit // d
+    g = np.random.default_rng(26)
+    Cb = rv(65536, d, 27)
+    Ce = [rv(256, d, 28 + e, 0.005) for e in range(n_ext)]
+    if dtype == "bf16":
+        Cb = inputs.f32_to_bf16_bits(Cb)
+    qb = g.integers(0, 65536, (M, N // d)).astype(np.int32)
+    qe = [g.integers(0, 256, (M, ncv)).astype(np.int32) for _ in range(n_ext)]
+    perm = g.permutation(N).astype(np.int32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    out = torch.empty(M, N, dtype=tdt, device="cuda")
+    C.crvq_dequant(M, N, d, dev(qb.ravel()), N // d, dev(Cb, dtype), out, n_crit=n_crit,
+                   q_ext=[dev(q.ravel()) for q in qe], ldq_ext=max(ncv, 1), C_ext=[dev(c) for c in Ce],
+                   perm=dev(perm))
+    torch.cuda.synchronize()
+    crit = opipe.crit_mask(M, N, d, n_crit)
+    codes = [qb.ravel()]
+    for q in qe:
+        z = np.zeros((M, N // d), np.int32)
+        z[:, :ncv] = q
+        codes.append(z.ravel())
+    R = oracle.reconstruct(codes, [Cb] + Ce, crit, [dtype] + ["f32"] * n_ext)
+    Rs = oracle.round_to(R, dtype).reshape(M, N)
+    np.testing.assert_array_equal(to_host_bits(out), oracle.scatter_columns(Rs, perm))
+
+
 @pytest.mark.parametrize("M,N,dtype,mode", [(513, 300, "f32", "sum"), (64, 1000, "f32", "max"),
                                             (1000, 96, "bf16", "sum"), (200, 77, "f32", "maxB"),
                                             (4096, 4096, "f32", "sum")])

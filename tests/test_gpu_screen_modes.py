@@ -56,6 +56,29 @@ def test_long_search_bf16():
     check(V, Cb, "bf16")
 
 
+@pytest.mark.parametrize("case", ["ties", "outliers", "tiny", "huge"])
+def test_long_search_bf16_exact_operands(case):
+    """bf16 rows against a bf16 codebook take the one-MFMA screen (exact fp16 operands)."""
+    say(f"long top-1 search bf16, exact-operand screen: {case}")
+    g = np.random.default_rng(44)
+    if case == "ties":
+        base = rv(16384, 8, 45)
+        Cb = np.ascontiguousarray(np.concatenate([base, base, base[::-1], base])[g.permutation(65536)])
+        V = np.concatenate([base[g.integers(0, 16384, 40000)], rv(25536 + 11, 8, 46)])
+    elif case == "outliers":
+        Cb = (g.standard_t(4.0, size=(65536 - 3, 8)) * 0.02).astype(np.float32)
+        Cb[:, 5] *= np.float32(10.0)
+        V = (g.standard_t(4.0, size=(65536 + 29, 8)) * 0.02).astype(np.float32)
+        big = g.choice(len(V), 300, replace=False)
+        V[big, g.integers(0, 8, 300)] *= np.float32(1e5)   # beyond the scaled fp16 range
+        tiny = g.choice(len(V), 300, replace=False)
+        V[tiny] *= np.float32(1e-9)                        # below the fp16 normal range once scaled
+    else:
+        s = np.float32(1e-30 if case == "tiny" else 1e30)
+        V, Cb = rv(65536, 8, 47) * s, rv(65536, 8, 48) * s
+    check(inputs.f32_to_bf16_bits(V), inputs.f32_to_bf16_bits(Cb), "bf16")
+
+
 def test_long_search_outlier_rows_and_heavy_tails():
     say("long top-1 search: t4 codebook with outlier columns, rows far outside the codebook range")
     g = np.random.default_rng(35)

@@ -67,6 +67,216 @@ def file_sha(path):
     return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
 
 
+# ------------------------------------------------------------------------------------------------
+# --table: one record per (workload, library call) with the oracle timed beside the GPU
+# ------------------------------------------------------------------------------------------------
+class TableHook:
+    """Around every library call of one layer pass: overwrite a 1 GiB buffer (so the last-level cache
+    holds none of the call's operands), HIP events on the library's stream, and host copies of the
+    call's inputs and outputs for the oracle."""
+
+    def __init__(self, flush):
+        import torch
+        self.torch = torch
+        self.flush = flush
+        self.calls = []
+        self.cur = None
+
+    @staticmethod
+    def _host(v):
+        import torch
+        if isinstance(v, torch.Tensor):
+            t = v.detach().cpu()
+            return t.view(torch.int16).numpy().view("uint16") if t.dtype == torch.bfloat16 else t.numpy()
+        if isinstance(v, (list, tuple)):
+            return [TableHook._host(x) for x in v]
+        return v
+
+    def pre(self, name, kw):
+        torch = self.torch
+        self.flush.fill_(len(self.calls))
+        self.cur = {"name": name, "in": {k: self._host(v) for k, v in kw.items()},
+                    "e0": torch.cuda.Event(enable_timing=True), "e1": torch.cuda.Event(enable_timing=True)}
+        self.cur["e0"].record()
+
+    def post(self, name, kw):
+        self.cur["e1"].record()
+        self.torch.cuda.synchronize()
+        self.cur["ms"] = self.cur["e0"].elapsed_time(self.cur["e1"])
+        self.cur["out"] = {k: self._host(v) for k, v in kw.items()}
+        del self.cur["e0"], self.cur["e1"]
+        self.calls.append(self.cur)
+        self.cur = None
+
+
+def table(args):
+    import zlib
+
+    import numpy as np
+    import torch
+
+    import oracle
+    from oracle import pipeline as opipe
+    from paper_2412_09282_amd import crvq, inputs
+    from paper_2412_09282_amd.pipeline import LayerConfig, LayerQuantizer
+
+    crvq.lib(build_if_missing=True)
+    oracle.build()
+    cores = oracle.num_threads()
+    torch.cuda.set_device(0)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    for wid in [int(w) for w in args.workloads.split(",")]:
+        wl = inputs.WORKLOADS[wid]
+        L = wl.layers[0]
+        M, N, d = L.M, L.N, wl.d
+        n = M * N // d
+        dt = L.dtype
+        es = 2 if dt == "bf16" else 4
+        log(f"table: workload {wid} ({L.name} {M}x{N} {dt})")
+        W = inputs.make_weight(wl, 0)
+        X = inputs.make_calib(wl, 0)
+        n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+        ncv_total = M * n_crit // d
+        base_idx = inputs.base_init_indices(wl, 0, n)
+        ext_idx = [inputs.ext_init_indices(wl, 0, t, ncv_total) for t in range(1, len(wl.K_ext) + 1)]
+        tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+        Wd = (torch.from_numpy(W.view(np.int16)).view(torch.bfloat16) if dt == "bf16" else torch.from_numpy(W)).cuda()
+        Xd = torch.from_numpy(X).cuda()
+        bi = torch.from_numpy(base_idx).cuda()
+        ei = [torch.from_numpy(e).cuda() for e in ext_idx]
+        cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
+        q = LayerQuantizer(M, N, tdt, cfg, L.tokens, device="cuda")
+        q.run(Wd, Xd, bi, ei)  # warm-up pass
+        torch.cuda.synchronize()
+        hook = TableHook(flush)
+        q.run(Wd, Xd, bi, ei, hooks=[hook])
+        torch.cuda.synchronize()
+        Ws = None
+        groups = {}
+        for c in hook.calls:
+            kind = c["name"].rsplit("_", 1)[0] if c["name"].split("_")[-1].isdigit() else c["name"]
+            groups.setdefault(kind, []).append(c)
+        g = np.random.default_rng([inputs.ROOT_SEED, wid, 99])
+
+        def rec(call, gpu_ms, calls, work, unit, peak, oracle_s, sample_frac, parity, **extra):
+            rate = work / (gpu_ms * 1e-3)
+            out = {"workload": wid, "layer": f"{L.name} {M}x{N} {dt}", "call": call, "calls": calls,
+                   "gpu_ms": round(gpu_ms, 4), "bound": "hbm" if unit == "B" else "mfma",
+                   "work_per_call": work, "work_unit": unit,
+                   "gpu_rate": rate, "frac": rate / peak,
+                   "oracle_s": round(oracle_s, 4), "oracle_rate": work * sample_frac / oracle_s,
+                   "oracle_sample": sample_frac, "cores": cores, "parity": parity}
+            out.update(extra)
+            print(json.dumps(out), flush=True)
+
+        HBM = PEAK_HBM_GBS * 1e9
+        F16 = PEAK_F16_MFMA_TFLOPS * 1e12
+        for kind, calls in groups.items():
+            c = calls[-1]
+            ms = float(np.median([x["ms"] for x in calls]))
+            t0 = time.perf_counter()
+            if kind == "hdiag":
+                exp = oracle.colreduce(X)
+                ts = time.perf_counter() - t0
+                got = c["out"]["out"]
+                ok = np.all(np.abs(got - exp) <= 1e-5 * np.abs(exp))
+                rec("channel_importance (Hessian diagonal)", ms, len(calls), X.size * 4 + N * 4, "B", HBM, ts, 1.0,
+                    "1e-5 rel" if ok else "FAIL")
+            elif kind == "importance":
+                exp = oracle.colreduce(W, scale=c["in"]["scale"].astype(np.float64), dtype=dt)
+                ts = time.perf_counter() - t0
+                ok = np.all(np.abs(c["out"]["out"] - exp) <= 1e-5 * np.abs(exp))
+                rec("channel_importance (W, scale = h)", ms, len(calls), M * N * es + 2 * N * 4, "B", HBM, ts, 1.0,
+                    "1e-5 rel" if ok else "FAIL")
+            elif kind == "reorder":
+                perm = oracle.rank_perm(c["in"]["importance"])
+                Ws_exp = oracle.gather_columns(W, perm)
+                ts = time.perf_counter() - t0
+                Ws = c["out"]["out"]
+                ok = np.array_equal(c["out"]["perm"], perm) and np.array_equal(Ws, Ws_exp)
+                rec("reorder (rank sort + column gather)", ms, len(calls), 2 * M * N * es + N * 4, "B", HBM, ts, 1.0,
+                    "bitwise" if ok else "FAIL")
+            elif kind.startswith("assign"):
+                base = kind.startswith("assign_base")
+                Xh = Ws if base else c["in"]["X"]
+                vdt = dt if base else "f32"
+                V = oracle.vectors(np.ascontiguousarray(Xh), d)
+                Cb = c["in"]["C"]
+                K = Cb.shape[0]
+                k = min(V.shape[0], max(256, int(6e11 / (K * d * 40))))  # about a second of oracle work
+                S = np.sort(g.choice(V.shape[0], size=k, replace=False))
+                t0 = time.perf_counter()
+                exp, _ = oracle.assign(V[S], Cb, vdt, vdt)
+                ts = time.perf_counter() - t0
+                same = int((c["out"]["codes"][S] == exp).sum())
+                rec(f"assign ({kind})", ms, len(calls), 2.0 * K * d * V.shape[0], "FLOP", F16, ts, k / V.shape[0],
+                    "exact" if same == k else f"{k - same} of {k} differ (ties allowed within 1e-6)",
+                    vectors=V.shape[0], K=K, sampled_vectors=k)
+            elif kind.startswith("update"):
+                base = kind.startswith("update_base")
+                Xh = Ws if base else c["in"]["X"]
+                vdt = dt if base else "f32"
+                V = oracle.vectors(np.ascontiguousarray(Xh), d)
+                Cexp, cnt, _ = oracle.kmeans_update(V, c["in"]["codes"], c["in"]["C"], vdt, vdt)
+                ts = time.perf_counter() - t0
+                got = oracle.widen(c["out"]["C"], vdt).astype(np.float64)
+                ex = oracle.widen(Cexp, vdt).astype(np.float64)
+                tol = 1e-5 if vdt == "f32" else 1e-2
+                ok = np.all(np.sqrt(((got - ex) ** 2).sum(1)) <= tol * np.sqrt((ex ** 2).sum(1)) + 1e-30)
+                K = Cexp.shape[0]
+                ves = 2 if vdt == "bf16" else 4
+                rec(f"kmeans_update ({kind})", ms, len(calls), (d * ves + 4) * V.shape[0] + K * d * ves + 4 * K, "B",
+                    HBM, ts, 1.0, f"{tol:g} rel per centroid" if ok else "FAIL", vectors=V.shape[0], K=K)
+            elif kind.startswith("residual"):
+                mdt = dt if kind == "residual_base" else "f32"
+                Mv = oracle.vectors(np.ascontiguousarray(c["in"]["minuend"]), d)
+                exp = oracle.residual(Mv, c["in"]["codes"].ravel(), c["in"]["book"], mdt, mdt)
+                ts = time.perf_counter() - t0
+                ok = np.array_equal(oracle.vectors(c["out"]["out"], d), exp)
+                mes = 2 if mdt == "bf16" else 4
+                rec(f"dequant ({kind}: E = W_crit - C[q])", ms, len(calls),
+                    Mv.size * (mes + 4) + 4 * Mv.shape[0] + c["in"]["book"].size * mes, "B", HBM, ts, 1.0,
+                    "bitwise" if ok else "FAIL")
+            elif kind == "beam":
+                Vc = oracle.vectors(np.ascontiguousarray(Ws[:, :n_crit]), d)
+                books = c["in"]["books"]
+                bdt = [dt] + ["f32"] * (len(books) - 1)
+                flops, width = 0.0, 1
+                for b in books:
+                    flops += 2.0 * d * width * b.shape[0]
+                    width = min(wl.beam, width * b.shape[0])
+                k = min(Vc.shape[0], max(256, int(3e11 / (flops / 2 * 10))))  # about a second of oracle work
+                S = np.sort(g.choice(Vc.shape[0], size=k, replace=False))
+                t0 = time.perf_counter()
+                exp_codes, exp_err = oracle.beam(Vc[S], books, wl.beam, dt, bdt)
+                ts = time.perf_counter() - t0
+                got = np.stack([c["out"]["codes_base"].ravel()[S]] + [x[S] for x in c["out"]["codes_ext"]])
+                same = int((got == exp_codes).all(0).sum())
+                rec(f"assign_residual_beam (width {wl.beam})", ms, len(calls), flops * Vc.shape[0], "FLOP", F16, ts,
+                    k / Vc.shape[0], "exact" if same == k else f"{k - same} of {k} tuples differ (ties allowed)",
+                    vectors=Vc.shape[0], books=[b.shape[0] for b in books], sampled_vectors=k)
+            elif kind == "dequant":
+                books = c["in"]["books"]
+                bdt = [dt] + ["f32"] * (len(books) - 1)
+                ncv, vpr = n_crit // d, N // d
+                qe = []
+                for x in c["in"]["codes_ext"]:
+                    z = np.zeros((M, vpr), np.int32)
+                    z[:, :ncv] = x.reshape(M, ncv)
+                    qe.append(z.ravel())
+                crit = opipe.crit_mask(M, N, d, n_crit)
+                R = oracle.reconstruct([c["in"]["codes"].ravel()] + qe, books, crit, bdt)
+                exp = oracle.scatter_columns(oracle.round_to(R, dt).reshape(M, N), c["in"]["perm"])
+                ts = time.perf_counter() - t0
+                ok = np.array_equal(c["out"]["out"], exp)
+                rec("dequant (reconstruction + reverse reorder)", ms, len(calls),
+                    M * N * es + 4 * n + 4 * ncv * M * len(qe) + sum(b.size * (2 if t == "bf16" else 4)
+                                                                     for b, t in zip(books, bdt)) + N * 4,
+                    "B", HBM, ts, 1.0, "bitwise" if ok else "FAIL")
+        del q, Wd, Xd, hook
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -76,10 +286,18 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one plain 1 GiB device-to-device copy (reference kernel for memory counters)")
+    ap.add_argument("--table", action="store_true",
+                    help="instead of the benchmark line: one JSON record per library call of one layer pass of each "
+                         "--workloads entry, GPU time beside the oracle's on the same inputs, with parity")
+    ap.add_argument("--workloads", default="1,2,3,4,5")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
         sys.exit(2)
+
+    if args.table:
+        table(args)
+        return
 
     import numpy as np
     import torch

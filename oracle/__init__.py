@@ -237,6 +237,27 @@ def reconstruct(codes: Sequence[np.ndarray], books: Sequence[np.ndarray], crit: 
     return R
 
 
+def gemv(M: int, N: int, d: int, n_crit: int, codes: Sequence[np.ndarray], books: Sequence[np.ndarray],
+         perm: Optional[np.ndarray], x: np.ndarray, book_dtypes: Optional[Sequence[str]] = None,
+         x_dtype: str = F32):
+    """Matrix-vector product with a CRVQ-quantized layer (Sec. 4.3, Fig. 3 right: the reconstructed
+    weights in original channel order), y = W_hat x, in fp64 from the exact (un-rounded) fp64 sum of
+    the codewords.  codes[0] is the basic code array [M][N/d], codes[b] (b >= 1) the extended codes
+    [M][n_crit/d] of the critical groups.  Returns (y, a) with a_i = sum_j |W_hat_ij x_j|, the scale
+    against which the rounding of a product in lower precision is measured."""
+    vpr, ncv = N // d, n_crit // d
+    full = [np.asarray(codes[0], dtype=np.int32).reshape(M, vpr).ravel()]
+    for c in codes[1:]:
+        z = np.zeros((M, vpr), np.int32)
+        z[:, :ncv] = np.asarray(c, dtype=np.int32).reshape(M, ncv)
+        full.append(z.ravel())
+    crit = (np.arange(M * vpr) % vpr < ncv).astype(np.uint8)
+    R = reconstruct(full, books, crit, book_dtypes).reshape(M, N)
+    Wh = scatter_columns(R, perm) if perm is not None else R
+    x64 = widen(np.asarray(x), x_dtype).astype(np.float64)
+    return Wh @ x64, np.abs(Wh) @ np.abs(x64)
+
+
 def residual(minuend: np.ndarray, codes: np.ndarray, book: np.ndarray, m_dtype: str = F32,
              c_dtype: str = F32) -> np.ndarray:
     """ComputeError of Alg. 1: E = minuend - C[q] (per vector, fp64), rounded to float32."""

@@ -393,3 +393,78 @@ def test_bits_printed_values():
     assert abs(v - 1.0678125) < 1e-9  # Eq. 8 as printed
     v1 = g["e"] / g["d"] + (g["m"] - 1) * g["lam"] * g["e"] / g["d"] + 2 ** (g["e"] - 20) * 1 * g["d"]
     assert abs(v1 - g["printed"]) <= g["printed_precision"]
+
+
+# ------------------------------------------------------------------------------------------------
+# matrix-vector product with a quantized layer (Sec. 4.3, Fig. 3 right)
+# ------------------------------------------------------------------------------------------------
+
+def _gemv_brute(M, N, d, n_crit, codes, books, perm, x):
+    """Element by element: W_hat[i, perm[k]] = sum over books of the codeword element, then the dot
+    product; Python integers / fractions-free loops on small integer data (exact)."""
+    vpr, ncv = N // d, n_crit // d
+    y = []
+    for i in range(M):
+        acc = 0
+        for k in range(N):
+            g, t = divmod(k, d)
+            w = int(books[0][codes[0][i * vpr + g]][t])
+            if g < ncv:
+                for b in range(1, len(books)):
+                    w += int(books[b][codes[b][i * ncv + g]][t])
+            col = int(perm[k]) if perm is not None else k
+            acc += w * int(x[col])
+        y.append(acc)
+    return np.array(y, dtype=np.float64)
+
+
+@pytest.mark.parametrize("n_ext,with_perm", [(0, False), (1, True), (3, True)])
+def test_gemv_bruteforce_integer(oracle_mod, n_ext, with_perm):
+    """Integer codebooks and input: every product and sum is exact in fp64, so the oracle must equal
+    the element-by-element brute force exactly (a dropped book, a wrong critical range, a transposed
+    permutation or a mis-indexed code all change some entry)."""
+    g = np.random.default_rng(71)
+    M, N, d, n_crit = 5, 48, 8, 16
+    K = [7] + [5] * n_ext
+    books = [g.integers(-9, 10, (k, d)).astype(np.float32) for k in K]
+    codes = [g.integers(0, K[0], M * N // d).astype(np.int32)] + \
+            [g.integers(0, K[b], M * n_crit // d).astype(np.int32) for b in range(1, 1 + n_ext)]
+    perm = g.permutation(N).astype(np.int32) if with_perm else None
+    x = g.integers(-5, 6, N).astype(np.float32)
+    y, a = oracle.gemv(M, N, d, n_crit, codes, books, perm, x)
+    np.testing.assert_array_equal(y, _gemv_brute(M, N, d, n_crit, codes, books, perm, x))
+    assert (a >= np.abs(y)).all()
+
+
+def test_gemv_permutation_identity(oracle_mod):
+    """Reordered storage (Sec. 4.2-4.3): W_hat x with W_hat[:, perm[k]] = R[:, k] equals R x[perm]."""
+    g = np.random.default_rng(72)
+    M, N, d, n_crit = 17, 64, 8, 24
+    books = [_rv(16, d, 73), _rv(8, d, 74, 0.1)]
+    codes = [g.integers(0, 16, M * N // d).astype(np.int32), g.integers(0, 8, M * n_crit // d).astype(np.int32)]
+    perm = g.permutation(N).astype(np.int32)
+    x = _rv(1, N, 75)[0]
+    y_perm, _ = oracle.gemv(M, N, d, n_crit, codes, books, perm, x)
+    y_sorted, _ = oracle.gemv(M, N, d, n_crit, codes, books, None, x[perm])
+    np.testing.assert_allclose(y_perm, y_sorted, rtol=1e-12, atol=1e-12)
+
+
+def test_gemv_matches_dense_reconstruction_bf16(oracle_mod):
+    """bf16 books and input: the product equals the dense reconstruction (weights summed in fp64
+    from the widened bf16 codewords) times the widened input."""
+    g = np.random.default_rng(76)
+    M, N, d, n_crit = 9, 32, 8, 8
+    b0 = inputs.f32_to_bf16_bits(_rv(32, d, 77))
+    b1 = _rv(4, d, 78, 0.01)
+    codes = [g.integers(0, 32, M * N // d).astype(np.int32), g.integers(0, 4, M * n_crit // d).astype(np.int32)]
+    xb = inputs.f32_to_bf16_bits(_rv(1, N, 79)[0])
+    y, _ = oracle.gemv(M, N, d, n_crit, codes, [b0, b1], None, xb, ["bf16", "f32"], "bf16")
+    W = np.zeros((M, N))
+    B0 = oracle.widen(b0, "bf16").astype(np.float64)
+    for i in range(M):
+        for gg in range(N // d):
+            W[i, gg * d:(gg + 1) * d] = B0[codes[0][i * (N // d) + gg]]
+            if gg < n_crit // d:
+                W[i, gg * d:(gg + 1) * d] += b1[codes[1][i * (n_crit // d) + gg]].astype(np.float64)
+    xw = oracle.widen(xb, "bf16").astype(np.float64)
+    np.testing.assert_allclose(y, W @ xw, rtol=1e-12, atol=1e-15)

@@ -277,6 +277,94 @@ def table(args):
         torch.cuda.empty_cache()
 
 
+# ------------------------------------------------------------------------------------------------
+# --gemv: y = W_hat x from 8-bit codes on the LLaMA gate projections the paper times (Table 7)
+# ------------------------------------------------------------------------------------------------
+GEMV_SHAPES = [("LLaMA-2-7B gate_proj", 11008, 4096), ("LLaMA-2-13B gate_proj", 13824, 5120),
+               ("LLaMA-30B gate_proj", 17920, 6656)]
+
+
+def gemv_bench(args):
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2412_09282_amd import crvq, inputs
+
+    crvq.lib(build_if_missing=True)
+    oracle.build()
+    cores = oracle.num_threads()
+    torch.cuda.set_device(0)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    reps = 20
+
+    def timed(fn):
+        ts = []
+        for r in range(reps + 3):
+            flush.fill_(r)
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if r >= 3:
+                ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts))
+
+    for name, M, N in GEMV_SHAPES:
+        d = 8
+        n_crit = inputs.n_crit_columns(N, d, 0.02)
+        ncv = n_crit // d
+        g = np.random.default_rng([inputs.ROOT_SEED, M, N])
+        for n_ext in (0, 1, 3):
+            log(f"gemv: {name} {M}x{N}, 8+8x{n_ext}")
+            books = [inputs.f32_to_bf16_bits(inputs.random_vectors(256, d, 500 + e, 0.02 if e == 0 else 0.005))
+                     for e in range(1 + n_ext)]
+            codes = [g.integers(0, 256, M * N // d).astype(np.uint8)] + \
+                    [g.integers(0, 256, M * ncv).astype(np.uint8) for _ in range(n_ext)]
+            perm = g.permutation(N).astype(np.int32)
+            x = inputs.f32_to_bf16_bits(inputs.random_vectors(1, N, 510, 1.0)[0])
+            bt = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+            Bd = [bt(b) for b in books]
+            Qd = [torch.from_numpy(c).cuda() for c in codes]
+            Pd = torch.from_numpy(perm).cuda()
+            Xd = bt(x)
+            y = torch.empty(M, dtype=torch.float32, device="cuda")
+            call = lambda: crvq.crvq_dequant_gemv(M, N, Qd[0], N // d, Bd[0], Xd, y, n_crit=n_crit, q_ext=Qd[1:],
+                                                  ldq_ext=max(1, ncv), C_ext=Bd[1:], perm=Pd)
+            call()
+            torch.cuda.synchronize()
+            ms = timed(call)
+            # the same layer as dense bf16 weights (the library's reconstruction in original column
+            # order) through torch's matrix-vector product: the 16-bit baseline of the paper's table
+            Wd = torch.empty(M, N, dtype=torch.bfloat16, device="cuda")
+            q32 = [q.to(torch.int32) for q in Qd]
+            crvq.crvq_dequant(M, N, d, q32[0], N // d, Bd[0], Wd, n_crit=n_crit, q_ext=q32[1:], ldq_ext=max(1, ncv),
+                              C_ext=Bd[1:], perm=Pd)
+            torch.cuda.synchronize()
+            ms_dense = timed(lambda: torch.mv(Wd, Xd))
+            del Wd, q32
+            t0 = time.perf_counter()
+            exp, a = oracle.gemv(M, N, d, n_crit, [c.astype(np.int32) for c in codes], books, perm, x,
+                                 ["bf16"] * (1 + n_ext), "bf16")
+            t_or = time.perf_counter() - t0
+            got = y.cpu().numpy().astype(np.float64)
+            worst = float((np.abs(got - exp) / (a + 1e-300)).max())
+            nbytes = M * N // d + n_ext * M * ncv + 2 * N + 4 * M + 4 * N + sum(b.size * 2 for b in books)
+            rate = nbytes / (ms * 1e-3)
+            print(json.dumps({
+                "workload": f"{name} {M}x{N}, 8+8x{n_ext}, lambda 2 % ({n_crit} critical columns), bf16 books and x",
+                "call": "crvq_dequant_gemv", "gpu_us": round(ms * 1e3, 2), "bytes": nbytes,
+                "GB/s": round(rate / 1e9, 1), "frac_hbm": rate / (PEAK_HBM_GBS * 1e9),
+                "dense_bf16_mv_us": round(ms_dense * 1e3, 2), "dense_bytes": 2 * M * N,
+                "speedup_vs_dense_bf16": ms_dense / ms,
+                "oracle_s": round(t_or, 3), "oracle_weights_per_s": M * N / t_or, "cores": cores,
+                "parity_worst_err_over_sum_abs": worst, "parity_ok": bool(worst <= 1e-5)}), flush=True)
+            del Bd, Qd, Xd, y
+            torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -290,6 +378,9 @@ def main():
                     help="instead of the benchmark line: one JSON record per library call of one layer pass of each "
                          "--workloads entry, GPU time beside the oracle's on the same inputs, with parity")
     ap.add_argument("--workloads", default="1,2,3,4,5")
+    ap.add_argument("--gemv", action="store_true",
+                    help="instead of the benchmark line: the quantized matrix-vector product on the LLaMA gate "
+                         "projections, beside a dense bf16 matrix-vector product and the oracle")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
@@ -297,6 +388,9 @@ def main():
 
     if args.table:
         table(args)
+        return
+    if args.gemv:
+        gemv_bench(args)
         return
 
     import numpy as np

@@ -207,6 +207,38 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
                          const void* minuend, int minuend_dtype, int64_t ld_min, void* out, int out_dtype,
                          int64_t ld_out, void* workspace, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------------------------------------
+ * crvq_dequant_gemv -- matrix-vector product with a CRVQ-quantized layer, the
+ * inference step the paper times (Sec. 4.3, Fig. 3 right; Table 7):
+ *
+ *   y = W_hat x,   W_hat[:, perm[k]] = R[:, k]   (W_hat = R when perm is NULL),
+ *   R[r, 8g+t] = C_base[q_base[r*ldq_base+g]][t]
+ *                + sum_{e < n_ext, g < n_crit/8} C_ext[e][q_ext[e][r*ldq_ext+g]][t]
+ *
+ * for an M x N layer stored as 8-bit codes (every book has K <= 256, d = 8),
+ * x of N elements (x_dtype), y of M floats.  N must be a multiple of 64;
+ * q_base 8-byte aligned with ldq_base a multiple of 8 and >= N/8; n_crit a
+ * multiple of 8 in [0, N].  Products are formed in fp32 (codeword elements and
+ * x widened exactly; per column group an 8-term fp32 dot product), partial sums
+ * in fp32 over at most 1024 columns and in fp64 across them: |y - W_hat x| is
+ * within a few times 2^-24 * sum_j |W_hat_rj x_j|.  A code outside its book or
+ * a perm entry outside [0, N) makes y_r NaN.  M = 0 is a no-op.  Deterministic.
+ * workspace: crvq_gemv_workspace_size(M, N, K_base) bytes.
+ */
+size_t crvq_gemv_workspace_size(int64_t M, int64_t N, int64_t K_base);
+crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_t* q_base, int64_t ldq_base,
+                              const void* C_base, int base_dtype, int64_t K_base, int32_t n_ext,
+                              const uint8_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
+                              const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* x,
+                              int x_dtype, float* y, void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_pack_codes_u8 -- 8-bit storage of codes (the e = 8 code width of Sec. 3.2
+ * Eq. 6 / Appendix A.1): out[i] = codes[i] & 255 for i < n.  Codes produced
+ * against a book of K <= 256 codewords lie in [0, K) and are stored exactly.
+ */
+crvq_status crvq_pack_codes_u8(const int32_t* codes, int64_t n, uint8_t* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

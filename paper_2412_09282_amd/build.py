@@ -28,6 +28,7 @@ SOURCES = {
     "k_colreduce.hip": [],
     "k_reorder.hip": [],
     "k_dequant.hip": [],
+    "k_gemv.hip": [],
 }
 
 COMMON = [

@@ -64,6 +64,10 @@ def lib(build_if_missing: bool = True):
                 "crvq_dequant_workspace_size": ([I64], SZ),
                 "crvq_dequant": ([I64, I64, I32, I64, P, I64, P, ctypes.c_int, I64, I32, PP, I64, PP, P, P, P, P, ctypes.c_int,
                                   I64, P, ctypes.c_int, I64, P, SZ, P], ctypes.c_int),
+                "crvq_gemv_workspace_size": ([I64, I64, I64], SZ),
+                "crvq_dequant_gemv": ([I64, I64, I64, P, I64, P, ctypes.c_int, I64, I32, PP, I64, PP, P, P, P, P,
+                                       ctypes.c_int, P, P, SZ, P], ctypes.c_int),
+                "crvq_pack_codes_u8": ([P, I64, P, P], ctypes.c_int),
             }
             for name, (args, res) in sigs.items():
                 f = getattr(L, name)
@@ -232,3 +236,25 @@ def crvq_dequant(M: int, n_cols: int, d: int, q_base: torch.Tensor, ldq_base: in
         _ptr(perm), _ptr(minuend), CRVQ_F32 if minuend is None else dtype_code(minuend),
         0 if minuend is None else minuend.stride(0), _ptr(out), dtype_code(out), out.stride(0), _ptr(ws),
         0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_pack_codes_u8(codes: torch.Tensor, out: torch.Tensor, stream=None) -> None:
+    assert codes.dtype == torch.int32 and out.dtype == torch.uint8 and out.numel() >= codes.numel()
+    _check("crvq_pack_codes_u8", lib().crvq_pack_codes_u8(_ptr(codes), codes.numel(), _ptr(out), _stream(stream)))
+
+
+def crvq_dequant_gemv(M: int, N: int, q_base: torch.Tensor, ldq_base: int, C_base: torch.Tensor, x: torch.Tensor,
+                      y: torch.Tensor, n_crit: int = 0, q_ext: Sequence[torch.Tensor] = (), ldq_ext: int = 0,
+                      C_ext: Sequence[torch.Tensor] = (), perm: Optional[torch.Tensor] = None, stream=None) -> None:
+    """y = W_hat x for a layer stored as 8-bit codes (uint8 tensors); see include/crvq.h."""
+    L = lib()
+    ne = len(C_ext)
+    ws = _workspace(L.crvq_gemv_workspace_size(M, N, C_base.shape[0]), y.device)
+    dts = (ctypes.c_int32 * max(1, ne))(*[dtype_code(c) for c in C_ext])
+    Ks = (ctypes.c_int64 * max(1, ne))(*[c.shape[0] for c in C_ext])
+    _check("crvq_dequant_gemv", L.crvq_dequant_gemv(
+        M, N, n_crit, _ptr(q_base), ldq_base, _ptr(C_base), dtype_code(C_base), C_base.shape[0], ne,
+        ctypes.cast(_ptr_array(q_ext), ctypes.POINTER(ctypes.c_void_p)) if ne else None, ldq_ext,
+        ctypes.cast(_ptr_array(C_ext), ctypes.POINTER(ctypes.c_void_p)) if ne else None,
+        ctypes.cast(dts, ctypes.c_void_p) if ne else None, ctypes.cast(Ks, ctypes.c_void_p) if ne else None,
+        _ptr(perm), _ptr(x), dtype_code(x), _ptr(y), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))

@@ -408,3 +408,62 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------------------------------------------------
+size_t crvq_gemv_workspace_size(int64_t M, int64_t N, int64_t K_base) {
+  if (M < 1 || N < 64 || K_base < 1 || K_base > 256) return 0;
+  return gemv_ws_bytes(M, N, static_cast<int>(K_base));
+}
+
+crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_t* q_base, int64_t ldq_base,
+                              const void* C_base, int base_dtype, int64_t K_base, int32_t n_ext,
+                              const uint8_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
+                              const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* x,
+                              int x_dtype, float* y, void* workspace, size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_dequant_gemv";
+  g_err.clear();
+  if (M < 0 || N < 1) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and N >= 1", fn);
+  if (N % 64) return fail(CRVQ_ERR_UNSUPPORTED, "%s: N = %lld is not a multiple of 64", fn, (long long)N);
+  if (n_crit < 0 || n_crit > N || n_crit % 8)
+    return fail(CRVQ_ERR_INVALID, "%s: n_crit = %lld must be a multiple of 8 in [0, N]", fn, (long long)n_crit);
+  if (M == 0) return CRVQ_OK;  // no rows: nothing to compute or write
+  if (!q_base || !C_base || !x || !y) return fail(CRVQ_ERR_INVALID, "%s: q_base, C_base, x and y must not be NULL", fn);
+  if (!dtype_ok(base_dtype) || !dtype_ok(x_dtype)) return fail(CRVQ_ERR_INVALID, "%s: invalid base or x dtype", fn);
+  if (K_base < 1 || K_base > 256) return fail(CRVQ_ERR_UNSUPPORTED, "%s: K_base = %lld outside [1, 256] (8-bit codes)", fn, (long long)K_base);
+  if (ldq_base < N / 8 || ldq_base % 8 || (reinterpret_cast<uintptr_t>(q_base) & 7))
+    return fail(CRVQ_ERR_INVALID, "%s: q_base must be 8-byte aligned with ldq_base >= N/8 and a multiple of 8", fn);
+  if (n_ext < 0 || n_ext > CRVQ_MAX_BOOKS - 1)
+    return fail(CRVQ_ERR_INVALID, "%s: n_ext = %d outside [0, %d]", fn, n_ext, CRVQ_MAX_BOOKS - 1);
+  GemvExt ext = {};
+  ext.n = n_ext;
+  ext.ldq = ldq_ext;
+  if (n_ext > 0) {
+    if (!q_ext || !C_ext || !ext_dtypes || !K_ext)
+      return fail(CRVQ_ERR_INVALID, "%s: q_ext, C_ext, ext_dtypes and K_ext must not be NULL when n_ext > 0", fn);
+    if (ldq_ext < n_crit / 8) return fail(CRVQ_ERR_INVALID, "%s: ldq_ext < n_crit / 8", fn);
+    for (int e = 0; e < n_ext; ++e) {
+      if (!q_ext[e] || !C_ext[e]) return fail(CRVQ_ERR_INVALID, "%s: q_ext[%d] or C_ext[%d] is NULL", fn, e, e);
+      if (!dtype_ok(ext_dtypes[e])) return fail(CRVQ_ERR_INVALID, "%s: ext_dtypes[%d] invalid", fn, e);
+      if (K_ext[e] < 1 || K_ext[e] > 256)
+        return fail(CRVQ_ERR_UNSUPPORTED, "%s: K_ext[%d] = %lld outside [1, 256] (8-bit codes)", fn, e, (long long)K_ext[e]);
+      ext.C[e] = C_ext[e];
+      ext.q[e] = q_ext[e];
+      ext.type[e] = ext_dtypes[e];
+      ext.K[e] = static_cast<int>(K_ext[e]);
+    }
+  }
+  crvq_status s;
+  if ((s = check_ws(workspace, ws_bytes, crvq_gemv_workspace_size(M, N, K_base), fn))) return s;
+  return hip_status(launch_gemv(M, N, n_crit, q_base, ldq_base, C_base, base_dtype, static_cast<int>(K_base), ext, perm,
+                                x, x_dtype, y, workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+crvq_status crvq_pack_codes_u8(const int32_t* codes, int64_t n, uint8_t* out, void* stream) {
+  static const char* fn = "crvq_pack_codes_u8";
+  g_err.clear();
+  if (n < 0) return fail(CRVQ_ERR_INVALID, "%s: n < 0", fn);
+  if (n == 0) return CRVQ_OK;
+  if (!codes || !out) return fail(CRVQ_ERR_INVALID, "%s: codes and out must not be NULL", fn);
+  return hip_status(launch_pack_codes_u8(codes, n, out, static_cast<hipStream_t>(stream)), fn);
+}

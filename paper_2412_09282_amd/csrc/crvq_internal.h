@@ -153,4 +153,27 @@ hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, cons
                           const int32_t* inv_perm, const int32_t* perm, const void* minuend, int min_type,
                           int64_t ld_min, void* out, int out_type, int64_t ld_out, hipStream_t stream);
 
+// ---- matrix-vector product with a quantized layer (k_gemv.hip) -----------------------------------
+struct GemvExt {
+  const void* C[8];
+  const uint8_t* q[8];
+  int type[8];
+  int K[8];
+  int n;        // extended books
+  int64_t ldq;  // row stride of their code arrays
+};
+struct GemvPlan {
+  int G;                   // groups per lane; a slice is 16 G groups
+  int n_slices;
+  size_t lds;              // bytes of LDS per workgroup (table, codebook, xs)
+  int64_t rows_per_block;  // a multiple of 32
+  int64_t row_blocks;
+};
+GemvPlan plan_gemv(int64_t M, int64_t N, int K_base);
+size_t gemv_ws_bytes(int64_t M, int64_t N, int K_base);
+hipError_t launch_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_t* q_base, int64_t ldq_base, const void* C_base,
+                       int base_type, int K_base, const GemvExt& ext, const int32_t* perm, const void* x, int x_type,
+                       float* y, void* ws, hipStream_t stream);
+hipError_t launch_pack_codes_u8(const int32_t* codes, int64_t n, uint8_t* out, hipStream_t stream);
+
 }  // namespace crvq

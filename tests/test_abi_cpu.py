@@ -131,6 +131,48 @@ def _imports(path):
     return set(re.findall(r"^\s*(?:from|import)\s+([\w\.]+)", src, re.M))
 
 
+def test_gemv_validation(L):
+    """crvq_dequant_gemv / crvq_pack_codes_u8 reject bad arguments before touching the device."""
+    ws = ctypes.c_void_p(0x100000)
+    big = 1 << 30
+    q8 = ctypes.c_void_p(0x2000)  # 8-byte aligned
+    ok = lambda **kw: dict(dict(M=16, N=128, n_crit=16, q=q8, ldq=16, C=FAKE, bdt=0, K=256, ne=0, qe=None, ldqe=0,
+                                Ce=None, edt=None, Ke=None, perm=None, x=FAKE, xdt=0, y=FAKE, ws=ws, wsb=big), **kw)
+    call = lambda a: L.crvq_dequant_gemv(a["M"], a["N"], a["n_crit"], a["q"], a["ldq"], a["C"], a["bdt"], a["K"],
+                                         a["ne"], a["qe"], a["ldqe"], a["Ce"], a["edt"], a["Ke"], a["perm"], a["x"],
+                                         a["xdt"], a["y"], a["ws"], a["wsb"], None)
+    assert call(ok(N=120)) == 2 and "multiple of 64" in err(L)
+    assert call(ok(n_crit=12)) == 1
+    assert call(ok(n_crit=136)) == 1
+    assert call(ok(K=257)) == 2 and "8-bit" in err(L)
+    assert call(ok(K=0)) == 2
+    assert call(ok(ldq=15)) == 1
+    assert call(ok(ldq=12)) == 1
+    assert call(ok(q=ctypes.c_void_p(0x2001))) == 1 and "aligned" in err(L)
+    assert call(ok(x=None)) == 1
+    assert call(ok(y=None)) == 1
+    assert call(ok(bdt=3)) == 1
+    assert call(ok(ne=8)) == 1
+    assert call(ok(ne=1)) == 1 and "must not be NULL" in err(L)
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    qe = (ctypes.c_void_p * 1)(0x3000)
+    ce = (ctypes.c_void_p * 1)(0x4000)
+    edt = (ctypes.c_int32 * 1)(0)
+    kbad = (ctypes.c_int64 * 1)(300)
+    ext = dict(ne=1, qe=ctypes.cast(qe, PP), ldqe=2, Ce=ctypes.cast(ce, PP), edt=ctypes.cast(edt, ctypes.c_void_p),
+               Ke=ctypes.cast(kbad, ctypes.c_void_p))
+    assert call(ok(**ext)) == 2 and "K_ext" in err(L)
+    kok = (ctypes.c_int64 * 1)(256)
+    ext["Ke"] = ctypes.cast(kok, ctypes.c_void_p)
+    assert call(ok(**dict(ext, ldqe=1))) == 1 and "ldq_ext" in err(L)
+    need = L.crvq_gemv_workspace_size(16, 128, 256)
+    assert need > 0 and L.crvq_gemv_workspace_size(16, 128, 300) == 0
+    assert call(ok(wsb=need - 1)) == 3
+    assert L.crvq_pack_codes_u8(FAKE, -1, FAKE, None) == 1
+    assert L.crvq_pack_codes_u8(None, 4, FAKE, None) == 1
+    assert L.crvq_pack_codes_u8(None, 0, None, None) == 0
+
+
 def test_oracle_and_gpu_path_share_no_code():
     odir = os.path.join(ROOT, "oracle")
     pdir = os.path.join(ROOT, "paper_2412_09282_amd")

@@ -164,12 +164,15 @@ struct GemvExt {
 };
 struct GemvPlan {
   int G;                   // groups per lane; a slice is 16 G groups
+  int fused;               // 1: the finishing kernel looks the extended codes up in LDS tables
   int n_slices;
-  size_t lds;              // bytes of LDS per workgroup (table, codebook, xs)
+  size_t lds;              // bytes of LDS per slice workgroup (table, xs)
+  size_t ext_lds;          // bytes of LDS of the extended-book workgroups' tables
+  int ext_cols;            // columns of workgroups for the extended books (0: none)
   int64_t rows_per_block;  // a multiple of 32
   int64_t row_blocks;
 };
-GemvPlan plan_gemv(int64_t M, int64_t N, int K_base);
+GemvPlan plan_gemv(int64_t M, int64_t N, int K_base, int64_t ncv, int ext_K_sum, int n_ext);
 size_t gemv_ws_bytes(int64_t M, int64_t N, int K_base);
 hipError_t launch_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_t* q_base, int64_t ldq_base, const void* C_base,
                        int base_type, int K_base, const GemvExt& ext, const int32_t* perm, const void* x, int x_type,

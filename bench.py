@@ -144,7 +144,7 @@ def table(args):
         Xd = torch.from_numpy(X).cuda()
         bi = torch.from_numpy(base_idx).cuda()
         ei = [torch.from_numpy(e).cuda() for e in ext_idx]
-        cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
+        cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, importance=args.importance)
         q = LayerQuantizer(M, N, tdt, cfg, L.tokens, device="cuda")
         q.run(Wd, Xd, bi, ei)  # warm-up pass
         torch.cuda.synchronize()
@@ -160,7 +160,8 @@ def table(args):
 
         def rec(call, gpu_ms, calls, work, unit, peak, oracle_s, sample_frac, parity, **extra):
             rate = work / (gpu_ms * 1e-3)
-            out = {"workload": wid, "layer": f"{L.name} {M}x{N} {dt}", "call": call, "calls": calls,
+            out = {"workload": wid, "layer": f"{L.name} {M}x{N} {dt}", "importance": args.importance,
+                   "call": call, "calls": calls,
                    "gpu_ms": round(gpu_ms, 4), "bound": "hbm" if unit == "B" else "mfma",
                    "work_per_call": work, "work_unit": unit,
                    "gpu_rate": rate, "frac": rate / peak,
@@ -183,11 +184,26 @@ def table(args):
                 rec("channel_importance (Hessian diagonal)", ms, len(calls), X.size * 4 + N * 4, "B", HBM, ts, 1.0,
                     "1e-5 rel" if ok else "FAIL")
             elif kind == "importance":
-                exp = oracle.colreduce(W, scale=c["in"]["scale"].astype(np.float64), dtype=dt)
+                if "B" in c["in"]:  # W-A: max_i (W - Wq)^2 scaled by h
+                    exp = oracle.colreduce(W, c["in"]["B"], scale=c["in"]["scale"].astype(np.float64), reduce="max",
+                                           dtype=dt)
+                    what, nb = "channel_importance (W - Wq, max, scale = h)", 2 * M * N * es + 2 * N * 4
+                elif "scale" in c["in"]:
+                    exp = oracle.colreduce(W, scale=c["in"]["scale"].astype(np.float64), dtype=dt)
+                    what, nb = "channel_importance (W, scale = h)", M * N * es + 2 * N * 4
+                else:
+                    exp = oracle.colreduce(W, reduce="max", dtype=dt)
+                    what, nb = "channel_importance (W, max)", M * N * es + N * 4
                 ts = time.perf_counter() - t0
                 ok = np.all(np.abs(c["out"]["out"] - exp) <= 1e-5 * np.abs(exp))
-                rec("channel_importance (W, scale = h)", ms, len(calls), M * N * es + 2 * N * 4, "B", HBM, ts, 1.0,
-                    "1e-5 rel" if ok else "FAIL")
+                rec(what, ms, len(calls), nb, "B", HBM, ts, 1.0, "1e-5 rel" if ok else "FAIL")
+            elif kind == "prequant":
+                R = oracle.reconstruct([c["in"]["codes"].ravel()], [c["in"]["book"]], np.zeros(n, np.uint8), [dt])
+                exp = oracle.round_to(R, dt).reshape(M, N)
+                ts = time.perf_counter() - t0
+                ok = np.array_equal(c["out"]["out"], exp)
+                rec("dequant (prequantized W, original order)", ms, len(calls),
+                    M * N * es + 4 * n + c["in"]["book"].size * es, "B", HBM, ts, 1.0, "bitwise" if ok else "FAIL")
             elif kind == "reorder":
                 perm = oracle.rank_perm(c["in"]["importance"])
                 Ws_exp = oracle.gather_columns(W, perm)
@@ -198,8 +214,9 @@ def table(args):
                     "bitwise" if ok else "FAIL")
             elif kind.startswith("assign"):
                 base = kind.startswith("assign_base")
-                Xh = Ws if base else c["in"]["X"]
-                vdt = dt if base else "f32"
+                pre = kind.startswith("assign_pre")
+                Xh = Ws if base else (W if pre else c["in"]["X"])
+                vdt = dt if (base or pre) else "f32"
                 V = oracle.vectors(np.ascontiguousarray(Xh), d)
                 Cb = c["in"]["C"]
                 K = Cb.shape[0]
@@ -214,8 +231,9 @@ def table(args):
                     vectors=V.shape[0], K=K, sampled_vectors=k)
             elif kind.startswith("update"):
                 base = kind.startswith("update_base")
-                Xh = Ws if base else c["in"]["X"]
-                vdt = dt if base else "f32"
+                pre = kind.startswith("update_pre")
+                Xh = Ws if base else (W if pre else c["in"]["X"])
+                vdt = dt if (base or pre) else "f32"
                 V = oracle.vectors(np.ascontiguousarray(Xh), d)
                 Cexp, cnt, _ = oracle.kmeans_update(V, c["in"]["codes"], c["in"]["C"], vdt, vdt)
                 ts = time.perf_counter() - t0
@@ -378,6 +396,8 @@ def main():
                     help="instead of the benchmark line: one JSON record per library call of one layer pass of each "
                          "--workloads entry, GPU time beside the oracle's on the same inputs, with parity")
     ap.add_argument("--workloads", default="1,2,3,4,5")
+    ap.add_argument("--importance", default="energy", choices=["energy", "w_only", "wa"],
+                    help="channel-importance strategy of the --table layer passes")
     ap.add_argument("--gemv", action="store_true",
                     help="instead of the benchmark line: the quantized matrix-vector product on the LLaMA gate "
                          "projections, beside a dense bf16 matrix-vector product and the oracle")

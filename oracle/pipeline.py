@@ -9,9 +9,13 @@ the paper's order:
   vectors -> reconstruction with the reverse reordering.
 
 Readings where the paper is silent (each also listed in the design notes):
-* importance: I_j = h_j * sum_i W_ij^2 with h = diag(X X^T) (the timed
-  workloads' metric; the paper's Eq. 7 / Eq. 10 forms are modes of
-  ``colreduce`` and are pinned separately);
+* importance (``importance=``): "energy" I_j = h_j * sum_i W_ij^2 with
+  h = diag(X X^T) (the timed workloads' metric); "w_only" I_j = max_i W_ij^2
+  (Sec. 4.1); "wa" the Hessian-proxy metric of Sec. 4.1 in the unpacked form of
+  Appendix A.2 Eq. 10, I_j = h_j * max_i (W_ij - Wq_ij)^2 with Wq the
+  prequantized W (Alg. 1 Prequantize: the basic VQ -- same K, init indices and
+  iterations -- on the unsorted W); Eq. 10's factor 1/2 is the same for every
+  channel and changes no ordering, so it is left out;
 * critical channels: the first d * ceil(lambda N / d) reordered columns;
 * K-means: initial codewords are the vectors at seeded indices (an input);
   one iteration = assign + update; ``iters`` iterations then a final assign;
@@ -68,12 +72,36 @@ def kmeans(V: np.ndarray, C0: np.ndarray, iters: int, v_dtype: str, c_dtype: str
     return C, q, dist, J
 
 
+def prequantize(W: np.ndarray, dtype: str, d: int, base_idx: np.ndarray, iters: int) -> np.ndarray:
+    """Alg. 1 Prequantize: the basic VQ of the unsorted W (K-means from the vectors at base_idx,
+    `iters` iterations, final assignment), reconstructed in W's storage type."""
+    V = vectors(W, d)
+    C, q, _, _ = kmeans(V, np.ascontiguousarray(V[base_idx]), iters, dtype, dtype)
+    R = reconstruct([q], [C], np.zeros(len(q), np.uint8), [dtype])
+    return round_to(R, dtype).reshape(W.shape)
+
+
+def channel_importance(W: np.ndarray, h: np.ndarray, dtype: str, mode: str, d: int = 8,
+                       base_idx: Optional[np.ndarray] = None, iters: int = 1) -> np.ndarray:
+    """Channel importance of Sec. 4.1 (modes as in the module notes), rounded to float32."""
+    if mode == "energy":
+        I = colreduce(W, scale=h.astype(np.float64), reduce="sum", dtype=dtype)
+    elif mode == "w_only":
+        I = colreduce(W, reduce="max", dtype=dtype)
+    elif mode == "wa":
+        Wq = prequantize(W, dtype, d, base_idx, iters)
+        I = colreduce(W, Wq, scale=h.astype(np.float64), reduce="max", dtype=dtype)
+    else:
+        raise ValueError(mode)
+    return round_to(I, F32)
+
+
 def quantize_layer(W: np.ndarray, X: np.ndarray, dtype: str, d: int, K_base: int, K_ext: List[int],
                    crit_frac: float, width: int, iters: int, base_idx: np.ndarray,
-                   ext_idx: List[np.ndarray]) -> LayerResult:
+                   ext_idx: List[np.ndarray], importance: str = "energy") -> LayerResult:
     M, N = W.shape
     h = round_to(colreduce(X, reduce="sum"), F32)
-    I = round_to(colreduce(W, scale=h.astype(np.float64), reduce="sum", dtype=dtype), F32)
+    I = channel_importance(W, h, dtype, importance, d, base_idx, iters)
     perm = rank_perm(I)
     Ws = gather_columns(W, perm)
     n_crit = n_crit_columns(N, d, crit_frac)

@@ -7,7 +7,12 @@ Update on the critical groups -> beam search over all codebooks for the
 critical vectors -> reconstruction with the reverse reordering.
 
 Readings where the paper leaves a choice open (shared with the design notes):
-importance I_j = h_j * sum_i W_ij^2 with h = diag(X X^T); the critical channels
+importance (LayerConfig.importance): "energy" I_j = h_j * sum_i W_ij^2 with
+h = diag(X X^T) (the timed workloads), "w_only" I_j = max_i W_ij^2 (Sec. 4.1),
+"wa" I_j = h_j * max_i (W_ij - Wq_ij)^2 with Wq the prequantized W (Alg. 1
+Prequantize: the basic VQ of the unsorted W; the Hessian-proxy metric of
+Sec. 4.1 in the unpacked form of Appendix A.2 Eq. 10 without its uniform
+factor 1/2); the critical channels
 are the first d * ceil(lambda N / d) reordered columns; K-means starts from the
 vectors at given indices, one iteration is assign + update, `iters` iterations
 are followed by a final assign, an empty cluster keeps its centroid; stored
@@ -40,6 +45,7 @@ class LayerConfig:
     crit_frac: float
     beam: int
     iters: int
+    importance: str = "energy"  # "energy" | "w_only" | "wa"
 
 
 def n_crit_columns(N: int, d: int, frac: float) -> int:
@@ -85,6 +91,12 @@ class LayerQuantizer:
         self.codes_ext = [torch.empty(M * self.ncv, dtype=i32, device=device) for _ in cfg.K_ext]
         self.beam_err = torch.empty(M * self.ncv, dtype=f32, device=device)
         self.W_hat = torch.empty(M, N, dtype=dtype, device=device)
+        if cfg.importance not in ("energy", "w_only", "wa"):
+            raise ValueError(f"importance {cfg.importance!r}")
+        if cfg.importance == "wa":  # Prequantize buffers: the basic VQ of the unsorted W
+            self.C_pre = torch.empty(cfg.K_base, d, dtype=dtype, device=device)
+            self.codes_pre = torch.empty(self.n, dtype=i32, device=device)
+            self.W_pre = torch.empty(M, N, dtype=dtype, device=device)
 
     def run(self, W: torch.Tensor, X: torch.Tensor, base_idx: torch.Tensor, ext_idx: List[torch.Tensor],
             trace: Optional[list] = None, hooks=()) -> LayerState:
@@ -98,8 +110,25 @@ class LayerQuantizer:
         C.crvq_channel_importance(X, self.hdiag)
         rec.post("hdiag", out=self.hdiag)
 
-        rec.pre("importance", A=W, scale=self.hdiag)
-        C.crvq_channel_importance(W, self.imp, scale=self.hdiag)
+        if cfg.importance == "energy":
+            rec.pre("importance", A=W, scale=self.hdiag)
+            C.crvq_channel_importance(W, self.imp, scale=self.hdiag)
+        elif cfg.importance == "w_only":
+            rec.pre("importance", A=W)
+            C.crvq_channel_importance(W, self.imp, reduce=C.CRVQ_REDUCE_MAX)
+        else:
+            # Alg. 1 Prequantize: K-means + final assign + reconstruction of the unsorted W
+            Vu = VecSet.of_matrix(W, d)
+            C.crvq_gather_vectors(Vu, base_idx, self.C_pre)
+            self._kmeans(Vu, self.C_pre, self.codes_pre, rec, "pre")
+            rec.pre("assign_pre_final", X=W, C=self.C_pre)
+            C.crvq_assign(Vu, self.C_pre, self.codes_pre)
+            rec.post("assign_pre_final", codes=self.codes_pre)
+            rec.pre("prequant", codes=self.codes_pre, book=self.C_pre)
+            C.crvq_dequant(M, N, d, self.codes_pre, N // d, self.C_pre, self.W_pre)
+            rec.post("prequant", out=self.W_pre)
+            rec.pre("importance", A=W, B=self.W_pre, scale=self.hdiag)
+            C.crvq_channel_importance(W, self.imp, B=self.W_pre, scale=self.hdiag, reduce=C.CRVQ_REDUCE_MAX)
         rec.post("importance", out=self.imp)
 
         rec.pre("reorder", inp=W, importance=self.imp)

@@ -468,3 +468,45 @@ def test_gemv_matches_dense_reconstruction_bf16(oracle_mod):
                 W[i, gg * d:(gg + 1) * d] += b1[codes[1][i * (n_crit // d) + gg]].astype(np.float64)
     xw = oracle.widen(xb, "bf16").astype(np.float64)
     np.testing.assert_allclose(y, W @ xw, rtol=1e-12, atol=1e-15)
+
+
+# ------------------------------------------------------------------------------------------------
+# importance strategies of Sec. 4.1 / Table 2 (W-only, W-A with prequantization)
+# ------------------------------------------------------------------------------------------------
+
+def test_wa_importance_is_unpacked_eq10(oracle_mod):
+    """W-A importance against the unpacked Hessian-proxy form (Appendix A.2 Eq. 10), element by
+    element from the activations themselves: I_i = max_j 1/2 sum_k (x_ik dw_ji)^2 with
+    dw = W - VQ(W); the pipeline leaves the uniform factor 1/2 out (an ordering-invariant scale)."""
+    g = np.random.default_rng(81)
+    M, N, T, d = 6, 16, 5, 8
+    W = (g.standard_normal((M, N)) * 0.02).astype(np.float32)
+    X = g.standard_normal((T, N)).astype(np.float32)     # tokens x N (the paper's X transposed)
+    base_idx = np.array([0, 5, 7], dtype=np.int64)        # K = 3 codewords from the unsorted vectors
+    h = oracle.round_to(oracle.colreduce(X), "f32")
+    got = opipe.channel_importance(W, h, "f32", "wa", d, base_idx, iters=2)
+    Wq = opipe.prequantize(W, "f32", d, base_idx, 2)
+    dw = W.astype(np.float64) - Wq.astype(np.float64)
+    brute = np.array([max(0.5 * sum((float(X[k, i]) * dw[j, i]) ** 2 for k in range(T)) for j in range(M))
+                      for i in range(N)])
+    np.testing.assert_allclose(got.astype(np.float64), 2.0 * brute, rtol=2e-6, atol=0)
+    assert np.argsort(-got, kind="stable").tolist() == np.argsort(-brute, kind="stable").tolist()
+
+
+def test_prequantize_exact_with_every_vector_as_codeword(oracle_mod):
+    """A basic book holding every (distinct) vector reconstructs W exactly, so the W-A importance is 0."""
+    g = np.random.default_rng(82)
+    M, N, d = 4, 24, 8
+    W = (g.standard_normal((M, N)) * 0.02).astype(np.float32)
+    n = M * N // d
+    Wq = opipe.prequantize(W, "f32", d, np.arange(n), iters=3)
+    np.testing.assert_array_equal(Wq, W)
+    h = np.ones(N, np.float32)
+    assert (opipe.channel_importance(W, h, "f32", "wa", d, np.arange(n), 3) == 0).all()
+
+
+def test_w_only_importance_is_max_square(oracle_mod):
+    g = np.random.default_rng(83)
+    W = (g.standard_normal((33, 40)) * 0.02).astype(np.float32)
+    got = opipe.channel_importance(W, np.ones(40, np.float32), "f32", "w_only")
+    np.testing.assert_array_equal(got, (W.astype(np.float64) ** 2).max(0).astype(np.float32))

@@ -126,7 +126,7 @@ def table(args):
     torch.cuda.set_device(0)
     flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     for wid in [int(w) for w in args.workloads.split(",")]:
-        wl = inputs.WORKLOADS[wid]
+        wl = inputs.workload(wid)
         L = wl.layers[0]
         M, N, d = L.M, L.N, wl.d
         n = M * N // d
@@ -139,17 +139,32 @@ def table(args):
         ncv_total = M * n_crit // d
         base_idx = inputs.base_init_indices(wl, 0, n)
         ext_idx = [inputs.ext_init_indices(wl, 0, t, ncv_total) for t in range(1, len(wl.K_ext) + 1)]
+        extra_idx = [inputs.extra_base_init_indices(wl, 0, b, n) for b in range(1, wl.m_base)]
         tdt = torch.bfloat16 if dt == "bf16" else torch.float32
         Wd = (torch.from_numpy(W.view(np.int16)).view(torch.bfloat16) if dt == "bf16" else torch.from_numpy(W)).cuda()
         Xd = torch.from_numpy(X).cuda()
         bi = torch.from_numpy(base_idx).cuda()
         ei = [torch.from_numpy(e).cuda() for e in ext_idx]
-        cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, importance=args.importance)
+        xi = [torch.from_numpy(e).cuda() for e in extra_idx]
+        cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, importance=args.importance,
+                          m_base=wl.m_base)
         q = LayerQuantizer(M, N, tdt, cfg, L.tokens, device="cuda")
-        q.run(Wd, Xd, bi, ei)  # warm-up pass
+        q.run(Wd, Xd, bi, ei, base_idx_extra=xi)  # warm-up pass
         torch.cuda.synchronize()
+        flush.fill_(0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        st = q.run(Wd, Xd, bi, ei, base_idx_extra=xi)  # whole layer pass, no hooks
+        e1.record()
+        torch.cuda.synchronize()
+        pass_ms = e0.elapsed_time(e1)
+        What = st.W_hat.float().cpu().numpy().astype(np.float64)
+        W64 = oracle.widen(W, dt).astype(np.float64)
+        rel_err = float(((W64 - What) ** 2).sum() / (W64 ** 2).sum())
+        bpw = crvq.crvq_bits_per_weight(M, N, d, n_crit, [wl.K_base] * wl.m_base, wl.K_ext)
+        del What, W64
         hook = TableHook(flush)
-        q.run(Wd, Xd, bi, ei, hooks=[hook])
+        q.run(Wd, Xd, bi, ei, hooks=[hook], base_idx_extra=xi)
         torch.cuda.synchronize()
         Ws = None
         groups = {}
@@ -213,7 +228,7 @@ def table(args):
                 rec("reorder (rank sort + column gather)", ms, len(calls), 2 * M * N * es + N * 4, "B", HBM, ts, 1.0,
                     "bitwise" if ok else "FAIL")
             elif kind.startswith("assign"):
-                base = kind.startswith("assign_base")
+                base = kind in ("assign_base", "assign_base_final")
                 pre = kind.startswith("assign_pre")
                 Xh = Ws if base else (W if pre else c["in"]["X"])
                 vdt = dt if (base or pre) else "f32"
@@ -230,7 +245,7 @@ def table(args):
                     "exact" if same == k else f"{k - same} of {k} differ (ties allowed within 1e-6)",
                     vectors=V.shape[0], K=K, sampled_vectors=k)
             elif kind.startswith("update"):
-                base = kind.startswith("update_base")
+                base = kind == "update_base"
                 pre = kind.startswith("update_pre")
                 Xh = Ws if base else (W if pre else c["in"]["X"])
                 vdt = dt if (base or pre) else "f32"
@@ -246,17 +261,27 @@ def table(args):
                 rec(f"kmeans_update ({kind})", ms, len(calls), (d * ves + 4) * V.shape[0] + K * d * ves + 4 * K, "B",
                     HBM, ts, 1.0, f"{tol:g} rel per centroid" if ok else "FAIL", vectors=V.shape[0], K=K)
             elif kind.startswith("residual"):
-                mdt = dt if kind == "residual_base" else "f32"
+                mdt = dt if kind in ("residual_base", "residual_all1") else "f32"
                 Mv = oracle.vectors(np.ascontiguousarray(c["in"]["minuend"]), d)
-                exp = oracle.residual(Mv, c["in"]["codes"].ravel(), c["in"]["book"], mdt, mdt)
+                if isinstance(c["in"]["codes"], list):  # several basic books
+                    books = c["in"]["book"]
+                    bdt = [dt] + ["f32"] * (len(books) - 1)
+                    exp = opipe.residual_books(Mv, [np.ascontiguousarray(x).ravel() for x in c["in"]["codes"]],
+                                               books, mdt, bdt)
+                    nbook = sum(b.size * (2 if t == "bf16" else 4) for b, t in zip(books, bdt))
+                    ncodes = len(books)
+                else:
+                    exp = oracle.residual(Mv, c["in"]["codes"].ravel(), c["in"]["book"], mdt, mdt)
+                    nbook = c["in"]["book"].size * (2 if mdt == "bf16" else 4)
+                    ncodes = 1
                 ts = time.perf_counter() - t0
                 ok = np.array_equal(oracle.vectors(c["out"]["out"], d), exp)
                 mes = 2 if mdt == "bf16" else 4
-                rec(f"dequant ({kind}: E = W_crit - C[q])", ms, len(calls),
-                    Mv.size * (mes + 4) + 4 * Mv.shape[0] + c["in"]["book"].size * mes, "B", HBM, ts, 1.0,
+                rec(f"dequant ({kind}: E = minuend - sum of codewords)", ms, len(calls),
+                    Mv.size * (mes + 4) + 4 * ncodes * Mv.shape[0] + nbook, "B", HBM, ts, 1.0,
                     "bitwise" if ok else "FAIL")
-            elif kind == "beam":
-                Vc = oracle.vectors(np.ascontiguousarray(Ws[:, :n_crit]), d)
+            elif kind in ("beam", "beam_basic"):
+                Vc = oracle.vectors(np.ascontiguousarray(Ws[:, :n_crit] if kind == "beam" else Ws), d)
                 books = c["in"]["books"]
                 bdt = [dt] + ["f32"] * (len(books) - 1)
                 flops, width = 0.0, 1
@@ -268,9 +293,15 @@ def table(args):
                 t0 = time.perf_counter()
                 exp_codes, exp_err = oracle.beam(Vc[S], books, wl.beam, dt, bdt)
                 ts = time.perf_counter() - t0
-                got = np.stack([c["out"]["codes_base"].ravel()[S]] + [x[S] for x in c["out"]["codes_ext"]])
+                if kind == "beam":
+                    got = np.stack([np.ascontiguousarray(x).ravel()[S] for x in c["out"]["codes_basic"]] +
+                                   [x[S] for x in c["out"]["codes_ext"]])
+                else:
+                    got = np.stack([x.ravel()[S] for x in c["out"]["codes"]])
                 same = int((got == exp_codes).all(0).sum())
-                rec(f"assign_residual_beam (width {wl.beam})", ms, len(calls), flops * Vc.shape[0], "FLOP", F16, ts,
+                what = "critical vectors" if kind == "beam" else "every vector, basic books"
+                rec(f"assign_residual_beam (width {wl.beam}, {what})", ms, len(calls), flops * Vc.shape[0], "FLOP",
+                    F16, ts,
                     k / Vc.shape[0], "exact" if same == k else f"{k - same} of {k} tuples differ (ties allowed)",
                     vectors=Vc.shape[0], books=[b.shape[0] for b in books], sampled_vectors=k)
             elif kind == "dequant":
@@ -283,14 +314,20 @@ def table(args):
                     z[:, :ncv] = x.reshape(M, ncv)
                     qe.append(z.ravel())
                 crit = opipe.crit_mask(M, N, d, n_crit)
-                R = oracle.reconstruct([c["in"]["codes"].ravel()] + qe, books, crit, bdt)
+                cb = [x.ravel() for x in c["in"]["codes_basic"]]
+                R = oracle.reconstruct(cb + qe, books, crit, bdt, n_full=len(cb))
                 exp = oracle.scatter_columns(oracle.round_to(R, dt).reshape(M, N), c["in"]["perm"])
                 ts = time.perf_counter() - t0
                 ok = np.array_equal(c["out"]["out"], exp)
                 rec("dequant (reconstruction + reverse reorder)", ms, len(calls),
-                    M * N * es + 4 * n + 4 * ncv * M * len(qe) + sum(b.size * (2 if t == "bf16" else 4)
+                    M * N * es + 4 * n * len(cb) + 4 * ncv * M * len(qe) + sum(b.size * (2 if t == "bf16" else 4)
                                                                      for b, t in zip(books, bdt)) + N * 4,
                     "B", HBM, ts, 1.0, "bitwise" if ok else "FAIL")
+        print(json.dumps({"workload": wid, "layer": f"{L.name} {M}x{N} {dt}", "importance": args.importance,
+                          "call": "whole layer pass", "name": wl.name, "gpu_ms": round(pass_ms, 3),
+                          "calls_in_pass": len(hook.calls), "sum_of_call_ms": round(sum(x["ms"] for x in hook.calls), 3),
+                          "rel_err": rel_err, "bits_per_weight": bpw, "d": d, "m_base": wl.m_base,
+                          "K_base": wl.K_base, "K_ext": wl.K_ext, "crit_cols": n_crit}), flush=True)
         del q, Wd, Xd, hook
         torch.cuda.empty_cache()
 

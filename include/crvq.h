@@ -208,6 +208,48 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
                          int64_t ld_out, void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * crvq_dequant_books -- crvq_dequant for a layout with n_base >= 1 basic
+ * codebooks (the additive basic VQ with m > 1 books of Sec. 3.2 and Sec. 6.4,
+ * e.g. m = 2 books on d = 16 vectors) followed by n_ext extended books:
+ *   R[r, g*d+t] = sum_{b < n_base} C[b][q[b][r*ldq_base+g]][t]
+ *                 + sum_{n_base <= b < n_base+n_ext, g < n_crit/d} C[b][q[b][r*ldq_ext+g]][t]
+ * summed in fp64 in book order, then written exactly as by crvq_dequant
+ * (residual mode with minuend, reverse reorder with perm, else plain), each
+ * element rounded once.  q, C, dtypes, Ks: host arrays of n_base + n_ext
+ * entries (device pointers for q and C).  n_base + n_ext <= 8.  crvq_dequant is
+ * this call with n_base = 1.  A code outside its codebook yields NaN for
+ * that vector.  workspace: crvq_dequant_workspace_size(n_cols) bytes (only
+ * used with perm).
+ */
+crvq_status crvq_dequant_books(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, int32_t n_base, int32_t n_ext,
+                               const int32_t* const* q, int64_t ldq_base, int64_t ldq_ext, const void* const* C,
+                               const int32_t* dtypes, const int64_t* Ks, const int32_t* perm, const void* minuend,
+                               int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out,
+                               void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_bits_per_weight -- average storage per weight of a quantized layer
+ * (Sec. 3.2 Eq. 6 and Appendix A.1 Eq. 8, counted for the exact layout):
+ *
+ *   bits = [ sum_{b < n_base} (rows*cols/d) * e_b
+ *            + sum_{n_base <= b < n_base+n_ext} (rows*n_crit/d) * e_b
+ *            + sum_b Ks[b] * d * codeword_bits + cols * perm_bits ] / (rows*cols)
+ *
+ * with e_b = ceil(log2 Ks[b]), the code width that indexes book b (0 for a
+ * one-codeword book).  The paper stores codewords in FP16 (codeword_bits =
+ * 16) and the channel permutation as 16-bit indices (perm_bits = 16, or 0 to
+ * leave it out as Eq. 8 does).  With n_crit = lambda*cols this is Eq. 8 with
+ * all m = n_base + n_ext codebooks counted in the codebook term; with
+ * n_ext = 0 and perm_bits = 0 it is Eq. 6.
+ * Host-only: Ks is a host array of n_base + n_ext entries, out a host double.
+ * Needs rows, cols >= 1, d in [1, 16] dividing cols, n_crit a multiple of d in
+ * [0, cols], n_base >= 1, n_ext >= 0, n_base + n_ext <= 8, Ks[b] in
+ * [1, 65536], codeword_bits in [1, 64], perm_bits in [0, 64].
+ */
+crvq_status crvq_bits_per_weight(int64_t rows, int64_t cols, int32_t d, int64_t n_crit, int32_t n_base, int32_t n_ext,
+                                 const int64_t* Ks, int32_t codeword_bits, int32_t perm_bits, double* out);
+
+/* ---------------------------------------------------------------------------
  * crvq_dequant_gemv -- matrix-vector product with a CRVQ-quantized layer, the
  * inference step the paper times (Sec. 4.3, Fig. 3 right; Table 7):
  *

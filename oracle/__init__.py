@@ -60,7 +60,7 @@ def _load():
         lib.oracle_kmeans_means.argtypes = [P, I64, I32, P, I64, P, P, P]
         lib.oracle_colreduce.argtypes = [P, I64, P, I64, I64, I64, P, I32, P]
         lib.oracle_beam.argtypes = [P, I64, I32, I32, P, P, I32, P, P]
-        lib.oracle_reconstruct.argtypes = [I64, I32, I32, P, P, P, P]
+        lib.oracle_reconstruct.argtypes = [I64, I32, I32, I32, P, P, P, P]
         lib.oracle_round_bf16.argtypes = [P, I64, P]
         lib.oracle_num_threads.restype = I32
         _lib = lib
@@ -218,11 +218,11 @@ def beam(V: np.ndarray, books: Sequence[np.ndarray], width: int, v_dtype: str = 
 
 
 def reconstruct(codes: Sequence[np.ndarray], books: Sequence[np.ndarray], crit: np.ndarray,
-                book_dtypes: Optional[Sequence[str]] = None) -> np.ndarray:
+                book_dtypes: Optional[Sequence[str]] = None, n_full: int = 1) -> np.ndarray:
     """Additive reconstruction of Sec. 4.3: a critical vector is the sum (fp64, book order) of its
-    codewords from the basic and every extended codebook; a non-critical one is its basic codeword.
-    codes[b] holds one code per vector for book b (entries of extended books are ignored where
-    crit is 0).  Returns fp64 (n x d)."""
+    codewords from the basic and every extended codebook; a non-critical one the sum of its codewords
+    from the n_full basic books (one unless the layout has several).  codes[b] holds one code per
+    vector for book b (entries of extended books are ignored where crit is 0).  Returns fp64 (n x d)."""
     if book_dtypes is None:
         book_dtypes = [F32] * len(books)
     B32 = [widen(b, t) for b, t in zip(books, book_dtypes)]
@@ -233,7 +233,7 @@ def reconstruct(codes: Sequence[np.ndarray], books: Sequence[np.ndarray], crit: 
     cr = np.ascontiguousarray(crit, dtype=np.uint8)
     arr = (ctypes.c_void_p * nb)(*[b.ctypes.data for b in B32])
     R = np.empty((n, d), dtype=np.float64)
-    _load().oracle_reconstruct(n, d, nb, arr, _p(q), _p(cr), _p(R))
+    _load().oracle_reconstruct(n, d, nb, n_full, arr, _p(q), _p(cr), _p(R))
     return R
 
 
@@ -274,11 +274,13 @@ def bits_per_weight_vq(m: int, e: int, d: int, rows: int = 4096, cols: int = 409
 
 
 def bits_per_weight_crvq(m: int, e: int, d: int, lam: float, rows: int = 4096, cols: int = 4096,
-                         include_perm: bool = False) -> float:
+                         include_perm: bool = False, m_base: int = 1) -> float:
     """Average bits per weight of CRVQ (Appendix A.1 Eq. 8): basic codes e/d, extended codes
-    (m-1)*lambda*e/d, m codebooks, optionally the 16-bit channel-permutation indices."""
+    (m-1)*lambda*e/d, m codebooks, optionally the 16-bit channel-permutation indices.  With m_base
+    basic books (Sec. 6.4's m = 2 setting) the basic codes take m_base*e/d and the extended ones
+    (m-m_base)*lambda*e/d."""
     n_w = rows * cols
-    bits = e / d + (m - 1) * lam * e / d + (2 ** e) * m * d * 16 / n_w
+    bits = m_base * e / d + (m - m_base) * lam * e / d + (2 ** e) * m * d * 16 / n_w
     if include_perm:
         bits += cols * 16 / n_w
     return bits

@@ -213,14 +213,15 @@ void oracle_beam(const float* V, int64_t n, int d, int n_books, const float* con
  * codewords from the basic and all extended codebooks; non-critical
  * vectors use the basic codebook only).
  *   R[i,t] = sum over books b = 0..nb_i-1 of books[b][codes[b][i], t]
- * in fp64, in book order; nb_i = n_books when crit[i] != 0, else 1.
- * codes is n_books arrays of n entries (codes[b*n + i]); entries of books
- * b >= 1 are ignored for non-critical vectors. */
-void oracle_reconstruct(int64_t n, int d, int n_books, const float* const* books,
+ * in fp64, in book order; nb_i = n_books when crit[i] != 0, else n_full (the
+ * basic books, 1 unless the layout has several).  codes is n_books arrays of
+ * n entries (codes[b*n + i]); entries of books b >= n_full are ignored for
+ * non-critical vectors. */
+void oracle_reconstruct(int64_t n, int d, int n_books, int n_full, const float* const* books,
                         const int32_t* codes, const uint8_t* crit, double* R) {
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n; ++i) {
-    int nb = crit[i] ? n_books : 1;
+    int nb = crit[i] ? n_books : n_full;
     for (int t = 0; t < d; ++t) {
       double acc = 0.0;
       for (int b = 0; b < nb; ++b) {

@@ -22,7 +22,15 @@ Readings where the paper is silent (each also listed in the design notes):
   an empty cluster keeps its centroid;
 * residuals are rounded to float32 when they are stored (E^t);
 * the final codes of critical vectors come from the beam search (width 1 =
-  greedy) over [basic, ext_1, ...] on the un-rounded (fp64) residual.
+  greedy) over [basic, ext_1, ...] on the un-rounded (fp64) residual;
+* several basic codebooks (``m_base`` > 1, the m = 2, d = 16 setting of
+  Sec. 3.2 / Sec. 6.4): basic book b >= 1 is fitted (K-means from seeded
+  indices) on the float32 residual of every vector after books < b and their
+  final assignments; then the beam search over the basic books gives the codes
+  of every vector; the extended books are fitted on the critical residual
+  after those codes, and the critical vectors' final codes come from the beam
+  over all books.  Basic books after the first are float32, like the residual
+  they are fitted on.
 """
 from __future__ import annotations
 
@@ -48,6 +56,8 @@ class LayerResult:
     beam_err: np.ndarray          # fp64 [M * n_crit/d]
     W_hat: np.ndarray             # reconstruction in original channel order, storage dtype of W
     objectives: Dict[str, List[float]]
+    C_basic: List[np.ndarray] = dataclasses.field(default_factory=list)      # all m_base basic books
+    codes_basic: List[np.ndarray] = dataclasses.field(default_factory=list)  # their int32 [M * N/d] codes
 
 
 def crit_mask(M: int, N: int, d: int, n_crit: int) -> np.ndarray:
@@ -96,9 +106,18 @@ def channel_importance(W: np.ndarray, h: np.ndarray, dtype: str, mode: str, d: i
     return round_to(I, F32)
 
 
+def residual_books(minuend: np.ndarray, codes: List[np.ndarray], books: List[np.ndarray], m_dtype: str,
+                   book_dtypes: List[str]) -> np.ndarray:
+    """ComputeError over several books: E = minuend - sum_b C_b[q_b] (fp64, book order), rounded to float32."""
+    Mv = widen(minuend, m_dtype).astype(np.float64)
+    R = reconstruct(codes, books, np.zeros(len(codes[0]), np.uint8), book_dtypes, n_full=len(books))
+    return (Mv - R).astype(np.float32)
+
+
 def quantize_layer(W: np.ndarray, X: np.ndarray, dtype: str, d: int, K_base: int, K_ext: List[int],
                    crit_frac: float, width: int, iters: int, base_idx: np.ndarray,
-                   ext_idx: List[np.ndarray], importance: str = "energy") -> LayerResult:
+                   ext_idx: List[np.ndarray], importance: str = "energy", m_base: int = 1,
+                   base_idx_extra: List[np.ndarray] = ()) -> LayerResult:
     M, N = W.shape
     h = round_to(colreduce(X, reduce="sum"), F32)
     I = channel_importance(W, h, dtype, importance, d, base_idx, iters)
@@ -110,10 +129,27 @@ def quantize_layer(W: np.ndarray, X: np.ndarray, dtype: str, d: int, K_base: int
 
     C_base, q_base, _, J = kmeans(V, np.ascontiguousarray(V[base_idx]), iters, dtype, dtype)
     objs["base"] = J
+    C_basic, q_basic, basic_dt = [C_base], [q_base], [dtype]
+    if m_base > 1:
+        # further basic books on the residual of every vector, then the beam over the basic books
+        Eall = residual(V, q_base, C_base, dtype, dtype)
+        for b in range(1, m_base):
+            Cb, qb, _, J = kmeans(Eall, np.ascontiguousarray(Eall[base_idx_extra[b - 1]]), iters, F32, F32)
+            objs[f"base{b + 1}"] = J
+            C_basic.append(Cb)
+            q_basic.append(qb)
+            basic_dt.append(F32)
+            if b + 1 < m_base:
+                Eall = residual(Eall, qb, Cb, F32, F32)
+        q_basic, _ = beam(V, C_basic, width, dtype, basic_dt)
+        q_base = q_basic[0]
 
     Vc = vectors(crit_slab(Ws, n_crit), d)
     crit_vec_idx = np.flatnonzero(crit_mask(M, N, d, n_crit))
-    E = residual(Vc, q_base[crit_vec_idx], C_base, dtype, dtype)
+    if m_base == 1:
+        E = residual(Vc, q_base[crit_vec_idx], C_base, dtype, dtype)
+    else:
+        E = residual_books(Vc, [q[crit_vec_idx] for q in q_basic], C_basic, dtype, basic_dt)
     C_ext = []
     for t in range(1, len(K_ext) + 1):
         Ct, qt, _, J = kmeans(E, np.ascontiguousarray(E[ext_idx[t - 1]]), iters, F32, F32)
@@ -123,21 +159,26 @@ def quantize_layer(W: np.ndarray, X: np.ndarray, dtype: str, d: int, K_base: int
         if t < len(K_ext):
             E = residual(E, qt, Ct, F32, F32)
 
-    books = [C_base] + C_ext
-    bdt = [dtype] + [F32] * len(C_ext)
+    books = C_basic + C_ext
+    bdt = basic_dt + [F32] * len(C_ext)
     codes_b, err = beam(Vc, books, width, dtype, bdt)
-    codes_base = q_base.copy()
-    codes_base[crit_vec_idx] = codes_b[0]
-    codes_ext = [codes_b[t] for t in range(1, len(books))]
+    codes_basic = [q.copy() for q in q_basic]
+    for b in range(m_base):
+        codes_basic[b][crit_vec_idx] = codes_b[b]
+    codes_ext = [codes_b[t] for t in range(m_base, len(books))]
 
-    # reconstruction in sorted order, then reverse reordering
-    full_codes = [codes_base] + [np.zeros(M * N // d, np.int32) for _ in C_ext]
+    # reconstruction in sorted order (basic books on every vector, extended ones on the critical
+    # groups), then reverse reordering
+    n = M * N // d
+    cm = crit_mask(M, N, d, n_crit)
+    full_codes = codes_basic + [np.zeros(n, np.int32) for _ in C_ext]
     for t in range(len(C_ext)):
-        full_codes[t + 1][crit_vec_idx] = codes_ext[t]
-    R = reconstruct(full_codes, books, crit_mask(M, N, d, n_crit), bdt)
+        full_codes[m_base + t][crit_vec_idx] = codes_ext[t]
+    R = reconstruct(full_codes, books, cm, bdt, n_full=m_base)
     Rs = round_to(R, dtype).reshape(M, N)
     W_hat = scatter_columns(Rs, perm)
-    return LayerResult(h, I, perm, n_crit, C_base, C_ext, codes_base, codes_ext, err, W_hat, objs)
+    return LayerResult(h, I, perm, n_crit, C_base, C_ext, codes_basic[0], codes_ext, err, W_hat, objs, C_basic,
+                       codes_basic)
 
 
 def frob_err(W: np.ndarray, W_hat: np.ndarray, dtype: str) -> float:

@@ -64,6 +64,9 @@ def lib(build_if_missing: bool = True):
                 "crvq_dequant_workspace_size": ([I64], SZ),
                 "crvq_dequant": ([I64, I64, I32, I64, P, I64, P, ctypes.c_int, I64, I32, PP, I64, PP, P, P, P, P, ctypes.c_int,
                                   I64, P, ctypes.c_int, I64, P, SZ, P], ctypes.c_int),
+                "crvq_dequant_books": ([I64, I64, I32, I64, I32, I32, PP, I64, I64, PP, P, P, P, P, ctypes.c_int, I64,
+                                        P, ctypes.c_int, I64, P, SZ, P], ctypes.c_int),
+                "crvq_bits_per_weight": ([I64, I64, I32, I64, I32, I32, P, I32, I32, P], ctypes.c_int),
                 "crvq_gemv_workspace_size": ([I64, I64, I64], SZ),
                 "crvq_dequant_gemv": ([I64, I64, I64, P, I64, P, ctypes.c_int, I64, I32, PP, I64, PP, P, P, P, P,
                                        ctypes.c_int, P, P, SZ, P], ctypes.c_int),
@@ -236,6 +239,40 @@ def crvq_dequant(M: int, n_cols: int, d: int, q_base: torch.Tensor, ldq_base: in
         _ptr(perm), _ptr(minuend), CRVQ_F32 if minuend is None else dtype_code(minuend),
         0 if minuend is None else minuend.stride(0), _ptr(out), dtype_code(out), out.stride(0), _ptr(ws),
         0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_dequant_books(M: int, n_cols: int, d: int, q_base: Sequence[torch.Tensor], ldq_base: int,
+                       C_base: Sequence[torch.Tensor], out: torch.Tensor, n_crit: int = 0,
+                       q_ext: Sequence[torch.Tensor] = (), ldq_ext: int = 0, C_ext: Sequence[torch.Tensor] = (),
+                       perm: Optional[torch.Tensor] = None, minuend: Optional[torch.Tensor] = None,
+                       stream=None) -> None:
+    """crvq_dequant with len(q_base) basic books covering every vector (see include/crvq.h)."""
+    L = lib()
+    assert len(q_base) == len(C_base) and len(q_ext) == len(C_ext)
+    books = list(C_base) + list(C_ext)
+    nb = len(books)
+    ws = _workspace(L.crvq_dequant_workspace_size(n_cols), out.device) if perm is not None else None
+    dts = (ctypes.c_int32 * nb)(*[dtype_code(c) for c in books])
+    Ks = (ctypes.c_int64 * nb)(*[c.shape[0] for c in books])
+    _check("crvq_dequant_books", L.crvq_dequant_books(
+        M, n_cols, d, n_crit, len(C_base), len(C_ext),
+        ctypes.cast(_ptr_array(list(q_base) + list(q_ext)), ctypes.POINTER(ctypes.c_void_p)), ldq_base, ldq_ext,
+        ctypes.cast(_ptr_array(books), ctypes.POINTER(ctypes.c_void_p)), ctypes.cast(dts, ctypes.c_void_p),
+        ctypes.cast(Ks, ctypes.c_void_p), _ptr(perm), _ptr(minuend),
+        CRVQ_F32 if minuend is None else dtype_code(minuend), 0 if minuend is None else minuend.stride(0), _ptr(out),
+        dtype_code(out), out.stride(0), _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_bits_per_weight(rows: int, cols: int, d: int, n_crit: int, K_base: Sequence[int], K_ext: Sequence[int] = (),
+                         codeword_bits: int = 16, perm_bits: int = 16) -> float:
+    """Average bits per stored weight of a quantized layer (Eq. 6 / Eq. 8 for the exact layout); host only."""
+    Ks = list(K_base) + list(K_ext)
+    arr = (ctypes.c_int64 * max(1, len(Ks)))(*Ks)
+    out = ctypes.c_double(0.0)
+    _check("crvq_bits_per_weight", lib().crvq_bits_per_weight(
+        rows, cols, d, n_crit, len(K_base), len(K_ext), ctypes.cast(arr, ctypes.c_void_p), codeword_bits, perm_bits,
+        ctypes.byref(out)))
+    return out.value
 
 
 def crvq_pack_codes_u8(codes: torch.Tensor, out: torch.Tensor, stream=None) -> None:

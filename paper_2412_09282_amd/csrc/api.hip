@@ -349,25 +349,27 @@ crvq_status crvq_gather_vectors(const void* X, int x_dtype, int64_t n_rows, int6
 // ------------------------------------------------------------------------------------------------
 size_t crvq_dequant_workspace_size(int64_t n_cols) { return n_cols < 1 ? 0 : align256(static_cast<size_t>(n_cols) * 4); }
 
-crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, const int32_t* q_base,
-                         int64_t ldq_base, const void* C_base, int base_dtype, int64_t K_base, int32_t n_ext,
-                         const int32_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
-                         const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* minuend,
-                         int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out, void* workspace,
-                         size_t ws_bytes, void* stream) {
-  static const char* fn = "crvq_dequant";
+// Shared by crvq_dequant (one basic book) and crvq_dequant_books (n_base of them): books[0, n_base)
+// cover every vector with code stride ldq_base, books[n_base, n_base + n_ext) the critical groups with
+// stride ldq_ext.
+static crvq_status dequant_impl(const char* fn, int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, int32_t n_base,
+                                int32_t n_ext, const int32_t* const* q, int64_t ldq_base, int64_t ldq_ext,
+                                const void* const* C, const int32_t* dtypes, const int64_t* Ks, const int32_t* perm,
+                                const void* minuend, int minuend_dtype, int64_t ld_min, void* out, int out_dtype,
+                                int64_t ld_out, void* workspace, size_t ws_bytes, void* stream) {
   g_err.clear();
   if (M < 0 || n_cols < 1) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and n_cols >= 1", fn);
   if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
   if (n_cols % d) return fail(CRVQ_ERR_INVALID, "%s: n_cols = %lld is not a multiple of d = %d", fn, (long long)n_cols, d);
   if (n_crit < 0 || n_crit > n_cols || n_crit % d)
     return fail(CRVQ_ERR_INVALID, "%s: n_crit = %lld must be a multiple of d in [0, n_cols]", fn, (long long)n_crit);
-  if (!q_base || !C_base || !out) return fail(CRVQ_ERR_INVALID, "%s: q_base, C_base and out must not be NULL", fn);
-  if (!dtype_ok(base_dtype) || !dtype_ok(out_dtype)) return fail(CRVQ_ERR_INVALID, "%s: invalid base or out dtype", fn);
-  crvq_status s = check_K(K_base, fn, "K_base");
-  if (s) return s;
+  if (n_base < 1 || n_ext < 0 || n_base + n_ext > CRVQ_MAX_BOOKS)
+    return fail(CRVQ_ERR_INVALID, "%s: need n_base >= 1, n_ext >= 0 and n_base + n_ext <= %d (got %d + %d)", fn,
+                CRVQ_MAX_BOOKS, n_base, n_ext);
+  if (!out) return fail(CRVQ_ERR_INVALID, "%s: out must not be NULL", fn);
+  if (!dtype_ok(out_dtype)) return fail(CRVQ_ERR_INVALID, "%s: invalid out dtype", fn);
   if (ldq_base < n_cols / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_base < n_cols / d", fn);
-  if (n_ext < 0 || n_ext > CRVQ_MAX_BOOKS - 1) return fail(CRVQ_ERR_INVALID, "%s: n_ext = %d outside [0, %d]", fn, n_ext, CRVQ_MAX_BOOKS - 1);
+  if (n_ext > 0 && ldq_ext < n_crit / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_ext < n_crit / d", fn);
   if (ld_out < n_cols) return fail(CRVQ_ERR_INVALID, "%s: ld_out < n_cols", fn);
   if (perm && minuend) return fail(CRVQ_ERR_INVALID, "%s: perm and minuend are mutually exclusive", fn);
   if (minuend) {
@@ -375,26 +377,19 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
     if (ld_min < n_cols) return fail(CRVQ_ERR_INVALID, "%s: ld_min < n_cols", fn);
   }
   DequantBooks b = {};
-  b.C[0] = C_base;
-  b.q[0] = q_base;
-  b.type[0] = base_dtype;
-  b.K[0] = K_base;
-  b.n = 1 + n_ext;
+  b.n = n_base + n_ext;
+  b.n_full = n_base;
   b.ldq_base = ldq_base;
   b.ldq_ext = ldq_ext;
-  if (n_ext > 0) {
-    if (!q_ext || !C_ext || !ext_dtypes || !K_ext)
-      return fail(CRVQ_ERR_INVALID, "%s: q_ext, C_ext, ext_dtypes and K_ext must not be NULL when n_ext > 0", fn);
-    if (ldq_ext < n_crit / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_ext < n_crit / d", fn);
-    for (int e = 0; e < n_ext; ++e) {
-      if (!q_ext[e] || !C_ext[e]) return fail(CRVQ_ERR_INVALID, "%s: q_ext[%d] or C_ext[%d] is NULL", fn, e, e);
-      if (!dtype_ok(ext_dtypes[e])) return fail(CRVQ_ERR_INVALID, "%s: ext_dtypes[%d] invalid", fn, e);
-      if ((s = check_K(K_ext[e], fn, "K_ext[e]"))) return s;
-      b.C[e + 1] = C_ext[e];
-      b.q[e + 1] = q_ext[e];
-      b.type[e + 1] = ext_dtypes[e];
-      b.K[e + 1] = K_ext[e];
-    }
+  crvq_status s = CRVQ_OK;
+  for (int e = 0; e < b.n; ++e) {
+    if (!q[e] || !C[e]) return fail(CRVQ_ERR_INVALID, "%s: the code array or codebook of book %d is NULL", fn, e);
+    if (!dtype_ok(dtypes[e])) return fail(CRVQ_ERR_INVALID, "%s: the dtype of book %d is invalid", fn, e);
+    if ((s = check_K(Ks[e], fn, "K"))) return s;
+    b.C[e] = C[e];
+    b.q[e] = q[e];
+    b.type[e] = dtypes[e];
+    b.K[e] = Ks[e];
   }
   if (perm && (s = check_ws(workspace, ws_bytes, crvq_dequant_workspace_size(n_cols), fn))) return s;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -405,6 +400,74 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
   }
   return hip_status(
       launch_dequant(M, n_cols, d, n_crit, b, inv, perm, minuend, minuend_dtype, ld_min, out, out_dtype, ld_out, st), fn);
+}
+
+crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, const int32_t* q_base,
+                         int64_t ldq_base, const void* C_base, int base_dtype, int64_t K_base, int32_t n_ext,
+                         const int32_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
+                         const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* minuend,
+                         int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out, void* workspace,
+                         size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_dequant";
+  g_err.clear();
+  if (n_ext < 0 || n_ext > CRVQ_MAX_BOOKS - 1)
+    return fail(CRVQ_ERR_INVALID, "%s: n_ext = %d outside [0, %d]", fn, n_ext, CRVQ_MAX_BOOKS - 1);
+  if (!q_base || !C_base) return fail(CRVQ_ERR_INVALID, "%s: q_base and C_base must not be NULL", fn);
+  if (n_ext > 0 && (!q_ext || !C_ext || !ext_dtypes || !K_ext))
+    return fail(CRVQ_ERR_INVALID, "%s: q_ext, C_ext, ext_dtypes and K_ext must not be NULL when n_ext > 0", fn);
+  const int32_t* q[CRVQ_MAX_BOOKS] = {q_base};
+  const void* C[CRVQ_MAX_BOOKS] = {C_base};
+  int32_t dts[CRVQ_MAX_BOOKS] = {base_dtype};
+  int64_t Ks[CRVQ_MAX_BOOKS] = {K_base};
+  for (int e = 0; e < n_ext; ++e) {
+    q[e + 1] = q_ext[e];
+    C[e + 1] = C_ext[e];
+    dts[e + 1] = ext_dtypes[e];
+    Ks[e + 1] = K_ext[e];
+  }
+  return dequant_impl(fn, M, n_cols, d, n_crit, 1, n_ext, q, ldq_base, ldq_ext, C, dts, Ks, perm, minuend, minuend_dtype,
+                      ld_min, out, out_dtype, ld_out, workspace, ws_bytes, stream);
+}
+
+crvq_status crvq_dequant_books(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, int32_t n_base, int32_t n_ext,
+                               const int32_t* const* q, int64_t ldq_base, int64_t ldq_ext, const void* const* C,
+                               const int32_t* dtypes, const int64_t* Ks, const int32_t* perm, const void* minuend,
+                               int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_dequant_books";
+  g_err.clear();
+  if (!q || !C || !dtypes || !Ks) return fail(CRVQ_ERR_INVALID, "%s: q, C, dtypes and Ks must not be NULL", fn);
+  return dequant_impl(fn, M, n_cols, d, n_crit, n_base, n_ext, q, ldq_base, ldq_ext, C, dtypes, Ks, perm, minuend,
+                      minuend_dtype, ld_min, out, out_dtype, ld_out, workspace, ws_bytes, stream);
+}
+
+crvq_status crvq_bits_per_weight(int64_t rows, int64_t cols, int32_t d, int64_t n_crit, int32_t n_base, int32_t n_ext,
+                                 const int64_t* Ks, int32_t codeword_bits, int32_t perm_bits, double* out) {
+  static const char* fn = "crvq_bits_per_weight";
+  g_err.clear();
+  if (rows < 1 || cols < 1) return fail(CRVQ_ERR_INVALID, "%s: need rows >= 1 and cols >= 1", fn);
+  if (d < 1 || d > CRVQ_MAX_D || cols % d) return fail(CRVQ_ERR_INVALID, "%s: d = %d must be in [1, %d] and divide cols", fn, d, CRVQ_MAX_D);
+  if (n_crit < 0 || n_crit > cols || n_crit % d)
+    return fail(CRVQ_ERR_INVALID, "%s: n_crit = %lld must be a multiple of d in [0, cols]", fn, (long long)n_crit);
+  if (n_base < 1 || n_ext < 0 || n_base + n_ext > CRVQ_MAX_BOOKS)
+    return fail(CRVQ_ERR_INVALID, "%s: need n_base >= 1, n_ext >= 0 and n_base + n_ext <= %d", fn, CRVQ_MAX_BOOKS);
+  if (codeword_bits < 1 || codeword_bits > 64 || perm_bits < 0 || perm_bits > 64)
+    return fail(CRVQ_ERR_INVALID, "%s: codeword_bits must be in [1, 64] and perm_bits in [0, 64]", fn);
+  if (!Ks || !out) return fail(CRVQ_ERR_INVALID, "%s: Ks and out must not be NULL", fn);
+  // every count below is an integer well inside 2^53, so the sums are exact in double
+  const double full_vecs = static_cast<double>(rows) * static_cast<double>(cols / d);
+  const double crit_vecs = static_cast<double>(rows) * static_cast<double>(n_crit / d);
+  double bits = static_cast<double>(cols) * perm_bits;
+  for (int b = 0; b < n_base + n_ext; ++b) {
+    crvq_status s = check_K(Ks[b], fn, "Ks[b]");
+    if (s) return s;
+    int e = 0;
+    while ((int64_t{1} << e) < Ks[b]) ++e;
+    bits += (b < n_base ? full_vecs : crit_vecs) * e;
+    bits += static_cast<double>(Ks[b]) * d * codeword_bits;
+  }
+  *out = bits / (static_cast<double>(rows) * static_cast<double>(cols));
+  return CRVQ_OK;
 }
 
 }  // extern "C"

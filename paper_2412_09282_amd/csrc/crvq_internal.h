@@ -146,8 +146,9 @@ struct DequantBooks {
   int type[8];
   int64_t K[8];
   int n;             // books in use (1 = basic only)
-  int64_t ldq_base;
-  int64_t ldq_ext;
+  int n_full;        // leading books that cover every vector (the basic books); the rest cover critical groups
+  int64_t ldq_base;  // row stride of the code arrays of the first n_full books
+  int64_t ldq_ext;   // row stride of the code arrays of the others
 };
 hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, const DequantBooks& books,
                           const int32_t* inv_perm, const int32_t* perm, const void* minuend, int min_type,

@@ -7,7 +7,8 @@
 // lanes per vector, each gathering and writing one 16-byte half, codes and outputs streamed with
 // nontemporal accesses; with a permutation, persistent blocks rebuild one row at a time in LDS and
 // write it out in original channel order through the inverse permutation (kept in LDS), 16 bytes
-// per store.  Other d: one thread per vector with the same arithmetic.
+// per store.  Other d, and layouts with several basic books: one thread per vector with the same
+// arithmetic.
 #include "crvq_internal.h"
 
 namespace crvq {
@@ -61,11 +62,13 @@ __device__ __forceinline__ bool recon_vec(const DequantBooks& b, int64_t r, int6
                                           double (&v)[kMaxD]) {
 #pragma unroll
   for (int t = 0; t < kMaxD; ++t) v[t] = 0.0;
-  const int32_t q0 = b.q[0][r * b.ldq_base + g];
-  if (q0 < 0 || q0 >= b.K[0]) return false;
-  add_codeword(b.C[0], b.type[0], q0, d, v);
+  for (int e = 0; e < b.n_full; ++e) {
+    const int32_t q = b.q[e][r * b.ldq_base + g];
+    if (q < 0 || q >= b.K[e]) return false;
+    add_codeword(b.C[e], b.type[e], q, d, v);
+  }
   if (g < n_crit_vec) {
-    for (int e = 1; e < b.n; ++e) {
+    for (int e = b.n_full; e < b.n; ++e) {
       const int32_t q = b.q[e][r * b.ldq_ext + g];
       if (q < 0 || q >= b.K[e]) return false;
       add_codeword(b.C[e], b.type[e], q, d, v);
@@ -479,7 +482,7 @@ hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, cons
   const int64_t ncv = n_crit / d;
   const int64_t nvec = M * (n_cols / d);
   // d = 8 fast paths: every book, the output and the minuend 16-byte aligned per vector
-  bool fast = d == 8;
+  bool fast = d == 8 && books.n_full == 1;
   for (int e = 0; e < books.n; ++e) fast = fast && (reinterpret_cast<uintptr_t>(books.C[e]) % 16 == 0);
   const int esize = out_type == ET_F32 ? 4 : 2;
   fast = fast && (reinterpret_cast<uintptr_t>(out) % 16 == 0) && ((ld_out * esize) % 16 == 0);

@@ -27,6 +27,7 @@ S_XSCALE = 2     # per-channel activation scales / outlier columns
 S_INIT_BASE = 3  # basic-codebook initial codeword indices
 S_INIT_EXT = 4   # extended codebook t uses stream S_INIT_EXT + t - 1
 S_SAMPLE = 9     # rows sampled for oracle checks on large layers
+S_INIT_BASE_EXTRA = 10  # basic codebook b >= 1 (layouts with m_base > 1 basic books) uses stream 10 + b - 1
 
 
 def rng(workload: int, layer: int, stream: int) -> np.random.Generator:
@@ -70,6 +71,7 @@ class Workload:
     crit_frac: float        # lambda, fraction of input channels treated as critical
     beam: int
     iters: int              # Lloyd iterations per codebook (each = assign + update), then a final assign
+    m_base: int = 1         # basic codebooks covering every vector (2 in the m = 2, d = 16 setting)
 
 
 W_STD = 0.02
@@ -127,6 +129,11 @@ def base_init_indices(wl: Workload, li: int, n: int) -> np.ndarray:
     return init_indices(n, wl.K_base, rng(wl.wid, li, S_INIT_BASE))
 
 
+def extra_base_init_indices(wl: Workload, li: int, b: int, n: int) -> np.ndarray:
+    """Indices for basic codebook b (b = 1 .. m_base-1) into the residual vectors of the whole layer."""
+    return init_indices(n, wl.K_base, rng(wl.wid, li, S_INIT_BASE_EXTRA + b - 1))
+
+
 def ext_init_indices(wl: Workload, li: int, t: int, n_crit_vec: int) -> np.ndarray:
     """Indices for extended codebook t (t = 1 .. m-1) into the critical residual vectors."""
     return init_indices(n_crit_vec, wl.K_ext[t - 1], rng(wl.wid, li, S_INIT_EXT + t - 1))
@@ -167,12 +174,37 @@ WORKLOADS = {
 }
 
 
+# Codebook-layout variants of Sec. 3.2 / Sec. 6.4 on the LLaMA-7B attention projection shape (the weights
+# and activations of workload 2): e = 8 with three extended books (8+8x3), two basic books on d = 16
+# vectors (m = 2) with three extended books, and wider basic books (e = 10, 12) with one extended book.
+VARIANT_WORKLOADS = {
+    21: Workload(2, "LLaMA-7B attention 4096x4096 fp32, 8+8x3: K=256 + 3 ext K=256 on top 2%",
+                 [LayerSpec("attn", 4096, 4096, 2048, "f32", "normal", "normal_scaled")],
+                 d=8, K_base=256, K_ext=[256, 256, 256], crit_frac=0.02, beam=1, iters=1),
+    22: Workload(2, "LLaMA-7B attention 4096x4096 fp32, m=2 d=16: 2 basic K=256 + 3 ext K=256 on top 2%",
+                 [LayerSpec("attn", 4096, 4096, 2048, "f32", "normal", "normal_scaled")],
+                 d=16, K_base=256, K_ext=[256, 256, 256], crit_frac=0.02, beam=1, iters=1, m_base=2),
+    23: Workload(2, "LLaMA-7B attention 4096x4096 fp32, e=10: K=1024 + 1 ext K=256 on top 2%",
+                 [LayerSpec("attn", 4096, 4096, 2048, "f32", "normal", "normal_scaled")],
+                 d=8, K_base=1024, K_ext=[256], crit_frac=0.02, beam=1, iters=1),
+    24: Workload(2, "LLaMA-7B attention 4096x4096 fp32, e=12: K=4096 + 1 ext K=256 on top 2%",
+                 [LayerSpec("attn", 4096, 4096, 2048, "f32", "normal", "normal_scaled")],
+                 d=8, K_base=4096, K_ext=[256], crit_frac=0.02, beam=1, iters=1),
+}
+
+
+def workload(wid: int) -> Workload:
+    """A timed workload (1-5) or a codebook-layout variant (21-24)."""
+    return WORKLOADS[wid] if wid in WORKLOADS else VARIANT_WORKLOADS[wid]
+
+
 def small_workload(M: int = 64, N: int = 64, tokens: int = 96, d: int = 8, K_base: int = 32,
                    K_ext: Sequence[int] = (16,), crit_frac: float = 0.1, beam: int = 2, iters: int = 3,
-                   dtype: str = "f32", wid: int = 100) -> Workload:
+                   dtype: str = "f32", wid: int = 100, m_base: int = 1) -> Workload:
     """A tiny workload of the same structure, for fast parity and pin tests."""
     return Workload(wid, f"small {M}x{N}", [LayerSpec("small", M, N, tokens, dtype, "normal", "normal_scaled")],
-                    d=d, K_base=K_base, K_ext=list(K_ext), crit_frac=crit_frac, beam=beam, iters=iters)
+                    d=d, K_base=K_base, K_ext=list(K_ext), crit_frac=crit_frac, beam=beam, iters=iters,
+                    m_base=m_base)
 
 
 def random_vectors(n: int, d: int, seed: int, scale: float = 0.02) -> np.ndarray:

@@ -17,7 +17,11 @@ are the first d * ceil(lambda N / d) reordered columns; K-means starts from the
 vectors at given indices, one iteration is assign + update, `iters` iterations
 are followed by a final assign, an empty cluster keeps its centroid; stored
 residuals are float32; the critical vectors' final codes come from the beam
-search (width 1 = greedy) on the exact residual.
+search (width 1 = greedy) on the exact residual.  With m_base > 1 basic books
+(the m = 2, d = 16 setting of Sec. 3.2 / Sec. 6.4) basic book b >= 1 (fp32) is
+fitted on the residual of every vector after books < b, the beam over the basic
+books then codes every vector, and the extended books are fitted on the
+critical residual after those codes.
 
 Every arithmetic step runs in the library's kernels; this module only
 allocates device tensors and sequences the calls.  Hooks see the device
@@ -29,7 +33,7 @@ from __future__ import annotations
 
 import dataclasses
 import math
-from typing import Dict, List, Optional
+from typing import Dict, List, Optional, Sequence
 
 import torch
 
@@ -46,6 +50,7 @@ class LayerConfig:
     beam: int
     iters: int
     importance: str = "energy"  # "energy" | "w_only" | "wa"
+    m_base: int = 1             # basic codebooks covering every vector (2 in the m = 2, d = 16 setting)
 
 
 def n_crit_columns(N: int, d: int, frac: float) -> int:
@@ -65,6 +70,8 @@ class LayerState:
     codes_ext: List[torch.Tensor]  # [M * n_crit/d] per extended book
     beam_err: torch.Tensor       # [M * n_crit/d]
     W_hat: torch.Tensor
+    C_basic: List[torch.Tensor] = dataclasses.field(default_factory=list)      # all m_base basic books
+    codes_basic: List[torch.Tensor] = dataclasses.field(default_factory=list)  # their codes [M * N/d]
 
 
 class LayerQuantizer:
@@ -91,6 +98,15 @@ class LayerQuantizer:
         self.codes_ext = [torch.empty(M * self.ncv, dtype=i32, device=device) for _ in cfg.K_ext]
         self.beam_err = torch.empty(M * self.ncv, dtype=f32, device=device)
         self.W_hat = torch.empty(M, N, dtype=dtype, device=device)
+        if cfg.m_base < 1 or cfg.m_base + len(cfg.K_ext) > 8:
+            raise ValueError(f"m_base {cfg.m_base} with {len(cfg.K_ext)} extended books")
+        # basic books after the first are fp32, like the residual they are fitted on
+        self.C_basic = [self.C_base] + [torch.empty(cfg.K_base, d, dtype=f32, device=device)
+                                        for _ in range(cfg.m_base - 1)]
+        self.codes_basic = [self.codes] + [torch.empty(self.n, dtype=i32, device=device)
+                                           for _ in range(cfg.m_base - 1)]
+        if cfg.m_base > 1:
+            self.E_all = [torch.empty(M, N, dtype=f32, device=device) for _ in range(min(2, cfg.m_base - 1))]
         if cfg.importance not in ("energy", "w_only", "wa"):
             raise ValueError(f"importance {cfg.importance!r}")
         if cfg.importance == "wa":  # Prequantize buffers: the basic VQ of the unsorted W
@@ -99,9 +115,10 @@ class LayerQuantizer:
             self.W_pre = torch.empty(M, N, dtype=dtype, device=device)
 
     def run(self, W: torch.Tensor, X: torch.Tensor, base_idx: torch.Tensor, ext_idx: List[torch.Tensor],
-            trace: Optional[list] = None, hooks=()) -> LayerState:
+            trace: Optional[list] = None, hooks=(), base_idx_extra: Sequence[torch.Tensor] = ()) -> LayerState:
         """hooks: objects with pre(name, inputs) / post(name, outputs), called right around each library
-        call; trace: a list that receives host copies of every call's inputs and outputs."""
+        call; trace: a list that receives host copies of every call's inputs and outputs;
+        base_idx_extra: initial-codeword indices of basic books 2 .. m_base."""
         cfg, d, M, N = self.cfg, self.cfg.d, self.M, self.N
         hooks = list(hooks) + ([TraceHook(trace)] if trace is not None else [])
         rec = _Recorder(hooks)
@@ -141,13 +158,35 @@ class LayerQuantizer:
         rec.pre("assign_base_final", X=self.Ws, C=self.C_base)
         C.crvq_assign(V, self.C_base, self.codes, self.dist)
         rec.post("assign_base_final", codes=self.codes, dist=self.dist)
+        mb = cfg.m_base
+        if mb > 1:
+            # further basic books on the residual of every vector, then the beam over the basic books
+            prev, src = (self.codes, self.C_base), self.Ws
+            for b in range(1, mb):
+                Eb = self.E_all[(b - 1) % 2]
+                rec.pre(f"residual_all{b}", minuend=src, codes=prev[0], book=prev[1])
+                C.crvq_dequant(M, N, d, prev[0], N // d, prev[1], Eb, minuend=src)
+                rec.post(f"residual_all{b}", out=Eb)
+                VE = VecSet.of_matrix(Eb, d)
+                Cb, qb = self.C_basic[b], self.codes_basic[b]
+                C.crvq_gather_vectors(VE, base_idx_extra[b - 1], Cb)
+                self._kmeans(VE, Cb, qb, rec, f"base{b + 1}")
+                rec.pre(f"assign_base{b + 1}_final", X=Eb, C=Cb)
+                C.crvq_assign(VE, Cb, qb)
+                rec.post(f"assign_base{b + 1}_final", codes=qb)
+                prev, src = (qb, Cb), Eb
+            rec.pre("beam_basic", X=self.Ws, books=self.C_basic, beam=cfg.beam)
+            C.crvq_assign_residual_beam(V, self.C_basic, cfg.beam, self.codes_basic, None)
+            rec.post("beam_basic", codes=list(self.codes_basic))
 
-        # residual of the critical slab after the basic codebook (Alg. 1 ComputeError)
+        # residual of the critical slab after the basic codebook(s) (Alg. 1 ComputeError)
         cur = 0
         if self.n_crit > 0:
-            rec.pre("residual_base", minuend=self.Ws[:, :self.n_crit], codes=self.codes.view(M, N // d)[:, :self.ncv],
-                    book=self.C_base)
-            C.crvq_dequant(M, self.n_crit, d, self.codes, N // d, self.C_base, self.E[cur], minuend=self.Ws)
+            crit_codes = [q.view(M, N // d)[:, :self.ncv] for q in self.codes_basic]
+            rec.pre("residual_base", minuend=self.Ws[:, :self.n_crit], codes=crit_codes[0] if mb == 1 else crit_codes,
+                    book=self.C_base if mb == 1 else self.C_basic)
+            C.crvq_dequant_books(M, self.n_crit, d, self.codes_basic, N // d, self.C_basic, self.E[cur],
+                                 minuend=self.Ws)
             rec.post("residual_base", out=self.E[cur])
             for t, Ct in enumerate(self.C_ext):
                 VE = VecSet.of_matrix(self.E[cur], d)
@@ -163,23 +202,24 @@ class LayerQuantizer:
                     rec.post(f"residual_ext{t + 1}", out=self.E[cur ^ 1])
                     cur ^= 1
 
-            # beam over all books for the critical vectors; basic codes land in the full code array
+            # beam over all books for the critical vectors; basic codes land in the full code arrays
             Vc = VecSet.of_matrix(self.Ws, d, self.n_crit)
-            books = [self.C_base] + self.C_ext
+            books = self.C_basic + self.C_ext
             rec.pre("beam", X=self.Ws[:, :self.n_crit], books=books, beam=cfg.beam)
-            C.crvq_assign_residual_beam(Vc, books, cfg.beam, [self.codes] + self.codes_ext, self.beam_err,
-                                        ldc=[N // d] + [self.ncv] * len(self.C_ext))
+            C.crvq_assign_residual_beam(Vc, books, cfg.beam, self.codes_basic + self.codes_ext, self.beam_err,
+                                        ldc=[N // d] * mb + [self.ncv] * len(self.C_ext))
             rec.post("beam", codes_base=self.codes.view(M, N // d)[:, :self.ncv],
+                     codes_basic=[q.view(M, N // d)[:, :self.ncv] for q in self.codes_basic],
                      codes_ext=list(self.codes_ext), err=self.beam_err)
 
-        rec.pre("dequant", codes=self.codes, codes_ext=list(self.codes_ext), books=[self.C_base] + self.C_ext,
-                perm=self.perm)
-        C.crvq_dequant(M, N, d, self.codes, N // d, self.C_base, self.W_hat, n_crit=self.n_crit,
-                       q_ext=self.codes_ext, ldq_ext=self.ncv, C_ext=self.C_ext, perm=self.perm)
+        rec.pre("dequant", codes=self.codes, codes_basic=list(self.codes_basic), codes_ext=list(self.codes_ext),
+                books=self.C_basic + self.C_ext, perm=self.perm)
+        C.crvq_dequant_books(M, N, d, self.codes_basic, N // d, self.C_basic, self.W_hat, n_crit=self.n_crit,
+                             q_ext=self.codes_ext, ldq_ext=self.ncv, C_ext=self.C_ext, perm=self.perm)
         rec.post("dequant", out=self.W_hat)
 
         return LayerState(self.hdiag, self.imp, self.perm, self.Ws, self.n_crit, self.C_base, self.C_ext, self.codes,
-                          self.codes_ext, self.beam_err, self.W_hat)
+                          self.codes_ext, self.beam_err, self.W_hat, self.C_basic, self.codes_basic)
 
     def _kmeans(self, V: VecSet, Cb: torch.Tensor, codes: torch.Tensor, rec, tag: str):
         for it in range(self.cfg.iters):

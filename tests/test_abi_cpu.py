@@ -186,3 +186,68 @@ def test_oracle_and_gpu_path_share_no_code():
                 assert not any(m.startswith("oracle") for m in _imports(p)), p
             if f.endswith((".hip", ".h", ".cpp")):
                 assert "oracle" not in open(p).read().lower(), p
+
+
+def test_dequant_books_validation(L):
+    """crvq_dequant_books rejects bad book counts and NULL arrays before touching the device."""
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    q = ctypes.cast((ctypes.c_void_p * 3)(0x1000, 0x2000, 0x3000), PP)
+    C = ctypes.cast((ctypes.c_void_p * 3)(0x4000, 0x5000, 0x6000), PP)
+    dts = ctypes.cast((ctypes.c_int32 * 3)(0, 0, 0), ctypes.c_void_p)
+    Ks = ctypes.cast((ctypes.c_int64 * 3)(256, 256, 16), ctypes.c_void_p)
+    call = lambda nb, ne, q=q, C=C, n_crit=16, ldq_ext=1: L.crvq_dequant_books(
+        4, 32, 16, n_crit, nb, ne, q, 2, ldq_ext, C, dts, Ks, None, None, 0, 0, FAKE, 0, 32, None, 0, None)
+    assert call(0, 1) == 1 and "n_base" in err(L)
+    assert call(2, 7) == 1
+    assert call(2, 1, q=None) == 1 and "must not be NULL" in err(L)
+    assert call(2, 1, C=None) == 1
+    assert call(2, 1, n_crit=8) == 1            # not a multiple of d = 16
+    assert call(2, 1, ldq_ext=0) == 1 and "ldq_ext" in err(L)
+    Kbad = ctypes.cast((ctypes.c_int64 * 3)(256, 0, 16), ctypes.c_void_p)
+    assert L.crvq_dequant_books(4, 32, 16, 16, 2, 1, q, 2, 1, C, dts, Kbad, None, None, 0, 0, FAKE, 0, 32, None, 0,
+                                None) == 1 and "outside" in err(L)
+    assert L.crvq_dequant_books(4, 32, 16, 16, 2, 1, q, 2, 1, C, dts, Ks, FAKE, None, 0, 0, FAKE, 0, 32, None, 0,
+                                None) == 3  # perm without the workspace
+
+
+def test_bits_per_weight_against_eq6_eq8():
+    """crvq_bits_per_weight (host-only) against Eq. 6 / Eq. 8 as the oracle states them, the paper's
+    printed values (tests/golden/bits_per_weight.json) and the increments each stored object adds."""
+    import json
+    import oracle
+    from paper_2412_09282_amd import crvq as C
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "bits_per_weight.json")))
+    g = gold["vq_m1_e8_d8"]
+    v = C.crvq_bits_per_weight(4096, 4096, 8, 0, [256], perm_bits=0)
+    assert abs(v - g["printed"]) <= g["printed_precision"]
+    assert v == oracle.bits_per_weight_vq(1, 8, 8)
+    # 8+8x3 at lambda = 0.02: 88 critical columns (8 * ceil(0.02 * 4096 / 8)) stand in for lambda N
+    for perm_bits in (0, 16):
+        v = C.crvq_bits_per_weight(4096, 4096, 8, 88, [256], [256] * 3, perm_bits=perm_bits)
+        e = oracle.bits_per_weight_crvq(4, 8, 8, 88 / 4096, include_perm=perm_bits == 16)
+        assert abs(v - e) < 1e-12, (v, e)
+    # the m = 2, d = 16 setting, with and without three extended books
+    v = C.crvq_bits_per_weight(4096, 4096, 16, 0, [256, 256], perm_bits=0)
+    assert v == oracle.bits_per_weight_vq(2, 8, 16)
+    v = C.crvq_bits_per_weight(4096, 4096, 16, 96, [256, 256], [256] * 3, perm_bits=0)
+    assert abs(v - oracle.bits_per_weight_crvq(5, 8, 16, 96 / 4096, m_base=2)) < 1e-12
+    # wider basic books (e = 10, 12) then one extended e = 8 book: Eq. 6 plus one extended book's share
+    for e in (10, 12):
+        base = C.crvq_bits_per_weight(4096, 4096, 8, 0, [2 ** e], perm_bits=0)
+        assert abs(base - oracle.bits_per_weight_vq(1, e, 8)) < 1e-12
+        v = C.crvq_bits_per_weight(4096, 4096, 8, 88, [2 ** e], [256], perm_bits=0)
+        inc = oracle.bits_per_weight_crvq(2, 8, 8, 88 / 4096) - oracle.bits_per_weight_vq(1, 8, 8)
+        assert abs(v - base - inc) < 1e-12
+    # a book of K codewords that is not a power of two takes ceil(log2 K)-bit codes and K stored codewords
+    v100 = C.crvq_bits_per_weight(64, 64, 8, 0, [100], perm_bits=0)
+    v128 = C.crvq_bits_per_weight(64, 64, 8, 0, [128], perm_bits=0)
+    assert abs((v128 - v100) - 28 * 8 * 16 / (64 * 64)) < 1e-12
+    assert C.crvq_bits_per_weight(64, 64, 8, 0, [1], perm_bits=0, codeword_bits=16) == 8 * 16 / (64 * 64)
+    with pytest.raises(C.CrvqError):
+        C.crvq_bits_per_weight(64, 60, 8, 0, [256])      # cols not a multiple of d
+    with pytest.raises(C.CrvqError):
+        C.crvq_bits_per_weight(64, 64, 8, 4, [256], [16])  # n_crit not a multiple of d
+    with pytest.raises(C.CrvqError):
+        C.crvq_bits_per_weight(64, 64, 8, 0, [0])
+    with pytest.raises(C.CrvqError):
+        C.crvq_bits_per_weight(64, 64, 8, 0, [256], codeword_bits=0)

@@ -510,3 +510,78 @@ def test_w_only_importance_is_max_square(oracle_mod):
     W = (g.standard_normal((33, 40)) * 0.02).astype(np.float32)
     got = opipe.channel_importance(W, np.ones(40, np.float32), "f32", "w_only")
     np.testing.assert_array_equal(got, (W.astype(np.float64) ** 2).max(0).astype(np.float32))
+
+
+# ------------------------------------------------------------------------------------------------
+# several basic codebooks (the m = 2, d = 16 setting of Sec. 3.2 / Sec. 6.4)
+# ------------------------------------------------------------------------------------------------
+def _two_book_layer(K_base, crit_frac, width, seed=5, M=8, N=32, d=16, K_ext=(4,), iters=2, dtype="f32"):
+    wl = inputs.small_workload(M=M, N=N, tokens=32, d=d, K_base=K_base, K_ext=K_ext, crit_frac=crit_frac,
+                               beam=width, iters=iters, dtype=dtype, wid=200 + seed, m_base=2)
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    n = M * N // d
+    n_crit = inputs.n_crit_columns(N, d, crit_frac)
+    base_idx = inputs.base_init_indices(wl, 0, n)
+    extra = [inputs.extra_base_init_indices(wl, 0, 1, n)]
+    ext_idx = [inputs.ext_init_indices(wl, 0, t + 1, M * n_crit // d) for t in range(len(K_ext))]
+    res = opipe.quantize_layer(W, X, dtype, d, K_base, list(K_ext), crit_frac, width, iters, base_idx, ext_idx,
+                               m_base=2, base_idx_extra=extra)
+    return W, res, n_crit
+
+
+def test_two_basic_books_exhaustive_when_beam_covers_first_book(oracle_mod):
+    """Beam width = K of the first basic book makes the basic-book search exhaustive over all K^2 pairs:
+    every non-critical vector must carry the brute-force best pair, and W_hat must be that pair's sum
+    (critical vectors: the sum of their three chosen codewords), put back in original channel order."""
+    K, d = 4, 16
+    W, res, n_crit = _two_book_layer(K, 0.5, K, M=32, N=64)
+    M, N = W.shape
+    C0, C1 = (b.astype(np.float64) for b in res.C_basic)
+    assert len(res.C_basic) == 2 and len(res.codes_basic) == 2 and len(res.C_ext) == 1
+    Ws = W[:, res.perm].astype(np.float64)
+    What_s = res.W_hat[:, res.perm].astype(np.float64)
+    pairs = C0[:, None, :] + C1[None, :, :]                       # K x K x d
+    ncv = n_crit // d
+    greedy_worse = 0
+    for r in range(M):
+        for g in range(N // d):
+            v = r * (N // d) + g
+            x = Ws[r, g * d:(g + 1) * d]
+            q0, q1 = res.codes_basic[0][v], res.codes_basic[1][v]
+            if g >= ncv:
+                dist = ((pairs - x) ** 2).sum(-1)
+                assert dist[q0, q1] == dist.min()
+                a = int(np.argmin(((C0 - x) ** 2).sum(-1)))
+                greedy_worse += dist[a].min() > dist.min()
+                exp = (C0[q0] + C1[q1]).astype(np.float32)
+            else:
+                qe = res.codes_ext[0][r * ncv + g]
+                exp = (C0[q0] + C1[q1] + res.C_ext[0][qe].astype(np.float64)).astype(np.float32)
+            np.testing.assert_array_equal(What_s[r, g * d:(g + 1) * d], exp)
+    assert greedy_worse > 0  # the inputs are ones where the joint search beats the greedy one
+    # the second basic book lowers every K-means objective it fits, and the total error drops below
+    # that of the first book alone
+    J2 = res.objectives["base2"]
+    assert all(b <= a * (1 + 1e-9) for a, b in zip(J2, J2[1:]))
+    err_noncrit = ((Ws[:, n_crit:] - What_s[:, n_crit:]) ** 2).sum()
+    first_only = sum(((Ws[r, g * d:(g + 1) * d] - C0[res.codes_basic[0][r * (N // d) + g]]) ** 2).sum()
+                     for r in range(M) for g in range(ncv, N // d))
+    assert err_noncrit <= first_only
+
+
+def test_two_basic_books_exact_when_every_vector_is_a_codeword(oracle_mod):
+    """With K at least the number of vectors the first basic book holds every vector exactly, the
+    residual is zero, so the second basic book and the extended one are zero and W_hat equals W."""
+    W, res, _ = _two_book_layer(32, 0.25, 2, K_ext=(4,))
+    np.testing.assert_array_equal(res.W_hat, W)
+    assert not res.C_basic[1].any() and not res.C_ext[0].any()
+
+
+def test_bits_two_basic_books():
+    """Eq. 8 with m_base basic books and no critical channels is Eq. 6 with m = m_base books; of the two
+    e = 8 settings near one bit the paper names, m = 1, d = 8 is the smaller."""
+    assert abs(oracle.bits_per_weight_crvq(2, 8, 16, 0.0, m_base=2) - oracle.bits_per_weight_vq(2, 8, 16)) < 1e-15
+    a, b = oracle.bits_per_weight_vq(1, 8, 8), oracle.bits_per_weight_vq(2, 8, 16)
+    assert 1.0 < a < b < 1.01
+    assert oracle.bits_per_weight_crvq(5, 8, 16, 0.02, m_base=2) > b

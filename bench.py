@@ -420,6 +420,146 @@ def gemv_bench(args):
             torch.cuda.empty_cache()
 
 
+# ------------------------------------------------------------------------------------------------
+# --refine: the loss-driven refinement loop (QuantLoss, FineTuneCodebook, width-1 code search) on a
+# full-size K = 256 layout, per call kind, with sampled oracle checks
+# ------------------------------------------------------------------------------------------------
+PEAK_FP64_TFLOPS = 78.6
+
+
+class RefineHook:
+    """HIP events around every library call of the refinement loop (no cache flush: the loop's own
+    reuse of H and the codebooks is part of what it costs), plus host copies of sampled inputs."""
+
+    def __init__(self, rows):
+        import torch
+        self.torch = torch
+        self.rows = rows
+        self.calls = []
+        self.checks = {}
+
+    def pre(self, name, kw):
+        torch = self.torch
+        if name == "gram" or (name.startswith("hessian") and "hessian" not in self.checks) or \
+                (name.startswith("refine") and name.endswith("_0") and "refine" not in self.checks):
+            torch.cuda.synchronize()
+            if name.startswith("hessian"):
+                self.checks["hessian"] = {"R": kw["R"][self.rows].cpu().numpy()}
+            elif name.startswith("refine"):
+                self.checks["refine"] = {"R": kw["R"][self.rows].cpu().numpy(), "C": kw["C"].cpu().numpy(),
+                                         "codes": kw["codes"].view(kw["R"].shape[0], -1)[self.rows].cpu().numpy(),
+                                         "n_cols": kw["n_cols"]}
+        self.cur = (name, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        self.cur[1].record()
+
+    def post(self, name, kw):
+        torch = self.torch
+        self.cur[2].record()
+        torch.cuda.synchronize()
+        self.calls.append((name, self.cur[1].elapsed_time(self.cur[2])))
+        if name == "gram":
+            self.checks["gram"] = {"H": kw["H"].cpu().numpy(), "Xs": kw["Xs"].cpu().numpy()}
+        elif name.startswith("hessian") and "G" not in self.checks.get("hessian", {}):
+            self.checks["hessian"]["G"] = kw["G"][self.rows].cpu().numpy()
+        elif name.startswith("refine") and "out" not in self.checks.get("refine", {"out": 1}):
+            self.checks["refine"]["out"] = kw["codes"].view(kw["R"].shape[0], -1)[self.rows].cpu().numpy()
+            self.checks["refine"]["R_out"] = kw["R"][self.rows].cpu().numpy()
+
+
+def refine_bench(args):
+    import numpy as np
+    import torch
+
+    import oracle
+    from oracle import refine as orf
+    from paper_2412_09282_amd import crvq, inputs
+    from paper_2412_09282_amd.pipeline import LayerConfig, LayerQuantizer
+
+    crvq.lib(build_if_missing=True)
+    torch.cuda.set_device(0)
+    wid = args.refine_workload
+    wl = inputs.workload(wid)
+    L = wl.layers[0]
+    M, N, d = L.M, L.N, wl.d
+    if L.dtype != "f32":
+        raise SystemExit("the refinement tunes fp32 codebooks: pick an fp32 workload")
+    n = M * N // d
+    n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    bi = torch.from_numpy(inputs.base_init_indices(wl, 0, n)).cuda()
+    ei = [torch.from_numpy(inputs.ext_init_indices(wl, 0, t, M * n_crit // d)).cuda()
+          for t in range(1, len(wl.K_ext) + 1)]
+    xi = [torch.from_numpy(inputs.extra_base_init_indices(wl, 0, b, n)).cuda() for b in range(1, wl.m_base)]
+    Wd, Xd = torch.from_numpy(W).cuda(), torch.from_numpy(X).cuda()
+    cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, m_base=wl.m_base)
+    q = LayerQuantizer(M, N, torch.float32, cfg, L.tokens, device="cuda")
+    kw = dict(rounds=args.rounds, steps=args.ft_steps, lr=args.lr)
+    # warm-up: one layer pass and one refinement loop
+    q.run(Wd, Xd, bi, ei, base_idx_extra=xi)
+    q.refine(Xd, **kw)
+    # timed: a fresh layer pass, then the loop with no hooks
+    q.run(Wd, Xd, bi, ei, base_idx_extra=xi)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    losses = q.refine(Xd, **kw)
+    e1.record()
+    torch.cuda.synchronize()
+    total_ms = e0.elapsed_time(e1)
+    # per call, with sampled oracle checks
+    rows = np.sort(np.random.default_rng([inputs.ROOT_SEED, wid, 77]).choice(M, 4, replace=False))
+    hook = RefineHook(rows)
+    q.run(Wd, Xd, bi, ei, base_idx_extra=xi)
+    losses_h = q.refine(Xd, hooks=[hook], **kw)
+    torch.cuda.synchronize()
+    ck = hook.checks
+    H, Xs = ck["gram"]["H"], ck["gram"]["Xs"].astype(np.float64)
+    g = np.random.default_rng(5)
+    ij = g.integers(0, N, (256, 2))
+    ok_gram = all(abs(H[i, j] - float(Xs[:, i] @ Xs[:, j])) <= 1e-12 * float(np.abs(Xs[:, i]) @ np.abs(Xs[:, j]))
+                  for i, j in ij)
+    Rr, Gr = ck["hessian"]["R"], ck["hessian"]["G"]
+    ok_hess = bool((np.abs(Gr - Rr @ H) <= 1e-12 * (np.abs(Rr) @ np.abs(H))).all())
+    rf = ck["refine"]
+    Ro, qo = rf["R"].copy(), rf["codes"].copy().ravel()
+    t0 = time.perf_counter()
+    orf.refine_book(Ro, H, rf["C"], qo, d, rf["n_cols"])
+    t_or = time.perf_counter() - t0
+    ok_ref = bool(np.array_equal(qo, rf["out"].ravel()) and np.array_equal(Ro, rf["R_out"]))
+    groups = {}
+    for name, ms in hook.calls:
+        kind = name.split("_")[0]
+        if kind in ("refine", "code"):
+            kind = kind + ("_basic" if int(name.split("_")[-1]) < wl.m_base else "_ext")
+        groups.setdefault(kind, []).append(ms)
+    F64 = PEAK_FP64_TFLOPS * 1e12
+    HBM = PEAK_HBM_GBS * 1e9
+    work = {"gram": (2.0 * N * N * L.tokens, "FLOP", F64),
+            "hessian": (2.0 * M * N * N, "FLOP", F64),
+            "residual": (M * N * 12.0 + 4.0 * n * (wl.m_base + len(wl.K_ext)), "B", HBM),
+            "code_basic": (M * N * 8.0 + 4.0 * n, "B", HBM),
+            "code_ext": (M * n_crit * 8.0 + 4.0 * M * (n_crit // d), "B", HBM),
+            "adam": (wl.K_base * d * 40.0, "B", HBM),
+            "refine_basic": (2.0 * M * N * N + 2.0 * M * (N // d) * wl.K_base * d, "FLOP", F64),
+            "refine_ext": (2.0 * M * N * n_crit + 2.0 * M * (n_crit // d) * 256 * d, "FLOP", F64)}
+    for kind, mss in groups.items():
+        w, unit, peak = work[kind]
+        med = float(np.median(mss))
+        rec = {"mode": "refine", "workload": wid, "layer": f"{L.name} {M}x{N} f32", "call": kind, "calls": len(mss),
+               "gpu_ms_median": round(med, 4), "gpu_ms_total": round(float(np.sum(mss)), 3),
+               "work_per_call": w, "work_unit": unit, "rate": w / (med * 1e-3), "frac": w / (med * 1e-3) / peak,
+               "bound": "fp64" if unit == "FLOP" else "hbm"}
+        print(json.dumps(rec), flush=True)
+    print(json.dumps({"mode": "refine", "workload": wid, "name": wl.name, "call": "whole refinement loop",
+                      "rounds": args.rounds, "adam_steps_per_round": args.ft_steps, "lr": args.lr,
+                      "gpu_ms": round(total_ms, 3), "quant_loss": losses, "quant_loss_hooked_run": losses_h,
+                      "rel_reduction": 1.0 - losses[-1] / losses[0],
+                      "parity": {"gram_sampled_entries": ok_gram, "hessian_sampled_rows": ok_hess,
+                                 "refine_book0_sampled_rows": ok_ref},
+                      "oracle_refine_rows_s": round(t_or, 3), "oracle_rows": len(rows)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -438,6 +578,12 @@ def main():
     ap.add_argument("--gemv", action="store_true",
                     help="instead of the benchmark line: the quantized matrix-vector product on the LLaMA gate "
                          "projections, beside a dense bf16 matrix-vector product and the oracle")
+    ap.add_argument("--refine", action="store_true",
+                    help="instead of the benchmark line: the loss-driven refinement loop on --refine-workload")
+    ap.add_argument("--refine-workload", type=int, default=21)
+    ap.add_argument("--rounds", type=int, default=2)
+    ap.add_argument("--ft-steps", type=int, default=5)
+    ap.add_argument("--lr", type=float, default=1e-4)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
@@ -448,6 +594,9 @@ def main():
         return
     if args.gemv:
         gemv_bench(args)
+        return
+    if args.refine:
+        refine_bench(args)
         return
 
     import numpy as np

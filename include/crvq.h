@@ -50,7 +50,9 @@ typedef enum {
   CRVQ_ERR_HIP = 4          /* the HIP runtime reported an error while enqueueing */
 } crvq_status;
 
-typedef enum { CRVQ_F32 = 0, CRVQ_BF16 = 1 } crvq_dtype;
+/* CRVQ_F64 is accepted only where a call says so (the fp64 operands of the
+ * refinement calls and the fp64 output of crvq_dequant / crvq_dequant_books). */
+typedef enum { CRVQ_F32 = 0, CRVQ_BF16 = 1, CRVQ_F64 = 2 } crvq_dtype;
 typedef enum { CRVQ_REDUCE_SUM = 0, CRVQ_REDUCE_MAX = 1 } crvq_reduce;
 
 #define CRVQ_MAX_K 65536   /* codewords per codebook (e <= 16 bits) */
@@ -194,7 +196,9 @@ crvq_status crvq_gather_vectors(const void* X, int x_dtype, int64_t n_rows, int6
  *   minuend != NULL (residual mode):  out[r*ld_out + c] = minuend[r*ld_min + c] - R[r, c]
  *   perm != NULL (reverse reorder):   out[r*ld_out + perm[c]] = R[r, c]
  *   otherwise:                        out[r*ld_out + c] = R[r, c]
- * each rounded once to out_dtype.  perm and minuend are mutually exclusive.
+ * each rounded once to out_dtype (CRVQ_F64 allowed when perm is NULL: the
+ * residual of the refinement calls, minuend - R exact up to one fp64 rounding).
+ * perm and minuend are mutually exclusive.
  * n_crit is a multiple of d, 0 <= n_crit <= n_cols.  A code outside its
  * codebook yields NaN for that vector.
  * workspace: crvq_dequant_workspace_size(n_cols) bytes (only used with perm).
@@ -248,6 +252,72 @@ crvq_status crvq_dequant_books(int64_t M, int64_t n_cols, int32_t d, int64_t n_c
  */
 crvq_status crvq_bits_per_weight(int64_t rows, int64_t cols, int32_t d, int64_t n_crit, int32_t n_base, int32_t n_ext,
                                  const int64_t* Ks, int32_t codeword_bits, int32_t perm_bits, double* out);
+
+/* ===========================================================================
+ * Loss-driven refinement (Alg. 1: QuantLoss, FineTuneCodebook,
+ * BeamSearchOptimize at width 1).  A layer is taken in reordered channel order
+ * (critical channels first).  With calibration activations X stored
+ * tokens x N, H = X^T X is the paper's X X^T, R = W - W_hat, and
+ *   QuantLoss = ||W X^T - W_hat X^T||_F^2 = sum_r R_r H R_r^T,
+ *   d QuantLoss / d W_hat = -2 R H.
+ * All refinement arithmetic is fp64; codebooks being tuned are fp32.
+ * ------------------------------------------------------------------------- */
+
+/* crvq_gram -- H = X^T X (Appendix A.2: the Hessian proxy X X^T of Eq. 9-10,
+ * full matrix).  X: n_rows x n_cols of x_dtype (F32 or F64), row stride ld.
+ * H: n_cols x n_cols fp64, row stride ldh >= n_cols.  Products are exact in
+ * fp64 for fp32 input; sums are fused multiply-adds in row order. */
+crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols, int64_t ld, double* H, int64_t ldh,
+                      void* stream);
+
+/* crvq_hessian_product -- G = R H[:, 0:n_out] (so -2 G is the gradient of
+ * QuantLoss w.r.t. W_hat on those columns) and, when row_loss != NULL (needs
+ * n_out == N), row_loss[r] = sum_j R[r][j] G[r][j], the QuantLoss of row r
+ * (Alg. 1 QuantLoss).  R: M x N fp64 (stride ldr), H: N x N fp64 (stride
+ * ldh), G: M x n_out fp64 (stride ldg >= n_out).  Deterministic. */
+crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const double* R, int64_t ldr, const double* H,
+                                 int64_t ldh, double* G, int64_t ldg, double* row_loss, void* stream);
+
+/* crvq_code_sums -- sums[k] = sum of the vectors x_v with codes[v] == k, in
+ * fp64, and counts[k] their number (the per-codeword gradient of
+ * FineTuneCodebook when X holds -2 R H, or plain cluster sums).  X: vector set
+ * (see conventions) of CRVQ_F64 elements; codes: int32[n]; codes outside
+ * [0, K) belong to no code.  sums: K x d fp64; counts: int32[K] or NULL.
+ * 1 <= K <= 1024.  Deterministic: every code's members are added in vector
+ * order per block, the blocks in block order.
+ * workspace: crvq_code_sums_workspace_size(n, d, K) bytes. */
+size_t crvq_code_sums_workspace_size(int64_t n_vectors, int32_t d, int64_t K);
+crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
+                           const int32_t* codes, int64_t K, double* sums, int32_t* counts, void* workspace,
+                           size_t ws_bytes, void* stream);
+
+/* crvq_adam_step -- one Adam step (Kingma & Ba, with bias correction; the
+ * paper fine-tunes codebooks with beta1 = 0.9, beta2 = 0.95) on n fp32
+ * parameters C with gradient g = grad_scale * grad (fp64):
+ *   m = b1 m + (1 - b1) g,  v = b2 v + (1 - b2) g^2,
+ *   C = C - lr * (m / (1 - b1^step)) / (sqrt(v / (1 - b2^step)) + eps)
+ * in fp64 (each operation rounded on its own), C rounded once to fp32.
+ * m, v: fp64 state of n entries (zero before step 1).  step >= 1. */
+crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, double* m, double* v, int64_t n,
+                           int64_t step, double lr, double beta1, double beta2, double eps, void* stream);
+
+/* crvq_refine_codes -- BeamSearchOptimize of Alg. 1 at the paper's width 1,
+ * under QuantLoss, for one codebook C (K x d, F32 or BF16) covering the
+ * column groups 0 .. n_cols/d - 1 of an M x N layer (n_cols = N for a basic
+ * book, n_crit for an extended one).  For every group in column order and
+ * every row independently, the group's code becomes the k minimising QuantLoss
+ * with all other codes fixed (lowest k among equal values); the residual
+ * R (M x N fp64, stride ldr, in/out) and codes (int32, row stride ldq >=
+ * n_cols/d, in/out) are updated as it goes.  H: N x N fp64.  The loss change
+ * of candidate k in group g is evaluated as
+ *   c_k^T H_gg c_k - 2 c_k . ((R H)_g + H_gg c_cur) (minus the same at c_cur),
+ * with (R H) kept current by subtracting delta^T H[g rows, :] on every change.
+ * A code outside [0, K) leaves that row's group unchanged.  K * d <= 8192.
+ * workspace: crvq_refine_workspace_size(M, n_cols) bytes. */
+size_t crvq_refine_workspace_size(int64_t M, int64_t n_cols);
+crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, double* R, int64_t ldr, const double* H,
+                              int64_t ldh, const void* C, int c_dtype, int64_t K, int32_t* codes, int64_t ldq,
+                              void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * crvq_dequant_gemv -- matrix-vector product with a CRVQ-quantized layer, the

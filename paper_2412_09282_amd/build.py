@@ -29,6 +29,7 @@ SOURCES = {
     "k_reorder.hip": [],
     "k_dequant.hip": [],
     "k_gemv.hip": [],
+    "k_refine.hip": [],
 }
 
 COMMON = [

@@ -22,7 +22,7 @@ LIB_PATH = os.path.join(_HERE, "libcrvq.so")
 _lock = threading.Lock()
 _lib = None
 
-CRVQ_F32, CRVQ_BF16 = 0, 1
+CRVQ_F32, CRVQ_BF16, CRVQ_F64 = 0, 1, 2
 CRVQ_REDUCE_SUM, CRVQ_REDUCE_MAX = 0, 1
 STATUS = {0: "CRVQ_OK", 1: "CRVQ_ERR_INVALID", 2: "CRVQ_ERR_UNSUPPORTED", 3: "CRVQ_ERR_WORKSPACE", 4: "CRVQ_ERR_HIP"}
 
@@ -67,6 +67,15 @@ def lib(build_if_missing: bool = True):
                 "crvq_dequant_books": ([I64, I64, I32, I64, I32, I32, PP, I64, I64, PP, P, P, P, P, ctypes.c_int, I64,
                                         P, ctypes.c_int, I64, P, SZ, P], ctypes.c_int),
                 "crvq_bits_per_weight": ([I64, I64, I32, I64, I32, I32, P, I32, I32, P], ctypes.c_int),
+                "crvq_gram": ([P, ctypes.c_int, I64, I64, I64, P, I64, P], ctypes.c_int),
+                "crvq_hessian_product": ([I64, I64, I64, P, I64, P, I64, P, I64, P, P], ctypes.c_int),
+                "crvq_code_sums_workspace_size": ([I64, I32, I64], SZ),
+                "crvq_code_sums": ([P, I64, I64, I64, I32, P, I64, P, P, P, SZ, P], ctypes.c_int),
+                "crvq_adam_step": ([P, P, ctypes.c_double, P, P, I64, I64, ctypes.c_double, ctypes.c_double,
+                                    ctypes.c_double, ctypes.c_double, P], ctypes.c_int),
+                "crvq_refine_workspace_size": ([I64, I64], SZ),
+                "crvq_refine_codes": ([I64, I64, I32, I64, P, I64, P, I64, P, ctypes.c_int, I64, P, I64, P, SZ, P],
+                                      ctypes.c_int),
                 "crvq_gemv_workspace_size": ([I64, I64, I64], SZ),
                 "crvq_dequant_gemv": ([I64, I64, I64, P, I64, P, ctypes.c_int, I64, I32, PP, I64, PP, P, P, P, P,
                                        ctypes.c_int, P, P, SZ, P], ctypes.c_int),
@@ -89,6 +98,8 @@ def dtype_code(t: torch.Tensor) -> int:
         return CRVQ_F32
     if t.dtype == torch.bfloat16:
         return CRVQ_BF16
+    if t.dtype == torch.float64:
+        return CRVQ_F64
     raise TypeError(f"unsupported element type {t.dtype}")
 
 
@@ -273,6 +284,53 @@ def crvq_bits_per_weight(rows: int, cols: int, d: int, n_crit: int, K_base: Sequ
         rows, cols, d, n_crit, len(K_base), len(K_ext), ctypes.cast(arr, ctypes.c_void_p), codeword_bits, perm_bits,
         ctypes.byref(out)))
     return out.value
+
+
+# ---- loss-driven refinement (fp64 operands) -------------------------------------------------------
+def crvq_gram(X: torch.Tensor, H: torch.Tensor, stream=None) -> None:
+    """H = X^T X (fp64) for activations X stored tokens x N (fp32 or fp64)."""
+    assert X.dim() == 2 and X.stride(1) == 1 and H.dtype == torch.float64 and H.stride(1) == 1
+    _check("crvq_gram", lib().crvq_gram(_ptr(X), dtype_code(X), X.shape[0], X.shape[1], X.stride(0), _ptr(H),
+                                        H.stride(0), _stream(stream)))
+
+
+def crvq_hessian_product(R: torch.Tensor, H: torch.Tensor, G: torch.Tensor, row_loss: Optional[torch.Tensor] = None,
+                         stream=None) -> None:
+    """G = R H[:, :G.shape[1]] and optionally the per-row QuantLoss sum_j R_rj G_rj (fp64)."""
+    M, N = R.shape
+    _check("crvq_hessian_product", lib().crvq_hessian_product(
+        M, N, G.shape[1], _ptr(R), R.stride(0), _ptr(H), H.stride(0), _ptr(G), G.stride(0), _ptr(row_loss),
+        _stream(stream)))
+
+
+def crvq_code_sums(X: VecSet, codes: torch.Tensor, K: int, sums: torch.Tensor, counts: Optional[torch.Tensor] = None,
+                   stream=None) -> None:
+    """sums[k] = sum of the fp64 vectors coded k (see include/crvq.h)."""
+    L = lib()
+    assert X.t.dtype == torch.float64 and sums.dtype == torch.float64
+    ws = _workspace(L.crvq_code_sums_workspace_size(X.n, X.d, K), sums.device)
+    _check("crvq_code_sums", L.crvq_code_sums(_ptr(X.t), X.n_rows, X.vecs_per_row, X.ld, X.d, _ptr(codes), K,
+                                              _ptr(sums), _ptr(counts), _ptr(ws), 0 if ws is None else ws.numel(),
+                                              _stream(stream)))
+
+
+def crvq_adam_step(C: torch.Tensor, grad: torch.Tensor, grad_scale: float, m: torch.Tensor, v: torch.Tensor,
+                   step: int, lr: float, beta1: float = 0.9, beta2: float = 0.95, eps: float = 1e-8,
+                   stream=None) -> None:
+    assert C.dtype == torch.float32 and grad.dtype == m.dtype == v.dtype == torch.float64
+    _check("crvq_adam_step", lib().crvq_adam_step(_ptr(C), _ptr(grad), grad_scale, _ptr(m), _ptr(v), C.numel(), step,
+                                                  lr, beta1, beta2, eps, _stream(stream)))
+
+
+def crvq_refine_codes(R: torch.Tensor, H: torch.Tensor, C: torch.Tensor, codes: torch.Tensor, d: int, n_cols: int,
+                      ldq: int, stream=None) -> None:
+    """Width-1 QuantLoss code search for one book covering columns [0, n_cols) (R, codes in/out)."""
+    L = lib()
+    M, N = R.shape
+    ws = _workspace(L.crvq_refine_workspace_size(M, n_cols), R.device)
+    _check("crvq_refine_codes", L.crvq_refine_codes(
+        M, N, d, n_cols, _ptr(R), R.stride(0), _ptr(H), H.stride(0), _ptr(C), dtype_code(C), C.shape[0], _ptr(codes),
+        ldq, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
 
 
 def crvq_pack_codes_u8(codes: torch.Tensor, out: torch.Tensor, stream=None) -> None:

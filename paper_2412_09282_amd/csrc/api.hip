@@ -1,6 +1,8 @@
 // Host side of the libcrvq C ABI: argument validation (before anything is enqueued), workspace
 // sizing, and dispatch to the kernel launchers.  See include/crvq.h for the contract of each call.
 #include "crvq.h"
+#include <cmath>
+
 #include "crvq_internal.h"
 
 #include <cstdarg>
@@ -367,7 +369,8 @@ static crvq_status dequant_impl(const char* fn, int64_t M, int64_t n_cols, int32
     return fail(CRVQ_ERR_INVALID, "%s: need n_base >= 1, n_ext >= 0 and n_base + n_ext <= %d (got %d + %d)", fn,
                 CRVQ_MAX_BOOKS, n_base, n_ext);
   if (!out) return fail(CRVQ_ERR_INVALID, "%s: out must not be NULL", fn);
-  if (!dtype_ok(out_dtype)) return fail(CRVQ_ERR_INVALID, "%s: invalid out dtype", fn);
+  if (!dtype_ok(out_dtype) && !(out_dtype == CRVQ_F64 && !perm))
+    return fail(CRVQ_ERR_INVALID, "%s: invalid out dtype (CRVQ_F64 only without perm)", fn);
   if (ldq_base < n_cols / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_base < n_cols / d", fn);
   if (n_ext > 0 && ldq_ext < n_crit / d) return fail(CRVQ_ERR_INVALID, "%s: ldq_ext < n_crit / d", fn);
   if (ld_out < n_cols) return fail(CRVQ_ERR_INVALID, "%s: ld_out < n_cols", fn);
@@ -468,6 +471,104 @@ crvq_status crvq_bits_per_weight(int64_t rows, int64_t cols, int32_t d, int64_t 
   }
   *out = bits / (static_cast<double>(rows) * static_cast<double>(cols));
   return CRVQ_OK;
+}
+
+// ---- loss-driven refinement ----------------------------------------------------------------------
+crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols, int64_t ld, double* H, int64_t ldh,
+                      void* stream) {
+  static const char* fn = "crvq_gram";
+  g_err.clear();
+  if (n_rows < 0 || n_cols < 0) return fail(CRVQ_ERR_INVALID, "%s: negative size", fn);
+  if (x_dtype != CRVQ_F32 && x_dtype != CRVQ_F64) return fail(CRVQ_ERR_INVALID, "%s: x_dtype must be F32 or F64", fn);
+  if (ld < n_cols || ldh < n_cols) return fail(CRVQ_ERR_INVALID, "%s: ld and ldh must be >= n_cols", fn);
+  if (n_cols == 0) return CRVQ_OK;
+  if (!H || (n_rows > 0 && !X)) return fail(CRVQ_ERR_INVALID, "%s: X and H must not be NULL", fn);
+  return hip_status(launch_gemm_f64(n_cols, n_cols, n_rows, X, x_dtype == CRVQ_F32 ? ET_F32 : ET_F64, true, ld, X,
+                                    x_dtype == CRVQ_F32 ? ET_F32 : ET_F64, ld, H, ldh, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const double* R, int64_t ldr, const double* H,
+                                 int64_t ldh, double* G, int64_t ldg, double* row_loss, void* stream) {
+  static const char* fn = "crvq_hessian_product";
+  g_err.clear();
+  if (M < 0 || N < 1 || n_out < 1 || n_out > N) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and 1 <= n_out <= N", fn);
+  if (ldr < N || ldh < N || ldg < n_out) return fail(CRVQ_ERR_INVALID, "%s: ldr, ldh >= N and ldg >= n_out needed", fn);
+  if (row_loss && n_out != N) return fail(CRVQ_ERR_INVALID, "%s: row_loss needs n_out == N", fn);
+  if (M == 0) return CRVQ_OK;
+  if (!R || !H || !G) return fail(CRVQ_ERR_INVALID, "%s: R, H and G must not be NULL", fn);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  crvq_status s = hip_status(launch_gemm_f64(M, n_out, N, R, ET_F64, false, ldr, H, ET_F64, ldh, G, ldg, st), fn);
+  if (s || !row_loss) return s;
+  return hip_status(launch_row_dot(M, N, R, ldr, G, ldg, row_loss, st), fn);
+}
+
+size_t crvq_code_sums_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
+  if (n_vectors < 0 || d < 1 || d > CRVQ_MAX_D || K < 1 || K > 1024) return 0;
+  return code_sums_ws_bytes(n_vectors, K, d);
+}
+
+crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
+                           const int32_t* codes, int64_t K, double* sums, int32_t* counts, void* workspace,
+                           size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_code_sums";
+  g_err.clear();
+  if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
+  if (n_rows < 0 || vecs_per_row < 0) return fail(CRVQ_ERR_INVALID, "%s: negative n_rows or vecs_per_row", fn);
+  if (ld < vecs_per_row * d) return fail(CRVQ_ERR_INVALID, "%s: ld < vecs_per_row * d", fn);
+  if (K < 1 || K > 1024) return fail(CRVQ_ERR_UNSUPPORTED, "%s: K = %lld outside [1, 1024]", fn, (long long)K);
+  const int64_t n = n_rows * vecs_per_row;
+  if (n > 0x7fffffffLL) return fail(CRVQ_ERR_UNSUPPORTED, "%s: too many vectors", fn);
+  if (!sums || (n > 0 && (!X || !codes))) return fail(CRVQ_ERR_INVALID, "%s: X, codes and sums must not be NULL", fn);
+  crvq_status s = check_ws(workspace, ws_bytes, code_sums_ws_bytes(n, K, d), fn);
+  if (s) return s;
+  return hip_status(launch_code_sums(X, vecs_per_row > 0 ? vecs_per_row : 1, ld, d, n, codes, K, sums, counts,
+                                     workspace, static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, double* m, double* v, int64_t n,
+                           int64_t step, double lr, double beta1, double beta2, double eps, void* stream) {
+  static const char* fn = "crvq_adam_step";
+  g_err.clear();
+  if (n < 0 || step < 1) return fail(CRVQ_ERR_INVALID, "%s: need n >= 0 and step >= 1", fn);
+  if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0))
+    return fail(CRVQ_ERR_INVALID, "%s: need 0 <= beta1, beta2 < 1 and eps >= 0", fn);
+  if (n == 0) return CRVQ_OK;
+  if (!C || !grad || !m || !v) return fail(CRVQ_ERR_INVALID, "%s: C, grad, m and v must not be NULL", fn);
+  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
+  return hip_status(launch_adam(n, C, grad, grad_scale, m, v, lr, beta1, beta2, bc1, bc2, eps,
+                                static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+size_t crvq_refine_workspace_size(int64_t M, int64_t n_cols) {
+  if (M < 1 || n_cols < 1) return 0;
+  return align256(static_cast<size_t>(M) * static_cast<size_t>(n_cols) * sizeof(double));
+}
+
+crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, double* R, int64_t ldr, const double* H,
+                              int64_t ldh, const void* C, int c_dtype, int64_t K, int32_t* codes, int64_t ldq,
+                              void* workspace, size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_refine_codes";
+  g_err.clear();
+  if (M < 0 || N < 1) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and N >= 1", fn);
+  if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
+  if (n_cols < 0 || n_cols > N || n_cols % d || N % d)
+    return fail(CRVQ_ERR_INVALID, "%s: n_cols must be a multiple of d in [0, N] and d must divide N", fn);
+  if (!dtype_ok(c_dtype)) return fail(CRVQ_ERR_INVALID, "%s: c_dtype must be F32 or BF16", fn);
+  if (K < 1 || K * d > 8192 || refine_lds_bytes(K, d) + 4096 > 160 * 1024)
+    return fail(CRVQ_ERR_UNSUPPORTED, "%s: K = %lld with d = %d exceeds K * d <= 8192 (and the LDS of one CU)", fn,
+                (long long)K, d);
+  if (ldr < N || ldh < N || ldq < n_cols / d) return fail(CRVQ_ERR_INVALID, "%s: ldr, ldh >= N and ldq >= n_cols / d", fn);
+  if (M == 0 || n_cols == 0) return CRVQ_OK;
+  if (!R || !H || !C || !codes) return fail(CRVQ_ERR_INVALID, "%s: R, H, C and codes must not be NULL", fn);
+  crvq_status s = check_ws(workspace, ws_bytes, crvq_refine_workspace_size(M, n_cols), fn);
+  if (s) return s;
+  return hip_status(launch_refine_book(M, N, d, n_cols, R, ldr, H, ldh, C, c_dtype, K, codes, ldq,
+                                       static_cast<double*>(workspace), static_cast<hipStream_t>(stream)),
+                    fn);
 }
 
 }  // extern "C"

@@ -96,6 +96,8 @@ __global__ __launch_bounds__(256) void dequant_rows(int64_t M, int64_t n_cols, i
       if (minuend) x = elem(minuend, min_type, r * ld_min + c0 + t) - x;
       if (out_type == ET_F32)
         static_cast<float*>(out)[r * ld_out + c0 + t] = static_cast<float>(x);
+      else if (out_type == ET_F64)
+        static_cast<double*>(out)[r * ld_out + c0 + t] = x;
       else
         static_cast<uint16_t*>(out)[r * ld_out + c0 + t] = bf16_from_double(x);
     }
@@ -482,9 +484,9 @@ hipError_t launch_dequant(int64_t M, int64_t n_cols, int d, int64_t n_crit, cons
   const int64_t ncv = n_crit / d;
   const int64_t nvec = M * (n_cols / d);
   // d = 8 fast paths: every book, the output and the minuend 16-byte aligned per vector
-  bool fast = d == 8 && books.n_full == 1;
+  bool fast = d == 8 && books.n_full == 1 && out_type != ET_F64;
   for (int e = 0; e < books.n; ++e) fast = fast && (reinterpret_cast<uintptr_t>(books.C[e]) % 16 == 0);
-  const int esize = out_type == ET_F32 ? 4 : 2;
+  const int esize = out_type == ET_F32 ? 4 : (out_type == ET_F64 ? 8 : 2);
   fast = fast && (reinterpret_cast<uintptr_t>(out) % 16 == 0) && ((ld_out * esize) % 16 == 0);
   if (fast && minuend) {
     const int msize = min_type == ET_F32 ? 4 : 2;

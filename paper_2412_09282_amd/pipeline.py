@@ -221,6 +221,75 @@ class LayerQuantizer:
         return LayerState(self.hdiag, self.imp, self.perm, self.Ws, self.n_crit, self.C_base, self.C_ext, self.codes,
                           self.codes_ext, self.beam_err, self.W_hat, self.C_basic, self.codes_basic)
 
+    def refine(self, X: torch.Tensor, rounds: int, steps: int, lr: float, eps: float = 0.0, beta1: float = 0.9,
+               beta2: float = 0.95, adam_eps: float = 1e-8, trace: Optional[list] = None, hooks=()) -> List[float]:
+        """The loss-driven refinement of Alg. 1 after run(): while QuantLoss >= eps and fewer than `rounds`
+        rounds ran, `steps` Adam steps on every codebook (codes fixed), then the width-1 QuantLoss code
+        search over every book in order.  Works in reordered channel order on the codebooks and codes
+        run() left (fp32 layers); rebuilds W_hat at the end.  Returns QuantLoss before the loop and after
+        every round."""
+        cfg, d, M, N = self.cfg, self.cfg.d, self.M, self.N
+        if self.dtype != torch.float32:
+            raise ValueError("refinement tunes fp32 codebooks: quantize the layer in fp32")
+        hooks = list(hooks) + ([TraceHook(trace)] if trace is not None else [])
+        rec = _Recorder(hooks)
+        f64 = torch.float64
+        dev = self.W_hat.device
+        if not hasattr(self, "H"):
+            self.H = torch.empty(N, N, dtype=f64, device=dev)
+            self.Xs = torch.empty(X.shape[0], N, dtype=torch.float32, device=dev)
+            self.R = torch.empty(M, N, dtype=f64, device=dev)
+            self.G = torch.empty(M, N, dtype=f64, device=dev)
+            self.row_loss = torch.empty(M, dtype=f64, device=dev)
+        books = self.C_basic + self.C_ext
+        codes = self.codes_basic + self.codes_ext
+        mb = cfg.m_base
+        cover = [N] * mb + [self.n_crit] * len(self.C_ext)
+        ldq = [N // d] * mb + [max(1, self.ncv)] * len(self.C_ext)
+        sums = [torch.empty(b.shape[0], d, dtype=f64, device=dev) for b in books]
+        moments = [(torch.zeros(b.shape[0], d, dtype=f64, device=dev), torch.zeros(b.shape[0], d, dtype=f64, device=dev))
+                   for b in books]
+
+        rec.pre("gram", X=X, perm=self.perm)
+        C.crvq_reorder(X, self.Xs, self.perm)
+        C.crvq_gram(self.Xs, self.H)
+        rec.post("gram", Xs=self.Xs, H=self.H)
+
+        def loss_now(tag):
+            rec.pre(f"residual_{tag}", minuend=self.Ws, codes=list(codes), books=list(books))
+            C.crvq_dequant_books(M, N, d, codes[:mb], N // d, books[:mb], self.R, n_crit=self.n_crit, q_ext=codes[mb:],
+                                 ldq_ext=max(1, self.ncv), C_ext=books[mb:], minuend=self.Ws)
+            rec.post(f"residual_{tag}", out=self.R)
+            rec.pre(f"hessian_{tag}", R=self.R, H=self.H)
+            C.crvq_hessian_product(self.R, self.H, self.G, self.row_loss)
+            rec.post(f"hessian_{tag}", G=self.G, row_loss=self.row_loss)
+            return float(self.row_loss.cpu().numpy().sum())
+
+        losses = [loss_now("start")]
+        t = 0
+        r = 0
+        while losses[-1] >= eps and r < rounds:
+            for s_ in range(steps):
+                t += 1
+                for b, Cb in enumerate(books):
+                    Vg = VecSet.of_matrix(self.G, d, cover[b])
+                    rec.pre(f"code_sums_{r}_{s_}_{b}", X=self.G[:, :cover[b]], codes=codes[b], K=Cb.shape[0])
+                    C.crvq_code_sums(Vg, codes[b], Cb.shape[0], sums[b])
+                    rec.post(f"code_sums_{r}_{s_}_{b}", sums=sums[b])
+                    rec.pre(f"adam_{r}_{s_}_{b}", C=Cb, grad=sums[b], m=moments[b][0], v=moments[b][1], step=t)
+                    C.crvq_adam_step(Cb, sums[b], -2.0, moments[b][0], moments[b][1], t, lr, beta1, beta2, adam_eps)
+                    rec.post(f"adam_{r}_{s_}_{b}", C=Cb, m=moments[b][0], v=moments[b][1])
+                loss_now(f"{r}_{s_}")
+            for b, Cb in enumerate(books):
+                rec.pre(f"refine_{r}_{b}", R=self.R, H=self.H, C=Cb, codes=codes[b], n_cols=cover[b])
+                C.crvq_refine_codes(self.R, self.H, Cb, codes[b], d, cover[b], ldq[b])
+                rec.post(f"refine_{r}_{b}", R=self.R, codes=codes[b])
+            losses.append(loss_now(f"round{r}"))
+            r += 1
+        C.crvq_dequant_books(M, N, d, codes[:mb], N // d, books[:mb], self.W_hat, n_crit=self.n_crit,
+                             q_ext=codes[mb:], ldq_ext=max(1, self.ncv), C_ext=books[mb:], perm=self.perm)
+        return losses
+
     def _kmeans(self, V: VecSet, Cb: torch.Tensor, codes: torch.Tensor, rec, tag: str):
         for it in range(self.cfg.iters):
             rec.pre(f"assign_{tag}_{it}", X=V.t, C=Cb)

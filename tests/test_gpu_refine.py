@@ -1,0 +1,233 @@
+"""GPU parity of the loss-driven refinement calls (Alg. 1 QuantLoss / FineTuneCodebook /
+BeamSearchOptimize at width 1) against the oracle in oracle/refine.py.
+
+Tolerances: H, G, the row losses and the per-code sums are fp64 sums of exact products in an order
+the oracle does not share, so each entry is compared within 1e-12 of the sum of the absolute values
+of its terms.  The residual, the code search (same fp64 decisions on the same inputs) and Adam (the
+same rounded operations) are compared bit for bit."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import refine as orf
+from oracle import pipeline as opipe
+from paper_2412_09282_amd import crvq as C
+from paper_2412_09282_amd import inputs
+from paper_2412_09282_amd.pipeline import LayerConfig, LayerQuantizer
+
+from gpu_util import dev, say
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-12
+
+
+def rv(shape, seed, scale=1.0):
+    return (np.random.default_rng(seed).standard_normal(shape) * scale).astype(np.float32)
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+@pytest.mark.parametrize("T,N", [(300, 200), (64, 1), (2048, 512), (5, 130)])
+def test_gram(T, N):
+    say(f"gram {T}x{N}")
+    X = rv((T, N), T + N)
+    H = torch.empty(N, N, dtype=torch.float64, device="cuda")
+    C.crvq_gram(dev(X), H)
+    torch.cuda.synchronize()
+    X64 = X.astype(np.float64)
+    exp = X64.T @ X64
+    scale = np.abs(X64).T @ np.abs(X64)
+    assert (np.abs(host(H) - exp) <= TOL * scale + 1e-300).all()
+
+
+@pytest.mark.parametrize("M,N,n_out", [(37, 200, 200), (130, 256, 64), (1, 8, 8), (300, 1000, 1000)])
+def test_hessian_product(M, N, n_out):
+    say(f"hessian product {M}x{N} -> {n_out}")
+    g = np.random.default_rng(M + N)
+    R = g.standard_normal((M, N)) * 0.01
+    X = g.standard_normal((N + 7, N))
+    H = X.T @ X
+    Gt = torch.empty(M, n_out, dtype=torch.float64, device="cuda")
+    loss = torch.empty(M, dtype=torch.float64, device="cuda") if n_out == N else None
+    C.crvq_hessian_product(torch.from_numpy(R).cuda(), torch.from_numpy(H).cuda(), Gt, loss)
+    torch.cuda.synchronize()
+    exp = R @ H[:, :n_out]
+    assert (np.abs(host(Gt) - exp) <= TOL * (np.abs(R) @ np.abs(H[:, :n_out])) + 1e-300).all()
+    if loss is not None:
+        el = np.sum(R * exp, axis=1)
+        assert (np.abs(host(loss) - el) <= TOL * np.sum(np.abs(R) * (np.abs(R) @ np.abs(H)), axis=1)).all()
+
+
+@pytest.mark.parametrize("M,N,d,cover,K", [(64, 256, 8, 256, 256), (300, 512, 8, 40, 1000), (17, 64, 16, 64, 7),
+                                           (5, 24, 3, 24, 1), (1000, 1024, 8, 1024, 256)])
+def test_code_sums(M, N, d, cover, K):
+    say(f"code sums {M}x{N} d={d} cover={cover} K={K}")
+    g = np.random.default_rng(M * 3 + K)
+    G = g.standard_normal((M, N))
+    n = M * (cover // d)
+    codes = g.integers(0, K, n).astype(np.int32)
+    codes[::97] = -1            # outside the book: counted nowhere
+    sums = torch.empty(K, d, dtype=torch.float64, device="cuda")
+    counts = torch.empty(K, dtype=torch.int32, device="cuda")
+    Gt = torch.from_numpy(G).cuda()
+    C.crvq_code_sums(C.VecSet.of_matrix(Gt, d, cover), dev(codes), K, sums, counts)
+    torch.cuda.synchronize()
+    V = G[:, :cover].reshape(-1, d)
+    ok = codes >= 0
+    exp = np.zeros((K, d))
+    np.add.at(exp, codes[ok], V[ok])
+    absn = np.zeros((K, d))
+    np.add.at(absn, codes[ok], np.abs(V[ok]))
+    assert (np.abs(host(sums) - exp) <= TOL * absn + 1e-300).all()
+    np.testing.assert_array_equal(host(counts), np.bincount(codes[ok], minlength=K))
+
+
+def test_adam_steps_bitwise():
+    say("adam 3 steps")
+    K, d = 300, 8
+    Cb = rv((K, d), 1, 0.05)
+    Ct = dev(Cb.copy())
+    m = torch.zeros(K, d, dtype=torch.float64, device="cuda")
+    v = torch.zeros(K, d, dtype=torch.float64, device="cuda")
+    st = orf.AdamState(np.zeros((K, d)), np.zeros((K, d)))
+    Co = Cb.copy()
+    for t in range(1, 4):
+        grad = np.random.default_rng(t).standard_normal((K, d)) * 10.0
+        grad[0] = 0.0
+        C.crvq_adam_step(Ct, torch.from_numpy(grad).cuda(), -2.0, m, v, t, 1e-3)
+        Co = orf.adam_step(Co, -2.0 * grad, st, 1e-3)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(host(Ct), Co)
+        np.testing.assert_array_equal(host(m), st.m)
+        np.testing.assert_array_equal(host(v), st.v)
+
+
+def refine_case(M, N, d, K, n_cols, c_dtype, seed):
+    g = np.random.default_rng(seed)
+    W = rv((M, N), seed, 0.02)
+    X = rv((2 * N + 3, N), seed + 1)
+    Cb = rv((K, d), seed + 2, 0.02)
+    if c_dtype == "bf16":
+        Cb = inputs.f32_to_bf16_bits(Cb)
+    codes = g.integers(0, K, M * (n_cols // d)).astype(np.int32)
+    H = orf.gram(X)
+    # residual of W against this one book on its columns (the rest of R as W itself)
+    R = W.astype(np.float64)
+    Cw = oracle.widen(Cb, c_dtype).astype(np.float64)
+    R[:, :n_cols] -= Cw[codes].reshape(M, n_cols)
+    return R, H, Cb, codes
+
+
+@pytest.mark.parametrize("M,N,d,K,n_cols,c_dtype", [(37, 256, 8, 64, 256, "f32"), (64, 256, 8, 256, 32, "f32"),
+                                                   (20, 128, 16, 50, 128, "f32"), (33, 96, 8, 16, 96, "bf16"),
+                                                   (9, 64, 4, 1024, 64, "f32")])
+def test_refine_codes(M, N, d, K, n_cols, c_dtype):
+    say(f"refine codes {M}x{N} d={d} K={K} cols={n_cols} {c_dtype}")
+    R, H, Cb, codes = refine_case(M, N, d, K, n_cols, c_dtype, M + K)
+    Rt = torch.from_numpy(R.copy()).cuda()
+    qt = dev(codes.copy())
+    C.crvq_refine_codes(Rt, torch.from_numpy(H).cuda(), dev(Cb, c_dtype), qt, d, n_cols, n_cols // d)
+    torch.cuda.synchronize()
+    Ro, qo = R.copy(), codes.copy()
+    changes = orf.refine_book(Ro, H, Cb, qo, d, n_cols, c_dtype)
+    got = host(qt)
+    np.testing.assert_array_equal(got, qo)
+    np.testing.assert_array_equal(host(Rt), Ro)
+    assert changes > 0
+    say(f"refine codes: {changes} of {len(codes)} codes moved, identical to the oracle")
+
+
+def test_refine_codes_sampled_rows_full_size():
+    """The code search on a 4096 x 4096 layer with a K = 256 book: rows are independent given H and
+    the book, so sampled rows are re-run on the oracle from the same inputs."""
+    M, N, d, K = 4096, 4096, 8, 256
+    say(f"refine codes full size {M}x{N} K={K}")
+    g = np.random.default_rng(7)
+    W = rv((M, N), 8, 0.02)
+    X = rv((2048, N), 9)
+    Cb = rv((K, d), 10, 0.02)
+    codes = g.integers(0, K, M * N // d).astype(np.int32)
+    Xt = dev(X)
+    Ht = torch.empty(N, N, dtype=torch.float64, device="cuda")
+    C.crvq_gram(Xt, Ht)
+    R = W.astype(np.float64) - Cb.astype(np.float64)[codes].reshape(M, N)
+    Rt = torch.from_numpy(R).cuda()
+    qt = dev(codes.copy())
+    C.crvq_refine_codes(Rt, Ht, dev(Cb), qt, d, N, N // d)
+    torch.cuda.synchronize()
+    H = host(Ht)
+    rows = np.sort(g.choice(M, 6, replace=False))
+    Ro = R[rows].copy()
+    qo = codes.reshape(M, -1)[rows].copy().ravel()
+    orf.refine_book(Ro, H, Cb, qo, d, N)
+    np.testing.assert_array_equal(host(qt).reshape(M, -1)[rows].ravel(), qo)
+    np.testing.assert_array_equal(host(Rt)[rows], Ro)
+
+
+def test_refine_loop_lockstep():
+    """The whole refinement loop after a layer pass: every call re-run on the oracle from the GPU's
+    inputs, then the loss trajectory and codes against the oracle's own loop from the same start."""
+    M, N, d = 96, 256, 8
+    wl = inputs.small_workload(M=M, N=N, tokens=128, d=d, K_base=64, K_ext=(16,), crit_frac=0.1, beam=1, iters=2,
+                               dtype="f32", wid=140)
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    n = M * N // d
+    n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    base_idx = inputs.base_init_indices(wl, 0, n)
+    ext_idx = [inputs.ext_init_indices(wl, 0, 1, M * n_crit // d)]
+    cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
+    q = LayerQuantizer(M, N, torch.float32, cfg, tokens=128, device="cuda")
+    Xt = torch.from_numpy(X).cuda()
+    st = q.run(dev(W), Xt, torch.from_numpy(base_idx).cuda(), [torch.from_numpy(e).cuda() for e in ext_idx])
+    torch.cuda.synchronize()
+    start_books = [host(b).copy() for b in q.C_basic + q.C_ext]
+    start_codes = [host(c).copy() for c in q.codes_basic + q.codes_ext]
+    perm = host(st.perm)
+    Ws = host(st.Ws)
+    trace = []
+    losses = q.refine(Xt, rounds=2, steps=3, lr=1e-4, trace=trace)
+    torch.cuda.synchronize()
+    H = None
+    for c in trace:
+        name, ci, co = c["name"], c["in"], c["out"]
+        if name == "gram":
+            Xs = oracle.gather_columns(X, perm)
+            np.testing.assert_array_equal(co["Xs"].numpy(), Xs)
+            H = co["H"].numpy()
+            exp = orf.gram(Xs)
+            assert (np.abs(H - exp) <= TOL * (np.abs(Xs).T.astype(np.float64) @ np.abs(Xs)) + 1e-300).all()
+        elif name.startswith("residual"):
+            books = [b.numpy() for b in ci["books"]]
+            codes = [x.numpy() for x in ci["codes"]]
+            exp = orf.residual_f64(Ws, "f32", d, n_crit, codes, books, ["f32"] * len(books), 1)
+            np.testing.assert_array_equal(co["out"].numpy(), exp)
+        elif name.startswith("hessian"):
+            R = ci["R"].numpy()
+            G = co["G"].numpy()
+            assert (np.abs(G - R @ H) <= TOL * (np.abs(R) @ np.abs(H)) + 1e-300).all()
+        elif name.startswith("refine"):
+            Ro = ci["R"].numpy().copy()
+            qo = ci["codes"].numpy().copy()
+            orf.refine_book(Ro, H, ci["C"].numpy(), qo, d, ci["n_cols"])
+            np.testing.assert_array_equal(co["codes"].numpy(), qo)
+            np.testing.assert_array_equal(co["R"].numpy(), Ro)
+        elif name.startswith("adam"):
+            grad = ci["grad"].numpy()
+            stt = orf.AdamState(ci["m"].numpy().copy(), ci["v"].numpy().copy(), ci["step"] - 1)
+            Cn = orf.adam_step(ci["C"].numpy(), -2.0 * grad, stt, 1e-4)
+            np.testing.assert_array_equal(co["C"].numpy(), Cn)
+    ref = orf.refine_layer(Ws, oracle.gather_columns(X, perm), d, n_crit, start_books, start_codes, 1, lr=1e-4,
+                           steps=3, max_rounds=2)
+    np.testing.assert_allclose(losses, ref.losses, rtol=1e-9)
+    assert losses[-1] < losses[0]
+    for a, b in zip(q.codes_basic + q.codes_ext, ref.codes):
+        np.testing.assert_array_equal(host(a), b)
+    Wh = host(st.W_hat)
+    assert orf.quant_loss(W, Wh, X) == pytest.approx(losses[-1], rel=1e-5)
+    say(f"refine loop: QuantLoss {losses[0]:.6e} -> {losses[-1]:.6e} over {len(losses) - 1} rounds, "
+        f"{len(trace)} calls matched")

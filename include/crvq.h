@@ -311,10 +311,13 @@ crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, doub
  * n_cols/d, in/out) are updated as it goes.  H: N x N fp64.  The loss change
  * of candidate k in group g is evaluated as
  *   c_k^T H_gg c_k - 2 c_k . ((R H)_g + H_gg c_cur) (minus the same at c_cur),
- * with (R H) kept current by subtracting delta^T H[g rows, :] on every change.
- * A code outside [0, K) leaves that row's group unchanged.  K * d <= 8192.
- * workspace: crvq_refine_workspace_size(M, n_cols) bytes. */
-size_t crvq_refine_workspace_size(int64_t M, int64_t n_cols);
+ * with (R H) kept current as codes move: within a block of 64 columns by
+ * delta^T H[g rows, block columns] per change, and for the later columns by one
+ * product (the block's deltas) x H per block.  A code outside [0, K) leaves
+ * that row's group unchanged.  K * d <= 8192 and (K d + K) * 8 bytes plus
+ * 36 KiB must fit the 160 KiB LDS of a CU (K <= 1024 at d = 8).
+ * workspace: crvq_refine_workspace_size(M, N, n_cols) bytes. */
+size_t crvq_refine_workspace_size(int64_t M, int64_t N, int64_t n_cols);
 crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, double* R, int64_t ldr, const double* H,
                               int64_t ldh, const void* C, int c_dtype, int64_t K, int32_t* codes, int64_t ldq,
                               void* workspace, size_t ws_bytes, void* stream);

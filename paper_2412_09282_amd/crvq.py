@@ -73,7 +73,7 @@ def lib(build_if_missing: bool = True):
                 "crvq_code_sums": ([P, I64, I64, I64, I32, P, I64, P, P, P, SZ, P], ctypes.c_int),
                 "crvq_adam_step": ([P, P, ctypes.c_double, P, P, I64, I64, ctypes.c_double, ctypes.c_double,
                                     ctypes.c_double, ctypes.c_double, P], ctypes.c_int),
-                "crvq_refine_workspace_size": ([I64, I64], SZ),
+                "crvq_refine_workspace_size": ([I64, I64, I64], SZ),
                 "crvq_refine_codes": ([I64, I64, I32, I64, P, I64, P, I64, P, ctypes.c_int, I64, P, I64, P, SZ, P],
                                       ctypes.c_int),
                 "crvq_gemv_workspace_size": ([I64, I64, I64], SZ),
@@ -327,7 +327,7 @@ def crvq_refine_codes(R: torch.Tensor, H: torch.Tensor, C: torch.Tensor, codes: 
     """Width-1 QuantLoss code search for one book covering columns [0, n_cols) (R, codes in/out)."""
     L = lib()
     M, N = R.shape
-    ws = _workspace(L.crvq_refine_workspace_size(M, n_cols), R.device)
+    ws = _workspace(L.crvq_refine_workspace_size(M, N, n_cols), R.device)
     _check("crvq_refine_codes", L.crvq_refine_codes(
         M, N, d, n_cols, _ptr(R), R.stride(0), _ptr(H), H.stride(0), _ptr(C), dtype_code(C), C.shape[0], _ptr(codes),
         ldq, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))

@@ -543,9 +543,9 @@ crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, doub
                     fn);
 }
 
-size_t crvq_refine_workspace_size(int64_t M, int64_t n_cols) {
-  if (M < 1 || n_cols < 1) return 0;
-  return align256(static_cast<size_t>(M) * static_cast<size_t>(n_cols) * sizeof(double));
+size_t crvq_refine_workspace_size(int64_t M, int64_t N, int64_t n_cols) {
+  if (M < 1 || n_cols < 1 || N < n_cols) return 0;
+  return refine_ws_bytes(M, n_cols, N);
 }
 
 crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, double* R, int64_t ldr, const double* H,
@@ -564,10 +564,10 @@ crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, d
   if (ldr < N || ldh < N || ldq < n_cols / d) return fail(CRVQ_ERR_INVALID, "%s: ldr, ldh >= N and ldq >= n_cols / d", fn);
   if (M == 0 || n_cols == 0) return CRVQ_OK;
   if (!R || !H || !C || !codes) return fail(CRVQ_ERR_INVALID, "%s: R, H, C and codes must not be NULL", fn);
-  crvq_status s = check_ws(workspace, ws_bytes, crvq_refine_workspace_size(M, n_cols), fn);
+  crvq_status s = check_ws(workspace, ws_bytes, crvq_refine_workspace_size(M, N, n_cols), fn);
   if (s) return s;
-  return hip_status(launch_refine_book(M, N, d, n_cols, R, ldr, H, ldh, C, c_dtype, K, codes, ldq,
-                                       static_cast<double*>(workspace), static_cast<hipStream_t>(stream)),
+  return hip_status(launch_refine_book(M, N, d, n_cols, R, ldr, H, ldh, C, c_dtype, K, codes, ldq, workspace,
+                                       static_cast<hipStream_t>(stream)),
                     fn);
 }
 

@@ -182,7 +182,8 @@ hipError_t launch_pack_codes_u8(const int32_t* codes, int64_t n, uint8_t* out, h
 
 // ---- loss-driven refinement (k_refine.hip) ---------------------------------------------------------
 hipError_t launch_gemm_f64(int64_t M, int64_t Nc, int64_t Kd, const void* A, int a_type, bool trans_a, int64_t lda,
-                           const void* B, int b_type, int64_t ldb, double* C, int64_t ldc, hipStream_t stream);
+                           const void* B, int b_type, int64_t ldb, double* C, int64_t ldc, hipStream_t stream,
+                           bool sub = false);
 hipError_t launch_row_dot(int64_t M, int64_t n, const double* A, int64_t lda, const double* B, int64_t ldb,
                           double* out, hipStream_t stream);
 size_t code_sums_ws_bytes(int64_t n, int64_t K, int d);
@@ -191,8 +192,9 @@ hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int
 hipError_t launch_adam(int64_t n, float* C, const double* grad, double scale, double* m, double* v, double lr,
                        double b1, double b2, double bc1, double bc2, double eps, hipStream_t stream);
 size_t refine_lds_bytes(int64_t K, int d);
+size_t refine_ws_bytes(int64_t M, int64_t n_cols, int64_t N);
 hipError_t launch_refine_book(int64_t M, int64_t N, int d, int64_t n_cols, double* R, int64_t ldr, const double* H,
                               int64_t ldh, const void* Cb, int c_type, int64_t K, int32_t* codes, int64_t ldq,
-                              double* S, hipStream_t stream);
+                              void* ws, hipStream_t stream);
 
 }  // namespace crvq

@@ -11,9 +11,10 @@
 //    owner thread per code adding its members in vector order, then the block partials folded in
 //    block order -- deterministic, no atomics.
 //  * adam_kernel: one Adam step (moments in fp64, bias correction from the host) on an fp32 book.
-//  * refine_group_kernel: the width-1 code search of one column group for every row, minimising
-//    QuantLoss with all other codes fixed; the running product S = R H of the later columns is
-//    updated by the chosen codeword change.  One wave per row, eight rows per workgroup.
+//  * refine_block_kernel: the width-1 code search over a block of column groups (64 columns) for
+//    every row, minimising QuantLoss with all other codes fixed; the running product S = R H is
+//    updated in LDS inside the block and, for the later columns, by one product D H per block (D the
+//    block's codeword changes).  One wave per row, eight rows per workgroup.
 #include "crvq_internal.h"
 
 namespace crvq {
@@ -26,23 +27,28 @@ __device__ __forceinline__ double to_f64(T x) {
   return static_cast<double>(x);
 }
 
-// C[i][j] = sum_k opA(i, k) B(k, j) for i < M, j < Nc, k < Kd, where opA(i, k) = A[i * lda + k], or
-// A[k * lda + i] when TRANS_A, and B(k, j) = B[k * ldb + j].  Products are formed in fp64 (exact for
+// C[i][j] = sum_k opA(i, k) B(k, j) (or C[i][j] - that sum when SUB) for i < M, j < Nc, k < Kd, where
+// opA(i, k) = A[i * lda + k], or A[k * lda + i] when TRANS_A, and B(k, j) = B[k * ldb + j].  Products are formed in fp64 (exact for
 // fp32 operands) and accumulated with fused multiply-adds in k order.
-template <typename TA, typename TB, bool TRANS_A>
+template <typename TA, typename TB, bool TRANS_A, bool SUB>
 __global__ __launch_bounds__(256) void gemm_f64_kernel(int64_t M, int64_t Nc, int64_t Kd, const TA* __restrict__ A,
                                                        int64_t lda, const TB* __restrict__ B, int64_t ldb,
-                                                       double* __restrict__ C, int64_t ldc) {
+                                                       double* __restrict__ C, int64_t ldc, int64_t kchunk,
+                                                       int64_t c_part) {
   __shared__ double As[kGBK][kGBM];
   __shared__ double Bs[kGBK][kGBN];
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
   const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kGBM, j0 = static_cast<int64_t>(blockIdx.x) * kGBN;
+  // split over k: part blockIdx.z takes k in [kb, ke) and writes its own slice of C
+  const int64_t kb = static_cast<int64_t>(blockIdx.z) * kchunk;
+  const int64_t ke = kb + kchunk < Kd ? kb + kchunk : Kd;
+  C += static_cast<int64_t>(blockIdx.z) * c_part;
   double acc[8][8];
 #pragma unroll
   for (int i = 0; i < 8; ++i)
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = 0.0;
-  for (int64_t k0 = 0; k0 < Kd; k0 += kGBK) {
+  for (int64_t k0 = kb; k0 < ke; k0 += kGBK) {
 #pragma unroll
     for (int s = 0; s < kGBM * kGBK / 256; ++s) {
       const int e = tid + 256 * s;
@@ -56,7 +62,7 @@ __global__ __launch_bounds__(256) void gemm_f64_kernel(int64_t M, int64_t Nc, in
       }
       const int64_t gi = i0 + ii, gk = k0 + kk;
       double v = 0.0;
-      if (gi < M && gk < Kd) v = to_f64(TRANS_A ? A[gk * lda + gi] : A[gi * lda + gk]);
+      if (gi < M && gk < ke) v = to_f64(TRANS_A ? A[gk * lda + gi] : A[gi * lda + gk]);
       As[kk][ii] = v;
     }
 #pragma unroll
@@ -64,7 +70,7 @@ __global__ __launch_bounds__(256) void gemm_f64_kernel(int64_t M, int64_t Nc, in
       const int e = tid + 256 * s;
       const int jj = e % kGBN, kk = e / kGBN;
       const int64_t gj = j0 + jj, gk = k0 + kk;
-      Bs[kk][jj] = (gj < Nc && gk < Kd) ? to_f64(B[gk * ldb + gj]) : 0.0;
+      Bs[kk][jj] = (gj < Nc && gk < ke) ? to_f64(B[gk * ldb + gj]) : 0.0;
     }
     __syncthreads();
 #pragma unroll
@@ -88,9 +94,20 @@ __global__ __launch_bounds__(256) void gemm_f64_kernel(int64_t M, int64_t Nc, in
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int64_t gj = j0 + tx + 16 * j;
-      if (gj < Nc) C[gi * ldc + gj] = acc[i][j];
+      if (gj < Nc) C[gi * ldc + gj] = SUB ? C[gi * ldc + gj] - acc[i][j] : acc[i][j];
     }
   }
+}
+
+// C[i][j] = sum over parts p = 0 .. P - 1 in order of part[p][i][j] (the split-k partial products).
+__global__ __launch_bounds__(256) void sum_parts_kernel(int64_t M, int64_t Nc, int P, const double* __restrict__ part,
+                                                        double* __restrict__ C, int64_t ldc) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= M * Nc) return;
+  double acc = part[e];
+  for (int p = 1; p < P; ++p) acc = acc + part[static_cast<int64_t>(p) * M * Nc + e];
+  const int64_t i = e / Nc, j = e - i * Nc;
+  C[i * ldc + j] = acc;
 }
 
 // out[r] = sum_{j < n} A[r * lda + j] * B[r * ldb + j]: strided per-thread sums, then a fixed tree.
@@ -219,118 +236,119 @@ __global__ __launch_bounds__(256) void adam_kernel(int64_t n, float* __restrict_
   C[i] = static_cast<float>(static_cast<double>(C[i]) - lr * mh / (sqrt(vh) + eps));
 }
 
-// ---- width-1 code search of one column group ------------------------------------------------------
+// ---- width-1 code search, one block of column groups per launch ----------------------------------
 constexpr int kRfRows = 8;      // rows per workgroup, one wave each
 constexpr int kRfThreads = 64 * kRfRows;
-constexpr int kRfChunk = 4096;  // doubles of the H block staged per chunk (kRfChunk / d columns)
+constexpr int kRbCols = 64;     // columns per block (whole groups: 64 / d of them)
 
 __device__ __forceinline__ double book_elem(const void* C, int type, int64_t i) {
   if (type == ET_F32) return static_cast<double>(static_cast<const float*>(C)[i]);
   return static_cast<double>(__uint_as_float(static_cast<uint32_t>(static_cast<const uint16_t*>(C)[i]) << 16));
 }
 
-// Group g (columns g*d .. g*d + d - 1) of rows blockIdx.x * 8 + wave.  With s = (R H)_g (held in S),
-// the loss change of moving the code from c0 to c_k is
-//   c_k^T Hgg c_k - 2 c_k . (s + Hgg c0) - (the same at c0),
+// The groups of columns [c0, c0 + bw) in order, for rows blockIdx.x * 8 + wave.  With s = (R H)_g, the
+// loss change of moving a group's code from c0 to c_k is
+//   c_k^T Hgg c_k - 2 c_k . (s + Hgg c_cur) - (the same at c_cur),
 // so the row takes the k minimising f(k) = a_k - 2 c_k . b with a_k = c_k^T Hgg c_k and
-// b = s + Hgg c0 (lowest k on ties).  A moved row subtracts delta = c_k - c0 from its residual and
-// delta^T H[g rows, c] from S[r, c] for the later columns c < n_cols.  A code outside [0, K) leaves the
-// row unchanged.
+// b = s + Hgg c_cur (lowest k on ties).  The block's H and the rows' (R H) on the block's columns are
+// held in LDS; a moved row subtracts delta = c_k - c_cur from its residual and delta^T H[g rows, c] from
+// its (R H) on the block's later columns, and writes delta (zero if unmoved) to D, from which one
+// product D H updates the columns after the block.  A code outside [0, K) leaves the group unchanged.
 template <int DMAX>
-__global__ __launch_bounds__(kRfThreads) void refine_group_kernel(int64_t M, int d, int64_t g, int64_t n_cols,
+__global__ __launch_bounds__(kRfThreads) void refine_block_kernel(int64_t M, int d, int64_t c0, int bw,
                                                                  double* __restrict__ R, int64_t ldr,
-                                                                 double* __restrict__ S, int64_t lds,
+                                                                 const double* __restrict__ S, int64_t lds,
                                                                  const double* __restrict__ H, int64_t ldh,
                                                                  const void* __restrict__ Cb, int c_type, int K,
-                                                                 int32_t* __restrict__ codes, int64_t ldq) {
+                                                                 int32_t* __restrict__ codes, int64_t ldq,
+                                                                 double* __restrict__ D, int64_t ldd) {
   extern __shared__ double sm[];
-  double* Cs = sm;             // K * d
-  double* Ak = Cs + K * d;     // K
-  double* Hg = Ak + K;         // d * d
-  double* Hc = Hg + 256;       // kRfChunk
-  __shared__ double s_delta[kRfRows][16];
+  double* Cs = sm;                      // K * d
+  double* Ak = Cs + K * d;              // K
+  double* Hb = Ak + K;                  // kRbCols x kRbCols
+  double* sS = Hb + kRbCols * kRbCols;  // kRfRows x kRbCols
   __shared__ double s_b[kRfRows][16];
-  __shared__ int s_moved[kRfRows];
+  __shared__ double s_delta[kRfRows][16];
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int64_t c0 = g * d;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kRfRows;
+  const int64_t r = r0 + w;
   for (int e = tid; e < K * d; e += kRfThreads) Cs[e] = book_elem(Cb, c_type, e);
-  for (int e = tid; e < d * d; e += kRfThreads) Hg[e] = H[(c0 + e / d) * ldh + c0 + e % d];
+  for (int e = tid; e < bw * bw; e += kRfThreads) {
+    const int i = e / bw, j = e - i * bw;
+    Hb[i * kRbCols + j] = H[(c0 + i) * ldh + c0 + j];
+  }
+  for (int e = tid; e < kRfRows * bw; e += kRfThreads) {
+    const int rr = e / bw, c = e - rr * bw;
+    sS[rr * kRbCols + c] = (r0 + rr < M) ? S[(r0 + rr) * lds + c0 + c] : 0.0;
+  }
   __syncthreads();
-  for (int k = tid; k < K; k += kRfThreads) {
-    double a = 0.0;
-    for (int t = 0; t < d; ++t) {
+  const int ng = bw / d;
+  for (int gi = 0; gi < ng; ++gi) {
+    const int cg = gi * d;
+    for (int k = tid; k < K; k += kRfThreads) {
+      double a = 0.0;
+      for (int t = 0; t < d; ++t) {
+        double h = 0.0;
+        for (int u = 0; u < d; ++u) h = h + Hb[(cg + t) * kRbCols + cg + u] * Cs[k * d + u];
+        a = a + Cs[k * d + t] * h;
+      }
+      Ak[k] = a;
+    }
+    const int64_t gq = c0 / d + gi;
+    const int cur = r < M ? codes[r * ldq + gq] : -1;
+    const bool active = cur >= 0 && cur < K;
+    if (active && lane < d) {  // b = s + Hgg c_cur, one lane per element
       double h = 0.0;
-      for (int u = 0; u < d; ++u) h = h + Hg[t * d + u] * Cs[k * d + u];
-      a = a + Cs[k * d + t] * h;
-    }
-    Ak[k] = a;
-  }
-  __syncthreads();
-  const int64_t r = static_cast<int64_t>(blockIdx.x) * kRfRows + w;
-  const int cur = r < M ? codes[r * ldq + g] : -1;
-  const bool active = cur >= 0 && cur < K;
-  if (active && lane < d) {  // b = s + Hgg c_cur, one lane per element
-    double h = 0.0;
-    for (int u = 0; u < d; ++u) h = h + Hg[lane * d + u] * Cs[cur * d + u];
-    s_b[w][lane] = S[r * lds + c0 + lane] + h;
-  }
-  __syncthreads();
-  int moved = 0;
-  if (active) {
-    double b[DMAX];
-#pragma unroll
-    for (int t = 0; t < DMAX; ++t) b[t] = t < d ? s_b[w][t] : 0.0;
-    double best = __builtin_inf();
-    int bk = K;
-#pragma unroll 1
-    for (int k = lane; k < K; k += 64) {
-      double dot = 0.0;
-#pragma unroll
-      for (int t = 0; t < DMAX; ++t)
-        if (t < d) dot = dot + Cs[k * d + t] * b[t];
-      const double f = Ak[k] - 2.0 * dot;
-      if (f < best) {
-        best = f;
-        bk = k;
-      }
-    }
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) {
-      const double ob = __shfl_xor(best, m);
-      const int ok = __shfl_xor(bk, m);
-      if (ob < best || (ob == best && ok < bk)) {
-        best = ob;
-        bk = ok;
-      }
-    }
-    if (bk < K && bk != cur) {
-      moved = 1;
-      if (lane < d) {
-        const double delta = Cs[bk * d + lane] - Cs[cur * d + lane];
-        s_delta[w][lane] = delta;
-        R[r * ldr + c0 + lane] = R[r * ldr + c0 + lane] - delta;
-      }
-      if (lane == 0) codes[r * ldq + g] = bk;
-    }
-  }
-  if (lane == 0) s_moved[w] = moved;
-  __syncthreads();
-  int any = 0;
-  for (int i = 0; i < kRfRows; ++i) any |= s_moved[i];
-  if (!any) return;  // the same for every thread of the block
-  const int64_t cw = kRfChunk / d;  // columns per chunk
-  for (int64_t cs = c0 + d; cs < n_cols; cs += cw) {
-    const int64_t cn = n_cols - cs < cw ? n_cols - cs : cw;
-    for (int64_t e = tid; e < d * cn; e += kRfThreads) {
-      const int64_t t = e / cn, c = e - t * cn;
-      Hc[t * cw + c] = H[(c0 + t) * ldh + cs + c];
+      for (int u = 0; u < d; ++u) h = h + Hb[(cg + lane) * kRbCols + cg + u] * Cs[cur * d + u];
+      s_b[w][lane] = sS[w * kRbCols + cg + lane] + h;
     }
     __syncthreads();
+    int moved = 0;
+    if (active) {
+      double b[DMAX];
+#pragma unroll
+      for (int t = 0; t < DMAX; ++t) b[t] = t < d ? s_b[w][t] : 0.0;
+      double best = __builtin_inf();
+      int bk = K;
+#pragma unroll 1
+      for (int k = lane; k < K; k += 64) {
+        double dot = 0.0;
+#pragma unroll
+        for (int t = 0; t < DMAX; ++t)
+          if (t < d) dot = dot + Cs[k * d + t] * b[t];
+        const double f = Ak[k] - 2.0 * dot;
+        if (f < best) {
+          best = f;
+          bk = k;
+        }
+      }
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const double ob = __shfl_xor(best, m);
+        const int ok = __shfl_xor(bk, m);
+        if (ob < best || (ob == best && ok < bk)) {
+          best = ob;
+          bk = ok;
+        }
+      }
+      if (bk < K && bk != cur) {
+        moved = 1;
+        if (lane < d) {
+          const double delta = Cs[bk * d + lane] - Cs[cur * d + lane];
+          s_delta[w][lane] = delta;
+          R[r * ldr + c0 + cg + lane] = R[r * ldr + c0 + cg + lane] - delta;
+          D[r * ldd + cg + lane] = delta;
+        }
+        if (lane == 0) codes[r * ldq + gq] = bk;
+      }
+    }
+    if (!moved && r < M && lane < d) D[r * ldd + cg + lane] = 0.0;
+    __syncthreads();
     if (moved) {
-      for (int64_t c = lane; c < cn; c += 64) {
+      for (int c = cg + d + lane; c < bw; c += 64) {
         double acc = 0.0;
-        for (int t = 0; t < d; ++t) acc = acc + s_delta[w][t] * Hc[t * cw + c];
-        S[r * lds + cs + c] = S[r * lds + cs + c] - acc;
+        for (int t = 0; t < d; ++t) acc = acc + s_delta[w][t] * Hb[(cg + t) * kRbCols + c];
+        sS[w * kRbCols + c] = sS[w * kRbCols + c] - acc;
       }
     }
     __syncthreads();
@@ -341,20 +359,49 @@ __global__ __launch_bounds__(kRfThreads) void refine_group_kernel(int64_t M, int
 
 // ---- launchers -----------------------------------------------------------------------------------
 hipError_t launch_gemm_f64(int64_t M, int64_t Nc, int64_t Kd, const void* A, int a_type, bool trans_a, int64_t lda,
-                           const void* B, int b_type, int64_t ldb, double* C, int64_t ldc, hipStream_t stream) {
+                           const void* B, int b_type, int64_t ldb, double* C, int64_t ldc, hipStream_t stream,
+                           bool sub) {
   if (M <= 0 || Nc <= 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(cdiv(Nc, kGBN)), static_cast<unsigned>(cdiv(M, kGBM)));
-#define CRVQ_GEMM(TA, TB, TR)                                                                              \
-  hipLaunchKernelGGL((gemm_f64_kernel<TA, TB, TR>), grid, dim3(256), 0, stream, M, Nc, Kd,                 \
-                     static_cast<const TA*>(A), lda, static_cast<const TB*>(B), ldb, C, ldc)
-  if (a_type == ET_F32 && b_type == ET_F32) {
-    if (trans_a) CRVQ_GEMM(float, float, true); else CRVQ_GEMM(float, float, false);
-  } else if (a_type == ET_F64 && b_type == ET_F64) {
-    if (trans_a) CRVQ_GEMM(double, double, true); else CRVQ_GEMM(double, double, false);
+#define CRVQ_GEMM(TA, TB, TR, SB)                                                                          \
+  hipLaunchKernelGGL((gemm_f64_kernel<TA, TB, TR, SB>), grid, dim3(256), 0, stream, M, Nc, Kd,             \
+                     static_cast<const TA*>(A), lda, static_cast<const TB*>(B), ldb, C, ldc, Kd, int64_t{0})
+  if (a_type == ET_F32 && b_type == ET_F32 && !sub) {
+    if (trans_a) CRVQ_GEMM(float, float, true, false); else CRVQ_GEMM(float, float, false, false);
+  } else if (a_type == ET_F64 && b_type == ET_F64 && !(trans_a && sub)) {
+    if (trans_a) CRVQ_GEMM(double, double, true, false);
+    else if (sub) CRVQ_GEMM(double, double, false, true);
+    else CRVQ_GEMM(double, double, false, false);
   } else {
     return hipErrorInvalidValue;
   }
 #undef CRVQ_GEMM
+  return hipGetLastError();
+}
+
+// C = A B (fp64, row-major, no transpose) split over k into P parts of at least 512 when the output
+// grid alone is too small to fill the device; part products go to ws (P x M x Nc doubles) and are
+// summed in part order, so the result does not depend on scheduling.
+int64_t gemm_split_parts(int64_t M, int64_t Nc, int64_t Kd) {
+  const int64_t tiles = cdiv(Nc, kGBN) * cdiv(M, kGBM);
+  int64_t P = tiles >= 256 ? 1 : cdiv(512, tiles);
+  const int64_t maxp = Kd / 512 > 1 ? Kd / 512 : 1;
+  return P < maxp ? P : maxp;
+}
+
+hipError_t launch_gemm_f64_split(int64_t M, int64_t Nc, int64_t Kd, const double* A, int64_t lda, const double* B,
+                                 int64_t ldb, double* C, int64_t ldc, double* ws, hipStream_t stream) {
+  if (M <= 0 || Nc <= 0) return hipSuccess;
+  const int64_t P = gemm_split_parts(M, Nc, Kd);
+  if (P <= 1) return launch_gemm_f64(M, Nc, Kd, A, ET_F64, false, lda, B, ET_F64, ldb, C, ldc, stream);
+  const int64_t kchunk = cdiv(cdiv(Kd, P), kGBK) * kGBK;
+  const int64_t parts = cdiv(Kd, kchunk);
+  const dim3 grid(static_cast<unsigned>(cdiv(Nc, kGBN)), static_cast<unsigned>(cdiv(M, kGBM)),
+                  static_cast<unsigned>(parts));
+  hipLaunchKernelGGL((gemm_f64_kernel<double, double, false, false>), grid, dim3(256), 0, stream, M, Nc, Kd, A, lda, B,
+                     ldb, ws, Nc, kchunk, M * Nc);
+  hipLaunchKernelGGL(sum_parts_kernel, dim3(static_cast<unsigned>(cdiv(M * Nc, 256))), dim3(256), 0, stream, M, Nc,
+                     static_cast<int>(parts), ws, C, ldc);
   return hipGetLastError();
 }
 
@@ -402,25 +449,46 @@ hipError_t launch_adam(int64_t n, float* C, const double* grad, double scale, do
 }
 
 size_t refine_lds_bytes(int64_t K, int d) {
-  return static_cast<size_t>(K * d + K + 256 + kRfChunk) * sizeof(double);
+  return static_cast<size_t>(K * d + K + kRbCols * kRbCols + kRfRows * kRbCols) * sizeof(double);
+}
+
+size_t refine_ws_bytes(int64_t M, int64_t n_cols, int64_t N) {
+  return align256(static_cast<size_t>(M) * static_cast<size_t>(n_cols) * sizeof(double)) +
+         align256(static_cast<size_t>(M) * kRbCols * sizeof(double)) +
+         align256(static_cast<size_t>(gemm_split_parts(M, n_cols, N)) * static_cast<size_t>(M) *
+                  static_cast<size_t>(n_cols) * sizeof(double));
 }
 
 hipError_t launch_refine_book(int64_t M, int64_t N, int d, int64_t n_cols, double* R, int64_t ldr, const double* H,
                               int64_t ldh, const void* Cb, int c_type, int64_t K, int32_t* codes, int64_t ldq,
-                              double* S, hipStream_t stream) {
+                              void* ws, hipStream_t stream) {
   if (M <= 0 || n_cols <= 0) return hipSuccess;
+  WsCursor cur(ws);
+  double* S = cur.take<double>(static_cast<size_t>(M) * static_cast<size_t>(n_cols));
+  double* D = cur.take<double>(static_cast<size_t>(M) * kRbCols);
+  double* parts = cur.take<double>(static_cast<size_t>(gemm_split_parts(M, n_cols, N)) * static_cast<size_t>(M) *
+                                   static_cast<size_t>(n_cols));
   // S = R H[:, 0:n_cols]
-  hipError_t e = launch_gemm_f64(M, n_cols, N, R, ET_F64, false, ldr, H, ET_F64, ldh, S, n_cols, stream);
+  hipError_t e = launch_gemm_f64_split(M, n_cols, N, R, ldr, H, ldh, S, n_cols, parts, stream);
   if (e != hipSuccess) return e;
   const size_t lds = refine_lds_bytes(K, d);
   const dim3 grid(static_cast<unsigned>(cdiv(M, kRfRows)));
-  for (int64_t g = 0; g < n_cols / d; ++g) {
+  const int64_t bw_max = (kRbCols / d) * d;
+  for (int64_t c0 = 0; c0 < n_cols; c0 += bw_max) {
+    const int bw = static_cast<int>(n_cols - c0 < bw_max ? n_cols - c0 : bw_max);
     if (d <= 8)
-      hipLaunchKernelGGL(refine_group_kernel<8>, grid, dim3(kRfThreads), lds, stream, M, d, g, n_cols, R, ldr, S, n_cols,
-                         H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq);
+      hipLaunchKernelGGL(refine_block_kernel<8>, grid, dim3(kRfThreads), lds, stream, M, d, c0, bw, R, ldr, S, n_cols,
+                         H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq, D, bw_max);
     else
-      hipLaunchKernelGGL(refine_group_kernel<16>, grid, dim3(kRfThreads), lds, stream, M, d, g, n_cols, R, ldr, S,
-                         n_cols, H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq);
+      hipLaunchKernelGGL(refine_block_kernel<16>, grid, dim3(kRfThreads), lds, stream, M, d, c0, bw, R, ldr, S, n_cols,
+                         H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq, D, bw_max);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    // the block's code changes reach the later columns: S[:, c0 + bw :] -= D H[c0 .. c0 + bw, c0 + bw :]
+    if (c0 + bw < n_cols) {
+      e = launch_gemm_f64(M, n_cols - c0 - bw, bw, D, ET_F64, false, bw_max, H + c0 * ldh + c0 + bw, ET_F64, ldh,
+                          S + c0 + bw, n_cols, stream, true);
+      if (e != hipSuccess) return e;
+    }
   }
   return hipGetLastError();
 }

@@ -7,9 +7,10 @@
 //  * gemm_f64_kernel: C = op(A) B in fp64 (H = X^T X from fp32 activations, G = R H), a 128 x 128
 //    tile per workgroup, 8 x 8 outputs per thread, operands staged through LDS as fp64.
 //  * row_dot_kernel: the per-row loss sum_j R_rj G_rj in a fixed order.
-//  * code_sum_partial / code_sum_final: per-code sums of fp64 vectors (the codebook gradient), one
-//    owner thread per code adding its members in vector order, then the block partials folded in
-//    block order -- deterministic, no atomics.
+//  * code_sum_wave_partial (K <= 256, d <= 8) or code_sum_partial, then code_sum_final: per-code sums
+//    of fp64 vectors (the codebook gradient) in a fixed order -- per-wave LDS tables filled by ballot
+//    peer groups, or one owner thread per code -- with the block partials folded in block order;
+//    deterministic, no atomics.
 //  * adam_kernel: one Adam step (moments in fp64, bias correction from the host) on an fp32 book.
 //  * refine_block_kernel: the width-1 code search over a block of column groups (64 columns) for
 //    every row, minimising QuantLoss with all other codes fixed; the running product S = R H is
@@ -187,6 +188,118 @@ __global__ __launch_bounds__(256) void code_sum_partial(const double* __restrict
     for (int t = 0; t < 16; ++t)
       if (t < d) part[(static_cast<int64_t>(k) * d + t) * nblocks + blockIdx.x] = acc[j][t];
     pcount[static_cast<int64_t>(k) * nblocks + blockIdx.x] = cnt[j];
+  }
+}
+
+// K <= 256, d <= 8: per-wave tables.  Every wave owns a private fp64 table of K x 8 sums in LDS and the
+// batches of 64 vectors wave, wave + W, ... (W waves in the grid).  Within a batch the lanes that share
+// a code find each other with eight ballots, and the lowest of them adds its peers' vectors (staged in
+// LDS) in ascending lane order to that code's entry, so every entry is a fixed-order sum over the
+// wave's batches; the block then folds its wave tables in wave order (layout [k * d + t][block]).
+constexpr int kCwWaves = 6;   // waves per block: 6 tables of 21 KiB fit one CU's LDS
+constexpr int kCwDepth = 2;   // batches in flight per wave
+
+struct CwTable {
+  double acc[256 * 8];
+  int cnt[256];
+  double stage[64][8];
+};
+
+__device__ __forceinline__ uint64_t code_peers(bool valid, int c) {
+  uint64_t peers = __ballot(valid);
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const bool bit = (c >> b) & 1;
+    const uint64_t m = __ballot(bit);
+    peers &= bit ? m : ~m;
+  }
+  return valid ? peers : 0ull;
+}
+
+__device__ __forceinline__ void cw_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// vector i of the set as 8 doubles (zero past d); a lane outside the set reads vector 0
+__device__ __forceinline__ void cw_load(const double* X, int64_t vpr, int64_t ld, int d, int64_t i, bool ok,
+                                        double (&v)[8]) {
+  const int64_t j = ok ? i : 0;
+  const int64_t r = j / vpr, g = j - r * vpr;
+  const double* p = X + r * ld + g * d;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) v[t] = t < d ? p[t] : 0.0;
+}
+
+__global__ __launch_bounds__(64 * kCwWaves) void code_sum_wave_partial(const double* __restrict__ X, int64_t vpr,
+                                                                       int64_t ld, int d, int64_t n,
+                                                                       const int32_t* __restrict__ codes, int K,
+                                                                       int64_t nblocks, double* __restrict__ part,
+                                                                       int* __restrict__ pcount) {
+  __shared__ CwTable tab[kCwWaves];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  CwTable& T = tab[w];
+  for (int e = lane; e < 256 * 8; e += 64) T.acc[e] = 0.0;
+  for (int e = lane; e < 256; e += 64) T.cnt[e] = 0;
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kCwWaves * 64;
+  const int64_t w0 = (static_cast<int64_t>(blockIdx.x) * kCwWaves + w) * 64;
+  double v[kCwDepth][8];
+  int cq[kCwDepth];
+#pragma unroll
+  for (int s = 0; s < kCwDepth; ++s) {
+    const int64_t i = w0 + stride * s + lane;
+    const bool ok = i < n;
+    cw_load(X, vpr, ld, d, i, ok, v[s]);
+    cq[s] = codes[ok ? i : 0];
+  }
+  for (int64_t base = w0; base < n; base += stride * kCwDepth) {
+#pragma unroll
+    for (int s = 0; s < kCwDepth; ++s) {
+      const int64_t bb = base + stride * s;
+      if (bb < n) {  // uniform across the wave
+        const int c = (bb + lane < n) ? cq[s] : -1;
+        const bool valid = c >= 0 && c < K;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) T.stage[lane][t] = v[s][t];
+        cw_sync();
+        const uint64_t peers = code_peers(valid, valid ? c : 0);
+        if (valid && (__ffsll(static_cast<long long>(peers)) - 1) == lane) {
+          double acc[8];
+#pragma unroll
+          for (int t = 0; t < 8; ++t) acc[t] = T.acc[c * 8 + t];
+          uint64_t m = peers;
+          while (m) {
+            const int sl = __ffsll(static_cast<long long>(m)) - 1;
+            m &= m - 1;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) acc[t] = acc[t] + T.stage[sl][t];
+          }
+#pragma unroll
+          for (int t = 0; t < 8; ++t) T.acc[c * 8 + t] = acc[t];
+          T.cnt[c] += __popcll(peers);
+        }
+        cw_sync();
+      }
+      const int64_t i = bb + stride * kCwDepth + lane;
+      const bool ok = i < n;
+      cw_load(X, vpr, ld, d, i, ok, v[s]);
+      cq[s] = codes[ok ? i : 0];
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < K * d; e += 64 * kCwWaves) {
+    const int k = e / d, t = e - k * d;
+    double acc = 0.0;
+#pragma unroll
+    for (int ww = 0; ww < kCwWaves; ++ww) acc = acc + tab[ww].acc[k * 8 + t];
+    part[static_cast<int64_t>(e) * nblocks + blockIdx.x] = acc;
+    if (t == 0) {
+      int cnt = 0;
+#pragma unroll
+      for (int ww = 0; ww < kCwWaves; ++ww) cnt += tab[ww].cnt[k];
+      pcount[static_cast<int64_t>(k) * nblocks + blockIdx.x] = cnt;
+    }
   }
 }
 
@@ -417,9 +530,16 @@ static int64_t code_sum_blocks(int64_t n) {
   return rounds < 1024 ? rounds : 1024;
 }
 
+// blocks of the per-wave scheme: at most one wave per batch of 64 vectors, 256 CUs' worth of waves
+static int64_t code_sum_wave_blocks(int64_t n) {
+  const int64_t batches = cdiv(n > 0 ? n : 1, 64);
+  const int64_t waves = batches < 256 * kCwWaves ? batches : 256 * kCwWaves;
+  return cdiv(waves, kCwWaves);
+}
+
 size_t code_sums_ws_bytes(int64_t n, int64_t K, int d) {
   WsCursor c(nullptr);
-  const int64_t nb = code_sum_blocks(n);
+  const int64_t nb = code_sum_blocks(n) > code_sum_wave_blocks(n) ? code_sum_blocks(n) : code_sum_wave_blocks(n);
   c.take<double>(static_cast<size_t>(nb * K * d));
   c.take<int>(static_cast<size_t>(nb * K));
   return c.used;
@@ -427,12 +547,25 @@ size_t code_sums_ws_bytes(int64_t n, int64_t K, int d) {
 
 hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int64_t n, const int32_t* codes,
                             int64_t K, double* sums, int32_t* counts, void* ws, hipStream_t stream) {
+  if (K <= 256 && d <= 8 && n > 0) {
+    WsCursor cw(ws);
+    const int64_t nbw = code_sum_wave_blocks(n);
+    const int64_t nbmax = code_sum_blocks(n) > nbw ? code_sum_blocks(n) : nbw;
+    double* part = cw.take<double>(static_cast<size_t>(nbmax * K * d));
+    int* pcount = cw.take<int>(static_cast<size_t>(nbmax * K));
+    hipLaunchKernelGGL(code_sum_wave_partial, dim3(static_cast<unsigned>(nbw)), dim3(64 * kCwWaves), 0, stream, X, vpr,
+                       ld, d, n, codes, static_cast<int>(K), nbw, part, pcount);
+    hipLaunchKernelGGL(code_sum_final, dim3(static_cast<unsigned>(cdiv(K * d, 4))), dim3(256), 0, stream, part, pcount,
+                       nbw, K, d, sums, counts);
+    return hipGetLastError();
+  }
   WsCursor cur(ws);
   int64_t nb = code_sum_blocks(n);
   const int64_t per_block = cdiv(cdiv(n > 0 ? n : 1, nb), kCsVec) * kCsVec;
   nb = cdiv(n > 0 ? n : 1, per_block);
-  double* part = cur.take<double>(static_cast<size_t>(code_sum_blocks(n) * K * d));
-  int* pcount = cur.take<int>(static_cast<size_t>(code_sum_blocks(n) * K));
+  const int64_t nbmax = code_sum_blocks(n) > code_sum_wave_blocks(n) ? code_sum_blocks(n) : code_sum_wave_blocks(n);
+  double* part = cur.take<double>(static_cast<size_t>(nbmax * K * d));
+  int* pcount = cur.take<int>(static_cast<size_t>(nbmax * K));
   hipLaunchKernelGGL(code_sum_partial, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, X, vpr, ld, d, n, codes,
                      static_cast<int>(K), per_block, nb, part, pcount);
   hipLaunchKernelGGL(code_sum_final, dim3(static_cast<unsigned>(cdiv(K * d, 4))), dim3(256), 0, stream, part, pcount,

@@ -251,3 +251,29 @@ def test_bits_per_weight_against_eq6_eq8():
         C.crvq_bits_per_weight(64, 64, 8, 0, [0])
     with pytest.raises(C.CrvqError):
         C.crvq_bits_per_weight(64, 64, 8, 0, [256], codeword_bits=0)
+
+
+def test_refinement_validation(L):
+    """The refinement calls reject bad arguments on the host (nothing is enqueued)."""
+    ws = ctypes.c_void_p(0x100000)
+    assert L.crvq_gram(FAKE, 1, 16, 8, 8, FAKE, 8, None) == 1            # bf16 activations not accepted
+    assert L.crvq_gram(FAKE, 0, 16, 8, 4, FAKE, 8, None) == 1            # ld < n_cols
+    assert L.crvq_gram(None, 0, 16, 0, 0, None, 0, None) == 0            # nothing to do
+    assert L.crvq_hessian_product(4, 8, 4, FAKE, 8, FAKE, 8, FAKE, 4, FAKE, None) == 1  # row_loss needs n_out == N
+    assert L.crvq_hessian_product(4, 8, 9, FAKE, 8, FAKE, 8, FAKE, 9, None, None) == 1
+    assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 2000, FAKE, None, ws, 1 << 30, None) == 2  # K > 1024
+    assert L.crvq_code_sums(FAKE, 4, 2, 8, 8, FAKE, 16, FAKE, None, ws, 1 << 30, None) == 1     # ld < vpr * d
+    assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 16, FAKE, None, ws, 0, None) == 3          # no workspace
+    assert L.crvq_code_sums_workspace_size(100, 8, 2000) == 0
+    dbl = ctypes.c_double
+    assert L.crvq_adam_step(FAKE, FAKE, dbl(-2.0), FAKE, FAKE, 8, 0, dbl(1e-3), dbl(0.9), dbl(0.95), dbl(1e-8),
+                            None) == 1                                    # step 0
+    assert L.crvq_adam_step(FAKE, FAKE, dbl(-2.0), FAKE, FAKE, 8, 1, dbl(1e-3), dbl(1.0), dbl(0.95), dbl(1e-8),
+                            None) == 1                                    # beta1 = 1
+    need = L.crvq_refine_workspace_size(64, 256, 256)
+    assert need > 64 * 256 * 8 and L.crvq_refine_workspace_size(64, 128, 256) == 0
+    assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 2048, FAKE, 32, ws, need, None) == 2
+    assert L.crvq_refine_codes(64, 256, 8, 250, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 32, ws, need, None) == 1
+    assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 31, ws, need, None) == 1
+    assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 32, ws, need - 1, None) == 3
+    assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 2, 256, FAKE, 32, ws, need, None) == 1

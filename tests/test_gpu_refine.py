@@ -231,3 +231,50 @@ def test_refine_loop_lockstep():
     assert orf.quant_loss(W, Wh, X) == pytest.approx(losses[-1], rel=1e-5)
     say(f"refine loop: QuantLoss {losses[0]:.6e} -> {losses[-1]:.6e} over {len(losses) - 1} rounds, "
         f"{len(trace)} calls matched")
+
+
+def test_refine_two_basic_books_d16():
+    """The refinement loop on the m = 2, d = 16 layout (two basic books on every vector) against the
+    oracle's loop from the same start."""
+    M, N, d = 64, 256, 16
+    wl = inputs.small_workload(M=M, N=N, tokens=96, d=d, K_base=32, K_ext=(16,), crit_frac=0.1, beam=2, iters=2,
+                               dtype="f32", wid=141, m_base=2)
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    n = M * N // d
+    n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, m_base=2)
+    q = LayerQuantizer(M, N, torch.float32, cfg, tokens=96, device="cuda")
+    Xt = torch.from_numpy(X).cuda()
+    st = q.run(dev(W), Xt, torch.from_numpy(inputs.base_init_indices(wl, 0, n)).cuda(),
+               [torch.from_numpy(inputs.ext_init_indices(wl, 0, 1, M * n_crit // d)).cuda()],
+               base_idx_extra=[torch.from_numpy(inputs.extra_base_init_indices(wl, 0, 1, n)).cuda()])
+    torch.cuda.synchronize()
+    books = [host(b).copy() for b in q.C_basic + q.C_ext]
+    codes = [host(c).copy() for c in q.codes_basic + q.codes_ext]
+    perm = host(st.perm)
+    losses = q.refine(Xt, rounds=2, steps=2, lr=1e-4)
+    torch.cuda.synchronize()
+    ref = orf.refine_layer(host(st.Ws), oracle.gather_columns(X, perm), d, n_crit, books, codes, 2, lr=1e-4, steps=2,
+                           max_rounds=2)
+    np.testing.assert_allclose(losses, ref.losses, rtol=1e-9)
+    for a, b in zip(q.codes_basic + q.codes_ext, ref.codes):
+        np.testing.assert_array_equal(host(a), b)
+    assert losses[-1] < losses[0]
+    say(f"refine m=2 d=16: QuantLoss {losses[0]:.6e} -> {losses[-1]:.6e}, codes identical to the oracle")
+
+
+def test_refine_rejects_bf16_layers():
+    M, N, d = 32, 64, 8
+    wl = inputs.small_workload(M=M, N=N, tokens=32, d=d, K_base=16, K_ext=(8,), crit_frac=0.25, beam=1, iters=1,
+                               dtype="bf16", wid=142)
+    W = inputs.make_weight(wl, 0)
+    X = inputs.make_calib(wl, 0)
+    n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
+    cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
+    q = LayerQuantizer(M, N, torch.bfloat16, cfg, tokens=32, device="cuda")
+    Xt = torch.from_numpy(X).cuda()
+    q.run(dev(W, "bf16"), Xt, torch.from_numpy(inputs.base_init_indices(wl, 0, M * N // d)).cuda(),
+          [torch.from_numpy(inputs.ext_init_indices(wl, 0, 1, M * n_crit // d)).cuda()])
+    with pytest.raises(ValueError):
+        q.refine(Xt, rounds=1, steps=1, lr=1e-4)

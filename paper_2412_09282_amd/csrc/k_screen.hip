@@ -1155,6 +1155,108 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
   if (valid && !certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
 }
 
+// Top-1 against a small codebook (at most 16 tiles of 16, one split): the split-bf16 screen of
+// screen_kernel, but every lane keeps its smallest screen value with the codeword index and its
+// second smallest value, so no tile needs re-scoring: after the four lane groups of a row are merged,
+// the row's winner alone is scored exactly in fp64 and certified against the second smallest screen
+// value with the same bound as finalize_kernel (R = ||x|| + sqrt(D)).  The row's result is written
+// directly (codes / dist, or rowD / rowK for a beam step); an uncertain row keeps it as its tentative
+// result and is appended to the rescue list.
+template <int CB>
+__global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const void* __restrict__ apack,
+                                                            const float* __restrict__ cnp, int64_t tiles,
+                                                            const void* __restrict__ C, int ct, int64_t K,
+                                                            ScreenBound bound, int* __restrict__ rcount,
+                                                            int* __restrict__ rlist, int32_t* __restrict__ codes,
+                                                            float* __restrict__ dist, double* __restrict__ rowD,
+                                                            int* __restrict__ rowK) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int jl = lane & 15;
+  const int g = lane >> 4;
+  const int64_t n = src.n;
+  const int d = src.d;
+  const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (16 * CB);
+  if (row0 >= n) return;  // no barriers below
+  SplitOps::B bop[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int64_t i = row0 + cb * 16 + jl;
+    bop[cb] = SplitOps::make_b(src, i, i < n, g);
+  }
+  float m1[CB], m2[CB];
+  int i1[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    m1[cb] = __builtin_inff();
+    m2[cb] = __builtin_inff();
+    i1[cb] = 0x7fffffff;
+  }
+  for (int64_t T = 0; T < tiles; ++T) {
+    const SplitOps::A a = SplitOps::load_a(apack, T, lane);
+    const f4 c4 = *reinterpret_cast<const f4*>(cnp + T * 16 + 4 * g);
+    const int kb = static_cast<int>(T) * 16 + 4 * g;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      const f4 acc = SplitOps::mfma(a, bop[cb], c4);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float v = acc[r];
+        m2[cb] = __builtin_amdgcn_fmed3f(m1[cb], m2[cb], v);  // m1 <= m2 holds throughout
+        const bool lt = v < m1[cb];
+        m1[cb] = lt ? v : m1[cb];
+        i1[cb] = lt ? kb + r : i1[cb];
+      }
+    }
+  }
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    // merge the four lane groups of the row (lanes jl, jl + 16, jl + 32, jl + 48)
+#pragma unroll
+    for (int sh = 16; sh <= 32; sh <<= 1) {
+      const float om1 = __shfl_xor(m1[cb], sh), om2 = __shfl_xor(m2[cb], sh);
+      const int oi1 = __shfl_xor(i1[cb], sh);
+      const float nm2 = fminf(fminf(m2[cb], om2), fmaxf(m1[cb], om1));
+      const bool take = om1 < m1[cb] || (om1 == m1[cb] && oi1 < i1[cb]);
+      m1[cb] = take ? om1 : m1[cb];
+      i1[cb] = take ? oi1 : i1[cb];
+      m2[cb] = nm2;
+    }
+    const int64_t i = row0 + cb * 16 + jl;
+    if (g != 0 || i >= n) continue;
+    double xd[8];
+    load_row_exact<8>(src, i, true, xd);
+    const int k1 = (i1[cb] >= 0 && i1[cb] < K) ? i1[cb] : 0;
+    float cw[8];
+    load_codeword<8>(C, ct, k1, d, true, cw);
+    double D1 = 0.0, xn2 = 0.0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      if (t < d) {
+        const double diff = xd[t] - static_cast<double>(cw[t]);
+        D1 = D1 + diff * diff;
+        xn2 = xn2 + xd[t] * xd[t];
+      }
+    }
+    bool certain = i1[cb] == k1;
+    if (certain && m2[cb] != __builtin_inff()) {
+      const double xn = sqrt(xn2);
+      const double R = xn + sqrt(D1);
+      const double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
+                           bound.abs_coef * (xn + R + 1.0) + 1e-35;
+      certain = D1 < static_cast<double>(m2[cb]) + xn2 - delta;
+    }
+    if (codes) {
+      codes[i] = k1;
+      if (dist) dist[i] = static_cast<float>(D1);
+    } else {
+      rowD[i] = D1;
+      rowK[i] = k1;
+    }
+    if (!certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
+  }
+}
+
 // Top-1 rescue.  Blocks take kRB listed rows at a time (rows b * kRB .., b = block, block + grid,
 // ...) and stream the codebook once for all of them.  For each codeword and row a fp32 direct-form
 // distance d_f = sum_t (x_t - c_t)^2 (fma, t ascending) is a filter: its error is at most ~10u of
@@ -1744,6 +1846,22 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (p.split && top == 1 && p.splits == 1 && p.tiles <= 16) {
+    // small codebook, top-1: screen, exact winner and certificate in one kernel, then the rescue
+    const ScreenBound bound = screen_bound(p, src.type, ct, src.d, nullptr);
+    const dim3 grid(static_cast<unsigned>(p.grid_x));
+    if (p.cb == CRVQ_CB_WIDE)
+      hipLaunchKernelGGL((screen_small1_kernel<CRVQ_CB_WIDE>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
+                         C, ct, K, bound, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
+    else
+      hipLaunchKernelGGL((screen_small1_kernel<2>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles, C, ct, K,
+                         bound, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
+    hipLaunchKernelGGL((rescue1_kernel<2>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C, ct, K,
+                       w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
+    return hipGetLastError();
+  }
   if (p.split) {
     e = launch_screen_ops<SplitOps>(src, C, ct, K, p, w, stream);
   } else {

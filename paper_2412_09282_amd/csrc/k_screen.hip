@@ -1222,13 +1222,28 @@ __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const vo
       i1[cb] = take ? oi1 : i1[cb];
       m2[cb] = nm2;
     }
-    const int64_t i = row0 + cb * 16 + jl;
-    if (g != 0 || i >= n) continue;
+  }
+  // Every lane group now holds the merged state of all CB column blocks; lane group g finishes the
+  // rows of blocks g, g + 4, ... so all 64 lanes share the exact epilogue.
+#pragma unroll
+  for (int rr = 0; rr < (CB + 3) / 4; ++rr) {
+    float s2 = __builtin_inff();
+    int k1 = 0x7fffffff;
+#pragma unroll
+    for (int cb = 4 * rr; cb < 4 * rr + 4 && cb < CB; ++cb) {
+      if (cb - 4 * rr == g) {
+        s2 = m2[cb];
+        k1 = i1[cb];
+      }
+    }
+    const int cbm = 4 * rr + g;
+    const int64_t i = row0 + cbm * 16 + jl;
+    if (cbm >= CB || i >= n) continue;
     double xd[8];
     load_row_exact<8>(src, i, true, xd);
-    const int k1 = (i1[cb] >= 0 && i1[cb] < K) ? i1[cb] : 0;
+    const int kk = (k1 >= 0 && k1 < K) ? k1 : 0;
     float cw[8];
-    load_codeword<8>(C, ct, k1, d, true, cw);
+    load_codeword<8>(C, ct, kk, d, true, cw);
     double D1 = 0.0, xn2 = 0.0;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
@@ -1238,20 +1253,20 @@ __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const vo
         xn2 = xn2 + xd[t] * xd[t];
       }
     }
-    bool certain = i1[cb] == k1;
-    if (certain && m2[cb] != __builtin_inff()) {
+    bool certain = k1 == kk;
+    if (certain && s2 != __builtin_inff()) {
       const double xn = sqrt(xn2);
       const double R = xn + sqrt(D1);
       const double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
                            bound.abs_coef * (xn + R + 1.0) + 1e-35;
-      certain = D1 < static_cast<double>(m2[cb]) + xn2 - delta;
+      certain = D1 < static_cast<double>(s2) + xn2 - delta;
     }
     if (codes) {
-      codes[i] = k1;
+      codes[i] = kk;
       if (dist) dist[i] = static_cast<float>(D1);
     } else {
       rowD[i] = D1;
-      rowK[i] = k1;
+      rowK[i] = kk;
     }
     if (!certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
   }

@@ -98,8 +98,11 @@ struct ScreenWs {
   int* pK;       // top-1: its codeword, [split][row]
   double* xn2;   // top-1: ||x||^2 per row (fp64)
   float* smax;   // 32 x 32 screen: partial maxima of |c|, then the scale alpha
-  int* rcount;   // number of rows that failed the certification
+  int* rcount;   // number of rows that failed the certification ([1]: that failed the second screen)
   int* rlist;    // those rows (any order), [n_rows]
+  int* rlist2;   // 32 x 32 screen on inexact operands: rows that failed the second screen too, [n_rows
+                 // rounded up to 256]; first the per-block slices of the first screen's failures
+  int* bcount;   // their per-block counts, then the blocks' offsets, [2 x blocks of 256 rows]
 };
 // Carves the screen's scratch out of `ws`; returns it (pointers null on a dry run).
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc);

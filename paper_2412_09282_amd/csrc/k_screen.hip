@@ -161,6 +161,19 @@ __device__ __forceinline__ void load_codeword(const void* C, int ct, int64_t k, 
     load_bf16_elems<DM>(static_cast<const uint16_t*>(C) + (ok ? k * d : 0), d, ok, c);
 }
 
+// Appends row i to the list when `fail`, one atomic per wave: the failing lanes of the wave take
+// consecutive slots after the wave's leader reserves them.  Every active lane of the wave must call it.
+__device__ __forceinline__ void list_append(bool fail, int64_t i, int* rcount, int* rlist) {
+  const uint64_t m = __ballot(fail);
+  if (m == 0) return;
+  const int lane = threadIdx.x & 63;
+  const int leader = __ffsll(static_cast<long long>(m)) - 1;
+  int base = 0;
+  if (lane == leader) base = atomicAdd(rcount, __popcll(m));
+  base = __shfl(base, leader);
+  if (fail) rlist[base + __popcll(m & ((1ull << lane) - 1ull))] = static_cast<int>(i);
+}
+
 __device__ __forceinline__ bool cless(double Da, int ka, double Db, int kb) {
   return Da < Db || (Da == Db && ka < kb);
 }
@@ -731,7 +744,8 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
   const float alpha = s32_alpha(sh[0]);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     alpha_out[0] = alpha;
-    *rcount = 0;
+    rcount[0] = 0;  // rows left uncertain by the first screen
+    rcount[1] = 0;  // rows left uncertain by the second (split) screen of those
   }
   const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (k >= tiles * kS32Tile) return;
@@ -770,18 +784,22 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
 // significand bits and the power-of-two scale only moves the exponent; values that land below the
 // fp16 normal range are covered by the underflow terms of the bound), so c2 = x2 = 0 and the
 // second MFMA alone, (c1|N).(x1|2^12), forms alpha^2 s: one v_mfma_f32_32x32x16_f16 per tile.
-template <int CB, int NC, bool ONE>
+// LIST: the rows are list[0 .. *list_n), and results go to their list positions (the second screen
+// of the rows the first one left uncertain).
+template <int CB, int NC, bool ONE, bool LIST>
 __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_t* apack,
                                                        const float* __restrict__ alpha_p, int64_t tiles, int64_t tps,
                                                        const void* __restrict__ C, int ct, int64_t K,
                                                        float* __restrict__ pR, double* __restrict__ pD,
-                                                       int* __restrict__ pK, double* __restrict__ xn2o) {
+                                                       int* __restrict__ pK, double* __restrict__ xn2o,
+                                                       const int* __restrict__ list, const int* __restrict__ list_n) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int j = lane & 31;
   const int h = lane >> 5;
   const int split = blockIdx.y;
-  const int64_t n = src.n;
+  const int64_t ns = src.n;                      // stride of the per-split outputs
+  const int64_t n = LIST ? *list_n : src.n;      // rows to screen
   const int d = src.d;
   const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
   if (row0 >= n) return;  // no barriers below
@@ -794,7 +812,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     const int64_t i = row0 + cb * 32 + j;
     const bool ok = i < n;
     float v[8];
-    const int64_t off = ok ? row_offset(src, i) : 0;
+    const int64_t off = ok ? row_offset(src, LIST ? list[i] : i) : 0;
     if (src.type == ET_F32) {
       load_f32_elems<8>(static_cast<const float*>(src.base) + off, d, ok, v);
     } else if (src.type == ET_BF16) {
@@ -912,6 +930,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   for (int cb = 0; cb < CB; ++cb) {
     const int64_t i = row0 + cb * 32 + j;
     const bool valid = i < n;
+    const int64_t pi = (LIST && valid) ? list[i] : i;  // the row's index in the source
     const float mg = m[cb];
     const float om = __shfl_xor(mg, 32);
     const int hw = (om < mg || (om == mg && h == 1)) ? 1 - h : h;
@@ -920,7 +939,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     if (forced[cb]) rr = -__builtin_inff();
     const int Tw = __shfl(id[cb], j + 32 * hw);
     double xd[8];
-    load_row_exact<8>(src, i, valid, xd);
+    load_row_exact<8>(src, pi, valid, xd);
     double D = __builtin_inf();
     int kk = INT_MAX;
 #pragma unroll
@@ -968,9 +987,9 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
 #pragma unroll
       for (int t = 0; t < 8; ++t)
         if (t < d) xn2 = xn2 + xd[t] * xd[t];
-      pD[static_cast<int64_t>(split) * n + i] = D;
-      pK[static_cast<int64_t>(split) * n + i] = kk;
-      pR[static_cast<int64_t>(split) * n + i] = rr;
+      pD[static_cast<int64_t>(split) * ns + i] = D;
+      pK[static_cast<int64_t>(split) * ns + i] = kk;
+      pR[static_cast<int64_t>(split) * ns + i] = rr;
       if (split == 0) xn2o[i] = xn2;
     }
   }
@@ -1152,7 +1171,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
   // An uncertain row is written with its tentative result (the rescue starts from that exact
   // distance) and goes to the rescue list; its order there does not affect any result.
   if (valid) emit_row<NB>(i, LD, LK, top, need, codes, dist, rowD, rowK);
-  if (valid && !certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
+  list_append(valid && !certain, i, rcount, rlist);
 }
 
 // Top-1 against a small codebook (at most 16 tiles of 16, one split): the split-bf16 screen of
@@ -1270,6 +1289,131 @@ __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const vo
     }
     if (!certain) rlist[atomicAdd(rcount, 1)] = static_cast<int>(i);
   }
+}
+
+// Top-1 result of row `row` from its screen results at position i (splits merged in (D, k) order)
+// and its certificate, written to the row's outputs; returns whether it is certain.
+__device__ __forceinline__ bool finish_top1(int64_t i, int64_t row, int splits, int64_t ns,
+                                            const float* __restrict__ pR, const double* __restrict__ pD,
+                                            const int* __restrict__ pK, const double* __restrict__ xn2a,
+                                            const ScreenBound& bound, int32_t* __restrict__ codes,
+                                            float* __restrict__ dist, double* __restrict__ rowD,
+                                            int* __restrict__ rowK) {
+  double Dl = __builtin_inf();
+  int kl = INT_MAX;
+  float rest = __builtin_inff();
+  for (int s = 0; s < splits; ++s) {
+    const double D = pD[static_cast<int64_t>(s) * ns + i];
+    const int k = pK[static_cast<int64_t>(s) * ns + i];
+    if (cless(D, k, Dl, kl)) {
+      Dl = D;
+      kl = k;
+    }
+    rest = fminf(rest, pR[static_cast<int64_t>(s) * ns + i]);
+  }
+  bool certain;
+  if (rest == __builtin_inff()) {
+    certain = true;  // every codeword was scored exactly
+  } else {
+    const double xn2 = xn2a[i];
+    const double xn = sqrt(xn2);
+    const double R = xn + sqrt(Dl);
+    double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
+                   bound.abs_coef * (xn + R + 1.0) + 1e-35;
+    double restd = static_cast<double>(rest);
+    if (bound.alpha) {
+      const double inv = 1.0 / static_cast<double>(bound.alpha[0]);
+      restd = restd * inv * inv;
+      delta += 0x1p-24 * 2.8285 * (R + 2.0 * xn) * inv + 0x1p-12 * inv * inv;
+    }
+    certain = Dl < restd + xn2 - delta;
+  }
+  if (codes) {
+    codes[row] = kl;
+    if (dist) dist[row] = static_cast<float>(Dl);
+  } else {
+    rowD[row] = Dl;
+    rowK[row] = kl;
+  }
+  return certain;
+}
+
+// Top-1 finalize of the first of two screens, over every row.  A large share of rows can fail its
+// wider certificate, so instead of one global counter (whose atomics serialize) each block packs its
+// failing rows, in row order, into its own slice tmp[256 b ..] and writes their number to bcount[b];
+// scan_counts_kernel and compact_list_kernel then build the dense list in block order.
+__global__ __launch_bounds__(256) void finalize1_first_kernel(int64_t n, int splits, const float* __restrict__ pR,
+                                                              const double* __restrict__ pD, const int* __restrict__ pK,
+                                                              const double* __restrict__ xn2a, ScreenBound bound,
+                                                              int* __restrict__ tmp, int* __restrict__ bcount,
+                                                              int32_t* __restrict__ codes, float* __restrict__ dist,
+                                                              double* __restrict__ rowD, int* __restrict__ rowK) {
+  __shared__ int s_wc[4];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const bool valid = i < n;
+  bool fail = false;
+  if (valid) fail = !finish_top1(i, i, splits, n, pR, pD, pK, xn2a, bound, codes, dist, rowD, rowK);
+  const uint64_t m = __ballot(fail);
+  if (lane == 0) s_wc[w] = __popcll(m);
+  __syncthreads();
+  int woff = 0;
+  for (int u = 0; u < w; ++u) woff += s_wc[u];
+  if (fail) tmp[static_cast<int64_t>(blockIdx.x) * 256 + woff + __popcll(m & ((1ull << lane) - 1ull))] = static_cast<int>(i);
+  if (threadIdx.x == 0) bcount[blockIdx.x] = s_wc[0] + s_wc[1] + s_wc[2] + s_wc[3];
+}
+
+// Exclusive prefix sums of the nb block counts (one block of 1024 threads; each thread sums a
+// contiguous run, the runs are scanned in LDS), and their total to *total.
+__global__ __launch_bounds__(1024) void scan_counts_kernel(const int* __restrict__ cnt, int64_t nb,
+                                                           int* __restrict__ offs, int* __restrict__ total) {
+  __shared__ int sh[1024];
+  const int t = threadIdx.x;
+  const int64_t per = (nb + 1023) / 1024;
+  const int64_t b0 = t * per, b1 = b0 + per < nb ? b0 + per : nb;
+  int sum = 0;
+  for (int64_t b = b0; b < b1; ++b) sum += cnt[b];
+  sh[t] = sum;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {  // inclusive Hillis-Steele scan
+    const int v = t >= off ? sh[t - off] : 0;
+    __syncthreads();
+    sh[t] += v;
+    __syncthreads();
+  }
+  int run = t > 0 ? sh[t - 1] : 0;
+  for (int64_t b = b0; b < b1; ++b) {
+    offs[b] = run;
+    run += cnt[b];
+  }
+  if (t == 1023) *total = sh[1023];
+}
+
+// rlist[offs[b] + j] = tmp[256 b + j] for j < cnt[b]: the per-block slices packed in block order.
+__global__ __launch_bounds__(256) void compact_list_kernel(const int* __restrict__ tmp, const int* __restrict__ cnt,
+                                                           const int* __restrict__ offs, int* __restrict__ rlist) {
+  const int b = blockIdx.x;
+  if (static_cast<int>(threadIdx.x) < cnt[b])
+    rlist[offs[b] + threadIdx.x] = tmp[static_cast<int64_t>(b) * 256 + threadIdx.x];
+}
+
+// Top-1 finalize of a second screen over a row list (rows list[0 .. *list_n), their screen results at
+// the list positions): the same merge of the splits and certificate, writing each row's result to its
+// own index; rows still uncertain (few) go to the next list.
+__global__ __launch_bounds__(256) void finalize1_list_kernel(int splits, int64_t ns, const int* __restrict__ list,
+                                                             const int* __restrict__ list_n, const float* __restrict__ pR,
+                                                             const double* __restrict__ pD, const int* __restrict__ pK,
+                                                             const double* __restrict__ xn2a, ScreenBound bound,
+                                                             int* __restrict__ rcount, int* __restrict__ rlist,
+                                                             int32_t* __restrict__ codes, float* __restrict__ dist,
+                                                             double* __restrict__ rowD, int* __restrict__ rowK) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (static_cast<int64_t>(blockIdx.x) * 256 >= *list_n) return;  // whole block past the list
+  const bool valid = i < *list_n;
+  const int64_t row = valid ? list[i] : 0;
+  bool fail = false;
+  if (valid) fail = !finish_top1(i, row, splits, ns, pR, pD, pK, xn2a, bound, codes, dist, rowD, rowK);
+  list_append(fail, row, rcount, rlist);
 }
 
 // Top-1 rescue.  Blocks take kRB listed rows at a time (rows b * kRB .., b = block, block + grid,
@@ -1721,7 +1865,7 @@ bool s32_exact_operands(int x_type, int ct) { return x_type == ET_BF16 && ct == 
 // Split bf16: a wider accumulation allowance (the 32-term bf16 MFMA sum, measured well below it),
 // the split remainder 2^-15 ||x|| R for each operand that is not bf16 already, and an absolute
 // term for subnormal operands or partial sums that the matrix core may flush.
-ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d, const float* alpha) {
+ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d, const float* alpha, bool one_mfma = false) {
   ScreenBound b;
   b.acc_ulps = static_cast<double>(4 * d + 24);
   b.split_coef = 0.0;
@@ -1730,7 +1874,9 @@ ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d, const f
   if (p.s32) {
     // remainders of both splits and the dropped c2.x2, each <= 2^-22 sum |c_t| |2 x_t|; none when
     // both operands are bf16 (exact in fp16 under the scale)
-    b.split_coef = s32_exact_operands(x_type, ct) ? 0.0 : 0x1p-19;
+    // one MFMA per tile on fp16-rounded operands instead: the dropped c1.x2 + c2.x1 + c2.x2 with
+    // |x2| <= 2^-11 |x1|, |c2| <= 2^-11 |c1| is at most 2^-10 (1 + 2^-10) sum |c_t| |2 x_t| <= 2^-9 (1 + 2^-10) ||x|| R
+    if (!s32_exact_operands(x_type, ct)) b.split_coef = one_mfma ? 0x1p-9 * (1.0 + 0x1p-9) : 0x1p-19;
     b.alpha = alpha;
   } else if (p.split) {
     if (b.acc_ulps < 96.0) b.acc_ulps = 96.0;
@@ -1804,8 +1950,10 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
     w.smax = nullptr;
   }
   w.pR = ws.take<float>(static_cast<size_t>(p.splits) * n_rows);
-  w.rcount = ws.take<int>(1);
+  w.rcount = ws.take<int>(2);
   w.rlist = ws.take<int>(static_cast<size_t>(n_rows));
+  w.rlist2 = p.s32 ? ws.take<int>(static_cast<size_t>(cdiv(n_rows, 256) * 256)) : nullptr;
+  w.bcount = p.s32 ? ws.take<int>(static_cast<size_t>(2 * cdiv(n_rows, 256))) : nullptr;
   if (p.nb == 1) {
     w.pT = nullptr;
     w.pM = nullptr;
@@ -1839,15 +1987,36 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                        stream, C, ct, K, src.d, p.tiles, w.smax, nparts, ap, alpha, w.rcount);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
-    if (s32_exact_operands(src.type, ct))
-      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true>), grid, dim3(256), 0, stream, src, ap,
-                         alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
-    else
-      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false>), grid, dim3(256), 0, stream, src, ap,
-                         alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2);
+    const bool exact = s32_exact_operands(src.type, ct);
+    // First screen: one MFMA per tile.  Exact for bf16 rows against a bf16 book; otherwise on
+    // fp16-rounded operands, certified with the wider bound.
+    hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true, false>), grid, dim3(256), 0, stream, src,
+                       ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr, nullptr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const ScreenBound bound = screen_bound(p, src.type, ct, src.d, alpha);
-    return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
+    if (exact) {
+      const ScreenBound bound = screen_bound(p, src.type, ct, src.d, alpha);
+      return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
+    }
+    const ScreenBound b1 = screen_bound(p, src.type, ct, src.d, alpha, true);
+    const int64_t nb = cdiv(src.n, 256);
+    // the uncertain rows, compacted through rlist2 (free until the second finalize) in row order
+    hipLaunchKernelGGL(finalize1_first_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, src.n, p.splits,
+                       w.pR, w.pD, w.pK, w.xn2, b1, w.rlist2, w.bcount, out_codes, out_dist, rowD, rowK);
+    hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, stream, w.bcount, nb, w.bcount + nb, w.rcount);
+    hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, w.rlist2, w.bcount,
+                       w.bcount + nb, w.rlist);
+    // Second screen, split form (two MFMAs per tile, the tight bound), over the rows the first one
+    // left uncertain; what still fails goes to the exact rescue.
+    hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true>), grid, dim3(256), 0, stream, src,
+                       ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
+    const ScreenBound b2 = screen_bound(p, src.type, ct, src.d, alpha);
+    hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
+                       p.splits, src.n, w.rlist, w.rcount, w.pR, w.pD, w.pK, w.xn2, b2, w.rcount + 1, w.rlist2,
+                       out_codes, out_dist, rowD, rowK);
+    const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
+    hipLaunchKernelGGL((rescue1_kernel<2>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C, ct, K,
+                       w.rcount + 1, w.rlist2, out_codes, out_dist, rowD, rowK);
+    return hipGetLastError();
   }
   const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
   if (p.split) {

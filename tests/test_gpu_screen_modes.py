@@ -1,8 +1,9 @@
 """GPU parity of the nearest-codeword search on the shapes that select each screen variant.
 
 Long top-1 searches (at least 256 16-codeword tiles per codebook split, e.g. 65536 rows x 65536
-codewords) run on 32 x 32 tiles with split-fp16 operands under a power-of-two codebook scale; shorter
-ones on 16 x 16 tiles with split-bf16 operands.  Whatever the variant, the certified screen plus the
+codewords) run on 32 x 32 tiles under a power-of-two codebook scale: one fp16 MFMA per tile, exact for
+bf16 operands, and for fp32 operands a second, split-fp16 screen of the rows the first leaves
+uncertain; shorter ones on 16 x 16 tiles with split-bf16 operands.  Whatever the variant, the certified screen plus the
 exact rescue must return the oracle's codes (the fp64 definition of Eq. 3, ties to the lower index)
 and its distances, including rows the scaled screen cannot represent (forced to the exact rescue),
 codebooks of extreme magnitude and ragged tails."""
@@ -126,3 +127,34 @@ def test_beam_width_one_long_codebook():
         bad = np.flatnonzero(got != exp_codes[t])
         assert len(bad) == 0, f"book {t}: {len(bad)} codes differ, e.g. rows {bad[:5]}"
     np.testing.assert_array_equal(err.cpu().numpy(), np.asarray(exp_err, dtype=np.float64).astype(np.float32))
+
+
+# Long searches on fp32 operands (here 262144 rows x 65536 codewords, four codebook splits) get two
+# screens: one MFMA per tile on fp16-rounded operands with the wider certificate, then the split form
+# on the rows it left uncertain, then the exact rescue of what is left.
+@pytest.mark.parametrize("case", ["plain", "ties", "mixed_bf16_book"])
+def test_two_pass_screen(case):
+    n, K, d = 262144 + 37, 65536, 8
+    say(f"two-pass screen fp32 n={n} K={K} ({case})")
+    g = np.random.default_rng(44)
+    if case == "ties":
+        base = rv(16384, 8, 45)
+        Cb = np.ascontiguousarray(np.concatenate([base, base, base[::-1], base])[g.permutation(K)])
+        V = np.concatenate([base[g.integers(0, 16384, n // 2)], rv(n - n // 2, 8, 46)])
+        check(V, Cb)
+    elif case == "mixed_bf16_book":
+        V = rv(n, d, 47)
+        Cb = inputs.f32_to_bf16_bits(rv(K, d, 48))
+        Vt, Ct = dev(V), dev(Cb, "bf16")
+        codes = torch.empty(n, dtype=torch.int32, device="cuda")
+        dist = torch.empty(n, dtype=torch.float32, device="cuda")
+        C.crvq_assign(VecSet.of_vectors(Vt), Ct, codes, dist)
+        torch.cuda.synchronize()
+        exp, ed = oracle.assign(V, Cb, "f32", "bf16")
+        np.testing.assert_array_equal(codes.cpu().numpy(), exp)
+        np.testing.assert_array_equal(dist.cpu().numpy(), ed.astype(np.float32))
+    else:
+        # codewords drawn near the rows, as K-means leaves them: many near-ties for the first screen
+        V = rv(n, d, 49)
+        Cb = np.ascontiguousarray(V[g.choice(n, K, replace=False)] + rv(K, d, 50, 0.002))
+        check(V, Cb)

@@ -801,9 +801,16 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   const int64_t ns = src.n;                      // stride of the per-split outputs
   const int64_t n = LIST ? *list_n : src.n;      // rows to screen
   const int d = src.d;
-  const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
-  if (row0 >= n) return;  // no barriers below
+  // LIST: the four waves of a block take the same 32 CB rows, each a quarter of the split's tiles,
+  // and merge through LDS at the end (the uncertain rows are few, so rows alone would leave most
+  // SIMDs idle).  Otherwise every wave has rows of its own.
+  const int64_t row0 = LIST ? static_cast<int64_t>(blockIdx.x) * (32 * CB)
+                            : (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
+  if (row0 >= n) return;  // uniform over the block in LIST mode; the only barrier is below
   const float alpha = alpha_p[0];
+  __shared__ double sD[LIST ? 4 : 1][LIST ? 32 * CB : 1];
+  __shared__ int sK[LIST ? 4 : 1][LIST ? 32 * CB : 1];
+  __shared__ float sR[LIST ? 4 : 1][LIST ? 32 * CB : 1];
 
   h8 b1[CB], b2[CB];
   bool forced[CB];
@@ -852,8 +859,14 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     id[cb] = -1;
   }
 
-  const int64_t t0 = static_cast<int64_t>(split) * tps;
-  const int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
+  int64_t t0 = static_cast<int64_t>(split) * tps;
+  int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
+  if (LIST) {
+    const int64_t q = (t1 - t0 + 7) / 8 * 2;  // even shares: chunks of two tiles stay aligned
+    const int64_t a = t0 + __builtin_amdgcn_readfirstlane(wave) * q;  // wave-uniform: scalar bounds
+    t1 = (a + q < t1) ? a + q : t1;
+    t0 = a;
+  }
   if (t0 < t1) {
     // Codebook tiles come in through a buffer resource: the per-lane byte offset is fixed, the
     // tile offset is a scalar, so a tile costs no vector address arithmetic.  Lanes 0-31 read c1
@@ -982,7 +995,20 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       D = oD;
       kk = ok2;
     }
-    if (h == 0 && valid) {
+    if (LIST) {
+      if (h == 0) {
+        sD[wave][cb * 32 + j] = D;
+        sK[wave][cb * 32 + j] = kk;
+        sR[wave][cb * 32 + j] = rr;
+      }
+      if (h == 0 && valid && wave == 0 && split == 0) {
+        double xn2 = 0.0;
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+          if (t < d) xn2 = xn2 + xd[t] * xd[t];
+        xn2o[i] = xn2;
+      }
+    } else if (h == 0 && valid) {
       double xn2 = 0.0;
 #pragma unroll
       for (int t = 0; t < 8; ++t)
@@ -991,6 +1017,28 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       pK[static_cast<int64_t>(split) * ns + i] = kk;
       pR[static_cast<int64_t>(split) * ns + i] = rr;
       if (split == 0) xn2o[i] = xn2;
+    }
+  }
+  if (LIST) {
+    // merge the four quarters as splits are merged: the (D, k)-smallest exact winner, the smallest rest
+    __syncthreads();
+    for (int r = threadIdx.x; r < 32 * CB; r += 256) {
+      const int64_t i = row0 + r;
+      if (i >= n) continue;
+      double D = sD[0][r];
+      int kk = sK[0][r];
+      float rr = sR[0][r];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) {
+        if (cless(sD[w][r], sK[w][r], D, kk)) {
+          D = sD[w][r];
+          kk = sK[w][r];
+        }
+        rr = fminf(rr, sR[w][r]);
+      }
+      pD[static_cast<int64_t>(split) * ns + i] = D;
+      pK[static_cast<int64_t>(split) * ns + i] = kk;
+      pR[static_cast<int64_t>(split) * ns + i] = rr;
     }
   }
 }
@@ -2007,7 +2055,8 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                        w.bcount + nb, w.rlist);
     // Second screen, split form (two MFMAs per tile, the tight bound), over the rows the first one
     // left uncertain; what still fails goes to the exact rescue.
-    hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true>), grid, dim3(256), 0, stream, src,
+    const dim3 grid2(static_cast<unsigned>(cdiv(src.n, 32 * CRVQ_S32_CB)), static_cast<unsigned>(p.splits));
+    hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true>), grid2, dim3(256), 0, stream, src,
                        ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
     const ScreenBound b2 = screen_bound(p, src.type, ct, src.d, alpha);
     hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,

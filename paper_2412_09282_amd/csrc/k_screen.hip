@@ -1161,6 +1161,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     }
     for (int s = 0; s < (NB > 1 ? splits : 0); ++s) {
       rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
+      // The kept tiles to re-score, as a bit set over the (group, slot) pairs, so that a wave loops
+      // over the most any of its rows needs (typically a handful) instead of every kept slot.
+      uint64_t todo = 0;
       for (int g = 0; g < 4; ++g) {
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
@@ -1171,6 +1174,15 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
             rest = fminf(rest, mj);
             continue;
           }
+          todo |= uint64_t{1} << (g * NB + j);
+        }
+      }
+      while (todo) {
+        const int q = __builtin_ctzll(todo);
+        todo &= todo - 1;
+        const int g = q / NB, j = q - (q / NB) * NB;
+        {
+          const int T = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
           float cw[4][DM];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -1836,6 +1848,107 @@ __global__ __launch_bounds__(256) void beam_merge_wave(int64_t n, int n_par, int
   }
 }
 
+// The same selection with eight lanes per vector (n_par <= 8, beam <= 8): lane b holds parent b's
+// child list, which the search emits in (D, code) order; at every step the eight list heads are
+// reduced to the smallest key (D, parent, code) with xor shuffles inside the lane group, the winning
+// parent drops its head, and lane s keeps the winner of step s and writes child slot s.  Exhausted or
+// invalid heads carry +inf and a parent index past every parent (distinct per lane), so the winners
+// come out in the order of the sequential merge above.
+__global__ __launch_bounds__(256) void beam_merge_lanes(int64_t n, int n_par, int n_next, int beam, int step,
+                                                        int n_books, const double* __restrict__ rowD,
+                                                        const int* __restrict__ rowK, RowSrc src0,
+                                                        const double* __restrict__ res_in, double* __restrict__ res_out,
+                                                        const int* __restrict__ tup_in, int* __restrict__ tup_out,
+                                                        double* __restrict__ err_out, const void* __restrict__ book,
+                                                        int bt, int64_t K, int d) {
+  const int sub = threadIdx.x & 7;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 32 + (threadIdx.x >> 3);
+  const bool live = i < n;  // no early exit: the lane groups shuffle among themselves only
+  const bool has = live && sub < n_par;
+  double hD[8];
+  int hK[8];
+#pragma unroll
+  for (int h = 0; h < 8; ++h) {
+    hD[h] = __builtin_inf();
+    hK[h] = -1;
+    if (has && h < beam) {
+      const int64_t r = (i * n_par + sub) * beam + h;
+      const int k = rowK[r];
+      if (k >= 0 && k < K) {
+        hD[h] = rowD[r];
+        hK[h] = k;
+      }
+    }
+  }
+  auto less = [](double Da, int ba, int ka, double Db, int bb, int kb) {
+    return Da < Db || (Da == Db && (ba < bb || (ba == bb && ka < kb)));
+  };
+  double myD = __builtin_inf();
+  int myB = -1, myK = -1;
+  for (int s = 0; s < n_next; ++s) {
+    const bool valid_head = hK[0] >= 0;
+    double mD = valid_head ? hD[0] : __builtin_inf();
+    int mB = valid_head ? sub : n_par + sub;
+    int mK = hK[0];
+#pragma unroll
+    for (int m = 1; m < 8; m <<= 1) {
+      const double oD = __shfl_xor(mD, m);
+      const int oB = __shfl_xor(mB, m);
+      const int oK = __shfl_xor(mK, m);
+      if (less(oD, oB, oK, mD, mB, mK)) {
+        mD = oD;
+        mB = oB;
+        mK = oK;
+      }
+    }
+    if (s == sub) {
+      myD = mD;
+      myB = mB;
+      myK = mK;
+    }
+    if (valid_head && mB == sub) {  // this parent's head was taken: drop it
+#pragma unroll
+      for (int h = 0; h < 7; ++h) {
+        hD[h] = hD[h + 1];
+        hK[h] = hK[h + 1];
+      }
+      hD[7] = __builtin_inf();
+      hK[7] = -1;
+    }
+  }
+  if (!live || sub >= n_next) return;
+  const int s = sub;
+  double* ro = res_out + (i * n_next + s) * d;
+  int* to = tup_out + (i * n_next + s) * n_books;
+  if (myK < 0 || myB >= n_par) {  // cannot happen when n_next = min(beam, n_par * K); kept as a guard
+    err_out[i * n_next + s] = __builtin_inf();
+    for (int t = 0; t < d; ++t) ro[t] = 0.0;
+    for (int u = 0; u <= step; ++u) to[u] = 0;
+    return;
+  }
+  if (d == 8 && step > 0 && bt == ET_F32 && (reinterpret_cast<uintptr_t>(book) & 15) == 0) {  // 16-byte accesses
+    const double2* pr = reinterpret_cast<const double2*>(res_in + (i * n_par + myB) * 8);
+    const float4* cw = reinterpret_cast<const float4*>(static_cast<const float*>(book) + static_cast<int64_t>(myK) * 8);
+    const float4 c0 = cw[0], c1 = cw[1];
+    const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+    double2* rw = reinterpret_cast<double2*>(ro);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const double2 pv = pr[h];
+      rw[h] = make_double2(pv.x - static_cast<double>(cc[2 * h]), pv.y - static_cast<double>(cc[2 * h + 1]));
+    }
+  } else {
+    const int64_t off0 = (step == 0) ? row_offset(src0, i) : 0;
+    for (int t = 0; t < d; ++t) {
+      const double parent = (step == 0) ? row_elem(src0, off0, t) : res_in[(i * n_par + myB) * d + t];
+      ro[t] = parent - cb_elem(book, bt, myK, d, t);
+    }
+  }
+  for (int u = 0; u < step; ++u) to[u] = tup_in[(i * n_par + myB) * n_books + u];
+  to[step] = myK;
+  err_out[i * n_next + s] = myD;
+}
+
 __global__ __launch_bounds__(256) void beam_emit_kernel(int64_t n, int64_t vpr, int n_par, int n_books,
                                                         const int* __restrict__ tup, const double* __restrict__ err,
                                                         CodePtrs outs, float* __restrict__ err_out) {
@@ -2120,7 +2233,11 @@ hipError_t launch_beam_merge(int64_t n, int n_par, int beam, int step, int n_boo
   if (n <= 0) return hipSuccess;
   int64_t nn = static_cast<int64_t>(n_par) * K;
   const int n_next = static_cast<int>(nn < beam ? nn : beam);
-  if (n_par * beam > 1) {  // a real merge: one wave per vector
+  if (n_par * beam > 1 && n_par <= 8 && beam <= 8) {  // a real merge: eight lanes per vector
+    hipLaunchKernelGGL(beam_merge_lanes, dim3(static_cast<unsigned>(cdiv(n, 32))), dim3(256), 0, stream, n, n_par,
+                       n_next, beam, step, n_books, rowD, rowK, src0, res_in, res_out, tup_in, tup_out, err_out, book,
+                       book_type, K, d);
+  } else if (n_par * beam > 1) {  // wider beams: one wave per vector
     hipLaunchKernelGGL(beam_merge_wave, dim3(static_cast<unsigned>(cdiv(n, 4))), dim3(256), 0, stream, n, n_par,
                        n_next, beam, step, n_books, rowD, rowK, src0, res_in, res_out, tup_in, tup_out, err_out, book,
                        book_type, K, d);

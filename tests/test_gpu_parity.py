@@ -310,6 +310,29 @@ def test_beam_parity(beam, Ks, n):
     d = 8
     V = rv(n, d, 26)
     books = [rv(K, d, 27 + t, 0.02 / (4 ** t)) for t, K in enumerate(Ks)]
+    check_beam(V, books, beam)
+
+
+@pytest.mark.parametrize("beam", [2, 4, 8])
+def test_beam_ties(beam):
+    """Small-integer vectors against books with every codeword twice: children of different parents
+    tie on their error all the time, so the merge's (error, parent rank, codeword) order decides which
+    tuples survive each step."""
+    say(f"beam ties B={beam} n=3001")
+    g = np.random.default_rng(40 + beam)
+    n, d = 3001, 8
+    V = g.integers(-3, 4, (n, d)).astype(np.float32)
+    books = []
+    for K, lo in ((64, -3), (16, -1), (16, -1)):
+        b = g.integers(lo, -lo + 1, (K, d)).astype(np.float32)
+        b[K // 2:] = b[:K // 2]
+        books.append(b)
+    check_beam(V, books, beam)
+
+
+def check_beam(V, books, beam):
+    n = V.shape[0]
+    Ks = [b.shape[0] for b in books]
     codes = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in Ks]
     err = torch.empty(n, dtype=torch.float32, device="cuda")
     C.crvq_assign_residual_beam(VecSet.of_vectors(dev(V)), [dev(b) for b in books], beam, codes, err)

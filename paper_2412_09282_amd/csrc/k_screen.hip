@@ -682,6 +682,7 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 
 constexpr int kS32Tile = 32;         // codewords per tile
 constexpr int64_t kRescueBlocks = 1024;  // persistent grid of the exact rescue
+constexpr int64_t kS32SharedRowsMaxN = int64_t{1} << 23;  // second screen: shared rows below this n
 constexpr int kS32TileHalves = 768;  // packed fp16 per tile: c1, c2, N terms, 32 x 8 each
 constexpr int kS32MaxParts = 256;    // partial maxima of the codebook scale reduction
 
@@ -786,7 +787,8 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
 // second MFMA alone, (c1|N).(x1|2^12), forms alpha^2 s: one v_mfma_f32_32x32x16_f16 per tile.
 // LIST: the rows are list[0 .. *list_n), and results go to their list positions (the second screen
 // of the rows the first one left uncertain).
-template <int CB, int NC, bool ONE, bool LIST>
+// QS (LIST only): the four waves of a block share their rows and split the codebook (few listed rows).
+template <int CB, int NC, bool ONE, bool LIST, bool QS = false>
 __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_t* apack,
                                                        const float* __restrict__ alpha_p, int64_t tiles, int64_t tps,
                                                        const void* __restrict__ C, int ct, int64_t K,
@@ -801,16 +803,17 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   const int64_t ns = src.n;                      // stride of the per-split outputs
   const int64_t n = LIST ? *list_n : src.n;      // rows to screen
   const int d = src.d;
-  // LIST: the four waves of a block take the same 32 CB rows, each a quarter of the split's tiles,
-  // and merge through LDS at the end (the uncertain rows are few, so rows alone would leave most
-  // SIMDs idle).  Otherwise every wave has rows of its own.
-  const int64_t row0 = LIST ? static_cast<int64_t>(blockIdx.x) * (32 * CB)
-                            : (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
-  if (row0 >= n) return;  // uniform over the block in LIST mode; the only barrier is below
+  // QS: the four waves of a block take the same 32 CB rows, each a quarter of the split's tiles, and
+  // merge through LDS at the end (when the listed rows are few, rows alone would leave most SIMDs
+  // idle).  Otherwise every wave has rows of its own.
+  static_assert(LIST || !QS, "the shared-row split is for listed rows");
+  const int64_t row0 = QS ? static_cast<int64_t>(blockIdx.x) * (32 * CB)
+                          : (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
+  if (row0 >= n) return;  // uniform over the block in QS mode; the only barrier is below
   const float alpha = alpha_p[0];
-  __shared__ double sD[LIST ? 4 : 1][LIST ? 32 * CB : 1];
-  __shared__ int sK[LIST ? 4 : 1][LIST ? 32 * CB : 1];
-  __shared__ float sR[LIST ? 4 : 1][LIST ? 32 * CB : 1];
+  __shared__ double sD[QS ? 4 : 1][QS ? 32 * CB : 1];
+  __shared__ int sK[QS ? 4 : 1][QS ? 32 * CB : 1];
+  __shared__ float sR[QS ? 4 : 1][QS ? 32 * CB : 1];
 
   h8 b1[CB], b2[CB];
   bool forced[CB];
@@ -861,7 +864,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
 
   int64_t t0 = static_cast<int64_t>(split) * tps;
   int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
-  if (LIST) {
+  if (QS) {
     const int64_t q = (t1 - t0 + 7) / 8 * 2;  // even shares: chunks of two tiles stay aligned
     const int64_t a = t0 + __builtin_amdgcn_readfirstlane(wave) * q;  // wave-uniform: scalar bounds
     t1 = (a + q < t1) ? a + q : t1;
@@ -995,7 +998,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       D = oD;
       kk = ok2;
     }
-    if (LIST) {
+    if (QS) {
       if (h == 0) {
         sD[wave][cb * 32 + j] = D;
         sK[wave][cb * 32 + j] = kk;
@@ -1019,7 +1022,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       if (split == 0) xn2o[i] = xn2;
     }
   }
-  if (LIST) {
+  if (QS) {
     // merge the four quarters as splits are merged: the (D, k)-smallest exact winner, the smallest rest
     __syncthreads();
     for (int r = threadIdx.x; r < 32 * CB; r += 256) {
@@ -2168,9 +2171,16 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                        w.bcount + nb, w.rlist);
     // Second screen, split form (two MFMAs per tile, the tight bound), over the rows the first one
     // left uncertain; what still fails goes to the exact rescue.
-    const dim3 grid2(static_cast<unsigned>(cdiv(src.n, 32 * CRVQ_S32_CB)), static_cast<unsigned>(p.splits));
-    hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true>), grid2, dim3(256), 0, stream, src,
-                       ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
+    // The listed rows are typically 7-9 % of n: below a few million rows the four waves of a block
+    // share 128 of them and split the codebook, above that every wave takes rows of its own.
+    if (src.n < kS32SharedRowsMaxN) {
+      const dim3 grid2(static_cast<unsigned>(cdiv(src.n, 32 * CRVQ_S32_CB)), static_cast<unsigned>(p.splits));
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true>), grid2, dim3(256), 0, stream,
+                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
+    } else {
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false>), grid, dim3(256), 0, stream,
+                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
+    }
     const ScreenBound b2 = screen_bound(p, src.type, ct, src.d, alpha);
     hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
                        p.splits, src.n, w.rlist, w.rcount, w.pR, w.pD, w.pK, w.xn2, b2, w.rcount + 1, w.rlist2,

@@ -1,6 +1,6 @@
 """Per-call timings of the library against its roofline, on one layer shape.
 
-    python -m paper_2412_09282_amd.kernel_bench [--workload 4] [--reps 10]
+    python -m paper_2412_09282_amd.kernel_bench [--workload 4] [--reps 10] [--skip-assign] [--calibrate-copy]
 
 Times every library call of the path with HIP events (median of --reps after warm-up) on the
 workload's first layer and prints one JSON object per call with the algorithmic bytes (or flops)
@@ -58,7 +58,16 @@ def main(argv=None):
     ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--skip-assign", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="start with a plain 1 GiB device-to-device copy (the reference for HBM counters)")
     a = ap.parse_args(argv)
+    if a.calibrate_copy:
+        src = torch.empty(1 << 28, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     wl = inputs.WORKLOADS[a.workload]
     L = wl.layers[0]
     M, N, d = L.M, L.N, wl.d

@@ -41,6 +41,9 @@
 #ifndef CRVQ_CHUNK
 #define CRVQ_CHUNK 8  // tiles per tracking chunk of the top-1 screen on long tile ranges
 #endif
+#ifndef CRVQ_CHUNK_TOPB
+#define CRVQ_CHUNK_TOPB 4  // tiles per chunk of the top-B screen (B = 2, 4, 8) on long tile ranges
+#endif
 #ifndef CRVQ_CHUNK_MIN_TILES
 #define CRVQ_CHUNK_MIN_TILES 128  // shorter tile ranges track single tiles (cheaper exact epilogue)
 #endif
@@ -526,15 +529,9 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __r
         fold(T0);
       }
     } else {
-      for (int64_t T = t0; T < t1; ++T) {
-        typename OPS::A a;
-        f4 c4;
-        advance(T, a, c4);
-        const int Ti = static_cast<int>(T);
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) {
-          const f4 acc = OPS::mfma(a, bop[cb], c4);
-          float x = fminf(fminf(acc[0], acc[1]), fminf(acc[2], acc[3]));
+      // Top-B: the minimum x of a tile (NC = 1) or of a chunk of NC tiles enters the sorted list of
+      // the NB smallest, keyed by the first tile; what falls off the list joins "rest".
+      auto insert = [&](int cb, float x, int Ti) {
           if constexpr (NB == 2) {
             // m0 <= m1 <= rest is kept sorted with medians: 10 VALU ops per tile and row
             const bool lt0 = x < m[cb][0];
@@ -559,6 +556,39 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __r
             }
             rest[cb] = fminf(rest[cb], x);
           }
+      };
+      if constexpr (NC == 1) {
+        for (int64_t T = t0; T < t1; ++T) {
+          typename OPS::A a;
+          f4 c4;
+          advance(T, a, c4);
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) {
+            const f4 acc = OPS::mfma(a, bop[cb], c4);
+            insert(cb, fminf(fminf(acc[0], acc[1]), fminf(acc[2], acc[3])), static_cast<int>(T));
+          }
+        }
+      } else {
+        // long tile ranges: inside a chunk every value only folds into the chunk minimum, the list
+        // insertion runs once per chunk
+        for (int64_t T0 = t0; T0 < t1; T0 += NC) {
+          const int64_t Te = (T0 + NC < t1) ? T0 + NC : t1;
+          float xc[CB];
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) xc[cb] = __builtin_inff();
+          for (int64_t T = T0; T < Te; ++T) {
+            typename OPS::A a;
+            f4 c4;
+            advance(T, a, c4);
+#pragma unroll
+            for (int cb = 0; cb < CB; ++cb) {
+              const f4 acc = OPS::mfma(a, bop[cb], c4);
+              xc[cb] = fminf(fminf(xc[cb], acc[0]), acc[1]);
+              xc[cb] = fminf(fminf(xc[cb], acc[2]), acc[3]);
+            }
+          }
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) insert(cb, xc[cb], static_cast<int>(T0));
         }
       }
     }
@@ -644,8 +674,9 @@ __global__ __launch_bounds__(256) void screen_kernel(RowSrc src, const void* __r
       }
     }
   } else {
-    // Top-B: per row and lane group the kept tile ids; per row the smallest minimum of every other
-    // tile over the four lane groups (a lower bound on the screen value of every codeword not kept).
+    // Top-B: per row and lane group the kept tile (or chunk) ids; per row the smallest minimum of
+    // every other tile or chunk over the four lane groups (a lower bound on the screen value of every
+    // codeword not kept).
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
       const int64_t i = row0 + cb * 16 + jl;
@@ -1085,7 +1116,8 @@ __device__ __forceinline__ void emit_row(int64_t row, const double (&ED)[NB], co
 
 // One thread per row; rows that fail the certification are appended to the rescue list.
 template <int KS, int NB>
-__global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int top, const int* __restrict__ pT,
+__global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, int chunk, int64_t tps, int64_t tiles,
+                                                       int top, const int* __restrict__ pT,
                                                        const float* __restrict__ pM,
                                                        const float* __restrict__ pR, const double* __restrict__ pD,
                                                        const int* __restrict__ pK, const double* __restrict__ xn2a,
@@ -1180,12 +1212,14 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
           todo |= uint64_t{1} << (g * NB + j);
         }
       }
+      const int64_t ts1 = (static_cast<int64_t>(s) + 1) * tps < tiles ? (static_cast<int64_t>(s) + 1) * tps : tiles;
       while (todo) {
         const int q = __builtin_ctzll(todo);
         todo &= todo - 1;
         const int g = q / NB, j = q - (q / NB) * NB;
-        {
-          const int T = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+        const int T0 = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+        for (int u = 0; u < chunk && T0 + u < ts1; ++u) {  // the kept tile, or every tile of its chunk
+          const int T = T0 + u;
           float cw[4][DM];
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
@@ -1982,10 +2016,18 @@ hipError_t launch_screen_ops(const RowSrc& src, const void* C, int ct, int64_t K
                                     : launch_screen_t<OPS, 1, 2, CRVQ_CHUNK>(src, C, ct, K, p, w, stream);
       return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 1, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
                                   : launch_screen_t<OPS, 1, 2>(src, C, ct, K, p, w, stream);
-    case 2: return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 2, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
-                             : launch_screen_t<OPS, 2, 2>(src, C, ct, K, p, w, stream);
-    case 4: return launch_screen_t<OPS, 4, 4>(src, C, ct, K, p, w, stream);
-    case 8: return launch_screen_t<OPS, 8, 2>(src, C, ct, K, p, w, stream);
+    case 2:
+      if (p.chunk > 1)
+        return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 2, CRVQ_CB_WIDE, CRVQ_CHUNK_TOPB>(src, C, ct, K, p, w, stream)
+                                    : launch_screen_t<OPS, 2, 2, CRVQ_CHUNK_TOPB>(src, C, ct, K, p, w, stream);
+      return p.cb == CRVQ_CB_WIDE ? launch_screen_t<OPS, 2, CRVQ_CB_WIDE>(src, C, ct, K, p, w, stream)
+                                  : launch_screen_t<OPS, 2, 2>(src, C, ct, K, p, w, stream);
+    case 4:
+      if (p.chunk > 1) return launch_screen_t<OPS, 4, 4, CRVQ_CHUNK_TOPB>(src, C, ct, K, p, w, stream);
+      return launch_screen_t<OPS, 4, 4>(src, C, ct, K, p, w, stream);
+    case 8:
+      if (p.chunk > 1) return launch_screen_t<OPS, 8, 2, CRVQ_CHUNK_TOPB>(src, C, ct, K, p, w, stream);
+      return launch_screen_t<OPS, 8, 2>(src, C, ct, K, p, w, stream);
     case 16: return launch_screen_t<OPS, 16, 1>(src, C, ct, K, p, w, stream);
   }
   return hipErrorInvalidValue;
@@ -1996,7 +2038,8 @@ hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K
                              const ScreenWs& w, const ScreenBound& bound, int32_t* codes, float* dist, double* rowD,
                              int* rowK, hipStream_t stream) {
   hipLaunchKernelGGL((finalize_kernel<KS, NB>), dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
-                     src, p.splits, top, w.pT, w.pM, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
+                     src, p.splits, NB > 1 ? static_cast<int>(p.chunk) : 1, p.tiles_per_split, p.tiles, top, w.pT,
+                     w.pM, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
                      dist, rowD, rowK);
   const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
   if (NB == 1 && CRVQ_RESCUE_FILTER)
@@ -2084,7 +2127,7 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   }
   p.tiles_per_split = cdiv(p.tiles, splits);
   p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
-  p.chunk = (p.nb == 1 && p.tiles_per_split >= CRVQ_CHUNK_MIN_TILES) ? CRVQ_CHUNK : 1;
+  p.chunk = (p.tiles_per_split >= CRVQ_CHUNK_MIN_TILES && p.nb <= 8) ? (p.nb == 1 ? CRVQ_CHUNK : CRVQ_CHUNK_TOPB) : 1;
   // Long top-1 searches: 32 x 32 split-fp16 tiles (two MFMAs per 1024 values instead of four).
   // The same rows per workgroup and codebook splits, counted in 32-codeword tiles.
   p.s32 = (p.split && CRVQ_S32_SCREEN && p.nb == 1 && p.tiles_per_split >= CRVQ_S32_MIN_TILES) ? 1 : 0;

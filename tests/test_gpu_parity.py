@@ -330,6 +330,20 @@ def test_beam_ties(beam):
     check_beam(V, books, beam)
 
 
+@pytest.mark.parametrize("beam", [2, 4, 8])
+def test_beam_long_codebook(beam):
+    """A first book of 65536 codewords drawn next to the rows (near-ties, as K-means leaves them) over
+    30001 rows: the top-B screen tracks chunks of tiles on its long tile ranges, and the finalize
+    re-scores whole kept chunks."""
+    say(f"beam long codebook B={beam} K=(65536, 64) n=30001")
+    g = np.random.default_rng(50 + beam)
+    n, d = 30001, 8
+    V = rv(n, d, 51)
+    b0 = V[g.choice(n, 65536, replace=True)] + (g.standard_normal((65536, d)) * 0.0005).astype(np.float32)
+    books = [b0.astype(np.float32), rv(64, d, 52, 0.005)]
+    check_beam(V, books, beam)
+
+
 def check_beam(V, books, beam):
     n = V.shape[0]
     Ks = [b.shape[0] for b in books]

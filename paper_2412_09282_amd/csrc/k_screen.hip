@@ -713,6 +713,8 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 
 constexpr int kS32Tile = 32;         // codewords per tile
 constexpr int64_t kRescueBlocks = 1024;  // persistent grid of the exact rescue
+constexpr int kRescueParts = 16;         // codeword ranges of a parted top-1 rescue
+constexpr int64_t kRescuePartMinK = 8192;  // codebooks from which the top-1 rescue is parted
 constexpr int64_t kS32SharedRowsMaxN = int64_t{1} << 23;  // second screen: shared rows below this n
 constexpr int kS32TileHalves = 768;  // packed fp16 per tile: c1, c2, N terms, 32 x 8 each
 constexpr int kS32MaxParts = 256;    // partial maxima of the codebook scale reduction
@@ -1521,12 +1523,19 @@ __global__ __launch_bounds__(256) void finalize1_list_kernel(int splits, int64_t
 // (sqrt(D_tent) + 2^-22 ||x||)^2 + 2^-120, D_tent being the exact distance of the tentative
 // winner.  Codewords that pass are scored exactly in fp64 and merged in (D, k) order.  A
 // non-finite threshold lets every codeword through (plain exact search).
+// Parts: with gridDim.y = P > 1 and room for every listed row's P partial results in partD / partK
+// (count * P <= cap), block (b, p) scans only the p-th of P equal codeword ranges and stores its
+// (D, k) minimum per row; rescue1_merge then takes the (D, k) minimum over the parts and emits the
+// row.  A few listed rows thus spread over P times as many workgroups (the scan of a long codebook
+// is the latency of the whole call otherwise).  Without the room, all blocks form one persistent
+// grid over the row batches, each scanning the whole codebook and emitting, as with P = 1.
 template <int KS>
 __global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const void* __restrict__ C, int ct,
                                                       int64_t K, const int* __restrict__ rcount,
                                                       const int* __restrict__ rlist, int32_t* __restrict__ codes,
                                                       float* __restrict__ dist, double* __restrict__ rowD,
-                                                      int* __restrict__ rowK) {
+                                                      int* __restrict__ rowK, double* __restrict__ partD,
+                                                      int* __restrict__ partK, int64_t cap) {
   constexpr int DM = 4 * KS;
   constexpr int kRB = 32 / DM;  // rows per batch: their 32 values live in scalar registers
   constexpr int kU = 4;         // codewords per thread in flight
@@ -1538,11 +1547,19 @@ __global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int d = src.d;
   const int count = *rcount;
+  const int P = static_cast<int>(gridDim.y);
+  const bool parted = P > 1 && static_cast<int64_t>(count) * P <= cap;
+  const int64_t kpart = parted ? (K + P - 1) / P : K;
+  const int64_t kb = parted ? static_cast<int64_t>(blockIdx.y) * kpart : 0;
+  const int64_t ke = (kb + kpart < K) ? kb + kpart : K;
 #if CRVQ_DEBUG_RESCUE
   if (blockIdx.x == 0 && threadIdx.x == 0) printf("[rescue] rows %d of %ld, K %ld\n", count, (long)src.n, (long)K);
 #endif
   const int nbatch = (count + kRB - 1) / kRB;
-  for (int bt = blockIdx.x; bt < nbatch; bt += gridDim.x) {
+  // parted: blocks (x, p) share part p's codeword range; otherwise all blocks are one persistent grid
+  const int bstart = parted ? static_cast<int>(blockIdx.x) : static_cast<int>(blockIdx.y * gridDim.x + blockIdx.x);
+  const int bstep = parted ? static_cast<int>(gridDim.x) : static_cast<int>(gridDim.x * gridDim.y);
+  for (int bt = bstart; bt < nbatch; bt += bstep) {
     const int ns = (count - bt * kRB < kRB) ? count - bt * kRB : kRB;  // rows in this batch
     if (tid < kRB) {
       float thr = -__builtin_inff();  // an empty slot passes nothing
@@ -1598,14 +1615,14 @@ __global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const
       bD[s] = __builtin_inf();
       bK[s] = INT_MAX;
     }
-    for (int64_t k0 = tid; k0 < K; k0 += kU * 256) {
+    for (int64_t k0 = kb + tid; k0 < ke; k0 += kU * 256) {
       float c[kU][DM];
 #pragma unroll
-      for (int u = 0; u < kU; ++u) load_codeword<DM>(C, ct, k0 + u * 256, d, k0 + u * 256 < K, c[u]);
+      for (int u = 0; u < kU; ++u) load_codeword<DM>(C, ct, k0 + u * 256, d, k0 + u * 256 < ke, c[u]);
 #pragma unroll
       for (int u = 0; u < kU; ++u) {
         const int64_t k = k0 + u * 256;
-        if (k >= K) continue;
+        if (k >= ke) continue;
 #pragma unroll
         for (int s = 0; s < kRB; ++s) {
           if (s >= ns) continue;  // uniform
@@ -1664,12 +1681,61 @@ __global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const
           k = wK[ww][tid];
         }
       }
-      const double ED[1] = {D};
-      const int EK[1] = {k};
-      emit_row<1>(srow[tid], ED, EK, top, 1, codes, dist, rowD, rowK);
+      if (parted) {
+        const int64_t slot = static_cast<int64_t>(bt) * kRB + tid;
+        partD[slot * P + blockIdx.y] = D;
+        partK[slot * P + blockIdx.y] = k;
+      } else {
+        const double ED[1] = {D};
+        const int EK[1] = {k};
+        emit_row<1>(srow[tid], ED, EK, top, 1, codes, dist, rowD, rowK);
+      }
     }
     __syncthreads();
   }
+}
+
+// The (D, k) minimum over the P parts of every listed row, emitted (parted rescues only).
+__global__ __launch_bounds__(256) void rescue1_merge(int top, int P, int64_t cap, const int* __restrict__ rcount,
+                                                     const int* __restrict__ rlist, const double* __restrict__ partD,
+                                                     const int* __restrict__ partK, int32_t* __restrict__ codes,
+                                                     float* __restrict__ dist, double* __restrict__ rowD,
+                                                     int* __restrict__ rowK) {
+  const int count = *rcount;
+  if (!(P > 1 && static_cast<int64_t>(count) * P <= cap)) return;
+  for (int64_t slot = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; slot < count;
+       slot += static_cast<int64_t>(gridDim.x) * 256) {
+    double D = partD[slot * P];
+    int k = partK[slot * P];
+    for (int q = 1; q < P; ++q) {
+      if (cless(partD[slot * P + q], partK[slot * P + q], D, k)) {
+        D = partD[slot * P + q];
+        k = partK[slot * P + q];
+      }
+    }
+    const double ED[1] = {D};
+    const int EK[1] = {k};
+    emit_row<1>(rlist[slot], ED, EK, top, 1, codes, dist, rowD, rowK);
+  }
+}
+
+// Top-1 rescue launch: codebooks of at least kRescuePartMinK codewords are scanned in
+// kRescueParts ranges when the free partial-result space (cap entries) holds them.
+template <int KS>
+hipError_t launch_rescue1(const RowSrc& src, int top, const void* C, int ct, int64_t K, const int* rcount,
+                          const int* rlist, int32_t* codes, float* dist, double* rowD, int* rowK, double* partD,
+                          int* partK, int64_t cap, hipStream_t stream) {
+  constexpr int kRB = 32 / (4 * KS);
+  const int P = (K >= kRescuePartMinK && partD && partK) ? kRescueParts : 1;
+  int64_t gx = cdiv(src.n, kRB);
+  const int64_t gmax = kRescueBlocks / P > 1 ? kRescueBlocks / P : 1;
+  if (gx > gmax) gx = gmax;
+  hipLaunchKernelGGL((rescue1_kernel<KS>), dim3(static_cast<unsigned>(gx), static_cast<unsigned>(P)), dim3(256), 0,
+                     stream, src, top, C, ct, K, rcount, rlist, codes, dist, rowD, rowK, partD, partK, cap);
+  if (P > 1)
+    hipLaunchKernelGGL(rescue1_merge, dim3(64), dim3(256), 0, stream, top, P, cap, rcount, rlist, partD, partK, codes,
+                       dist, rowD, rowK);
+  return hipGetLastError();
 }
 
 // Exact fp64 search of every listed row over the whole codebook.  Persistent: block b takes rows
@@ -2042,9 +2108,9 @@ hipError_t launch_finalize_t(const RowSrc& src, const void* C, int ct, int64_t K
                      w.pM, w.pR, w.pD, w.pK, w.xn2, C, ct, K, bound, w.rcount, w.rlist, codes,
                      dist, rowD, rowK);
   const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
-  if (NB == 1 && CRVQ_RESCUE_FILTER)
-    hipLaunchKernelGGL((rescue1_kernel<KS>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C,
-                       ct, K, w.rcount, w.rlist, codes, dist, rowD, rowK);
+  if (NB == 1 && CRVQ_RESCUE_FILTER)  // pD / pK are free once the finalize has read them
+    return launch_rescue1<KS>(src, top, C, ct, K, w.rcount, w.rlist, codes, dist, rowD, rowK, w.pD, w.pK,
+                              static_cast<int64_t>(p.splits) * src.n, stream);
   else
     hipLaunchKernelGGL((rescue_kernel<KS, NB>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C,
                        ct, K, w.rcount, w.rlist, codes, dist, rowD, rowK);
@@ -2228,10 +2294,9 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,
                        p.splits, src.n, w.rlist, w.rcount, w.pR, w.pD, w.pK, w.xn2, b2, w.rcount + 1, w.rlist2,
                        out_codes, out_dist, rowD, rowK);
-    const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
-    hipLaunchKernelGGL((rescue1_kernel<2>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C, ct, K,
-                       w.rcount + 1, w.rlist2, out_codes, out_dist, rowD, rowK);
-    return hipGetLastError();
+    // pD / pK are free once the second finalize has read them
+    return launch_rescue1<2>(src, top, C, ct, K, w.rcount + 1, w.rlist2, out_codes, out_dist, rowD, rowK, w.pD, w.pK,
+                             static_cast<int64_t>(p.splits) * src.n, stream);
   }
   const unsigned prep_grid = static_cast<unsigned>(cdiv(p.tiles * 16, 256));
   if (p.split) {
@@ -2256,10 +2321,8 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       hipLaunchKernelGGL((screen_small1_kernel<2>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles, C, ct, K,
                          bound, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t rgrid = src.n < kRescueBlocks ? src.n : kRescueBlocks;
-    hipLaunchKernelGGL((rescue1_kernel<2>), dim3(static_cast<unsigned>(rgrid)), dim3(256), 0, stream, src, top, C, ct, K,
-                       w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
-    return hipGetLastError();
+    return launch_rescue1<2>(src, top, C, ct, K, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK, nullptr, nullptr, 0,
+                             stream);
   }
   if (p.split) {
     e = launch_screen_ops<SplitOps>(src, C, ct, K, p, w, stream);

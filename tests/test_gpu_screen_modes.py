@@ -158,3 +158,24 @@ def test_two_pass_screen(case):
         V = rv(n, d, 49)
         Cb = np.ascontiguousarray(V[g.choice(n, K, replace=False)] + rv(K, d, 50, 0.002))
         check(V, Cb)
+
+
+def test_rescue_of_most_rows():
+    """Rows equal to codewords that the book holds four times (exact ties on every row, so nearly every
+    row reaches the exact rescue) over 1,048,579 rows: more listed rows than the parted rescue has
+    room for, so the rescue scans the whole codebook per row batch; sampled rows against the oracle."""
+    say("long top-1 search, 1048579 rows that all tie: whole-codebook rescue")
+    g = np.random.default_rng(44)
+    base = rv(16384, 8, 45)
+    Cb = np.ascontiguousarray(np.concatenate([base, base, base, base])[g.permutation(65536)])
+    n = 1048579
+    V = np.ascontiguousarray(base[g.integers(0, 16384, n)])
+    codes = torch.empty(n, dtype=torch.int32, device="cuda")
+    dist = torch.empty(n, dtype=torch.float32, device="cuda")
+    C.crvq_assign(VecSet.of_vectors(dev(V)), dev(Cb), codes, dist)
+    torch.cuda.synchronize()
+    S = np.sort(g.choice(n, 3000, replace=False))
+    S[-1] = n - 1
+    exp, ed = oracle.assign(V[S], Cb)
+    np.testing.assert_array_equal(codes.cpu().numpy()[S], exp)
+    np.testing.assert_array_equal(dist.cpu().numpy()[S], ed.astype(np.float32))

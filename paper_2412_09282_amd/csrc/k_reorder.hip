@@ -14,28 +14,40 @@
 namespace crvq {
 namespace {
 
-__device__ __forceinline__ bool precedes(float vi, int i, float vj, int j) {
-  const bool ni = vi != vi, nj = vj != vj;  // NaN test that survives -fno-honor-nans builds of other TUs
-  if (ni != nj) return nj;                  // a number precedes a NaN
-  if (!ni && vi != vj) return vi > vj;      // larger importance first
-  return i < j;                             // equal (or both NaN): lower channel first
+// The reorder's order as one unsigned 64-bit key: larger importance first, equal importances (and
+// -0 / +0) by channel, every NaN after every number and NaNs by channel.  The high word orders -v,
+// the low word is the channel.
+__device__ __forceinline__ uint64_t rank_key(float v, int64_t i) {
+  uint32_t hi;
+  if (v != v) {
+    hi = 0xffffffffu;
+  } else {
+    const float f = (v == 0.0f) ? 0.0f : -v;
+    const uint32_t u = __float_as_uint(f);
+    hi = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  }
+  return (static_cast<uint64_t>(hi) << 32) | static_cast<uint32_t>(i);
 }
 
-// Partial ranks: block (x, y) counts, for 256 channels, the channels of chunk y that precede them.
+// Partial ranks: block (x, y) counts, for 256 channels, the channels of chunk y that precede them
+// (keys compared as integers, staged in LDS).
 __global__ __launch_bounds__(256) void rank_partial_kernel(const float* __restrict__ imp, int64_t N, int64_t chunk,
                                                            int32_t* __restrict__ part) {
-  __shared__ float tile[1024];
+  __shared__ uint64_t tile[1024];
   const int64_t j = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  const float vj = (j < N) ? imp[j] : 0.0f;
+  const uint64_t kj = rank_key((j < N) ? imp[j] : 0.0f, j);
   const int64_t i0 = static_cast<int64_t>(blockIdx.y) * chunk;
   const int64_t i1 = (i0 + chunk < N) ? i0 + chunk : N;
   int rank = 0;
   for (int64_t base = i0; base < i1; base += 1024) {
-    for (int t = threadIdx.x; t < 1024; t += 256) tile[t] = (base + t < i1) ? imp[base + t] : 0.0f;
+    // past the chunk: the largest key, which precedes nothing
+    for (int t = threadIdx.x; t < 1024; t += 256)
+      tile[t] = (base + t < i1) ? rank_key(imp[base + t], base + t) : ~uint64_t{0};
     __syncthreads();
     const int lim = static_cast<int>((i1 - base) < 1024 ? (i1 - base) : 1024);
-    if (j < N)
-      for (int t = 0; t < lim; ++t) rank += precedes(tile[t], static_cast<int>(base + t), vj, static_cast<int>(j)) ? 1 : 0;
+    const int lim8 = (lim + 7) & ~7;  // the padding keys are never below kj
+#pragma unroll 8
+    for (int t = 0; t < lim8; ++t) rank += (tile[t] < kj) ? 1 : 0;
     __syncthreads();
   }
   if (j < N) part[static_cast<int64_t>(blockIdx.y) * N + j] = rank;
@@ -158,7 +170,7 @@ __global__ __launch_bounds__(256) void gather_vectors_kernel(RowSrc src, const i
 }  // namespace
 
 int rank_chunks(int64_t N) {
-  const int64_t c = cdiv(N, 512);
+  const int64_t c = cdiv(N, 256);
   return static_cast<int>(c < 1 ? 1 : (c > 64 ? 64 : c));
 }
 

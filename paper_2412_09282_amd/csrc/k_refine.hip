@@ -22,6 +22,9 @@ namespace crvq {
 namespace {
 
 constexpr int kGBM = 128, kGBN = 128, kGBK = 8;
+#ifndef CRVQ_GEMM_MFMA
+#define CRVQ_GEMM_MFMA 1  // fp64 products without transpose on the matrix cores
+#endif
 
 template <typename T>
 __device__ __forceinline__ double to_f64(T x) {
@@ -98,6 +101,89 @@ __global__ __launch_bounds__(256) void gemm_f64_kernel(int64_t M, int64_t Nc, in
       if (gj < Nc) C[gi * ldc + gj] = SUB ? C[gi * ldc + gj] - acc[i][j] : acc[i][j];
     }
   }
+}
+
+// The same product for fp64 A (row-major, not transposed) and B on the matrix cores: a 32 MW x 32 MW
+// tile of C per workgroup, 16 MW x 16 MW per wave as MW x MW v_mfma_f64_16x16x4f64 tiles (MW = 4 for
+// the long products, 2 for the short-k updates of the code search, which need more workgroups in
+// flight to hide their loads), k staged through
+// LDS 16 at a time (k-major, so the 16 lanes of an operand group read consecutive doubles).  Lane l
+// of an MFMA supplies A[i0 + l % 16][k + l / 16] and B[k + l / 16][j0 + l % 16] and holds
+// C[i0 + l / 16 + 4 r][j0 + l % 16], r < 4.  Each element is an fp64 dot product over its k range
+// (the matrix core's accumulation within a group of 4, then k order).
+constexpr int kMT = 128;  // C tile per workgroup and dimension of the long products (MW = 4)
+constexpr int kMK = 16;   // k per LDS stage
+typedef double d4v __attribute__((ext_vector_type(4)));
+template <bool SUB, int kMW>
+__global__ __launch_bounds__(256) void gemm_f64_mfma_kernel(int64_t M, int64_t Nc, int64_t Kd, const double* __restrict__ A,
+                                                            int64_t lda, const double* __restrict__ B, int64_t ldb,
+                                                            double* __restrict__ C, int64_t ldc, int64_t kchunk,
+                                                            int64_t c_part) {
+  constexpr int kMT = 2 * 16 * kMW;  // C tile per workgroup and dimension (2 x 2 waves)
+  __shared__ double As[kMK][kMT + 2];
+  __shared__ double Bs[kMK][kMT + 2];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wi = (wave >> 1) * 16 * kMW, wj = (wave & 1) * 16 * kMW;
+  const int li = lane & 15, lk = lane >> 4;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kMT, j0 = static_cast<int64_t>(blockIdx.x) * kMT;
+  const int64_t kb = static_cast<int64_t>(blockIdx.z) * kchunk;
+  const int64_t ke = kb + kchunk < Kd ? kb + kchunk : Kd;
+  C += static_cast<int64_t>(blockIdx.z) * c_part;
+  d4v acc[kMW][kMW];
+#pragma unroll
+  for (int a = 0; a < kMW; ++a)
+#pragma unroll
+    for (int b = 0; b < kMW; ++b) acc[a][b] = d4v{0.0, 0.0, 0.0, 0.0};
+  // stage k0's operands are read into registers one stage ahead, so their loads overlap the MFMAs
+  constexpr int kL = kMT * kMK / 256;
+  double pa[kL], pb[kL];
+  auto fetch = [&](int64_t k0) {
+#pragma unroll
+    for (int s = 0; s < kL; ++s) {
+      const int e = tid + 256 * s;
+      const int kk = e % kMK, ii = e / kMK;  // consecutive threads: consecutive k of one row of A
+      const int64_t gi = i0 + ii, gk = k0 + kk;
+      pa[s] = (gi < M && gk < ke) ? A[gi * lda + gk] : 0.0;
+      const int jj = e % kMT, kb2 = e / kMT;  // consecutive threads: consecutive j of one row of B
+      const int64_t gj = j0 + jj, gk2 = k0 + kb2;
+      pb[s] = (gj < Nc && gk2 < ke) ? B[gk2 * ldb + gj] : 0.0;
+    }
+  };
+  if (kb < ke) fetch(kb);
+  for (int64_t k0 = kb; k0 < ke; k0 += kMK) {
+#pragma unroll
+    for (int s = 0; s < kL; ++s) {
+      const int e = tid + 256 * s;
+      As[e % kMK][e / kMK] = pa[s];
+      Bs[e / kMT][e % kMT] = pb[s];
+    }
+    __syncthreads();
+    if (k0 + kMK < ke) fetch(k0 + kMK);
+#pragma unroll
+    for (int ks = 0; ks < kMK; ks += 4) {
+      double a[kMW], b[kMW];
+#pragma unroll
+      for (int t = 0; t < kMW; ++t) {
+        a[t] = As[ks + lk][wi + 16 * t + li];
+        b[t] = Bs[ks + lk][wj + 16 * t + li];
+      }
+#pragma unroll
+      for (int ta = 0; ta < kMW; ++ta)
+#pragma unroll
+        for (int tb = 0; tb < kMW; ++tb)
+          acc[ta][tb] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[ta], b[tb], acc[ta][tb], 0, 0, 0);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int ta = 0; ta < kMW; ++ta)
+#pragma unroll
+    for (int tb = 0; tb < kMW; ++tb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t gi = i0 + wi + 16 * ta + lk + 4 * r, gj = j0 + wj + 16 * tb + li;
+        if (gi < M && gj < Nc) C[gi * ldc + gj] = SUB ? C[gi * ldc + gj] - acc[ta][tb][r] : acc[ta][tb][r];
+      }
 }
 
 // C[i][j] = sum over parts p = 0 .. P - 1 in order of part[p][i][j] (the split-k partial products).
@@ -481,6 +567,15 @@ hipError_t launch_gemm_f64(int64_t M, int64_t Nc, int64_t Kd, const void* A, int
                      static_cast<const TA*>(A), lda, static_cast<const TB*>(B), ldb, C, ldc, Kd, int64_t{0})
   if (a_type == ET_F32 && b_type == ET_F32 && !sub) {
     if (trans_a) CRVQ_GEMM(float, float, true, false); else CRVQ_GEMM(float, float, false, false);
+  } else if (a_type == ET_F64 && b_type == ET_F64 && !trans_a && CRVQ_GEMM_MFMA) {
+    const dim3 gm(static_cast<unsigned>(cdiv(Nc, kMT)), static_cast<unsigned>(cdiv(M, kMT)));
+    const dim3 gs(static_cast<unsigned>(cdiv(Nc, kMT / 2)), static_cast<unsigned>(cdiv(M, kMT / 2)));
+    if (sub)
+      hipLaunchKernelGGL((gemm_f64_mfma_kernel<true, 2>), gs, dim3(256), 0, stream, M, Nc, Kd,
+                         static_cast<const double*>(A), lda, static_cast<const double*>(B), ldb, C, ldc, Kd, int64_t{0});
+    else
+      hipLaunchKernelGGL((gemm_f64_mfma_kernel<false, 4>), gm, dim3(256), 0, stream, M, Nc, Kd,
+                         static_cast<const double*>(A), lda, static_cast<const double*>(B), ldb, C, ldc, Kd, int64_t{0});
   } else if (a_type == ET_F64 && b_type == ET_F64 && !(trans_a && sub)) {
     if (trans_a) CRVQ_GEMM(double, double, true, false);
     else if (sub) CRVQ_GEMM(double, double, false, true);
@@ -496,7 +591,7 @@ hipError_t launch_gemm_f64(int64_t M, int64_t Nc, int64_t Kd, const void* A, int
 // grid alone is too small to fill the device; part products go to ws (P x M x Nc doubles) and are
 // summed in part order, so the result does not depend on scheduling.
 int64_t gemm_split_parts(int64_t M, int64_t Nc, int64_t Kd) {
-  const int64_t tiles = cdiv(Nc, kGBN) * cdiv(M, kGBM);
+  const int64_t tiles = CRVQ_GEMM_MFMA ? cdiv(Nc, kMT) * cdiv(M, kMT) : cdiv(Nc, kGBN) * cdiv(M, kGBM);
   int64_t P = tiles >= 256 ? 1 : cdiv(512, tiles);
   const int64_t maxp = Kd / 512 > 1 ? Kd / 512 : 1;
   return P < maxp ? P : maxp;
@@ -507,12 +602,18 @@ hipError_t launch_gemm_f64_split(int64_t M, int64_t Nc, int64_t Kd, const double
   if (M <= 0 || Nc <= 0) return hipSuccess;
   const int64_t P = gemm_split_parts(M, Nc, Kd);
   if (P <= 1) return launch_gemm_f64(M, Nc, Kd, A, ET_F64, false, lda, B, ET_F64, ldb, C, ldc, stream);
-  const int64_t kchunk = cdiv(cdiv(Kd, P), kGBK) * kGBK;
+  const int64_t kchunk = cdiv(cdiv(Kd, P), kMK) * kMK;
   const int64_t parts = cdiv(Kd, kchunk);
-  const dim3 grid(static_cast<unsigned>(cdiv(Nc, kGBN)), static_cast<unsigned>(cdiv(M, kGBM)),
-                  static_cast<unsigned>(parts));
-  hipLaunchKernelGGL((gemm_f64_kernel<double, double, false, false>), grid, dim3(256), 0, stream, M, Nc, Kd, A, lda, B,
-                     ldb, ws, Nc, kchunk, M * Nc);
+  if (CRVQ_GEMM_MFMA) {
+    const dim3 gm(static_cast<unsigned>(cdiv(Nc, kMT)), static_cast<unsigned>(cdiv(M, kMT)), static_cast<unsigned>(parts));
+    hipLaunchKernelGGL((gemm_f64_mfma_kernel<false, 4>), gm, dim3(256), 0, stream, M, Nc, Kd, A, lda, B, ldb, ws, Nc,
+                       kchunk, M * Nc);
+  } else {
+    const dim3 grid(static_cast<unsigned>(cdiv(Nc, kGBN)), static_cast<unsigned>(cdiv(M, kGBM)),
+                    static_cast<unsigned>(parts));
+    hipLaunchKernelGGL((gemm_f64_kernel<double, double, false, false>), grid, dim3(256), 0, stream, M, Nc, Kd, A, lda,
+                       B, ldb, ws, Nc, kchunk, M * Nc);
+  }
   hipLaunchKernelGGL(sum_parts_kernel, dim3(static_cast<unsigned>(cdiv(M * Nc, 256))), dim3(256), 0, stream, M, Nc,
                      static_cast<int>(parts), ws, C, ldc);
   return hipGetLastError();

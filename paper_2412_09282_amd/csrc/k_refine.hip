@@ -114,9 +114,9 @@ __global__ __launch_bounds__(256) void gemm_f64_kernel(int64_t M, int64_t Nc, in
 constexpr int kMT = 128;  // C tile per workgroup and dimension of the long products (MW = 4)
 constexpr int kMK = 16;   // k per LDS stage
 typedef double d4v __attribute__((ext_vector_type(4)));
-template <bool SUB, int kMW>
-__global__ __launch_bounds__(256) void gemm_f64_mfma_kernel(int64_t M, int64_t Nc, int64_t Kd, const double* __restrict__ A,
-                                                            int64_t lda, const double* __restrict__ B, int64_t ldb,
+template <bool SUB, int kMW, typename TA = double, typename TB = double, bool TRANS_A = false>
+__global__ __launch_bounds__(256) void gemm_f64_mfma_kernel(int64_t M, int64_t Nc, int64_t Kd, const TA* __restrict__ A,
+                                                            int64_t lda, const TB* __restrict__ B, int64_t ldb,
                                                             double* __restrict__ C, int64_t ldc, int64_t kchunk,
                                                             int64_t c_part) {
   constexpr int kMT = 2 * 16 * kMW;  // C tile per workgroup and dimension (2 x 2 waves)
@@ -141,12 +141,13 @@ __global__ __launch_bounds__(256) void gemm_f64_mfma_kernel(int64_t M, int64_t N
 #pragma unroll
     for (int s = 0; s < kL; ++s) {
       const int e = tid + 256 * s;
-      const int kk = e % kMK, ii = e / kMK;  // consecutive threads: consecutive k of one row of A
+      // consecutive threads: consecutive k of one row of A, or consecutive i of one row of A^T
+      const int kk = TRANS_A ? e / kMT : e % kMK, ii = TRANS_A ? e % kMT : e / kMK;
       const int64_t gi = i0 + ii, gk = k0 + kk;
-      pa[s] = (gi < M && gk < ke) ? A[gi * lda + gk] : 0.0;
+      pa[s] = (gi < M && gk < ke) ? to_f64(TRANS_A ? A[gk * lda + gi] : A[gi * lda + gk]) : 0.0;
       const int jj = e % kMT, kb2 = e / kMT;  // consecutive threads: consecutive j of one row of B
       const int64_t gj = j0 + jj, gk2 = k0 + kb2;
-      pb[s] = (gj < Nc && gk2 < ke) ? B[gk2 * ldb + gj] : 0.0;
+      pb[s] = (gj < Nc && gk2 < ke) ? to_f64(B[gk2 * ldb + gj]) : 0.0;
     }
   };
   if (kb < ke) fetch(kb);
@@ -154,7 +155,10 @@ __global__ __launch_bounds__(256) void gemm_f64_mfma_kernel(int64_t M, int64_t N
 #pragma unroll
     for (int s = 0; s < kL; ++s) {
       const int e = tid + 256 * s;
-      As[e % kMK][e / kMK] = pa[s];
+      if (TRANS_A)
+        As[e / kMT][e % kMT] = pa[s];
+      else
+        As[e % kMK][e / kMK] = pa[s];
       Bs[e / kMT][e % kMT] = pb[s];
     }
     __syncthreads();
@@ -565,7 +569,12 @@ hipError_t launch_gemm_f64(int64_t M, int64_t Nc, int64_t Kd, const void* A, int
 #define CRVQ_GEMM(TA, TB, TR, SB)                                                                          \
   hipLaunchKernelGGL((gemm_f64_kernel<TA, TB, TR, SB>), grid, dim3(256), 0, stream, M, Nc, Kd,             \
                      static_cast<const TA*>(A), lda, static_cast<const TB*>(B), ldb, C, ldc, Kd, int64_t{0})
-  if (a_type == ET_F32 && b_type == ET_F32 && !sub) {
+  if (a_type == ET_F32 && b_type == ET_F32 && !sub && trans_a && CRVQ_GEMM_MFMA) {
+    // the Gram matrix X^T X of fp32 activations, widened exactly on load
+    const dim3 gm(static_cast<unsigned>(cdiv(Nc, kMT)), static_cast<unsigned>(cdiv(M, kMT)));
+    hipLaunchKernelGGL((gemm_f64_mfma_kernel<false, 4, float, float, true>), gm, dim3(256), 0, stream, M, Nc, Kd,
+                       static_cast<const float*>(A), lda, static_cast<const float*>(B), ldb, C, ldc, Kd, int64_t{0});
+  } else if (a_type == ET_F32 && b_type == ET_F32 && !sub) {
     if (trans_a) CRVQ_GEMM(float, float, true, false); else CRVQ_GEMM(float, float, false, false);
   } else if (a_type == ET_F64 && b_type == ET_F64 && !trans_a && CRVQ_GEMM_MFMA) {
     const dim3 gm(static_cast<unsigned>(cdiv(Nc, kMT)), static_cast<unsigned>(cdiv(M, kMT)));

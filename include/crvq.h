@@ -57,7 +57,7 @@ typedef enum { CRVQ_REDUCE_SUM = 0, CRVQ_REDUCE_MAX = 1 } crvq_reduce;
 
 #define CRVQ_MAX_K 65536   /* codewords per codebook (e <= 16 bits) */
 #define CRVQ_MAX_D 16      /* sub-vector length */
-#define CRVQ_MAX_BEAM 16   /* residual beam width */
+#define CRVQ_MAX_BEAM 16   /* residual beam width (each lane group keeps its top-B list in registers) */
 #define CRVQ_MAX_BOOKS 8   /* basic + extended codebooks */
 
 /* Library version (major * 10000 + minor * 100 + patch). */
@@ -273,10 +273,14 @@ crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols
 /* crvq_hessian_product -- G = R H[:, 0:n_out] (so -2 G is the gradient of
  * QuantLoss w.r.t. W_hat on those columns) and, when row_loss != NULL (needs
  * n_out == N), row_loss[r] = sum_j R[r][j] G[r][j], the QuantLoss of row r
- * (Alg. 1 QuantLoss).  R: M x N fp64 (stride ldr), H: N x N fp64 (stride
- * ldh), G: M x n_out fp64 (stride ldg >= n_out).  Deterministic. */
+ * (Alg. 1 QuantLoss).  When loss_total != NULL (needs row_loss), loss_total[0]
+ * = sum_r row_loss[r], the layer's QuantLoss, summed on the device in a fixed
+ * order (so a caller's loop guard needs no host-side reduction).
+ * R: M x N fp64 (stride ldr), H: N x N fp64 (stride ldh), G: M x n_out fp64
+ * (stride ldg >= n_out); loss_total: one fp64 device value.  Deterministic. */
 crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const double* R, int64_t ldr, const double* H,
-                                 int64_t ldh, double* G, int64_t ldg, double* row_loss, void* stream);
+                                 int64_t ldh, double* G, int64_t ldg, double* row_loss, double* loss_total,
+                                 void* stream);
 
 /* crvq_code_sums -- sums[k] = sum of the vectors x_v with codes[v] == k, in
  * fp64, and counts[k] their number (the per-codeword gradient of
@@ -346,6 +350,37 @@ crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_
                               const uint8_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
                               const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* x,
                               int x_dtype, float* y, void* workspace, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * crvq_workspace_size -- one entry for every call's workspace size: the value
+ * the per-call *_workspace_size function above returns for the same shape.
+ * op selects the call; each op reads only the arguments listed (others are
+ * ignored and may be 0 / NULL):
+ *   CRVQ_OP_IMPORTANCE  M, N                         (crvq_channel_importance)
+ *   CRVQ_OP_REORDER     N                            (crvq_reorder)
+ *   CRVQ_OP_ASSIGN      n_vectors, d, K              (crvq_assign)
+ *   CRVQ_OP_BEAM        n_vectors, d, n_books, Ks, beam  (crvq_assign_residual_beam)
+ *   CRVQ_OP_KMEANS      n_vectors, d, K              (crvq_kmeans_update)
+ *   CRVQ_OP_DEQUANT     N = n_cols                   (crvq_dequant, crvq_dequant_books)
+ *   CRVQ_OP_CODE_SUMS   n_vectors, d, K              (crvq_code_sums)
+ *   CRVQ_OP_REFINE      M, N, n_cols                 (crvq_refine_codes)
+ *   CRVQ_OP_GEMV        M, N, K = K_base             (crvq_dequant_gemv)
+ * Returns 0 for an unknown op or a shape the call rejects (and for calls that
+ * need no workspace at that shape).  Ks is a host array of n_books entries.
+ */
+typedef enum {
+  CRVQ_OP_IMPORTANCE = 0,
+  CRVQ_OP_REORDER = 1,
+  CRVQ_OP_ASSIGN = 2,
+  CRVQ_OP_BEAM = 3,
+  CRVQ_OP_KMEANS = 4,
+  CRVQ_OP_DEQUANT = 5,
+  CRVQ_OP_CODE_SUMS = 6,
+  CRVQ_OP_REFINE = 7,
+  CRVQ_OP_GEMV = 8
+} crvq_op;
+size_t crvq_workspace_size(int op, int64_t n_vectors, int64_t K, int32_t beam, int32_t n_books, int32_t d,
+                           const int64_t* Ks, int64_t M, int64_t N, int64_t n_cols);
 
 /* ---------------------------------------------------------------------------
  * crvq_pack_codes_u8 -- 8-bit storage of codes (the e = 8 code width of Sec. 3.2

@@ -68,7 +68,8 @@ def lib(build_if_missing: bool = True):
                                         P, ctypes.c_int, I64, P, SZ, P], ctypes.c_int),
                 "crvq_bits_per_weight": ([I64, I64, I32, I64, I32, I32, P, I32, I32, P], ctypes.c_int),
                 "crvq_gram": ([P, ctypes.c_int, I64, I64, I64, P, I64, P], ctypes.c_int),
-                "crvq_hessian_product": ([I64, I64, I64, P, I64, P, I64, P, I64, P, P], ctypes.c_int),
+                "crvq_hessian_product": ([I64, I64, I64, P, I64, P, I64, P, I64, P, P, P], ctypes.c_int),
+                "crvq_workspace_size": ([ctypes.c_int, I64, I64, I32, I32, I32, P, I64, I64, I64], SZ),
                 "crvq_code_sums_workspace_size": ([I64, I32, I64], SZ),
                 "crvq_code_sums": ([P, I64, I64, I64, I32, P, I64, P, P, P, SZ, P], ctypes.c_int),
                 "crvq_adam_step": ([P, P, ctypes.c_double, P, P, I64, I64, ctypes.c_double, ctypes.c_double,
@@ -295,12 +296,24 @@ def crvq_gram(X: torch.Tensor, H: torch.Tensor, stream=None) -> None:
 
 
 def crvq_hessian_product(R: torch.Tensor, H: torch.Tensor, G: torch.Tensor, row_loss: Optional[torch.Tensor] = None,
-                         stream=None) -> None:
-    """G = R H[:, :G.shape[1]] and optionally the per-row QuantLoss sum_j R_rj G_rj (fp64)."""
+                         loss_total: Optional[torch.Tensor] = None, stream=None) -> None:
+    """G = R H[:, :G.shape[1]], optionally the per-row QuantLoss sum_j R_rj G_rj and their total (fp64)."""
     M, N = R.shape
     _check("crvq_hessian_product", lib().crvq_hessian_product(
         M, N, G.shape[1], _ptr(R), R.stride(0), _ptr(H), H.stride(0), _ptr(G), G.stride(0), _ptr(row_loss),
-        _stream(stream)))
+        _ptr(loss_total), _stream(stream)))
+
+
+CRVQ_OP = {"importance": 0, "reorder": 1, "assign": 2, "beam": 3, "kmeans": 4, "dequant": 5, "code_sums": 6,
+           "refine": 7, "gemv": 8}
+
+
+def crvq_workspace_size(op: str, n_vectors: int = 0, K: int = 0, beam: int = 0, Ks: Sequence[int] = (), d: int = 0,
+                        M: int = 0, N: int = 0, n_cols: int = 0) -> int:
+    """Workspace bytes of the call `op` names (a key of CRVQ_OP) at the given shape."""
+    arr = (ctypes.c_int64 * max(1, len(Ks)))(*Ks)
+    return int(lib().crvq_workspace_size(CRVQ_OP[op], n_vectors, K, beam, len(Ks), d, ctypes.cast(arr, ctypes.c_void_p),
+                                         M, N, n_cols))
 
 
 def crvq_code_sums(X: VecSet, codes: torch.Tensor, K: int, sums: torch.Tensor, counts: Optional[torch.Tensor] = None,

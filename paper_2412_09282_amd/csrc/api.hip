@@ -489,18 +489,21 @@ crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols
 }
 
 crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const double* R, int64_t ldr, const double* H,
-                                 int64_t ldh, double* G, int64_t ldg, double* row_loss, void* stream) {
+                                 int64_t ldh, double* G, int64_t ldg, double* row_loss, double* loss_total,
+                                 void* stream) {
   static const char* fn = "crvq_hessian_product";
   g_err.clear();
   if (M < 0 || N < 1 || n_out < 1 || n_out > N) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and 1 <= n_out <= N", fn);
   if (ldr < N || ldh < N || ldg < n_out) return fail(CRVQ_ERR_INVALID, "%s: ldr, ldh >= N and ldg >= n_out needed", fn);
   if (row_loss && n_out != N) return fail(CRVQ_ERR_INVALID, "%s: row_loss needs n_out == N", fn);
-  if (M == 0) return CRVQ_OK;
-  if (!R || !H || !G) return fail(CRVQ_ERR_INVALID, "%s: R, H and G must not be NULL", fn);
+  if (loss_total && !row_loss) return fail(CRVQ_ERR_INVALID, "%s: loss_total needs row_loss", fn);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  if (M == 0) return loss_total ? hip_status(launch_sum_f64(0, nullptr, loss_total, st), fn) : CRVQ_OK;
+  if (!R || !H || !G) return fail(CRVQ_ERR_INVALID, "%s: R, H and G must not be NULL", fn);
   crvq_status s = hip_status(launch_gemm_f64(M, n_out, N, R, ET_F64, false, ldr, H, ET_F64, ldh, G, ldg, st), fn);
   if (s || !row_loss) return s;
-  return hip_status(launch_row_dot(M, N, R, ldr, G, ldg, row_loss, st), fn);
+  if ((s = hip_status(launch_row_dot(M, N, R, ldr, G, ldg, row_loss, st), fn)) || !loss_total) return s;
+  return hip_status(launch_sum_f64(M, row_loss, loss_total, st), fn);
 }
 
 size_t crvq_code_sums_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
@@ -577,6 +580,22 @@ crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, d
 size_t crvq_gemv_workspace_size(int64_t M, int64_t N, int64_t K_base) {
   if (M < 1 || N < 64 || K_base < 1 || K_base > 256) return 0;
   return gemv_ws_bytes(M, N, static_cast<int>(K_base));
+}
+
+size_t crvq_workspace_size(int op, int64_t n_vectors, int64_t K, int32_t beam, int32_t n_books, int32_t d,
+                           const int64_t* Ks, int64_t M, int64_t N, int64_t n_cols) {
+  switch (op) {
+    case CRVQ_OP_IMPORTANCE: return crvq_importance_workspace_size(M, N);
+    case CRVQ_OP_REORDER: return crvq_reorder_workspace_size(N);
+    case CRVQ_OP_ASSIGN: return crvq_assign_workspace_size(n_vectors, d, K);
+    case CRVQ_OP_BEAM: return crvq_beam_workspace_size(n_vectors, d, n_books, Ks, beam);
+    case CRVQ_OP_KMEANS: return crvq_kmeans_workspace_size(n_vectors, d, K);
+    case CRVQ_OP_DEQUANT: return crvq_dequant_workspace_size(N);
+    case CRVQ_OP_CODE_SUMS: return crvq_code_sums_workspace_size(n_vectors, d, K);
+    case CRVQ_OP_REFINE: return crvq_refine_workspace_size(M, N, n_cols);
+    case CRVQ_OP_GEMV: return crvq_gemv_workspace_size(M, N, K);
+    default: return 0;
+  }
 }
 
 crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_t* q_base, int64_t ldq_base,

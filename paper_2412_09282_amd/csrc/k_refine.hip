@@ -218,6 +218,22 @@ __global__ __launch_bounds__(256) void row_dot_kernel(int64_t n, const double* _
   if (threadIdx.x == 0) out[r] = red[0];
 }
 
+// out[0] = sum_{i < n} x[i] (the layer's QuantLoss from its per-row terms): one block, strided
+// per-thread sums in index order, then the same fixed tree.
+__global__ __launch_bounds__(256) void sum_f64_kernel(int64_t n, const double* __restrict__ x,
+                                                      double* __restrict__ out) {
+  __shared__ double red[256];
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < n; i += 256) acc = acc + x[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (static_cast<int>(threadIdx.x) < w) red[threadIdx.x] = red[threadIdx.x] + red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[0] = red[0];
+}
+
 // ---- per-code sums ------------------------------------------------------------------------------
 constexpr int kCsVec = 256;      // vectors staged per round
 constexpr int kCsMaxOwn = 4;     // codes per thread (K <= 1024)
@@ -632,6 +648,11 @@ hipError_t launch_row_dot(int64_t M, int64_t n, const double* A, int64_t lda, co
                           double* out, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
   hipLaunchKernelGGL(row_dot_kernel, dim3(static_cast<unsigned>(M)), dim3(256), 0, stream, n, A, lda, B, ldb, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_f64(int64_t n, const double* x, double* out, hipStream_t stream) {
+  hipLaunchKernelGGL(sum_f64_kernel, dim3(1), dim3(256), 0, stream, n, x, out);
   return hipGetLastError();
 }
 

@@ -1101,16 +1101,19 @@ struct ScreenBound {
 template <int NB>
 __device__ __forceinline__ void emit_row(int64_t row, const double (&ED)[NB], const int (&EK)[NB], int top, int need,
                                          int32_t* codes, float* dist, double* rowD, int* rowK) {
+  // INT_MAX: no codeword compared below +inf (a row with a NaN element); the code is then 0, a
+  // defined in-range value, and the distance NaN
   if (codes) {
-    codes[row] = EK[0];
-    if (dist) dist[row] = static_cast<float>(ED[0]);
+    const bool none = EK[0] == INT_MAX;
+    codes[row] = none ? 0 : EK[0];
+    if (dist) dist[row] = none ? __builtin_nanf("") : static_cast<float>(ED[0]);
   } else {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       if (j < top) {
         const bool real = j < need;
         rowD[row * top + j] = real ? ED[j] : __builtin_inf();
-        rowK[row * top + j] = real ? EK[j] : -1;
+        rowK[row * top + j] = real ? (EK[j] == INT_MAX ? 0 : EK[j]) : -1;
       }
     }
   }
@@ -1427,6 +1430,10 @@ __device__ __forceinline__ bool finish_top1(int64_t i, int64_t row, int splits, 
     }
     certain = Dl < restd + xn2 - delta;
   }
+  if (kl == INT_MAX) {  // no score compared below +inf (a NaN element): leave it to the rescue
+    kl = 0;
+    certain = false;
+  }
   if (codes) {
     codes[row] = kl;
     if (dist) dist[row] = static_cast<float>(Dl);
@@ -1570,9 +1577,12 @@ __global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const
         load_row_exact<DM>(src, row, true, xd);
         double Dt;
         if (codes) {
+          // the tentative code is re-scored only when it indexes the book; otherwise the threshold
+          // starts at +inf and every codeword is scored exactly
           const int k0 = codes[row];
+          const bool okc = k0 >= 0 && k0 < K;
           float c0[DM];
-          load_codeword<DM>(C, ct, k0, d, true, c0);
+          load_codeword<DM>(C, ct, okc ? k0 : 0, d, okc, c0);
           Dt = 0.0;
 #pragma unroll
           for (int t = 0; t < DM; ++t) {
@@ -1581,6 +1591,7 @@ __global__ __launch_bounds__(256) void rescue1_kernel(RowSrc src, int top, const
               Dt = Dt + diff * diff;
             }
           }
+          if (!okc) Dt = __builtin_inf();
         } else {
           Dt = rowD[static_cast<int64_t>(row) * top];
         }

@@ -241,6 +241,7 @@ class LayerQuantizer:
             self.R = torch.empty(M, N, dtype=f64, device=dev)
             self.G = torch.empty(M, N, dtype=f64, device=dev)
             self.row_loss = torch.empty(M, dtype=f64, device=dev)
+            self.loss_total = torch.empty(1, dtype=f64, device=dev)
         books = self.C_basic + self.C_ext
         codes = self.codes_basic + self.codes_ext
         mb = cfg.m_base
@@ -261,11 +262,15 @@ class LayerQuantizer:
                                  ldq_ext=max(1, self.ncv), C_ext=books[mb:], minuend=self.Ws)
             rec.post(f"residual_{tag}", out=self.R)
             rec.pre(f"hessian_{tag}", R=self.R, H=self.H)
-            C.crvq_hessian_product(self.R, self.H, self.G, self.row_loss)
-            rec.post(f"hessian_{tag}", G=self.G, row_loss=self.row_loss)
-            return float(self.row_loss.cpu().numpy().sum())
+            C.crvq_hessian_product(self.R, self.H, self.G, self.row_loss, self.loss_total)
+            rec.post(f"hessian_{tag}", G=self.G, row_loss=self.row_loss, loss_total=self.loss_total)
 
-        losses = [loss_now("start")]
+        def loss_value():
+            # the only host read of the loop: QuantLoss for the guard, once per round
+            return float(self.loss_total.item())
+
+        loss_now("start")
+        losses = [loss_value()]
         t = 0
         r = 0
         while losses[-1] >= eps and r < rounds:
@@ -284,7 +289,8 @@ class LayerQuantizer:
                 rec.pre(f"refine_{r}_{b}", R=self.R, H=self.H, C=Cb, codes=codes[b], n_cols=cover[b])
                 C.crvq_refine_codes(self.R, self.H, Cb, codes[b], d, cover[b], ldq[b])
                 rec.post(f"refine_{r}_{b}", R=self.R, codes=codes[b])
-            losses.append(loss_now(f"round{r}"))
+            loss_now(f"round{r}")
+            losses.append(loss_value())
             r += 1
         C.crvq_dequant_books(M, N, d, codes[:mb], N // d, books[:mb], self.W_hat, n_crit=self.n_crit,
                              q_ext=codes[mb:], ldq_ext=max(1, self.ncv), C_ext=books[mb:], perm=self.perm)

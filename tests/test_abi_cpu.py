@@ -259,8 +259,10 @@ def test_refinement_validation(L):
     assert L.crvq_gram(FAKE, 1, 16, 8, 8, FAKE, 8, None) == 1            # bf16 activations not accepted
     assert L.crvq_gram(FAKE, 0, 16, 8, 4, FAKE, 8, None) == 1            # ld < n_cols
     assert L.crvq_gram(None, 0, 16, 0, 0, None, 0, None) == 0            # nothing to do
-    assert L.crvq_hessian_product(4, 8, 4, FAKE, 8, FAKE, 8, FAKE, 4, FAKE, None) == 1  # row_loss needs n_out == N
-    assert L.crvq_hessian_product(4, 8, 9, FAKE, 8, FAKE, 8, FAKE, 9, None, None) == 1
+    assert L.crvq_hessian_product(4, 8, 4, FAKE, 8, FAKE, 8, FAKE, 4, FAKE, None, None) == 1  # row_loss: n_out == N
+    assert L.crvq_hessian_product(4, 8, 9, FAKE, 8, FAKE, 8, FAKE, 9, None, None, None) == 1
+    assert L.crvq_hessian_product(4, 8, 8, FAKE, 8, FAKE, 8, FAKE, 8, None, FAKE, None) == 1  # total needs row_loss
+    assert "loss_total" in err(L)
     assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 2000, FAKE, None, ws, 1 << 30, None) == 2  # K > 1024
     assert L.crvq_code_sums(FAKE, 4, 2, 8, 8, FAKE, 16, FAKE, None, ws, 1 << 30, None) == 1     # ld < vpr * d
     assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 16, FAKE, None, ws, 0, None) == 3          # no workspace
@@ -277,3 +279,28 @@ def test_refinement_validation(L):
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 31, ws, need, None) == 1
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 32, ws, need - 1, None) == 3
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 2, 256, FAKE, 32, ws, need, None) == 1
+
+
+def test_workspace_size_dispatcher(L):
+    """crvq_workspace_size(op, ...) returns what the per-call sizing function returns for the same
+    shape, for every op, and 0 for an unknown op or a rejected shape."""
+    from paper_2412_09282_amd import crvq as C
+    for n, d, K in [(1, 8, 1), (8192, 8, 256), (2097152, 8, 65536), (300, 5, 2000), (70001, 16, 4096)]:
+        assert C.crvq_workspace_size("assign", n_vectors=n, d=d, K=K) == L.crvq_assign_workspace_size(n, d, K) > 0
+        assert C.crvq_workspace_size("kmeans", n_vectors=n, d=d, K=K) == L.crvq_kmeans_workspace_size(n, d, K)
+        if K <= 1024:
+            assert C.crvq_workspace_size("code_sums", n_vectors=n, d=d, K=K) == \
+                L.crvq_code_sums_workspace_size(n, d, K) > 0
+    Ks = [65536, 256, 256]
+    arr = (ctypes.c_int64 * 3)(*Ks)
+    for beam in (1, 4, 16):
+        assert C.crvq_workspace_size("beam", n_vectors=65536, d=8, Ks=Ks, beam=beam) == \
+            L.crvq_beam_workspace_size(65536, 8, 3, ctypes.cast(arr, ctypes.c_void_p), beam) > 0
+    assert C.crvq_workspace_size("beam", n_vectors=100, d=8, Ks=Ks, beam=17) == 0
+    assert C.crvq_workspace_size("importance", M=28672, N=8192) == L.crvq_importance_workspace_size(28672, 8192) > 0
+    assert C.crvq_workspace_size("reorder", N=13824) == L.crvq_reorder_workspace_size(13824) > 0
+    assert C.crvq_workspace_size("dequant", N=8192) == L.crvq_dequant_workspace_size(8192) > 0
+    assert C.crvq_workspace_size("refine", M=300, N=2056, n_cols=64) == L.crvq_refine_workspace_size(300, 2056, 64) > 0
+    assert C.crvq_workspace_size("gemv", M=11008, N=4096, K=256) == L.crvq_gemv_workspace_size(11008, 4096, 256) > 0
+    assert L.crvq_workspace_size(99, 100, 16, 1, 1, 8, None, 1, 1, 1) == 0
+    assert C.crvq_workspace_size("assign", n_vectors=100, d=8, K=65537) == 0

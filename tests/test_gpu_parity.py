@@ -205,6 +205,58 @@ def test_dequant_reverse_reorder_rows(M, N, dtype, n_ext, n_crit):
     np.testing.assert_array_equal(to_host_bits(out), oracle.scatter_columns(Rs, perm))
 
 
+@pytest.mark.parametrize("M,N,dtype,n_ext,n_crit,K_ext", [(4100, 8192, "f32", 1, 168, 65536),
+                                                           (3077, 8192, "f32", 2, 200, 256),
+                                                           (2600, 13824, "bf16", 1, 696, 256)])
+def test_dequant_reverse_reorder_many_rows(M, N, dtype, n_ext, n_crit, K_ext):
+    """Reverse-reorder reconstruction of more rows than the kernel keeps resident workgroups (several
+    rows per workgroup), compared in full: the 70B MLP width with a K = 65536 extended book, two
+    extended books, and the 13B down-projection width in bf16."""
+    say(f"dequant reverse reorder, many rows: M={M} N={N} {dtype} ext={n_ext}x{K_ext} n_crit={n_crit}")
+    d = 8
+    ncv = n_crit // d
+    g = np.random.default_rng(61)
+    Cb = rv(65536, d, 62)
+    Ce = [rv(K_ext, d, 63 + e, 0.005) for e in range(n_ext)]
+    if dtype == "bf16":
+        Cb = inputs.f32_to_bf16_bits(Cb)
+    qb = g.integers(0, 65536, (M, N // d)).astype(np.int32)
+    qe = [g.integers(0, K_ext, (M, ncv)).astype(np.int32) for _ in range(n_ext)]
+    perm = g.permutation(N).astype(np.int32)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    out = torch.empty(M, N, dtype=tdt, device="cuda")
+    C.crvq_dequant(M, N, d, dev(qb.ravel()), N // d, dev(Cb, dtype), out, n_crit=n_crit,
+                   q_ext=[dev(q.ravel()) for q in qe], ldq_ext=ncv, C_ext=[dev(c) for c in Ce], perm=dev(perm))
+    torch.cuda.synchronize()
+    crit = opipe.crit_mask(M, N, d, n_crit)
+    codes = [qb.ravel()]
+    for q in qe:
+        z = np.zeros((M, N // d), np.int32)
+        z[:, :ncv] = q
+        codes.append(z.ravel())
+    R = oracle.reconstruct(codes, [Cb] + Ce, crit, [dtype] + ["f32"] * n_ext)
+    Rs = oracle.round_to(R, dtype).reshape(M, N)
+    np.testing.assert_array_equal(to_host_bits(out), oracle.scatter_columns(Rs, perm))
+
+
+def test_assign_rows_with_nan_elements():
+    """Inputs must be finite; a row holding a NaN still gets an in-range code (0) and a NaN distance,
+    and every other row the oracle's result, on each search variant (small book, generic screen,
+    long-book two-screen path)."""
+    for n, K in [(5000, 256), (3000, 1000), (70000, 65536)]:
+        say(f"assign with NaN rows n={n} K={K}")
+        V = rv(n, 8, 71)
+        Cb = rv(K, 8, 72)
+        bad = np.array([0, 17, n // 2, n - 1])
+        V[bad, 3] = np.nan
+        got, gd = run_assign(V, Cb)
+        assert (got[bad] == 0).all() and np.isnan(gd[bad]).all()
+        ok = np.setdiff1d(np.arange(n), bad)
+        exp, ed = oracle.assign(V[ok], Cb)
+        np.testing.assert_array_equal(got[ok], exp)
+        np.testing.assert_array_equal(gd[ok], ed.astype(np.float32))
+
+
 @pytest.mark.parametrize("M,N,dtype,mode", [(513, 300, "f32", "sum"), (64, 1000, "f32", "max"),
                                             (1000, 96, "bf16", "sum"), (200, 77, "f32", "maxB"),
                                             (4096, 4096, "f32", "sum")])

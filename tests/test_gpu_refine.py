@@ -53,13 +53,16 @@ def test_hessian_product(M, N, n_out):
     H = X.T @ X
     Gt = torch.empty(M, n_out, dtype=torch.float64, device="cuda")
     loss = torch.empty(M, dtype=torch.float64, device="cuda") if n_out == N else None
-    C.crvq_hessian_product(torch.from_numpy(R).cuda(), torch.from_numpy(H).cuda(), Gt, loss)
+    total = torch.empty(1, dtype=torch.float64, device="cuda") if n_out == N else None
+    C.crvq_hessian_product(torch.from_numpy(R).cuda(), torch.from_numpy(H).cuda(), Gt, loss, total)
     torch.cuda.synchronize()
     exp = R @ H[:, :n_out]
     assert (np.abs(host(Gt) - exp) <= TOL * (np.abs(R) @ np.abs(H[:, :n_out])) + 1e-300).all()
     if loss is not None:
         el = np.sum(R * exp, axis=1)
-        assert (np.abs(host(loss) - el) <= TOL * np.sum(np.abs(R) * (np.abs(R) @ np.abs(H)), axis=1)).all()
+        terms = np.sum(np.abs(R) * (np.abs(R) @ np.abs(H)), axis=1)
+        assert (np.abs(host(loss) - el) <= TOL * terms).all()
+        assert abs(float(host(total)[0]) - el.sum()) <= TOL * terms.sum()
 
 
 @pytest.mark.parametrize("M,N,d,cover,K", [(64, 256, 8, 256, 256), (300, 512, 8, 40, 1000), (17, 64, 16, 64, 7),
@@ -124,7 +127,11 @@ def refine_case(M, N, d, K, n_cols, c_dtype, seed):
 
 @pytest.mark.parametrize("M,N,d,K,n_cols,c_dtype", [(37, 256, 8, 64, 256, "f32"), (64, 256, 8, 256, 32, "f32"),
                                                    (20, 128, 16, 50, 128, "f32"), (33, 96, 8, 16, 96, "bf16"),
-                                                   (9, 64, 4, 1024, 64, "f32")])
+                                                   (9, 64, 4, 1024, 64, "f32"),
+                                                   # few output tiles, long k: S = R H[:, :n_cols] split over k
+                                                   # into parts (ragged last part, M and n_cols not multiples
+                                                   # of the 128 x 128 tile)
+                                                   (300, 2056, 8, 256, 64, "f32"), (130, 2049, 1, 64, 48, "f32")])
 def test_refine_codes(M, N, d, K, n_cols, c_dtype):
     say(f"refine codes {M}x{N} d={d} K={K} cols={n_cols} {c_dtype}")
     R, H, Cb, codes = refine_case(M, N, d, K, n_cols, c_dtype, M + K)
@@ -210,6 +217,8 @@ def test_refine_loop_lockstep():
             R = ci["R"].numpy()
             G = co["G"].numpy()
             assert (np.abs(G - R @ H) <= TOL * (np.abs(R) @ np.abs(H)) + 1e-300).all()
+            terms = np.sum(np.abs(R) * (np.abs(R) @ np.abs(H)))
+            assert abs(float(co["loss_total"].numpy()[0]) - np.sum(R * (R @ H))) <= TOL * terms
         elif name.startswith("refine"):
             Ro = ci["R"].numpy().copy()
             qo = ci["codes"].numpy().copy()

@@ -160,6 +160,19 @@ def test_two_pass_screen(case):
         check(V, Cb)
 
 
+def test_second_screen_own_rows_full():
+    """From 2^23 rows up the second (split) screen of fp32 rows gives every wave rows of its own
+    instead of sharing them across a workgroup.  Every row of a (2^23 + 37)-row search against 4096
+    codewords drawn next to the rows (so several percent of the rows reach the second screen) is
+    compared with the oracle."""
+    n, K, d = (1 << 23) + 37, 4096, 8
+    say(f"two-pass screen fp32 n={n} K={K}: second screen with rows per wave, full comparison")
+    g = np.random.default_rng(51)
+    V = rv(n, d, 52)
+    Cb = np.ascontiguousarray(V[g.choice(n, K, replace=False)] + rv(K, d, 53, 0.002))
+    check(V, Cb)
+
+
 def test_rescue_of_most_rows():
     """Rows equal to codewords that the book holds four times (exact ties on every row, so nearly every
     row reaches the exact rescue) over 1,048,579 rows: more listed rows than the parted rescue has

@@ -585,3 +585,21 @@ def test_bits_two_basic_books():
     a, b = oracle.bits_per_weight_vq(1, 8, 8), oracle.bits_per_weight_vq(2, 8, 16)
     assert 1.0 < a < b < 1.01
     assert oracle.bits_per_weight_crvq(5, 8, 16, 0.02, m_base=2) > b
+
+
+def test_critical_column_counts_of_the_workloads():
+    """n_crit = d * ceil(lambda N / d) (at least lambda N columns, whole groups) gives the critical
+    column counts of the five workloads: 2 % of 256, 3 % and 5 % of 4096, 2 % of 8192, 5 % of 5120 and
+    5 % of 13824.  Rounding lambda N / d to the nearest group instead would give 8, 120, 208, 160, 256
+    and 688, so the ceiling is what these pin; the input generator's copy must agree."""
+    from paper_2412_09282_amd import inputs
+    cases = [(256, 0.02, 8), (4096, 0.03, 128), (4096, 0.05, 208), (8192, 0.02, 168), (5120, 0.05, 256),
+             (13824, 0.05, 696)]
+    for N, lam, want in cases:
+        assert oracle.n_crit_columns(N, 8, lam) == want, (N, lam)
+        assert inputs.n_crit_columns(N, 8, lam) == want, (N, lam)
+        assert want >= lam * N and want - 8 < lam * N and want % 8 == 0
+    assert oracle.n_crit_columns(64, 8, 1.0) == 64 and oracle.n_crit_columns(64, 8, 0.0) == 0
+    for wid, wl in inputs.WORKLOADS.items():
+        for L in wl.layers:
+            assert inputs.n_crit_columns(L.N, wl.d, wl.crit_frac) == oracle.n_crit_columns(L.N, wl.d, wl.crit_frac)

@@ -128,6 +128,25 @@ crvq_status crvq_assign(const void* X, int x_dtype, int64_t n_rows, int64_t vecs
                         void* workspace, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * crvq_assign_noalloc -- crvq_assign for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same arguments and results without a workspace.  Its
+ * scratch is a fixed array of CRVQ_NOALLOC_SCRATCH_BYTES inside the library's
+ * device memory, one per GPU, held until the process ends; the call allocates
+ * nothing.  A request whose crvq_assign_workspace_size(n, d, K) exceeds that
+ * size returns CRVQ_ERR_UNSUPPORTED before anything is enqueued (128 MiB holds
+ * about 4 million vectors against 65536 codewords).  Every call on a GPU
+ * shares that GPU's array: calls that overlap on one GPU (on different
+ * streams or from different threads) race and must be ordered by the caller;
+ * calls on one stream are ordered already.  The array's contents left by one
+ * call are never read by the next (every counter is reset by the call).
+ */
+#define CRVQ_NOALLOC_SCRATCH_BYTES (128LL << 20)
+crvq_status crvq_assign_noalloc(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                                int32_t d, const void* C, int c_dtype, int64_t K, int32_t* codes, float* dist,
+                                void* stream);
+
+/* ---------------------------------------------------------------------------
  * crvq_assign_residual_beam -- joint code choice over additive codebooks by
  * beam search (Sec. 3.1 last paragraph; Sec. 4.3; Alg. 1 BeamSearchOptimize),
  * under the squared Euclidean error of the residual.

@@ -55,6 +55,8 @@ def lib(build_if_missing: bool = True):
                 "crvq_reorder": ([P, I64, P, I64, ctypes.c_int, I64, I64, P, P, ctypes.c_int, P, SZ, P], ctypes.c_int),
                 "crvq_assign_workspace_size": ([I64, I32, I64], SZ),
                 "crvq_assign": ([P, ctypes.c_int, I64, I64, I64, I32, P, ctypes.c_int, I64, P, P, P, SZ, P], ctypes.c_int),
+                "crvq_assign_noalloc": ([P, ctypes.c_int, I64, I64, I64, I32, P, ctypes.c_int, I64, P, P, P],
+                                        ctypes.c_int),
                 "crvq_beam_workspace_size": ([I64, I32, I32, P, I32], SZ),
                 "crvq_assign_residual_beam": ([P, ctypes.c_int, I64, I64, I64, I32, I32, PP, P, P, I32, PP, P, P, P, SZ, P],
                                               ctypes.c_int),
@@ -202,6 +204,14 @@ def crvq_assign(X: VecSet, C: torch.Tensor, codes: torch.Tensor, dist: Optional[
     ws = _workspace(L.crvq_assign_workspace_size(X.n, X.d, K), C.device)
     _check("crvq_assign", L.crvq_assign(*X.args(), _ptr(C), dtype_code(C), K, _ptr(codes), _ptr(dist), _ptr(ws),
                                         0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def crvq_assign_noalloc(X: VecSet, C: torch.Tensor, codes: torch.Tensor, dist: Optional[torch.Tensor] = None,
+                        stream=None) -> None:
+    """crvq_assign on the library's fixed per-GPU scratch: no workspace is allocated."""
+    K = C.shape[0]
+    _check("crvq_assign_noalloc", lib().crvq_assign_noalloc(*X.args(), _ptr(C), dtype_code(C), K, _ptr(codes),
+                                                            _ptr(dist), _stream(stream)))
 
 
 def crvq_assign_residual_beam(X: VecSet, books: Sequence[torch.Tensor], beam: int, codes: Sequence[torch.Tensor],

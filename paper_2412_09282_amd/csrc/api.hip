@@ -7,9 +7,15 @@
 
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 using namespace crvq;
+
+// Scratch of crvq_assign_noalloc: one array per GPU in the library's own device memory, kept until
+// the process ends.  In host code `scratch` names a host-side stand-in, never the device array: its
+// device address comes from hipGetSymbolAddress, once per device (scratch_on_device below).
+static __device__ __align__(256) unsigned char scratch[CRVQ_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -224,6 +230,62 @@ crvq_status crvq_assign(const void* X, int x_dtype, int64_t n_rows, int64_t vecs
   RowSrc src = vec_src(X, x_dtype, n_rows, vecs_per_row, ld, d);
   ScreenPlan p = plan_screen(n, d, K, 1);
   WsCursor c(workspace);
+  ScreenWs w = carve_screen(c, p, n, K);
+  return hip_status(launch_screen(src, C, c_dtype, K, 1, p, w, codes, dist, nullptr, nullptr,
+                                  static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
+// ------------------------------------------------------------------------------------------------
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// The device address of `scratch` on the current device (looked up on the first call there).
+crvq_status scratch_on_device(void** out, const char* fn) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e, fn);
+  if (dev < 0 || dev >= kMaxDevices) return fail(CRVQ_ERR_UNSUPPORTED, "%s: device %d beyond %d", fn, dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, fn);
+    if (!p) return fail(CRVQ_ERR_HIP, "%s: no device address for the scratch array on device %d", fn, dev);
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return CRVQ_OK;
+}
+
+}  // namespace
+
+crvq_status crvq_assign_noalloc(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
+                                int32_t d, const void* C, int c_dtype, int64_t K, int32_t* codes, float* dist,
+                                void* stream) {
+  static const char* fn = "crvq_assign_noalloc";
+  g_err.clear();
+  crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
+  if (s) return s;
+  if (!dtype_ok(c_dtype)) return fail(CRVQ_ERR_INVALID, "%s: c_dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, c_dtype);
+  if ((s = check_K(K, fn, "K"))) return s;
+  if (!C) return fail(CRVQ_ERR_INVALID, "%s: C must not be NULL", fn);
+  const int64_t n = n_rows * vecs_per_row;
+  if (n > 0 && !codes) return fail(CRVQ_ERR_INVALID, "%s: codes must not be NULL", fn);
+  if (n == 0) return CRVQ_OK;
+  const size_t need = assign_ws(n, d, K);
+  if (need > static_cast<size_t>(CRVQ_NOALLOC_SCRATCH_BYTES))
+    return fail(CRVQ_ERR_UNSUPPORTED, "%s: %lld vectors against %lld codewords need %zu bytes of scratch, beyond the "
+                "fixed %lld (use crvq_assign with a workspace)", fn, (long long)n, (long long)K, need,
+                (long long)CRVQ_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((s = scratch_on_device(&ws, fn))) return s;
+  RowSrc src = vec_src(X, x_dtype, n_rows, vecs_per_row, ld, d);
+  ScreenPlan p = plan_screen(n, d, K, 1);
+  WsCursor c(ws);
   ScreenWs w = carve_screen(c, p, n, K);
   return hip_status(launch_screen(src, C, c_dtype, K, 1, p, w, codes, dist, nullptr, nullptr,
                                   static_cast<hipStream_t>(stream)),

@@ -81,6 +81,7 @@ struct ScreenPlan {
   int split;         // 1: split-bf16 MFMA screen (d <= 8), 0: fp32 MFMA screen
   int chunk;         // top-1: tiles per tracking chunk (1 = single tiles)
   int s32;           // 1: top-1 screen on 32 x 32 split-fp16 tiles (tiles then count 32 codewords)
+  int prune;         // 1 (s32 only): codebook and rows in key order, certified chunk skipping
   int64_t tiles;     // 16-codeword tiles (ceil(K / 16))
   int64_t grid_x;    // row groups
   int splits;        // codebook splits (grid y)
@@ -103,6 +104,17 @@ struct ScreenWs {
   int* rlist2;   // 32 x 32 screen on inexact operands: rows that failed the second screen too, [n_rows
                  // rounded up to 256]; first the per-block slices of the first screen's failures
   int* bcount;   // their per-block counts, then the blocks' offsets, [2 x blocks of 256 rows]
+  // pruned screen (prune): key order of codewords and rows, chunk ranges, binning parameters
+  int* corder;   // sorted codeword position -> codeword [tiles x 32]
+  int* ckey;     // codeword keys [K]
+  int* coff;     // first sorted position of every key [32768]
+  int* hist;     // key counts then cursors, codewords [32768] and rows [32768]
+  uint4* cbnd;   // chunk ranges [tiles / 2]
+  uint32_t* cminS;
+  uint32_t* cmaxP;
+  float* prm;    // binning parameters and the scaled largest codeword norm [4]
+  int* rkey;     // row keys [n_rows]
+  int* rord;     // rows in key order [n_rows]
 };
 // Carves the screen's scratch out of `ws`; returns it (pointers null on a dry run).
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc);

@@ -68,6 +68,9 @@
 #ifndef CRVQ_S32_SCHED
 #define CRVQ_S32_SCHED 1  // pin the MFMA / VALU interleave of the 32 x 32 screen
 #endif
+#ifndef CRVQ_PRUNE
+#define CRVQ_PRUNE 1  // certified chunk skipping in the first long top-1 screen (norm and coordinate bands)
+#endif
 
 namespace crvq {
 namespace {
@@ -719,6 +722,417 @@ constexpr int64_t kS32SharedRowsMaxN = int64_t{1} << 23;  // second screen: shar
 constexpr int kS32TileHalves = 768;  // packed fp16 per tile: c1, c2, N terms, 32 x 8 each
 constexpr int kS32MaxParts = 256;    // partial maxima of the codebook scale reduction
 
+// ------------------------------------------------------------------------------------------------
+// Certified tile skipping for the long top-1 screen.  For any codeword c and row x, both
+//   | ||x|| - ||c|| | <= ||x - c||   and   | x_j - c_j | <= ||x - c||   (one coordinate j),
+// so once a row's best distance is known to be at most D_up, a codeword whose norm or coordinate j
+// lies further than sqrt(D_up) from the row's can neither win nor tie.  Codewords are packed in the
+// order of a key (norm bin major, bin of coordinate j minor), rows are screened in the order of the
+// same key, and each wave keeps, per pair of tiles ("chunk" of 64 codewords), the range of the
+// codewords' norms and coordinate j: a chunk outside every row's band is skipped.  D_up comes from
+// the wave's running screen minimum m:  D(c_m) <= m / alpha^2 + ||x||^2 + delta, delta the screen's
+// error bound taken with R = the largest codeword norm.  Every quantity is in units of the codebook
+// scale alpha (exact powers of two), rounded outward, so the test is conservative; a skipped
+// codeword is strictly worse than the kept chunk's exact winner, so the certificate and the results
+// are those of the full screen.
+constexpr int kPruneBins1 = 128;               // norm bins (major key)
+constexpr int kPruneBins2 = 128;               // coordinate bins (minor key)
+constexpr int kPruneKeys = kPruneBins1 * kPruneBins2;
+constexpr int64_t kPruneMinRows = 32768;       // rows from which the screen is pruned
+
+struct PruneData {
+  const int* corder;        // sorted codeword position -> codeword
+  const int* coff;          // first sorted position of every key
+  const uint4* cbnd;        // per chunk: ordered keys of {min, max} scaled norm, {min, max} scaled c_j
+  const uint32_t* cminS;    // suffix minimum over chunks of the norm minimum key
+  const uint32_t* cmaxP;    // prefix maximum over chunks of the norm maximum key
+  const int* rord;          // rows in key order
+  const int* rkey;          // key of every row
+  const float* prm;         // {max ||c||, min c_j, max c_j, scaled max ||c|| rounded up}
+  int jp;                   // the coordinate j
+};
+
+// Order-preserving map of a float (both zeros to the same key) to an unsigned integer, so that wave
+// uniform comparisons run on the scalar unit.
+__device__ __forceinline__ uint32_t okey(float f) {
+  const uint32_t u = (f == 0.0f) ? 0u : __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float okey_inv(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+// float just below / above a non-negative double
+__device__ __forceinline__ float f32_down(double x) {
+  float f = static_cast<float>(x);
+  if (static_cast<double>(f) > x) f = (f > 0.0f) ? __uint_as_float(__float_as_uint(f) - 1u) : -__uint_as_float(1u);
+  return f;
+}
+__device__ __forceinline__ float f32_up(double x) {
+  float f = static_cast<float>(x);
+  if (static_cast<double>(f) < x) f = (f >= 0.0f) ? __uint_as_float(__float_as_uint(f) + 1u) : -0.0f;
+  return f;
+}
+
+__device__ __forceinline__ int prune_key(float nrm, float xj, const float (&prm)[3]) {
+  float f1 = nrm * (static_cast<float>(kPruneBins1) / fmaxf(prm[0], 0x1p-126f));
+  f1 = fminf(fmaxf(f1, 0.0f), static_cast<float>(kPruneBins1 - 1));
+  const float span = prm[2] - prm[1];
+  float f2 = (span > 0.0f) ? (xj - prm[1]) * (static_cast<float>(kPruneBins2) / span) : 0.0f;
+  f2 = fminf(fmaxf(f2, 0.0f), static_cast<float>(kPruneBins2 - 1));
+  return static_cast<int>(f1) * kPruneBins2 + static_cast<int>(f2);
+}
+
+constexpr int kPruneTile = 4096;  // vectors per block of the key counting and scatter
+constexpr int kPruneParts = 256;  // partial blocks of the binning ranges
+
+// Partial binning ranges of the codebook (max norm, min and max of coordinate j) over a strided
+// share of the codewords, and (every block a share) the cleared key counts of codewords and rows.
+__global__ __launch_bounds__(256) void prune_stats_partial(const void* __restrict__ C, int ct, int64_t K, int d,
+                                                           int jp, float* __restrict__ part, int* __restrict__ hist2) {
+  __shared__ float s_mx[256], s_lo[256], s_hi[256];
+  const int tid = threadIdx.x;
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + tid; e < 2 * kPruneKeys; e += gridDim.x * 256) hist2[e] = 0;
+  float mx = 0.0f, lo = __builtin_inff(), hi = -__builtin_inff();
+  for (int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + tid; k < K; k += static_cast<int64_t>(gridDim.x) * 256) {
+    float v[8];
+    if (ct == ET_F32)
+      load_f32_elems<8>(static_cast<const float*>(C) + k * d, d, true, v);
+    else
+      load_bf16_elems<8>(static_cast<const uint16_t*>(C) + k * d, d, true, v);
+    float n2 = 0.0f, cj = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      n2 = n2 + v[t] * v[t];
+      cj = (t == jp) ? v[t] : cj;
+    }
+    mx = fmaxf(mx, sqrtf(n2));
+    lo = fminf(lo, cj);
+    hi = fmaxf(hi, cj);
+  }
+  s_mx[tid] = mx;
+  s_lo[tid] = lo;
+  s_hi[tid] = hi;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (tid < w) {
+      s_mx[tid] = fmaxf(s_mx[tid], s_mx[tid + w]);
+      s_lo[tid] = fminf(s_lo[tid], s_lo[tid + w]);
+      s_hi[tid] = fmaxf(s_hi[tid], s_hi[tid + w]);
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    part[blockIdx.x] = s_mx[0];
+    part[kPruneParts + blockIdx.x] = s_lo[0];
+    part[2 * kPruneParts + blockIdx.x] = s_hi[0];
+  }
+}
+
+// Every block folds the partial ranges (the first one also publishes them to prm[0..2]).
+__device__ __forceinline__ void prune_fold_ranges(const float* __restrict__ part, int nparts, float* __restrict__ prm,
+                                                  float (&r)[3]) {
+  __shared__ float s_r[3][256];
+  const int tid = threadIdx.x;
+  s_r[0][tid] = tid < nparts ? part[tid] : 0.0f;
+  s_r[1][tid] = tid < nparts ? part[kPruneParts + tid] : __builtin_inff();
+  s_r[2][tid] = tid < nparts ? part[2 * kPruneParts + tid] : -__builtin_inff();
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (tid < w) {
+      s_r[0][tid] = fmaxf(s_r[0][tid], s_r[0][tid + w]);
+      s_r[1][tid] = fminf(s_r[1][tid], s_r[1][tid + w]);
+      s_r[2][tid] = fmaxf(s_r[2][tid], s_r[2][tid + w]);
+    }
+    __syncthreads();
+  }
+  r[0] = s_r[0][0];
+  r[1] = s_r[1][0];
+  r[2] = s_r[2][0];
+  if (blockIdx.x == 0 && tid == 0) {
+    prm[0] = r[0];
+    prm[1] = r[1];
+    prm[2] = r[2];
+  }
+}
+
+// Key of vector i of src (the rows, or the codewords as a set of K rows).
+__device__ __forceinline__ int prune_vec_key(const RowSrc& src, int64_t i, int jp, const float (&r)[3]) {
+  float v[8];
+  const int64_t off = row_offset(src, i);
+  if (src.type == ET_F32)
+    load_f32_elems<8>(static_cast<const float*>(src.base) + off, src.d, true, v);
+  else
+    load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, src.d, true, v);
+  float n2 = 0.0f, xj = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    n2 = n2 + v[t] * v[t];
+    xj = (t == jp) ? v[t] : xj;
+  }
+  return prune_key(sqrtf(n2), xj, r);
+}
+
+// Keys of kPruneTile vectors per block, counted in LDS, the block's nonzero counts added to the
+// global counts (one integer atomic per key present in the block).
+__global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, const float* __restrict__ part,
+                                                          int nparts, float* __restrict__ prm, int* __restrict__ keys,
+                                                          int* __restrict__ hist) {
+  __shared__ int h[kPruneKeys];
+  float r[3];
+  prune_fold_ranges(part, nparts, prm, r);
+  const int tid = threadIdx.x;
+  for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
+  __syncthreads();
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
+  for (int q = 0; q < kPruneTile / 256; ++q) {
+    const int64_t i = i0 + q * 256 + tid;
+    if (i < src.n) {
+      const int key = prune_vec_key(src, i, jp, r);
+      keys[i] = key;
+      atomicAdd(h + key, 1);
+    }
+  }
+  __syncthreads();
+  for (int b = tid; b < kPruneKeys; b += 256)
+    if (h[b]) atomicAdd(hist + b, h[b]);
+}
+
+// Exclusive prefix sums of the key counts, in place (the scatter's cursors), and a copy in off.
+__global__ __launch_bounds__(1024) void prune_scan_kernel(int* __restrict__ hist, int* __restrict__ off) {
+  __shared__ int sh[1024];
+  constexpr int kPer = kPruneKeys / 1024;
+  const int t = threadIdx.x;
+  int v[kPer];
+  int sum = 0;
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    v[q] = hist[t * kPer + q];
+    sum += v[q];
+  }
+  sh[t] = sum;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const int a = t >= o ? sh[t - o] : 0;
+    __syncthreads();
+    sh[t] += a;
+    __syncthreads();
+  }
+  int run = t > 0 ? sh[t - 1] : 0;
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    hist[t * kPer + q] = run;
+    if (off) off[t * kPer + q] = run;
+    run += v[q];
+  }
+}
+
+// order[...] = i in key order: ranks within the block from LDS counters, one global cursor advance
+// per key present in the block.  The order within a key is not fixed; results do not depend on it.
+__global__ __launch_bounds__(256) void prune_order_kernel(const int* __restrict__ keys, int64_t n,
+                                                          int* __restrict__ cursor, int* __restrict__ order) {
+  __shared__ int h[kPruneKeys];
+  const int tid = threadIdx.x;
+  for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
+  __syncthreads();
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
+  constexpr int kQ = kPruneTile / 256;
+  int key[kQ], rank[kQ];
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) {
+    const int64_t i = i0 + q * 256 + tid;
+    key[q] = i < n ? keys[i] : -1;
+    rank[q] = key[q] >= 0 ? atomicAdd(h + key[q], 1) : 0;
+  }
+  __syncthreads();
+  for (int b = tid; b < kPruneKeys; b += 256)
+    if (h[b]) h[b] = atomicAdd(cursor + b, h[b]);
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < kQ; ++q) {
+    const int64_t i = i0 + q * 256 + tid;
+    if (key[q] >= 0) {
+      const int pos = h[key[q]] + rank[q];
+      if (pos >= 0 && pos < n) order[pos] = static_cast<int>(i);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void prune_fill_kernel(int* __restrict__ p, int64_t n, int v) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Per chunk (sorted positions 64 c .. 64 c + 63, one wave): the range of alpha ||c|| (fp64, rounded
+// outward) and of alpha c_j (exact), as ordered keys; an empty chunk gets an empty range.
+__global__ __launch_bounds__(256) void prune_chunks_kernel(const void* __restrict__ C, int ct, int64_t K, int d, int jp,
+                                                           const int* __restrict__ corder, const float* __restrict__ alpha_p,
+                                                           int64_t nch, uint4* __restrict__ cbnd) {
+  const int lane = threadIdx.x & 63;
+  const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (c >= nch) return;  // whole waves
+  const double a = static_cast<double>(alpha_p[0]);
+  double lo1 = __builtin_inf(), hi1 = -__builtin_inf();
+  float lo2 = __builtin_inff(), hi2 = -__builtin_inff();
+  const int64_t q = 64 * c + lane;
+  const int64_t k = q < K ? corder[q] : -1;
+  if (k >= 0 && k < K) {
+    float v[8];
+    if (ct == ET_F32)
+      load_f32_elems<8>(static_cast<const float*>(C) + k * d, d, true, v);
+    else
+      load_bf16_elems<8>(static_cast<const uint16_t*>(C) + k * d, d, true, v);
+    double n2 = 0.0;
+    float cj = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      n2 = n2 + static_cast<double>(v[t]) * static_cast<double>(v[t]);
+      cj = (t == jp) ? v[t] : cj;
+    }
+    lo1 = hi1 = sqrt(n2) * a;
+    lo2 = hi2 = cj * static_cast<float>(a);  // exact: a power of two, alpha |c| < 2^12
+  }
+#pragma unroll
+  for (int sh = 1; sh < 64; sh <<= 1) {
+    const double o1 = __shfl_xor(lo1, sh), o2 = __shfl_xor(hi1, sh);
+    lo1 = o1 < lo1 ? o1 : lo1;
+    hi1 = o2 > hi1 ? o2 : hi1;
+    lo2 = fminf(lo2, __shfl_xor(lo2, sh));
+    hi2 = fmaxf(hi2, __shfl_xor(hi2, sh));
+  }
+  if (lane == 0) {
+    uint4 b;
+    b.x = okey(lo1 <= hi1 ? f32_down(lo1) : __builtin_inff());
+    b.y = okey(lo1 <= hi1 ? f32_up(hi1) : -__builtin_inff());
+    b.z = okey(lo2);
+    b.w = okey(hi2);
+    cbnd[c] = b;
+  }
+}
+
+// Envelopes for the wave's stop tests (suffix minimum of the norm minima, prefix maximum of the
+// norm maxima) and the largest scaled codeword norm (rounded up) for the screen bound.
+__global__ __launch_bounds__(1024) void prune_envelope_kernel(const uint4* __restrict__ cbnd, int nch,
+                                                              uint32_t* __restrict__ cminS, uint32_t* __restrict__ cmaxP,
+                                                              float* __restrict__ prm) {
+  __shared__ uint32_t smin[1024], smax[1024];
+  const int t = threadIdx.x;
+  const uint4 b = t < nch ? cbnd[t] : make_uint4(0xffffffffu, 0u, 0u, 0u);
+  smin[t] = b.x;  // suffix min: scan from the end
+  smax[t] = b.y;
+  __syncthreads();
+  for (int o = 1; o < 1024; o <<= 1) {
+    const uint32_t a = (t + o < 1024) ? smin[t + o] : 0xffffffffu;
+    const uint32_t c = (t >= o) ? smax[t - o] : 0u;
+    __syncthreads();
+    smin[t] = smin[t] < a ? smin[t] : a;
+    smax[t] = smax[t] > c ? smax[t] : c;
+    __syncthreads();
+  }
+  if (t < nch) {
+    cminS[t] = smin[t];
+    cmaxP[t] = smax[t];
+  }
+  if (t == 0) prm[3] = fmaxf(okey_inv(smax[nch - 1]), 0.0f);
+}
+
+// The wave's walk over the chunks: two lists in LDS, the chunks above the start in ascending order
+// (U) and those below it in descending order (D), consumed alternately (U[ui], D[di], ...).  After
+// each narrowing of the bands the unvisited rest of each list is filtered in place, one chunk per
+// lane: a chunk leaves it when outside a band, and a list ends at the first chunk past its side's
+// envelope (every later chunk of that side is outside too).  The positions, lengths and bands are
+// wave-uniform scalars; taking a chunk is one LDS read.
+struct PruneCursor {
+  int ui, un, di, dn, turn;
+  uint32_t lo1, hi1, lo2, hi2;
+};
+
+__device__ __forceinline__ uint32_t rfl(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ bool prune_keep(const uint4& b, const PruneCursor& s) {
+  return !((b.y < s.lo1) | (b.x > s.hi1) | (b.w < s.lo2) | (b.z > s.hi2));
+}
+
+// L[i0 .. n) filtered under the current bands into L[0 ..); returns the new length.
+__device__ __forceinline__ int prune_filter(uint16_t* L, int i0, int n, bool up, const PruneCursor& s,
+                                            const PruneData& pd, int lane) {
+  int w = 0;
+  for (int b = i0; b < n; b += 64) {
+    const int i = b + lane;
+    int c = 0;
+    bool keep = false, end = false;
+    if (i < n) {
+      c = L[i];
+      const uint32_t env = up ? pd.cminS[c] : pd.cmaxP[c];
+      const uint4 bd = pd.cbnd[c];
+      end = up ? (env > s.hi1) : (env < s.lo1);
+      keep = !end & prune_keep(bd, s);
+    }
+    const uint64_t em = __ballot(end);
+    uint64_t km = __ballot(keep);
+    if (em) km &= (uint64_t{1} << __builtin_ctzll(em)) - 1ull;  // nothing from the first end on
+    const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+    if ((km >> lane) & 1ull) L[w + __popcll(km & lt)] = static_cast<uint16_t>(c);
+    w += __popcll(km);
+    if (em) break;
+  }
+  return static_cast<int>(rfl(static_cast<uint32_t>(w)));
+}
+
+// The next chunk to screen, or -1 when both lists are exhausted.
+__device__ __forceinline__ int prune_take(PruneCursor& s, const uint16_t* U, const uint16_t* D) {
+  if (s.ui < s.un && (s.turn == 0 || s.di >= s.dn)) {
+    s.turn = 1;
+    return static_cast<int>(rfl(U[s.ui++]));
+  }
+  if (s.di < s.dn) {
+    s.turn = 0;
+    return static_cast<int>(rfl(D[s.di++]));
+  }
+  return -1;
+}
+
+// New bands from the rows' running minima m (each lane: the rows of its column blocks, both lane
+// halves of a row hold its two halves of every tile); band terms of row (cb, j) at sb[cb * 96 + k * 32 + j].
+template <int CB>
+__device__ __forceinline__ void prune_band(PruneCursor& s, const float (&m)[CB], const float* sb, int j) {
+  float lo1 = __builtin_inff(), hi1 = -__builtin_inff(), lo2 = __builtin_inff(), hi2 = -__builtin_inff();
+  bool open = false;
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const float mr = fminf(m[cb], __shfl_xor(m[cb], 32));
+    const float A = sb[cb * 96 + j], P = sb[cb * 96 + 32 + j], B = sb[cb * 96 + 64 + j];
+    if (B >= 0.0f) {
+      if (!(mr < __builtin_inff())) {
+        open = true;
+      } else {
+        // every operation below errs by at most 2^-24 of its operands; the margins are 16x that
+        const float Dup = fmaxf((mr + B) + 0x1p-20f * (fabsf(mr) + B) + 0x1p-10f, 0.0f);
+        const float r = sqrtf(Dup) * (1.0f + 0x1p-20f);
+        const float s1 = 0x1p-20f * (A + r) + 0x1p-10f, s2 = 0x1p-20f * (fabsf(P) + r) + 0x1p-10f;
+        lo1 = fminf(lo1, (A - r) - s1);
+        hi1 = fmaxf(hi1, (A + r) + s1);
+        lo2 = fminf(lo2, (P - r) - s2);
+        hi2 = fmaxf(hi2, (P + r) + s2);
+      }
+    }
+  }
+  if (open) {
+    lo1 = lo2 = -__builtin_inff();
+    hi1 = hi2 = __builtin_inff();
+  }
+#pragma unroll
+  for (int sh = 1; sh < 64; sh <<= 1) {
+    lo1 = fminf(lo1, __shfl_xor(lo1, sh));
+    hi1 = fmaxf(hi1, __shfl_xor(hi1, sh));
+    lo2 = fminf(lo2, __shfl_xor(lo2, sh));
+    hi2 = fmaxf(hi2, __shfl_xor(hi2, sh));
+  }
+  s.lo1 = rfl(okey(lo1));
+  s.hi1 = rfl(okey(hi1));
+  s.lo2 = rfl(okey(lo2));
+  s.hi2 = rfl(okey(hi2));
+}
+
 // min(c, a[0..15]) as a depth-3 tree of eight v_min3
 __device__ __forceinline__ float min_fold16(float c, const f16v& a) {
   const float m0 = fminf(fminf(a[0], a[1]), a[2]);
@@ -766,6 +1180,7 @@ __device__ __forceinline__ float s32_alpha(float mx) {
 // Every block folds the partial maxima, block 0 publishes alpha; then thread k packs codeword k.
 __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict__ C, int ct, int64_t K, int d,
                                                          int64_t tiles, const float* __restrict__ part, int nparts,
+                                                         const int* __restrict__ corder,
                                                          uint16_t* __restrict__ apack, float* __restrict__ alpha_out,
                                                          int* __restrict__ rcount) {
   __shared__ float sh[256];
@@ -783,10 +1198,13 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
   }
   const int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (k >= tiles * kS32Tile) return;
+  // position k holds codeword corder[k] when the book is packed in key order
+  int64_t ks = (k < K) ? (corder ? static_cast<int64_t>(corder[k]) : k) : -1;
+  if (ks >= K) ks = -1;
   float c[8];
 #pragma unroll
   for (int t = 0; t < 8; ++t)
-    c[t] = (k < K && t < d) ? alpha * static_cast<float>(cb_elem(C, ct, k, d, t)) : 0.0f;
+    c[t] = (ks >= 0 && t < d) ? alpha * static_cast<float>(cb_elem(C, ct, ks, d, t)) : 0.0f;
   u16x8 p1, p2, pn;
   float N = 0.0f;
 #pragma unroll
@@ -797,7 +1215,7 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
     p2[t] = f16_bits(c[t] - f16_val(h1));
     pn[t] = 0;
   }
-  if (k < K) {
+  if (ks >= 0) {
     const float v = N * 0x1p-12f;
     const uint16_t n1 = f16_bits(v);
     const float r1 = v - f16_val(n1);
@@ -821,13 +1239,19 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
 // LIST: the rows are list[0 .. *list_n), and results go to their list positions (the second screen
 // of the rows the first one left uncertain).
 // QS (LIST only): the four waves of a block share their rows and split the codebook (few listed rows).
-template <int CB, int NC, bool ONE, bool LIST, bool QS = false>
+// PRUNE (first screen only): rows in key order (pd.rord), results at the rows' own indices, chunks
+// visited outward from the wave's key and skipped when outside every row's band (see PruneData).
+// corder (when the codebook is packed in key order): sorted position -> codeword.
+template <int CB, int NC, bool ONE, bool LIST, bool QS = false, bool PRUNE = false>
 __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_t* apack,
                                                        const float* __restrict__ alpha_p, int64_t tiles, int64_t tps,
                                                        const void* __restrict__ C, int ct, int64_t K,
                                                        float* __restrict__ pR, double* __restrict__ pD,
                                                        int* __restrict__ pK, double* __restrict__ xn2o,
-                                                       const int* __restrict__ list, const int* __restrict__ list_n) {
+                                                       const int* __restrict__ list, const int* __restrict__ list_n,
+                                                       const int* __restrict__ corder, PruneData pd, double bacc,
+                                                       double bsplit) {
+  static_assert(!PRUNE || (ONE && !LIST && !QS), "pruning is for the first screen");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int j = lane & 31;
@@ -847,6 +1271,10 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   __shared__ double sD[QS ? 4 : 1][QS ? 32 * CB : 1];
   __shared__ int sK[QS ? 4 : 1][QS ? 32 * CB : 1];
   __shared__ float sR[QS ? 4 : 1][QS ? 32 * CB : 1];
+  // PRUNE: per row alpha ||x||, alpha x_j and the scaled D_up offset (negative: the row takes no part);
+  // per wave the lists of chunks above and below its start
+  __shared__ float sBand[PRUNE ? 4 : 1][PRUNE ? CB : 1][3][32];
+  __shared__ uint16_t sList[PRUNE ? 4 : 1][2][PRUNE ? 1024 : 1];
 
   h8 b1[CB], b2[CB];
   bool forced[CB];
@@ -855,7 +1283,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     const int64_t i = row0 + cb * 32 + j;
     const bool ok = i < n;
     float v[8];
-    const int64_t off = ok ? row_offset(src, LIST ? list[i] : i) : 0;
+    const int64_t off = ok ? row_offset(src, LIST ? list[i] : (PRUNE ? pd.rord[i] : i)) : 0;
     if (src.type == ET_F32) {
       load_f32_elems<8>(static_cast<const float*>(src.base) + off, d, ok, v);
     } else if (src.type == ET_BF16) {
@@ -883,6 +1311,23 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     b1[cb] = __builtin_bit_cast(h8, p1);
     b2[cb] = __builtin_bit_cast(h8, p2);
     forced[cb] = over;
+    if (PRUNE && h == 0) {
+      // the row's band terms in units of alpha: ||x|| and x_j exactly (fp64), and
+      // D_up - m = alpha^2 ||x||^2 + alpha^2 delta(R = max ||c||), rounded up
+      double xn2 = 0.0, xj = 0.0;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        xn2 = xn2 + static_cast<double>(v[t]) * static_cast<double>(v[t]);
+        xj = (t == pd.jp) ? static_cast<double>(v[t]) : xj;
+      }
+      const double a = static_cast<double>(alpha);
+      const double An = sqrt(xn2) * a, cm = static_cast<double>(pd.prm[3]);
+      const double B = a * a * xn2 + bacc * 0x1p-24 * (cm * cm + 2.0 * An * cm) + bsplit * An * cm +
+                       0x1p-24 * 2.8285 * (cm + 2.0 * An) + 0x1p-12;
+      sBand[wave][cb][0][j] = static_cast<float>(An);
+      sBand[wave][cb][1][j] = static_cast<float>(xj * a);
+      sBand[wave][cb][2][j] = (ok && !over) ? f32_up(B) * (1.0f + 0x1p-20f) : -1.0f;
+    }
   }
 
   float m[CB], rest[CB], cm[CB];
@@ -951,9 +1396,56 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
         id[cb] = lt ? Ci : id[cb];
       }
     };
+    static_assert(NC == 1 || NC == 2, "chunks of one or two tiles");
+    static_assert(!PRUNE || NC == 2, "pruning works on chunks of two tiles");
+    if (PRUNE) {
+      // Chunks (tile pairs) from the wave's key outward, alternately above and below; a side stops
+      // where the envelope leaves the norm band, a chunk is skipped when outside either band.  The
+      // bands start open and narrow as the running minima fall (recomputed after 4, 8, 16, ...
+      // chunks).  All of this is wave-uniform control on the scalar unit.
+      const int c0 = static_cast<int>(t0 >> 1), c1 = static_cast<int>(t1 >> 1);
+      const int64_t mid = (row0 + 64 < n) ? row0 + 64 : n - 1;
+      // (readfirstlane: the wave index is uniform, which the compiler cannot see)
+      int cc = __builtin_amdgcn_readfirstlane(pd.coff[pd.rkey[pd.rord[mid]]] >> 6);
+      cc = cc < c0 ? c0 : (cc >= c1 ? c1 - 1 : cc);
+      PruneCursor cur = {0, c1 - cc, 0, cc - c0, 0, 0u, 0xffffffffu, 0u, 0xffffffffu};
+      uint16_t* Ul = &sList[wave][0][0];
+      uint16_t* Dl = &sList[wave][1][0];
+      for (int i = lane; i < cur.un; i += 64) Ul[i] = static_cast<uint16_t>(cc + i);
+      for (int i = lane; i < cur.dn; i += 64) Dl[i] = static_cast<uint16_t>(cc - 1 - i);
+      // The chunk after next is chosen at the end of an iteration, so the body (MFMAs, minimum
+      // folds, the next chunk's loads) stays straight-line; past the last chunk the loads repeat
+      // a valid tile and are not used.
+      h8 qa, qb;
+      int Cc = prune_take(cur, Ul, Dl);
+      int Cn = Cc >= 0 ? prune_take(cur, Ul, Dl) : -1;
+      if (Cc >= 0) {
+        load(2 * Cc, qa, qa);
+        load(2 * Cc + 1, qb, qb);
+      }
+      int done = 0, at = 4;
+      while (Cc >= 0) {
+        const int Tn = Cn >= 0 ? 2 * Cn : 2 * Cc;
+        tile(qa, qa, true);
+        load(Tn, qa, qa);
+        tile(qb, qb, false);
+        fold(2 * Cc);
+        load(Tn + 1, qb, qb);
+        if (++done == at) {
+          prune_band<CB>(cur, m, &sBand[wave][0][0][0], j);
+          // the chunk already taken for the next iteration stays; the rest is filtered
+          cur.un = prune_filter(Ul, cur.ui, cur.un, true, cur, pd, lane);
+          cur.dn = prune_filter(Dl, cur.di, cur.dn, false, cur, pd, lane);
+          cur.ui = 0;
+          cur.di = 0;
+          at = at < 128 ? 2 * at : at + 128;
+        }
+        Cc = Cn;
+        Cn = Cn >= 0 ? prune_take(cur, Ul, Dl) : -1;
+      }
+    } else {
     // Two tiles per iteration from two register sets; each set is refilled right after its MFMAs,
     // one iteration ahead of its next use.
-    static_assert(NC == 1 || NC == 2, "chunks of one or two tiles");
     h8 qa1, qa2, qb1, qb2;
     load(T0, qa1, qa2);
     load((T0 + 1 < T1) ? T0 + 1 : T1 - 1, qb1, qb2);
@@ -970,6 +1462,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       tile(qa1, qa2, true);
       fold(T);
     }
+    }
   }
 
   // The lane half with the smaller kept-chunk minimum wins the row; the other half's best chunk
@@ -979,7 +1472,9 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   for (int cb = 0; cb < CB; ++cb) {
     const int64_t i = row0 + cb * 32 + j;
     const bool valid = i < n;
-    const int64_t pi = (LIST && valid) ? list[i] : i;  // the row's index in the source
+    // the row's index in the source (where a first screen in key order writes its results)
+    const int64_t pi = (LIST && valid) ? list[i] : ((PRUNE && valid) ? pd.rord[i] : i);
+    const int64_t oi = PRUNE ? pi : i;
     const float mg = m[cb];
     const float om = __shfl_xor(mg, 32);
     const int hw = (om < mg || (om == mg && h == 1)) ? 1 - h : h;
@@ -1000,10 +1495,13 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
         const int64_t k0 = T * kS32Tile + 8 * (2 * h + q) + 4 * hw;
         float cw[4][8];
         bool ok[4];
+        int64_t ko[4];
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
           ok[s] = valid && Tw >= 0 && T < t1 && k0 + s < K;
-          load_codeword<8>(C, ct, k0 + s, d, ok[s], cw[s]);
+          ko[s] = (corder && ok[s]) ? static_cast<int64_t>(corder[k0 + s]) : k0 + s;
+          ok[s] = ok[s] && ko[s] >= 0 && ko[s] < K;
+          load_codeword<8>(C, ct, ko[s], d, ok[s], cw[s]);
         }
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
@@ -1016,7 +1514,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
                 Du = Du + diff * diff;
               }
             }
-            const int ku = static_cast<int>(k0 + s);
+            const int ku = static_cast<int>(ko[s]);
             if (cless(Du, ku, D, kk)) {
               D = Du;
               kk = ku;
@@ -1049,10 +1547,10 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
 #pragma unroll
       for (int t = 0; t < 8; ++t)
         if (t < d) xn2 = xn2 + xd[t] * xd[t];
-      pD[static_cast<int64_t>(split) * ns + i] = D;
-      pK[static_cast<int64_t>(split) * ns + i] = kk;
-      pR[static_cast<int64_t>(split) * ns + i] = rr;
-      if (split == 0) xn2o[i] = xn2;
+      pD[static_cast<int64_t>(split) * ns + oi] = D;
+      pK[static_cast<int64_t>(split) * ns + oi] = kk;
+      pR[static_cast<int64_t>(split) * ns + oi] = rr;
+      if (split == 0) xn2o[oi] = xn2;
     }
   }
   if (QS) {
@@ -2208,11 +2706,17 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
   // Long top-1 searches: 32 x 32 split-fp16 tiles (two MFMAs per 1024 values instead of four).
   // The same rows per workgroup and codebook splits, counted in 32-codeword tiles.
   p.s32 = (p.split && CRVQ_S32_SCREEN && p.nb == 1 && p.tiles_per_split >= CRVQ_S32_MIN_TILES) ? 1 : 0;
+  p.prune = 0;
   if (p.s32) {
     p.cb = CRVQ_S32_CB;
     p.grid_x = cdiv(n_rows, 128 * p.cb);
     p.tiles = cdiv(K, kS32Tile);
+    // many rows: codebook and rows in key order, chunks of two tiles skipped when certified useless
+    // (only without codebook splits: a split would see a slice of the key order and prune little)
+    p.prune = (CRVQ_PRUNE && CRVQ_S32_CHUNK == 2 && splits == 1 && n_rows >= kPruneMinRows) ? 1 : 0;
+    if (p.prune) p.tiles += p.tiles & 1;  // whole chunks; a padding tile never wins
     p.tiles_per_split = cdiv(p.tiles, splits);
+    if (p.prune) p.tiles_per_split += p.tiles_per_split & 1;
     p.splits = static_cast<int>(cdiv(p.tiles, p.tiles_per_split));
     p.chunk = CRVQ_S32_CHUNK;
   }
@@ -2222,11 +2726,29 @@ ScreenPlan plan_screen(int64_t n_rows, int d, int64_t K, int top) {
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc) {
   ScreenWs w;
   const int64_t tiles = cdiv(K_alloc, 16);
+  w.corder = w.ckey = w.coff = w.hist = w.rkey = w.rord = nullptr;
+  w.cbnd = nullptr;
+  w.cminS = w.cmaxP = nullptr;
+  w.prm = nullptr;
   if (p.s32) {
     // 32-codeword tiles of 768 fp16, the scale reduction's partial maxima and alpha
-    w.apack = ws.take<float>(static_cast<size_t>(cdiv(K_alloc, kS32Tile) * kS32TileHalves / 2));
+    const int64_t t32 = p.tiles > cdiv(K_alloc, kS32Tile) ? p.tiles : cdiv(K_alloc, kS32Tile);
+    w.apack = ws.take<float>(static_cast<size_t>(t32 * kS32TileHalves / 2));
     w.cnp = nullptr;
     w.smax = ws.take<float>(static_cast<size_t>(kS32MaxParts + 1));
+    if (p.prune) {
+      const int64_t nch = t32 / 2 + 1;
+      w.corder = ws.take<int>(static_cast<size_t>(t32 * kS32Tile));
+      w.ckey = ws.take<int>(static_cast<size_t>(K_alloc));
+      w.coff = ws.take<int>(static_cast<size_t>(kPruneKeys));
+      w.hist = ws.take<int>(static_cast<size_t>(2 * kPruneKeys));
+      w.cbnd = ws.take<uint4>(static_cast<size_t>(nch));
+      w.cminS = ws.take<uint32_t>(static_cast<size_t>(nch));
+      w.cmaxP = ws.take<uint32_t>(static_cast<size_t>(nch));
+      w.prm = ws.take<float>(4 + 3 * kPruneParts);  // the parameters, then the partial ranges
+      w.rkey = ws.take<int>(static_cast<size_t>(n_rows));
+      w.rord = ws.take<int>(static_cast<size_t>(n_rows));
+    }
   } else {
     // fp32: 64 lanes x ks floats per tile; split: 16 codewords x 16 bf16 per tile
     w.apack = ws.take<float>(static_cast<size_t>(p.split ? tiles * 128 : tiles * 64 * p.ks));
@@ -2267,21 +2789,71 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     float* alpha = w.smax + kS32MaxParts;
     uint16_t* ap = reinterpret_cast<uint16_t*>(w.apack);
     hipLaunchKernelGGL(cb_absmax_partial, dim3(nparts), dim3(256), 0, stream, C, ct, count, w.smax);
-    hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
-                       stream, C, ct, K, src.d, p.tiles, w.smax, nparts, ap, alpha, w.rcount);
+    PruneData pd = {};
+    const int jp = 0;  // the coordinate of the second band
+    if (p.prune) {
+      // the codebook in key order (the packed tiles follow it), its chunk ranges, then the rows
+      RowSrc cbs;
+      cbs.base = C;
+      cbs.type = ct;
+      cbs.d = src.d;
+      cbs.vpr = 1;
+      cbs.ld = src.d;
+      cbs.n = K;
+      const int64_t nch = p.tiles / 2;
+      const int sparts = static_cast<int>(cdiv(K, 256) < kPruneParts ? cdiv(K, 256) : kPruneParts);
+      hipLaunchKernelGGL(prune_stats_partial, dim3(sparts), dim3(256), 0, stream, C, ct, K, src.d, jp, w.prm + 4,
+                         w.hist);
+      hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
+                         jp, w.prm + 4, sparts, w.prm, w.ckey, w.hist);
+      hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist, w.coff);
+      hipLaunchKernelGGL(prune_fill_kernel, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
+                         stream, w.corder, p.tiles * kS32Tile, -1);
+      hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream,
+                         w.ckey, K, w.hist, w.corder);
+      hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
+                         stream, C, ct, K, src.d, p.tiles, w.smax, nparts, w.corder, ap, alpha, w.rcount);
+      hipLaunchKernelGGL(prune_chunks_kernel, dim3(static_cast<unsigned>(cdiv(nch, 4))), dim3(256), 0, stream, C, ct,
+                         K, src.d, jp, w.corder, alpha, nch, w.cbnd);
+      hipLaunchKernelGGL(prune_envelope_kernel, dim3(1), dim3(1024), 0, stream, w.cbnd, static_cast<int>(nch), w.cminS,
+                         w.cmaxP, w.prm);
+      hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
+                         src, jp, w.prm + 4, sparts, w.prm, w.rkey, w.hist + kPruneKeys);
+      hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist + kPruneKeys, nullptr);
+      hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
+                         w.rkey, src.n, w.hist + kPruneKeys, w.rord);
+      pd.corder = w.corder;
+      pd.coff = w.coff;
+      pd.cbnd = w.cbnd;
+      pd.cminS = w.cminS;
+      pd.cmaxP = w.cmaxP;
+      pd.rord = w.rord;
+      pd.rkey = w.rkey;
+      pd.prm = w.prm;
+      pd.jp = jp;
+    } else {
+      hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
+                         stream, C, ct, K, src.d, p.tiles, w.smax, nparts, nullptr, ap, alpha, w.rcount);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     dim3 grid(static_cast<unsigned>(p.grid_x), static_cast<unsigned>(p.splits));
     const bool exact = s32_exact_operands(src.type, ct);
     // First screen: one MFMA per tile.  Exact for bf16 rows against a bf16 book; otherwise on
     // fp16-rounded operands, certified with the wider bound.
-    hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true, false>), grid, dim3(256), 0, stream, src,
-                       ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr, nullptr);
+    const ScreenBound b1 = screen_bound(p, src.type, ct, src.d, alpha, !exact);
+    if (p.prune)
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true, false, false, true>), grid, dim3(256), 0,
+                         stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr,
+                         nullptr, pd.corder, pd, b1.acc_ulps, b1.split_coef);
+    else
+      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true, false>), grid, dim3(256), 0, stream, src,
+                         ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr, nullptr,
+                         nullptr, pd, 0.0, 0.0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (exact) {
       const ScreenBound bound = screen_bound(p, src.type, ct, src.d, alpha);
       return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
     }
-    const ScreenBound b1 = screen_bound(p, src.type, ct, src.d, alpha, true);
     const int64_t nb = cdiv(src.n, 256);
     // the uncertain rows, compacted through rlist2 (free until the second finalize) in row order
     hipLaunchKernelGGL(finalize1_first_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, src.n, p.splits,
@@ -2296,10 +2868,12 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     if (src.n < kS32SharedRowsMaxN) {
       const dim3 grid2(static_cast<unsigned>(cdiv(src.n, 32 * CRVQ_S32_CB)), static_cast<unsigned>(p.splits));
       hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true>), grid2, dim3(256), 0, stream,
-                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
+                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount,
+                         pd.corder, PruneData{}, 0.0, 0.0);
     } else {
       hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false>), grid, dim3(256), 0, stream,
-                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount);
+                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount,
+                         pd.corder, PruneData{}, 0.0, 0.0);
     }
     const ScreenBound b2 = screen_bound(p, src.type, ct, src.d, alpha);
     hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,

@@ -173,6 +173,39 @@ def test_second_screen_own_rows_full():
     check(V, Cb)
 
 
+# From about a million rows (no codebook splits) the first screen visits the codebook in the order
+# of a key (norm, then one coordinate) and skips pairs of tiles whose norms or coordinates are
+# certified too far from every row of a wave; the results must stay the oracle's exactly.
+@pytest.mark.parametrize("case,K", [("near", 65536), ("bf16", 16384), ("outliers", 16384), ("ties", 16384),
+                                    ("tiny", 4096)])
+def test_pruned_first_screen(case, K):
+    n, d = (1 << 20) + 4096 + 37, 8
+    say(f"pruned first screen n={n} K={K} ({case})")
+    g = np.random.default_rng(60)
+    if case in ("near", "bf16"):
+        V = rv(n, d, 61)
+        Cb = np.ascontiguousarray(V[g.choice(n, K, replace=False)] + rv(K, d, 62, 0.002))
+        if case == "bf16":
+            check(inputs.f32_to_bf16_bits(V), inputs.f32_to_bf16_bits(Cb), "bf16")
+            return
+    elif case == "outliers":
+        Cb = (g.standard_t(4.0, size=(K, d)) * 0.02).astype(np.float32)
+        Cb[:, 0] *= np.float32(10.0)                       # the coordinate of the second band
+        V = (g.standard_t(4.0, size=(n, d)) * 0.02).astype(np.float32)
+        big = g.choice(n, 500, replace=False)
+        V[big, g.integers(0, d, 500)] *= np.float32(1e5)   # beyond the scaled fp16 range: rescued exactly
+        tiny = g.choice(n, 500, replace=False)
+        V[tiny] *= np.float32(1e-6)
+    elif case == "ties":
+        base = rv(K // 4, d, 63)
+        Cb = np.ascontiguousarray(np.concatenate([base, base, base[::-1], base])[g.permutation(K)])
+        V = np.concatenate([base[g.integers(0, K // 4, n // 2)], rv(n - n // 2, d, 64)])
+    else:  # magnitudes far below one: the bands are kept in units of the codebook scale
+        V = rv(n, d, 65) * np.float32(1e-30)
+        Cb = rv(K, d, 66) * np.float32(1e-30)
+    check(V, Cb)
+
+
 def test_rescue_of_most_rows():
     """Rows equal to codewords that the book holds four times (exact ties on every row, so nearly every
     row reaches the exact rescue) over 1,048,579 rows: more listed rows than the parted rescue has

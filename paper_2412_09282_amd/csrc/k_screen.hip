@@ -71,6 +71,12 @@
 #ifndef CRVQ_PRUNE
 #define CRVQ_PRUNE 1  // certified chunk skipping in the first long top-1 screen (norm and coordinate bands)
 #endif
+#ifndef CRVQ_PRUNE_FIRST
+#define CRVQ_PRUNE_FIRST 4  // chunks screened before the first band; the band is renewed after 2x, 4x, ...
+#endif
+#ifndef CRVQ_PRUNE_CAP
+#define CRVQ_PRUNE_CAP 128  // ... and then every this many chunks
+#endif
 
 namespace crvq {
 namespace {
@@ -1052,28 +1058,44 @@ __device__ __forceinline__ bool prune_keep(const uint4& b, const PruneCursor& s)
   return !((b.y < s.lo1) | (b.x > s.hi1) | (b.w < s.lo2) | (b.z > s.hi2));
 }
 
-// L[i0 .. n) filtered under the current bands into L[0 ..); returns the new length.
+// L[i0 .. n) filtered under the current bands into L[0 ..); returns the new length.  Four groups of
+// 64 entries are examined per round, all their loads issued before any is used.
 __device__ __forceinline__ int prune_filter(uint16_t* L, int i0, int n, bool up, const PruneCursor& s,
                                             const PruneData& pd, int lane) {
+  constexpr int kG = 4;
   int w = 0;
-  for (int b = i0; b < n; b += 64) {
-    const int i = b + lane;
-    int c = 0;
-    bool keep = false, end = false;
-    if (i < n) {
-      c = L[i];
-      const uint32_t env = up ? pd.cminS[c] : pd.cmaxP[c];
-      const uint4 bd = pd.cbnd[c];
-      end = up ? (env > s.hi1) : (env < s.lo1);
-      keep = !end & prune_keep(bd, s);
+  const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+  for (int b = i0; b < n; b += 64 * kG) {
+    int c[kG];
+    uint32_t env[kG];
+    uint4 bd[kG];
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      const int i = b + 64 * g + lane;
+      c[g] = i < n ? static_cast<int>(L[i]) : -1;
     }
-    const uint64_t em = __ballot(end);
-    uint64_t km = __ballot(keep);
-    if (em) km &= (uint64_t{1} << __builtin_ctzll(em)) - 1ull;  // nothing from the first end on
-    const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
-    if ((km >> lane) & 1ull) L[w + __popcll(km & lt)] = static_cast<uint16_t>(c);
-    w += __popcll(km);
-    if (em) break;
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      const int cc = c[g] >= 0 ? c[g] : 0;
+      env[g] = up ? pd.cminS[cc] : pd.cmaxP[cc];
+      bd[g] = pd.cbnd[cc];
+    }
+    bool stop = false;
+#pragma unroll
+    for (int g = 0; g < kG; ++g) {
+      const bool valid = c[g] >= 0;
+      const bool end = !valid || (up ? (env[g] > s.hi1) : (env[g] < s.lo1));
+      const bool keep = !end & prune_keep(bd[g], s);
+      const uint64_t em = __ballot(end);
+      uint64_t km = __ballot(keep);
+      if (em) km &= (uint64_t{1} << __builtin_ctzll(em)) - 1ull;  // nothing from the first end on
+      if (!stop) {
+        if ((km >> lane) & 1ull) L[w + __popcll(km & lt)] = static_cast<uint16_t>(c[g]);
+        w += __popcll(km);
+      }
+      stop = stop || em != 0ull;
+    }
+    if (stop) break;
   }
   return static_cast<int>(rfl(static_cast<uint32_t>(w)));
 }
@@ -1264,8 +1286,11 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   // merge through LDS at the end (when the listed rows are few, rows alone would leave most SIMDs
   // idle).  Otherwise every wave has rows of its own.
   static_assert(LIST || !QS, "the shared-row split is for listed rows");
+  // PRUNE: blocks take the key order from its upper end, where the bands are widest, so that the
+  // longest waves start first
+  const int64_t bx = PRUNE ? static_cast<int64_t>(gridDim.x) - 1 - blockIdx.x : static_cast<int64_t>(blockIdx.x);
   const int64_t row0 = QS ? static_cast<int64_t>(blockIdx.x) * (32 * CB)
-                          : (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (32 * CB);
+                          : (bx * 4 + wave) * (32 * CB);
   if (row0 >= n) return;  // uniform over the block in QS mode; the only barrier is below
   const float alpha = alpha_p[0];
   __shared__ double sD[QS ? 4 : 1][QS ? 32 * CB : 1];
@@ -1416,6 +1441,18 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       // The chunk after next is chosen at the end of an iteration, so the body (MFMAs, minimum
       // folds, the next chunk's loads) stays straight-line; past the last chunk the loads repeat
       // a valid tile and are not used.
+      int done = 0, at = CRVQ_PRUNE_FIRST;
+      auto renew = [&]() {
+        if (++done == at) {
+          prune_band<CB>(cur, m, &sBand[wave][0][0][0], j);
+          // chunks already taken stay; the rest is filtered
+          cur.un = prune_filter(Ul, cur.ui, cur.un, true, cur, pd, lane);
+          cur.dn = prune_filter(Dl, cur.di, cur.dn, false, cur, pd, lane);
+          cur.ui = 0;
+          cur.di = 0;
+          at = at < CRVQ_PRUNE_CAP ? 2 * at : at + CRVQ_PRUNE_CAP;
+        }
+      };
       h8 qa, qb;
       int Cc = prune_take(cur, Ul, Dl);
       int Cn = Cc >= 0 ? prune_take(cur, Ul, Dl) : -1;
@@ -1423,7 +1460,6 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
         load(2 * Cc, qa, qa);
         load(2 * Cc + 1, qb, qb);
       }
-      int done = 0, at = 4;
       while (Cc >= 0) {
         const int Tn = Cn >= 0 ? 2 * Cn : 2 * Cc;
         tile(qa, qa, true);
@@ -1431,15 +1467,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
         tile(qb, qb, false);
         fold(2 * Cc);
         load(Tn + 1, qb, qb);
-        if (++done == at) {
-          prune_band<CB>(cur, m, &sBand[wave][0][0][0], j);
-          // the chunk already taken for the next iteration stays; the rest is filtered
-          cur.un = prune_filter(Ul, cur.ui, cur.un, true, cur, pd, lane);
-          cur.dn = prune_filter(Dl, cur.di, cur.dn, false, cur, pd, lane);
-          cur.ui = 0;
-          cur.di = 0;
-          at = at < 128 ? 2 * at : at + 128;
-        }
+        renew();
         Cc = Cn;
         Cn = Cn >= 0 ? prune_take(cur, Ul, Dl) : -1;
       }
@@ -1472,9 +1500,9 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   for (int cb = 0; cb < CB; ++cb) {
     const int64_t i = row0 + cb * 32 + j;
     const bool valid = i < n;
-    // the row's index in the source (where a first screen in key order writes its results)
+    // the row's index in the source; results go to the row's position i (list or key order)
     const int64_t pi = (LIST && valid) ? list[i] : ((PRUNE && valid) ? pd.rord[i] : i);
-    const int64_t oi = PRUNE ? pi : i;
+    const int64_t oi = i;
     const float mg = m[cb];
     const float om = __shfl_xor(mg, 32);
     const int hw = (om < mg || (om == mg && h == 1)) ? 1 - h : h;
@@ -1604,7 +1632,8 @@ __device__ __forceinline__ void emit_row(int64_t row, const double (&ED)[NB], co
   if (codes) {
     const bool none = EK[0] == INT_MAX;
     codes[row] = none ? 0 : EK[0];
-    if (dist) dist[row] = none ? __builtin_nanf("") : static_cast<float>(ED[0]);
+    // (the NaN as a bit pattern: this file is compiled without NaN semantics)
+    if (dist) dist[row] = none ? __uint_as_float(0x7fc00000u) : static_cast<float>(ED[0]);
   } else {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
@@ -1946,9 +1975,11 @@ __device__ __forceinline__ bool finish_top1(int64_t i, int64_t row, int splits, 
 // wider certificate, so instead of one global counter (whose atomics serialize) each block packs its
 // failing rows, in row order, into its own slice tmp[256 b ..] and writes their number to bcount[b];
 // scan_counts_kernel and compact_list_kernel then build the dense list in block order.
+// rmap (when the screen ran in key order): the row at position i; results are at positions.
 __global__ __launch_bounds__(256) void finalize1_first_kernel(int64_t n, int splits, const float* __restrict__ pR,
                                                               const double* __restrict__ pD, const int* __restrict__ pK,
                                                               const double* __restrict__ xn2a, ScreenBound bound,
+                                                              const int* __restrict__ rmap,
                                                               int* __restrict__ tmp, int* __restrict__ bcount,
                                                               int32_t* __restrict__ codes, float* __restrict__ dist,
                                                               double* __restrict__ rowD, int* __restrict__ rowK) {
@@ -1956,14 +1987,15 @@ __global__ __launch_bounds__(256) void finalize1_first_kernel(int64_t n, int spl
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   const bool valid = i < n;
+  const int64_t row = (valid && rmap) ? static_cast<int64_t>(rmap[i]) : i;
   bool fail = false;
-  if (valid) fail = !finish_top1(i, i, splits, n, pR, pD, pK, xn2a, bound, codes, dist, rowD, rowK);
+  if (valid) fail = !finish_top1(i, row, splits, n, pR, pD, pK, xn2a, bound, codes, dist, rowD, rowK);
   const uint64_t m = __ballot(fail);
   if (lane == 0) s_wc[w] = __popcll(m);
   __syncthreads();
   int woff = 0;
   for (int u = 0; u < w; ++u) woff += s_wc[u];
-  if (fail) tmp[static_cast<int64_t>(blockIdx.x) * 256 + woff + __popcll(m & ((1ull << lane) - 1ull))] = static_cast<int>(i);
+  if (fail) tmp[static_cast<int64_t>(blockIdx.x) * 256 + woff + __popcll(m & ((1ull << lane) - 1ull))] = static_cast<int>(row);
   if (threadIdx.x == 0) bcount[blockIdx.x] = s_wc[0] + s_wc[1] + s_wc[2] + s_wc[3];
 }
 
@@ -2850,14 +2882,27 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                          ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr, nullptr,
                          nullptr, pd, 0.0, 0.0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (exact) {
+    if (exact && !p.prune) {
       const ScreenBound bound = screen_bound(p, src.type, ct, src.d, alpha);
       return launch_finalize_ks<2>(src, C, ct, K, top, p, w, bound, out_codes, out_dist, rowD, rowK, stream);
+    }
+    if (exact) {
+      // results at key-order positions: certify by position, compact the uncertain rows, rescue them
+      const int64_t nbx = cdiv(src.n, 256);
+      hipLaunchKernelGGL(finalize1_first_kernel, dim3(static_cast<unsigned>(nbx)), dim3(256), 0, stream, src.n,
+                         p.splits, w.pR, w.pD, w.pK, w.xn2, b1, w.rord, w.rlist2, w.bcount, out_codes, out_dist, rowD,
+                         rowK);
+      hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, stream, w.bcount, nbx, w.bcount + nbx, w.rcount);
+      hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nbx)), dim3(256), 0, stream, w.rlist2,
+                         w.bcount, w.bcount + nbx, w.rlist);
+      return launch_rescue1<2>(src, top, C, ct, K, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK, w.pD, w.pK,
+                               static_cast<int64_t>(p.splits) * src.n, stream);
     }
     const int64_t nb = cdiv(src.n, 256);
     // the uncertain rows, compacted through rlist2 (free until the second finalize) in row order
     hipLaunchKernelGGL(finalize1_first_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, src.n, p.splits,
-                       w.pR, w.pD, w.pK, w.xn2, b1, w.rlist2, w.bcount, out_codes, out_dist, rowD, rowK);
+                       w.pR, w.pD, w.pK, w.xn2, b1, p.prune ? w.rord : nullptr, w.rlist2, w.bcount, out_codes, out_dist,
+                       rowD, rowK);
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, stream, w.bcount, nb, w.bcount + nb, w.rcount);
     hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, w.rlist2, w.bcount,
                        w.bcount + nb, w.rlist);

@@ -129,6 +129,32 @@ def colreduce(A: np.ndarray, B: Optional[np.ndarray] = None, scale: Optional[np.
     return out
 
 
+def hessian_inverse_diagonal(H: np.ndarray, damp: float = 0.01) -> np.ndarray:
+    """Denominator of the W-A importance of Sec. 4.1 Eq. 7: [(X X^T)^-1]_jj for every channel j,
+    in fp64.  H = X X^T (N x N; stored tokens x N activations give H = X^T X).
+
+    Reading (the paper is silent): X X^T is singular whenever the calibration set has fewer tokens
+    than channels or a channel is never active, so the inverse is taken of the damped matrix
+    H + damp * mean_j(H_jj) * I, the dampening of the OBS-style quantizers the paper builds on
+    (damp = 1 %).  If the damped matrix is not positive definite (for instance an all-zero H)
+    every entry of the result is NaN.  The definition, written out: the diagonal of the inverse."""
+    H = np.asarray(H, dtype=np.float64)
+    N = H.shape[0]
+    assert H.shape == (N, N)
+    Hd = H + damp * np.mean(np.diag(H)) * np.eye(N) if N else H
+    try:
+        np.linalg.cholesky(Hd)  # positive definiteness check only
+    except np.linalg.LinAlgError:
+        return np.full(N, np.nan)
+    return np.diag(np.linalg.inv(Hd)).copy()
+
+
+def obs_scale(hinv: np.ndarray) -> np.ndarray:
+    """Per-channel factor of Sec. 4.1 Eq. 7, 1 / (2 [(X X^T)^-1]_jj), rounded once to float32 (the
+    form the importance reduction takes its scale in), returned as fp64."""
+    return np.asarray(1.0 / (2.0 * np.asarray(hinv, np.float64)), np.float32).astype(np.float64)
+
+
 def rank_perm(importance: np.ndarray) -> np.ndarray:
     """Channel reordering of Sec. 4.2 (Alg. 1 ReorderChannels): channels sorted by importance, most
     important first.  Reading: a stable sort -- equal importance keeps the lower channel index

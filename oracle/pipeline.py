@@ -15,7 +15,10 @@ Readings where the paper is silent (each also listed in the design notes):
   Appendix A.2 Eq. 10, I_j = h_j * max_i (W_ij - Wq_ij)^2 with Wq the
   prequantized W (Alg. 1 Prequantize: the basic VQ -- same K, init indices and
   iterations -- on the unsorted W); Eq. 10's factor 1/2 is the same for every
-  channel and changes no ordering, so it is left out;
+  channel and changes no ordering, so it is left out; "obs" Eq. 7 as printed,
+  I_j = max_i (W_ij - Wq_ij)^2 / (2 [(X X^T)^-1]_jj), the inverse taken of the
+  damped Hessian proxy (``hessian_inverse_diagonal``), the factor rounded to
+  float32 before the reduction;
 * critical channels: the first d * ceil(lambda N / d) reordered columns;
 * K-means: initial codewords are the vectors at seeded indices (an input);
   one iteration = assign + update; ``iters`` iterations then a final assign;
@@ -39,8 +42,10 @@ from typing import Dict, List, Optional
 
 import numpy as np
 
-from . import (F32, BF16, assign, beam, colreduce, gather_columns, kmeans_update, n_crit_columns,
-               objective, rank_perm, reconstruct, residual, round_to, scatter_columns, vectors, widen)
+from . import (F32, BF16, assign, beam, colreduce, gather_columns, hessian_inverse_diagonal, kmeans_update,
+               n_crit_columns, objective, obs_scale, rank_perm, reconstruct, residual, round_to, scatter_columns,
+               vectors, widen)
+from .refine import gram
 
 
 @dataclasses.dataclass
@@ -92,9 +97,15 @@ def prequantize(W: np.ndarray, dtype: str, d: int, base_idx: np.ndarray, iters: 
 
 
 def channel_importance(W: np.ndarray, h: np.ndarray, dtype: str, mode: str, d: int = 8,
-                       base_idx: Optional[np.ndarray] = None, iters: int = 1) -> np.ndarray:
-    """Channel importance of Sec. 4.1 (modes as in the module notes), rounded to float32."""
-    if mode == "energy":
+                       base_idx: Optional[np.ndarray] = None, iters: int = 1,
+                       H: Optional[np.ndarray] = None, damp: float = 0.01) -> np.ndarray:
+    """Channel importance of Sec. 4.1 (modes as in the module notes), rounded to float32.  Mode
+    "obs" needs H = X X^T (fp64, N x N)."""
+    if mode == "obs":
+        Wq = prequantize(W, dtype, d, base_idx, iters)
+        s = obs_scale(hessian_inverse_diagonal(H, damp))
+        I = colreduce(W, Wq, scale=s, reduce="max", dtype=dtype)
+    elif mode == "energy":
         I = colreduce(W, scale=h.astype(np.float64), reduce="sum", dtype=dtype)
     elif mode == "w_only":
         I = colreduce(W, reduce="max", dtype=dtype)
@@ -117,10 +128,11 @@ def residual_books(minuend: np.ndarray, codes: List[np.ndarray], books: List[np.
 def quantize_layer(W: np.ndarray, X: np.ndarray, dtype: str, d: int, K_base: int, K_ext: List[int],
                    crit_frac: float, width: int, iters: int, base_idx: np.ndarray,
                    ext_idx: List[np.ndarray], importance: str = "energy", m_base: int = 1,
-                   base_idx_extra: List[np.ndarray] = ()) -> LayerResult:
+                   base_idx_extra: List[np.ndarray] = (), damp: float = 0.01) -> LayerResult:
     M, N = W.shape
     h = round_to(colreduce(X, reduce="sum"), F32)
-    I = channel_importance(W, h, dtype, importance, d, base_idx, iters)
+    H = gram(X) if importance == "obs" else None
+    I = channel_importance(W, h, dtype, importance, d, base_idx, iters, H, damp)
     perm = rank_perm(I)
     Ws = gather_columns(W, perm)
     n_crit = n_crit_columns(N, d, crit_frac)

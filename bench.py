@@ -147,7 +147,7 @@ def table(args):
         ei = [torch.from_numpy(e).cuda() for e in ext_idx]
         xi = [torch.from_numpy(e).cuda() for e in extra_idx]
         cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, importance=args.importance,
-                          m_base=wl.m_base)
+                          m_base=wl.m_base, damp=args.damp)
         q = LayerQuantizer(M, N, tdt, cfg, L.tokens, device="cuda")
         q.run(Wd, Xd, bi, ei, base_idx_extra=xi)  # warm-up pass
         torch.cuda.synchronize()
@@ -198,8 +198,23 @@ def table(args):
                 ok = np.all(np.abs(got - exp) <= 1e-5 * np.abs(exp))
                 rec("channel_importance (Hessian diagonal)", ms, len(calls), X.size * 4 + N * 4, "B", HBM, ts, 1.0,
                     "1e-5 rel" if ok else "FAIL")
+            elif kind == "gram":
+                X64 = X.astype(np.float64)
+                exp = X64.T @ X64
+                ts = time.perf_counter() - t0
+                got = c["out"]["H"]
+                ok = np.all(np.abs(got - exp) <= 1e-12 * (np.abs(X64).T @ np.abs(X64)))
+                rec("gram (H = X^T X, fp64)", ms, len(calls), 2.0 * X.shape[0] * N * N, "FLOP", 78.6e12, ts, 1.0,
+                    "1e-12 of sum|terms|" if ok else "FAIL")
+            elif kind == "hinv":
+                exp = oracle.obs_scale(oracle.hessian_inverse_diagonal(c["in"]["H"], args.damp))
+                ts = time.perf_counter() - t0
+                got = c["out"]["scale"].astype(np.float64)
+                ok = np.all(np.abs(got - exp) <= 1e-6 * np.abs(exp))
+                rec("hessian_inverse_diagonal (Eq. 7 factor, fp64 Cholesky)", ms, len(calls), 2.0 * N ** 3 / 3, "FLOP",
+                    78.6e12, ts, 1.0, "1e-6 rel" if ok else "FAIL")
             elif kind == "importance":
-                if "B" in c["in"]:  # W-A: max_i (W - Wq)^2 scaled by h
+                if "B" in c["in"]:  # W-A: max_i (W - Wq)^2 scaled by h (Eq. 10) or by 1 / (2 hinv) (Eq. 7)
                     exp = oracle.colreduce(W, c["in"]["B"], scale=c["in"]["scale"].astype(np.float64), reduce="max",
                                            dtype=dt)
                     what, nb = "channel_importance (W - Wq, max, scale = h)", 2 * M * N * es + 2 * N * 4
@@ -573,7 +588,7 @@ def main():
                     help="instead of the benchmark line: one JSON record per library call of one layer pass of each "
                          "--workloads entry, GPU time beside the oracle's on the same inputs, with parity")
     ap.add_argument("--workloads", default="1,2,3,4,5")
-    ap.add_argument("--importance", default="energy", choices=["energy", "w_only", "wa"],
+    ap.add_argument("--importance", default="energy", choices=["energy", "w_only", "wa", "obs"],
                     help="channel-importance strategy of the --table layer passes")
     ap.add_argument("--gemv", action="store_true",
                     help="instead of the benchmark line: the quantized matrix-vector product on the LLaMA gate "
@@ -584,7 +599,14 @@ def main():
     ap.add_argument("--rounds", type=int, default=2)
     ap.add_argument("--ft-steps", type=int, default=5)
     ap.add_argument("--lr", type=float, default=1e-4)
+    ap.add_argument("--damp", type=float, default=0.01,
+                    help="--importance obs: the inverse is taken of H + damp * mean(diag H) * I")
+    ap.add_argument("--oracle-threads", type=int, default=0,
+                    help="host threads of the oracle's timed runs (0: all it is given)")
     args = ap.parse_args()
+    if args.oracle_threads > 0:
+        import oracle
+        oracle.set_num_threads(args.oracle_threads)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
         sys.exit(2)

@@ -289,6 +289,29 @@ crvq_status crvq_bits_per_weight(int64_t rows, int64_t cols, int32_t d, int64_t 
 crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols, int64_t ld, double* H, int64_t ldh,
                       void* stream);
 
+/* crvq_hessian_inverse_diagonal -- the denominator of the W-A channel
+ * importance of Sec. 4.1 Eq. 7, [(X X^T)^-1]_jj, for every channel j:
+ *
+ *   hinv[j]  = [(H + delta I)^-1]_jj,   delta = damp * (sum_j H_jj) / N,
+ *   scale[j] = float(1 / (2 hinv[j]))   (Eq. 7's factor, rounded once),
+ *
+ * so that crvq_channel_importance(W, B = the prequantized W, scale, MAX)
+ * gives Eq. 7's I_j.  The damping (damp >= 0; 0.01 is the usual choice)
+ * makes the proxy invertible when the calibration set has fewer tokens than
+ * channels or a channel is never active.  H: N x N fp64, row stride ldh >= N,
+ * symmetric; only its lower triangle (j <= i) is read.  hinv: double[N] and
+ * scale: float[N], device memory, either may be NULL (not both).  Computed in
+ * fp64 by a blocked Cholesky factorization A = L L^T with the inverse factor
+ * T = L^-1 formed alongside ([A^-1]_jj = sum_i T_ij^2); deterministic.  If
+ * the damped matrix is not positive definite (a pivot <= 0, NaN or infinite),
+ * every hinv[j] and scale[j] is NaN: the status does not report it, since the
+ * check runs on the device.  N <= 65536.
+ * workspace: crvq_hessian_inverse_workspace_size(N) bytes (about 16 N^2).
+ */
+size_t crvq_hessian_inverse_workspace_size(int64_t N);
+crvq_status crvq_hessian_inverse_diagonal(const double* H, int64_t ldh, int64_t N, double damp, double* hinv,
+                                          float* scale, void* workspace, size_t ws_bytes, void* stream);
+
 /* crvq_hessian_product -- G = R H[:, 0:n_out] (so -2 G is the gradient of
  * QuantLoss w.r.t. W_hat on those columns) and, when row_loss != NULL (needs
  * n_out == N), row_loss[r] = sum_j R[r][j] G[r][j], the QuantLoss of row r
@@ -384,6 +407,7 @@ crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_
  *   CRVQ_OP_CODE_SUMS   n_vectors, d, K              (crvq_code_sums)
  *   CRVQ_OP_REFINE      M, N, n_cols                 (crvq_refine_codes)
  *   CRVQ_OP_GEMV        M, N, K = K_base             (crvq_dequant_gemv)
+ *   CRVQ_OP_HINV        N                            (crvq_hessian_inverse_diagonal)
  * Returns 0 for an unknown op or a shape the call rejects (and for calls that
  * need no workspace at that shape).  Ks is a host array of n_books entries.
  */
@@ -396,7 +420,8 @@ typedef enum {
   CRVQ_OP_DEQUANT = 5,
   CRVQ_OP_CODE_SUMS = 6,
   CRVQ_OP_REFINE = 7,
-  CRVQ_OP_GEMV = 8
+  CRVQ_OP_GEMV = 8,
+  CRVQ_OP_HINV = 9
 } crvq_op;
 size_t crvq_workspace_size(int op, int64_t n_vectors, int64_t K, int32_t beam, int32_t n_books, int32_t d,
                            const int64_t* Ks, int64_t M, int64_t N, int64_t n_cols);

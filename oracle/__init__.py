@@ -63,6 +63,7 @@ def _load():
         lib.oracle_reconstruct.argtypes = [I64, I32, I32, I32, P, P, P, P]
         lib.oracle_round_bf16.argtypes = [P, I64, P]
         lib.oracle_num_threads.restype = I32
+        lib.oracle_set_num_threads.argtypes = [I32]
         _lib = lib
     return _lib
 
@@ -73,6 +74,11 @@ def _p(a: Optional[np.ndarray]):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Host threads the oracle's parallel loops use from now on (for timing it on fewer cores)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 # ----------------------------------------------------------------------------------------------

@@ -274,3 +274,12 @@ int oracle_num_threads(void) {
   return 1;
 #endif
 }
+
+/* Host threads of the parallel loops from now on (n >= 1); for timing the oracle on fewer cores. */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}

@@ -30,6 +30,7 @@ SOURCES = {
     "k_dequant.hip": [],
     "k_gemv.hip": [],
     "k_refine.hip": [],
+    "k_hinv.hip": [],
 }
 
 COMMON = [

@@ -71,6 +71,8 @@ def lib(build_if_missing: bool = True):
                 "crvq_bits_per_weight": ([I64, I64, I32, I64, I32, I32, P, I32, I32, P], ctypes.c_int),
                 "crvq_gram": ([P, ctypes.c_int, I64, I64, I64, P, I64, P], ctypes.c_int),
                 "crvq_hessian_product": ([I64, I64, I64, P, I64, P, I64, P, I64, P, P, P], ctypes.c_int),
+                "crvq_hessian_inverse_workspace_size": ([I64], SZ),
+                "crvq_hessian_inverse_diagonal": ([P, I64, I64, ctypes.c_double, P, P, P, SZ, P], ctypes.c_int),
                 "crvq_workspace_size": ([ctypes.c_int, I64, I64, I32, I32, I32, P, I64, I64, I64], SZ),
                 "crvq_code_sums_workspace_size": ([I64, I32, I64], SZ),
                 "crvq_code_sums": ([P, I64, I64, I64, I32, P, I64, P, P, P, SZ, P], ctypes.c_int),
@@ -305,6 +307,21 @@ def crvq_gram(X: torch.Tensor, H: torch.Tensor, stream=None) -> None:
                                         H.stride(0), _stream(stream)))
 
 
+def crvq_hessian_inverse_diagonal(H: torch.Tensor, hinv: Optional[torch.Tensor] = None,
+                                  scale: Optional[torch.Tensor] = None, damp: float = 0.01, stream=None) -> None:
+    """hinv = diag((H + damp * mean(diag H) I)^-1) (fp64) and/or scale = float32(1 / (2 hinv)), the
+    factor of the W-A importance of Sec. 4.1 Eq. 7."""
+    assert H.dim() == 2 and H.shape[0] == H.shape[1] and H.dtype == torch.float64 and H.stride(1) == 1
+    assert hinv is None or (hinv.dtype == torch.float64 and hinv.is_contiguous())
+    assert scale is None or (scale.dtype == torch.float32 and scale.is_contiguous())
+    L = lib()
+    N = H.shape[0]
+    ws = _workspace(L.crvq_hessian_inverse_workspace_size(N), H.device)
+    _check("crvq_hessian_inverse_diagonal", L.crvq_hessian_inverse_diagonal(
+        _ptr(H), H.stride(0), N, float(damp), _ptr(hinv), _ptr(scale), _ptr(ws), 0 if ws is None else ws.numel(),
+        _stream(stream)))
+
+
 def crvq_hessian_product(R: torch.Tensor, H: torch.Tensor, G: torch.Tensor, row_loss: Optional[torch.Tensor] = None,
                          loss_total: Optional[torch.Tensor] = None, stream=None) -> None:
     """G = R H[:, :G.shape[1]], optionally the per-row QuantLoss sum_j R_rj G_rj and their total (fp64)."""
@@ -315,7 +332,7 @@ def crvq_hessian_product(R: torch.Tensor, H: torch.Tensor, G: torch.Tensor, row_
 
 
 CRVQ_OP = {"importance": 0, "reorder": 1, "assign": 2, "beam": 3, "kmeans": 4, "dequant": 5, "code_sums": 6,
-           "refine": 7, "gemv": 8}
+           "refine": 7, "gemv": 8, "hinv": 9}
 
 
 def crvq_workspace_size(op: str, n_vectors: int = 0, K: int = 0, beam: int = 0, Ks: Sequence[int] = (), d: int = 0,

@@ -550,6 +550,25 @@ crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols
                     fn);
 }
 
+size_t crvq_hessian_inverse_workspace_size(int64_t N) {
+  if (N < 1 || N > 65536) return 0;
+  return hinv_ws_bytes(N);
+}
+
+crvq_status crvq_hessian_inverse_diagonal(const double* H, int64_t ldh, int64_t N, double damp, double* hinv,
+                                          float* scale, void* workspace, size_t ws_bytes, void* stream) {
+  static const char* fn = "crvq_hessian_inverse_diagonal";
+  g_err.clear();
+  if (N < 0 || N > 65536) return fail(CRVQ_ERR_INVALID, "%s: N = %lld outside [0, 65536]", fn, (long long)N);
+  if (ldh < N) return fail(CRVQ_ERR_INVALID, "%s: ldh must be >= N", fn);
+  if (!(damp >= 0.0 && damp < INFINITY)) return fail(CRVQ_ERR_INVALID, "%s: damp must be finite and >= 0", fn);
+  if (N == 0) return CRVQ_OK;
+  if (!H || (!hinv && !scale)) return fail(CRVQ_ERR_INVALID, "%s: H and one of hinv, scale must not be NULL", fn);
+  crvq_status s = check_ws(workspace, ws_bytes, crvq_hessian_inverse_workspace_size(N), fn);
+  if (s) return s;
+  return hip_status(launch_hinv(H, ldh, N, damp, hinv, scale, workspace, static_cast<hipStream_t>(stream)), fn);
+}
+
 crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const double* R, int64_t ldr, const double* H,
                                  int64_t ldh, double* G, int64_t ldg, double* row_loss, double* loss_total,
                                  void* stream) {
@@ -656,6 +675,7 @@ size_t crvq_workspace_size(int op, int64_t n_vectors, int64_t K, int32_t beam, i
     case CRVQ_OP_CODE_SUMS: return crvq_code_sums_workspace_size(n_vectors, d, K);
     case CRVQ_OP_REFINE: return crvq_refine_workspace_size(M, N, n_cols);
     case CRVQ_OP_GEMV: return crvq_gemv_workspace_size(M, N, K);
+    case CRVQ_OP_HINV: return crvq_hessian_inverse_workspace_size(N);
     default: return 0;
   }
 }

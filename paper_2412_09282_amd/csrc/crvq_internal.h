@@ -202,6 +202,11 @@ hipError_t launch_gemm_f64(int64_t M, int64_t Nc, int64_t Kd, const void* A, int
 hipError_t launch_row_dot(int64_t M, int64_t n, const double* A, int64_t lda, const double* B, int64_t ldb,
                           double* out, hipStream_t stream);
 hipError_t launch_sum_f64(int64_t n, const double* x, double* out, hipStream_t stream);
+
+// ---- inverse Hessian diagonal (k_hinv.hip) ------------------------------------------------------
+size_t hinv_ws_bytes(int64_t N);
+hipError_t launch_hinv(const double* H, int64_t ldh, int64_t N, double damp, double* hinv, float* scale, void* ws,
+                       hipStream_t stream);
 size_t code_sums_ws_bytes(int64_t n, int64_t K, int d);
 hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int64_t n, const int32_t* codes,
                             int64_t K, double* sums, int32_t* counts, void* ws, hipStream_t stream);

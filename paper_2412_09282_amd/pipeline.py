@@ -12,7 +12,8 @@ h = diag(X X^T) (the timed workloads), "w_only" I_j = max_i W_ij^2 (Sec. 4.1),
 "wa" I_j = h_j * max_i (W_ij - Wq_ij)^2 with Wq the prequantized W (Alg. 1
 Prequantize: the basic VQ of the unsorted W; the Hessian-proxy metric of
 Sec. 4.1 in the unpacked form of Appendix A.2 Eq. 10 without its uniform
-factor 1/2); the critical channels
+factor 1/2), "obs" Eq. 7 as printed, I_j = max_i (W_ij - Wq_ij)^2 /
+(2 [(X X^T)^-1]_jj), the inverse taken of H + damp * mean(diag H) * I; the critical channels
 are the first d * ceil(lambda N / d) reordered columns; K-means starts from the
 vectors at given indices, one iteration is assign + update, `iters` iterations
 are followed by a final assign, an empty cluster keeps its centroid; stored
@@ -49,8 +50,9 @@ class LayerConfig:
     crit_frac: float
     beam: int
     iters: int
-    importance: str = "energy"  # "energy" | "w_only" | "wa"
+    importance: str = "energy"  # "energy" | "w_only" | "wa" | "obs"
     m_base: int = 1             # basic codebooks covering every vector (2 in the m = 2, d = 16 setting)
+    damp: float = 0.01          # "obs": the inverse is taken of H + damp * mean(diag H) * I
 
 
 def n_crit_columns(N: int, d: int, frac: float) -> int:
@@ -107,12 +109,15 @@ class LayerQuantizer:
                                            for _ in range(cfg.m_base - 1)]
         if cfg.m_base > 1:
             self.E_all = [torch.empty(M, N, dtype=f32, device=device) for _ in range(min(2, cfg.m_base - 1))]
-        if cfg.importance not in ("energy", "w_only", "wa"):
+        if cfg.importance not in ("energy", "w_only", "wa", "obs"):
             raise ValueError(f"importance {cfg.importance!r}")
-        if cfg.importance == "wa":  # Prequantize buffers: the basic VQ of the unsorted W
+        if cfg.importance in ("wa", "obs"):  # Prequantize buffers: the basic VQ of the unsorted W
             self.C_pre = torch.empty(cfg.K_base, d, dtype=dtype, device=device)
             self.codes_pre = torch.empty(self.n, dtype=i32, device=device)
             self.W_pre = torch.empty(M, N, dtype=dtype, device=device)
+        if cfg.importance == "obs":  # Eq. 7: the Hessian proxy and its inverse's diagonal
+            self.H = torch.empty(N, N, dtype=torch.float64, device=device)
+            self.obs_scale = torch.empty(N, dtype=f32, device=device)
 
     def run(self, W: torch.Tensor, X: torch.Tensor, base_idx: torch.Tensor, ext_idx: List[torch.Tensor],
             trace: Optional[list] = None, hooks=(), base_idx_extra: Sequence[torch.Tensor] = ()) -> LayerState:
@@ -144,8 +149,17 @@ class LayerQuantizer:
             rec.pre("prequant", codes=self.codes_pre, book=self.C_pre)
             C.crvq_dequant(M, N, d, self.codes_pre, N // d, self.C_pre, self.W_pre)
             rec.post("prequant", out=self.W_pre)
-            rec.pre("importance", A=W, B=self.W_pre, scale=self.hdiag)
-            C.crvq_channel_importance(W, self.imp, B=self.W_pre, scale=self.hdiag, reduce=C.CRVQ_REDUCE_MAX)
+            scale = self.hdiag
+            if cfg.importance == "obs":
+                rec.pre("gram", X=X)
+                C.crvq_gram(X, self.H)
+                rec.post("gram", H=self.H)
+                rec.pre("hinv", H=self.H)
+                C.crvq_hessian_inverse_diagonal(self.H, scale=self.obs_scale, damp=cfg.damp)
+                rec.post("hinv", scale=self.obs_scale)
+                scale = self.obs_scale
+            rec.pre("importance", A=W, B=self.W_pre, scale=scale)
+            C.crvq_channel_importance(W, self.imp, B=self.W_pre, scale=scale, reduce=C.CRVQ_REDUCE_MAX)
         rec.post("importance", out=self.imp)
 
         rec.pre("reorder", inp=W, importance=self.imp)

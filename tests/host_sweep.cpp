@@ -5,7 +5,8 @@
 // computed its grid, workspace layout and split plan.
 //
 // Covered: plan_screen / carve_screen for top 1..16, gemm_split_parts and the split-k GEMM launcher,
-// the refinement, code-sum, K-means, column-reduction, reorder, dequant and GEMV sizers, and every
+// the refinement, code-sum, K-means, column-reduction, reorder, dequant, GEMV and inverse-Hessian
+// sizers, and every
 // public entry point with shapes at and around the tile sizes (1, 15, 16, 17, 511, 512, 1024, ...),
 // vector sets narrower than d, and n_cols below d.
 #include <cstdio>
@@ -88,6 +89,7 @@ int main() {
       (void)crvq_reorder_workspace_size(N);
       for (int64_t nc : {int64_t{1}, int64_t{8}, N}) (void)crvq_refine_workspace_size(M, N, nc);
       if (N % 64 == 0) (void)gemv_ws_bytes(M, N, 256);
+      (void)crvq_hessian_inverse_workspace_size(N);
     }
 
   // every entry point on valid shapes (fake device pointers, enough workspace)
@@ -153,6 +155,10 @@ int main() {
                                             nullptr),
                        "crvq_hessian_product");
       expect_ok_or_hip(crvq_gram(X, CRVQ_F32, M, N, N, static_cast<double*>(fake(24)), N, nullptr), "crvq_gram");
+      expect_ok_or_hip(crvq_hessian_inverse_diagonal(static_cast<const double*>(fake(22)), N, N, 0.01,
+                                                     static_cast<double*>(fake(28)), static_cast<float*>(fake(29)),
+                                                     ws, big, nullptr),
+                       "crvq_hessian_inverse_diagonal");
       if (N % 64 == 0)
         expect_ok_or_hip(crvq_dequant_gemv(M, N, 8, static_cast<const uint8_t*>(fake(27)), N / 8, Cb, CRVQ_BF16,
                                            256, 0, nullptr, 0, nullptr, nullptr, nullptr, codes, X, CRVQ_F32,

@@ -279,6 +279,16 @@ def test_refinement_validation(L):
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 31, ws, need, None) == 1
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 32, ws, need - 1, None) == 3
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 2, 256, FAKE, 32, ws, need, None) == 1
+    dbl = ctypes.c_double
+    nh = L.crvq_hessian_inverse_workspace_size(100)
+    assert nh >= 16 * 128 * 128 and L.crvq_hessian_inverse_workspace_size(0) == 0
+    assert L.crvq_hessian_inverse_diagonal(FAKE, 99, 100, dbl(0.01), FAKE, None, ws, nh, None) == 1   # ldh < N
+    assert L.crvq_hessian_inverse_diagonal(FAKE, 100, 100, dbl(-0.5), FAKE, None, ws, nh, None) == 1  # damp < 0
+    assert L.crvq_hessian_inverse_diagonal(FAKE, 100, 100, dbl(float("nan")), FAKE, None, ws, nh, None) == 1
+    assert L.crvq_hessian_inverse_diagonal(FAKE, 100, 100, dbl(0.01), None, None, ws, nh, None) == 1  # no output
+    assert L.crvq_hessian_inverse_diagonal(FAKE, 100, 100, dbl(0.01), FAKE, None, ws, nh - 1, None) == 3
+    assert L.crvq_hessian_inverse_diagonal(FAKE, 70000, 70000, dbl(0.01), FAKE, None, ws, nh, None) == 1
+    assert L.crvq_hessian_inverse_diagonal(None, 0, 0, dbl(0.01), None, None, None, 0, None) == 0     # N = 0
 
 
 def test_workspace_size_dispatcher(L):
@@ -302,5 +312,7 @@ def test_workspace_size_dispatcher(L):
     assert C.crvq_workspace_size("dequant", N=8192) == L.crvq_dequant_workspace_size(8192) > 0
     assert C.crvq_workspace_size("refine", M=300, N=2056, n_cols=64) == L.crvq_refine_workspace_size(300, 2056, 64) > 0
     assert C.crvq_workspace_size("gemv", M=11008, N=4096, K=256) == L.crvq_gemv_workspace_size(11008, 4096, 256) > 0
+    assert C.crvq_workspace_size("hinv", N=4097) == L.crvq_hessian_inverse_workspace_size(4097) >= 16 * 4160 ** 2
+    assert C.crvq_workspace_size("hinv", N=65537) == 0
     assert L.crvq_workspace_size(99, 100, 16, 1, 1, 8, None, 1, 1, 1) == 0
     assert C.crvq_workspace_size("assign", n_vectors=100, d=8, K=65537) == 0

@@ -1,6 +1,7 @@
 """GPU parity of the channel-importance strategies of Sec. 4.1 / Table 2 through the layer pipeline:
-W-only (I_j = max_i W_ij^2) and W-A (I_j = h_j max_i (W_ij - Wq_ij)^2, Wq the prequantized W of
-Alg. 1 Prequantize).  Every call the pipeline makes for the strategy is re-run on the oracle from the
+W-only (I_j = max_i W_ij^2), W-A in the unpacked form of Eq. 10 (I_j = h_j max_i (W_ij - Wq_ij)^2, Wq the
+prequantized W of Alg. 1 Prequantize) and W-A as Eq. 7 prints it (I_j = max_i (W_ij - Wq_ij)^2 /
+(2 [(X X^T)^-1]_jj), the proxy damped by 1 %).  Every call the pipeline makes for the strategy is re-run on the oracle from the
 GPU's own inputs (lockstep), then the whole layer is compared with the oracle's pipeline: the same
 permutation, critical set and reconstruction error."""
 import numpy as np
@@ -17,7 +18,8 @@ from gpu_util import check_codes, dev, rel_close, say, to_host_bits
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("mode,dtype", [("w_only", "f32"), ("wa", "f32"), ("wa", "bf16")])
+@pytest.mark.parametrize("mode,dtype", [("w_only", "f32"), ("wa", "f32"), ("wa", "bf16"), ("obs", "f32"),
+                                        ("obs", "bf16")])
 def test_importance_strategy_lockstep(mode, dtype):
     M, N, d = 96, 128, 8
     say(f"importance strategy {mode} {dtype} {M}x{N}")
@@ -40,7 +42,7 @@ def test_importance_strategy_lockstep(mode, dtype):
     bits = lambda t: to_host_bits(t) if isinstance(t, torch.Tensor) else t
     h = bits(calls["hdiag"]["out"]["out"])
     # lockstep: the prequantization calls and the importance
-    if mode == "wa":
+    if mode in ("wa", "obs"):
         Vu = oracle.vectors(W, d)
         for name, c in calls.items():
             if name.startswith("assign_pre"):
@@ -55,7 +57,16 @@ def test_importance_strategy_lockstep(mode, dtype):
         R = oracle.reconstruct([bits(c["in"]["codes"])], [bits(c["in"]["book"])], np.zeros(n, np.uint8), [dtype])
         Wq = oracle.round_to(R, dtype).reshape(M, N)
         np.testing.assert_array_equal(bits(c["out"]["out"]), Wq)
-        exp_I = oracle.colreduce(W, Wq, scale=h.astype(np.float64), reduce="max", dtype=dtype)
+        scale = h.astype(np.float64)
+        if mode == "obs":
+            X64 = X.astype(np.float64)
+            H = bits(calls["gram"]["out"]["H"])
+            assert np.all(np.abs(H - X64.T @ X64) <= 1e-12 * (np.abs(X64).T @ np.abs(X64))), "gram"
+            s_got = bits(calls["hinv"]["out"]["scale"]).astype(np.float64)
+            s_exp = oracle.obs_scale(oracle.hessian_inverse_diagonal(bits(calls["hinv"]["in"]["H"]), 0.01))
+            rel_close(s_got, s_exp, 1e-6, "Eq. 7 factor")
+            scale = s_got
+        exp_I = oracle.colreduce(W, Wq, scale=scale, reduce="max", dtype=dtype)
     else:
         exp_I = oracle.colreduce(W, reduce="max", dtype=dtype)
     got_I = bits(calls["importance"]["out"]["out"])

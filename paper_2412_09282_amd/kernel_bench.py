@@ -41,14 +41,15 @@ def timed(fn, reps, flush=None):
     return float(np.median(ts))
 
 
-def report(name, ms, nbytes=None, flops=None, **extra):
+def report(name, ms, nbytes=None, flops=None, peak_tflops=F16_MFMA_TFLOPS, **extra):
     out = {"call": name, "ms": round(ms, 4)}
     if nbytes is not None:
         gbs = nbytes / (ms * 1e-3) / 1e9
         out.update({"bound": "hbm", "bytes": int(nbytes), "GB/s": round(gbs, 1), "frac": round(gbs / HBM_GBS, 4)})
     if flops is not None:
         tf = flops / (ms * 1e-3) / 1e12
-        out.update({"bound": "mfma", "flop": int(flops), "TFLOP/s": round(tf, 2), "frac": round(tf / F16_MFMA_TFLOPS, 4)})
+        out.update({"bound": "mfma", "flop": int(flops), "TFLOP/s": round(tf, 2), "frac": round(tf / peak_tflops, 4),
+                    "peak_tflops": peak_tflops})
     out.update(extra)
     print(json.dumps(out), flush=True)
 
@@ -58,6 +59,8 @@ def main(argv=None):
     ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--reps", type=int, default=10)
     ap.add_argument("--skip-assign", action="store_true")
+    ap.add_argument("--hinv", action="store_true",
+                    help="also time the Eq. 7 pieces: the fp64 proxy and the diagonal of its damped inverse")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="start with a plain 1 GiB device-to-device copy (the reference for HBM counters)")
     a = ap.parse_args(argv)
@@ -84,6 +87,16 @@ def main(argv=None):
     h = torch.empty(N, dtype=torch.float32, device="cuda")
     ms = timed(lambda: C.crvq_channel_importance(Xd, h), a.reps, flush)
     report("crvq_channel_importance (Hessian diagonal, X tokens x N)", ms, nbytes=X.size * 4 + N * 4, shape=[L.tokens, N])
+    if a.hinv:
+        # Eq. 7's denominator: the fp64 proxy H = X^T X, then the diagonal of its damped inverse
+        H = torch.empty(N, N, dtype=torch.float64, device="cuda")
+        ms = timed(lambda: C.crvq_gram(Xd, H), max(2, a.reps // 5), flush)
+        report("crvq_gram (H = X^T X, fp64)", ms, flops=2.0 * L.tokens * N * N, peak_tflops=78.6, shape=[L.tokens, N])
+        sc = torch.empty(N, dtype=torch.float32, device="cuda")
+        ms = timed(lambda: C.crvq_hessian_inverse_diagonal(H, scale=sc, damp=0.01), max(2, a.reps // 5), flush)
+        report("crvq_hessian_inverse_diagonal (fp64 Cholesky + inverse factor)", ms, flops=2.0 * N ** 3 / 3,
+               peak_tflops=78.6, N=N)
+        del H
     imp = torch.empty(N, dtype=torch.float32, device="cuda")
     ms = timed(lambda: C.crvq_channel_importance(Wd, imp, scale=h), a.reps, flush)
     report("crvq_channel_importance (W, scale = h)", ms, nbytes=M * N * es + 2 * N * 4, shape=[M, N])

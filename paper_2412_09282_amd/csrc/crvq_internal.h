@@ -115,6 +115,9 @@ struct ScreenWs {
   float* prm;    // binning parameters and the scaled largest codeword norm [4]
   int* rkey;     // row keys [n_rows]
   int* rord;     // rows in key order [n_rows]
+  float* tD;     // the first screen's exact distance of each uncertain row, per-block slices [n_rows
+                 // rounded up to 256], then compacted beside the row list into lD [n_rows]
+  float* lD;
 };
 // Carves the screen's scratch out of `ws`; returns it (pointers null on a dry run).
 ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t K_alloc);

@@ -74,6 +74,12 @@
 #ifndef CRVQ_PRUNE_FIRST
 #define CRVQ_PRUNE_FIRST 4  // chunks screened before the first band; the band is renewed after 2x, 4x, ...
 #endif
+#ifndef CRVQ_PRUNE2
+#define CRVQ_PRUNE2 1  // the second screen after a pruned first one skips chunks too (fixed bands)
+#endif
+#ifndef CRVQ_PRUNE2_SB
+#define CRVQ_PRUNE2_SB 1
+#endif
 #ifndef CRVQ_PRUNE_CAP
 #define CRVQ_PRUNE_CAP 128  // ... and then every this many chunks
 #endif
@@ -755,6 +761,7 @@ struct PruneData {
   const int* rord;          // rows in key order
   const int* rkey;          // key of every row
   const float* prm;         // {max ||c||, min c_j, max c_j, scaled max ||c|| rounded up}
+  const float* lD;          // second screen: per listed row, its first-screen exact distance rounded up
   int jp;                   // the coordinate j
 };
 
@@ -776,6 +783,25 @@ __device__ __forceinline__ float f32_down(double x) {
 __device__ __forceinline__ float f32_up(double x) {
   float f = static_cast<float>(x);
   if (static_cast<double>(f) < x) f = (f >= 0.0f) ? __uint_as_float(__float_as_uint(f) + 1u) : -0.0f;
+  return f;
+}
+
+// The float next to finite f towards +inf / -inf (bit steps; a zero steps to the smallest subnormal).
+__device__ __forceinline__ float f32_next_up(float f) {
+  if (f == 0.0f) return __uint_as_float(1u);
+  const uint32_t u = __float_as_uint(f);
+  return __uint_as_float(f > 0.0f ? u + 1u : u - 1u);
+}
+__device__ __forceinline__ float f32_next_down(float f) { return -f32_next_up(-f); }
+// float at or below / at or above any double (the bounds of a band that may be negative)
+__device__ __forceinline__ float f32_down_any(double x) {
+  float f = static_cast<float>(x);
+  if (static_cast<double>(f) > x) f = f32_next_down(f);
+  return f;
+}
+__device__ __forceinline__ float f32_up_any(double x) {
+  float f = static_cast<float>(x);
+  if (static_cast<double>(f) < x) f = f32_next_up(f);
   return f;
 }
 
@@ -1261,8 +1287,12 @@ __global__ __launch_bounds__(256) void prep_codebook_s32(const void* __restrict_
 // LIST: the rows are list[0 .. *list_n), and results go to their list positions (the second screen
 // of the rows the first one left uncertain).
 // QS (LIST only): the four waves of a block share their rows and split the codebook (few listed rows).
-// PRUNE (first screen only): rows in key order (pd.rord), results at the rows' own indices, chunks
-// visited outward from the wave's key and skipped when outside every row's band (see PruneData).
+// PRUNE, first screen: rows in key order (pd.rord), results at the key positions, chunks visited
+// outward from the wave's key and skipped when outside every row's band (see PruneData).
+// PRUNE with LIST (second screen after a pruned first one): the listed rows are in key order and each
+// has an exact upper bound on its best distance from the first screen (pd.lD), so the bands are fixed
+// from the start; the chunks meeting them are listed once and screened in order (QS: every fourth
+// to each wave).
 // corder (when the codebook is packed in key order): sorted position -> codeword.
 template <int CB, int NC, bool ONE, bool LIST, bool QS = false, bool PRUNE = false>
 __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_t* apack,
@@ -1273,7 +1303,9 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
                                                        const int* __restrict__ list, const int* __restrict__ list_n,
                                                        const int* __restrict__ corder, PruneData pd, double bacc,
                                                        double bsplit) {
-  static_assert(!PRUNE || (ONE && !LIST && !QS), "pruning is for the first screen");
+  constexpr bool PRUNE1 = PRUNE && !LIST, PRUNE2 = PRUNE && LIST;
+  static_assert(!PRUNE1 || (ONE && !QS), "the first screen's pruning walks rows of its own");
+  static_assert(!PRUNE2 || !ONE, "the pruned list screen is the split form");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int j = lane & 31;
@@ -1288,7 +1320,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   static_assert(LIST || !QS, "the shared-row split is for listed rows");
   // PRUNE: blocks take the key order from its upper end, where the bands are widest, so that the
   // longest waves start first
-  const int64_t bx = PRUNE ? static_cast<int64_t>(gridDim.x) - 1 - blockIdx.x : static_cast<int64_t>(blockIdx.x);
+  const int64_t bx = PRUNE1 ? static_cast<int64_t>(gridDim.x) - 1 - blockIdx.x : static_cast<int64_t>(blockIdx.x);
   const int64_t row0 = QS ? static_cast<int64_t>(blockIdx.x) * (32 * CB)
                           : (bx * 4 + wave) * (32 * CB);
   if (row0 >= n) return;  // uniform over the block in QS mode; the only barrier is below
@@ -1298,8 +1330,10 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   __shared__ float sR[QS ? 4 : 1][QS ? 32 * CB : 1];
   // PRUNE: per row alpha ||x||, alpha x_j and the scaled D_up offset (negative: the row takes no part);
   // per wave the lists of chunks above and below its start
-  __shared__ float sBand[PRUNE ? 4 : 1][PRUNE ? CB : 1][3][32];
-  __shared__ uint16_t sList[PRUNE ? 4 : 1][2][PRUNE ? 1024 : 1];
+  __shared__ float sBand[PRUNE1 ? 4 : 1][PRUNE1 ? CB : 1][3][32];
+  __shared__ uint16_t sList[PRUNE ? 4 : 1][PRUNE1 ? 2 : 1][PRUNE ? 1024 : 1];
+  // PRUNE2: the wave's union band, as float bounds {lo1, hi1, lo2, hi2} in the scaled units
+  float blo1 = __builtin_inff(), bhi1 = -__builtin_inff(), blo2 = __builtin_inff(), bhi2 = -__builtin_inff();
 
   h8 b1[CB], b2[CB];
   bool forced[CB];
@@ -1308,7 +1342,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     const int64_t i = row0 + cb * 32 + j;
     const bool ok = i < n;
     float v[8];
-    const int64_t off = ok ? row_offset(src, LIST ? list[i] : (PRUNE ? pd.rord[i] : i)) : 0;
+    const int64_t off = ok ? row_offset(src, LIST ? list[i] : (PRUNE1 ? pd.rord[i] : i)) : 0;
     if (src.type == ET_F32) {
       load_f32_elems<8>(static_cast<const float*>(src.base) + off, d, ok, v);
     } else if (src.type == ET_BF16) {
@@ -1336,7 +1370,26 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     b1[cb] = __builtin_bit_cast(h8, p1);
     b2[cb] = __builtin_bit_cast(h8, p2);
     forced[cb] = over;
-    if (PRUNE && h == 0) {
+    if (PRUNE2 && h == 0 && ok && !over) {
+      // |x| and x_j exactly (fp64) and the first screen's exact distance (rounded up): every codeword
+      // that can tie or beat it lies within sqrt(D) of them; bounds rounded outward with 2^-20
+      // relative and 2^-10 absolute margins in the scaled units
+      double xn2 = 0.0, xj = 0.0;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        xn2 = xn2 + static_cast<double>(v[t]) * static_cast<double>(v[t]);
+        xj = (t == pd.jp) ? static_cast<double>(v[t]) : xj;
+      }
+      const double a = static_cast<double>(alpha);
+      const double An = sqrt(xn2) * a, Pj = xj * a;
+      const double r = sqrt(static_cast<double>(pd.lD[i])) * a;
+      const double m1 = 0x1p-20 * (An + r) + 0x1p-10, m2 = 0x1p-20 * (fabs(Pj) + r) + 0x1p-10;
+      blo1 = fminf(blo1, f32_down_any(An - r - m1));
+      bhi1 = fmaxf(bhi1, f32_up_any(An + r + m1));
+      blo2 = fminf(blo2, f32_down_any(Pj - r - m2));
+      bhi2 = fmaxf(bhi2, f32_up_any(Pj + r + m2));
+    }
+    if (PRUNE1 && h == 0) {
       // the row's band terms in units of alpha: ||x|| and x_j exactly (fp64), and
       // D_up - m = alpha^2 ||x||^2 + alpha^2 delta(R = max ||c||), rounded up
       double xn2 = 0.0, xj = 0.0;
@@ -1367,7 +1420,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
 
   int64_t t0 = static_cast<int64_t>(split) * tps;
   int64_t t1 = (t0 + tps < tiles) ? t0 + tps : tiles;
-  if (QS) {
+  if (QS && !PRUNE2) {
     const int64_t q = (t1 - t0 + 7) / 8 * 2;  // even shares: chunks of two tiles stay aligned
     const int64_t a = t0 + __builtin_amdgcn_readfirstlane(wave) * q;  // wave-uniform: scalar bounds
     t1 = (a + q < t1) ? a + q : t1;
@@ -1423,7 +1476,65 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     };
     static_assert(NC == 1 || NC == 2, "chunks of one or two tiles");
     static_assert(!PRUNE || NC == 2, "pruning works on chunks of two tiles");
-    if (PRUNE) {
+    if constexpr (PRUNE2) {
+      // the wave's band (its rows' union), then the chunks of the split's range that meet it, listed
+      // in LDS in ascending order; the loads of the next chunk are issued before the current one's MFMAs
+#pragma unroll
+      for (int sh = 1; sh < 64; sh <<= 1) {
+        blo1 = fminf(blo1, __shfl_xor(blo1, sh));
+        bhi1 = fmaxf(bhi1, __shfl_xor(bhi1, sh));
+        blo2 = fminf(blo2, __shfl_xor(blo2, sh));
+        bhi2 = fmaxf(bhi2, __shfl_xor(bhi2, sh));
+      }
+      PruneCursor cur = {0, 0, 0, 0, 0, rfl(okey(blo1)), rfl(okey(bhi1)), rfl(okey(blo2)), rfl(okey(bhi2))};
+      const int c0 = static_cast<int>(t0 >> 1), c1 = static_cast<int>(t1 >> 1);
+      uint16_t* Lc = &sList[wave][0][0];
+      int cnt = 0;
+      const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
+      for (int cb0 = c0; cb0 < c1; cb0 += 64) {
+        const int c = cb0 + lane;
+        const bool keep = c < c1 && prune_keep(pd.cbnd[c < c1 ? c : c0], cur);
+        const uint64_t km = __ballot(keep);
+        if (keep) Lc[cnt + __popcll(km & lt)] = static_cast<uint16_t>(c);
+        cnt += __popcll(km);
+      }
+      cnt = static_cast<int>(rfl(static_cast<uint32_t>(cnt)));
+      const int step = QS ? 4 : 1;
+      int li = QS ? static_cast<int>(rfl(static_cast<uint32_t>(wave))) : 0;
+      auto next = [&]() {
+        const int c = li < cnt ? static_cast<int>(rfl(Lc[li])) : -1;
+        li += step;
+        return c;
+      };
+      h8 qa1, qa2, qb1, qb2;
+      int Cc = next();
+      int Cn = Cc >= 0 ? next() : -1;
+      if (Cc >= 0) {
+        load(2 * Cc, qa1, qa2);
+        load(2 * Cc + 1, qb1, qb2);
+      }
+      while (Cc >= 0) {
+        const int Tn = Cn >= 0 ? 2 * Cn : 2 * Cc;
+        tile(qa1, qa2, true);
+        load(Tn, qa1, qa2);
+        // the first tile's minima are complete before the second tile's matrix products start (left
+        // to the compiler, both tiles' accumulators were live at once: twice the registers)
+        if (CRVQ_PRUNE2_SB) {
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) __asm__ volatile("" : "+v"(cm[cb]));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        tile(qb1, qb2, false);
+        if (CRVQ_PRUNE2_SB) {
+#pragma unroll
+          for (int cb = 0; cb < CB; ++cb) __asm__ volatile("" : "+v"(cm[cb]));
+        }
+        fold(2 * Cc);
+        load(Tn + 1, qb1, qb2);
+        Cc = Cn;
+        Cn = Cn >= 0 ? next() : -1;
+      }
+    } else if constexpr (PRUNE1) {
       // Chunks (tile pairs) from the wave's key outward, alternately above and below; a side stops
       // where the envelope leaves the norm band, a chunk is skipped when outside either band.  The
       // bands start open and narrow as the running minima fall (recomputed after 4, 8, 16, ...
@@ -1501,7 +1612,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     const int64_t i = row0 + cb * 32 + j;
     const bool valid = i < n;
     // the row's index in the source; results go to the row's position i (list or key order)
-    const int64_t pi = (LIST && valid) ? list[i] : ((PRUNE && valid) ? pd.rord[i] : i);
+    const int64_t pi = (LIST && valid) ? list[i] : ((PRUNE1 && valid) ? pd.rord[i] : i);
     const int64_t oi = i;
     const float mg = m[cb];
     const float om = __shfl_xor(mg, 32);
@@ -1980,7 +2091,8 @@ __global__ __launch_bounds__(256) void finalize1_first_kernel(int64_t n, int spl
                                                               const double* __restrict__ pD, const int* __restrict__ pK,
                                                               const double* __restrict__ xn2a, ScreenBound bound,
                                                               const int* __restrict__ rmap,
-                                                              int* __restrict__ tmp, int* __restrict__ bcount,
+                                                              int* __restrict__ tmp, float* __restrict__ tmpD,
+                                                              int* __restrict__ bcount,
                                                               int32_t* __restrict__ codes, float* __restrict__ dist,
                                                               double* __restrict__ rowD, int* __restrict__ rowK) {
   __shared__ int s_wc[4];
@@ -1995,7 +2107,15 @@ __global__ __launch_bounds__(256) void finalize1_first_kernel(int64_t n, int spl
   __syncthreads();
   int woff = 0;
   for (int u = 0; u < w; ++u) woff += s_wc[u];
-  if (fail) tmp[static_cast<int64_t>(blockIdx.x) * 256 + woff + __popcll(m & ((1ull << lane) - 1ull))] = static_cast<int>(row);
+  if (fail) {
+    const int64_t slot = static_cast<int64_t>(blockIdx.x) * 256 + woff + __popcll(m & ((1ull << lane) - 1ull));
+    tmp[slot] = static_cast<int>(row);
+    if (tmpD) {  // the row's tentative exact distance, rounded up: a bound for the second screen's bands
+      double Dt = pD[i];
+      for (int sp = 1; sp < splits; ++sp) Dt = fmin(Dt, pD[static_cast<int64_t>(sp) * n + i]);
+      tmpD[slot] = f32_up_any(Dt);
+    }
+  }
   if (threadIdx.x == 0) bcount[blockIdx.x] = s_wc[0] + s_wc[1] + s_wc[2] + s_wc[3];
 }
 
@@ -2026,11 +2146,14 @@ __global__ __launch_bounds__(1024) void scan_counts_kernel(const int* __restrict
 }
 
 // rlist[offs[b] + j] = tmp[256 b + j] for j < cnt[b]: the per-block slices packed in block order.
-__global__ __launch_bounds__(256) void compact_list_kernel(const int* __restrict__ tmp, const int* __restrict__ cnt,
-                                                           const int* __restrict__ offs, int* __restrict__ rlist) {
+__global__ __launch_bounds__(256) void compact_list_kernel(const int* __restrict__ tmp, const float* __restrict__ tmpD,
+                                                           const int* __restrict__ cnt, const int* __restrict__ offs,
+                                                           int* __restrict__ rlist, float* __restrict__ rlistD) {
   const int b = blockIdx.x;
-  if (static_cast<int>(threadIdx.x) < cnt[b])
+  if (static_cast<int>(threadIdx.x) < cnt[b]) {
     rlist[offs[b] + threadIdx.x] = tmp[static_cast<int64_t>(b) * 256 + threadIdx.x];
+    if (tmpD) rlistD[offs[b] + threadIdx.x] = tmpD[static_cast<int64_t>(b) * 256 + threadIdx.x];
+  }
 }
 
 // Top-1 finalize of a second screen over a row list (rows list[0 .. *list_n), their screen results at
@@ -2762,6 +2885,7 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
   w.cbnd = nullptr;
   w.cminS = w.cmaxP = nullptr;
   w.prm = nullptr;
+  w.tD = w.lD = nullptr;
   if (p.s32) {
     // 32-codeword tiles of 768 fp16, the scale reduction's partial maxima and alpha
     const int64_t t32 = p.tiles > cdiv(K_alloc, kS32Tile) ? p.tiles : cdiv(K_alloc, kS32Tile);
@@ -2780,6 +2904,8 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
       w.prm = ws.take<float>(4 + 3 * kPruneParts);  // the parameters, then the partial ranges
       w.rkey = ws.take<int>(static_cast<size_t>(n_rows));
       w.rord = ws.take<int>(static_cast<size_t>(n_rows));
+      w.tD = ws.take<float>(static_cast<size_t>(cdiv(n_rows, 256) * 256));
+      w.lD = ws.take<float>(static_cast<size_t>(n_rows));
     }
   } else {
     // fp32: 64 lanes x ks floats per tile; split: 16 codewords x 16 bf16 per tile
@@ -2890,35 +3016,50 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       // results at key-order positions: certify by position, compact the uncertain rows, rescue them
       const int64_t nbx = cdiv(src.n, 256);
       hipLaunchKernelGGL(finalize1_first_kernel, dim3(static_cast<unsigned>(nbx)), dim3(256), 0, stream, src.n,
-                         p.splits, w.pR, w.pD, w.pK, w.xn2, b1, w.rord, w.rlist2, w.bcount, out_codes, out_dist, rowD,
-                         rowK);
+                         p.splits, w.pR, w.pD, w.pK, w.xn2, b1, w.rord, w.rlist2, nullptr, w.bcount, out_codes, out_dist,
+                         rowD, rowK);
       hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, stream, w.bcount, nbx, w.bcount + nbx, w.rcount);
-      hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nbx)), dim3(256), 0, stream, w.rlist2,
-                         w.bcount, w.bcount + nbx, w.rlist);
+      hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nbx)), dim3(256), 0, stream, w.rlist2, nullptr,
+                         w.bcount, w.bcount + nbx, w.rlist, nullptr);
       return launch_rescue1<2>(src, top, C, ct, K, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK, w.pD, w.pK,
                                static_cast<int64_t>(p.splits) * src.n, stream);
     }
     const int64_t nb = cdiv(src.n, 256);
     // the uncertain rows, compacted through rlist2 (free until the second finalize) in row order
     hipLaunchKernelGGL(finalize1_first_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, src.n, p.splits,
-                       w.pR, w.pD, w.pK, w.xn2, b1, p.prune ? w.rord : nullptr, w.rlist2, w.bcount, out_codes, out_dist,
-                       rowD, rowK);
+                       w.pR, w.pD, w.pK, w.xn2, b1, p.prune ? w.rord : nullptr, w.rlist2, p.prune ? w.tD : nullptr,
+                       w.bcount, out_codes, out_dist, rowD, rowK);
     hipLaunchKernelGGL(scan_counts_kernel, dim3(1), dim3(1024), 0, stream, w.bcount, nb, w.bcount + nb, w.rcount);
-    hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, w.rlist2, w.bcount,
-                       w.bcount + nb, w.rlist);
+    hipLaunchKernelGGL(compact_list_kernel, dim3(static_cast<unsigned>(nb)), dim3(256), 0, stream, w.rlist2,
+                       p.prune ? w.tD : nullptr, w.bcount, w.bcount + nb, w.rlist, p.prune ? w.lD : nullptr);
     // Second screen, split form (two MFMAs per tile, the tight bound), over the rows the first one
     // left uncertain; what still fails goes to the exact rescue.
     // The listed rows are typically 7-9 % of n: below a few million rows the four waves of a block
     // share 128 of them and split the codebook, above that every wave takes rows of its own.
+    // After a pruned first screen the listed rows are in key order with exact distance bounds, and
+    // the second screen skips the chunks outside their bands.
+    PruneData pd2 = pd;
+    pd2.lD = w.lD;
+    const bool prune2 = p.prune && CRVQ_PRUNE2;
     if (src.n < kS32SharedRowsMaxN) {
       const dim3 grid2(static_cast<unsigned>(cdiv(src.n, 32 * CRVQ_S32_CB)), static_cast<unsigned>(p.splits));
-      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true>), grid2, dim3(256), 0, stream,
-                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount,
-                         pd.corder, PruneData{}, 0.0, 0.0);
+      if (prune2)
+        hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true, true>), grid2, dim3(256), 0,
+                           stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
+                           w.rlist, w.rcount, pd.corder, pd2, 0.0, 0.0);
+      else
+        hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true>), grid2, dim3(256), 0,
+                           stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
+                           w.rlist, w.rcount, pd.corder, PruneData{}, 0.0, 0.0);
     } else {
-      hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false>), grid, dim3(256), 0, stream,
-                         src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, w.rlist, w.rcount,
-                         pd.corder, PruneData{}, 0.0, 0.0);
+      if (prune2)
+        hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false, true>), grid, dim3(256), 0,
+                           stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
+                           w.rlist, w.rcount, pd.corder, pd2, 0.0, 0.0);
+      else
+        hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false>), grid, dim3(256), 0,
+                           stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
+                           w.rlist, w.rcount, pd.corder, PruneData{}, 0.0, 0.0);
     }
     const ScreenBound b2 = screen_bound(p, src.type, ct, src.d, alpha);
     hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,

@@ -329,8 +329,10 @@ crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const doub
  * FineTuneCodebook when X holds -2 R H, or plain cluster sums).  X: vector set
  * (see conventions) of CRVQ_F64 elements; codes: int32[n]; codes outside
  * [0, K) belong to no code.  sums: K x d fp64; counts: int32[K] or NULL.
- * 1 <= K <= 1024.  Deterministic: every code's members are added in vector
- * order per block, the blocks in block order.
+ * 1 <= K <= 65536.  Deterministic: every code's members are added in vector
+ * order per block, the blocks in block order (K > 1024: the vectors are first
+ * grouped by the high byte of their code, and a code's members are added in
+ * vector order per chunk of its group, the chunks in order).
  * workspace: crvq_code_sums_workspace_size(n, d, K) bytes. */
 size_t crvq_code_sums_workspace_size(int64_t n_vectors, int32_t d, int64_t K);
 crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
@@ -360,8 +362,10 @@ crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, doub
  * with (R H) kept current as codes move: within a block of 64 columns by
  * delta^T H[g rows, block columns] per change, and for the later columns by one
  * product (the block's deltas) x H per block.  A code outside [0, K) leaves
- * that row's group unchanged.  K * d <= 8192 and (K d + K) * 8 bytes plus
- * 36 KiB must fit the 160 KiB LDS of a CU (K <= 1024 at d = 8).
+ * that row's group unchanged.  1 <= K <= 65536: a codebook that fits a CU's
+ * LDS (K d <= 8192) is searched from LDS by each workgroup's rows, group after
+ * group; a larger one one group at a time over all rows, in codebook slices
+ * merged per row (the same values and choices either way).
  * workspace: crvq_refine_workspace_size(M, N, n_cols) bytes. */
 size_t crvq_refine_workspace_size(int64_t M, int64_t N, int64_t n_cols);
 crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, double* R, int64_t ldr, const double* H,

@@ -588,7 +588,7 @@ crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const doub
 }
 
 size_t crvq_code_sums_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
-  if (n_vectors < 0 || d < 1 || d > CRVQ_MAX_D || K < 1 || K > 1024) return 0;
+  if (n_vectors < 0 || d < 1 || d > CRVQ_MAX_D || K < 1 || K > CRVQ_MAX_K) return 0;
   return code_sums_ws_bytes(n_vectors, K, d);
 }
 
@@ -600,7 +600,7 @@ crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row
   if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
   if (n_rows < 0 || vecs_per_row < 0) return fail(CRVQ_ERR_INVALID, "%s: negative n_rows or vecs_per_row", fn);
   if (ld < vecs_per_row * d) return fail(CRVQ_ERR_INVALID, "%s: ld < vecs_per_row * d", fn);
-  if (K < 1 || K > 1024) return fail(CRVQ_ERR_UNSUPPORTED, "%s: K = %lld outside [1, 1024]", fn, (long long)K);
+  if (K < 1 || K > CRVQ_MAX_K) return fail(CRVQ_ERR_UNSUPPORTED, "%s: K = %lld outside [1, %d]", fn, (long long)K, CRVQ_MAX_K);
   const int64_t n = n_rows * vecs_per_row;
   if (n > 0x7fffffffLL) return fail(CRVQ_ERR_UNSUPPORTED, "%s: too many vectors", fn);
   if (!sums || (n > 0 && (!X || !codes))) return fail(CRVQ_ERR_INVALID, "%s: X, codes and sums must not be NULL", fn);
@@ -642,9 +642,7 @@ crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, d
   if (n_cols < 0 || n_cols > N || n_cols % d || N % d)
     return fail(CRVQ_ERR_INVALID, "%s: n_cols must be a multiple of d in [0, N] and d must divide N", fn);
   if (!dtype_ok(c_dtype)) return fail(CRVQ_ERR_INVALID, "%s: c_dtype must be F32 or BF16", fn);
-  if (K < 1 || K * d > 8192 || refine_lds_bytes(K, d) + 4096 > 160 * 1024)
-    return fail(CRVQ_ERR_UNSUPPORTED, "%s: K = %lld with d = %d exceeds K * d <= 8192 (and the LDS of one CU)", fn,
-                (long long)K, d);
+  if (K < 1 || K > CRVQ_MAX_K) return fail(CRVQ_ERR_UNSUPPORTED, "%s: K = %lld outside [1, %d]", fn, (long long)K, CRVQ_MAX_K);
   if (ldr < N || ldh < N || ldq < n_cols / d) return fail(CRVQ_ERR_INVALID, "%s: ldr, ldh >= N and ldq >= n_cols / d", fn);
   if (M == 0 || n_cols == 0) return CRVQ_OK;
   if (!R || !H || !C || !codes) return fail(CRVQ_ERR_INVALID, "%s: R, H, C and codes must not be NULL", fn);

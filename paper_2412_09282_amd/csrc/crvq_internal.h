@@ -211,6 +211,9 @@ size_t hinv_ws_bytes(int64_t N);
 hipError_t launch_hinv(const double* H, int64_t ldh, int64_t N, double damp, double* hinv, float* scale, void* ws,
                        hipStream_t stream);
 size_t code_sums_ws_bytes(int64_t n, int64_t K, int d);
+size_t code_sums_large_ws_bytes(int64_t n, int64_t K);
+hipError_t launch_code_sums_large(const RowSrc& src, const int32_t* codes, int64_t K, double* sums, int32_t* counts,
+                                  void* ws, hipStream_t stream);
 hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int64_t n, const int32_t* codes,
                             int64_t K, double* sums, int32_t* counts, void* ws, hipStream_t stream);
 hipError_t launch_adam(int64_t n, float* C, const double* grad, double scale, double* m, double* v, double lr,

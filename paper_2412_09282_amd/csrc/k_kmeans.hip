@@ -32,6 +32,7 @@ __device__ __forceinline__ int64_t row_offset(const RowSrc& s, int64_t i) {
 
 __device__ __forceinline__ double row_elem(const RowSrc& s, int64_t off, int t) {
   if (s.type == ET_F32) return static_cast<double>(static_cast<const float*>(s.base)[off + t]);
+  if (s.type == ET_F64) return static_cast<const double*>(s.base)[off + t];
   return static_cast<double>(bf16_to_f(static_cast<const uint16_t*>(s.base)[off + t]));
 }
 
@@ -314,7 +315,8 @@ __device__ __forceinline__ void add_vector(const RowSrc& s, int64_t off, double 
       }
       return;
     }
-  } else if (d == 8 && (reinterpret_cast<uintptr_t>(static_cast<const uint16_t*>(s.base) + off) & 15) == 0) {
+  } else if (s.type == ET_BF16 && d == 8 &&
+             (reinterpret_cast<uintptr_t>(static_cast<const uint16_t*>(s.base) + off) & 15) == 0) {
     const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(s.base) + off);
     const uint32_t u[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
@@ -817,6 +819,25 @@ __global__ __launch_bounds__(256) void bucket_final(const double* __restrict__ p
   if (cnt > 0) store_centroid(C, ct, k, d, t, acc / static_cast<double>(cnt));
 }
 
+// Per-code sums and counts instead of means (the gradient sums of the codebook fine-tuning).
+__global__ __launch_bounds__(256) void bucket_final_sums(const double* __restrict__ part, const int* __restrict__ pcount,
+                                                         const int* __restrict__ cstart, int64_t K, int d,
+                                                         double* __restrict__ sums, int32_t* __restrict__ counts) {
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= K * d) return;
+  const int64_t k = e / d;
+  const int t = static_cast<int>(e - k * d);
+  const int b = static_cast<int>(k >> 8), low = static_cast<int>(k & 255);
+  double acc = 0.0;
+  int cnt = 0;
+  for (int blk = cstart[b]; blk < cstart[b + 1]; ++blk) {
+    acc = acc + part[(static_cast<int64_t>(blk) * 256 + low) * d + t];
+    cnt += pcount[static_cast<int64_t>(blk) * 256 + low];
+  }
+  sums[e] = acc;
+  if (counts && t == 0) counts[k] = cnt;
+}
+
 struct KmWs {
   int* keys;
   int* vals;
@@ -873,6 +894,36 @@ size_t kmeans_ws_bytes(int64_t n, int64_t K) {
   }
   carve(c, n, K);
   return c.used;
+}
+
+size_t code_sums_large_ws_bytes(int64_t n, int64_t K) {
+  WsCursor c(nullptr);
+  carve(c, n, K);
+  return c.used;
+}
+
+// Per-code sums of the vectors of src (any element type, d <= 16) for 256 < K <= 65536: the radix
+// grouping of the large-codebook K-means update, with sums and counts as the result.  Every code's
+// members are added in ascending vector order within a chunk of its bucket, the chunks in order.
+hipError_t launch_code_sums_large(const RowSrc& src, const int32_t* codes, int64_t K, double* sums, int32_t* counts,
+                                  void* ws, hipStream_t stream) {
+  const int64_t n = src.n;
+  WsCursor cur(ws);
+  KmWs w = carve(cur, n, K);
+  const int64_t n_tiles = cdiv(n > 0 ? n : 1, kTile);
+  hipError_t e;
+  hipLaunchKernelGGL(radix_hist, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, codes, nullptr, n, K, 0, 8,
+                     n_tiles, w.hist);
+  if ((e = exclusive_scan(w.hist, 256 * n_tiles, w.sums, w.offs, w.n_valid, stream)) != hipSuccess) return e;
+  hipLaunchKernelGGL(radix_scatter, dim3(static_cast<unsigned>(n_tiles)), dim3(256), 0, stream, codes, nullptr, nullptr,
+                     n, K, 0, 8, n_tiles, w.offs, w.keys, w.vals);
+  hipLaunchKernelGGL(bucket_bounds, dim3(1), dim3(256), 0, stream, w.offs, n_tiles, w.n_valid, w.bstart, w.cstart,
+                     w.lstart);
+  hipLaunchKernelGGL(bucket_partial, dim3(static_cast<unsigned>(w.max_chunks)), dim3(256), 0, stream, src, w.keys,
+                     w.vals, w.bstart, w.cstart, w.part, w.pcount);
+  hipLaunchKernelGGL(bucket_final_sums, dim3(static_cast<unsigned>(cdiv(K * src.d, 256))), dim3(256), 0, stream,
+                     w.part, w.pcount, w.cstart, K, src.d, sums, counts);
+  return hipGetLastError();
 }
 
 hipError_t launch_kmeans_update(const RowSrc& src, const int32_t* codes, int64_t K, void* C, int c_type,

@@ -237,6 +237,7 @@ __global__ __launch_bounds__(256) void sum_f64_kernel(int64_t n, const double* _
 // ---- per-code sums ------------------------------------------------------------------------------
 constexpr int kCsVec = 256;      // vectors staged per round
 constexpr int kCsMaxOwn = 4;     // codes per thread (K <= 1024)
+constexpr int64_t kCsMaxK = 256 * kCsMaxOwn;  // larger books are grouped by a radix pass (k_kmeans.hip)
 
 // Block b sums the vectors [b * per_block, ...) of a vector set over an fp64 matrix (vector
 // v = r * vpr + g at element r * ld + g * d).  Thread t owns codes t, t + 256, ... and adds, in
@@ -574,6 +575,142 @@ __global__ __launch_bounds__(kRfThreads) void refine_block_kernel(int64_t M, int
   }
 }
 
+// ---- the same search for books too large for one CU's LDS ------------------------------------------
+// One group at a time over all rows: refine_scan_kernel finds, for 64 rows per workgroup and one slice
+// of the codebook per grid row y, the k minimising f(k) = a_k - 2 c_k . b (the formulas and orders of
+// refine_block_kernel, so the same values); refine_apply_kernel merges the slices (lowest k among equal
+// values) and moves the rows' codes, updating R, D and the block's later columns of S = R H in memory.
+constexpr int kRsRows = 64;      // rows per workgroup of the scan
+constexpr int kRsTile = 256;     // codewords staged in LDS per round
+constexpr int kRsMaxSlices = 8;  // codebook slices (grid y) at most
+
+template <int DMAX>
+__global__ __launch_bounds__(256) void refine_scan_kernel(int64_t M, int d, int64_t col, int64_t gq,
+                                                          const double* __restrict__ S, int64_t lds,
+                                                          const double* __restrict__ H, int64_t ldh,
+                                                          const void* __restrict__ Cb, int c_type, int K, int slice,
+                                                          const int32_t* __restrict__ codes, int64_t ldq,
+                                                          double* __restrict__ bestF, int* __restrict__ bestK) {
+  __shared__ double Hg[16 * 16];
+  __shared__ double sb[kRsRows][16];
+  __shared__ double Cs[kRsTile * 16];
+  __shared__ double Ak[kRsTile];
+  __shared__ double rf[4][kRsRows];
+  __shared__ int rk[4][kRsRows];
+  const int tid = threadIdx.x, row = tid & 63, sub = tid >> 6;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kRsRows;
+  const int k0 = static_cast<int>(blockIdx.y) * slice;
+  const int k1 = k0 + slice < K ? k0 + slice : K;
+  for (int e = tid; e < d * d; e += 256) Hg[e] = H[(col + e / d) * ldh + col + e % d];
+  __syncthreads();
+  // b = s + Hgg c_cur per row (a row with a code outside [0, K) takes no part)
+  for (int e = tid; e < kRsRows * d; e += 256) {
+    const int rr = e / d, t = e - rr * d;
+    const int64_t r = r0 + rr;
+    const int cur = r < M ? codes[r * ldq + gq] : -1;
+    double v = 0.0;
+    if (cur >= 0 && cur < K) {
+      double h = 0.0;
+      for (int u = 0; u < d; ++u) h = h + Hg[t * d + u] * book_elem(Cb, c_type, static_cast<int64_t>(cur) * d + u);
+      v = S[r * lds + col + t] + h;
+    }
+    sb[rr][t] = v;
+  }
+  __syncthreads();
+  double b[DMAX];
+#pragma unroll
+  for (int t = 0; t < DMAX; ++t) b[t] = t < d ? sb[row][t] : 0.0;
+  double best = __builtin_inf();
+  int bk = K;
+  for (int kt = k0; kt < k1; kt += kRsTile) {
+    const int tn = k1 - kt < kRsTile ? k1 - kt : kRsTile;
+    for (int e = tid; e < tn * d; e += 256) Cs[e] = book_elem(Cb, c_type, static_cast<int64_t>(kt) * d + e);
+    __syncthreads();
+    if (tid < tn) {  // a_k = c_k^T Hgg c_k
+      double a = 0.0;
+      for (int t = 0; t < d; ++t) {
+        double h = 0.0;
+        for (int u = 0; u < d; ++u) h = h + Hg[t * d + u] * Cs[tid * d + u];
+        a = a + Cs[tid * d + t] * h;
+      }
+      Ak[tid] = a;
+    }
+    __syncthreads();
+    for (int jj = sub; jj < tn; jj += 4) {
+      double dot = 0.0;
+#pragma unroll
+      for (int t = 0; t < DMAX; ++t)
+        if (t < d) dot = dot + Cs[jj * d + t] * b[t];
+      const double f = Ak[jj] - 2.0 * dot;
+      if (f < best) {
+        best = f;
+        bk = kt + jj;
+      }
+    }
+    __syncthreads();
+  }
+  rf[sub][row] = best;
+  rk[sub][row] = bk;
+  __syncthreads();
+  if (sub == 0 && r0 + row < M) {
+    for (int q = 1; q < 4; ++q)
+      if (rf[q][row] < best || (rf[q][row] == best && rk[q][row] < bk)) {
+        best = rf[q][row];
+        bk = rk[q][row];
+      }
+    bestF[static_cast<int64_t>(blockIdx.y) * M + r0 + row] = best;
+    bestK[static_cast<int64_t>(blockIdx.y) * M + r0 + row] = bk;
+  }
+}
+
+template <int DMAX>
+__global__ __launch_bounds__(256) void refine_apply_kernel(int64_t M, int d, int64_t c0, int cg, int bw, int64_t gq,
+                                                           double* __restrict__ R, int64_t ldr, double* __restrict__ S,
+                                                           int64_t lds, const double* __restrict__ H, int64_t ldh,
+                                                           const void* __restrict__ Cb, int c_type, int K,
+                                                           int32_t* __restrict__ codes, int64_t ldq,
+                                                           double* __restrict__ D, int64_t ldd, int nslice,
+                                                           const double* __restrict__ bestF,
+                                                           const int* __restrict__ bestK) {
+  const int64_t r = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (r >= M) return;
+  const int cur = codes[r * ldq + gq];
+  double best = __builtin_inf();
+  int bk = K;
+  for (int sl = 0; sl < nslice; ++sl) {
+    const double f = bestF[static_cast<int64_t>(sl) * M + r];
+    const int k = bestK[static_cast<int64_t>(sl) * M + r];
+    if (f < best || (f == best && k < bk)) {
+      best = f;
+      bk = k;
+    }
+  }
+  const bool moved = cur >= 0 && cur < K && bk < K && bk != cur;
+  double delta[DMAX];
+#pragma unroll
+  for (int t = 0; t < DMAX; ++t) {
+    delta[t] = 0.0;
+    if (t < d && moved)
+      delta[t] = book_elem(Cb, c_type, static_cast<int64_t>(bk) * d + t) -
+                 book_elem(Cb, c_type, static_cast<int64_t>(cur) * d + t);
+  }
+#pragma unroll
+  for (int t = 0; t < DMAX; ++t)
+    if (t < d) D[r * ldd + cg + t] = delta[t];
+  if (!moved) return;
+  codes[r * ldq + gq] = bk;
+#pragma unroll
+  for (int t = 0; t < DMAX; ++t)
+    if (t < d) R[r * ldr + c0 + cg + t] = R[r * ldr + c0 + cg + t] - delta[t];
+  for (int c = cg + d; c < bw; ++c) {
+    double acc = 0.0;
+#pragma unroll
+    for (int t = 0; t < DMAX; ++t)
+      if (t < d) acc = acc + delta[t] * H[(c0 + cg + t) * ldh + c0 + c];
+    S[r * lds + c0 + c] = S[r * lds + c0 + c] - acc;
+  }
+}
+
 }  // namespace
 
 // ---- launchers -----------------------------------------------------------------------------------
@@ -669,6 +806,7 @@ static int64_t code_sum_wave_blocks(int64_t n) {
 }
 
 size_t code_sums_ws_bytes(int64_t n, int64_t K, int d) {
+  if (K > kCsMaxK) return code_sums_large_ws_bytes(n, K);
   WsCursor c(nullptr);
   const int64_t nb = code_sum_blocks(n) > code_sum_wave_blocks(n) ? code_sum_blocks(n) : code_sum_wave_blocks(n);
   c.take<double>(static_cast<size_t>(nb * K * d));
@@ -678,6 +816,16 @@ size_t code_sums_ws_bytes(int64_t n, int64_t K, int d) {
 
 hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int64_t n, const int32_t* codes,
                             int64_t K, double* sums, int32_t* counts, void* ws, hipStream_t stream) {
+  if (K > kCsMaxK) {
+    RowSrc src;
+    src.base = X;
+    src.type = ET_F64;
+    src.d = d;
+    src.vpr = vpr;
+    src.ld = ld;
+    src.n = n;
+    return launch_code_sums_large(src, codes, K, sums, counts, ws, stream);
+  }
   if (K <= 256 && d <= 8 && n > 0) {
     WsCursor cw(ws);
     const int64_t nbw = code_sum_wave_blocks(n);
@@ -720,8 +868,13 @@ size_t refine_ws_bytes(int64_t M, int64_t n_cols, int64_t N) {
   return align256(static_cast<size_t>(M) * static_cast<size_t>(n_cols) * sizeof(double)) +
          align256(static_cast<size_t>(M) * kRbCols * sizeof(double)) +
          align256(static_cast<size_t>(gemm_split_parts(M, n_cols, N)) * static_cast<size_t>(M) *
-                  static_cast<size_t>(n_cols) * sizeof(double));
+                  static_cast<size_t>(n_cols) * sizeof(double)) +
+         align256(static_cast<size_t>(kRsMaxSlices) * static_cast<size_t>(M) * sizeof(double)) +
+         align256(static_cast<size_t>(kRsMaxSlices) * static_cast<size_t>(M) * sizeof(int));
 }
+
+// The codebook fits the block kernel's LDS (with H's block and the rows' S).
+bool refine_book_in_lds(int64_t K, int d) { return K * d <= 8192 && refine_lds_bytes(K, d) + 4096 <= 160 * 1024; }
 
 hipError_t launch_refine_book(int64_t M, int64_t N, int d, int64_t n_cols, double* R, int64_t ldr, const double* H,
                               int64_t ldh, const void* Cb, int c_type, int64_t K, int32_t* codes, int64_t ldq,
@@ -732,15 +885,44 @@ hipError_t launch_refine_book(int64_t M, int64_t N, int d, int64_t n_cols, doubl
   double* D = cur.take<double>(static_cast<size_t>(M) * kRbCols);
   double* parts = cur.take<double>(static_cast<size_t>(gemm_split_parts(M, n_cols, N)) * static_cast<size_t>(M) *
                                    static_cast<size_t>(n_cols));
+  double* bestF = cur.take<double>(static_cast<size_t>(kRsMaxSlices) * static_cast<size_t>(M));
+  int* bestK = cur.take<int>(static_cast<size_t>(kRsMaxSlices) * static_cast<size_t>(M));
   // S = R H[:, 0:n_cols]
   hipError_t e = launch_gemm_f64_split(M, n_cols, N, R, ldr, H, ldh, S, n_cols, parts, stream);
   if (e != hipSuccess) return e;
   const size_t lds = refine_lds_bytes(K, d);
   const dim3 grid(static_cast<unsigned>(cdiv(M, kRfRows)));
   const int64_t bw_max = (kRbCols / d) * d;
+  const bool in_lds = refine_book_in_lds(K, d);
+  // large books: enough codebook slices to give the scan about 512 workgroups
+  const int64_t row_tiles = cdiv(M, kRsRows);
+  int64_t nslice = cdiv(512, row_tiles);
+  nslice = nslice < kRsMaxSlices ? nslice : kRsMaxSlices;
+  nslice = nslice < cdiv(K, kRsTile) ? nslice : cdiv(K, kRsTile);
+  const int slice = static_cast<int>(cdiv(cdiv(K, nslice), kRsTile) * kRsTile);
+  nslice = cdiv(K, slice);
   for (int64_t c0 = 0; c0 < n_cols; c0 += bw_max) {
     const int bw = static_cast<int>(n_cols - c0 < bw_max ? n_cols - c0 : bw_max);
-    if (d <= 8)
+    if (!in_lds) {
+      for (int cg = 0; cg < bw; cg += d) {
+        const int64_t gq = c0 / d + cg / d;
+        const dim3 gs(static_cast<unsigned>(row_tiles), static_cast<unsigned>(nslice));
+        const unsigned ga = static_cast<unsigned>(cdiv(M, 256));
+        if (d <= 8) {
+          hipLaunchKernelGGL(refine_scan_kernel<8>, gs, dim3(256), 0, stream, M, d, c0 + cg, gq, S, n_cols, H, ldh, Cb,
+                             c_type, static_cast<int>(K), slice, codes, ldq, bestF, bestK);
+          hipLaunchKernelGGL(refine_apply_kernel<8>, dim3(ga), dim3(256), 0, stream, M, d, c0, cg, bw, gq, R, ldr, S,
+                             n_cols, H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq, D, bw_max,
+                             static_cast<int>(nslice), bestF, bestK);
+        } else {
+          hipLaunchKernelGGL(refine_scan_kernel<16>, gs, dim3(256), 0, stream, M, d, c0 + cg, gq, S, n_cols, H, ldh,
+                             Cb, c_type, static_cast<int>(K), slice, codes, ldq, bestF, bestK);
+          hipLaunchKernelGGL(refine_apply_kernel<16>, dim3(ga), dim3(256), 0, stream, M, d, c0, cg, bw, gq, R, ldr, S,
+                             n_cols, H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq, D, bw_max,
+                             static_cast<int>(nslice), bestF, bestK);
+        }
+      }
+    } else if (d <= 8)
       hipLaunchKernelGGL(refine_block_kernel<8>, grid, dim3(kRfThreads), lds, stream, M, d, c0, bw, R, ldr, S, n_cols,
                          H, ldh, Cb, c_type, static_cast<int>(K), codes, ldq, D, bw_max);
     else

@@ -117,10 +117,9 @@ int main() {
             expect_ok_or_hip(crvq_assign_residual_beam(X, CRVQ_F32, rows, vpr, vpr * d, d, 3, books, dts, Ks, beam,
                                                        cs, nullptr, dist, ws, big, nullptr),
                              "crvq_assign_residual_beam");
-          if (K <= 1024)
-            expect_ok_or_hip(crvq_code_sums(static_cast<const double*>(X), rows, vpr, vpr * d, d, codes, K,
-                                            static_cast<double*>(Cb), codes, ws, big, nullptr),
-                             "crvq_code_sums");
+          expect_ok_or_hip(crvq_code_sums(static_cast<const double*>(X), rows, vpr, vpr * d, d, codes, K,
+                                          static_cast<double*>(Cb), codes, ws, big, nullptr),
+                           "crvq_code_sums");
         }
   for (int64_t M : {int64_t{1}, int64_t{15}, int64_t{16}, int64_t{17}, int64_t{511}, int64_t{512}, int64_t{1024}})
     for (int64_t N : {int64_t{8}, int64_t{16}, int64_t{64}, int64_t{128}, int64_t{1024}, int64_t{8200}}) {
@@ -143,10 +142,11 @@ int main() {
                                                   CRVQ_F32, N, ws, big, nullptr),
                                "crvq_dequant_books");
             }
-          expect_ok_or_hip(crvq_refine_codes(M, N, d, n_crit, static_cast<double*>(fake(22)), N,
-                                             static_cast<const double*>(fake(23)), N, Cb, CRVQ_F32,
-                                             d == 16 ? 512 : 256, codes, N / d, ws, big, nullptr),
-                           "crvq_refine_codes");
+          for (int64_t Kr : {int64_t{d == 16 ? 512 : 256}, int64_t{4097}, int64_t{65536}})
+            expect_ok_or_hip(crvq_refine_codes(M, N, d, n_crit, static_cast<double*>(fake(22)), N,
+                                               static_cast<const double*>(fake(23)), N, Cb, CRVQ_F32, Kr, codes,
+                                               N / d, ws, big, nullptr),
+                             "crvq_refine_codes");
         }
       }
       expect_ok_or_hip(crvq_hessian_product(M, N, N, static_cast<const double*>(fake(22)), N,

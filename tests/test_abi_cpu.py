@@ -263,10 +263,11 @@ def test_refinement_validation(L):
     assert L.crvq_hessian_product(4, 8, 9, FAKE, 8, FAKE, 8, FAKE, 9, None, None, None) == 1
     assert L.crvq_hessian_product(4, 8, 8, FAKE, 8, FAKE, 8, FAKE, 8, None, FAKE, None) == 1  # total needs row_loss
     assert "loss_total" in err(L)
-    assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 2000, FAKE, None, ws, 1 << 30, None) == 2  # K > 1024
+    assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 70000, FAKE, None, ws, 1 << 30, None) == 2  # K > 65536
     assert L.crvq_code_sums(FAKE, 4, 2, 8, 8, FAKE, 16, FAKE, None, ws, 1 << 30, None) == 1     # ld < vpr * d
     assert L.crvq_code_sums(FAKE, 4, 2, 16, 8, FAKE, 16, FAKE, None, ws, 0, None) == 3          # no workspace
-    assert L.crvq_code_sums_workspace_size(100, 8, 2000) == 0
+    assert L.crvq_code_sums_workspace_size(100, 8, 70000) == 0
+    assert L.crvq_code_sums_workspace_size(100, 8, 65536) > L.crvq_code_sums_workspace_size(100, 8, 1024) > 0
     dbl = ctypes.c_double
     assert L.crvq_adam_step(FAKE, FAKE, dbl(-2.0), FAKE, FAKE, 8, 0, dbl(1e-3), dbl(0.9), dbl(0.95), dbl(1e-8),
                             None) == 1                                    # step 0
@@ -274,7 +275,7 @@ def test_refinement_validation(L):
                             None) == 1                                    # beta1 = 1
     need = L.crvq_refine_workspace_size(64, 256, 256)
     assert need > 64 * 256 * 8 and L.crvq_refine_workspace_size(64, 128, 256) == 0
-    assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 2048, FAKE, 32, ws, need, None) == 2
+    assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 70000, FAKE, 32, ws, need, None) == 2
     assert L.crvq_refine_codes(64, 256, 8, 250, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 32, ws, need, None) == 1
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 31, ws, need, None) == 1
     assert L.crvq_refine_codes(64, 256, 8, 256, FAKE, 256, FAKE, 256, FAKE, 0, 256, FAKE, 32, ws, need - 1, None) == 3

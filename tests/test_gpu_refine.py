@@ -66,7 +66,10 @@ def test_hessian_product(M, N, n_out):
 
 
 @pytest.mark.parametrize("M,N,d,cover,K", [(64, 256, 8, 256, 256), (300, 512, 8, 40, 1000), (17, 64, 16, 64, 7),
-                                           (5, 24, 3, 24, 1), (1000, 1024, 8, 1024, 256)])
+                                           (5, 24, 3, 24, 1), (1000, 1024, 8, 1024, 256),
+                                           # books past 1024 codewords: grouped by a radix pass first
+                                           (300, 512, 8, 512, 4096), (40, 96, 16, 96, 1025), (7, 30, 3, 30, 2000),
+                                           (2048, 4096, 8, 4096, 65536)])
 def test_code_sums(M, N, d, cover, K):
     say(f"code sums {M}x{N} d={d} cover={cover} K={K}")
     g = np.random.default_rng(M * 3 + K)
@@ -131,7 +134,12 @@ def refine_case(M, N, d, K, n_cols, c_dtype, seed):
                                                    # few output tiles, long k: S = R H[:, :n_cols] split over k
                                                    # into parts (ragged last part, M and n_cols not multiples
                                                    # of the 128 x 128 tile)
-                                                   (300, 2056, 8, 256, 64, "f32"), (130, 2049, 1, 64, 48, "f32")])
+                                                   (300, 2056, 8, 256, 64, "f32"), (130, 2049, 1, 64, 48, "f32"),
+                                                   # books too large for one CU's LDS: searched one group at a
+                                                   # time over all rows, in codebook slices
+                                                   (40, 256, 8, 4096, 256, "f32"), (65, 128, 8, 65536, 64, "f32"),
+                                                   (33, 96, 8, 2048, 96, "bf16"), (9, 64, 16, 600, 64, "f32"),
+                                                   (130, 512, 8, 1100, 200, "f32")])
 def test_refine_codes(M, N, d, K, n_cols, c_dtype):
     say(f"refine codes {M}x{N} d={d} K={K} cols={n_cols} {c_dtype}")
     R, H, Cb, codes = refine_case(M, N, d, K, n_cols, c_dtype, M + K)
@@ -173,6 +181,34 @@ def test_refine_codes_sampled_rows_full_size():
     orf.refine_book(Ro, H, Cb, qo, d, N)
     np.testing.assert_array_equal(host(qt).reshape(M, -1)[rows].ravel(), qo)
     np.testing.assert_array_equal(host(Rt)[rows], Ro)
+
+
+def test_refine_codes_sampled_rows_full_size_k65536():
+    """The code search on a 4096 x 4096 layer against a K = 65536 book (searched in slices, one group
+    at a time): sampled rows re-run on the oracle from the same inputs."""
+    M, N, d, K = 4096, 4096, 8, 65536
+    say(f"refine codes full size {M}x{N} K={K}")
+    g = np.random.default_rng(17)
+    W = rv((M, N), 18, 0.02)
+    X = rv((2048, N), 19)
+    Cb = rv((K, d), 20, 0.02)
+    codes = g.integers(0, K, M * N // d).astype(np.int32)
+    Xt = dev(X)
+    Ht = torch.empty(N, N, dtype=torch.float64, device="cuda")
+    C.crvq_gram(Xt, Ht)
+    R = W.astype(np.float64) - Cb.astype(np.float64)[codes].reshape(M, N)
+    Rt = torch.from_numpy(R).cuda()
+    qt = dev(codes.copy())
+    C.crvq_refine_codes(Rt, Ht, dev(Cb), qt, d, N, N // d)
+    torch.cuda.synchronize()
+    H = host(Ht)
+    rows = np.sort(g.choice(M, 3, replace=False))
+    Ro = R[rows].copy()
+    qo = codes.reshape(M, -1)[rows].copy().ravel()
+    moved = orf.refine_book(Ro, H, Cb, qo, d, N)
+    np.testing.assert_array_equal(host(qt).reshape(M, -1)[rows].ravel(), qo)
+    np.testing.assert_array_equal(host(Rt)[rows], Ro)
+    say(f"refine codes K={K}: sampled rows identical ({moved} codes moved in them)")
 
 
 def test_refine_loop_lockstep():

@@ -31,7 +31,7 @@ from typing import List, Optional, Sequence
 
 import numpy as np
 
-from . import F32, reconstruct, widen
+from . import BF16, F32, reconstruct, round_to, widen
 
 
 def gram(X: np.ndarray, x_dtype: str = F32) -> np.ndarray:
@@ -148,18 +148,25 @@ class RefineResult:
 
 def refine_layer(Ws: np.ndarray, Xs: np.ndarray, d: int, n_crit: int, books: Sequence[np.ndarray],
                  codes: Sequence[np.ndarray], n_base: int, lr: float, steps: int, max_rounds: int,
-                 eps: float = 0.0, beta1: float = 0.9, beta2: float = 0.95, adam_eps: float = 1e-8) -> RefineResult:
-    """The refinement loop of Alg. 1 on one layer in sorted order (fp32 W and codebooks): while
-    QuantLoss >= eps and rounds < max_rounds, ``steps`` Adam steps on the codebooks, then a width-1
-    code search over every book in order."""
+                 eps: float = 0.0, beta1: float = 0.9, beta2: float = 0.95, adam_eps: float = 1e-8,
+                 w_dtype: str = F32) -> RefineResult:
+    """The refinement loop of Alg. 1 on one layer in sorted order: while QuantLoss >= eps and rounds <
+    max_rounds, ``steps`` Adam steps on the codebooks, then a width-1 code search over every book in
+    order.  The first basic book has the layer's type (``w_dtype``), the others are fp32.
+
+    Reading for bf16 layers (the paper fine-tunes a half-precision model without saying how): a bf16
+    book is tuned through an fp32 master copy, set from the book when the loop starts; Adam moves the
+    master exactly as it moves an fp32 book, and after every step the book is the master rounded to
+    bf16 (nearest-even), which QuantLoss, the gradients and the code search then use."""
     M, N = Ws.shape
-    books = [np.asarray(b, dtype=np.float32).copy() for b in books]
+    dts = [w_dtype] + [F32] * (len(books) - 1)
+    books = [np.asarray(b, dtype=np.uint16 if t == BF16 else np.float32).copy() for b, t in zip(books, dts)]
+    masters = [widen(b, t).astype(np.float32) if t == BF16 else None for b, t in zip(books, dts)]
     codes = [np.asarray(c, dtype=np.int32).copy() for c in codes]
-    dts = [F32] * len(books)
     H = gram(Xs)
     Ks = [b.shape[0] for b in books]
     adam = [AdamState(np.zeros(b.shape), np.zeros(b.shape)) for b in books]
-    R = residual_f64(Ws, F32, d, n_crit, codes, books, dts, n_base)
+    R = residual_f64(Ws, w_dtype, d, n_crit, codes, books, dts, n_base)
     losses = [float(np.sum(R * (R @ H)))]
     changes = []
     rounds = 0
@@ -167,13 +174,17 @@ def refine_layer(Ws: np.ndarray, Xs: np.ndarray, d: int, n_crit: int, books: Seq
         for _ in range(steps):
             grads, _ = codebook_grads(R, H, d, n_crit, codes, Ks, n_base)
             for b in range(len(books)):
-                books[b] = adam_step(books[b], grads[b], adam[b], lr, beta1, beta2, adam_eps)
-            R = residual_f64(Ws, F32, d, n_crit, codes, books, dts, n_base)
+                if dts[b] == BF16:
+                    masters[b] = adam_step(masters[b], grads[b], adam[b], lr, beta1, beta2, adam_eps)
+                    books[b] = round_to(masters[b].astype(np.float64), BF16)
+                else:
+                    books[b] = adam_step(books[b], grads[b], adam[b], lr, beta1, beta2, adam_eps)
+            R = residual_f64(Ws, w_dtype, d, n_crit, codes, books, dts, n_base)
         ch = 0
         for b in range(len(books)):
             n_cols = N if b < n_base else n_crit
-            ch += refine_book(R, H, books[b], codes[b], d, n_cols)
-        R = residual_f64(Ws, F32, d, n_crit, codes, books, dts, n_base)
+            ch += refine_book(R, H, books[b], codes[b], d, n_cols, dts[b])
+        R = residual_f64(Ws, w_dtype, d, n_crit, codes, books, dts, n_base)
         changes.append(ch)
         losses.append(float(np.sum(R * (R @ H))))
         rounds += 1

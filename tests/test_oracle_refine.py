@@ -171,3 +171,46 @@ def test_refine_layer_loss_decreases(oracle_mod):
     res_e = orf.refine_layer(W, X, d, n_crit, books, codes, 1, lr=1e-3, steps=5, max_rounds=3,
                              eps=res0.losses[0] * 2)
     assert res_e.rounds == 0
+
+
+def test_bf16_layer_reduces_to_the_fp32_loop_without_steps(oracle_mod):
+    """With bf16-representable values and no codebook steps, the bf16 path (bf16 W and first book) runs
+    the same code search as the fp32 path on the widened values: the same codes and losses."""
+    M, N, d, K, n_crit = 16, 48, 8, 12, 16
+    W = oracle.round_to(rv((M, N), 41, 0.5).astype(np.float64), "bf16")
+    X = rv((30, N), 42)
+    g = np.random.default_rng(43)
+    b0 = oracle.round_to(rv((K, d), 44, 0.5).astype(np.float64), "bf16")
+    b1 = rv((K, d), 45, 0.1)
+    codes = [g.integers(0, K, M * N // d).astype(np.int32), g.integers(0, K, M * n_crit // d).astype(np.int32)]
+    a = orf.refine_layer(W, X, d, n_crit, [b0, b1], codes, 1, lr=1e-3, steps=0, max_rounds=2, w_dtype="bf16")
+    f = orf.refine_layer(oracle.widen(W, "bf16"), X, d, n_crit, [oracle.widen(b0, "bf16"), b1], codes, 1, lr=1e-3,
+                         steps=0, max_rounds=2)
+    assert a.changes[0] > 0
+    np.testing.assert_array_equal(a.losses, f.losses)
+    for x, y in zip(a.codes, f.codes):
+        np.testing.assert_array_equal(x, y)
+    np.testing.assert_array_equal(a.books[0], b0)  # no step: the bf16 book is untouched
+
+
+def test_bf16_book_is_its_master_rounded(oracle_mod):
+    """A bf16 book after Adam steps is the nearest bf16 (ties to even) of an fp32 master that moved by
+    the fp32 rule: every entry is within half a bf16 step of a value the fp32 update could reach, and
+    the book does move when the steps exceed half an ulp."""
+    M, N, d, K, n_crit = 16, 48, 8, 12, 16
+    W = oracle.round_to(rv((M, N), 51, 0.5).astype(np.float64), "bf16")
+    X = rv((30, N), 52)
+    g = np.random.default_rng(53)
+    b0 = oracle.round_to(rv((K, d), 54, 0.5).astype(np.float64), "bf16")
+    codes = [g.integers(0, K, M * N // d).astype(np.int32)]
+    res = orf.refine_layer(W, X, d, 0, [b0], codes, 1, lr=0.05, steps=3, max_rounds=1, w_dtype="bf16")
+    book = res.books[0]
+    assert book.dtype == np.uint16 and (book != b0).any()
+    # brute force nearest-even on the bf16 grid around every entry is what round_to gives
+    v = oracle.widen(book, "bf16").astype(np.float64)
+    for x in (v * (1 + 2 ** -12)).ravel()[:64]:
+        lo = np.float32(x).view(np.uint32) & 0xFFFF0000
+        cands = [lo, lo + 0x10000]
+        vals = [float(np.uint32(c).view(np.float32)) for c in cands]
+        best = min(range(2), key=lambda i: (abs(vals[i] - x), cands[i] & 0x10000))
+        assert oracle.round_to(np.array([x]), "bf16")[0] == np.uint16(cands[best] >> 16)

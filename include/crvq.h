@@ -349,6 +349,15 @@ crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row
 crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, double* m, double* v, int64_t n,
                            int64_t step, double lr, double beta1, double beta2, double eps, void* stream);
 
+/* crvq_adam_step_bf16 -- the same step for a bf16 codebook C (bit patterns)
+ * tuned through an fp32 master copy (n floats, state like m and v): at step 1
+ * the master is first set to C (exact); the master then moves as
+ * crvq_adam_step moves an fp32 codebook, and C becomes the master rounded to
+ * bf16, nearest-even (Alg. 1 FineTuneCodebook, as read for bf16 layers). */
+crvq_status crvq_adam_step_bf16(uint16_t* C, float* master, const double* grad, double grad_scale, double* m,
+                                double* v, int64_t n, int64_t step, double lr, double beta1, double beta2, double eps,
+                                void* stream);
+
 /* crvq_refine_codes -- BeamSearchOptimize of Alg. 1 at the paper's width 1,
  * under QuantLoss, for one codebook C (K x d, F32 or BF16) covering the
  * column groups 0 .. n_cols/d - 1 of an M x N layer (n_cols = N for a basic

@@ -76,6 +76,8 @@ def lib(build_if_missing: bool = True):
                 "crvq_workspace_size": ([ctypes.c_int, I64, I64, I32, I32, I32, P, I64, I64, I64], SZ),
                 "crvq_code_sums_workspace_size": ([I64, I32, I64], SZ),
                 "crvq_code_sums": ([P, I64, I64, I64, I32, P, I64, P, P, P, SZ, P], ctypes.c_int),
+                "crvq_adam_step_bf16": ([P, P, P, ctypes.c_double, P, P, I64, I64, ctypes.c_double, ctypes.c_double,
+                                         ctypes.c_double, ctypes.c_double, P], ctypes.c_int),
                 "crvq_adam_step": ([P, P, ctypes.c_double, P, P, I64, I64, ctypes.c_double, ctypes.c_double,
                                     ctypes.c_double, ctypes.c_double, P], ctypes.c_int),
                 "crvq_refine_workspace_size": ([I64, I64, I64], SZ),
@@ -360,6 +362,17 @@ def crvq_adam_step(C: torch.Tensor, grad: torch.Tensor, grad_scale: float, m: to
     assert C.dtype == torch.float32 and grad.dtype == m.dtype == v.dtype == torch.float64
     _check("crvq_adam_step", lib().crvq_adam_step(_ptr(C), _ptr(grad), grad_scale, _ptr(m), _ptr(v), C.numel(), step,
                                                   lr, beta1, beta2, eps, _stream(stream)))
+
+
+def crvq_adam_step_bf16(C: torch.Tensor, master: torch.Tensor, grad: torch.Tensor, grad_scale: float, m: torch.Tensor,
+                        v: torch.Tensor, step: int, lr: float, beta1: float = 0.9, beta2: float = 0.95,
+                        eps: float = 1e-8, stream=None) -> None:
+    """Adam on the fp32 master of a bf16 codebook (set from it at step 1), the book re-rounded from it."""
+    assert C.dtype == torch.bfloat16 and master.dtype == torch.float32 and master.numel() == C.numel()
+    assert grad.dtype == m.dtype == v.dtype == torch.float64
+    _check("crvq_adam_step_bf16", lib().crvq_adam_step_bf16(_ptr(C), _ptr(master), _ptr(grad), grad_scale, _ptr(m),
+                                                            _ptr(v), C.numel(), step, lr, beta1, beta2, eps,
+                                                            _stream(stream)))
 
 
 def crvq_refine_codes(R: torch.Tensor, H: torch.Tensor, C: torch.Tensor, codes: torch.Tensor, d: int, n_cols: int,

@@ -627,6 +627,24 @@ crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, doub
                     fn);
 }
 
+crvq_status crvq_adam_step_bf16(uint16_t* C, float* master, const double* grad, double grad_scale, double* m,
+                                double* v, int64_t n, int64_t step, double lr, double beta1, double beta2, double eps,
+                                void* stream) {
+  static const char* fn = "crvq_adam_step_bf16";
+  g_err.clear();
+  if (n < 0 || step < 1) return fail(CRVQ_ERR_INVALID, "%s: need n >= 0 and step >= 1", fn);
+  if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0) || !(eps >= 0.0))
+    return fail(CRVQ_ERR_INVALID, "%s: need 0 <= beta1, beta2 < 1 and eps >= 0", fn);
+  if (n == 0) return CRVQ_OK;
+  if (!C || !master || !grad || !m || !v)
+    return fail(CRVQ_ERR_INVALID, "%s: C, master, grad, m and v must not be NULL", fn);
+  const double bc1 = 1.0 - std::pow(beta1, static_cast<double>(step));
+  const double bc2 = 1.0 - std::pow(beta2, static_cast<double>(step));
+  return hip_status(launch_adam_bf16(n, C, master, grad, grad_scale, m, v, lr, beta1, beta2, bc1, bc2, eps, step == 1,
+                                     static_cast<hipStream_t>(stream)),
+                    fn);
+}
+
 size_t crvq_refine_workspace_size(int64_t M, int64_t N, int64_t n_cols) {
   if (M < 1 || n_cols < 1 || N < n_cols) return 0;
   return refine_ws_bytes(M, n_cols, N);

@@ -216,6 +216,9 @@ hipError_t launch_code_sums_large(const RowSrc& src, const int32_t* codes, int64
                                   void* ws, hipStream_t stream);
 hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int64_t n, const int32_t* codes,
                             int64_t K, double* sums, int32_t* counts, void* ws, hipStream_t stream);
+hipError_t launch_adam_bf16(int64_t n, uint16_t* C, float* master, const double* grad, double scale, double* m,
+                            double* v, double lr, double b1, double b2, double bc1, double bc2, double eps, bool first,
+                            hipStream_t stream);
 hipError_t launch_adam(int64_t n, float* C, const double* grad, double scale, double* m, double* v, double lr,
                        double b1, double b2, double bc1, double bc2, double eps, hipStream_t stream);
 size_t refine_lds_bytes(int64_t K, int d);

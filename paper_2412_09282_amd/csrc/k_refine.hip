@@ -456,6 +456,30 @@ __global__ __launch_bounds__(256) void adam_kernel(int64_t n, float* __restrict_
   C[i] = static_cast<float>(static_cast<double>(C[i]) - lr * mh / (sqrt(vh) + eps));
 }
 
+// The same step on an fp32 master of a bf16 codebook (set from the book at step 1), then the book as
+// the master rounded to bf16, nearest-even (the master is finite here: rounding on its bits).
+__global__ __launch_bounds__(256) void adam_bf16_kernel(int64_t n, uint16_t* __restrict__ C, float* __restrict__ master,
+                                                        const double* __restrict__ grad, double scale,
+                                                        double* __restrict__ m, double* __restrict__ v, double lr,
+                                                        double b1, double b2, double bc1, double bc2, double eps,
+                                                        int first) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float x0 = first ? __uint_as_float(static_cast<uint32_t>(C[i]) << 16) : master[i];
+  const double g = scale * grad[i];
+  const double mi = b1 * m[i] + (1.0 - b1) * g;
+  const double vi = b2 * v[i] + (1.0 - b2) * (g * g);
+  m[i] = mi;
+  v[i] = vi;
+  const double mh = mi / bc1;
+  const double vh = vi / bc2;
+  const float x = static_cast<float>(static_cast<double>(x0) - lr * mh / (sqrt(vh) + eps));
+  master[i] = x;
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7f800000u) != 0x7f800000u) u += 0x7fffu + ((u >> 16) & 1u);  // inf and NaN keep their bits
+  C[i] = static_cast<uint16_t>(u >> 16);
+}
+
 // ---- width-1 code search, one block of column groups per launch ----------------------------------
 constexpr int kRfRows = 8;      // rows per workgroup, one wave each
 constexpr int kRfThreads = 64 * kRfRows;
@@ -849,6 +873,15 @@ hipError_t launch_code_sums(const double* X, int64_t vpr, int64_t ld, int d, int
                      static_cast<int>(K), per_block, nb, part, pcount);
   hipLaunchKernelGGL(code_sum_final, dim3(static_cast<unsigned>(cdiv(K * d, 4))), dim3(256), 0, stream, part, pcount,
                      nb, K, d, sums, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam_bf16(int64_t n, uint16_t* C, float* master, const double* grad, double scale, double* m,
+                            double* v, double lr, double b1, double b2, double bc1, double bc2, double eps, bool first,
+                            hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(adam_bf16_kernel, dim3(static_cast<unsigned>(cdiv(n, 256))), dim3(256), 0, stream, n, C, master,
+                     grad, scale, m, v, lr, b1, b2, bc1, bc2, eps, first ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -240,11 +240,10 @@ class LayerQuantizer:
         """The loss-driven refinement of Alg. 1 after run(): while QuantLoss >= eps and fewer than `rounds`
         rounds ran, `steps` Adam steps on every codebook (codes fixed), then the width-1 QuantLoss code
         search over every book in order.  Works in reordered channel order on the codebooks and codes
-        run() left (fp32 layers); rebuilds W_hat at the end.  Returns QuantLoss before the loop and after
-        every round."""
+        run() left; a bf16 book (the first basic book of a bf16 layer) is tuned through an fp32 master
+        copy and re-rounded after every step.  Rebuilds W_hat at the end.  Returns QuantLoss before the
+        loop and after every round."""
         cfg, d, M, N = self.cfg, self.cfg.d, self.M, self.N
-        if self.dtype != torch.float32:
-            raise ValueError("refinement tunes fp32 codebooks: quantize the layer in fp32")
         hooks = list(hooks) + ([TraceHook(trace)] if trace is not None else [])
         rec = _Recorder(hooks)
         f64 = torch.float64
@@ -263,6 +262,8 @@ class LayerQuantizer:
         ldq = [N // d] * mb + [max(1, self.ncv)] * len(self.C_ext)
         sums = [torch.empty(b.shape[0], d, dtype=f64, device=dev) for b in books]
         moments = [(torch.zeros(b.shape[0], d, dtype=f64, device=dev), torch.zeros(b.shape[0], d, dtype=f64, device=dev))
+                   for b in books]
+        masters = [torch.empty(b.shape[0], d, dtype=torch.float32, device=dev) if b.dtype == torch.bfloat16 else None
                    for b in books]
 
         rec.pre("gram", X=X, perm=self.perm)
@@ -295,9 +296,17 @@ class LayerQuantizer:
                     rec.pre(f"code_sums_{r}_{s_}_{b}", X=self.G[:, :cover[b]], codes=codes[b], K=Cb.shape[0])
                     C.crvq_code_sums(Vg, codes[b], Cb.shape[0], sums[b])
                     rec.post(f"code_sums_{r}_{s_}_{b}", sums=sums[b])
-                    rec.pre(f"adam_{r}_{s_}_{b}", C=Cb, grad=sums[b], m=moments[b][0], v=moments[b][1], step=t)
-                    C.crvq_adam_step(Cb, sums[b], -2.0, moments[b][0], moments[b][1], t, lr, beta1, beta2, adam_eps)
-                    rec.post(f"adam_{r}_{s_}_{b}", C=Cb, m=moments[b][0], v=moments[b][1])
+                    if masters[b] is not None:
+                        rec.pre(f"adam_{r}_{s_}_{b}", C=Cb, master=masters[b], grad=sums[b], m=moments[b][0],
+                                v=moments[b][1], step=t)
+                        C.crvq_adam_step_bf16(Cb, masters[b], sums[b], -2.0, moments[b][0], moments[b][1], t, lr, beta1,
+                                              beta2, adam_eps)
+                        rec.post(f"adam_{r}_{s_}_{b}", C=Cb, master=masters[b], m=moments[b][0], v=moments[b][1])
+                    else:
+                        rec.pre(f"adam_{r}_{s_}_{b}", C=Cb, grad=sums[b], m=moments[b][0], v=moments[b][1], step=t)
+                        C.crvq_adam_step(Cb, sums[b], -2.0, moments[b][0], moments[b][1], t, lr, beta1, beta2,
+                                         adam_eps)
+                        rec.post(f"adam_{r}_{s_}_{b}", C=Cb, m=moments[b][0], v=moments[b][1])
                 loss_now(f"{r}_{s_}")
             for b, Cb in enumerate(books):
                 rec.pre(f"refine_{r}_{b}", R=self.R, H=self.H, C=Cb, codes=codes[b], n_cols=cover[b])

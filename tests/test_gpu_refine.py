@@ -309,17 +309,75 @@ def test_refine_two_basic_books_d16():
     say(f"refine m=2 d=16: QuantLoss {losses[0]:.6e} -> {losses[-1]:.6e}, codes identical to the oracle")
 
 
-def test_refine_rejects_bf16_layers():
-    M, N, d = 32, 64, 8
-    wl = inputs.small_workload(M=M, N=N, tokens=32, d=d, K_base=16, K_ext=(8,), crit_frac=0.25, beam=1, iters=1,
+def tbits(t):
+    """A trace tensor (CPU) as numpy; bf16 as uint16 bit patterns."""
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def test_refine_loop_lockstep_bf16():
+    """The refinement loop on a bf16 layer: the first basic book is bf16 and tuned through an fp32
+    master (set from the book at step 1, re-rounded after every step); every call re-run on the oracle
+    from the GPU's inputs, then the whole loop against the oracle's from the same start."""
+    M, N, d = 64, 128, 8
+    wl = inputs.small_workload(M=M, N=N, tokens=96, d=d, K_base=32, K_ext=(8,), crit_frac=0.25, beam=1, iters=1,
                                dtype="bf16", wid=142)
     W = inputs.make_weight(wl, 0)
     X = inputs.make_calib(wl, 0)
     n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
     cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters)
-    q = LayerQuantizer(M, N, torch.bfloat16, cfg, tokens=32, device="cuda")
+    q = LayerQuantizer(M, N, torch.bfloat16, cfg, tokens=96, device="cuda")
     Xt = torch.from_numpy(X).cuda()
-    q.run(dev(W, "bf16"), Xt, torch.from_numpy(inputs.base_init_indices(wl, 0, M * N // d)).cuda(),
-          [torch.from_numpy(inputs.ext_init_indices(wl, 0, 1, M * n_crit // d)).cuda()])
-    with pytest.raises(ValueError):
-        q.refine(Xt, rounds=1, steps=1, lr=1e-4)
+    st = q.run(dev(W, "bf16"), Xt, torch.from_numpy(inputs.base_init_indices(wl, 0, M * N // d)).cuda(),
+               [torch.from_numpy(inputs.ext_init_indices(wl, 0, 1, M * n_crit // d)).cuda()])
+    torch.cuda.synchronize()
+    books_gpu = q.C_basic + q.C_ext
+    start_books = [tbits(b.cpu()).copy() for b in books_gpu]
+    start_codes = [host(c).copy() for c in q.codes_basic + q.codes_ext]
+    perm = host(st.perm)
+    Ws = tbits(st.Ws.cpu())
+    lr = 2e-3
+    trace = []
+    losses = q.refine(Xt, rounds=2, steps=3, lr=lr, trace=trace)
+    torch.cuda.synchronize()
+    H = None
+    dts = ["bf16", "f32"]
+    n_adam_bf16 = 0
+    for c in trace:
+        name, ci, co = c["name"], c["in"], c["out"]
+        if name == "gram":
+            H = co["H"].numpy()
+        elif name.startswith("residual"):
+            books = [tbits(b) for b in ci["books"]]
+            codes = [x.numpy() for x in ci["codes"]]
+            exp = orf.residual_f64(Ws, "bf16", d, n_crit, codes, books, dts, 1)
+            np.testing.assert_array_equal(co["out"].numpy(), exp)
+        elif name.startswith("refine"):
+            Ro = ci["R"].numpy().copy()
+            qo = ci["codes"].numpy().copy()
+            b = int(name.rsplit("_", 1)[1])
+            orf.refine_book(Ro, H, tbits(ci["C"]), qo, d, ci["n_cols"], dts[b])
+            np.testing.assert_array_equal(co["codes"].numpy(), qo)
+            np.testing.assert_array_equal(co["R"].numpy(), Ro)
+        elif name.startswith("adam"):
+            grad = ci["grad"].numpy()
+            stt = orf.AdamState(ci["m"].numpy().copy(), ci["v"].numpy().copy(), ci["step"] - 1)
+            if "master" in ci:
+                n_adam_bf16 += 1
+                m_in = oracle.widen(tbits(ci["C"]), "bf16").astype(np.float32) if ci["step"] == 1 else ci["master"].numpy()
+                m_out = orf.adam_step(m_in, -2.0 * grad, stt, lr)
+                np.testing.assert_array_equal(co["master"].numpy(), m_out)
+                np.testing.assert_array_equal(tbits(co["C"]), oracle.round_to(m_out.astype(np.float64), "bf16"))
+            else:
+                np.testing.assert_array_equal(co["C"].numpy(), orf.adam_step(ci["C"].numpy(), -2.0 * grad, stt, lr))
+    assert n_adam_bf16 == 6
+    ref = orf.refine_layer(Ws, oracle.gather_columns(X, perm), d, n_crit, start_books, start_codes, 1, lr=lr,
+                           steps=3, max_rounds=2, w_dtype="bf16")
+    np.testing.assert_allclose(losses, ref.losses, rtol=1e-9)
+    assert losses[-1] < losses[0]
+    for a, b in zip(q.codes_basic + q.codes_ext, ref.codes):
+        np.testing.assert_array_equal(host(a), b)
+    np.testing.assert_array_equal(tbits(q.C_basic[0].cpu()), ref.books[0])
+    assert (tbits(q.C_basic[0].cpu()) != start_books[0]).any()  # the bf16 book did move
+    say(f"refine loop bf16: QuantLoss {losses[0]:.6e} -> {losses[-1]:.6e}, {len(trace)} calls matched")

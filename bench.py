@@ -461,7 +461,9 @@ class RefineHook:
             if name.startswith("hessian"):
                 self.checks["hessian"] = {"R": kw["R"][self.rows].cpu().numpy()}
             elif name.startswith("refine"):
-                self.checks["refine"] = {"R": kw["R"][self.rows].cpu().numpy(), "C": kw["C"].cpu().numpy(),
+                Cc = kw["C"].cpu()
+                Cc = Cc.view(torch.int16).numpy().view("uint16") if Cc.dtype == torch.bfloat16 else Cc.numpy()
+                self.checks["refine"] = {"R": kw["R"][self.rows].cpu().numpy(), "C": Cc,
                                          "codes": kw["codes"].view(kw["R"].shape[0], -1)[self.rows].cpu().numpy(),
                                          "n_cols": kw["n_cols"]}
         self.cur = (name, torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -496,8 +498,7 @@ def refine_bench(args):
     wl = inputs.workload(wid)
     L = wl.layers[0]
     M, N, d = L.M, L.N, wl.d
-    if L.dtype != "f32":
-        raise SystemExit("the refinement tunes fp32 codebooks: pick an fp32 workload")
+    tdt = torch.bfloat16 if L.dtype == "bf16" else torch.float32
     n = M * N // d
     n_crit = inputs.n_crit_columns(N, d, wl.crit_frac)
     W = inputs.make_weight(wl, 0)
@@ -506,9 +507,10 @@ def refine_bench(args):
     ei = [torch.from_numpy(inputs.ext_init_indices(wl, 0, t, M * n_crit // d)).cuda()
           for t in range(1, len(wl.K_ext) + 1)]
     xi = [torch.from_numpy(inputs.extra_base_init_indices(wl, 0, b, n)).cuda() for b in range(1, wl.m_base)]
-    Wd, Xd = torch.from_numpy(W).cuda(), torch.from_numpy(X).cuda()
+    Wd = (torch.from_numpy(W.view(np.int16)).view(torch.bfloat16) if L.dtype == "bf16" else torch.from_numpy(W)).cuda()
+    Xd = torch.from_numpy(X).cuda()
     cfg = LayerConfig(d, wl.K_base, wl.K_ext, wl.crit_frac, wl.beam, wl.iters, m_base=wl.m_base)
-    q = LayerQuantizer(M, N, torch.float32, cfg, L.tokens, device="cuda")
+    q = LayerQuantizer(M, N, tdt, cfg, L.tokens, device="cuda")
     kw = dict(rounds=args.rounds, steps=args.ft_steps, lr=args.lr)
     # warm-up: one layer pass and one refinement loop
     q.run(Wd, Xd, bi, ei, base_idx_extra=xi)
@@ -539,7 +541,7 @@ def refine_bench(args):
     rf = ck["refine"]
     Ro, qo = rf["R"].copy(), rf["codes"].copy().ravel()
     t0 = time.perf_counter()
-    orf.refine_book(Ro, H, rf["C"], qo, d, rf["n_cols"])
+    orf.refine_book(Ro, H, rf["C"], qo, d, rf["n_cols"], L.dtype)
     t_or = time.perf_counter() - t0
     ok_ref = bool(np.array_equal(qo, rf["out"].ravel()) and np.array_equal(Ro, rf["R_out"]))
     groups = {}
@@ -557,11 +559,13 @@ def refine_bench(args):
             "code_ext": (M * n_crit * 8.0 + 4.0 * M * (n_crit // d), "B", HBM),
             "adam": (wl.K_base * d * 40.0, "B", HBM),
             "refine_basic": (2.0 * M * N * N + 2.0 * M * (N // d) * wl.K_base * d, "FLOP", F64),
-            "refine_ext": (2.0 * M * N * n_crit + 2.0 * M * (n_crit // d) * 256 * d, "FLOP", F64)}
+            "refine_ext": (2.0 * M * N * n_crit + 2.0 * M * (n_crit // d) * (wl.K_ext[0] if wl.K_ext else 0) * d,
+                           "FLOP", F64)}
     for kind, mss in groups.items():
         w, unit, peak = work[kind]
         med = float(np.median(mss))
-        rec = {"mode": "refine", "workload": wid, "layer": f"{L.name} {M}x{N} f32", "call": kind, "calls": len(mss),
+        rec = {"mode": "refine", "workload": wid, "layer": f"{L.name} {M}x{N} {L.dtype}", "call": kind,
+               "calls": len(mss),
                "gpu_ms_median": round(med, 4), "gpu_ms_total": round(float(np.sum(mss)), 3),
                "work_per_call": w, "work_unit": unit, "rate": w / (med * 1e-3), "frac": w / (med * 1e-3) / peak,
                "bound": "fp64" if unit == "FLOP" else "hbm"}

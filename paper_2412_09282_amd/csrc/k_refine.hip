@@ -608,6 +608,9 @@ constexpr int kRsRows = 64;      // rows per workgroup of the scan
 constexpr int kRsTile = 256;     // codewords staged in LDS per round
 constexpr int kRsMaxSlices = 8;  // codebook slices (grid y) at most
 
+// Thread (rg, ks) = (tid % 16, tid / 16) scores rows 4 rg .. 4 rg + 3 against every sixteenth
+// codeword of each staged round (so a codeword read from LDS serves four rows); the next round's
+// codewords are loaded into registers while the current one is scored.
 template <int DMAX>
 __global__ __launch_bounds__(256) void refine_scan_kernel(int64_t M, int d, int64_t col, int64_t gq,
                                                           const double* __restrict__ S, int64_t lds,
@@ -615,13 +618,14 @@ __global__ __launch_bounds__(256) void refine_scan_kernel(int64_t M, int d, int6
                                                           const void* __restrict__ Cb, int c_type, int K, int slice,
                                                           const int32_t* __restrict__ codes, int64_t ldq,
                                                           double* __restrict__ bestF, int* __restrict__ bestK) {
+  constexpr int kPer = kRsTile * DMAX / 256;  // staged elements per thread and round
   __shared__ double Hg[16 * 16];
   __shared__ double sb[kRsRows][16];
-  __shared__ double Cs[kRsTile * 16];
+  __shared__ double Cs[kRsTile * DMAX];
   __shared__ double Ak[kRsTile];
-  __shared__ double rf[4][kRsRows];
-  __shared__ int rk[4][kRsRows];
-  const int tid = threadIdx.x, row = tid & 63, sub = tid >> 6;
+  __shared__ double rf[16][kRsRows];
+  __shared__ int rk[16][kRsRows];
+  const int tid = threadIdx.x, rg = tid & 15, ks = tid >> 4;
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kRsRows;
   const int k0 = static_cast<int>(blockIdx.y) * slice;
   const int k1 = k0 + slice < K ? k0 + slice : K;
@@ -641,15 +645,36 @@ __global__ __launch_bounds__(256) void refine_scan_kernel(int64_t M, int d, int6
     sb[rr][t] = v;
   }
   __syncthreads();
-  double b[DMAX];
+  double b[4][DMAX];
 #pragma unroll
-  for (int t = 0; t < DMAX; ++t) b[t] = t < d ? sb[row][t] : 0.0;
-  double best = __builtin_inf();
-  int bk = K;
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int t = 0; t < DMAX; ++t) b[q][t] = t < d ? sb[4 * rg + q][t] : 0.0;
+  double best[4];
+  int bk[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    best[q] = __builtin_inf();
+    bk[q] = K;
+  }
+  // round kt's codewords as kPer elements per thread (element e = tid + 256 i of the round)
+  double pf[kPer];
+  auto fetch = [&](int kt) {
+    const int64_t base = static_cast<int64_t>(kt) * d, lim = static_cast<int64_t>(k1) * d;
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int64_t e = base + tid + 256 * i;
+      pf[i] = e < lim ? book_elem(Cb, c_type, e) : 0.0;
+    }
+  };
+  if (k0 < k1) fetch(k0);
   for (int kt = k0; kt < k1; kt += kRsTile) {
     const int tn = k1 - kt < kRsTile ? k1 - kt : kRsTile;
-    for (int e = tid; e < tn * d; e += 256) Cs[e] = book_elem(Cb, c_type, static_cast<int64_t>(kt) * d + e);
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      if (tid + 256 * i < tn * d) Cs[tid + 256 * i] = pf[i];
     __syncthreads();
+    if (kt + kRsTile < k1) fetch(kt + kRsTile);  // in flight while this round is scored
     if (tid < tn) {  // a_k = c_k^T Hgg c_k
       double a = 0.0;
       for (int t = 0; t < d; ++t) {
@@ -660,30 +685,42 @@ __global__ __launch_bounds__(256) void refine_scan_kernel(int64_t M, int d, int6
       Ak[tid] = a;
     }
     __syncthreads();
-    for (int jj = sub; jj < tn; jj += 4) {
-      double dot = 0.0;
+    for (int jj = ks; jj < tn; jj += 16) {
+      double c[DMAX];
 #pragma unroll
-      for (int t = 0; t < DMAX; ++t)
-        if (t < d) dot = dot + Cs[jj * d + t] * b[t];
-      const double f = Ak[jj] - 2.0 * dot;
-      if (f < best) {
-        best = f;
-        bk = kt + jj;
+      for (int t = 0; t < DMAX; ++t) c[t] = t < d ? Cs[jj * d + t] : 0.0;
+      const double a = Ak[jj];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        double dot = 0.0;
+#pragma unroll
+        for (int t = 0; t < DMAX; ++t)
+          if (t < d) dot = dot + c[t] * b[q][t];
+        const double f = a - 2.0 * dot;
+        if (f < best[q]) {
+          best[q] = f;
+          bk[q] = kt + jj;
+        }
       }
     }
     __syncthreads();
   }
-  rf[sub][row] = best;
-  rk[sub][row] = bk;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    rf[ks][4 * rg + q] = best[q];
+    rk[ks][4 * rg + q] = bk[q];
+  }
   __syncthreads();
-  if (sub == 0 && r0 + row < M) {
-    for (int q = 1; q < 4; ++q)
-      if (rf[q][row] < best || (rf[q][row] == best && rk[q][row] < bk)) {
-        best = rf[q][row];
-        bk = rk[q][row];
+  if (tid < kRsRows && r0 + tid < M) {
+    double f0 = rf[0][tid];
+    int k = rk[0][tid];
+    for (int q = 1; q < 16; ++q)
+      if (rf[q][tid] < f0 || (rf[q][tid] == f0 && rk[q][tid] < k)) {
+        f0 = rf[q][tid];
+        k = rk[q][tid];
       }
-    bestF[static_cast<int64_t>(blockIdx.y) * M + r0 + row] = best;
-    bestK[static_cast<int64_t>(blockIdx.y) * M + r0 + row] = bk;
+    bestF[static_cast<int64_t>(blockIdx.y) * M + r0 + tid] = f0;
+    bestK[static_cast<int64_t>(blockIdx.y) * M + r0 + tid] = k;
   }
 }
 

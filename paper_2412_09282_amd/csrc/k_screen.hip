@@ -320,6 +320,23 @@ __device__ __forceinline__ void bf16_split(float v, uint16_t& hi, uint16_t& lo) 
   lo = bf16_rn_bits(v - __uint_as_float(static_cast<uint32_t>(hi) << 16));
 }
 
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+typedef float f2v __attribute__((ext_vector_type(2)));
+
+// bf16 nearest-even of (a, b), a in the low half: one v_cvt_pk_bf16_f32, which rounds every finite
+// fp32 value (subnormals included) to the same bits as bf16_rn_bits.
+__device__ __forceinline__ uint32_t bf16x2_rn(float a, float b) {
+  const f2v p = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(p, bf2v));
+}
+
+// The pair (a, b) of bf16_split: hi terms when !lo_term, else the lo terms.
+__device__ __forceinline__ uint32_t bf16x2_split(float a, float b, bool lo_term) {
+  const uint32_t h = bf16x2_rn(a, b);
+  const uint32_t l = bf16x2_rn(a - __uint_as_float(h << 16), b - __uint_as_float(h & 0xffff0000u));
+  return lo_term ? l : h;
+}
+
 // Screen operand policies.  Each gives the per-lane A (codebook tile) and B (-2x of the wave's rows)
 // operands of one 16 x 16 tile of s values and the MFMA sequence that accumulates them onto ||c||^2.
 // Both leave lane l the values of codewords 4 (l / 16) + r, r = 0..3, for row l % 16.
@@ -367,6 +384,7 @@ struct F32Ops {
 // is exact (c2 = x2 = 0).
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 struct SplitOps {
   static constexpr int DM = 8;
@@ -396,13 +414,13 @@ struct SplitOps {
       else
         load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, src.d, ok, v);
     }
-    u16x8 h;
+    return make_b_vals(v, g);
+  }
+  // the B operand of lane group g from the row's first 8 elements (zero past d)
+  __device__ static __forceinline__ B make_b_vals(const float (&v)[8], int g) {
+    u32x4 h;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      uint16_t hi, lo;
-      bf16_split(-2.0f * v[t], hi, lo);
-      h[t] = (g & 1) ? lo : hi;
-    }
+    for (int q = 0; q < 4; ++q) h[q] = bf16x2_split(-2.0f * v[2 * q], -2.0f * v[2 * q + 1], (g & 1) != 0);
     B b;
     b.v = __builtin_bit_cast(bf8, h);
     return b;
@@ -1914,14 +1932,52 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
   list_append(valid && !certain, i, rcount, rlist);
 }
 
+// Fast forms of the small-codebook kernel: FT 1 = fp32 rows packed back to back (d = 8, 16-byte
+// aligned) against an fp32 codebook, FT 2 = bf16 rows packed back to back (d = 8, 16-byte aligned)
+// against a bf16 codebook; FT 0 = any layout and type.  Row i and codeword k of a fast form are one
+// 32- or 16-byte load at a fixed stride.
+template <int FT>
+__device__ __forceinline__ void small1_row(const void* base, int64_t i, float (&v)[8]) {
+  if constexpr (FT == 1) {
+    const f4* p = static_cast<const f4*>(base) + 2 * i;
+    const f4 a = p[0], b = p[1];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      v[t] = a[t];
+      v[4 + t] = b[t];
+    }
+  } else {
+    const uint4 q = static_cast<const uint4*>(base)[i];
+    const uint32_t u[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      v[2 * t] = __uint_as_float(u[t] << 16);
+      v[2 * t + 1] = __uint_as_float(u[t] & 0xffff0000u);
+    }
+  }
+}
+
+// The fast form that applies to these rows and this codebook (0 when none does).
+int small1_form(const RowSrc& src, const void* C, int ct) {
+  if (src.d != 8 || src.ld != src.vpr * 8) return 0;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(src.base) | reinterpret_cast<uintptr_t>(C);
+  if ((a & 15) != 0) return 0;
+  if (src.type == ET_F32 && ct == ET_F32) return 1;
+  if (src.type == ET_BF16 && ct == ET_BF16) return 2;
+  return 0;
+}
+
 // Top-1 against a small codebook (at most 16 tiles of 16, one split): the split-bf16 screen of
-// screen_kernel, but every lane keeps its smallest screen value with the codeword index and its
-// second smallest value, so no tile needs re-scoring: after the four lane groups of a row are merged,
-// the row's winner alone is scored exactly in fp64 and certified against the second smallest screen
-// value with the same bound as finalize_kernel (R = ||x|| + sqrt(D)).  The row's result is written
-// directly (codes / dist, or rowD / rowK for a beam step); an uncertain row keeps it as its tentative
-// result and is appended to the rescue list.
-template <int CB>
+// screen_kernel, tracked per cell.  A cell is the four codewords 16 T + 4 g .. 16 T + 4 g + 3 whose
+// screen values one MFMA tile T gives lane group g for a row; every lane keeps, per row, the smallest
+// cell minimum with the cell's first codeword and the second smallest cell minimum (two VALU
+// operations per four values for the cell minimum, four per cell for the tracking).  After the four
+// lane groups of a row are merged, the four codewords of the row's winning cell are scored exactly in
+// fp64 and taken in (D, k) order; the winner is certified against the smallest screen value outside
+// that cell with the same bound as finalize_kernel (R = ||x|| + sqrt(D)).  The row's result is
+// written directly (codes / dist, or rowD / rowK for a beam step); an uncertain row keeps it as its
+// tentative result and is appended to the rescue list.
+template <int CB, int FT>
 __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const void* __restrict__ apack,
                                                             const float* __restrict__ cnp, int64_t tiles,
                                                             const void* __restrict__ C, int ct, int64_t K,
@@ -1937,36 +1993,53 @@ __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const vo
   const int d = src.d;
   const int64_t row0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * (16 * CB);
   if (row0 >= n) return;  // no barriers below
+  const int dd = FT ? 8 : d;
   SplitOps::B bop[CB];
+  if constexpr (FT == 0) {
 #pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const int64_t i = row0 + cb * 16 + jl;
-    bop[cb] = SplitOps::make_b(src, i, i < n, g);
+    for (int cb = 0; cb < CB; ++cb) {
+      const int64_t i = row0 + cb * 16 + jl;
+      bop[cb] = SplitOps::make_b(src, i, i < n, g);
+    }
+  } else {
+    // every load in flight before the first split; a row past the end repeats the last row (its
+    // screen column is never read)
+    float v[CB][8];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      const int64_t i = row0 + cb * 16 + jl;
+      small1_row<FT>(src.base, i < n ? i : n - 1, v[cb]);
+    }
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) bop[cb] = SplitOps::make_b_vals(v[cb], g);
   }
   float m1[CB], m2[CB];
-  int i1[CB];
+  int i1[CB];  // first codeword of the cell holding m1
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     m1[cb] = __builtin_inff();
     m2[cb] = __builtin_inff();
     i1[cb] = 0x7fffffff;
   }
+  // tile T + 1's operands are loaded while tile T is screened (the last tile loads itself again)
+  SplitOps::A a = SplitOps::load_a(apack, 0, lane);
+  f4 c4 = *reinterpret_cast<const f4*>(cnp + 4 * g);
   for (int64_t T = 0; T < tiles; ++T) {
-    const SplitOps::A a = SplitOps::load_a(apack, T, lane);
-    const f4 c4 = *reinterpret_cast<const f4*>(cnp + T * 16 + 4 * g);
+    const int64_t Tn = (T + 1 < tiles) ? T + 1 : T;
+    const SplitOps::A an = SplitOps::load_a(apack, Tn, lane);
+    const f4 c4n = *reinterpret_cast<const f4*>(cnp + Tn * 16 + 4 * g);
     const int kb = static_cast<int>(T) * 16 + 4 * g;
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
       const f4 acc = SplitOps::mfma(a, bop[cb], c4);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float v = acc[r];
-        m2[cb] = __builtin_amdgcn_fmed3f(m1[cb], m2[cb], v);  // m1 <= m2 holds throughout
-        const bool lt = v < m1[cb];
-        m1[cb] = lt ? v : m1[cb];
-        i1[cb] = lt ? kb + r : i1[cb];
-      }
+      const float cm = fminf(fminf(acc[0], acc[1]), fminf(acc[2], acc[3]));
+      m2[cb] = __builtin_amdgcn_fmed3f(m1[cb], m2[cb], cm);  // m1 <= m2 holds throughout
+      const bool lt = cm < m1[cb];
+      m1[cb] = lt ? cm : m1[cb];
+      i1[cb] = lt ? kb : i1[cb];
     }
+    a = an;
+    c4 = c4n;
   }
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
@@ -1976,7 +2049,8 @@ __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const vo
       const float om1 = __shfl_xor(m1[cb], sh), om2 = __shfl_xor(m2[cb], sh);
       const int oi1 = __shfl_xor(i1[cb], sh);
       const float nm2 = fminf(fminf(m2[cb], om2), fmaxf(m1[cb], om1));
-      const bool take = om1 < m1[cb] || (om1 == m1[cb] && oi1 < i1[cb]);
+      // evaluated without short-circuit, so the compiler selects instead of branching
+      const bool take = (om1 < m1[cb]) | ((om1 == m1[cb]) & (oi1 < i1[cb]));
       m1[cb] = take ? om1 : m1[cb];
       i1[cb] = take ? oi1 : i1[cb];
       m2[cb] = nm2;
@@ -1998,21 +2072,48 @@ __global__ __launch_bounds__(256) void screen_small1_kernel(RowSrc src, const vo
     const int cbm = 4 * rr + g;
     const int64_t i = row0 + cbm * 16 + jl;
     if (cbm >= CB || i >= n) continue;
+    // a winning cell has a screen value below +inf, so its first codeword is a real one (padding
+    // codewords, past K, screen to +inf); no winner (a NaN row) leaves the row to the rescue
+    const bool has = k1 >= 0 && k1 < K;
+    const int kc = has ? k1 : 0;
     double xd[8];
-    load_row_exact<8>(src, i, true, xd);
-    const int kk = (k1 >= 0 && k1 < K) ? k1 : 0;
-    float cw[8];
-    load_codeword<8>(C, ct, kk, d, true, cw);
-    double D1 = 0.0, xn2 = 0.0;
+    float cw[4][8];
+    if constexpr (FT == 0) {
+      load_row_exact<8>(src, i, true, xd);
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      if (t < d) {
-        const double diff = xd[t] - static_cast<double>(cw[t]);
-        D1 = D1 + diff * diff;
-        xn2 = xn2 + xd[t] * xd[t];
+      for (int r = 0; r < 4; ++r) load_codeword<8>(C, ct, kc + r, d, kc + r < K, cw[r]);
+    } else {
+      float v[8];
+      small1_row<FT>(src.base, i, v);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) small1_row<FT>(C, kc + r < K ? kc + r : kc, cw[r]);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) xd[t] = static_cast<double>(v[t]);
+    }
+    double xn2 = 0.0;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      if (t < dd) xn2 = xn2 + xd[t] * xd[t];
+    double D1 = 0.0;
+    int kk = kc;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      double D = 0.0;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        if (t < dd) {
+          const double diff = xd[t] - static_cast<double>(cw[r][t]);
+          D = D + diff * diff;
+        }
+      }
+      if (r == 0) {
+        D1 = D;
+      } else if (kc + r < K && cless(D, kc + r, D1, kk)) {
+        D1 = D;
+        kk = kc + r;
       }
     }
-    bool certain = k1 == kk;
+    bool certain = has;
     if (certain && s2 != __builtin_inff()) {
       const double xn = sqrt(xn2);
       const double R = xn + sqrt(D1);
@@ -3085,12 +3186,21 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     // small codebook, top-1: screen, exact winner and certificate in one kernel, then the rescue
     const ScreenBound bound = screen_bound(p, src.type, ct, src.d, nullptr);
     const dim3 grid(static_cast<unsigned>(p.grid_x));
-    if (p.cb == CRVQ_CB_WIDE)
-      hipLaunchKernelGGL((screen_small1_kernel<CRVQ_CB_WIDE>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles,
-                         C, ct, K, bound, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
-    else
-      hipLaunchKernelGGL((screen_small1_kernel<2>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles, C, ct, K,
-                         bound, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK);
+    const int ft = small1_form(src, C, ct);
+#define CRVQ_SMALL1(CBV, FTV)                                                                                    \
+  hipLaunchKernelGGL((screen_small1_kernel<CBV, FTV>), grid, dim3(256), 0, stream, src, w.apack, w.cnp, p.tiles, C, \
+                     ct, K, bound, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK)
+    if (p.cb == CRVQ_CB_WIDE) {
+      if (ft == 1)
+        CRVQ_SMALL1(CRVQ_CB_WIDE, 1);
+      else if (ft == 2)
+        CRVQ_SMALL1(CRVQ_CB_WIDE, 2);
+      else
+        CRVQ_SMALL1(CRVQ_CB_WIDE, 0);
+    } else {
+      CRVQ_SMALL1(2, 0);
+    }
+#undef CRVQ_SMALL1
     if ((e = hipGetLastError()) != hipSuccess) return e;
     return launch_rescue1<2>(src, top, C, ct, K, w.rcount, w.rlist, out_codes, out_dist, rowD, rowK, nullptr, nullptr, 0,
                              stream);

@@ -107,12 +107,13 @@ struct ScreenWs {
   // pruned screen (prune): key order of codewords and rows, chunk ranges, binning parameters
   int* corder;   // sorted codeword position -> codeword [tiles x 32]
   int* ckey;     // codeword keys [K]
-  int* coff;     // first sorted position of every key [32768]
-  int* hist;     // key counts then cursors, codewords [32768] and rows [32768]
-  uint4* cbnd;   // chunk ranges [tiles / 2]
+  int* coff;     // first sorted position of every key [16384]
+  int* hist;     // key counts then cursors, codewords [16384] and rows [16384]
+  uint4* cbnd;   // chunk ranges of the norm and coordinate j [tiles / 2]
+  uint2* cbnd3;  // chunk ranges of coordinate q [tiles / 2]
   uint32_t* cminS;
   uint32_t* cmaxP;
-  float* prm;    // binning parameters and the scaled largest codeword norm [4]
+  float* prm;    // binning parameters and the scaled largest codeword norm [6], then partial ranges
   int* rkey;     // row keys [n_rows]
   int* rord;     // rows in key order [n_rows]
   float* tD;     // the first screen's exact distance of each uncertain row, per-block slices [n_rows

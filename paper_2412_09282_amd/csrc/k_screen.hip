@@ -753,34 +753,38 @@ constexpr int kS32TileHalves = 768;  // packed fp16 per tile: c1, c2, N terms, 3
 constexpr int kS32MaxParts = 256;    // partial maxima of the codebook scale reduction
 
 // ------------------------------------------------------------------------------------------------
-// Certified tile skipping for the long top-1 screen.  For any codeword c and row x, both
-//   | ||x|| - ||c|| | <= ||x - c||   and   | x_j - c_j | <= ||x - c||   (one coordinate j),
-// so once a row's best distance is known to be at most D_up, a codeword whose norm or coordinate j
-// lies further than sqrt(D_up) from the row's can neither win nor tie.  Codewords are packed in the
-// order of a key (norm bin major, bin of coordinate j minor), rows are screened in the order of the
-// same key, and each wave keeps, per pair of tiles ("chunk" of 64 codewords), the range of the
-// codewords' norms and coordinate j: a chunk outside every row's band is skipped.  D_up comes from
+// Certified tile skipping for the long top-1 screen.  For any codeword c and row x,
+//   | ||x|| - ||c|| | <= ||x - c||   and   | x_t - c_t | <= ||x - c||   (any coordinate t),
+// so once a row's best distance is known to be at most D_up, a codeword whose norm, coordinate j or
+// coordinate q lies further than sqrt(D_up) from the row's can neither win nor tie.  Codewords are
+// packed in the order of a key (norm bin major, then the bin of coordinate j, then the bin of
+// coordinate q), rows are screened in the order of the same key, and each wave keeps, per pair of
+// tiles ("chunk" of 64 codewords), the ranges of the codewords' norms and coordinates j and q: a
+// chunk outside every row's band in any of the three is skipped.  D_up comes from
 // the wave's running screen minimum m:  D(c_m) <= m / alpha^2 + ||x||^2 + delta, delta the screen's
 // error bound taken with R = the largest codeword norm.  Every quantity is in units of the codebook
 // scale alpha (exact powers of two), rounded outward, so the test is conservative; a skipped
 // codeword is strictly worse than the kept chunk's exact winner, so the certificate and the results
 // are those of the full screen.
-constexpr int kPruneBins1 = 128;               // norm bins (major key)
-constexpr int kPruneBins2 = 128;               // coordinate bins (minor key)
-constexpr int kPruneKeys = kPruneBins1 * kPruneBins2;
+constexpr int kPruneBins1 = 16;                // norm bins (major key)
+constexpr int kPruneBins2 = 16;                // bins of coordinate j (middle key)
+constexpr int kPruneBins3 = 64;                // bins of coordinate q (minor key)
+constexpr int kPruneKeys = kPruneBins1 * kPruneBins2 * kPruneBins3;
 constexpr int64_t kPruneMinRows = 32768;       // rows from which the screen is pruned
 
 struct PruneData {
   const int* corder;        // sorted codeword position -> codeword
   const int* coff;          // first sorted position of every key
   const uint4* cbnd;        // per chunk: ordered keys of {min, max} scaled norm, {min, max} scaled c_j
+  const uint2* cbnd3;       // per chunk: ordered keys of {min, max} scaled c_q
   const uint32_t* cminS;    // suffix minimum over chunks of the norm minimum key
   const uint32_t* cmaxP;    // prefix maximum over chunks of the norm maximum key
   const int* rord;          // rows in key order
   const int* rkey;          // key of every row
-  const float* prm;         // {max ||c||, min c_j, max c_j, scaled max ||c|| rounded up}
+  const float* prm;         // {max ||c||, min c_j, max c_j, scaled max ||c|| rounded up, min c_q, max c_q}
   const float* lD;          // second screen: per listed row, its first-screen exact distance rounded up
   int jp;                   // the coordinate j
+  int jq;                   // the coordinate q
 };
 
 // Order-preserving map of a float (both zeros to the same key) to an unsigned integer, so that wave
@@ -823,13 +827,21 @@ __device__ __forceinline__ float f32_up_any(double x) {
   return f;
 }
 
-__device__ __forceinline__ int prune_key(float nrm, float xj, const float (&prm)[3]) {
-  float f1 = nrm * (static_cast<float>(kPruneBins1) / fmaxf(prm[0], 0x1p-126f));
-  f1 = fminf(fmaxf(f1, 0.0f), static_cast<float>(kPruneBins1 - 1));
-  const float span = prm[2] - prm[1];
-  float f2 = (span > 0.0f) ? (xj - prm[1]) * (static_cast<float>(kPruneBins2) / span) : 0.0f;
-  f2 = fminf(fmaxf(f2, 0.0f), static_cast<float>(kPruneBins2 - 1));
-  return static_cast<int>(f1) * kPruneBins2 + static_cast<int>(f2);
+// Bin of x in [lo, hi] out of nb (clamped; one bin when the range is empty).
+__device__ __forceinline__ int prune_bin(float x, float lo, float hi, int nb) {
+  const float span = hi - lo;
+  float f = (span > 0.0f) ? (x - lo) * (static_cast<float>(nb) / span) : 0.0f;
+  f = fminf(fmaxf(f, 0.0f), static_cast<float>(nb - 1));
+  return static_cast<int>(f);
+}
+
+// r = {max ||c||, min c_j, max c_j, min c_q, max c_q}.  The key only orders the vectors; the
+// skipping tests use the exact ranges of every chunk, so any binning is correct.
+__device__ __forceinline__ int prune_key(float nrm, float xj, float xq, const float (&r)[5]) {
+  const int f1 = prune_bin(nrm, 0.0f, fmaxf(r[0], 0x1p-126f), kPruneBins1);
+  const int f2 = prune_bin(xj, r[1], r[2], kPruneBins2);
+  const int f3 = prune_bin(xq, r[3], r[4], kPruneBins3);
+  return (f1 * kPruneBins2 + f2) * kPruneBins3 + f3;
 }
 
 constexpr int kPruneTile = 4096;  // vectors per block of the key counting and scatter
@@ -838,97 +850,109 @@ constexpr int kPruneParts = 256;  // partial blocks of the binning ranges
 // Partial binning ranges of the codebook (max norm, min and max of coordinate j) over a strided
 // share of the codewords, and (every block a share) the cleared key counts of codewords and rows.
 __global__ __launch_bounds__(256) void prune_stats_partial(const void* __restrict__ C, int ct, int64_t K, int d,
-                                                           int jp, float* __restrict__ part, int* __restrict__ hist2) {
-  __shared__ float s_mx[256], s_lo[256], s_hi[256];
+                                                           int jp, int jq, float* __restrict__ part,
+                                                           int* __restrict__ hist2) {
+  __shared__ float s_r[5][256];
   const int tid = threadIdx.x;
   for (int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + tid; e < 2 * kPruneKeys; e += gridDim.x * 256) hist2[e] = 0;
-  float mx = 0.0f, lo = __builtin_inff(), hi = -__builtin_inff();
+  float r[5] = {0.0f, __builtin_inff(), -__builtin_inff(), __builtin_inff(), -__builtin_inff()};
   for (int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + tid; k < K; k += static_cast<int64_t>(gridDim.x) * 256) {
     float v[8];
     if (ct == ET_F32)
       load_f32_elems<8>(static_cast<const float*>(C) + k * d, d, true, v);
     else
       load_bf16_elems<8>(static_cast<const uint16_t*>(C) + k * d, d, true, v);
-    float n2 = 0.0f, cj = 0.0f;
+    float n2 = 0.0f, cj = 0.0f, cq = 0.0f;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       n2 = n2 + v[t] * v[t];
       cj = (t == jp) ? v[t] : cj;
+      cq = (t == jq) ? v[t] : cq;
     }
-    mx = fmaxf(mx, sqrtf(n2));
-    lo = fminf(lo, cj);
-    hi = fmaxf(hi, cj);
+    r[0] = fmaxf(r[0], sqrtf(n2));
+    r[1] = fminf(r[1], cj);
+    r[2] = fmaxf(r[2], cj);
+    r[3] = fminf(r[3], cq);
+    r[4] = fmaxf(r[4], cq);
   }
-  s_mx[tid] = mx;
-  s_lo[tid] = lo;
-  s_hi[tid] = hi;
-  __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if (tid < w) {
-      s_mx[tid] = fmaxf(s_mx[tid], s_mx[tid + w]);
-      s_lo[tid] = fminf(s_lo[tid], s_lo[tid + w]);
-      s_hi[tid] = fmaxf(s_hi[tid], s_hi[tid + w]);
-    }
-    __syncthreads();
-  }
-  if (tid == 0) {
-    part[blockIdx.x] = s_mx[0];
-    part[kPruneParts + blockIdx.x] = s_lo[0];
-    part[2 * kPruneParts + blockIdx.x] = s_hi[0];
-  }
-}
-
-// Every block folds the partial ranges (the first one also publishes them to prm[0..2]).
-__device__ __forceinline__ void prune_fold_ranges(const float* __restrict__ part, int nparts, float* __restrict__ prm,
-                                                  float (&r)[3]) {
-  __shared__ float s_r[3][256];
-  const int tid = threadIdx.x;
-  s_r[0][tid] = tid < nparts ? part[tid] : 0.0f;
-  s_r[1][tid] = tid < nparts ? part[kPruneParts + tid] : __builtin_inff();
-  s_r[2][tid] = tid < nparts ? part[2 * kPruneParts + tid] : -__builtin_inff();
+#pragma unroll
+  for (int q = 0; q < 5; ++q) s_r[q][tid] = r[q];
   __syncthreads();
   for (int w = 128; w >= 1; w >>= 1) {
     if (tid < w) {
       s_r[0][tid] = fmaxf(s_r[0][tid], s_r[0][tid + w]);
       s_r[1][tid] = fminf(s_r[1][tid], s_r[1][tid + w]);
       s_r[2][tid] = fmaxf(s_r[2][tid], s_r[2][tid + w]);
+      s_r[3][tid] = fminf(s_r[3][tid], s_r[3][tid + w]);
+      s_r[4][tid] = fmaxf(s_r[4][tid], s_r[4][tid + w]);
     }
     __syncthreads();
   }
-  r[0] = s_r[0][0];
-  r[1] = s_r[1][0];
-  r[2] = s_r[2][0];
+  if (tid == 0) {
+#pragma unroll
+    for (int q = 0; q < 5; ++q) part[q * kPruneParts + blockIdx.x] = s_r[q][0];
+  }
+}
+
+// Every block folds the partial ranges r = {max ||c||, min c_j, max c_j, min c_q, max c_q} (the
+// first one also publishes them to prm[0..2] and prm[4..5]).
+__device__ __forceinline__ void prune_fold_ranges(const float* __restrict__ part, int nparts, float* __restrict__ prm,
+                                                  float (&r)[5]) {
+  __shared__ float s_r[5][256];
+  const int tid = threadIdx.x;
+  const bool in = tid < nparts;
+  s_r[0][tid] = in ? part[tid] : 0.0f;
+  s_r[1][tid] = in ? part[kPruneParts + tid] : __builtin_inff();
+  s_r[2][tid] = in ? part[2 * kPruneParts + tid] : -__builtin_inff();
+  s_r[3][tid] = in ? part[3 * kPruneParts + tid] : __builtin_inff();
+  s_r[4][tid] = in ? part[4 * kPruneParts + tid] : -__builtin_inff();
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (tid < w) {
+      s_r[0][tid] = fmaxf(s_r[0][tid], s_r[0][tid + w]);
+      s_r[1][tid] = fminf(s_r[1][tid], s_r[1][tid + w]);
+      s_r[2][tid] = fmaxf(s_r[2][tid], s_r[2][tid + w]);
+      s_r[3][tid] = fminf(s_r[3][tid], s_r[3][tid + w]);
+      s_r[4][tid] = fmaxf(s_r[4][tid], s_r[4][tid + w]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 5; ++q) r[q] = s_r[q][0];
   if (blockIdx.x == 0 && tid == 0) {
     prm[0] = r[0];
     prm[1] = r[1];
     prm[2] = r[2];
+    prm[4] = r[3];
+    prm[5] = r[4];
   }
 }
 
 // Key of vector i of src (the rows, or the codewords as a set of K rows).
-__device__ __forceinline__ int prune_vec_key(const RowSrc& src, int64_t i, int jp, const float (&r)[3]) {
+__device__ __forceinline__ int prune_vec_key(const RowSrc& src, int64_t i, int jp, int jq, const float (&r)[5]) {
   float v[8];
   const int64_t off = row_offset(src, i);
   if (src.type == ET_F32)
     load_f32_elems<8>(static_cast<const float*>(src.base) + off, src.d, true, v);
   else
     load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, src.d, true, v);
-  float n2 = 0.0f, xj = 0.0f;
+  float n2 = 0.0f, xj = 0.0f, xq = 0.0f;
 #pragma unroll
   for (int t = 0; t < 8; ++t) {
     n2 = n2 + v[t] * v[t];
     xj = (t == jp) ? v[t] : xj;
+    xq = (t == jq) ? v[t] : xq;
   }
-  return prune_key(sqrtf(n2), xj, r);
+  return prune_key(sqrtf(n2), xj, xq, r);
 }
 
 // Keys of kPruneTile vectors per block, counted in LDS, the block's nonzero counts added to the
 // global counts (one integer atomic per key present in the block).
-__global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, const float* __restrict__ part,
+__global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, int jq, const float* __restrict__ part,
                                                           int nparts, float* __restrict__ prm, int* __restrict__ keys,
                                                           int* __restrict__ hist) {
   __shared__ int h[kPruneKeys];
-  float r[3];
+  float r[5];
   prune_fold_ranges(part, nparts, prm, r);
   const int tid = threadIdx.x;
   for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
@@ -937,7 +961,7 @@ __global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, co
   for (int q = 0; q < kPruneTile / 256; ++q) {
     const int64_t i = i0 + q * 256 + tid;
     if (i < src.n) {
-      const int key = prune_vec_key(src, i, jp, r);
+      const int key = prune_vec_key(src, i, jp, jq, r);
       keys[i] = key;
       atomicAdd(h + key, 1);
     }
@@ -1013,16 +1037,17 @@ __global__ __launch_bounds__(256) void prune_fill_kernel(int* __restrict__ p, in
 }
 
 // Per chunk (sorted positions 64 c .. 64 c + 63, one wave): the range of alpha ||c|| (fp64, rounded
-// outward) and of alpha c_j (exact), as ordered keys; an empty chunk gets an empty range.
+// outward) and of alpha c_j and alpha c_q (exact), as ordered keys; an empty chunk gets empty ranges.
 __global__ __launch_bounds__(256) void prune_chunks_kernel(const void* __restrict__ C, int ct, int64_t K, int d, int jp,
-                                                           const int* __restrict__ corder, const float* __restrict__ alpha_p,
-                                                           int64_t nch, uint4* __restrict__ cbnd) {
+                                                           int jq, const int* __restrict__ corder,
+                                                           const float* __restrict__ alpha_p, int64_t nch,
+                                                           uint4* __restrict__ cbnd, uint2* __restrict__ cbnd3) {
   const int lane = threadIdx.x & 63;
   const int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
   if (c >= nch) return;  // whole waves
   const double a = static_cast<double>(alpha_p[0]);
   double lo1 = __builtin_inf(), hi1 = -__builtin_inf();
-  float lo2 = __builtin_inff(), hi2 = -__builtin_inff();
+  float lo2 = __builtin_inff(), hi2 = -__builtin_inff(), lo3 = __builtin_inff(), hi3 = -__builtin_inff();
   const int64_t q = 64 * c + lane;
   const int64_t k = q < K ? corder[q] : -1;
   if (k >= 0 && k < K) {
@@ -1032,14 +1057,16 @@ __global__ __launch_bounds__(256) void prune_chunks_kernel(const void* __restric
     else
       load_bf16_elems<8>(static_cast<const uint16_t*>(C) + k * d, d, true, v);
     double n2 = 0.0;
-    float cj = 0.0f;
+    float cj = 0.0f, cq = 0.0f;
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
       n2 = n2 + static_cast<double>(v[t]) * static_cast<double>(v[t]);
       cj = (t == jp) ? v[t] : cj;
+      cq = (t == jq) ? v[t] : cq;
     }
     lo1 = hi1 = sqrt(n2) * a;
     lo2 = hi2 = cj * static_cast<float>(a);  // exact: a power of two, alpha |c| < 2^12
+    lo3 = hi3 = cq * static_cast<float>(a);
   }
 #pragma unroll
   for (int sh = 1; sh < 64; sh <<= 1) {
@@ -1048,6 +1075,8 @@ __global__ __launch_bounds__(256) void prune_chunks_kernel(const void* __restric
     hi1 = o2 > hi1 ? o2 : hi1;
     lo2 = fminf(lo2, __shfl_xor(lo2, sh));
     hi2 = fmaxf(hi2, __shfl_xor(hi2, sh));
+    lo3 = fminf(lo3, __shfl_xor(lo3, sh));
+    hi3 = fmaxf(hi3, __shfl_xor(hi3, sh));
   }
   if (lane == 0) {
     uint4 b;
@@ -1056,6 +1085,7 @@ __global__ __launch_bounds__(256) void prune_chunks_kernel(const void* __restric
     b.z = okey(lo2);
     b.w = okey(hi2);
     cbnd[c] = b;
+    cbnd3[c] = make_uint2(okey(lo3), okey(hi3));
   }
 }
 
@@ -1093,13 +1123,13 @@ __global__ __launch_bounds__(1024) void prune_envelope_kernel(const uint4* __res
 // wave-uniform scalars; taking a chunk is one LDS read.
 struct PruneCursor {
   int ui, un, di, dn, turn;
-  uint32_t lo1, hi1, lo2, hi2;
+  uint32_t lo1, hi1, lo2, hi2, lo3, hi3;
 };
 
 __device__ __forceinline__ uint32_t rfl(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
-__device__ __forceinline__ bool prune_keep(const uint4& b, const PruneCursor& s) {
-  return !((b.y < s.lo1) | (b.x > s.hi1) | (b.w < s.lo2) | (b.z > s.hi2));
+__device__ __forceinline__ bool prune_keep(const uint4& b, const uint2& b3, const PruneCursor& s) {
+  return !((b.y < s.lo1) | (b.x > s.hi1) | (b.w < s.lo2) | (b.z > s.hi2) | (b3.y < s.lo3) | (b3.x > s.hi3));
 }
 
 // L[i0 .. n) filtered under the current bands into L[0 ..); returns the new length.  Four groups of
@@ -1113,6 +1143,7 @@ __device__ __forceinline__ int prune_filter(uint16_t* L, int i0, int n, bool up,
     int c[kG];
     uint32_t env[kG];
     uint4 bd[kG];
+    uint2 bd3[kG];
 #pragma unroll
     for (int g = 0; g < kG; ++g) {
       const int i = b + 64 * g + lane;
@@ -1123,13 +1154,14 @@ __device__ __forceinline__ int prune_filter(uint16_t* L, int i0, int n, bool up,
       const int cc = c[g] >= 0 ? c[g] : 0;
       env[g] = up ? pd.cminS[cc] : pd.cmaxP[cc];
       bd[g] = pd.cbnd[cc];
+      bd3[g] = pd.cbnd3[cc];
     }
     bool stop = false;
 #pragma unroll
     for (int g = 0; g < kG; ++g) {
       const bool valid = c[g] >= 0;
       const bool end = !valid || (up ? (env[g] > s.hi1) : (env[g] < s.lo1));
-      const bool keep = !end & prune_keep(bd[g], s);
+      const bool keep = !end & prune_keep(bd[g], bd3[g], s);
       const uint64_t em = __ballot(end);
       uint64_t km = __ballot(keep);
       if (em) km &= (uint64_t{1} << __builtin_ctzll(em)) - 1ull;  // nothing from the first end on
@@ -1158,15 +1190,16 @@ __device__ __forceinline__ int prune_take(PruneCursor& s, const uint16_t* U, con
 }
 
 // New bands from the rows' running minima m (each lane: the rows of its column blocks, both lane
-// halves of a row hold its two halves of every tile); band terms of row (cb, j) at sb[cb * 96 + k * 32 + j].
+// halves of a row hold its two halves of every tile); band terms of row (cb, j) at sb[cb * 128 + k * 32 + j].
 template <int CB>
 __device__ __forceinline__ void prune_band(PruneCursor& s, const float (&m)[CB], const float* sb, int j) {
   float lo1 = __builtin_inff(), hi1 = -__builtin_inff(), lo2 = __builtin_inff(), hi2 = -__builtin_inff();
+  float lo3 = __builtin_inff(), hi3 = -__builtin_inff();
   bool open = false;
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const float mr = fminf(m[cb], __shfl_xor(m[cb], 32));
-    const float A = sb[cb * 96 + j], P = sb[cb * 96 + 32 + j], B = sb[cb * 96 + 64 + j];
+    const float A = sb[cb * 128 + j], P = sb[cb * 128 + 32 + j], Q = sb[cb * 128 + 64 + j], B = sb[cb * 128 + 96 + j];
     if (B >= 0.0f) {
       if (!(mr < __builtin_inff())) {
         open = true;
@@ -1175,16 +1208,19 @@ __device__ __forceinline__ void prune_band(PruneCursor& s, const float (&m)[CB],
         const float Dup = fmaxf((mr + B) + 0x1p-20f * (fabsf(mr) + B) + 0x1p-10f, 0.0f);
         const float r = sqrtf(Dup) * (1.0f + 0x1p-20f);
         const float s1 = 0x1p-20f * (A + r) + 0x1p-10f, s2 = 0x1p-20f * (fabsf(P) + r) + 0x1p-10f;
+        const float s3 = 0x1p-20f * (fabsf(Q) + r) + 0x1p-10f;
         lo1 = fminf(lo1, (A - r) - s1);
         hi1 = fmaxf(hi1, (A + r) + s1);
         lo2 = fminf(lo2, (P - r) - s2);
         hi2 = fmaxf(hi2, (P + r) + s2);
+        lo3 = fminf(lo3, (Q - r) - s3);
+        hi3 = fmaxf(hi3, (Q + r) + s3);
       }
     }
   }
   if (open) {
-    lo1 = lo2 = -__builtin_inff();
-    hi1 = hi2 = __builtin_inff();
+    lo1 = lo2 = lo3 = -__builtin_inff();
+    hi1 = hi2 = hi3 = __builtin_inff();
   }
 #pragma unroll
   for (int sh = 1; sh < 64; sh <<= 1) {
@@ -1192,11 +1228,15 @@ __device__ __forceinline__ void prune_band(PruneCursor& s, const float (&m)[CB],
     hi1 = fmaxf(hi1, __shfl_xor(hi1, sh));
     lo2 = fminf(lo2, __shfl_xor(lo2, sh));
     hi2 = fmaxf(hi2, __shfl_xor(hi2, sh));
+    lo3 = fminf(lo3, __shfl_xor(lo3, sh));
+    hi3 = fmaxf(hi3, __shfl_xor(hi3, sh));
   }
   s.lo1 = rfl(okey(lo1));
   s.hi1 = rfl(okey(hi1));
   s.lo2 = rfl(okey(lo2));
   s.hi2 = rfl(okey(hi2));
+  s.lo3 = rfl(okey(lo3));
+  s.hi3 = rfl(okey(hi3));
 }
 
 // min(c, a[0..15]) as a depth-3 tree of eight v_min3
@@ -1346,12 +1386,13 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
   __shared__ double sD[QS ? 4 : 1][QS ? 32 * CB : 1];
   __shared__ int sK[QS ? 4 : 1][QS ? 32 * CB : 1];
   __shared__ float sR[QS ? 4 : 1][QS ? 32 * CB : 1];
-  // PRUNE: per row alpha ||x||, alpha x_j and the scaled D_up offset (negative: the row takes no part);
-  // per wave the lists of chunks above and below its start
-  __shared__ float sBand[PRUNE1 ? 4 : 1][PRUNE1 ? CB : 1][3][32];
+  // PRUNE: per row alpha ||x||, alpha x_j, alpha x_q and the scaled D_up offset (negative: the row
+  // takes no part); per wave the lists of chunks above and below its start
+  __shared__ float sBand[PRUNE1 ? 4 : 1][PRUNE1 ? CB : 1][4][32];
   __shared__ uint16_t sList[PRUNE ? 4 : 1][PRUNE1 ? 2 : 1][PRUNE ? 1024 : 1];
   // PRUNE2: the wave's union band, as float bounds {lo1, hi1, lo2, hi2} in the scaled units
   float blo1 = __builtin_inff(), bhi1 = -__builtin_inff(), blo2 = __builtin_inff(), bhi2 = -__builtin_inff();
+  float blo3 = __builtin_inff(), bhi3 = -__builtin_inff();
 
   h8 b1[CB], b2[CB];
   bool forced[CB];
@@ -1389,32 +1430,37 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
     b2[cb] = __builtin_bit_cast(h8, p2);
     forced[cb] = over;
     if (PRUNE2 && h == 0 && ok && !over) {
-      // |x| and x_j exactly (fp64) and the first screen's exact distance (rounded up): every codeword
-      // that can tie or beat it lies within sqrt(D) of them; bounds rounded outward with 2^-20
-      // relative and 2^-10 absolute margins in the scaled units
-      double xn2 = 0.0, xj = 0.0;
+      // |x|, x_j and x_q exactly (fp64) and the first screen's exact distance (rounded up): every
+      // codeword that can tie or beat it lies within sqrt(D) of them; bounds rounded outward with
+      // 2^-20 relative and 2^-10 absolute margins in the scaled units
+      double xn2 = 0.0, xj = 0.0, xq = 0.0;
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         xn2 = xn2 + static_cast<double>(v[t]) * static_cast<double>(v[t]);
         xj = (t == pd.jp) ? static_cast<double>(v[t]) : xj;
+        xq = (t == pd.jq) ? static_cast<double>(v[t]) : xq;
       }
       const double a = static_cast<double>(alpha);
-      const double An = sqrt(xn2) * a, Pj = xj * a;
+      const double An = sqrt(xn2) * a, Pj = xj * a, Qq = xq * a;
       const double r = sqrt(static_cast<double>(pd.lD[i])) * a;
       const double m1 = 0x1p-20 * (An + r) + 0x1p-10, m2 = 0x1p-20 * (fabs(Pj) + r) + 0x1p-10;
+      const double m3 = 0x1p-20 * (fabs(Qq) + r) + 0x1p-10;
       blo1 = fminf(blo1, f32_down_any(An - r - m1));
       bhi1 = fmaxf(bhi1, f32_up_any(An + r + m1));
       blo2 = fminf(blo2, f32_down_any(Pj - r - m2));
       bhi2 = fmaxf(bhi2, f32_up_any(Pj + r + m2));
+      blo3 = fminf(blo3, f32_down_any(Qq - r - m3));
+      bhi3 = fmaxf(bhi3, f32_up_any(Qq + r + m3));
     }
     if (PRUNE1 && h == 0) {
-      // the row's band terms in units of alpha: ||x|| and x_j exactly (fp64), and
+      // the row's band terms in units of alpha: ||x||, x_j and x_q exactly (fp64), and
       // D_up - m = alpha^2 ||x||^2 + alpha^2 delta(R = max ||c||), rounded up
-      double xn2 = 0.0, xj = 0.0;
+      double xn2 = 0.0, xj = 0.0, xq = 0.0;
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
         xn2 = xn2 + static_cast<double>(v[t]) * static_cast<double>(v[t]);
         xj = (t == pd.jp) ? static_cast<double>(v[t]) : xj;
+        xq = (t == pd.jq) ? static_cast<double>(v[t]) : xq;
       }
       const double a = static_cast<double>(alpha);
       const double An = sqrt(xn2) * a, cm = static_cast<double>(pd.prm[3]);
@@ -1422,7 +1468,8 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
                        0x1p-24 * 2.8285 * (cm + 2.0 * An) + 0x1p-12;
       sBand[wave][cb][0][j] = static_cast<float>(An);
       sBand[wave][cb][1][j] = static_cast<float>(xj * a);
-      sBand[wave][cb][2][j] = (ok && !over) ? f32_up(B) * (1.0f + 0x1p-20f) : -1.0f;
+      sBand[wave][cb][2][j] = static_cast<float>(xq * a);
+      sBand[wave][cb][3][j] = (ok && !over) ? f32_up(B) * (1.0f + 0x1p-20f) : -1.0f;
     }
   }
 
@@ -1503,15 +1550,19 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
         bhi1 = fmaxf(bhi1, __shfl_xor(bhi1, sh));
         blo2 = fminf(blo2, __shfl_xor(blo2, sh));
         bhi2 = fmaxf(bhi2, __shfl_xor(bhi2, sh));
+        blo3 = fminf(blo3, __shfl_xor(blo3, sh));
+        bhi3 = fmaxf(bhi3, __shfl_xor(bhi3, sh));
       }
-      PruneCursor cur = {0, 0, 0, 0, 0, rfl(okey(blo1)), rfl(okey(bhi1)), rfl(okey(blo2)), rfl(okey(bhi2))};
+      PruneCursor cur = {0, 0, 0, 0, 0, rfl(okey(blo1)), rfl(okey(bhi1)), rfl(okey(blo2)), rfl(okey(bhi2)),
+                         rfl(okey(blo3)), rfl(okey(bhi3))};
       const int c0 = static_cast<int>(t0 >> 1), c1 = static_cast<int>(t1 >> 1);
       uint16_t* Lc = &sList[wave][0][0];
       int cnt = 0;
       const uint64_t lt = lane ? (~0ull >> (64 - lane)) : 0ull;
       for (int cb0 = c0; cb0 < c1; cb0 += 64) {
         const int c = cb0 + lane;
-        const bool keep = c < c1 && prune_keep(pd.cbnd[c < c1 ? c : c0], cur);
+        const int cs = c < c1 ? c : c0;
+        const bool keep = c < c1 && prune_keep(pd.cbnd[cs], pd.cbnd3[cs], cur);
         const uint64_t km = __ballot(keep);
         if (keep) Lc[cnt + __popcll(km & lt)] = static_cast<uint16_t>(c);
         cnt += __popcll(km);
@@ -1562,7 +1613,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       // (readfirstlane: the wave index is uniform, which the compiler cannot see)
       int cc = __builtin_amdgcn_readfirstlane(pd.coff[pd.rkey[pd.rord[mid]]] >> 6);
       cc = cc < c0 ? c0 : (cc >= c1 ? c1 - 1 : cc);
-      PruneCursor cur = {0, c1 - cc, 0, cc - c0, 0, 0u, 0xffffffffu, 0u, 0xffffffffu};
+      PruneCursor cur = {0, c1 - cc, 0, cc - c0, 0, 0u, 0xffffffffu, 0u, 0xffffffffu, 0u, 0xffffffffu};
       uint16_t* Ul = &sList[wave][0][0];
       uint16_t* Dl = &sList[wave][1][0];
       for (int i = lane; i < cur.un; i += 64) Ul[i] = static_cast<uint16_t>(cc + i);
@@ -2984,6 +3035,7 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
   const int64_t tiles = cdiv(K_alloc, 16);
   w.corder = w.ckey = w.coff = w.hist = w.rkey = w.rord = nullptr;
   w.cbnd = nullptr;
+  w.cbnd3 = nullptr;
   w.cminS = w.cmaxP = nullptr;
   w.prm = nullptr;
   w.tD = w.lD = nullptr;
@@ -3000,9 +3052,10 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
       w.coff = ws.take<int>(static_cast<size_t>(kPruneKeys));
       w.hist = ws.take<int>(static_cast<size_t>(2 * kPruneKeys));
       w.cbnd = ws.take<uint4>(static_cast<size_t>(nch));
+      w.cbnd3 = ws.take<uint2>(static_cast<size_t>(nch));
       w.cminS = ws.take<uint32_t>(static_cast<size_t>(nch));
       w.cmaxP = ws.take<uint32_t>(static_cast<size_t>(nch));
-      w.prm = ws.take<float>(4 + 3 * kPruneParts);  // the parameters, then the partial ranges
+      w.prm = ws.take<float>(8 + 5 * kPruneParts);  // the parameters, then the partial ranges
       w.rkey = ws.take<int>(static_cast<size_t>(n_rows));
       w.rord = ws.take<int>(static_cast<size_t>(n_rows));
       w.tD = ws.take<float>(static_cast<size_t>(cdiv(n_rows, 256) * 256));
@@ -3049,7 +3102,8 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     uint16_t* ap = reinterpret_cast<uint16_t*>(w.apack);
     hipLaunchKernelGGL(cb_absmax_partial, dim3(nparts), dim3(256), 0, stream, C, ct, count, w.smax);
     PruneData pd = {};
-    const int jp = 0;  // the coordinate of the second band
+    const int jp = 0;                    // the coordinate of the second band
+    const int jq = src.d > 1 ? 1 : 0;    // and of the third
     if (p.prune) {
       // the codebook in key order (the packed tiles follow it), its chunk ranges, then the rows
       RowSrc cbs;
@@ -3061,10 +3115,10 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       cbs.n = K;
       const int64_t nch = p.tiles / 2;
       const int sparts = static_cast<int>(cdiv(K, 256) < kPruneParts ? cdiv(K, 256) : kPruneParts);
-      hipLaunchKernelGGL(prune_stats_partial, dim3(sparts), dim3(256), 0, stream, C, ct, K, src.d, jp, w.prm + 4,
+      hipLaunchKernelGGL(prune_stats_partial, dim3(sparts), dim3(256), 0, stream, C, ct, K, src.d, jp, jq, w.prm + 8,
                          w.hist);
       hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
-                         jp, w.prm + 4, sparts, w.prm, w.ckey, w.hist);
+                         jp, jq, w.prm + 8, sparts, w.prm, w.ckey, w.hist);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist, w.coff);
       hipLaunchKernelGGL(prune_fill_kernel, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, w.corder, p.tiles * kS32Tile, -1);
@@ -3073,23 +3127,25 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, C, ct, K, src.d, p.tiles, w.smax, nparts, w.corder, ap, alpha, w.rcount);
       hipLaunchKernelGGL(prune_chunks_kernel, dim3(static_cast<unsigned>(cdiv(nch, 4))), dim3(256), 0, stream, C, ct,
-                         K, src.d, jp, w.corder, alpha, nch, w.cbnd);
+                         K, src.d, jp, jq, w.corder, alpha, nch, w.cbnd, w.cbnd3);
       hipLaunchKernelGGL(prune_envelope_kernel, dim3(1), dim3(1024), 0, stream, w.cbnd, static_cast<int>(nch), w.cminS,
                          w.cmaxP, w.prm);
       hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
-                         src, jp, w.prm + 4, sparts, w.prm, w.rkey, w.hist + kPruneKeys);
+                         src, jp, jq, w.prm + 8, sparts, w.prm, w.rkey, w.hist + kPruneKeys);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist + kPruneKeys, nullptr);
       hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
                          w.rkey, src.n, w.hist + kPruneKeys, w.rord);
       pd.corder = w.corder;
       pd.coff = w.coff;
       pd.cbnd = w.cbnd;
+      pd.cbnd3 = w.cbnd3;
       pd.cminS = w.cminS;
       pd.cmaxP = w.cmaxP;
       pd.rord = w.rord;
       pd.rkey = w.rkey;
       pd.prm = w.prm;
       pd.jp = jp;
+      pd.jq = jq;
     } else {
       hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, C, ct, K, src.d, p.tiles, w.smax, nparts, nullptr, ap, alpha, w.rcount);

@@ -108,7 +108,8 @@ struct ScreenWs {
   int* corder;   // sorted codeword position -> codeword [tiles x 32]
   int* ckey;     // codeword keys [K]
   int* coff;     // first sorted position of every key [16384]
-  int* hist;     // key counts then cursors, codewords [16384] and rows [16384]
+  int* hist;     // key counts then cursors, codewords [16384] and rows [16384]; then the fine
+                 // histograms of the three key features over the codebook [3 x 4096]
   uint4* cbnd;   // chunk ranges of the norm and coordinate j [tiles / 2]
   uint2* cbnd3;  // chunk ranges of coordinate q [tiles / 2]
   uint32_t* cminS;

@@ -770,6 +770,7 @@ constexpr int kPruneBins1 = 16;                // norm bins (major key)
 constexpr int kPruneBins2 = 16;                // bins of coordinate j (middle key)
 constexpr int kPruneBins3 = 64;                // bins of coordinate q (minor key)
 constexpr int kPruneKeys = kPruneBins1 * kPruneBins2 * kPruneBins3;
+constexpr int kPruneFine = 4096;               // fine bins of each key feature (quantile edges)
 constexpr int64_t kPruneMinRows = 32768;       // rows from which the screen is pruned
 
 struct PruneData {
@@ -835,13 +836,28 @@ __device__ __forceinline__ int prune_bin(float x, float lo, float hi, int nb) {
   return static_cast<int>(f);
 }
 
-// r = {max ||c||, min c_j, max c_j, min c_q, max c_q}.  The key only orders the vectors; the
-// skipping tests use the exact ranges of every chunk, so any binning is correct.
-__device__ __forceinline__ int prune_key(float nrm, float xj, float xq, const float (&r)[5]) {
-  const int f1 = prune_bin(nrm, 0.0f, fmaxf(r[0], 0x1p-126f), kPruneBins1);
-  const int f2 = prune_bin(xj, r[1], r[2], kPruneBins2);
-  const int f3 = prune_bin(xq, r[3], r[4], kPruneBins3);
-  return (f1 * kPruneBins2 + f2) * kPruneBins3 + f3;
+// Fine bin of feature value x over [lo, hi] (clamped).
+__device__ __forceinline__ int prune_fine(float x, float lo, float hi) { return prune_bin(x, lo, hi, kPruneFine); }
+
+// The three key features of a vector: ||v||, v_j, v_q.
+__device__ __forceinline__ void prune_features(const float (&v)[8], int jp, int jq, float (&f)[3]) {
+  float n2 = 0.0f, xj = 0.0f, xq = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 8; ++t) {
+    n2 = n2 + v[t] * v[t];
+    xj = (t == jp) ? v[t] : xj;
+    xq = (t == jq) ? v[t] : xq;
+  }
+  f[0] = sqrtf(n2);
+  f[1] = xj;
+  f[2] = xq;
+}
+
+// Fine bins of the features, r = {max ||c||, min c_j, max c_j, min c_q, max c_q}.
+__device__ __forceinline__ void prune_fine3(const float (&f)[3], const float (&r)[5], int (&b)[3]) {
+  b[0] = prune_fine(f[0], 0.0f, fmaxf(r[0], 0x1p-126f));
+  b[1] = prune_fine(f[1], r[1], r[2]);
+  b[2] = prune_fine(f[2], r[3], r[4]);
 }
 
 constexpr int kPruneTile = 4096;  // vectors per block of the key counting and scatter
@@ -854,7 +870,8 @@ __global__ __launch_bounds__(256) void prune_stats_partial(const void* __restric
                                                            int* __restrict__ hist2) {
   __shared__ float s_r[5][256];
   const int tid = threadIdx.x;
-  for (int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + tid; e < 2 * kPruneKeys; e += gridDim.x * 256) hist2[e] = 0;
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + tid; e < 2 * kPruneKeys + 3 * kPruneFine; e += gridDim.x * 256)
+    hist2[e] = 0;
   float r[5] = {0.0f, __builtin_inff(), -__builtin_inff(), __builtin_inff(), -__builtin_inff()};
   for (int64_t k = static_cast<int64_t>(blockIdx.x) * 256 + tid; k < K; k += static_cast<int64_t>(gridDim.x) * 256) {
     float v[8];
@@ -928,32 +945,117 @@ __device__ __forceinline__ void prune_fold_ranges(const float* __restrict__ part
   }
 }
 
-// Key of vector i of src (the rows, or the codewords as a set of K rows).
-__device__ __forceinline__ int prune_vec_key(const RowSrc& src, int64_t i, int jp, int jq, const float (&r)[5]) {
+// The key features of vector i of src (the rows, or the codewords as a set of K rows).
+__device__ __forceinline__ void prune_vec_features(const RowSrc& src, int64_t i, int jp, int jq, float (&f)[3]) {
   float v[8];
   const int64_t off = row_offset(src, i);
   if (src.type == ET_F32)
     load_f32_elems<8>(static_cast<const float*>(src.base) + off, src.d, true, v);
   else
     load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, src.d, true, v);
-  float n2 = 0.0f, xj = 0.0f, xq = 0.0f;
+  prune_features(v, jp, jq, f);
+}
+
+// Fine histograms of the codebook's three key features over their ranges (kPruneTile codewords per
+// block, counted in LDS, nonzero counts added to fine[3][kPruneFine] with integer atomics).
+__global__ __launch_bounds__(256) void prune_fine_kernel(RowSrc cbs, int jp, int jq, const float* __restrict__ part,
+                                                         int nparts, float* __restrict__ prm, int* __restrict__ fine) {
+  __shared__ int h[3 * kPruneFine];
+  float r[5];
+  prune_fold_ranges(part, nparts, prm, r);
+  const int tid = threadIdx.x;
+  for (int b = tid; b < 3 * kPruneFine; b += 256) h[b] = 0;
+  __syncthreads();
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
+  for (int q = 0; q < kPruneTile / 256; ++q) {
+    const int64_t i = i0 + q * 256 + tid;
+    if (i < cbs.n) {
+      float f[3];
+      int b[3];
+      prune_vec_features(cbs, i, jp, jq, f);
+      prune_fine3(f, r, b);
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
-    n2 = n2 + v[t] * v[t];
-    xj = (t == jp) ? v[t] : xj;
-    xq = (t == jq) ? v[t] : xq;
+      for (int a = 0; a < 3; ++a) atomicAdd(h + a * kPruneFine + b[a], 1);
+    }
   }
-  return prune_key(sqrtf(n2), xj, xq, r);
+  __syncthreads();
+  for (int b = tid; b < 3 * kPruneFine; b += 256)
+    if (h[b]) atomicAdd(fine + b, h[b]);
+}
+
+// Coarse bin of every fine bin from the codebook's fine histograms: nb equal-width bins over a
+// robust range of the feature, median +- 3 interquartile ranges (about +-4 sigma for normal data, the
+// whole range of the codewords there), with the values outside it in the end bins, so that heavy
+// tails and outlier columns do not squeeze the bulk of the codewords into one bin.  256 threads,
+// 16 fine bins each.
+__device__ __forceinline__ void prune_build_lut(const int* __restrict__ fine, uint8_t (*lut)[kPruneFine],
+                                                int* scan) {
+  __shared__ int s_q[3];
+  const int tid = threadIdx.x;
+  constexpr int kPer = kPruneFine / 256;
+  const int nb[3] = {kPruneBins1, kPruneBins2, kPruneBins3};
+  for (int a = 0; a < 3; ++a) {
+    int c[kPer];
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      c[q] = fine[a * kPruneFine + tid * kPer + q];
+      sum += c[q];
+    }
+    scan[tid] = sum;
+    if (tid < 3) s_q[tid] = 0;
+    __syncthreads();
+    for (int o = 1; o < 256; o <<= 1) {
+      const int v = tid >= o ? scan[tid - o] : 0;
+      __syncthreads();
+      scan[tid] += v;
+      __syncthreads();
+    }
+    const int64_t total = scan[255];
+    // the fine bins holding the quartiles: quartile u is the first bin whose cumulative count exceeds
+    // u * total / 4 (exactly one thread owns it)
+    {
+      int64_t run = scan[tid] - sum;
+#pragma unroll
+      for (int q = 0; q < kPer; ++q) {
+        const int64_t nxt = run + c[q];
+#pragma unroll
+        for (int u = 0; u < 3; ++u) {
+          const int64_t tgt = (total * (u + 1)) / 4;
+          if (run <= tgt && tgt < nxt) s_q[u] = tid * kPer + q;
+        }
+        run = nxt;
+      }
+    }
+    __syncthreads();
+    const int iqr = s_q[2] - s_q[0];
+    int flo = s_q[1] - 3 * iqr - 1, fhi = s_q[1] + 3 * iqr + 1;
+    flo = flo < 0 ? 0 : flo;
+    fhi = fhi > kPruneFine - 1 ? kPruneFine - 1 : fhi;
+    const int span = fhi - flo + 1;
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      const int f = tid * kPer + q;
+      int cb = f < flo ? 0 : ((f - flo) * nb[a]) / span;
+      cb = cb < nb[a] ? cb : nb[a] - 1;
+      lut[a][f] = static_cast<uint8_t>(cb);
+    }
+    __syncthreads();
+  }
 }
 
 // Keys of kPruneTile vectors per block, counted in LDS, the block's nonzero counts added to the
 // global counts (one integer atomic per key present in the block).
 __global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, int jq, const float* __restrict__ part,
-                                                          int nparts, float* __restrict__ prm, int* __restrict__ keys,
+                                                          int nparts, float* __restrict__ prm,
+                                                          const int* __restrict__ fine, int* __restrict__ keys,
                                                           int* __restrict__ hist) {
   __shared__ int h[kPruneKeys];
+  __shared__ uint8_t lut[3][kPruneFine];
+  __shared__ int scan[256];
   float r[5];
   prune_fold_ranges(part, nparts, prm, r);
+  prune_build_lut(fine, lut, scan);
   const int tid = threadIdx.x;
   for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
   __syncthreads();
@@ -961,7 +1063,11 @@ __global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, in
   for (int q = 0; q < kPruneTile / 256; ++q) {
     const int64_t i = i0 + q * 256 + tid;
     if (i < src.n) {
-      const int key = prune_vec_key(src, i, jp, jq, r);
+      float f[3];
+      int b[3];
+      prune_vec_features(src, i, jp, jq, f);
+      prune_fine3(f, r, b);
+      const int key = (static_cast<int>(lut[0][b[0]]) * kPruneBins2 + lut[1][b[1]]) * kPruneBins3 + lut[2][b[2]];
       keys[i] = key;
       atomicAdd(h + key, 1);
     }
@@ -3050,7 +3156,7 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
       w.corder = ws.take<int>(static_cast<size_t>(t32 * kS32Tile));
       w.ckey = ws.take<int>(static_cast<size_t>(K_alloc));
       w.coff = ws.take<int>(static_cast<size_t>(kPruneKeys));
-      w.hist = ws.take<int>(static_cast<size_t>(2 * kPruneKeys));
+      w.hist = ws.take<int>(static_cast<size_t>(2 * kPruneKeys + 3 * kPruneFine));
       w.cbnd = ws.take<uint4>(static_cast<size_t>(nch));
       w.cbnd3 = ws.take<uint2>(static_cast<size_t>(nch));
       w.cminS = ws.take<uint32_t>(static_cast<size_t>(nch));
@@ -3117,8 +3223,11 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       const int sparts = static_cast<int>(cdiv(K, 256) < kPruneParts ? cdiv(K, 256) : kPruneParts);
       hipLaunchKernelGGL(prune_stats_partial, dim3(sparts), dim3(256), 0, stream, C, ct, K, src.d, jp, jq, w.prm + 8,
                          w.hist);
+      int* fine = w.hist + 2 * kPruneKeys;
+      hipLaunchKernelGGL(prune_fine_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
+                         jp, jq, w.prm + 8, sparts, w.prm, fine);
       hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
-                         jp, jq, w.prm + 8, sparts, w.prm, w.ckey, w.hist);
+                         jp, jq, w.prm + 8, sparts, w.prm, fine, w.ckey, w.hist);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist, w.coff);
       hipLaunchKernelGGL(prune_fill_kernel, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, w.corder, p.tiles * kS32Tile, -1);
@@ -3131,7 +3240,7 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       hipLaunchKernelGGL(prune_envelope_kernel, dim3(1), dim3(1024), 0, stream, w.cbnd, static_cast<int>(nch), w.cminS,
                          w.cmaxP, w.prm);
       hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
-                         src, jp, jq, w.prm + 8, sparts, w.prm, w.rkey, w.hist + kPruneKeys);
+                         src, jp, jq, w.prm + 8, sparts, w.prm, fine, w.rkey, w.hist + kPruneKeys);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist + kPruneKeys, nullptr);
       hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
                          w.rkey, src.n, w.hist + kPruneKeys, w.rord);

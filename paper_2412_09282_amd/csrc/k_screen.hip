@@ -1044,19 +1044,29 @@ __device__ __forceinline__ void prune_build_lut(const int* __restrict__ fine, ui
   }
 }
 
+// The lookup table of prune_build_lut, built once (one block) into lut_g[3][kPruneFine].
+__global__ __launch_bounds__(256) void prune_lut_kernel(const int* __restrict__ fine, uint8_t* __restrict__ lut_g) {
+  __shared__ uint8_t lut[3][kPruneFine];
+  __shared__ int scan[256];
+  prune_build_lut(fine, lut, scan);
+  const uint4* src = reinterpret_cast<const uint4*>(&lut[0][0]);
+  uint4* dst = reinterpret_cast<uint4*>(lut_g);
+  for (int e = threadIdx.x; e < 3 * kPruneFine / 16; e += 256) dst[e] = src[e];
+}
+
 // Keys of kPruneTile vectors per block, counted in LDS, the block's nonzero counts added to the
 // global counts (one integer atomic per key present in the block).
 __global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, int jq, const float* __restrict__ part,
                                                           int nparts, float* __restrict__ prm,
-                                                          const int* __restrict__ fine, int* __restrict__ keys,
+                                                          const uint8_t* __restrict__ lut_g, int* __restrict__ keys,
                                                           int* __restrict__ hist) {
   __shared__ int h[kPruneKeys];
   __shared__ uint8_t lut[3][kPruneFine];
-  __shared__ int scan[256];
   float r[5];
   prune_fold_ranges(part, nparts, prm, r);
-  prune_build_lut(fine, lut, scan);
   const int tid = threadIdx.x;
+  for (int e = tid; e < 3 * kPruneFine / 16; e += 256)
+    reinterpret_cast<uint4*>(&lut[0][0])[e] = reinterpret_cast<const uint4*>(lut_g)[e];
   for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
   __syncthreads();
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
@@ -3156,7 +3166,8 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
       w.corder = ws.take<int>(static_cast<size_t>(t32 * kS32Tile));
       w.ckey = ws.take<int>(static_cast<size_t>(K_alloc));
       w.coff = ws.take<int>(static_cast<size_t>(kPruneKeys));
-      w.hist = ws.take<int>(static_cast<size_t>(2 * kPruneKeys + 3 * kPruneFine));
+      // key counts, the fine histograms and their lookup table (3 x kPruneFine bytes)
+      w.hist = ws.take<int>(static_cast<size_t>(2 * kPruneKeys + 3 * kPruneFine + 3 * kPruneFine / 4));
       w.cbnd = ws.take<uint4>(static_cast<size_t>(nch));
       w.cbnd3 = ws.take<uint2>(static_cast<size_t>(nch));
       w.cminS = ws.take<uint32_t>(static_cast<size_t>(nch));
@@ -3226,8 +3237,10 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       int* fine = w.hist + 2 * kPruneKeys;
       hipLaunchKernelGGL(prune_fine_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
                          jp, jq, w.prm + 8, sparts, w.prm, fine);
+      uint8_t* lut = reinterpret_cast<uint8_t*>(fine + 3 * kPruneFine);
+      hipLaunchKernelGGL(prune_lut_kernel, dim3(1), dim3(256), 0, stream, fine, lut);
       hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
-                         jp, jq, w.prm + 8, sparts, w.prm, fine, w.ckey, w.hist);
+                         jp, jq, w.prm + 8, sparts, w.prm, lut, w.ckey, w.hist);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist, w.coff);
       hipLaunchKernelGGL(prune_fill_kernel, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, w.corder, p.tiles * kS32Tile, -1);
@@ -3240,7 +3253,7 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       hipLaunchKernelGGL(prune_envelope_kernel, dim3(1), dim3(1024), 0, stream, w.cbnd, static_cast<int>(nch), w.cminS,
                          w.cmaxP, w.prm);
       hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
-                         src, jp, jq, w.prm + 8, sparts, w.prm, fine, w.rkey, w.hist + kPruneKeys);
+                         src, jp, jq, w.prm + 8, sparts, w.prm, lut, w.rkey, w.hist + kPruneKeys);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist + kPruneKeys, nullptr);
       hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
                          w.rkey, src.n, w.hist + kPruneKeys, w.rord);

@@ -174,12 +174,17 @@ def test_second_screen_own_rows_full():
 
 
 # From about a million rows (no codebook splits) the first screen visits the codebook in the order
-# of a key (norm, then one coordinate) and skips pairs of tiles whose norms or coordinates are
-# certified too far from every row of a wave; the results must stay the oracle's exactly.
+# of a key (norm, then two coordinates, each binned over a robust range of the codebook) and skips
+# pairs of tiles whose norms or coordinates are certified too far from every row of a wave; the
+# results must stay the oracle's exactly.  "constant": both key coordinates constant over the codebook
+# (no spread to bin); "outlier_cols": heavy tails with 10x outlier coordinates in 8 % of the vectors
+# (the bins follow the bulk, the outliers fall into the end bins); "d1": one dimension (both key
+# coordinates are the same one).
 @pytest.mark.parametrize("case,K", [("near", 65536), ("bf16", 16384), ("outliers", 16384), ("ties", 16384),
-                                    ("tiny", 4096)])
+                                    ("tiny", 4096), ("constant", 16384), ("outlier_cols", 16384),
+                                    ("d1", 4096)])
 def test_pruned_first_screen(case, K):
-    n, d = (1 << 20) + 4096 + 37, 8
+    n, d = (1 << 20) + 4096 + 37, (1 if case == "d1" else 8)
     say(f"pruned first screen n={n} K={K} ({case})")
     g = np.random.default_rng(60)
     if case in ("near", "bf16"):
@@ -200,6 +205,20 @@ def test_pruned_first_screen(case, K):
         base = rv(K // 4, d, 63)
         Cb = np.ascontiguousarray(np.concatenate([base, base, base[::-1], base])[g.permutation(K)])
         V = np.concatenate([base[g.integers(0, K // 4, n // 2)], rv(n - n // 2, d, 64)])
+    elif case == "constant":
+        V = rv(n, d, 67)
+        Cb = rv(K, d, 68)
+        Cb[:, 0] = np.float32(0.01)
+        Cb[:, 1] = np.float32(-0.02)
+        V[: n // 2, 0] = np.float32(0.01)
+    elif case == "outlier_cols":
+        V = (g.standard_t(4.0, size=(n, d)) * 0.02).astype(np.float32)
+        hit = g.random(n) < 0.08
+        V[hit, g.integers(0, d, int(hit.sum()))] *= np.float32(10.0)
+        Cb = np.ascontiguousarray(V[g.choice(n, K, replace=False)])
+    elif case == "d1":
+        V = rv(n, d, 69)
+        Cb = rv(K, d, 70)
     else:  # magnitudes far below one: the bands are kept in units of the codebook scale
         V = rv(n, d, 65) * np.float32(1e-30)
         Cb = rv(K, d, 66) * np.float32(1e-30)

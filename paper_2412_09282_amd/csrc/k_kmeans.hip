@@ -407,6 +407,14 @@ __global__ __launch_bounds__(256) void small_k_partial(RowSrc src, const int32_t
 constexpr int kSkWaves = 8;
 constexpr int kSkDepth = 4;
 
+// LDS layout of a wave's table and stage.  Sum t of code c sits at c * 8 + (t ^ ((c >> 1) & 7)): with
+// the plain c * 8 + t, the 64 lanes of a batch (one code each) read dimension t from only two 8-byte
+// bank pairs of the 32 banks (codes of equal parity collide), a 32-way conflict per access; the
+// swizzle spreads them over all 16 pairs.  Half h of lane l's staged vector sits at slot
+// 2 l + (h ^ ((l >> 2) & 1)), so a wave's 16-byte stores and loads cover every bank.
+__device__ __forceinline__ int sk_slot(int c, int t) { return c * 8 + (t ^ ((c >> 1) & 7)); }
+__device__ __forceinline__ int sk_stage(int l, int h) { return 2 * l + (h ^ ((l >> 2) & 1)); }
+
 struct SkTable {
   double acc[256 * 8];
   int cnt[256];
@@ -481,25 +489,25 @@ __global__ __launch_bounds__(64 * kSkWaves) void small_k_wave_partial(RowSrc src
       if (bb < w1) {  // uniform
         const int c = (bb + lane < w1) ? cq[s] : -1;
         const bool valid = c >= 0 && c < K;
-        T.stage[lane][0] = va[s];
-        T.stage[lane][1] = vb[s];
+        (&T.stage[0][0])[sk_stage(lane, 0)] = va[s];
+        (&T.stage[0][0])[sk_stage(lane, 1)] = vb[s];
         wave_lds_sync();  // staged vectors and the previous batch's table updates are visible
         const uint64_t peers = peer_mask(valid, valid ? c : 0);
         if (valid && (__ffsll(static_cast<long long>(peers)) - 1) == lane) {
           double acc[8];
 #pragma unroll
-          for (int t = 0; t < 8; ++t) acc[t] = T.acc[c * 8 + t];
+          for (int t = 0; t < 8; ++t) acc[t] = T.acc[sk_slot(c, t)];
           uint64_t m = peers;
           while (m) {
             const int sl = __ffsll(static_cast<long long>(m)) - 1;
             m &= m - 1;
-            const float4 x0 = T.stage[sl][0], x1 = T.stage[sl][1];
+            const float4 x0 = (&T.stage[0][0])[sk_stage(sl, 0)], x1 = (&T.stage[0][0])[sk_stage(sl, 1)];
             const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
 #pragma unroll
             for (int t = 0; t < 8; ++t) acc[t] = acc[t] + static_cast<double>(x[t]);
           }
 #pragma unroll
-          for (int t = 0; t < 8; ++t) T.acc[c * 8 + t] = acc[t];
+          for (int t = 0; t < 8; ++t) T.acc[sk_slot(c, t)] = acc[t];
           T.cnt[c] += __popcll(peers);
         }
         wave_lds_sync();  // the stage is rewritten by the next batch
@@ -516,7 +524,7 @@ __global__ __launch_bounds__(64 * kSkWaves) void small_k_wave_partial(RowSrc src
     const int t = static_cast<int>(e - k * d);
     double acc = 0.0;
 #pragma unroll
-    for (int ww = 0; ww < kSkWaves; ++ww) acc = acc + tab[ww].acc[k * 8 + t];
+    for (int ww = 0; ww < kSkWaves; ++ww) acc = acc + tab[ww].acc[sk_slot(static_cast<int>(k), t)];
     part[e * nblocks + blockIdx.x] = acc;
     if (t == 0) {
       int cnt = 0;

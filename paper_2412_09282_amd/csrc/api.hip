@@ -5,6 +5,8 @@
 
 #include "crvq_internal.h"
 
+#include <rocprofiler-sdk-roctx/roctx.h>
+
 #include <cstdarg>
 #include <cstdio>
 #include <mutex>
@@ -18,6 +20,15 @@ using namespace crvq;
 static __device__ __align__(256) unsigned char scratch[CRVQ_NOALLOC_SCRATCH_BYTES];
 
 namespace {
+
+// A profiler range named after the entry point around each call that enqueues device work (seen by
+// rocprofv3 --marker-trace; a function call and a check when no profiler is attached).
+struct ApiRange {
+  explicit ApiRange(const char* name) { roctxRangePushA(name); }
+  ~ApiRange() { roctxRangePop(); }
+  ApiRange(const ApiRange&) = delete;
+  ApiRange& operator=(const ApiRange&) = delete;
+};
 
 thread_local std::string g_err;
 
@@ -145,6 +156,7 @@ size_t crvq_importance_workspace_size(int64_t M, int64_t N) {
 crvq_status crvq_channel_importance(const void* A, int64_t lda, const void* B, int64_t ldb, int dtype, int64_t M,
                                     int64_t N, const float* scale, int reduce, float* out, void* workspace,
                                     size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_channel_importance");
   static const char* fn = "crvq_channel_importance";
   g_err.clear();
   if (!dtype_ok(dtype)) return fail(CRVQ_ERR_INVALID, "%s: dtype %d is not CRVQ_F32 or CRVQ_BF16", fn, dtype);
@@ -169,6 +181,7 @@ size_t crvq_reorder_workspace_size(int64_t N) {
 crvq_status crvq_reorder(const void* in, int64_t ld_in, void* out, int64_t ld_out, int dtype, int64_t M, int64_t N,
                          const float* importance, int32_t* perm, int inverse, void* workspace, size_t ws_bytes,
                          void* stream) {
+  const ApiRange range("crvq_reorder");
   static const char* fn = "crvq_reorder";
   g_err.clear();
   if (N < 1 || N > (1LL << 20)) return fail(CRVQ_ERR_INVALID, "%s: N = %lld outside [1, 2^20]", fn, (long long)N);
@@ -216,6 +229,7 @@ size_t crvq_assign_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
 crvq_status crvq_assign(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
                         const void* C, int c_dtype, int64_t K, int32_t* codes, float* dist, void* workspace,
                         size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_assign");
   static const char* fn = "crvq_assign";
   g_err.clear();
   crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
@@ -266,6 +280,7 @@ crvq_status scratch_on_device(void** out, const char* fn) {
 crvq_status crvq_assign_noalloc(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
                                 int32_t d, const void* C, int c_dtype, int64_t K, int32_t* codes, float* dist,
                                 void* stream) {
+  const ApiRange range("crvq_assign_noalloc");
   static const char* fn = "crvq_assign_noalloc";
   g_err.clear();
   crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
@@ -309,6 +324,7 @@ crvq_status crvq_assign_residual_beam(const void* X, int x_dtype, int64_t n_rows
                                       int32_t d, int32_t n_books, const void* const* books, const int32_t* book_dtypes,
                                       const int64_t* Ks, int32_t beam, int32_t* const* codes, const int64_t* ldc,
                                       float* err, void* workspace, size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_assign_residual_beam");
   static const char* fn = "crvq_assign_residual_beam";
   g_err.clear();
   crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
@@ -378,6 +394,7 @@ size_t crvq_kmeans_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
 crvq_status crvq_kmeans_update(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
                                const int32_t* codes, int64_t K, void* C, int c_dtype, int32_t* counts, void* workspace,
                                size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_kmeans_update");
   static const char* fn = "crvq_kmeans_update";
   g_err.clear();
   crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
@@ -396,6 +413,7 @@ crvq_status crvq_kmeans_update(const void* X, int x_dtype, int64_t n_rows, int64
 // ------------------------------------------------------------------------------------------------
 crvq_status crvq_gather_vectors(const void* X, int x_dtype, int64_t n_rows, int64_t vecs_per_row, int64_t ld,
                                 int32_t d, const int64_t* idx, int64_t count, void* out, int out_dtype, void* stream) {
+  const ApiRange range("crvq_gather_vectors");
   static const char* fn = "crvq_gather_vectors";
   g_err.clear();
   crvq_status s = check_vectors(X, x_dtype, n_rows, vecs_per_row, ld, d, fn);
@@ -473,6 +491,7 @@ crvq_status crvq_dequant(int64_t M, int64_t n_cols, int32_t d, int64_t n_crit, c
                          const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* minuend,
                          int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out, void* workspace,
                          size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_dequant");
   static const char* fn = "crvq_dequant";
   g_err.clear();
   if (n_ext < 0 || n_ext > CRVQ_MAX_BOOKS - 1)
@@ -499,6 +518,7 @@ crvq_status crvq_dequant_books(int64_t M, int64_t n_cols, int32_t d, int64_t n_c
                                const int32_t* dtypes, const int64_t* Ks, const int32_t* perm, const void* minuend,
                                int minuend_dtype, int64_t ld_min, void* out, int out_dtype, int64_t ld_out,
                                void* workspace, size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_dequant_books");
   static const char* fn = "crvq_dequant_books";
   g_err.clear();
   if (!q || !C || !dtypes || !Ks) return fail(CRVQ_ERR_INVALID, "%s: q, C, dtypes and Ks must not be NULL", fn);
@@ -538,6 +558,7 @@ crvq_status crvq_bits_per_weight(int64_t rows, int64_t cols, int32_t d, int64_t 
 // ---- loss-driven refinement ----------------------------------------------------------------------
 crvq_status crvq_gram(const void* X, int x_dtype, int64_t n_rows, int64_t n_cols, int64_t ld, double* H, int64_t ldh,
                       void* stream) {
+  const ApiRange range("crvq_gram");
   static const char* fn = "crvq_gram";
   g_err.clear();
   if (n_rows < 0 || n_cols < 0) return fail(CRVQ_ERR_INVALID, "%s: negative size", fn);
@@ -557,6 +578,7 @@ size_t crvq_hessian_inverse_workspace_size(int64_t N) {
 
 crvq_status crvq_hessian_inverse_diagonal(const double* H, int64_t ldh, int64_t N, double damp, double* hinv,
                                           float* scale, void* workspace, size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_hessian_inverse_diagonal");
   static const char* fn = "crvq_hessian_inverse_diagonal";
   g_err.clear();
   if (N < 0 || N > 65536) return fail(CRVQ_ERR_INVALID, "%s: N = %lld outside [0, 65536]", fn, (long long)N);
@@ -572,6 +594,7 @@ crvq_status crvq_hessian_inverse_diagonal(const double* H, int64_t ldh, int64_t 
 crvq_status crvq_hessian_product(int64_t M, int64_t N, int64_t n_out, const double* R, int64_t ldr, const double* H,
                                  int64_t ldh, double* G, int64_t ldg, double* row_loss, double* loss_total,
                                  void* stream) {
+  const ApiRange range("crvq_hessian_product");
   static const char* fn = "crvq_hessian_product";
   g_err.clear();
   if (M < 0 || N < 1 || n_out < 1 || n_out > N) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and 1 <= n_out <= N", fn);
@@ -595,6 +618,7 @@ size_t crvq_code_sums_workspace_size(int64_t n_vectors, int32_t d, int64_t K) {
 crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row, int64_t ld, int32_t d,
                            const int32_t* codes, int64_t K, double* sums, int32_t* counts, void* workspace,
                            size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_code_sums");
   static const char* fn = "crvq_code_sums";
   g_err.clear();
   if (d < 1 || d > CRVQ_MAX_D) return fail(CRVQ_ERR_UNSUPPORTED, "%s: d = %d outside [1, %d]", fn, d, CRVQ_MAX_D);
@@ -613,6 +637,7 @@ crvq_status crvq_code_sums(const double* X, int64_t n_rows, int64_t vecs_per_row
 
 crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, double* m, double* v, int64_t n,
                            int64_t step, double lr, double beta1, double beta2, double eps, void* stream) {
+  const ApiRange range("crvq_adam_step");
   static const char* fn = "crvq_adam_step";
   g_err.clear();
   if (n < 0 || step < 1) return fail(CRVQ_ERR_INVALID, "%s: need n >= 0 and step >= 1", fn);
@@ -630,6 +655,7 @@ crvq_status crvq_adam_step(float* C, const double* grad, double grad_scale, doub
 crvq_status crvq_adam_step_bf16(uint16_t* C, float* master, const double* grad, double grad_scale, double* m,
                                 double* v, int64_t n, int64_t step, double lr, double beta1, double beta2, double eps,
                                 void* stream) {
+  const ApiRange range("crvq_adam_step_bf16");
   static const char* fn = "crvq_adam_step_bf16";
   g_err.clear();
   if (n < 0 || step < 1) return fail(CRVQ_ERR_INVALID, "%s: need n >= 0 and step >= 1", fn);
@@ -653,6 +679,7 @@ size_t crvq_refine_workspace_size(int64_t M, int64_t N, int64_t n_cols) {
 crvq_status crvq_refine_codes(int64_t M, int64_t N, int32_t d, int64_t n_cols, double* R, int64_t ldr, const double* H,
                               int64_t ldh, const void* C, int c_dtype, int64_t K, int32_t* codes, int64_t ldq,
                               void* workspace, size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_refine_codes");
   static const char* fn = "crvq_refine_codes";
   g_err.clear();
   if (M < 0 || N < 1) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and N >= 1", fn);
@@ -701,6 +728,7 @@ crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_
                               const uint8_t* const* q_ext, int64_t ldq_ext, const void* const* C_ext,
                               const int32_t* ext_dtypes, const int64_t* K_ext, const int32_t* perm, const void* x,
                               int x_dtype, float* y, void* workspace, size_t ws_bytes, void* stream) {
+  const ApiRange range("crvq_dequant_gemv");
   static const char* fn = "crvq_dequant_gemv";
   g_err.clear();
   if (M < 0 || N < 1) return fail(CRVQ_ERR_INVALID, "%s: need M >= 0 and N >= 1", fn);
@@ -741,6 +769,7 @@ crvq_status crvq_dequant_gemv(int64_t M, int64_t N, int64_t n_crit, const uint8_
 }
 
 crvq_status crvq_pack_codes_u8(const int32_t* codes, int64_t n, uint8_t* out, void* stream) {
+  const ApiRange range("crvq_pack_codes_u8");
   static const char* fn = "crvq_pack_codes_u8";
   g_err.clear();
   if (n < 0) return fail(CRVQ_ERR_INVALID, "%s: n < 0", fn);

@@ -43,7 +43,9 @@ def test_host_code_under_ubsan():
             for s in syms:
                 f.write(f"char {s}[4096] __attribute__((aligned(4096))) = {{0}};\n")
         _run(["gcc", "-c", "fatbin_stub.c", "-o", "fatbin_stub.o"], tmp)
-        _run([HIPCC, "-Xarch_host", "-fsanitize=undefined", "-o", "sweep"] + objs + ["fatbin_stub.o"], tmp)
+        _run([HIPCC, "-Xarch_host", "-fsanitize=undefined", "-o", "sweep"] + objs + ["fatbin_stub.o",
+                                                                          "-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx",
+                                                                          "-Wl,-rpath,/opt/rocm/lib"], tmp)
         r = subprocess.run(["./sweep"], cwd=tmp, capture_output=True, text=True, timeout=300,
                            env=dict(os.environ, UBSAN_OPTIONS="print_stacktrace=1:halt_on_error=1"))
         assert r.returncode == 0, f"host sweep failed:\n{r.stdout}\n{r.stderr}"

@@ -244,3 +244,35 @@ def test_rescue_of_most_rows():
     exp, ed = oracle.assign(V[S], Cb)
     np.testing.assert_array_equal(codes.cpu().numpy()[S], exp)
     np.testing.assert_array_equal(dist.cpu().numpy()[S], ed.astype(np.float32))
+
+
+# Small codebooks (K <= 256) at row counts that take the wide top-1 kernel (128 rows per wave): fp32 and
+# bf16 rows packed at a 16-byte aligned base take its fast forms, any other layout the generic form;
+# codes and distances must equal the oracle's, including exact ties (duplicated codewords, rescued)
+# and a last tile of padding codewords (K = 37).
+@pytest.mark.parametrize("case", ["f32", "f32_k37", "bf16", "unaligned", "ties"])
+def test_small_book_wide_forms(case):
+    n, d = 600_001, 8
+    say(f"small-book top-1, wide form: {case}, n={n}")
+    K = 37 if case == "f32_k37" else 256
+    V = rv(n, d, 71)
+    Cb = rv(K, d, 72)
+    if case == "ties":
+        Cb[128:] = Cb[:128]
+        V[: n // 3] = Cb[np.random.default_rng(73).integers(0, 128, n // 3)]
+    if case == "bf16":
+        check(inputs.f32_to_bf16_bits(V), inputs.f32_to_bf16_bits(Cb), "bf16")
+        return
+    if case == "unaligned":
+        buf = torch.empty(n * d + 1, dtype=torch.float32, device="cuda")
+        buf[1:] = torch.from_numpy(V.reshape(-1)).cuda()
+        Vt = buf[1:].view(n, d)  # base 4 bytes past a 16-byte boundary
+        codes = torch.empty(n, dtype=torch.int32, device="cuda")
+        dist = torch.empty(n, dtype=torch.float32, device="cuda")
+        C.crvq_assign(VecSet.of_vectors(Vt), dev(Cb), codes, dist)
+        torch.cuda.synchronize()
+        exp, ed = oracle.assign(V, Cb)
+        np.testing.assert_array_equal(codes.cpu().numpy(), exp)
+        np.testing.assert_array_equal(dist.cpu().numpy(), ed.astype(np.float32))
+        return
+    check(V, Cb)

@@ -69,7 +69,7 @@
 #define CRVQ_S32_SCHED 1  // pin the MFMA / VALU interleave of the 32 x 32 screen
 #endif
 #ifndef CRVQ_PRUNE
-#define CRVQ_PRUNE 1  // certified chunk skipping in the first long top-1 screen (norm and coordinate bands)
+#define CRVQ_PRUNE 1  // certified chunk skipping in the long top-1 screens (a norm band and two coordinate bands)
 #endif
 #ifndef CRVQ_PRUNE_FIRST
 #define CRVQ_PRUNE_FIRST 4  // chunks screened before the first band; the band is renewed after 2x, 4x, ...
@@ -901,8 +901,9 @@ __device__ __forceinline__ void prune_fine3(const float (&f)[3], const float (&r
 constexpr int kPruneTile = 4096;  // vectors per block of the key counting and scatter
 constexpr int kPruneParts = 256;  // partial blocks of the binning ranges
 
-// Partial binning ranges of the codebook (max norm, min and max of coordinate j) over a strided
-// share of the codewords, and (every block a share) the cleared key counts of codewords and rows.
+// Partial ranges of the codebook's key features (max norm, min and max of coordinates j and q) over a
+// strided share of the codewords, and (every block a share) the cleared key counts of codewords and
+// rows and the cleared fine histograms.
 __global__ __launch_bounds__(256) void prune_stats_partial(const void* __restrict__ C, int ct, int64_t K, int d,
                                                            int jp, int jq, float* __restrict__ part,
                                                            int* __restrict__ hist2) {

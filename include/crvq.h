@@ -135,7 +135,7 @@ crvq_status crvq_assign(const void* X, int x_dtype, int64_t n_rows, int64_t vecs
  * device memory, one per GPU, held until the process ends; the call allocates
  * nothing.  A request whose crvq_assign_workspace_size(n, d, K) exceeds that
  * size returns CRVQ_ERR_UNSUPPORTED before anything is enqueued (128 MiB holds
- * about 2.7 million vectors against 65536 codewords, 4.8 million against 256).  Every call on a GPU
+ * about 2.5 million vectors against 65536 codewords, 4.8 million against 256).  Every call on a GPU
  * shares that GPU's array: calls that overlap on one GPU (on different
  * streams or from different threads) race and must be ordered by the caller;
  * calls on one stream are ordered already.  The array's contents left by one

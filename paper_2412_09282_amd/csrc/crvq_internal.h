@@ -98,6 +98,8 @@ struct ScreenWs {
   double* pD;    // top-1: exact distance of the split's winner, [split][row]
   int* pK;       // top-1: its codeword, [split][row]
   double* xn2;   // top-1: ||x||^2 per row (fp64)
+  float* xe;     // 32 x 32 top-1 screen on fp16-rounded operands: per row the factor of R in its bound's
+                 // split term (written by the first screen)
   float* smax;   // 32 x 32 screen: partial maxima of |c|, then the scale alpha
   int* rcount;   // number of rows that failed the certification ([1]: that failed the second screen)
   int* rlist;    // those rows (any order), [n_rows]

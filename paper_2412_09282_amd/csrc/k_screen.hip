@@ -1513,6 +1513,7 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
                                                        const void* __restrict__ C, int ct, int64_t K,
                                                        float* __restrict__ pR, double* __restrict__ pD,
                                                        int* __restrict__ pK, double* __restrict__ xn2o,
+                                                       float* __restrict__ xeo,
                                                        const int* __restrict__ list, const int* __restrict__ list_n,
                                                        const int* __restrict__ corder, PruneData pd, double bacc,
                                                        double bsplit) {
@@ -1580,6 +1581,24 @@ __global__ __launch_bounds__(256) void screen32_kernel(RowSrc src, const uint16_
       p1[t] = x1;
       p2[t] = h ? static_cast<uint16_t>(t < 3 ? 0x6c00 : 0)  // 0x6c00 = 2^12
                 : (ONE ? x1 : f16_bits(x - f16_val(x1)));
+    }
+    if (ONE && xeo && h == 0 && ok && split == 0) {
+      // The screen on fp16-rounded operands (scaled: a = alpha c and y = -2 alpha x exactly, a = a1 + a2,
+      // y = y1 + y2) drops sum_t a_t y2_t + sum_t a2_t y1_t per codeword, with |a2_t| <= 2^-11 |a_t|
+      // (elements below the fp16 normal range: the bound's underflow terms).  For ||c|| <= R that is at
+      // most R (||y2|| + 2^-11 (1 + 2^-11) ||y||) / alpha: the row's own remainder instead of its worst
+      // case 2^-11 ||y|| (on average about 0.4 of it).  fp64 rows add the rounding of x to fp32,
+      // 2^-24 ||y|| / alpha.  The fp32 sums err far less than the 2^-9 margin.
+      float y2s = 0.0f, ys = 0.0f;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const float y2 = over ? 0.0f : xs[t] - f16_val(p1[t]);
+        y2s = y2s + y2 * y2;
+        ys = ys + xs[t] * xs[t];
+      }
+      const float ny = sqrtf(ys);
+      const float e = sqrtf(y2s) + 0x1p-11f * (1.0f + 0x1p-11f) * ny + (src.type == ET_F64 ? 0x1p-23f * ny : 0.0f);
+      xeo[i] = over ? 0.0f : (e / alpha) * (1.0f + 0x1p-9f);
     }
     b1[cb] = __builtin_bit_cast(h8, p1);
     b2[cb] = __builtin_bit_cast(h8, p2);
@@ -1955,6 +1974,7 @@ struct ScreenBound {
   double split_coef;
   double abs_coef;
   const float* alpha;
+  const float* row_e;  // when set: per row (position) the split term's factor of R, replacing split_coef ||x||
 };
 
 // Writes a row's result: its code and distance (top-1) or its sorted (D, k) list, padded with
@@ -2385,7 +2405,8 @@ __device__ __forceinline__ bool finish_top1(int64_t i, int64_t row, int splits, 
     const double xn2 = xn2a[i];
     const double xn = sqrt(xn2);
     const double R = xn + sqrt(Dl);
-    double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + bound.split_coef * xn * R +
+    const double sc = bound.row_e ? static_cast<double>(bound.row_e[i]) : bound.split_coef * xn;
+    double delta = bound.acc_ulps * 0x1p-24 * (R * R + 2.0 * xn * R) + sc * R +
                    bound.abs_coef * (xn + R + 1.0) + 1e-35;
     double restd = static_cast<double>(rest);
     if (bound.alpha) {
@@ -3135,6 +3156,7 @@ ScreenBound screen_bound(const ScreenPlan& p, int x_type, int ct, int d, const f
   b.split_coef = 0.0;
   b.abs_coef = 0.0;
   b.alpha = nullptr;
+  b.row_e = nullptr;
   if (p.s32) {
     // remainders of both splits and the dropped c2.x2, each <= 2^-22 sum |c_t| |2 x_t|; none when
     // both operands are bf16 (exact in fp16 under the scale)
@@ -3214,6 +3236,7 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
   w.cminS = w.cmaxP = nullptr;
   w.prm = nullptr;
   w.tD = w.lD = nullptr;
+  w.xe = nullptr;
   if (p.s32) {
     // 32-codeword tiles of 768 fp16, the scale reduction's partial maxima and alpha
     const int64_t t32 = p.tiles > cdiv(K_alloc, kS32Tile) ? p.tiles : cdiv(K_alloc, kS32Tile);
@@ -3254,6 +3277,7 @@ ScreenWs carve_screen(WsCursor& ws, const ScreenPlan& p, int64_t n_rows, int64_t
     w.pD = ws.take<double>(static_cast<size_t>(p.splits) * n_rows);
     w.pK = ws.take<int>(static_cast<size_t>(p.splits) * n_rows);
     w.xn2 = ws.take<double>(static_cast<size_t>(n_rows));
+    w.xe = p.s32 ? ws.take<float>(static_cast<size_t>(n_rows)) : nullptr;
   } else {
     w.pT = ws.take<int>(static_cast<size_t>(p.splits) * 4 * p.nb * n_rows);
     w.pM = ws.take<float>(static_cast<size_t>(p.splits) * 4 * p.nb * n_rows);
@@ -3336,14 +3360,17 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
     const bool exact = s32_exact_operands(src.type, ct);
     // First screen: one MFMA per tile.  Exact for bf16 rows against a bf16 book; otherwise on
     // fp16-rounded operands, certified with the wider bound.
-    const ScreenBound b1 = screen_bound(p, src.type, ct, src.d, alpha, !exact);
+    // (fp16-rounded operands: each row's own split term, from the screen, replaces the worst case)
+    ScreenBound b1 = screen_bound(p, src.type, ct, src.d, alpha, !exact);
+    float* const xe = exact ? nullptr : w.xe;
+    b1.row_e = xe;
     if (p.prune)
       hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true, false, false, true>), grid, dim3(256), 0,
-                         stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr,
-                         nullptr, pd.corder, pd, b1.acc_ulps, b1.split_coef);
+                         stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, xe,
+                         nullptr, nullptr, pd.corder, pd, b1.acc_ulps, b1.split_coef);
     else
       hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, true, false>), grid, dim3(256), 0, stream, src,
-                         ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, nullptr, nullptr,
+                         ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2, xe, nullptr, nullptr,
                          nullptr, pd, 0.0, 0.0);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (exact && !p.prune) {
@@ -3384,20 +3411,20 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       if (prune2)
         hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true, true>), grid2, dim3(256), 0,
                            stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
-                           w.rlist, w.rcount, pd.corder, pd2, 0.0, 0.0);
+                           nullptr, w.rlist, w.rcount, pd.corder, pd2, 0.0, 0.0);
       else
         hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, true>), grid2, dim3(256), 0,
                            stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
-                           w.rlist, w.rcount, pd.corder, PruneData{}, 0.0, 0.0);
+                           nullptr, w.rlist, w.rcount, pd.corder, PruneData{}, 0.0, 0.0);
     } else {
       if (prune2)
         hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false, true>), grid, dim3(256), 0,
                            stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
-                           w.rlist, w.rcount, pd.corder, pd2, 0.0, 0.0);
+                           nullptr, w.rlist, w.rcount, pd.corder, pd2, 0.0, 0.0);
       else
         hipLaunchKernelGGL((screen32_kernel<CRVQ_S32_CB, CRVQ_S32_CHUNK, false, true, false>), grid, dim3(256), 0,
                            stream, src, ap, alpha, p.tiles, p.tiles_per_split, C, ct, K, w.pR, w.pD, w.pK, w.xn2,
-                           w.rlist, w.rcount, pd.corder, PruneData{}, 0.0, 0.0);
+                           nullptr, w.rlist, w.rcount, pd.corder, PruneData{}, 0.0, 0.0);
     }
     const ScreenBound b2 = screen_bound(p, src.type, ct, src.d, alpha);
     hipLaunchKernelGGL(finalize1_list_kernel, dim3(static_cast<unsigned>(cdiv(src.n, 256))), dim3(256), 0, stream,

@@ -898,7 +898,22 @@ __device__ __forceinline__ void prune_fine3(const float (&f)[3], const float (&r
   b[2] = prune_fine(f[2], r[3], r[4]);
 }
 
-constexpr int kPruneTile = 4096;  // vectors per block of the key counting and scatter
+constexpr int kPruneTile = 4096;  // codewords per block of the fine histograms
+// threads and vectors per block of the key counting and scatter, codebook and rows
+#ifndef CRVQ_PRUNE_CB_NT
+#define CRVQ_PRUNE_CB_NT 1024
+#endif
+#ifndef CRVQ_PRUNE_CB_TILE
+#define CRVQ_PRUNE_CB_TILE 4096
+#endif
+#ifndef CRVQ_PRUNE_ROW_NT
+#define CRVQ_PRUNE_ROW_NT 1024
+#endif
+#ifndef CRVQ_PRUNE_ROW_TILE
+#define CRVQ_PRUNE_ROW_TILE 8192
+#endif
+constexpr int kPruneCbThreads = CRVQ_PRUNE_CB_NT, kPruneCbTile = CRVQ_PRUNE_CB_TILE;
+constexpr int kPruneRowThreads = CRVQ_PRUNE_ROW_NT, kPruneRowTile = CRVQ_PRUNE_ROW_TILE;
 constexpr int kPruneParts = 256;  // partial blocks of the binning ranges
 
 // Partial ranges of the codebook's key features (max norm, min and max of coordinates j and q) over a
@@ -954,14 +969,18 @@ __global__ __launch_bounds__(256) void prune_stats_partial(const void* __restric
 // first one also publishes them to prm[0..2] and prm[4..5]).
 __device__ __forceinline__ void prune_fold_ranges(const float* __restrict__ part, int nparts, float* __restrict__ prm,
                                                   float (&r)[5]) {
-  __shared__ float s_r[5][256];
+  // (blocks of 256 threads or more; the first 256 fold the 256 partial ranges)
+  static_assert(kPruneParts == 256, "the fold halves 256 entries");
+  __shared__ float s_r[5][kPruneParts];
   const int tid = threadIdx.x;
-  const bool in = tid < nparts;
-  s_r[0][tid] = in ? part[tid] : 0.0f;
-  s_r[1][tid] = in ? part[kPruneParts + tid] : __builtin_inff();
-  s_r[2][tid] = in ? part[2 * kPruneParts + tid] : -__builtin_inff();
-  s_r[3][tid] = in ? part[3 * kPruneParts + tid] : __builtin_inff();
-  s_r[4][tid] = in ? part[4 * kPruneParts + tid] : -__builtin_inff();
+  if (tid < kPruneParts) {
+    const bool in = tid < nparts;
+    s_r[0][tid] = in ? part[tid] : 0.0f;
+    s_r[1][tid] = in ? part[kPruneParts + tid] : __builtin_inff();
+    s_r[2][tid] = in ? part[2 * kPruneParts + tid] : -__builtin_inff();
+    s_r[3][tid] = in ? part[3 * kPruneParts + tid] : __builtin_inff();
+    s_r[4][tid] = in ? part[4 * kPruneParts + tid] : -__builtin_inff();
+  }
   __syncthreads();
   for (int w = 128; w >= 1; w >>= 1) {
     if (tid < w) {
@@ -1093,24 +1112,27 @@ __global__ __launch_bounds__(256) void prune_lut_kernel(const int* __restrict__ 
   for (int e = threadIdx.x; e < 3 * kPruneFine / 16; e += 256) dst[e] = src[e];
 }
 
-// Keys of kPruneTile vectors per block, counted in LDS, the block's nonzero counts added to the
-// global counts (one integer atomic per key present in the block).
-__global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, int jq, const float* __restrict__ part,
-                                                          int nparts, float* __restrict__ prm,
-                                                          const uint8_t* __restrict__ lut_g, int* __restrict__ keys,
-                                                          int* __restrict__ hist) {
+// Keys of TILE vectors per block of NT threads, counted in LDS, the block's nonzero counts added to
+// the global counts (one integer atomic per key present in the block).  The LDS counters cost the
+// same per block whatever its tile, so larger tiles and blocks spread them over more vectors.
+template <int NT, int TILE>
+__global__ __launch_bounds__(NT) void prune_count_kernel(RowSrc src, int jp, int jq, const float* __restrict__ part,
+                                                         int nparts, float* __restrict__ prm,
+                                                         const uint8_t* __restrict__ lut_g, int* __restrict__ keys,
+                                                         int* __restrict__ hist) {
+  static_assert(TILE % NT == 0 && kPruneKeys % (4 * NT) == 0, "whole rounds");
   __shared__ int h[kPruneKeys];
   __shared__ uint8_t lut[3][kPruneFine];
   float r[5];
   prune_fold_ranges(part, nparts, prm, r);
   const int tid = threadIdx.x;
-  for (int e = tid; e < 3 * kPruneFine / 16; e += 256)
+  for (int e = tid; e < 3 * kPruneFine / 16; e += NT)
     reinterpret_cast<uint4*>(&lut[0][0])[e] = reinterpret_cast<const uint4*>(lut_g)[e];
-  for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
+  for (int b = tid; b < kPruneKeys / 4; b += NT) reinterpret_cast<int4*>(h)[b] = make_int4(0, 0, 0, 0);
   __syncthreads();
-  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
-  for (int q = 0; q < kPruneTile / 256; ++q) {
-    const int64_t i = i0 + q * 256 + tid;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * TILE;
+  for (int q = 0; q < TILE / NT; ++q) {
+    const int64_t i = i0 + q * NT + tid;
     if (i < src.n) {
       float f[3];
       int b[3];
@@ -1122,7 +1144,7 @@ __global__ __launch_bounds__(256) void prune_count_kernel(RowSrc src, int jp, in
     }
   }
   __syncthreads();
-  for (int b = tid; b < kPruneKeys; b += 256)
+  for (int b = tid; b < kPruneKeys; b += NT)
     if (h[b]) atomicAdd(hist + b, h[b]);
 }
 
@@ -1157,28 +1179,30 @@ __global__ __launch_bounds__(1024) void prune_scan_kernel(int* __restrict__ hist
 
 // order[...] = i in key order: ranks within the block from LDS counters, one global cursor advance
 // per key present in the block.  The order within a key is not fixed; results do not depend on it.
-__global__ __launch_bounds__(256) void prune_order_kernel(const int* __restrict__ keys, int64_t n,
-                                                          int* __restrict__ cursor, int* __restrict__ order) {
+template <int NT, int TILE>
+__global__ __launch_bounds__(NT) void prune_order_kernel(const int* __restrict__ keys, int64_t n,
+                                                         int* __restrict__ cursor, int* __restrict__ order) {
+  static_assert(TILE % NT == 0 && kPruneKeys % (4 * NT) == 0, "whole rounds");
   __shared__ int h[kPruneKeys];
   const int tid = threadIdx.x;
-  for (int b = tid; b < kPruneKeys; b += 256) h[b] = 0;
+  for (int b = tid; b < kPruneKeys / 4; b += NT) reinterpret_cast<int4*>(h)[b] = make_int4(0, 0, 0, 0);
   __syncthreads();
-  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
-  constexpr int kQ = kPruneTile / 256;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.x) * TILE;
+  constexpr int kQ = TILE / NT;
   int key[kQ], rank[kQ];
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
-    const int64_t i = i0 + q * 256 + tid;
+    const int64_t i = i0 + q * NT + tid;
     key[q] = i < n ? keys[i] : -1;
     rank[q] = key[q] >= 0 ? atomicAdd(h + key[q], 1) : 0;
   }
   __syncthreads();
-  for (int b = tid; b < kPruneKeys; b += 256)
+  for (int b = tid; b < kPruneKeys; b += NT)
     if (h[b]) h[b] = atomicAdd(cursor + b, h[b]);
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
-    const int64_t i = i0 + q * 256 + tid;
+    const int64_t i = i0 + q * NT + tid;
     if (key[q] >= 0) {
       const int pos = h[key[q]] + rank[q];
       if (pos >= 0 && pos < n) order[pos] = static_cast<int>(i);
@@ -3322,12 +3346,14 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                          jp, jq, w.prm + 8, sparts, w.prm, fine);
       uint8_t* lut = reinterpret_cast<uint8_t*>(fine + 3 * kPruneFine);
       hipLaunchKernelGGL(prune_lut_kernel, dim3(1), dim3(256), 0, stream, fine, lut);
-      hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
+      hipLaunchKernelGGL((prune_count_kernel<kPruneCbThreads, kPruneCbTile>),
+                         dim3(static_cast<unsigned>(cdiv(K, kPruneCbTile))), dim3(kPruneCbThreads), 0, stream, cbs,
                          jp, jq, w.prm + 8, sparts, w.prm, lut, w.ckey, w.hist);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist, w.coff);
       hipLaunchKernelGGL(prune_fill_kernel, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, w.corder, p.tiles * kS32Tile, -1);
-      hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream,
+      hipLaunchKernelGGL((prune_order_kernel<kPruneCbThreads, kPruneCbTile>),
+                         dim3(static_cast<unsigned>(cdiv(K, kPruneCbTile))), dim3(kPruneCbThreads), 0, stream,
                          w.ckey, K, w.hist, w.corder);
       hipLaunchKernelGGL(prep_codebook_s32, dim3(static_cast<unsigned>(cdiv(p.tiles * kS32Tile, 256))), dim3(256), 0,
                          stream, C, ct, K, src.d, p.tiles, w.smax, nparts, w.corder, ap, alpha, w.rcount);
@@ -3335,10 +3361,12 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
                          K, src.d, jp, jq, w.corder, alpha, nch, w.cbnd, w.cbnd3);
       hipLaunchKernelGGL(prune_envelope_kernel, dim3(1), dim3(1024), 0, stream, w.cbnd, static_cast<int>(nch), w.cminS,
                          w.cmaxP, w.prm);
-      hipLaunchKernelGGL(prune_count_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
+      hipLaunchKernelGGL((prune_count_kernel<kPruneRowThreads, kPruneRowTile>),
+                         dim3(static_cast<unsigned>(cdiv(src.n, kPruneRowTile))), dim3(kPruneRowThreads), 0, stream,
                          src, jp, jq, w.prm + 8, sparts, w.prm, lut, w.rkey, w.hist + kPruneKeys);
       hipLaunchKernelGGL(prune_scan_kernel, dim3(1), dim3(1024), 0, stream, w.hist + kPruneKeys, nullptr);
-      hipLaunchKernelGGL(prune_order_kernel, dim3(static_cast<unsigned>(cdiv(src.n, kPruneTile))), dim3(256), 0, stream,
+      hipLaunchKernelGGL((prune_order_kernel<kPruneRowThreads, kPruneRowTile>),
+                         dim3(static_cast<unsigned>(cdiv(src.n, kPruneRowTile))), dim3(kPruneRowThreads), 0, stream,
                          w.rkey, src.n, w.hist + kPruneKeys, w.rord);
       pd.corder = w.corder;
       pd.coff = w.coff;

@@ -1015,18 +1015,20 @@ __device__ __forceinline__ void prune_vec_features(const RowSrc& src, int64_t i,
 }
 
 // Fine histograms of the codebook's three key features over their ranges (kPruneTile codewords per
-// block, counted in LDS, nonzero counts added to fine[3][kPruneFine] with integer atomics).
-__global__ __launch_bounds__(256) void prune_fine_kernel(RowSrc cbs, int jp, int jq, const float* __restrict__ part,
-                                                         int nparts, float* __restrict__ prm, int* __restrict__ fine) {
+// block of NT threads, counted in LDS, nonzero counts added to fine[3][kPruneFine] with integer atomics).
+template <int NT>
+__global__ __launch_bounds__(NT) void prune_fine_kernel(RowSrc cbs, int jp, int jq, const float* __restrict__ part,
+                                                        int nparts, float* __restrict__ prm, int* __restrict__ fine) {
+  static_assert(kPruneTile % NT == 0, "whole rounds");
   __shared__ int h[3 * kPruneFine];
   float r[5];
   prune_fold_ranges(part, nparts, prm, r);
   const int tid = threadIdx.x;
-  for (int b = tid; b < 3 * kPruneFine; b += 256) h[b] = 0;
+  for (int b = tid; b < 3 * kPruneFine; b += NT) h[b] = 0;
   __syncthreads();
   const int64_t i0 = static_cast<int64_t>(blockIdx.x) * kPruneTile;
-  for (int q = 0; q < kPruneTile / 256; ++q) {
-    const int64_t i = i0 + q * 256 + tid;
+  for (int q = 0; q < kPruneTile / NT; ++q) {
+    const int64_t i = i0 + q * NT + tid;
     if (i < cbs.n) {
       float f[3];
       int b[3];
@@ -1037,7 +1039,7 @@ __global__ __launch_bounds__(256) void prune_fine_kernel(RowSrc cbs, int jp, int
     }
   }
   __syncthreads();
-  for (int b = tid; b < 3 * kPruneFine; b += 256)
+  for (int b = tid; b < 3 * kPruneFine; b += NT)
     if (h[b]) atomicAdd(fine + b, h[b]);
 }
 
@@ -3342,7 +3344,8 @@ hipError_t launch_screen(const RowSrc& src, const void* C, int ct, int64_t K, in
       hipLaunchKernelGGL(prune_stats_partial, dim3(sparts), dim3(256), 0, stream, C, ct, K, src.d, jp, jq, w.prm + 8,
                          w.hist);
       int* fine = w.hist + 2 * kPruneKeys;
-      hipLaunchKernelGGL(prune_fine_kernel, dim3(static_cast<unsigned>(cdiv(K, kPruneTile))), dim3(256), 0, stream, cbs,
+      hipLaunchKernelGGL((prune_fine_kernel<kPruneCbThreads>), dim3(static_cast<unsigned>(cdiv(K, kPruneTile))),
+                         dim3(kPruneCbThreads), 0, stream, cbs,
                          jp, jq, w.prm + 8, sparts, w.prm, fine);
       uint8_t* lut = reinterpret_cast<uint8_t*>(fine + 3 * kPruneFine);
       hipLaunchKernelGGL(prune_lut_kernel, dim3(1), dim3(256), 0, stream, fine, lut);

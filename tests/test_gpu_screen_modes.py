@@ -160,6 +160,29 @@ def test_two_pass_screen(case):
         check(V, Cb)
 
 
+# The first screen on fp16-rounded operands certifies each row with its own fp16 remainder: with
+# a = alpha c and y = -2 alpha x = y1 + y2 the dropped terms are sum_t a_t y2_t + sum_t a2_t y1_t, bounded
+# by R (||y2|| + 2^-11 (1 + 2^-11) ||y||) / alpha.  Here every row sits just below the midpoint between
+# two fp16 values after the power-of-two scale (each y2_t positive and 2^-13 short of half a spacing,
+# the largest it can be), and the codewords share the rows' signs, so sum_t a_t y2_t is close to its
+# Cauchy-Schwarz bound; the codewords come in near-tied pairs, so many rows stay uncertain.  Codes
+# and distances must remain the oracle's (unpruned: 4 codebook splits; pruned: one split, key order).
+@pytest.mark.parametrize("n,K", [(262144 + 37, 65536), ((1 << 20) + 37, 16384)])
+def test_first_screen_aligned_remainders(n, K):
+    d = 8
+    say(f"first screen, remainders aligned with the codewords: n={n} K={K}")
+    g = np.random.default_rng(71)
+    # -2^12 x in [256, 512), where fp16 values are 0.25 apart: 256 + 0.25 j + (0.125 - 2^-13), exact in fp32
+    j = g.integers(0, 1024, size=(n, d)).astype(np.float64)
+    V = (-(256.0 + 0.25 * j + (0.125 - 2.0 ** -13)) / 4096.0).astype(np.float32)
+    base = V[g.choice(n, K // 2, replace=False)]
+    e1 = (g.random((K // 2, d)) * 2e-6).astype(np.float32)
+    e2 = (g.random((K // 2, d)) * 2e-6).astype(np.float32)
+    Cb = np.ascontiguousarray(np.concatenate([base - e1, base - e2])[g.permutation(K)])
+    assert (Cb < 0).all() and (V < 0).all()
+    check(V, Cb)
+
+
 def test_second_screen_own_rows_full():
     """From 2^23 rows up the second (split) screen of fp32 rows gives every wave rows of its own
     instead of sharing them across a workgroup.  Every row of a (2^23 + 37)-row search against 4096

@@ -2083,20 +2083,36 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
     // their minima join "rest", so the certificate below stays exact (a row whose answer lies in
     // a skipped tile fails it and is rescued).
     float thr = __builtin_inff();
+    // the first split's kept minima stay in registers from the threshold to the selection (with one
+    // split, the usual case, pM is read once; the kept tile ids only for the tiles re-scored)
+    float pm0[NB > 1 ? 4 : 1][NB];
     if (NB > 1 && valid) {
-      float sm[NB];  // the NB smallest kept tile minima, ascending
+      // the NB smallest kept tile minima, ascending: each lane group's list is ascending already, so
+      // it is merged in (the smaller of the running list and the group's taken in reverse is a
+      // bitonic sequence holding the NB smallest of both; a half-cleaner network sorts it)
+      float sm[NB];
 #pragma unroll
       for (int j = 0; j < NB; ++j) sm[j] = __builtin_inff();
       for (int s = 0; s < splits; ++s) {
+#pragma unroll
         for (int g = 0; g < 4; ++g) {
+          float b[NB];
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
-            float v = pM[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+            b[j] = pM[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+            if (s == 0) pm0[g][j] = b[j];
+          }
 #pragma unroll
-            for (int q = 0; q < NB; ++q) {
-              const float lo = fminf(sm[q], v);
-              v = fmaxf(sm[q], v);
-              sm[q] = lo;
+          for (int j = 0; j < NB; ++j) sm[j] = fminf(sm[j], b[NB - 1 - j]);
+#pragma unroll
+          for (int w = NB / 2; w >= 1; w >>= 1) {
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+              if ((j & w) == 0) {
+                const float lo = fminf(sm[j], sm[j + w]), hi = fmaxf(sm[j], sm[j + w]);
+                sm[j] = lo;
+                sm[j + w] = hi;
+              }
             }
           }
         }
@@ -2107,22 +2123,39 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
         if (q == need - 1) mt = sm[q];
       thr = mt + 0x1p-12f * (fabsf(mt) + static_cast<float>(xn2));
     }
-    for (int s = 0; s < (NB > 1 ? splits : 0); ++s) {
-      rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
-      // The kept tiles to re-score, as a bit set over the (group, slot) pairs, so that a wave loops
-      // over the most any of its rows needs (typically a handful) instead of every kept slot.
-      uint64_t todo = 0;
+    // The kept tiles to re-score, as a bit set over the (group, slot) pairs, so that a wave loops over
+    // the most any of its rows needs (typically a handful) instead of every kept slot; the others'
+    // minima bound their codewords and join "rest".  A slot holding no tile has the minimum +inf: it
+    // joins neither (nor does it below, where its tile id is negative).  The first split's set is
+    // taken here, from the minima in registers.
+    uint64_t todo0 = 0;
+    if (NB > 1) {
+#pragma unroll
       for (int g = 0; g < 4; ++g) {
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
-          const int T = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
-          if (T < 0) continue;
-          const float mj = pM[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
-          if (!(mj <= thr)) {  // not re-scored: its minimum bounds its codewords
+          const float mj = pm0[g][j];
+          if (mj <= thr)
+            todo0 |= uint64_t{1} << (g * NB + j);
+          else
             rest = fminf(rest, mj);
-            continue;
+        }
+      }
+    }
+    for (int s = 0; s < (NB > 1 ? splits : 0); ++s) {
+      rest = fminf(rest, pR[static_cast<int64_t>(s) * n + i]);
+      uint64_t todo = todo0;
+      if (s > 0) {
+        todo = 0;
+        for (int g = 0; g < 4; ++g) {
+#pragma unroll
+          for (int j = 0; j < NB; ++j) {
+            const float mj = pM[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+            if (mj <= thr)
+              todo |= uint64_t{1} << (g * NB + j);
+            else
+              rest = fminf(rest, mj);
           }
-          todo |= uint64_t{1} << (g * NB + j);
         }
       }
       const int64_t ts1 = (static_cast<int64_t>(s) + 1) * tps < tiles ? (static_cast<int64_t>(s) + 1) * tps : tiles;
@@ -2131,6 +2164,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(RowSrc src, int splits, i
         todo &= todo - 1;
         const int g = q / NB, j = q - (q / NB) * NB;
         const int T0 = pT[((static_cast<int64_t>(s) * 4 + g) * NB + j) * n + i];
+        if (T0 < 0) continue;  // an empty slot (the threshold is +inf)
         for (int u = 0; u < chunk && T0 + u < ts1; ++u) {  // the kept tile, or every tile of its chunk
           const int T = T0 + u;
           float cw[4][DM];

@@ -1007,10 +1007,14 @@ __device__ __forceinline__ void prune_fold_ranges(const float* __restrict__ part
 __device__ __forceinline__ void prune_vec_features(const RowSrc& src, int64_t i, int jp, int jq, float (&f)[3]) {
   float v[8];
   const int64_t off = row_offset(src, i);
-  if (src.type == ET_F32)
+  if (src.type == ET_F32) {
     load_f32_elems<8>(static_cast<const float*>(src.base) + off, src.d, true, v);
-  else
+  } else if (src.type == ET_BF16) {
     load_bf16_elems<8>(static_cast<const uint16_t*>(src.base) + off, src.d, true, v);
+  } else {  // fp64 rows (residuals), rounded to fp32 as the screen's operands are: the key only orders
+#pragma unroll
+    for (int t = 0; t < 8; ++t) v[t] = t < src.d ? static_cast<float>(static_cast<const double*>(src.base)[off + t]) : 0.0f;
+  }
   prune_features(v, jp, jq, f);
 }
 

@@ -129,6 +129,27 @@ def test_beam_width_one_long_codebook():
     np.testing.assert_array_equal(err.cpu().numpy(), np.asarray(exp_err, dtype=np.float64).astype(np.float32))
 
 
+@pytest.mark.parametrize("n", [65536 + 37, (1 << 20) + 37])
+def test_beam_width_one_long_extended_book(n):
+    """Width 1 over a K=4096 basic and a K=65536 extended book: the extended step searches the fp64
+    residuals on the 32 x 32 fp16 screens (unpruned with codebook splits at 65,573 rows, pruned in key
+    order at 1,048,613), whose operands are the residuals rounded to fp32; the certificate adds that
+    rounding to each row's own fp16 remainder."""
+    say(f"residual beam, width 1, K=4096 basic + K=65536 extended over fp64 residuals, n={n}")
+    V = rv(n, 8, 81)
+    books = [rv(4096, 8, 82), rv(65536, 8, 83, 0.006)]
+    codes = [torch.empty(n, dtype=torch.int32, device="cuda") for _ in books]
+    err = torch.empty(n, dtype=torch.float32, device="cuda")
+    C.crvq_assign_residual_beam(VecSet.of_vectors(dev(V)), [dev(b) for b in books], 1, codes, err)
+    torch.cuda.synchronize()
+    exp_codes, exp_err = oracle.beam(V, books, 1)
+    for t in range(2):
+        got = codes[t].cpu().numpy()
+        bad = np.flatnonzero(got != exp_codes[t])
+        assert len(bad) == 0, f"book {t}: {len(bad)} codes differ, e.g. rows {bad[:5]}"
+    np.testing.assert_array_equal(err.cpu().numpy(), np.asarray(exp_err, dtype=np.float64).astype(np.float32))
+
+
 # Long searches on fp32 operands (here 262144 rows x 65536 codewords, four codebook splits) get two
 # screens: one MFMA per tile on fp16-rounded operands with the wider certificate, then the split form
 # on the rows it left uncertain, then the exact rescue of what is left.

@@ -45,7 +45,7 @@ extern "C" {
 typedef enum {
   CRVQ_OK = 0,
   CRVQ_ERR_INVALID = 1,     /* a NULL required pointer or an out-of-range size / option */
-  CRVQ_ERR_UNSUPPORTED = 2, /* a valid request outside what this build implements */
+  CRVQ_ERR_UNSUPPORTED = 2, /* a valid request outside what the library implements */
   CRVQ_ERR_WORKSPACE = 3,   /* workspace missing or smaller than the *_workspace_size() result */
   CRVQ_ERR_HIP = 4          /* the HIP runtime reported an error while enqueueing */
 } crvq_status;
